@@ -1,0 +1,364 @@
+/*
+ * DriftSched admission hot path: plain single-threaded CPU oracle.
+ *
+ * TEST INFRASTRUCTURE. Only the test suite, the smoke check and the
+ * benchmark's CPU-baseline leg may load or call this library. The product
+ * path (the HIP library and its binding) never does; it shares no source,
+ * header, table or helper with this file.
+ *
+ * Every routine here is written to be read against the paper
+ * ("DriftSched: Adaptive QoS-Aware Scheduling under Runtime Token Drift for
+ * Multi-Tenant GPU Inference"), not to be fast: plain loops, fp64 throughout,
+ * built with -ffp-contract=off so that no multiply-add is fused.
+ *
+ * Functions and the passages they follow:
+ *   dsref_count_words      whitespace proxy, Python str.split() semantics
+ *                          (Sec. "Workload Characterization and Token Budget
+ *                          Estimation"; Sec. "Admission-Time Workload
+ *                          Characterization Overhead", tab:tokenizer_overhead)
+ *   dsref_characterize     the same, over a packed batch of prompts
+ *   dsref_calibrate        EMA update, Eq. (5) with the ratio of Eq. (6)
+ *                          (Sec. "Runtime Calibration and Feedback Adaptation")
+ *   dsref_score            Eq. (1), Eq. (2) in the order of Alg. 1, Eq. (4)
+ *   dsref_order            FIFO, Priority, Weighted, SJF, Aging Priority
+ *                          (Sec. "Scheduling Engine" and its subsections)
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* ------------------------------------------------------------------------ */
+/* Whitespace proxy                                                          */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * The paper counts input words with Python's str.split() (its platform table
+ * names Python 3.10.12). With no argument, str.split() separates on the code
+ * points for which str.isspace() is true. That set is written out here; the
+ * test suite regenerates it from the running Python by enumerating every code
+ * point and checks this function against it.
+ */
+int dsref_is_space(uint32_t cp)
+{
+    if (cp >= 0x09 && cp <= 0x0D) return 1;   /* TAB LF VT FF CR */
+    if (cp >= 0x1C && cp <= 0x20) return 1;   /* FS GS RS US SPACE */
+    if (cp == 0x85) return 1;                 /* NEXT LINE */
+    if (cp == 0xA0) return 1;                 /* NO-BREAK SPACE */
+    if (cp == 0x1680) return 1;               /* OGHAM SPACE MARK */
+    if (cp >= 0x2000 && cp <= 0x200A) return 1; /* EN QUAD .. HAIR SPACE */
+    if (cp == 0x2028) return 1;               /* LINE SEPARATOR */
+    if (cp == 0x2029) return 1;               /* PARAGRAPH SEPARATOR */
+    if (cp == 0x202F) return 1;               /* NARROW NO-BREAK SPACE */
+    if (cp == 0x205F) return 1;               /* MEDIUM MATHEMATICAL SPACE */
+    if (cp == 0x3000) return 1;               /* IDEOGRAPHIC SPACE */
+    return 0;
+}
+
+static int is_cont(uint8_t b) { return b >= 0x80 && b <= 0xBF; }
+
+/*
+ * Decode one well-formed UTF-8 sequence starting at s (avail bytes left),
+ * following the Unicode table of well-formed byte sequences. Returns its
+ * length and stores the code point, or returns 0 when the bytes at s do not
+ * begin a well-formed sequence.
+ */
+static int decode_one(const uint8_t *s, uint64_t avail, uint32_t *cp)
+{
+    uint8_t b0 = s[0];
+    if (b0 <= 0x7F) { *cp = b0; return 1; }
+    if (b0 >= 0xC2 && b0 <= 0xDF) {
+        if (avail < 2 || !is_cont(s[1])) return 0;
+        *cp = ((uint32_t)(b0 & 0x1F) << 6) | (s[1] & 0x3F);
+        return 2;
+    }
+    if (b0 >= 0xE0 && b0 <= 0xEF) {
+        uint8_t lo = 0x80, hi = 0xBF;
+        if (b0 == 0xE0) lo = 0xA0;
+        if (b0 == 0xED) hi = 0x9F;
+        if (avail < 3 || s[1] < lo || s[1] > hi || !is_cont(s[2])) return 0;
+        *cp = ((uint32_t)(b0 & 0x0F) << 12) | ((uint32_t)(s[1] & 0x3F) << 6) | (s[2] & 0x3F);
+        return 3;
+    }
+    if (b0 >= 0xF0 && b0 <= 0xF4) {
+        uint8_t lo = 0x80, hi = 0xBF;
+        if (b0 == 0xF0) lo = 0x90;
+        if (b0 == 0xF4) hi = 0x8F;
+        if (avail < 4 || s[1] < lo || s[1] > hi || !is_cont(s[2]) || !is_cont(s[3])) return 0;
+        *cp = ((uint32_t)(b0 & 0x07) << 18) | ((uint32_t)(s[1] & 0x3F) << 12) |
+              ((uint32_t)(s[2] & 0x3F) << 6) | (s[3] & 0x3F);
+        return 4;
+    }
+    return 0;
+}
+
+/*
+ * Number of items len(prompt.split()) for one prompt of len bytes: the number
+ * of maximal runs of non-whitespace characters. The prompt is decoded on its
+ * own. A byte that does not start a well-formed sequence is taken as one
+ * non-whitespace character, which is what decoding with the surrogateescape
+ * error handler does; since every multi-byte whitespace code point begins
+ * with a byte that is never a continuation byte, it does not matter for the
+ * count how many bytes one decoding error spans.
+ */
+uint32_t dsref_count_words(const uint8_t *s, uint64_t len)
+{
+    uint32_t n = 0;
+    int in_word = 0;
+    uint64_t p = 0;
+    while (p < len) {
+        uint32_t cp = 0;
+        int k = decode_one(s + p, len - p, &cp);
+        int space;
+        if (k == 0) { space = 0; k = 1; }
+        else space = dsref_is_space(cp);
+        if (space) {
+            in_word = 0;
+        } else {
+            if (!in_word) n++;
+            in_word = 1;
+        }
+        p += (uint64_t)k;
+    }
+    return n;
+}
+
+/*
+ * Stage 1 over a batch: prompt i is text[offsets[i] .. offsets[i+1]).
+ * Returns 0, or -1 if the offsets are not nondecreasing or exceed text_bytes.
+ */
+int dsref_characterize(const uint8_t *text, uint64_t text_bytes,
+                       const uint64_t *offsets, uint64_t n, uint32_t *counts)
+{
+    for (uint64_t i = 0; i < n; i++) {
+        uint64_t a = offsets[i], b = offsets[i + 1];
+        if (b < a || b > text_bytes) return -1;
+        counts[i] = dsref_count_words(text + a, b - a);
+    }
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Calibration: Eq. (5) and Eq. (6)                                         */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Completion events are taken in array order, which is completion order.
+ * For an event of group g with admission estimate est (the B-free estimate
+ * T_base*S*F of the request) and observed output length obs:
+ *     B_measured = obs / est                       (Eq. 6)
+ *     B[g] = (1 - alpha) * B[g] + alpha * B_measured  (Eq. 5)
+ * evaluated as t1 = (1-alpha)*B; t2 = alpha*r; B = t1 + t2.
+ * An event whose est is not finite or not positive carries no usable ratio
+ * and leaves B[g] unchanged. trace[e] (if trace is not NULL) is B[g] after
+ * event e. Events whose group is >= n_groups are rejected (return -1).
+ */
+int dsref_calibrate(const uint32_t *group, const double *est, const uint32_t *obs,
+                    uint64_t n_events, double alpha, uint32_t n_groups,
+                    double *state, double *trace)
+{
+    for (uint64_t e = 0; e < n_events; e++)
+        if (group[e] >= n_groups) return -1;
+    for (uint64_t e = 0; e < n_events; e++) {
+        uint32_t g = group[e];
+        double x = est[e];
+        if (isfinite(x) && x > 0.0) {
+            double r = (double)obs[e] / x;
+            double t1 = (1.0 - alpha) * state[g];
+            double t2 = alpha * r;
+            state[g] = t1 + t2;
+        }
+        if (trace) trace[e] = state[g];
+    }
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Budget and class: Eq. (1), Eq. (2), Alg. 1, Eq. (4)                      */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * For request i with word count n_i = counts[i], semantic category cat_i,
+ * tenant ten_i and calibration group g_i:
+ *   F       = 1 + n_i / f_ref                       (prompt complexity factor)
+ *   est     = T_base[cat] * B[g] * S[ten] * F       (Eq. 2, left to right as
+ *                                                    Alg. 1 gathers them)
+ *   est_base= T_base[cat] * S[ten] * F              (the same without B)
+ *   budget  = n_i + est                             (Eq. 1)
+ *   class   = 0 short if budget <= short_max, 1 medium if <= medium_max,
+ *             2 long otherwise                      (Eq. 4)
+ * est_base may be NULL. Returns -1 if an index is out of range.
+ */
+int dsref_score(uint64_t n, const uint32_t *counts, const uint8_t *category,
+                const uint32_t *tenant, const uint32_t *group,
+                const double *t_base, uint32_t n_cat,
+                const double *s_tenant, uint32_t n_tenants,
+                const double *state, uint32_t n_groups,
+                double f_ref, double short_max, double medium_max,
+                double *est_base, double *est, double *budget, uint8_t *job_class)
+{
+    for (uint64_t i = 0; i < n; i++) {
+        if (category[i] >= n_cat || tenant[i] >= n_tenants || group[i] >= n_groups)
+            return -1;
+        double words = (double)counts[i];
+        double F = 1.0 + words / f_ref;
+        double tb = t_base[category[i]];
+        double s = s_tenant[tenant[i]];
+        double b = state[group[i]];
+        double e = tb * b;
+        e = e * s;
+        e = e * F;
+        if (est_base) {
+            double e0 = tb * s;
+            e0 = e0 * F;
+            est_base[i] = e0;
+        }
+        est[i] = e;
+        double total = words + e;
+        budget[i] = total;
+        uint8_t c;
+        if (total <= short_max) c = 0;
+        else if (total <= medium_max) c = 1;
+        else c = 2;
+        job_class[i] = c;
+    }
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Dispatch orders                                                           */
+/* ------------------------------------------------------------------------ */
+
+enum { REF_FIFO = 0, REF_PRIORITY = 1, REF_WEIGHTED = 2, REF_SJF = 3, REF_AGING = 4 };
+
+/* Sort context: primary key (may be NULL), then arrival, then index. */
+struct sort_ctx {
+    const double *primary;
+    const double *arrival;
+};
+
+static int cmp_req(const void *pa, const void *pb, void *vctx)
+{
+    const struct sort_ctx *c = (const struct sort_ctx *)vctx;
+    uint32_t a = *(const uint32_t *)pa, b = *(const uint32_t *)pb;
+    if (c->primary) {
+        if (c->primary[a] < c->primary[b]) return -1;
+        if (c->primary[a] > c->primary[b]) return 1;
+    }
+    if (c->arrival[a] < c->arrival[b]) return -1;
+    if (c->arrival[a] > c->arrival[b]) return 1;
+    if (a < b) return -1;
+    if (a > b) return 1;
+    return 0;
+}
+
+static void sort_requests(uint32_t *perm, uint32_t n, const double *primary,
+                          const double *arrival)
+{
+    struct sort_ctx c = { primary, arrival };
+    for (uint32_t i = 0; i < n; i++) perm[i] = i;
+    qsort_r(perm, n, sizeof(uint32_t), cmp_req, &c);
+}
+
+/*
+ * Dispatch order of n pending requests under one policy. perm[k] is the
+ * request dispatched k-th. key (optional) receives each request's primary
+ * key under the policy. Every policy ends ties in arrival order, and equal
+ * arrivals by lower request index (FIFO within a tier, Sec. "Priority
+ * Scheduling").
+ *
+ *  FIFO      arrival order (Sec. "FIFO Scheduling"). key = arrival.
+ *  Priority  requests taken from the highest-priority non-empty tier queue,
+ *            FIFO within a tier: the exact order of the score
+ *            priority*10^12 + arrival of Sec. "Priority Scheduling", with a
+ *            lower tier_priority value served first (Premium = 0).
+ *            key = tier_priority[tier].
+ *  Weighted  a cyclic dispatcher over the tier queues (Sec. "Weighted
+ *            Scheduling"): each round serves up to weight[q] requests from
+ *            queue q, q = 0, 1, ..., in FIFO order; an empty queue is passed
+ *            over. key = the round in which the request is served.
+ *  SJF       lower estimated budget first (Sec. "Shortest-Job-First
+ *            Scheduling"). key = budget.
+ *  Aging     effective score e = max(floor, p - rate * max(0, t_now - a)),
+ *            lower first, where p = tier_priority[tier] and a = arrival:
+ *            waiting lowers the score (Sec. "Aging Priority Scheduling").
+ *            key = e.
+ * Returns -1 on a tier >= n_tiers, a zero weight or an unknown policy.
+ */
+int dsref_order(int policy, uint32_t n, const uint8_t *tier, const double *arrival,
+                const double *budget, uint32_t n_tiers, const uint32_t *weight,
+                const double *tier_priority, double aging_rate, double t_now,
+                double aging_floor, uint32_t *perm, double *key)
+{
+    for (uint32_t i = 0; i < n; i++)
+        if (tier[i] >= n_tiers) return -1;
+    if (policy == REF_FIFO) {
+        sort_requests(perm, n, NULL, arrival);
+        if (key) for (uint32_t i = 0; i < n; i++) key[i] = arrival[i];
+        return 0;
+    }
+    if (policy == REF_PRIORITY) {
+        double *p = (double *)malloc(sizeof(double) * (n ? n : 1));
+        for (uint32_t i = 0; i < n; i++) p[i] = tier_priority[tier[i]];
+        sort_requests(perm, n, p, arrival);
+        if (key) memcpy(key, p, sizeof(double) * n);
+        free(p);
+        return 0;
+    }
+    if (policy == REF_SJF) {
+        sort_requests(perm, n, budget, arrival);
+        if (key) for (uint32_t i = 0; i < n; i++) key[i] = budget[i];
+        return 0;
+    }
+    if (policy == REF_AGING) {
+        double *e = (double *)malloc(sizeof(double) * (n ? n : 1));
+        for (uint32_t i = 0; i < n; i++) {
+            double w = t_now - arrival[i];
+            if (w < 0.0) w = 0.0;
+            double d = aging_rate * w;
+            double v = tier_priority[tier[i]] - d;
+            if (v < aging_floor) v = aging_floor;
+            e[i] = v;
+        }
+        sort_requests(perm, n, e, arrival);
+        if (key) memcpy(key, e, sizeof(double) * n);
+        free(e);
+        return 0;
+    }
+    if (policy == REF_WEIGHTED) {
+        for (uint32_t q = 0; q < n_tiers; q++)
+            if (weight[q] == 0) return -1;
+        /* tier queues in FIFO order */
+        uint32_t *fifo = (uint32_t *)malloc(sizeof(uint32_t) * (n ? n : 1));
+        sort_requests(fifo, n, NULL, arrival);
+        uint32_t *len = (uint32_t *)calloc(n_tiers, sizeof(uint32_t));
+        uint32_t *start = (uint32_t *)calloc(n_tiers, sizeof(uint32_t));
+        uint32_t *head = (uint32_t *)calloc(n_tiers, sizeof(uint32_t));
+        uint32_t *queue = (uint32_t *)malloc(sizeof(uint32_t) * (n ? n : 1));
+        for (uint32_t k = 0; k < n; k++) len[tier[fifo[k]]]++;
+        for (uint32_t q = 1; q < n_tiers; q++) start[q] = start[q - 1] + len[q - 1];
+        for (uint32_t k = 0; k < n; k++) {
+            uint32_t i = fifo[k], q = tier[i];
+            queue[start[q] + head[q]++] = i;
+        }
+        memset(head, 0, sizeof(uint32_t) * n_tiers);
+        uint32_t pos = 0;
+        double round = 0.0;
+        while (pos < n) {
+            for (uint32_t q = 0; q < n_tiers; q++) {
+                uint32_t take = 0;
+                while (take < weight[q] && head[q] < len[q]) {
+                    uint32_t i = queue[start[q] + head[q]];
+                    perm[pos++] = i;
+                    if (key) key[i] = round;
+                    head[q]++;
+                    take++;
+                }
+            }
+            round += 1.0;
+        }
+        free(fifo); free(len); free(start); free(head); free(queue);
+        return 0;
+    }
+    return -1;
+}
