@@ -1,0 +1,229 @@
+/*
+ * driftsched.h - C ABI of the DriftSched admission hot path on AMD Instinct
+ * MI355X (gfx950).
+ *
+ * The paper ("DriftSched: Adaptive QoS-Aware Scheduling under Runtime Token
+ * Drift for Multi-Tenant GPU Inference") admits each request by estimating
+ * its token budget from its prompt, folds completed requests' observed
+ * output lengths into calibration factors, classifies the request, and
+ * dispatches it under one of five policies. This library runs those steps
+ * over a whole batch of pending requests on one GPU:
+ *
+ *   ds_characterize   word counts of the prompts (whitespace proxy)
+ *   ds_calibrate      EMA calibration factors from completion events
+ *   ds_score          calibrated output estimate, budget and runtime class
+ *   ds_order          dispatch permutation for one policy
+ *
+ * Conventions shared by every entry point:
+ *  - Array arguments are DEVICE pointers (memory from hipMalloc or any
+ *    allocator of the same device, e.g. torch tensors); parameter structs
+ *    are HOST pointers, read during the call only.
+ *  - The caller owns every buffer. The library never allocates or frees
+ *    device memory and keeps no state between calls. Scratch memory is a
+ *    caller-provided workspace of at least ds_workspace_bytes() bytes,
+ *    256-byte aligned; its contents need no initialisation and are
+ *    undefined after the call.
+ *  - Work is enqueued on `stream` (a hipStream_t; NULL is the null stream)
+ *    and the call returns without waiting, except with DS_VALIDATE, where
+ *    it waits for the stream to report data errors.
+ *  - Host-checkable errors (NULL pointers, sizes, parameter ranges, a short
+ *    workspace) are returned before anything is enqueued. A launch failure
+ *    returns DS_ERR_HIP. Without DS_VALIDATE, device data that break a
+ *    stated contract give unspecified results but never out-of-bounds
+ *    memory accesses.
+ *  - n == 0 is valid and enqueues nothing.
+ *  - No C++ exception crosses this interface.
+ */
+#ifndef DRIFTSCHED_H
+#define DRIFTSCHED_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    DS_OK = 0,
+    DS_ERR_NULL = -1,       /* a required pointer is NULL */
+    DS_ERR_ARG = -2,        /* a scalar argument or parameter is out of range */
+    DS_ERR_SIZE = -3,       /* a count exceeds the supported maximum */
+    DS_ERR_WORKSPACE = -4,  /* workspace NULL, misaligned or smaller than required */
+    DS_ERR_DATA = -5,       /* DS_VALIDATE found device data breaking the contract */
+    DS_ERR_HIP = -6,        /* the HIP runtime reported an error */
+    DS_ERR_ALIGN = -7       /* an array pointer is not aligned as required */
+} ds_status;
+
+typedef enum {
+    DS_FIFO = 0,            /* arrival order */
+    DS_PRIORITY = 1,        /* tier priority first, FIFO within equal priority */
+    DS_WEIGHTED = 2,        /* cyclic weighted round robin over tier queues */
+    DS_SJF = 3,             /* smaller budget first */
+    DS_AGING = 4            /* aged priority, smaller first */
+} ds_policy;
+
+typedef enum {
+    DS_OP_CHARACTERIZE = 0,
+    DS_OP_CALIBRATE = 1,
+    DS_OP_SCORE = 2,
+    DS_OP_ORDER = 3
+} ds_op;
+
+/* flags */
+#define DS_VALIDATE 1u      /* check device data, wait, and report DS_ERR_DATA */
+
+#define DS_MAX_TIERS 16
+#define DS_MAX_ITEMS (1u << 30)   /* max events for ds_calibrate, requests for ds_order */
+
+typedef void *ds_stream;    /* hipStream_t */
+
+/* Parameters of the budget estimate (Eq. 2) and the classes (Eq. 4). */
+typedef struct {
+    double f_ref;           /* prompt-complexity factor F = 1 + n / f_ref; > 0 */
+    double short_max;       /* budget <= short_max is short (128 in the paper) */
+    double medium_max;      /* budget <= medium_max is medium (512 in the paper) */
+} ds_score_params;
+
+/* Parameters of the dispatch policies. */
+typedef struct {
+    uint32_t n_tiers;                    /* 1..DS_MAX_TIERS; tier values < n_tiers */
+    uint32_t weight[DS_MAX_TIERS];       /* DS_WEIGHTED: requests per round, >= 1 */
+    double tier_priority[DS_MAX_TIERS];  /* DS_PRIORITY/DS_AGING: smaller first; finite */
+    double aging_rate;                   /* DS_AGING: priority units per second, >= 0 */
+    double t_now;                        /* DS_AGING: current time (same clock as arrival) */
+    double aging_floor;                  /* DS_AGING: lower clamp of the aged score (may be -inf) */
+} ds_order_params;
+
+/*
+ * Stage 1: whitespace-proxy word counts (Sec. "Workload Characterization and
+ * Token Budget Estimation"; the split() column of tab:tokenizer_overhead).
+ *
+ * counts[i] = len(p.decode('utf-8', 'surrogateescape').split()) for prompt
+ * p = text[offsets[i] .. offsets[i+1]), i < n: the number of maximal runs of
+ * characters that are not among the 29 code points Python's str.split()
+ * separates on (ASCII 09-0D, 1C-20; U+0085, U+00A0, U+1680, U+2000-200A,
+ * U+2028, U+2029, U+202F, U+205F, U+3000). Each prompt is decoded on its own;
+ * an undecodable byte counts as a non-space character.
+ *
+ *  text       device, text_bytes bytes, 16-byte aligned; read-only
+ *  text_bytes size of the text buffer; the kernels read exactly [0, text_bytes)
+ *  offsets    device, n+1 uint64; contract: nondecreasing, offsets[n] <= text_bytes
+ *  n          number of prompts (< 2^32 - 1)
+ *  counts     device, n uint32; written
+ *  ws         workspace of ds_workspace_bytes(DS_OP_CHARACTERIZE, n, 0) bytes
+ */
+ds_status ds_characterize(const uint8_t *text, uint64_t text_bytes,
+                          const uint64_t *offsets, uint32_t n, uint32_t *counts,
+                          void *ws, size_t ws_bytes, uint32_t flags, ds_stream stream);
+
+/*
+ * Stage 2: calibration factors, Eq. (5) with the ratio of Eq. (6)
+ * (Sec. "Runtime Calibration and Feedback Adaptation").
+ *
+ * Events are in completion order. For each event e with est[e] finite and
+ * > 0, in that order, the factor of its group g = group[e] is updated
+ *     state[g] <- (1 - alpha) * state[g] + alpha * (observed[e] / est[e]);
+ * other events leave it unchanged. trace[e] receives state[g] after event e.
+ * The GPU evaluates the recurrence as a parallel scan over the affine maps
+ * x -> a x + b, so results match the sequential evaluation up to rounding
+ * (relative differences of order 1e-15; the contract is 1e-12).
+ *
+ *  group      device, n_events uint32; contract: < n_groups
+ *  est        device, n_events double: the B-free admission estimate
+ *             T_base * S_tenant * F_input of the completed request
+ *  observed   device, n_events uint32: observed output tokens
+ *  n_events   <= DS_MAX_ITEMS
+ *  alpha      EMA rate, 0 <= alpha <= 1
+ *  n_groups   number of calibration groups (>= 1)
+ *  state      device, n_groups double; in: factors before the events (1.0
+ *             initially), out: after. Groups without events are unchanged.
+ *  trace      device, n_events double, or NULL
+ *  ws         workspace of ds_workspace_bytes(DS_OP_CALIBRATE, n_events, n_groups)
+ */
+ds_status ds_calibrate(const uint32_t *group, const double *est, const uint32_t *observed,
+                       uint64_t n_events, double alpha, uint32_t n_groups,
+                       double *state, double *trace,
+                       void *ws, size_t ws_bytes, uint32_t flags, ds_stream stream);
+
+/*
+ * Stage 3: budget and class, Eq. (1), Eq. (2) in the order of Alg. 1, Eq. (4)
+ * (Sec. "Workload Characterization and Token Budget Estimation" and
+ * "Workload Classification"). For request i, with n_i = counts[i]:
+ *     F         = 1 + n_i / f_ref
+ *     est[i]    = ((t_base[category[i]] * state[group[i]]) * s_tenant[tenant[i]]) * F
+ *     est_base  = (t_base[category[i]] * s_tenant[tenant[i]]) * F
+ *     budget[i] = n_i + est[i]
+ *     class[i]  = 0 if budget <= short_max, 1 if <= medium_max, else 2
+ * in IEEE double with no fused multiply-add, so results are bit-identical to
+ * any plain evaluation in that order.
+ *
+ *  counts, category, tenant, group   device, n entries; contract: indices in range
+ *  t_base     device, n_cat double (baseline estimate per semantic category)
+ *  s_tenant   device, n_tenants double (tenant safety scaling)
+ *  state      device, n_groups double (calibration factors, e.g. from ds_calibrate)
+ *  est_base   device, n double, or NULL
+ *  est, budget device, n double; job_class device, n uint8
+ *  params     host; f_ref > 0
+ *  ws         workspace of ds_workspace_bytes(DS_OP_SCORE, n, 0) bytes (used
+ *             by DS_VALIDATE only; may be NULL without that flag)
+ * Out-of-range indices (without DS_VALIDATE) give NaN estimates and class 2.
+ */
+ds_status ds_score(uint32_t n, const uint32_t *counts, const uint8_t *category,
+                   const uint32_t *tenant, const uint32_t *group,
+                   const double *t_base, uint32_t n_cat,
+                   const double *s_tenant, uint32_t n_tenants,
+                   const double *state, uint32_t n_groups,
+                   const ds_score_params *params,
+                   double *est_base, double *est, double *budget, uint8_t *job_class,
+                   void *ws, size_t ws_bytes, uint32_t flags, ds_stream stream);
+
+/*
+ * Stage 4: dispatch order of one policy (Sec. "Scheduling Engine").
+ * perm[k] is the index of the request dispatched k-th. Every policy breaks
+ * ties by FIFO rank: arrival, then lower request index (-0.0 equals +0.0).
+ *
+ *  DS_FIFO      key (arrival, index)                   (Sec. "FIFO Scheduling")
+ *  DS_PRIORITY  key (tier_priority[tier], FIFO rank): the exact order of the
+ *               score priority * 10^12 + arrival       (Sec. "Priority Scheduling")
+ *  DS_WEIGHTED  blocked cyclic round robin: round r serves, for q = 0, 1, ...,
+ *               the requests of tier q with FIFO rank within the tier in
+ *               [r w_q, (r+1) w_q); empty queues are passed over
+ *                                                      (Sec. "Weighted Scheduling")
+ *  DS_SJF       key (budget, FIFO rank)                (Sec. "Shortest-Job-First Scheduling")
+ *  DS_AGING     key (e, FIFO rank), e = max(aging_floor,
+ *               tier_priority[tier] - aging_rate * max(0, t_now - arrival))
+ *                                                      (Sec. "Aging Priority Scheduling")
+ *
+ *  tier       device, n uint8; contract: < params->n_tiers
+ *  arrival    device, n double; contract: not NaN
+ *  budget     device, n double (DS_SJF only; else may be NULL); contract: not NaN
+ *  fifo_in    device, n uint32, or NULL. When given it must be the DS_FIFO
+ *             permutation of the same arrival array (e.g. a previous DS_FIFO
+ *             call's perm); the FIFO sort is then skipped.
+ *  perm       device, n uint32; written
+ *  key        device, n double, or NULL: each request's primary key (arrival,
+ *             tier_priority, round number, budget, or e)
+ *  n          <= DS_MAX_ITEMS
+ *  ws         workspace of ds_workspace_bytes(DS_OP_ORDER, n, 0) bytes
+ */
+ds_status ds_order(ds_policy policy, uint32_t n, const uint8_t *tier, const double *arrival,
+                   const double *budget, const uint32_t *fifo_in,
+                   const ds_order_params *params, uint32_t *perm, double *key,
+                   void *ws, size_t ws_bytes, uint32_t flags, ds_stream stream);
+
+/* Workspace size for op at size n (prompts, events or requests); n_groups
+ * is used by DS_OP_CALIBRATE only. */
+size_t ds_workspace_bytes(ds_op op, uint64_t n, uint32_t n_groups);
+
+/* Static description of a status code. */
+const char *ds_status_string(ds_status status);
+
+/* Library version as major*10000 + minor*100 + patch. */
+uint32_t ds_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DRIFTSCHED_H */

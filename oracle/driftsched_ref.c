@@ -23,6 +23,7 @@
  *   dsref_order            FIFO, Priority, Weighted, SJF, Aging Priority
  *                          (Sec. "Scheduling Engine" and its subsections)
  */
+#define _GNU_SOURCE
 #include <math.h>
 #include <stdint.h>
 #include <stdlib.h>

@@ -1,0 +1,194 @@
+// C ABI of the DriftSched admission hot path: argument checks, workspace
+// carving, validation, and kernel launches on the caller's stream.
+#include <math.h>
+#include <string.h>
+
+#include "../../include/driftsched.h"
+#include "common.h"
+#include "kernels.h"
+
+using namespace ds;
+
+namespace {
+
+constexpr size_t kFlagBytes = 256;   // validation word at the start of every workspace
+
+ds_status hip_status(hipError_t e) { return e == hipSuccess ? DS_OK : DS_ERR_HIP; }
+
+bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// Runs the enqueue function twice under DS_VALIDATE: first the data checks
+// (with a cleared flag), then, if the stream reports no violation, the work.
+template <typename F>
+ds_status run(void *ws, uint32_t flags, hipStream_t s, F &&enqueue)
+{
+    uint32_t *flag = static_cast<uint32_t *>(ws);
+    if (flags & DS_VALIDATE) {
+        hipError_t e = fill_u32(flag, 0u, 1, s);
+        if (e == hipSuccess) e = enqueue(flag);
+        uint32_t host = 0;
+        if (e == hipSuccess) e = hipMemcpyAsync(&host, flag, 4, hipMemcpyDeviceToHost, s);
+        if (e == hipSuccess) e = hipStreamSynchronize(s);
+        if (e != hipSuccess) return DS_ERR_HIP;
+        if (host) return DS_ERR_DATA;
+    }
+    return hip_status(enqueue(nullptr));
+}
+
+void *after_flag(void *ws) { return static_cast<uint8_t *>(ws) + kFlagBytes; }
+
+}  // namespace
+
+extern "C" {
+
+uint32_t ds_version(void) { return 10000u; }
+
+const char *ds_status_string(ds_status st)
+{
+    switch (st) {
+    case DS_OK: return "ok";
+    case DS_ERR_NULL: return "a required pointer is NULL";
+    case DS_ERR_ARG: return "argument out of range";
+    case DS_ERR_SIZE: return "size exceeds the supported maximum";
+    case DS_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
+    case DS_ERR_DATA: return "device data violate the call's contract";
+    case DS_ERR_HIP: return "HIP runtime error";
+    case DS_ERR_ALIGN: return "array pointer misaligned";
+    }
+    return "unknown status";
+}
+
+size_t ds_workspace_bytes(ds_op op, uint64_t n, uint32_t n_groups)
+{
+    switch (op) {
+    case DS_OP_CHARACTERIZE: return kFlagBytes + char_ws_bytes(n);
+    case DS_OP_CALIBRATE: return kFlagBytes + cal_ws_bytes(n, n_groups ? n_groups : 1);
+    case DS_OP_SCORE: return kFlagBytes;
+    case DS_OP_ORDER: return kFlagBytes + order_ws_bytes(n);
+    }
+    return 0;
+}
+
+static ds_status check_ws(void *ws, size_t ws_bytes, size_t need)
+{
+    if (!ws || ws_bytes < need || !aligned(ws, 256)) return DS_ERR_WORKSPACE;
+    return DS_OK;
+}
+
+ds_status ds_characterize(const uint8_t *text, uint64_t text_bytes, const uint64_t *offsets,
+                          uint32_t n, uint32_t *counts, void *ws, size_t ws_bytes, uint32_t flags,
+                          ds_stream stream)
+{
+    if (n == 0xFFFFFFFFu) return DS_ERR_SIZE;
+    if (n == 0) return DS_OK;
+    if (!offsets || !counts || (text_bytes > 0 && !text)) return DS_ERR_NULL;
+    if (text && !aligned(text, 16)) return DS_ERR_ALIGN;
+    if (!aligned(offsets, 8) || !aligned(counts, 4)) return DS_ERR_ALIGN;
+    if (text_bytes >= (1ull << 46)) return DS_ERR_SIZE;
+    ds_status st = check_ws(ws, ws_bytes, ds_workspace_bytes(DS_OP_CHARACTERIZE, n, 0));
+    if (st != DS_OK) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    return run(ws, flags, s, [&](uint32_t *flag) {
+        return char_launch(text, text_bytes, offsets, n, counts, after_flag(ws), flag, s);
+    });
+}
+
+ds_status ds_calibrate(const uint32_t *group, const double *est, const uint32_t *observed,
+                       uint64_t n_events, double alpha, uint32_t n_groups, double *state,
+                       double *trace, void *ws, size_t ws_bytes, uint32_t flags, ds_stream stream)
+{
+    if (n_events > DS_MAX_ITEMS) return DS_ERR_SIZE;
+    if (!(alpha >= 0.0 && alpha <= 1.0)) return DS_ERR_ARG;
+    if (n_groups == 0) return DS_ERR_ARG;
+    if (n_events == 0) return DS_OK;
+    if (!group || !est || !observed || !state) return DS_ERR_NULL;
+    if (!aligned(group, 4) || !aligned(est, 8) || !aligned(observed, 4) || !aligned(state, 8) ||
+        (trace && !aligned(trace, 8)))
+        return DS_ERR_ALIGN;
+    ds_status st = check_ws(ws, ws_bytes, ds_workspace_bytes(DS_OP_CALIBRATE, n_events, n_groups));
+    if (st != DS_OK) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    return run(ws, flags, s, [&](uint32_t *flag) {
+        return cal_launch(group, est, observed, (uint32_t)n_events, alpha, n_groups, state, trace,
+                          after_flag(ws), flag, s);
+    });
+}
+
+ds_status ds_score(uint32_t n, const uint32_t *counts, const uint8_t *category,
+                   const uint32_t *tenant, const uint32_t *group, const double *t_base,
+                   uint32_t n_cat, const double *s_tenant, uint32_t n_tenants, const double *state,
+                   uint32_t n_groups, const ds_score_params *params, double *est_base, double *est,
+                   double *budget, uint8_t *job_class, void *ws, size_t ws_bytes, uint32_t flags,
+                   ds_stream stream)
+{
+    if (!params) return DS_ERR_NULL;
+    if (!(params->f_ref > 0.0) || isnan(params->short_max) || isnan(params->medium_max))
+        return DS_ERR_ARG;
+    if (n_cat == 0 || n_tenants == 0 || n_groups == 0) return DS_ERR_ARG;
+    if (n == 0) return DS_OK;
+    if (!counts || !category || !tenant || !group || !t_base || !s_tenant || !state || !est ||
+        !budget || !job_class)
+        return DS_ERR_NULL;
+    if (!aligned(counts, 4) || !aligned(tenant, 4) || !aligned(group, 4) || !aligned(t_base, 8) ||
+        !aligned(s_tenant, 8) || !aligned(state, 8) || !aligned(est, 8) || !aligned(budget, 8) ||
+        (est_base && !aligned(est_base, 8)))
+        return DS_ERR_ALIGN;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (flags & DS_VALIDATE) {
+        ds_status st = check_ws(ws, ws_bytes, ds_workspace_bytes(DS_OP_SCORE, n, 0));
+        if (st != DS_OK) return st;
+    }
+    return run(ws, flags, s, [&](uint32_t *flag) {
+        return score_launch(n, counts, category, tenant, group, t_base, n_cat, s_tenant, n_tenants,
+                            state, n_groups, params->f_ref, params->short_max, params->medium_max,
+                            est_base, est, budget, job_class, flag, s);
+    });
+}
+
+ds_status ds_order(ds_policy policy, uint32_t n, const uint8_t *tier, const double *arrival,
+                   const double *budget, const uint32_t *fifo_in, const ds_order_params *params,
+                   uint32_t *perm, double *key, void *ws, size_t ws_bytes, uint32_t flags,
+                   ds_stream stream)
+{
+    if (!params) return DS_ERR_NULL;
+    if ((int)policy < 0 || (int)policy > 4) return DS_ERR_ARG;
+    if (params->n_tiers < 1 || params->n_tiers > DS_MAX_TIERS) return DS_ERR_ARG;
+    for (uint32_t q = 0; q < params->n_tiers; q++) {
+        if (policy == DS_WEIGHTED && params->weight[q] == 0) return DS_ERR_ARG;
+        if (!isfinite(params->tier_priority[q])) return DS_ERR_ARG;
+    }
+    if (policy == DS_AGING &&
+        (!(params->aging_rate >= 0.0) || !isfinite(params->aging_rate) ||
+         !isfinite(params->t_now) || isnan(params->aging_floor)))
+        return DS_ERR_ARG;
+    if (n > DS_MAX_ITEMS) return DS_ERR_SIZE;
+    if (n == 0) return DS_OK;
+    if (!tier || !arrival || !perm || (policy == DS_SJF && !budget)) return DS_ERR_NULL;
+    if (!aligned(arrival, 8) || !aligned(perm, 4) || (budget && !aligned(budget, 8)) ||
+        (key && !aligned(key, 8)) || (fifo_in && !aligned(fifo_in, 4)))
+        return DS_ERR_ALIGN;
+    ds_status st = check_ws(ws, ws_bytes, ds_workspace_bytes(DS_OP_ORDER, n, 0));
+    if (st != DS_OK) return st;
+    OrderArgs a;
+    memset(&a, 0, sizeof(a));
+    a.policy = (int)policy;
+    a.n = n;
+    a.tier = tier;
+    a.arrival = arrival;
+    a.budget = budget;
+    a.fifo_in = fifo_in;
+    a.n_tiers = params->n_tiers;
+    for (uint32_t q = 0; q < DS_MAX_TIERS; q++) {
+        a.weight[q] = q < params->n_tiers ? params->weight[q] : 1u;
+        a.prio[q] = q < params->n_tiers ? params->tier_priority[q] : 0.0;
+    }
+    a.aging_rate = params->aging_rate;
+    a.t_now = params->t_now;
+    a.aging_floor = params->aging_floor;
+    a.perm = perm;
+    a.key = key;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    return run(ws, flags, s, [&](uint32_t *flag) { return order_launch(a, after_flag(ws), flag, s); });
+}
+
+}  // extern "C"

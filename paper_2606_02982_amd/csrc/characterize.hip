@@ -1,0 +1,461 @@
+// Stage 1: whitespace-proxy word counts over a packed UTF-8 prompt buffer.
+//
+// counts[i] = number of maximal runs of non-whitespace characters in prompt
+// i, whitespace being the 29 code points str.split() separates on
+// (Sec. "Workload Characterization and Token Budget Estimation").
+//
+// Byte formulation used here: byte p of prompt i is a word start when p is
+// not whitespace and either p is the prompt's first byte or byte p-1 is
+// whitespace. A byte is whitespace when it is one of the ASCII separators
+// 09-0D, 1C-20, or belongs to one of the multi-byte separators
+// C2 85, C2 A0, E1 9A 80, E2 80 80..8A, E2 80 A8, E2 80 A9, E2 80 AF,
+// E2 81 9F, E3 80 80 lying entirely inside the prompt. Because none of these
+// sequences starts with a continuation byte, this equals decoding each prompt
+// on its own (undecodable bytes as ordinary characters) and splitting.
+//
+// Layout of the work: the text is cut into equal byte ranges, one per wave;
+// each wave streams its range in rounds of 1 KiB (64 lanes x 16 bytes, 16-byte
+// loads, four rounds in flight) and classifies 4 bytes per 32-bit operation.
+// A round with no prompt boundary and no byte >= 0x80 takes a SWAR fast path;
+// other rounds resolve multi-byte separators and segment starts per lane with
+// 16-bit masks. Word starts are attributed to prompts through prefix sums:
+// each prompt boundary receives the number of word starts in its wave's range
+// before it; a second kernel scans the per-wave totals and a third forms
+// counts[i] = P(offsets[i+1]) - P(offsets[i]). No atomics; results are exact
+// integers independent of scheduling.
+#include "common.h"
+#include "kernels.h"
+
+namespace ds {
+namespace {
+
+constexpr uint32_t kRound = 1024;        // bytes per wave per round
+constexpr uint32_t kLoadRounds = 4;      // rounds loaded together
+constexpr uint32_t kBlock = 256;         // 4 independent waves per block
+constexpr uint32_t kMaxWaves = 16384;
+constexpr uint64_t kNone = ~0ull;
+
+// 0x80 in each byte of x that is an ASCII separator 09-0D or 1C-20.
+// Per-byte exact: every add stays below 0x100 within its byte.
+__device__ __forceinline__ uint32_t ascii_space_hb(uint32_t x)
+{
+    uint32_t a = x & 0x7F7F7F7Fu;
+    uint32_t lt21 = ~((a + 0x5F5F5F5Fu) | x) & 0x80808080u;   // b < 0x21
+    uint32_t ge1c = a + 0x64646464u;                             // b >= 0x1C
+    uint32_t ge09 = a + 0x77777777u;                             // b >= 0x09
+    uint32_t ge0e = a + 0x72727272u;                             // b >= 0x0E
+    return lt21 & (ge1c | (ge09 & ~ge0e));
+}
+
+// 0x80 in each byte >= 0xC0 (UTF-8 lead bytes of multi-byte sequences).
+__device__ __forceinline__ uint32_t lead_hb(uint32_t x) { return x & (x << 1) & 0x80808080u; }
+
+// bits 7, 15, 23, 31 -> bits 0..3
+__device__ __forceinline__ uint32_t compact4(uint32_t hb)
+{
+    return ((hb >> 7) | (hb >> 14) | (hb >> 21) | (hb >> 28)) & 0xFu;
+}
+
+__device__ __forceinline__ uint32_t compact16(uint32_t a, uint32_t b, uint32_t c, uint32_t d)
+{
+    return compact4(a) | (compact4(b) << 4) | (compact4(c) << 8) | (compact4(d) << 12);
+}
+
+// Length (2 or 3) of a multi-byte separator whose bytes are the low bytes of
+// v (little-endian), or 0.
+__device__ __forceinline__ uint32_t mb_space_len(uint32_t v)
+{
+    uint32_t v2 = v & 0xFFFFu, v3 = v & 0xFFFFFFu;
+    if (v2 == 0x85C2u || v2 == 0xA0C2u) return 2;                   // U+0085, U+00A0
+    if (v3 == 0x809AE1u || v3 == 0x9F81E2u || v3 == 0x8080E3u) return 3;  // U+1680, U+205F, U+3000
+    if (v2 == 0x80E2u) {                                             // U+2000..200A, 2028, 2029, 202F
+        uint32_t b2 = (v >> 16) & 0xFFu;
+        if (b2 - 0x80u <= 0x0Au || b2 == 0xA8u || b2 == 0xA9u || b2 == 0xAFu) return 3;
+    }
+    return 0;
+}
+
+__device__ __forceinline__ uint4 load16(const uint8_t *t, uint64_t B, uint64_t c)
+{
+    if (c + 16 <= B) return *reinterpret_cast<const uint4 *>(t + c);
+    uint32_t w[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int k = 0; k < 16; k++)
+        if (c + k < B) w[k >> 2] |= (uint32_t)t[c + k] << (8 * (k & 3));
+    return make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+__device__ __forceinline__ uint32_t load4(const uint8_t *t, uint64_t B, uint64_t c)
+{
+    if (c + 4 <= B) return *reinterpret_cast<const uint32_t *>(t + c);
+    uint32_t w = 0;
+#pragma unroll
+    for (int k = 0; k < 4; k++)
+        if (c + k < B) w |= (uint32_t)t[c + k] << (8 * k);
+    return w;
+}
+
+__device__ __forceinline__ uint64_t win_load(const uint64_t *off, uint32_t N, uint32_t wb, int lane)
+{
+    uint64_t i = (uint64_t)wb + (uint64_t)lane;
+    return i <= (uint64_t)N ? off[i] : kNone;
+}
+
+// First index i in [0, count) with off[i] >= x, or count (wave-cooperative
+// 64-ary search; every step is one round of loads).
+__device__ uint32_t lower_bound_wave(const uint64_t *off, uint64_t count, uint64_t x, int lane)
+{
+    uint64_t lo = 0, hi = count;
+    while (hi - lo > 64) {
+        uint64_t step = (hi - lo + 63) / 64;
+        uint64_t idx = lo + (uint64_t)lane * step;
+        bool lt = idx < hi && off[idx] < x;
+        uint32_t k = (uint32_t)__popcll(__ballot(lt));
+        if (k == 0) { hi = lo; break; }
+        uint64_t nlo = lo + (uint64_t)(k - 1) * step + 1;
+        uint64_t nhi = lo + (uint64_t)k * step;
+        lo = nlo;
+        hi = nhi < hi ? nhi : hi;
+    }
+    bool lt = (lo + (uint64_t)lane < hi) && off[lo + lane] < x;
+    return (uint32_t)(lo + (uint64_t)__popcll(__ballot(lt)));
+}
+
+// Bytes j..j+3 (little-endian) of the 20-byte window d0..d3, dn.
+__device__ __forceinline__ uint32_t bytes_at(const uint4 &d, uint32_t dn, uint32_t j)
+{
+    uint32_t k = j >> 2, s = j & 3u;
+    uint32_t lo = k == 0 ? d.x : k == 1 ? d.y : k == 2 ? d.z : d.w;
+    uint32_t hi = k == 0 ? d.y : k == 1 ? d.z : k == 2 ? d.w : dn;
+    return __builtin_amdgcn_alignbyte(hi, lo, s);
+}
+
+struct WaveState {
+    uint32_t s_ptr;     // first boundary index not yet consumed
+    uint32_t wb;        // boundary index held by lane 0 of win
+    uint64_t win;       // offsets[wb + lane] (kNone past the end)
+    uint64_t running;   // word starts in [ws_start, current round)
+    uint32_t acc;       // per-lane starts of fast rounds not yet in running
+    uint32_t ws_prev;   // whitespace bit of the byte before the round
+    uint32_t spill;     // separator bits spilling into the round's first bytes
+};
+
+struct RangeCtx {
+    const uint64_t *off;
+    uint32_t N;
+    uint64_t ws_start, ws_end;
+    uint32_t *ploc;
+};
+
+__device__ __forceinline__ void ensure_window(WaveState &st, const RangeCtx &rc, uint32_t s, int lane)
+{
+    if (s < st.wb || s - st.wb >= 64) {
+        st.wb = s;
+        st.win = win_load(rc.off, rc.N, s, lane);
+    }
+}
+
+__device__ __forceinline__ void process_round(WaveState &st, const RangeCtx &rc, const uint4 &d,
+                                              uint32_t dn_top, uint64_t rb, int lane)
+{
+    const uint64_t c = rb + 16u * (uint32_t)lane;
+    const uint32_t h0 = ascii_space_hb(d.x), h1 = ascii_space_hb(d.y);
+    const uint32_t h2 = ascii_space_hb(d.z), h3 = ascii_space_hb(d.w);
+    const uint32_t high = (d.x | d.y | d.z | d.w) & 0x80808080u;
+
+    const bool edge = rb < rc.ws_start || rb + kRound > rc.ws_end;
+    const uint64_t lim = rb + kRound + 2;
+    ensure_window(st, rc, st.s_ptr, lane);
+    const uint64_t nb = readlane64(st.win, (int)(st.s_ptr - st.wb));
+    const bool bnd = nb < lim;
+
+    if (!edge && !bnd && st.spill == 0 && __ballot(high != 0) == 0) {
+        // fast path: ASCII only, no prompt boundary, every byte counted
+        uint32_t up = __shfl_up(h3, 1, 64);
+        uint32_t p0 = lane == 0 ? (st.ws_prev << 31) : up;
+        uint32_t s0 = ~h0 & __builtin_amdgcn_alignbyte(h0, p0, 3);
+        uint32_t s1 = ~h1 & __builtin_amdgcn_alignbyte(h1, h0, 3);
+        uint32_t s2 = ~h2 & __builtin_amdgcn_alignbyte(h2, h1, 3);
+        uint32_t s3 = ~h3 & __builtin_amdgcn_alignbyte(h3, h2, 3);
+        st.acc += __popc(s0) + __popc(s1) + __popc(s2) + __popc(s3);
+        st.ws_prev = readlane32(h3 >> 31, 63);
+        st.spill = 0;
+        return;
+    }
+
+    // boundary bits: bit r set if a prompt starts at byte c + r, r in [0, 18)
+    uint32_t bd = 0;
+    if (bnd) {
+        uint32_t s = st.s_ptr;
+        while (true) {
+            ensure_window(st, rc, s, lane);
+            uint32_t kk = s - st.wb;
+            uint64_t m = __ballot((uint32_t)lane >= kk && st.win < lim);
+            uint64_t mm = m;
+            while (mm) {
+                int j = __ffsll((unsigned long long)mm) - 1;
+                mm &= mm - 1;
+                int64_t r = (int64_t)(readlane64(st.win, j) - c);
+                if (r >= 0 && r < 18) bd |= 1u << (uint32_t)r;
+            }
+            if ((m >> 63) & 1ull) { s = st.wb + 64; if (s > rc.N) break; continue; }
+            break;
+        }
+    }
+
+    // whitespace bits of the 16 bytes, then multi-byte separators
+    uint32_t ws16 = compact16(h0, h1, h2, h3);
+    uint32_t lead = compact16(lead_hb(d.x), lead_hb(d.y), lead_hb(d.z), lead_hb(d.w));
+    uint32_t dn = __shfl_down(d.x, 1, 64);
+    if (lane == 63) dn = dn_top;
+    uint32_t cov = 0;
+    while (__ballot(lead != 0)) {
+        if (lead) {
+            uint32_t j = (uint32_t)__ffs(lead) - 1;
+            lead &= lead - 1;
+            uint32_t L = mb_space_len(bytes_at(d, dn, j));
+            if (L) {
+                uint32_t inner = (bd >> (j + 1)) & ((1u << (L - 1)) - 1u);
+                if (!inner) cov |= ((1u << L) - 1u) << j;
+            }
+        }
+    }
+    uint32_t spill_out = cov >> 16;
+    uint32_t spill_in = __shfl_up(spill_out, 1, 64);
+    if (lane == 0) spill_in = st.spill;
+    ws16 |= (cov & 0xFFFFu) | spill_in;
+    uint32_t wsp = __shfl_up(ws16 >> 15, 1, 64) & 1u;
+    if (lane == 0) wsp = st.ws_prev;
+
+    uint32_t valid = 0xFFFFu;
+    if (edge) {
+        int64_t a = (int64_t)rc.ws_start - (int64_t)c;
+        int64_t b = (int64_t)rc.ws_end - (int64_t)c;
+        a = a < 0 ? 0 : a;
+        b = b > 16 ? 16 : b;
+        valid = b > a ? (((1u << (uint32_t)b) - 1u) & ~((1u << (uint32_t)a) - 1u)) : 0u;
+    }
+    uint32_t start = ~ws16 & ((ws16 << 1) | wsp | bd) & valid & 0xFFFFu;
+    uint32_t cnt = (uint32_t)__popc(start);
+    st.ws_prev = readlane32((ws16 >> 15) & 1u, 63);
+    st.spill = readlane32(spill_out, 63);
+
+    if (!bnd) {
+        st.acc += cnt;
+        return;
+    }
+    // boundary round: exact prefix of word starts at every boundary it owns
+    st.running += wave_sum(st.acc);
+    st.acc = 0;
+    uint32_t incl = wave_incl_scan(cnt);
+    uint32_t excl = incl - cnt;
+    uint32_t tot = readlane32(incl, 63);
+    const uint64_t rend = rb + kRound;
+    uint32_t s = st.s_ptr;
+    while (true) {
+        ensure_window(st, rc, s, lane);
+        uint32_t kk = s - st.wb;
+        bool cons = (uint32_t)lane >= kk && st.win < rend;
+        uint64_t m = __ballot(cons);
+        uint64_t rel = st.win - rb;
+        int src = (int)((rel >> 4) & 63u);
+        uint32_t ex = __shfl(excl, src, 64);
+        uint32_t sm = __shfl(start, src, 64);
+        if (cons && st.win >= rc.ws_start && st.win < rc.ws_end) {
+            uint32_t bit = (uint32_t)(rel & 15u);
+            rc.ploc[st.wb + (uint32_t)lane] =
+                (uint32_t)st.running + ex + (uint32_t)__popc(sm & ((1u << bit) - 1u));
+        }
+        if ((m >> 63) & 1ull) { s = st.wb + 64; if (s > rc.N) break; continue; }
+        s = st.wb + kk + (uint32_t)__popcll(m);
+        break;
+    }
+    st.s_ptr = s;
+    st.running += tot;
+}
+
+__global__ __launch_bounds__(kBlock) void k_char_main(const uint8_t *__restrict__ text, uint64_t B,
+                                                      const uint64_t *__restrict__ off, uint32_t N,
+                                                      uint64_t Rw, uint32_t nwaves,
+                                                      uint32_t *__restrict__ ploc,
+                                                      uint64_t *__restrict__ wavetot)
+{
+    const int lane = lane_id();
+    const uint32_t w = blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
+    if (w >= nwaves) return;
+    RangeCtx rc;
+    rc.off = off;
+    rc.N = N;
+    rc.ws_start = (uint64_t)w * Rw;
+    rc.ws_end = rc.ws_start + Rw < B ? rc.ws_start + Rw : B;
+    rc.ploc = ploc;
+    if (rc.ws_start >= B) {
+        if (lane == 0) wavetot[w] = 0;
+        return;
+    }
+    WaveState st;
+    const bool has_pre = rc.ws_start > 0;   // then ws_start >= Rw >= kRound
+    st.s_ptr = lower_bound_wave(off, (uint64_t)N + 1, has_pre ? rc.ws_start - 16 : 0, lane);
+    st.wb = st.s_ptr;
+    st.win = win_load(off, N, st.wb, lane);
+    st.running = 0;
+    st.acc = 0;
+    st.ws_prev = 1;
+    st.spill = 0;
+
+    const uint64_t load_end = rc.ws_end + 16;
+    for (uint64_t sb = has_pre ? rc.ws_start - kRound : rc.ws_start; sb < rc.ws_end;
+         sb += (uint64_t)kRound * kLoadRounds) {
+        uint4 d[kLoadRounds];
+#pragma unroll
+        for (uint32_t u = 0; u < kLoadRounds; u++) {
+            uint64_t rb = sb + (uint64_t)u * kRound;
+            uint64_t c = rb + 16u * (uint32_t)lane;
+            bool pre_only = rb + kRound <= rc.ws_start && lane < 63;
+            d[u] = (!pre_only && c < load_end && c < B) ? load16(text, B, c)
+                                                         : make_uint4(0u, 0u, 0u, 0u);
+        }
+        uint32_t tail = 0;
+        uint64_t tpos = sb + (uint64_t)kRound * kLoadRounds;
+        if (tpos < load_end) tail = load4(text, B, tpos);
+#pragma unroll
+        for (uint32_t u = 0; u < kLoadRounds; u++) {
+            uint64_t rb = sb + (uint64_t)u * kRound;
+            if (rb >= rc.ws_end) break;
+            uint32_t dn_top = u + 1 < kLoadRounds ? readlane32(d[u + 1 < kLoadRounds ? u + 1 : u].x, 0)
+                                                  : tail;
+            process_round(st, rc, d[u], dn_top, rb, lane);
+        }
+    }
+    uint64_t total = st.running + wave_sum(st.acc);
+    if (lane == 0) wavetot[w] = total;
+}
+
+// Exclusive scan of the per-wave totals (one block of 1024 threads).
+__global__ __launch_bounds__(1024) void k_char_scan(const uint64_t *__restrict__ wavetot,
+                                                    uint32_t nwaves, uint64_t *__restrict__ wavepre,
+                                                    uint64_t *__restrict__ total)
+{
+    __shared__ uint64_t part[1024];
+    const uint32_t t = threadIdx.x;
+    const uint32_t per = (nwaves + 1023) / 1024;
+    const uint32_t b = t * per;
+    uint64_t sum = 0;
+    for (uint32_t k = 0; k < per; k++)
+        if (b + k < nwaves) sum += wavetot[b + k];
+    part[t] = sum;
+    __syncthreads();
+    for (uint32_t d = 1; d < 1024; d <<= 1) {
+        uint64_t v = t >= d ? part[t - d] : 0;
+        __syncthreads();
+        part[t] += v;
+        __syncthreads();
+    }
+    uint64_t run = part[t] - sum;   // exclusive
+    for (uint32_t k = 0; k < per; k++) {
+        if (b + k < nwaves) {
+            wavepre[b + k] = run;
+            run += wavetot[b + k];
+        }
+    }
+    if (t == 1023) *total = part[1023];
+}
+
+__device__ __forceinline__ uint64_t prefix_at(uint64_t pos, uint64_t B, uint32_t rw_kib,
+                                              const uint64_t *wavepre, const uint32_t *ploc,
+                                              uint32_t i, uint64_t total)
+{
+    if (pos >= B) return total;
+    uint32_t w = (uint32_t)(pos >> 10) / rw_kib;
+    return wavepre[w] + ploc[i];
+}
+
+__global__ __launch_bounds__(256) void k_char_fin(const uint64_t *__restrict__ off, uint32_t N,
+                                                  uint64_t B, uint32_t rw_kib,
+                                                  const uint64_t *__restrict__ wavepre,
+                                                  const uint32_t *__restrict__ ploc,
+                                                  const uint64_t *__restrict__ total_p,
+                                                  uint32_t *__restrict__ counts)
+{
+    const uint64_t total = *total_p;
+    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < N;
+         i += (uint64_t)gridDim.x * blockDim.x) {
+        uint64_t a = prefix_at(off[i], B, rw_kib, wavepre, ploc, (uint32_t)i, total);
+        uint64_t b = prefix_at(off[i + 1], B, rw_kib, wavepre, ploc, (uint32_t)i + 1, total);
+        counts[i] = (uint32_t)(b - a);
+    }
+}
+
+// DS_VALIDATE: offsets nondecreasing and offsets[N] <= B.
+__global__ void k_char_validate(const uint64_t *__restrict__ off, uint32_t N, uint64_t B,
+                                uint32_t *__restrict__ flag)
+{
+    uint32_t bad = 0;
+    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < N;
+         i += (uint64_t)gridDim.x * blockDim.x)
+        if (off[i] > off[i + 1]) bad = 1;
+    if (blockIdx.x == 0 && threadIdx.x == 0 && off[N] > B) bad = 1;
+    if (bad) atomicOr(flag, 1u);
+}
+
+}  // namespace
+
+size_t char_ws_bytes(uint64_t n)
+{
+    return align_up((n + 1) * 4, 256) + 2 * align_up((uint64_t)kMaxWaves * 8, 256) + 256;
+}
+
+hipError_t char_launch(const uint8_t *text, uint64_t B, const uint64_t *offsets, uint32_t n,
+                       uint32_t *counts, void *ws, uint32_t *flag, hipStream_t s)
+{
+    uint8_t *p = static_cast<uint8_t *>(ws);
+    uint32_t *ploc = reinterpret_cast<uint32_t *>(p);
+    p += align_up(((uint64_t)n + 1) * 4, 256);
+    uint64_t *wavetot = reinterpret_cast<uint64_t *>(p);
+    p += align_up((uint64_t)kMaxWaves * 8, 256);
+    uint64_t *wavepre = reinterpret_cast<uint64_t *>(p);
+    p += align_up((uint64_t)kMaxWaves * 8, 256);
+    uint64_t *total = reinterpret_cast<uint64_t *>(p);
+
+    if (flag) {
+        uint32_t blocks = (uint32_t)(cdiv(n, 256) < 1024 ? cdiv(n, 256) : 1024);
+        if (blocks == 0) blocks = 1;
+        hipLaunchKernelGGL(k_char_validate, dim3(blocks), dim3(256), 0, s, offsets, n, B, flag);
+        return hipGetLastError();
+    }
+    // waves: ranges of whole KiB, at least 4 KiB each, at most kMaxWaves
+    // one wave range per resident wave: CUs x resident blocks per CU x 4
+    static int resident_cache[64];
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    int resident = dev >= 0 && dev < 64 ? resident_cache[dev] : 0;
+    if (resident == 0) {
+        int n_cu = 0, per_cu = 0;
+        e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
+        if (e != hipSuccess) return e;
+        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_char_main, kBlock, 0);
+        if (e != hipSuccess) return e;
+        resident = (n_cu > 0 ? n_cu : 1) * (per_cu > 0 ? per_cu : 1) * (int)(kBlock / 64);
+        if (dev >= 0 && dev < 64) resident_cache[dev] = resident;
+    }
+    uint64_t target = (uint64_t)resident;
+    if (target > kMaxWaves) target = kMaxWaves;
+    uint64_t Rw = align_up(cdiv(B ? B : 1, target), kRound);
+    if (Rw < 4 * kRound) Rw = 4 * kRound;
+    uint32_t nwaves = (uint32_t)cdiv(B, Rw);
+    if (nwaves > 0) {
+        uint32_t blocks = (uint32_t)cdiv(nwaves, kBlock / 64);
+        hipLaunchKernelGGL(k_char_main, dim3(blocks), dim3(kBlock), 0, s, text, B, offsets, n, Rw,
+                           nwaves, ploc, wavetot);
+    }
+    hipLaunchKernelGGL(k_char_scan, dim3(1), dim3(1024), 0, s, wavetot, nwaves, wavepre, total);
+    uint64_t fb = cdiv(n, 256);
+    uint32_t fblocks = (uint32_t)(fb < 4096 ? fb : 4096);
+    if (fblocks)
+        hipLaunchKernelGGL(k_char_fin, dim3(fblocks), dim3(256), 0, s, offsets, n, B,
+                           (uint32_t)(Rw >> 10), wavepre, ploc, total, counts);
+    return hipGetLastError();
+}
+
+}  // namespace ds

@@ -1,0 +1,86 @@
+// Host-side launchers of the DriftSched kernels (internal to the library).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace ds {
+
+// ---- stage 1: characterize -------------------------------------------------
+size_t char_ws_bytes(uint64_t n);
+// flag: device word set non-zero by the validation kernel (NULL: no checks)
+hipError_t char_launch(const uint8_t *text, uint64_t text_bytes, const uint64_t *offsets,
+                       uint32_t n, uint32_t *counts, void *ws, uint32_t *flag,
+                       hipStream_t s);
+
+// ---- radix sort machinery ----------------------------------------------------
+// Producers of (key, value) pairs for the sorts used by calibrate and order.
+enum class SortKind : int {
+    Fifo = 0,      // key = ordered(arrival[j]), val = j
+    Budget = 1,    // key = ordered(budget[fifo[j]]), val = fifo[j]
+    Aging = 2,     // key = ordered(aged score of fifo[j]), val = fifo[j]
+    Class = 3,     // key = cls[tier[fifo[j]]], val = fifo[j]  (1 pass)
+    Tier = 4,      // key = tier[fifo[j]], val = fifo[j]       (1 pass, weighted scatter)
+    Group = 5      // key = group[j], val = j                  (calibration partition)
+};
+
+struct SortInput {
+    SortKind kind;
+    uint32_t n;
+    const double *arrival;
+    const double *budget;
+    const uint8_t *tier;
+    const uint32_t *group;
+    const uint32_t *fifo;      // sequence to reorder (Budget/Aging/Class/Tier)
+    double *key_out;           // optional per-request key (indexed by request)
+    uint32_t n_tiers;
+    uint32_t cls[16];          // Class: priority class of each tier
+    double prio[16];           // Aging/Class keys
+    uint32_t weight[16];       // Tier: weighted round robin
+    double aging_rate, t_now, aging_floor;
+    uint32_t key_bits;         // number of significant key bits (<= 64)
+};
+
+size_t sort_ws_bytes(uint64_t n, uint32_t key_bits);
+// Stable sort of the produced pairs by key; writes the values, in key order,
+// to out (n entries). For SortKind::Tier the values are scattered to their
+// weighted-round-robin positions instead.
+hipError_t sort_launch(const SortInput &in, uint32_t *out, void *ws, hipStream_t s);
+
+// ---- stage 2: calibrate -------------------------------------------------------
+size_t cal_ws_bytes(uint64_t n, uint32_t n_groups);
+hipError_t cal_launch(const uint32_t *group, const double *est, const uint32_t *obs,
+                      uint32_t n, double alpha, uint32_t n_groups, double *state,
+                      double *trace, void *ws, uint32_t *flag, hipStream_t s);
+
+// ---- stage 3: score --------------------------------------------------------------
+hipError_t score_launch(uint32_t n, const uint32_t *counts, const uint8_t *category,
+                        const uint32_t *tenant, const uint32_t *group, const double *t_base,
+                        uint32_t n_cat, const double *s_tenant, uint32_t n_tenants,
+                        const double *state, uint32_t n_groups, double f_ref,
+                        double short_max, double medium_max, double *est_base, double *est,
+                        double *budget, uint8_t *job_class, uint32_t *flag, hipStream_t s);
+
+// ---- stage 4: order ---------------------------------------------------------------
+size_t order_ws_bytes(uint64_t n);
+struct OrderArgs {
+    int policy;
+    uint32_t n;
+    const uint8_t *tier;
+    const double *arrival;
+    const double *budget;
+    const uint32_t *fifo_in;
+    uint32_t n_tiers;
+    uint32_t weight[16];
+    double prio[16];
+    double aging_rate, t_now, aging_floor;
+    uint32_t *perm;
+    double *key;
+};
+hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_t s);
+
+// ---- misc --------------------------------------------------------------------------
+hipError_t fill_u32(uint32_t *p, uint32_t v, uint64_t n, hipStream_t s);
+
+}  // namespace ds

@@ -1,0 +1,159 @@
+// Stage 4: dispatch order of one policy (Sec. "Scheduling Engine").
+//
+// Every policy ends ties in FIFO order, so each one is a stable reordering
+// of the FIFO sequence:
+//   FIFO      radix sort of (arrival, index)
+//   Priority  stable partition of the FIFO sequence by priority class
+//   Weighted  stable partition by tier, then each request goes straight to
+//             its cyclic round-robin position (closed form of the round)
+//   SJF       stable radix sort of the FIFO sequence by budget
+//   Aging     stable radix sort of the FIFO sequence by the aged score
+#include <algorithm>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace ds {
+namespace {
+
+__global__ void k_copy_fifo(const uint32_t *__restrict__ fifo, const double *__restrict__ arrival,
+                            uint32_t n, uint32_t *__restrict__ perm, double *__restrict__ key)
+{
+    for (uint32_t j = blockIdx.x * blockDim.x + threadIdx.x; j < n; j += gridDim.x * blockDim.x) {
+        perm[j] = fifo[j];
+        if (key) key[j] = arrival[j];
+    }
+}
+
+__global__ void k_order_validate(OrderArgs a, uint32_t *__restrict__ flag)
+{
+    uint32_t bad = 0;
+    for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < a.n; i += gridDim.x * blockDim.x) {
+        if (a.tier[i] >= a.n_tiers) bad = 1;
+        if (isnan(a.arrival[i])) bad = 1;
+        if (a.policy == 3 && isnan(a.budget[i])) bad = 1;
+        if (a.fifo_in) {
+            // strictly increasing in (arrival, index) and in range: a permutation
+            uint32_t f = a.fifo_in[i];
+            if (f >= a.n) {
+                bad = 1;
+            } else if (i + 1 < a.n) {
+                uint32_t h = a.fifo_in[i + 1];
+                if (h >= a.n) {
+                    bad = 1;
+                } else {
+                    double x = a.arrival[f], y = a.arrival[h];
+                    if (!(x < y || (x == y && f < h))) bad = 1;
+                }
+            }
+        }
+    }
+    if (bad) atomicOr(flag, 1u);
+}
+
+}  // namespace
+
+size_t order_ws_bytes(uint64_t n)
+{
+    return sort_ws_bytes(n, 64) + align_up(n * 4, 256);
+}
+
+hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_t s)
+{
+    const uint32_t n = a.n;
+    if (flag) {
+        uint64_t nb = cdiv(n, 256);
+        uint32_t vb = (uint32_t)(nb < 1024 ? nb : 1024);
+        if (vb) hipLaunchKernelGGL(k_order_validate, dim3(vb), dim3(256), 0, s, a, flag);
+        return hipGetLastError();
+    }
+    if (n == 0) return hipSuccess;
+    uint8_t *p = static_cast<uint8_t *>(ws);
+    void *sort_ws = p;
+    p += sort_ws_bytes(n, 64);
+    uint32_t *fifo_ws = reinterpret_cast<uint32_t *>(p);
+
+    SortInput in = {};
+    in.n = n;
+    in.arrival = a.arrival;
+    in.budget = a.budget;
+    in.tier = a.tier;
+    in.n_tiers = a.n_tiers;
+    for (int q = 0; q < 16; q++) {
+        in.prio[q] = a.prio[q];
+        in.weight[q] = a.weight[q];
+    }
+    in.aging_rate = a.aging_rate;
+    in.t_now = a.t_now;
+    in.aging_floor = a.aging_floor;
+
+    const uint32_t *fifo = a.fifo_in;
+    hipError_t err;
+    if (!fifo) {
+        uint32_t *target = a.policy == 0 ? a.perm : fifo_ws;
+        SortInput f = in;
+        f.kind = SortKind::Fifo;
+        f.key_bits = 64;
+        f.key_out = a.policy == 0 ? a.key : nullptr;
+        err = sort_launch(f, target, sort_ws, s);
+        if (err != hipSuccess) return err;
+        fifo = target;
+        if (a.policy == 0) return hipSuccess;
+    }
+    in.fifo = fifo;
+    in.key_out = a.key;
+    switch (a.policy) {
+    case 0: {
+        uint64_t nb = cdiv(n, 256);
+        uint32_t blocks = (uint32_t)(nb < 4096 ? nb : 4096);
+        hipLaunchKernelGGL(k_copy_fifo, dim3(blocks), dim3(256), 0, s, fifo, a.arrival, n, a.perm, a.key);
+        return hipGetLastError();
+    }
+    case 1: {
+        // priority classes: rank of each tier's priority among the distinct values
+        double vals[16];
+        for (uint32_t q = 0; q < a.n_tiers; q++) vals[q] = a.prio[q];
+        std::sort(vals, vals + a.n_tiers);
+        uint32_t nd = (uint32_t)(std::unique(vals, vals + a.n_tiers) - vals);
+        for (uint32_t q = 0; q < 16; q++) {
+            uint32_t c = 0;
+            if (q < a.n_tiers) {
+                while (c + 1 < nd && vals[c] < a.prio[q]) c++;
+            }
+            in.cls[q] = c;
+        }
+        in.kind = SortKind::Class;
+        in.key_bits = 8;
+        return sort_launch(in, a.perm, sort_ws, s);
+    }
+    case 2:
+        in.kind = SortKind::Tier;
+        in.key_bits = 8;
+        return sort_launch(in, a.perm, sort_ws, s);
+    case 3:
+        in.kind = SortKind::Budget;
+        in.key_bits = 64;
+        return sort_launch(in, a.perm, sort_ws, s);
+    default:
+        in.kind = SortKind::Aging;
+        in.key_bits = 64;
+        return sort_launch(in, a.perm, sort_ws, s);
+    }
+}
+
+__global__ void k_fill_u32(uint32_t *__restrict__ p, uint32_t v, uint64_t n)
+{
+    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (uint64_t)gridDim.x * blockDim.x)
+        p[i] = v;
+}
+
+hipError_t fill_u32(uint32_t *p, uint32_t v, uint64_t n, hipStream_t s)
+{
+    uint64_t nb = cdiv(n, 256);
+    uint32_t blocks = (uint32_t)(nb < 1024 ? nb : 1024);
+    if (blocks) hipLaunchKernelGGL(k_fill_u32, dim3(blocks), dim3(256), 0, s, p, v, n);
+    return hipGetLastError();
+}
+
+}  // namespace ds

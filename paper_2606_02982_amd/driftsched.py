@@ -1,0 +1,225 @@
+"""Python binding of the DriftSched C ABI (include/driftsched.h).
+
+Argument marshalling only: every step runs in the HIP library
+``libdriftsched.so``. Arrays are torch tensors on the current HIP device;
+work is enqueued on torch's current stream. Unsigned 32-bit arrays travel as
+torch.int32 and uint64 offsets as torch.int64 (same bits for the values the
+library accepts).
+
+The library must be built (``paper_2606_02982_amd.build.build()``); without
+it importing this module fails. There is no fallback.
+"""
+import ctypes
+import os
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libdriftsched.so")
+
+FIFO, PRIORITY, WEIGHTED, SJF, AGING = 0, 1, 2, 3, 4
+POLICIES = {"fifo": FIFO, "priority": PRIORITY, "weighted": WEIGHTED, "sjf": SJF, "aging": AGING}
+OP_CHARACTERIZE, OP_CALIBRATE, OP_SCORE, OP_ORDER = 0, 1, 2, 3
+DS_VALIDATE = 1
+MAX_TIERS = 16
+
+
+class DriftSchedError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__("%s (status %d)" % (msg, status))
+        self.status = status
+
+
+class ScoreParams(ctypes.Structure):
+    _fields_ = [("f_ref", ctypes.c_double), ("short_max", ctypes.c_double),
+                ("medium_max", ctypes.c_double)]
+
+
+class OrderParams(ctypes.Structure):
+    _fields_ = [("n_tiers", ctypes.c_uint32), ("weight", ctypes.c_uint32 * MAX_TIERS),
+                ("tier_priority", ctypes.c_double * MAX_TIERS), ("aging_rate", ctypes.c_double),
+                ("t_now", ctypes.c_double), ("aging_floor", ctypes.c_double)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError("libdriftsched.so is not built (run paper_2606_02982_amd.build.build())")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, u32, u64, f64, i32 = (ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint64,
+                             ctypes.c_double, ctypes.c_int)
+    sz = ctypes.c_size_t
+    lib.ds_characterize.argtypes = [P, u64, P, u32, P, P, sz, u32, P]
+    lib.ds_calibrate.argtypes = [P, P, P, u64, f64, u32, P, P, P, sz, u32, P]
+    lib.ds_score.argtypes = [u32, P, P, P, P, P, u32, P, u32, P, u32, ctypes.POINTER(ScoreParams),
+                             P, P, P, P, P, sz, u32, P]
+    lib.ds_order.argtypes = [i32, u32, P, P, P, P, ctypes.POINTER(OrderParams), P, P, P, sz, u32, P]
+    for f in (lib.ds_characterize, lib.ds_calibrate, lib.ds_score, lib.ds_order):
+        f.restype = i32
+    lib.ds_workspace_bytes.argtypes = [i32, u64, u32]
+    lib.ds_workspace_bytes.restype = sz
+    lib.ds_status_string.argtypes = [i32]
+    lib.ds_status_string.restype = ctypes.c_char_p
+    lib.ds_version.argtypes = []
+    lib.ds_version.restype = u32
+    return lib
+
+
+lib = _load()
+
+_ws_cache = {}
+
+
+def status_string(status):
+    return lib.ds_status_string(int(status)).decode()
+
+
+def workspace_bytes(op, n, n_groups=0):
+    return int(lib.ds_workspace_bytes(int(op), int(n), int(n_groups)))
+
+
+def workspace(op, n, n_groups=0, device=None):
+    """Cached device workspace (uint8 tensor) big enough for op at size n."""
+    device = torch.device(device) if device is not None else torch.device("cuda", torch.cuda.current_device())
+    need = max(workspace_bytes(op, n, n_groups), 256)
+    key = (device.index, op)
+    buf = _ws_cache.get(key)
+    if buf is None or buf.numel() < need:
+        buf = torch.empty(need, dtype=torch.uint8, device=device)
+        _ws_cache[key] = buf
+    return buf
+
+
+def _check(status):
+    if status != 0:
+        raise DriftSchedError(status, status_string(status))
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _flags(validate):
+    return DS_VALIDATE if validate else 0
+
+
+def _dev(t, dtype, name):
+    if not t.is_cuda:
+        raise ValueError("%s must be a device tensor" % name)
+    if t.dtype != dtype:
+        raise ValueError("%s must be %s, got %s" % (name, dtype, t.dtype))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    return t
+
+
+def characterize(text, offsets, counts=None, ws=None, validate=False):
+    """Word counts (str.split() semantics) of the prompts text[offsets[i]:offsets[i+1]]."""
+    _dev(text, torch.uint8, "text")
+    _dev(offsets, torch.int64, "offsets")
+    n = offsets.numel() - 1
+    if counts is None:
+        counts = torch.empty(max(n, 0), dtype=torch.int32, device=offsets.device)
+    _dev(counts, torch.int32, "counts")
+    if ws is None:
+        ws = workspace(OP_CHARACTERIZE, n, 0, offsets.device)
+    _check(lib.ds_characterize(_ptr(text) if text.numel() else None, text.numel(), _ptr(offsets), n,
+                               _ptr(counts), _ptr(ws), ws.numel(), _flags(validate), _stream()))
+    return counts
+
+
+def calibrate(group, est, observed, alpha, state, trace=True, ws=None, validate=False):
+    """EMA calibration factors (Eq. 5/6). Updates ``state`` in place.
+
+    Returns (state, trace or None)."""
+    _dev(group, torch.int32, "group")
+    _dev(est, torch.float64, "est")
+    _dev(observed, torch.int32, "observed")
+    _dev(state, torch.float64, "state")
+    n = group.numel()
+    tr = None
+    if trace is True:
+        tr = torch.empty(n, dtype=torch.float64, device=group.device)
+    elif trace is not None and trace is not False:
+        tr = _dev(trace, torch.float64, "trace")
+    if ws is None:
+        ws = workspace(OP_CALIBRATE, n, state.numel(), group.device)
+    _check(lib.ds_calibrate(_ptr(group), _ptr(est), _ptr(observed), n, float(alpha), state.numel(),
+                            _ptr(state), _ptr(tr), _ptr(ws), ws.numel(), _flags(validate), _stream()))
+    return state, tr
+
+
+def score(counts, category, tenant, group, t_base, s_tenant, state, f_ref=1024.0,
+          short_max=128.0, medium_max=512.0, want_est_base=True, out=None, ws=None,
+          validate=False):
+    """Budget estimate (Eq. 1/2) and class (Eq. 4). Returns (est_base, est, budget, class)."""
+    _dev(counts, torch.int32, "counts")
+    _dev(category, torch.uint8, "category")
+    _dev(tenant, torch.int32, "tenant")
+    _dev(group, torch.int32, "group")
+    _dev(t_base, torch.float64, "t_base")
+    _dev(s_tenant, torch.float64, "s_tenant")
+    _dev(state, torch.float64, "state")
+    n = counts.numel()
+    dev = counts.device
+    if out is None:
+        est_base = torch.empty(n, dtype=torch.float64, device=dev) if want_est_base else None
+        est = torch.empty(n, dtype=torch.float64, device=dev)
+        budget = torch.empty(n, dtype=torch.float64, device=dev)
+        cls = torch.empty(n, dtype=torch.uint8, device=dev)
+    else:
+        est_base, est, budget, cls = out
+    if ws is None and validate:
+        ws = workspace(OP_SCORE, n, 0, dev)
+    p = ScoreParams(float(f_ref), float(short_max), float(medium_max))
+    _check(lib.ds_score(n, _ptr(counts), _ptr(category), _ptr(tenant), _ptr(group), _ptr(t_base),
+                        t_base.numel(), _ptr(s_tenant), s_tenant.numel(), _ptr(state), state.numel(),
+                        ctypes.byref(p), _ptr(est_base), _ptr(est), _ptr(budget), _ptr(cls),
+                        _ptr(ws), ws.numel() if ws is not None else 0, _flags(validate), _stream()))
+    return est_base, est, budget, cls
+
+
+def order_params(n_tiers=3, weights=(4, 2, 1), tier_priority=(0.0, 1.0, 2.0), aging_rate=0.01,
+                 t_now=0.0, aging_floor=0.0):
+    p = OrderParams()
+    p.n_tiers = int(n_tiers)
+    for q in range(MAX_TIERS):
+        p.weight[q] = int(weights[q]) if q < len(weights) else 1
+        p.tier_priority[q] = float(tier_priority[q]) if q < len(tier_priority) else 0.0
+    p.aging_rate = float(aging_rate)
+    p.t_now = float(t_now)
+    p.aging_floor = float(aging_floor)
+    return p
+
+
+def order(policy, tier, arrival, budget=None, fifo=None, params=None, perm=None, key=False,
+          ws=None, validate=False, **kw):
+    """Dispatch permutation of one policy. Returns (perm, key or None)."""
+    if isinstance(policy, str):
+        policy = POLICIES[policy]
+    _dev(tier, torch.uint8, "tier")
+    _dev(arrival, torch.float64, "arrival")
+    if budget is not None:
+        _dev(budget, torch.float64, "budget")
+    if fifo is not None:
+        _dev(fifo, torch.int32, "fifo")
+    n = tier.numel()
+    dev = tier.device
+    if params is None:
+        params = order_params(**kw)
+    if perm is None:
+        perm = torch.empty(n, dtype=torch.int32, device=dev)
+    k = None
+    if key is True:
+        k = torch.empty(n, dtype=torch.float64, device=dev)
+    elif key is not False and key is not None:
+        k = _dev(key, torch.float64, "key")
+    if ws is None:
+        ws = workspace(OP_ORDER, n, 0, dev)
+    _check(lib.ds_order(int(policy), n, _ptr(tier), _ptr(arrival), _ptr(budget), _ptr(fifo),
+                        ctypes.byref(params), _ptr(perm), _ptr(k), _ptr(ws), ws.numel(),
+                        _flags(validate), _stream()))
+    return perm, k

@@ -1,0 +1,108 @@
+"""The C ABI library: it loads, exports every entry point the header
+declares, and rejects bad host arguments before touching a device (these
+calls return before any HIP call, so they run without a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "driftsched.h")
+
+
+@pytest.fixture(scope="module")
+def ds():
+    from paper_2606_02982_amd import driftsched
+    return driftsched
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(ds_[a-z_]+)\s*\(", src)))
+
+
+def test_exports_every_declared_symbol(ds):
+    names = declared_functions()
+    assert names == ["ds_calibrate", "ds_characterize", "ds_order", "ds_score",
+                     "ds_status_string", "ds_version", "ds_workspace_bytes"]
+    for name in names:
+        assert hasattr(ds.lib, name), name
+
+
+def test_status_strings(ds):
+    for code in range(-7, 1):
+        s = ds.status_string(code)
+        assert s and s != "unknown status"
+    assert ds.status_string(-99) == "unknown status"
+    assert ds.lib.ds_version() == 10000
+
+
+def test_workspace_sizes(ds):
+    for op in range(4):
+        sizes = [ds.workspace_bytes(op, n, 64) for n in (0, 1, 4096, 65536, 1 << 20)]
+        assert all(s >= 256 for s in sizes)
+        assert sizes == sorted(sizes)
+    assert ds.workspace_bytes(ds.OP_SCORE, 1 << 20) == 256
+
+
+P = ctypes.c_void_p
+NULL = None
+FAKE = P(0x1000)          # never dereferenced: every call below fails host checks
+FAKE_WS = P(0x100000)
+
+
+def test_characterize_host_errors(ds):
+    f = ds.lib.ds_characterize
+    assert f(NULL, 0, NULL, 0, NULL, NULL, 0, 0, NULL) == 0          # n == 0: nothing to do
+    assert f(FAKE, 16, NULL, 4, FAKE, FAKE_WS, 1 << 30, 0, NULL) == -1
+    assert f(NULL, 16, FAKE, 4, FAKE, FAKE_WS, 1 << 30, 0, NULL) == -1
+    assert f(P(0x1001), 16, FAKE, 4, FAKE, FAKE_WS, 1 << 30, 0, NULL) == -7
+    assert f(FAKE, 16, FAKE, 4, FAKE, FAKE_WS, 16, 0, NULL) == -4      # short workspace
+    assert f(FAKE, 16, FAKE, 4, FAKE, P(0x100001), 1 << 30, 0, NULL) == -4
+    assert f(FAKE, 16, FAKE, 0xFFFFFFFF, FAKE, FAKE_WS, 1 << 30, 0, NULL) == -3
+
+
+def test_calibrate_host_errors(ds):
+    f = ds.lib.ds_calibrate
+    assert f(FAKE, FAKE, FAKE, 10, 1.5, 4, FAKE, NULL, FAKE_WS, 1 << 30, 0, NULL) == -2
+    assert f(FAKE, FAKE, FAKE, 10, -0.1, 4, FAKE, NULL, FAKE_WS, 1 << 30, 0, NULL) == -2
+    assert f(FAKE, FAKE, FAKE, 10, float("nan"), 4, FAKE, NULL, FAKE_WS, 1 << 30, 0, NULL) == -2
+    assert f(FAKE, FAKE, FAKE, 10, 0.1, 0, FAKE, NULL, FAKE_WS, 1 << 30, 0, NULL) == -2
+    assert f(FAKE, FAKE, FAKE, (1 << 30) + 1, 0.1, 4, FAKE, NULL, FAKE_WS, 1 << 40, 0, NULL) == -3
+    assert f(NULL, FAKE, FAKE, 10, 0.1, 4, FAKE, NULL, FAKE_WS, 1 << 30, 0, NULL) == -1
+    assert f(FAKE, FAKE, FAKE, 10, 0.1, 4, FAKE, NULL, FAKE_WS, 100, 0, NULL) == -4
+    assert f(FAKE, FAKE, FAKE, 0, 0.1, 4, FAKE, NULL, NULL, 0, 0, NULL) == 0
+
+
+def test_score_host_errors(ds):
+    f = ds.lib.ds_score
+    good = ds.ScoreParams(1024.0, 128.0, 512.0)
+    bad = ds.ScoreParams(0.0, 128.0, 512.0)
+    args = [FAKE] * 4 + [FAKE, 4, FAKE, 3, FAKE, 3]
+    assert f(10, *args, ctypes.byref(bad), NULL, FAKE, FAKE, FAKE, NULL, 0, 0, NULL) == -2
+    assert f(10, *args, None, NULL, FAKE, FAKE, FAKE, NULL, 0, 0, NULL) == -1
+    assert f(10, NULL, *args[1:], ctypes.byref(good), NULL, FAKE, FAKE, FAKE, NULL, 0, 0, NULL) == -1
+    assert f(10, *args, ctypes.byref(good), NULL, FAKE, FAKE, FAKE, NULL, 0, 1, NULL) == -4
+    assert f(0, *args, ctypes.byref(good), NULL, FAKE, FAKE, FAKE, NULL, 0, 0, NULL) == 0
+
+
+def test_order_host_errors(ds):
+    f = ds.lib.ds_order
+    p = ds.order_params()
+    ws = 1 << 40
+    assert f(7, 10, FAKE, FAKE, FAKE, NULL, ctypes.byref(p), FAKE, NULL, FAKE_WS, ws, 0, NULL) == -2
+    q = ds.order_params(n_tiers=0)
+    assert f(0, 10, FAKE, FAKE, FAKE, NULL, ctypes.byref(q), FAKE, NULL, FAKE_WS, ws, 0, NULL) == -2
+    q = ds.order_params(n_tiers=17)
+    assert f(0, 10, FAKE, FAKE, FAKE, NULL, ctypes.byref(q), FAKE, NULL, FAKE_WS, ws, 0, NULL) == -2
+    q = ds.order_params(weights=(1, 0, 1))
+    assert f(2, 10, FAKE, FAKE, FAKE, NULL, ctypes.byref(q), FAKE, NULL, FAKE_WS, ws, 0, NULL) == -2
+    q = ds.order_params(aging_rate=-1.0)
+    assert f(4, 10, FAKE, FAKE, FAKE, NULL, ctypes.byref(q), FAKE, NULL, FAKE_WS, ws, 0, NULL) == -2
+    assert f(3, 10, FAKE, FAKE, NULL, NULL, ctypes.byref(p), FAKE, NULL, FAKE_WS, ws, 0, NULL) == -1
+    assert f(0, (1 << 30) + 1, FAKE, FAKE, NULL, NULL, ctypes.byref(p), FAKE, NULL, FAKE_WS, ws, 0,
+             NULL) == -3
+    assert f(0, 10, FAKE, FAKE, NULL, NULL, ctypes.byref(p), FAKE, NULL, FAKE_WS, 64, 0, NULL) == -4
+    assert f(0, 0, NULL, NULL, NULL, NULL, ctypes.byref(p), NULL, NULL, NULL, 0, 0, NULL) == 0

@@ -1,0 +1,149 @@
+"""Stage 4 on the GPU against the oracle.
+
+Given the same inputs, every policy's keys are computed with the same
+IEEE operations on both sides, so the permutations must match exactly
+(FIFO, Priority and Weighted are integer-exact; SJF and Aging keys are
+bit-identical here because both sides receive the same budget array).
+"""
+import numpy as np
+import pytest
+
+from paper_2606_02982_amd import synth
+from tests.gpu_util import dev, host
+
+pytestmark = pytest.mark.gpu
+POLICIES = [0, 1, 2, 3, 4]
+
+
+@pytest.fixture(scope="module")
+def ds():
+    from paper_2606_02982_amd import driftsched
+    return driftsched
+
+
+def run(ds, pol, tier, arr, bud=None, fifo=None, **kw):
+    n_tiers = kw.pop("n_tiers", 3)
+    perm, key = ds.order(pol, dev(np.asarray(tier, np.uint8)), dev(np.asarray(arr, np.float64)),
+                         None if bud is None else dev(np.asarray(bud, np.float64)),
+                         fifo=fifo, key=True, n_tiers=n_tiers, **kw)
+    return host(perm, np.uint32), host(key)
+
+
+def check(ds, oracle, pol, tier, arr, bud, **kw):
+    n_tiers = kw.get("n_tiers", 3)
+    okw = dict(weights=kw.get("weights", (4, 2, 1)), tier_priority=kw.get("tier_priority", (0.0, 1.0, 2.0)),
+               aging_rate=kw.get("aging_rate", 0.01), t_now=kw.get("t_now", 0.0),
+               aging_floor=kw.get("aging_floor", 0.0))
+    assert len(okw["weights"]) == n_tiers
+    w_perm, w_key = oracle.order(pol, tier, arr, bud, **okw)
+    g_perm, g_key = run(ds, pol, tier, arr, bud, **kw)
+    bad = np.flatnonzero(g_perm != w_perm)
+    assert bad.size == 0, "policy %d: first difference at %d of %d" % (pol, bad[0], len(w_perm))
+    assert np.array_equal(g_key, w_key)
+    return g_perm
+
+
+def _batch(seed, n, q=None, tiers=3):
+    rng = np.random.default_rng(seed)
+    arr = rng.uniform(0.0, 10.0, n)
+    if q:
+        arr = np.round(arr / q) * q
+    tier = rng.integers(0, tiers, n).astype(np.uint8)
+    bud = np.round(rng.uniform(1, 3000, n), 1)
+    return tier, arr, bud
+
+
+@pytest.mark.parametrize("pol", POLICIES)
+@pytest.mark.parametrize("n", [1, 2, 63, 4095, 4096, 4097, 50000])
+def test_sizes(ds, oracle, pol, n):
+    tier, arr, bud = _batch(n, n)
+    check(ds, oracle, pol, tier, arr, bud, t_now=10.0, aging_rate=0.1)
+
+
+@pytest.mark.parametrize("pol", POLICIES)
+def test_many_ties(ds, oracle, pol):
+    tier, arr, bud = _batch(7, 30000, q=0.25)
+    bud = np.round(bud / 500) * 500
+    arr[:50] = 0.0
+    arr[50:100] = -0.0
+    check(ds, oracle, pol, tier, arr, bud, t_now=10.0, aging_rate=0.3)
+
+
+@pytest.mark.parametrize("pol", POLICIES)
+def test_constant_keys(ds, oracle, pol):
+    n = 9000
+    tier = np.zeros(n, np.uint8)
+    arr = np.full(n, 3.5)
+    bud = np.full(n, 100.0)
+    check(ds, oracle, pol, tier, arr, bud, t_now=3.5)
+
+
+def test_weighted_many_tiers(ds, oracle):
+    rng = np.random.default_rng(4)
+    for Q in (1, 2, 5, 16):
+        w = tuple(int(x) for x in rng.integers(1, 60, Q))
+        tier = rng.integers(0, Q, 20000).astype(np.uint8)
+        tier[tier == Q // 2] = 0 if Q > 1 else tier[tier == Q // 2]
+        arr = rng.uniform(0, 5, 20000)
+        check(ds, oracle, 2, tier, arr, None, n_tiers=Q, weights=w,
+              tier_priority=tuple(float(q) for q in range(Q)))
+    check(ds, oracle, 2, rng.integers(0, 3, 20000).astype(np.uint8), rng.uniform(0, 5, 20000), None,
+          weights=(50, 30, 20))
+
+
+def test_priority_equal_and_unordered_priorities(ds, oracle):
+    tier, arr, bud = _batch(9, 20000, tiers=4)
+    for prio in [(2.0, 0.0, 1.0, -1.0), (1.0, 1.0, 0.0, 1.0), (0.5, 0.5, 0.5, 0.5)]:
+        check(ds, oracle, 1, tier, arr, bud, n_tiers=4, weights=(1, 1, 1, 1), tier_priority=prio)
+        check(ds, oracle, 4, tier, arr, bud, n_tiers=4, weights=(1, 1, 1, 1), tier_priority=prio,
+              t_now=12.0, aging_rate=0.2)
+
+
+@pytest.mark.parametrize("floor,rate", [(0.0, 0.0), (-np.inf, 0.01), (0.5, 1.0), (-1.0, 0.25)])
+def test_aging_parameters(ds, oracle, floor, rate):
+    tier, arr, bud = _batch(10, 40000)
+    check(ds, oracle, 4, tier, arr, bud, t_now=10.0, aging_rate=rate, aging_floor=floor)
+
+
+@pytest.mark.parametrize("name", ["batch4k", "batch64k", "chat1m"])
+def test_workloads(ds, oracle, name):
+    b = synth.generate(name, with_text=False)
+    st, _ = oracle.calibrate(b.ev_group, b.ev_est, b.ev_obs, 0.1, np.ones(b.n_groups), False)
+    _, _, budget, _ = oracle.score(b.words, b.category, b.tenant, b.group, b.t_base, b.s_tenant, st)
+    kw = dict(weights=tuple(int(x) for x in b.weights), tier_priority=tuple(b.tier_priority),
+              aging_rate=b.aging_rate, t_now=b.t_now, aging_floor=b.aging_floor)
+    fifo = None
+    for pol in POLICIES:
+        check(ds, oracle, pol, b.tier, b.arrival, budget, **kw)
+    # reuse of the FIFO permutation gives the same orders
+    fifo, _ = ds.order(0, dev(b.tier), dev(b.arrival), key=False, **kw)
+    for pol in POLICIES:
+        p1, _ = ds.order(pol, dev(b.tier), dev(b.arrival), dev(budget), fifo=fifo, **kw)
+        p2, _ = ds.order(pol, dev(b.tier), dev(b.arrival), dev(budget), **kw)
+        assert np.array_equal(host(p1), host(p2))
+
+
+@pytest.mark.parametrize("k", [1, 17, 40, 64])
+def test_drift_aging_ticks(ds, oracle, k):
+    b = synth.generate("drift4m")
+    n = int(b.tick_n[k - 1])
+    t = float(b.tick_t[k - 1])
+    kw = dict(tier_priority=tuple(b.tier_priority), aging_rate=b.aging_rate, t_now=t,
+              aging_floor=b.aging_floor)
+    check(ds, oracle, 4, b.tier[:n], b.arrival[:n], None, **kw)
+
+
+def test_validate_flag(ds):
+    tier = dev(np.array([0, 3], np.uint8))
+    arr = dev(np.array([0.0, 1.0]))
+    with pytest.raises(ds.DriftSchedError) as e:
+        ds.order(0, tier, arr, validate=True)
+    assert e.value.status == -5
+    tier = dev(np.array([0, 1, 2], np.uint8))
+    arr = dev(np.array([2.0, 1.0, 3.0]))
+    bad_fifo = dev(np.array([0, 1, 2], np.uint32))
+    with pytest.raises(ds.DriftSchedError):
+        ds.order(1, tier, arr, fifo=bad_fifo, validate=True)
+    good = dev(np.array([1, 0, 2], np.uint32))
+    p, _ = ds.order(1, tier, arr, fifo=good, validate=True)
+    assert list(host(p)) == [0, 1, 2]

@@ -1,0 +1,67 @@
+"""Stage 3 on the GPU against the oracle: bit-identical estimates, budgets
+and classes given the same word counts and calibration factors."""
+import numpy as np
+import pytest
+
+from paper_2606_02982_amd import synth
+from tests.gpu_util import dev, host
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def ds():
+    from paper_2606_02982_amd import driftsched
+    return driftsched
+
+
+def run(ds, counts, cat, ten, grp, tb, s, state, **kw):
+    out = ds.score(dev(np.asarray(counts, np.uint32)), dev(np.asarray(cat, np.uint8)),
+                   dev(np.asarray(ten, np.uint32)), dev(np.asarray(grp, np.uint32)),
+                   dev(np.asarray(tb, np.float64)), dev(np.asarray(s, np.float64)),
+                   dev(np.asarray(state, np.float64)), **kw)
+    return [host(x) for x in out]
+
+
+@pytest.mark.parametrize("name", ["batch4k", "batch64k", "chat1m"])
+def test_workload_bitwise(ds, oracle, name):
+    b = synth.generate(name, with_text=False)
+    st, _ = oracle.calibrate(b.ev_group, b.ev_est, b.ev_obs, 0.1, np.ones(b.n_groups), False)
+    want = oracle.score(b.words, b.category, b.tenant, b.group, b.t_base, b.s_tenant, st)
+    got = run(ds, b.words, b.category, b.tenant, b.group, b.t_base, b.s_tenant, st)
+    for g, w in zip(got, want):
+        assert np.array_equal(g, w)
+
+
+def test_random_bitwise(ds, oracle):
+    rng = np.random.default_rng(2)
+    n, T, G = 100003, 37, 11
+    counts = rng.integers(0, 50000, n).astype(np.uint32)
+    cat = rng.integers(0, 4, n).astype(np.uint8)
+    ten = rng.integers(0, T, n).astype(np.uint32)
+    grp = rng.integers(0, G, n).astype(np.uint32)
+    tb = rng.uniform(1, 600, 4)
+    s = rng.uniform(0.5, 2, T)
+    st = rng.uniform(0.3, 3, G)
+    for f_ref, lo, hi in [(1024.0, 128.0, 512.0), (333.3, 1000.0, 5000.0)]:
+        want = oracle.score(counts, cat, ten, grp, tb, s, st, f_ref, lo, hi)
+        got = run(ds, counts, cat, ten, grp, tb, s, st, f_ref=f_ref, short_max=lo, medium_max=hi)
+        for g, w in zip(got, want):
+            assert np.array_equal(g, w)
+
+
+def test_dyadic_and_boundaries(ds):
+    est_base, est, budget, cls = run(ds, [10, 0, 0, 0, 0], [0, 1, 2, 3, 3], [0, 1, 1, 1, 1],
+                                     [0, 1, 1, 1, 1],
+                                     [64.0, 128.0, 512.0, np.nextafter(512.0, 1e9)],
+                                     [1.25, 1.0], [1.5, 1.0])
+    assert est[0] == 121.171875 and budget[0] == 131.171875 and est_base[0] == 80.78125
+    assert list(cls) == [1, 0, 1, 2, 2]
+
+
+def test_out_of_range_is_nan_not_fault(ds):
+    est_base, est, budget, cls = run(ds, [1, 1], [9, 0], [0, 5], [0, 0], [1.0], [1.0], [1.0])
+    assert np.isnan(est[0]) and np.isnan(est[1]) and list(cls) == [2, 2]
+    with pytest.raises(ds.DriftSchedError) as e:
+        run(ds, [1], [9], [0], [0], [1.0], [1.0], [1.0], validate=True)
+    assert e.value.status == -5
