@@ -1,0 +1,234 @@
+"""Benchmark of the DriftSched admission hot path on one MI355X.
+
+One step = the whole hot path over one batch already resident in HBM:
+characterize (word counts of every prompt), calibrate (EMA factors from the
+batch's completion events), score (budgets and classes), and the dispatch
+orders of all five policies (FIFO first; the other four reuse its
+permutation). Default workload: 65,536 requests, 64 tenants, 32-2,048-word
+prompts (the synthetic batch64k workload).
+
+Prints one JSON line: whole-step throughput in requests/s, the roofline of
+the dominant stage (characterize, HBM-bound) from HIP events on the stream it
+runs on, and the single-threaded CPU oracle's throughput on a bounded sample.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+PROFILE = os.path.join(ROOT, "profiles", "pipeline_batch64k.md")
+CHAR_SRC = os.path.join(ROOT, "paper_2606_02982_amd", "csrc", "characterize.hip")
+METRIC = "requests characterized+ordered/sec and achieved HBM GB/s (fraction of peak)"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="batch64k")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="run a plain 1 GiB device copy first (to scale memory counters)")
+    return ap.parse_args()
+
+
+def to_dev(a):
+    import torch
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.uint32:
+        a = a.view(np.int32)
+    elif a.dtype == np.uint64:
+        a = a.view(np.int64)
+    return torch.from_numpy(a).cuda()
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py: this build runs the admission hot path on one GPU; --gpus %d is not "
+              "supported (the design note on sharding is in the documentation)" % args.gpus,
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2606_02982_amd import driftsched as ds
+    from paper_2606_02982_amd import synth
+
+    torch.cuda.set_device(0)
+    wl = synth.WORKLOADS[args.workload]
+    if not wl.has_text or len(wl.policies) < 5:
+        print("bench.py: the step needs a workload with text and all five policies", file=sys.stderr)
+        sys.exit(2)
+    t0 = time.time()
+    b = synth.generate(wl)
+    gen_s = time.time() - t0
+    N = b.n
+    B = len(b.text)
+    print("bench: workload %s, %d requests, %d text bytes (generated in %.1fs)" % (
+        wl.name, N, B, gen_s), file=sys.stderr, flush=True)
+
+    if args.copy_probe:
+        x = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+        y = torch.empty_like(x)
+        for _ in range(3):
+            y.copy_(x)
+        torch.cuda.synchronize()
+        del x, y
+
+    # device-resident inputs
+    text, offsets = to_dev(b.text), to_dev(b.offsets)
+    ev_group, ev_est, ev_obs = to_dev(b.ev_group), to_dev(b.ev_est), to_dev(b.ev_obs)
+    category, tenant, group = to_dev(b.category), to_dev(b.tenant), to_dev(b.group)
+    t_base, s_tenant = to_dev(b.t_base), to_dev(b.s_tenant)
+    tier, arrival = to_dev(b.tier), to_dev(b.arrival)
+    state = torch.ones(b.n_groups, dtype=torch.float64, device="cuda")
+    # outputs
+    counts = torch.empty(N, dtype=torch.int32, device="cuda")
+    trace = torch.empty(N, dtype=torch.float64, device="cuda")
+    sc_out = (torch.empty(N, dtype=torch.float64, device="cuda"),
+              torch.empty(N, dtype=torch.float64, device="cuda"),
+              torch.empty(N, dtype=torch.float64, device="cuda"),
+              torch.empty(N, dtype=torch.uint8, device="cuda"))
+    perms = [torch.empty(N, dtype=torch.int32, device="cuda") for _ in range(5)]
+    params = ds.order_params(weights=tuple(int(w) for w in b.weights),
+                             tier_priority=tuple(b.tier_priority), aging_rate=b.aging_rate,
+                             t_now=b.t_now, aging_floor=b.aging_floor)
+    ws = {op: ds.workspace(op, N, b.n_groups) for op in range(4)}
+    alpha = b.alphas[0]
+    torch.cuda.synchronize()
+
+    def step(ev=None):
+        if ev: ev[0].record()
+        ds.characterize(text, offsets, counts=counts, ws=ws[ds.OP_CHARACTERIZE])
+        if ev: ev[1].record()
+        ds.calibrate(ev_group, ev_est, ev_obs, alpha, state, trace=trace, ws=ws[ds.OP_CALIBRATE])
+        if ev: ev[2].record()
+        budget = sc_out[2]
+        ds.score(counts, category, tenant, group, t_base, s_tenant, state, out=sc_out)
+        if ev: ev[3].record()
+        ds.order(0, tier, arrival, params=params, perm=perms[0], ws=ws[ds.OP_ORDER])
+        for pol in (1, 2, 3, 4):
+            ds.order(pol, tier, arrival, budget, fifo=perms[0], params=params, perm=perms[pol],
+                     ws=ws[ds.OP_ORDER])
+        if ev: ev[4].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        step(evs[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    stage_ms = np.zeros(4)
+    for e in evs:
+        for s in range(4):
+            stage_ms[s] += e[s].elapsed_time(e[s + 1])
+    stage_ms /= args.steps
+    ms_per_step = wall * 1e3 / args.steps
+    value = N * args.steps / wall
+
+    # algorithmic bytes (what the method must move) per stage
+    char_bytes = B + 8 * (N + 1) + 4 * N
+    cal_bytes = 16 * N + 8 * N + 16 * b.n_groups
+    score_bytes = (4 + 1 + 4 + 4) * N + (8 + 8 + 8 + 1) * N
+    order_bytes = (12 + 13 + 13 + 20 + 13) * N
+    char_gbs = char_bytes / (stage_ms[0] * 1e-3) / 1e9
+    total_gbs = (char_bytes + cal_bytes + score_bytes + order_bytes) / (ms_per_step * 1e-3) / 1e9
+
+    # sanity: the counts of the last step equal the generator's word counts
+    assert np.array_equal(counts.cpu().numpy().view(np.uint32), b.words), "counts mismatch"
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(b, args.cpu_seconds)
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "requests/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u8+f64",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "requests": N, "text_bytes": B, "tenants": b.n_groups,
+                   "events": N, "policies": 5, "description": wl.note},
+        "hbm_gbs_step": round(total_gbs, 1),
+        "hbm_frac_step": round(total_gbs / HBM_PEAK_GBS, 4),
+        "stages_ms": {"characterize": round(stage_ms[0], 4), "calibrate": round(stage_ms[1], 4),
+                      "score": round(stage_ms[2], 4), "order_x5": round(stage_ms[3], 4)},
+        "roofline": {"kernel": "characterize (k_char_main + k_char_scan + k_char_fin)",
+                     "bound": "hbm", "achieved": round(char_gbs, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(char_gbs / HBM_PEAK_GBS, 4),
+                     "algorithmic_bytes": int(char_bytes),
+                     "traffic": measured_traffic(wl.name)},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def measured_traffic(workload):
+    """HBM bytes per characterize call from the committed rocprofv3 counter
+    summary, if it was taken on this workload with the current kernel source."""
+    import hashlib
+    if workload != "batch64k" or not os.path.exists(PROFILE):
+        return None
+    vals = {}
+    for line in open(PROFILE):
+        if ":" in line and line.split(":")[0].strip() in ("traffic_bytes_per_call",
+                                                          "characterize_source_sha256_16"):
+            k, v = line.split(":", 1)
+            vals[k.strip()] = v.strip()
+    sha = hashlib.sha256(open(CHAR_SRC, "rb").read()).hexdigest()[:16]
+    if vals.get("characterize_source_sha256_16") != sha:
+        return None
+    return int(vals["traffic_bytes_per_call"])
+
+
+def cpu_baseline(b, budget_s):
+    """The oracle as it stands, single-threaded, on the same step."""
+    import oracle
+    N = b.n
+    kw = dict(weights=tuple(int(w) for w in b.weights), tier_priority=tuple(b.tier_priority),
+              aging_rate=b.aging_rate, t_now=b.t_now, aging_floor=b.aging_floor)
+    reps = 0
+    t0 = time.perf_counter()
+    state = np.ones(b.n_groups)
+    while True:
+        counts = oracle.characterize(b.text, b.offsets)
+        state, _ = oracle.calibrate(b.ev_group, b.ev_est, b.ev_obs, b.alphas[0], state)
+        _, _, budget, _ = oracle.score(counts, b.category, b.tenant, b.group, b.t_base,
+                                       b.s_tenant, state)
+        for pol in range(5):
+            oracle.order(pol, b.tier, b.arrival, budget, **kw)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or reps >= 50:
+            break
+    return {"value": round(N * reps / el, 1), "unit": "requests/s", "cores": 1, "kind": "oracle",
+            "sample": "%d full step(s) of the same %d-request batch (all stages, five orders), "
+                      "%.1f s" % (reps, N, el)}
+
+
+if __name__ == "__main__":
+    main()
