@@ -37,6 +37,8 @@ def parse():
     ap.add_argument("--workload", default="batch64k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--stage", choices=["pipeline", "characterize"], default="pipeline",
+                    help="characterize: time only stage 1 on --workload (any workload with text)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="run a plain 1 GiB device copy first (to scale memory counters)")
     return ap.parse_args()
@@ -67,6 +69,8 @@ def main():
 
     torch.cuda.set_device(0)
     wl = synth.WORKLOADS[args.workload]
+    if args.stage == "characterize":
+        return bench_characterize(args, wl)
     if not wl.has_text or len(wl.policies) < 5:
         print("bench.py: the step needs a workload with text and all five policies", file=sys.stderr)
         sys.exit(2)
@@ -104,7 +108,9 @@ def main():
     params = ds.order_params(weights=tuple(int(w) for w in b.weights),
                              tier_priority=tuple(b.tier_priority), aging_rate=b.aging_rate,
                              t_now=b.t_now, aging_floor=b.aging_floor)
-    ws = {op: ds.workspace(op, N, b.n_groups) for op in range(4)}
+    ws = {op: ds.workspace(op, N, b.n_groups) for op in range(5)}
+    ALL = (0, 1, 2, 3, 4)
+    perm_map = dict(enumerate(perms))
     alpha = b.alphas[0]
     torch.cuda.synchronize()
 
@@ -117,10 +123,8 @@ def main():
         budget = sc_out[2]
         ds.score(counts, category, tenant, group, t_base, s_tenant, state, out=sc_out)
         if ev: ev[3].record()
-        ds.order(0, tier, arrival, params=params, perm=perms[0], ws=ws[ds.OP_ORDER])
-        for pol in (1, 2, 3, 4):
-            ds.order(pol, tier, arrival, budget, fifo=perms[0], params=params, perm=perms[pol],
-                     ws=ws[ds.OP_ORDER])
+        ds.order_multi(ALL, tier, arrival, budget, params=params, perms=perm_map,
+                       ws=ws[ds.OP_ORDER_MULTI])
         if ev: ev[4].record()
 
     for _ in range(args.warmup):
@@ -185,6 +189,37 @@ def main():
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
+
+
+def bench_characterize(args, wl):
+    """Stage 1 alone on one workload: HBM roofline of the word counter."""
+    import torch
+    from paper_2606_02982_amd import driftsched as ds
+    from paper_2606_02982_amd import synth
+    b = synth.generate(wl)
+    N, B = b.n, len(b.text)
+    text, offsets = to_dev(b.text), to_dev(b.offsets)
+    counts = torch.empty(N, dtype=torch.int32, device="cuda")
+    ws = ds.workspace(ds.OP_CHARACTERIZE, N)
+    for _ in range(args.warmup):
+        ds.characterize(text, offsets, counts=counts, ws=ws)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    torch.cuda.synchronize()
+    ev[0].record()
+    for _ in range(args.steps):
+        ds.characterize(text, offsets, counts=counts, ws=ws)
+    ev[1].record()
+    torch.cuda.synchronize()
+    ms = ev[0].elapsed_time(ev[1]) / args.steps
+    assert np.array_equal(counts.cpu().numpy().view(np.uint32), b.words), "counts mismatch"
+    nbytes = B + 8 * (N + 1) + 4 * N
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    print(json.dumps({"metric": "characterize HBM GB/s", "value": round(gbs, 1), "unit": "GB/s",
+                      "frac": round(gbs / HBM_PEAK_GBS, 4), "ms_per_call": round(ms, 4),
+                      "requests_per_s": round(N / (ms * 1e-3), 1), "steps": args.steps,
+                      "config": {"workload": wl.name, "requests": N, "text_bytes": B,
+                                 "nonascii_byte_frac": round(float((b.text >= 0x80).mean()), 4)}}),
+          flush=True)
 
 
 def measured_traffic(workload):

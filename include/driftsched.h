@@ -67,7 +67,8 @@ typedef enum {
     DS_OP_CHARACTERIZE = 0,
     DS_OP_CALIBRATE = 1,
     DS_OP_SCORE = 2,
-    DS_OP_ORDER = 3
+    DS_OP_ORDER = 3,
+    DS_OP_ORDER_MULTI = 4
 } ds_op;
 
 /* flags */
@@ -211,6 +212,27 @@ ds_status ds_order(ds_policy policy, uint32_t n, const uint8_t *tier, const doub
                    const double *budget, const uint32_t *fifo_in,
                    const ds_order_params *params, uint32_t *perm, double *key,
                    void *ws, size_t ws_bytes, uint32_t flags, ds_stream stream);
+
+/*
+ * Stage 4 for several policies in one call: the FIFO permutation is computed
+ * once (or taken from fifo_in) and the requested policy sorts run together,
+ * sharing kernel launches. Results are identical to separate ds_order calls.
+ *
+ *  policy_mask  bit p set: produce the order of policy p (ds_policy values);
+ *               non-zero, at most 0x1F
+ *  perms        HOST array of 5 device pointers; perms[p] (n uint32) must be
+ *               non-NULL for every requested p, others are ignored
+ *  keys         HOST array of 5 device pointers (n double each, or NULL
+ *               entries), or NULL for no keys
+ *  budget       required when DS_SJF is requested
+ *  ws           workspace of ds_workspace_bytes(DS_OP_ORDER_MULTI, n, 0) bytes
+ * Other arguments and errors as ds_order.
+ */
+ds_status ds_order_multi(uint32_t policy_mask, uint32_t n, const uint8_t *tier,
+                         const double *arrival, const double *budget, const uint32_t *fifo_in,
+                         const ds_order_params *params, uint32_t *const *perms,
+                         double *const *keys, void *ws, size_t ws_bytes, uint32_t flags,
+                         ds_stream stream);
 
 /* Workspace size for op at size n (prompts, events or requests); n_groups
  * is used by DS_OP_CALIBRATE only. */

@@ -64,7 +64,8 @@ size_t ds_workspace_bytes(ds_op op, uint64_t n, uint32_t n_groups)
     case DS_OP_CHARACTERIZE: return kFlagBytes + char_ws_bytes(n);
     case DS_OP_CALIBRATE: return kFlagBytes + cal_ws_bytes(n, n_groups ? n_groups : 1);
     case DS_OP_SCORE: return kFlagBytes;
-    case DS_OP_ORDER: return kFlagBytes + order_ws_bytes(n);
+    case DS_OP_ORDER: return kFlagBytes + order_ws_bytes(n, 1);
+    case DS_OP_ORDER_MULTI: return kFlagBytes + order_ws_bytes(n, 4);
     }
     return 0;
 }
@@ -145,33 +146,44 @@ ds_status ds_score(uint32_t n, const uint32_t *counts, const uint8_t *category,
     });
 }
 
-ds_status ds_order(ds_policy policy, uint32_t n, const uint8_t *tier, const double *arrival,
-                   const double *budget, const uint32_t *fifo_in, const ds_order_params *params,
-                   uint32_t *perm, double *key, void *ws, size_t ws_bytes, uint32_t flags,
-                   ds_stream stream)
+static ds_status check_order_params(const ds_order_params *params, uint32_t mask)
 {
     if (!params) return DS_ERR_NULL;
-    if ((int)policy < 0 || (int)policy > 4) return DS_ERR_ARG;
     if (params->n_tiers < 1 || params->n_tiers > DS_MAX_TIERS) return DS_ERR_ARG;
     for (uint32_t q = 0; q < params->n_tiers; q++) {
-        if (policy == DS_WEIGHTED && params->weight[q] == 0) return DS_ERR_ARG;
+        if ((mask & (1u << DS_WEIGHTED)) && params->weight[q] == 0) return DS_ERR_ARG;
         if (!isfinite(params->tier_priority[q])) return DS_ERR_ARG;
     }
-    if (policy == DS_AGING &&
+    if ((mask & (1u << DS_AGING)) &&
         (!(params->aging_rate >= 0.0) || !isfinite(params->aging_rate) ||
          !isfinite(params->t_now) || isnan(params->aging_floor)))
         return DS_ERR_ARG;
+    return DS_OK;
+}
+
+static ds_status order_common(uint32_t mask, uint32_t n, const uint8_t *tier,
+                              const double *arrival, const double *budget,
+                              const uint32_t *fifo_in, const ds_order_params *params,
+                              uint32_t *const *perms, double *const *keys, void *ws,
+                              size_t ws_bytes, ds_op op, uint32_t flags, ds_stream stream)
+{
+    ds_status st = check_order_params(params, mask);
+    if (st != DS_OK) return st;
     if (n > DS_MAX_ITEMS) return DS_ERR_SIZE;
     if (n == 0) return DS_OK;
-    if (!tier || !arrival || !perm || (policy == DS_SJF && !budget)) return DS_ERR_NULL;
-    if (!aligned(arrival, 8) || !aligned(perm, 4) || (budget && !aligned(budget, 8)) ||
-        (key && !aligned(key, 8)) || (fifo_in && !aligned(fifo_in, 4)))
+    if (!tier || !arrival || ((mask & (1u << DS_SJF)) && !budget)) return DS_ERR_NULL;
+    for (int p = 0; p < 5; p++)
+        if ((mask >> p) & 1u) {
+            if (!perms[p]) return DS_ERR_NULL;
+            if (!aligned(perms[p], 4) || (keys && keys[p] && !aligned(keys[p], 8))) return DS_ERR_ALIGN;
+        }
+    if (!aligned(arrival, 8) || (budget && !aligned(budget, 8)) || (fifo_in && !aligned(fifo_in, 4)))
         return DS_ERR_ALIGN;
-    ds_status st = check_ws(ws, ws_bytes, ds_workspace_bytes(DS_OP_ORDER, n, 0));
+    st = check_ws(ws, ws_bytes, ds_workspace_bytes(op, n, 0));
     if (st != DS_OK) return st;
     OrderArgs a;
     memset(&a, 0, sizeof(a));
-    a.policy = (int)policy;
+    a.mask = mask;
     a.n = n;
     a.tier = tier;
     a.arrival = arrival;
@@ -185,10 +197,38 @@ ds_status ds_order(ds_policy policy, uint32_t n, const uint8_t *tier, const doub
     a.aging_rate = params->aging_rate;
     a.t_now = params->t_now;
     a.aging_floor = params->aging_floor;
-    a.perm = perm;
-    a.key = key;
+    for (int p = 0; p < 5; p++) {
+        a.perm[p] = ((mask >> p) & 1u) ? perms[p] : nullptr;
+        a.key[p] = ((mask >> p) & 1u) && keys ? keys[p] : nullptr;
+    }
     hipStream_t s = static_cast<hipStream_t>(stream);
     return run(ws, flags, s, [&](uint32_t *flag) { return order_launch(a, after_flag(ws), flag, s); });
+}
+
+ds_status ds_order(ds_policy policy, uint32_t n, const uint8_t *tier, const double *arrival,
+                   const double *budget, const uint32_t *fifo_in, const ds_order_params *params,
+                   uint32_t *perm, double *key, void *ws, size_t ws_bytes, uint32_t flags,
+                   ds_stream stream)
+{
+    if ((int)policy < 0 || (int)policy > 4) return DS_ERR_ARG;
+    uint32_t *perms[5] = {nullptr, nullptr, nullptr, nullptr, nullptr};
+    double *keys[5] = {nullptr, nullptr, nullptr, nullptr, nullptr};
+    perms[policy] = perm;
+    keys[policy] = key;
+    return order_common(1u << policy, n, tier, arrival, budget, fifo_in, params, perms, keys, ws,
+                        ws_bytes, DS_OP_ORDER, flags, stream);
+}
+
+ds_status ds_order_multi(uint32_t policy_mask, uint32_t n, const uint8_t *tier,
+                         const double *arrival, const double *budget, const uint32_t *fifo_in,
+                         const ds_order_params *params, uint32_t *const *perms,
+                         double *const *keys, void *ws, size_t ws_bytes, uint32_t flags,
+                         ds_stream stream)
+{
+    if (policy_mask == 0 || policy_mask > 0x1Fu) return DS_ERR_ARG;
+    if (!perms) return DS_ERR_NULL;
+    return order_common(policy_mask, n, tier, arrival, budget, fifo_in, params, perms, keys, ws,
+                        ws_bytes, DS_OP_ORDER_MULTI, flags, stream);
 }
 
 }  // extern "C"

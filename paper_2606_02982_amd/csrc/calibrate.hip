@@ -7,11 +7,11 @@
 // associative, so the whole event stream is evaluated as a segmented scan:
 //   1. stable partition of the events by group (radix sort on the group id;
 //      completion order is kept inside each group),
-//   2. per 4096-event tile, per-thread sequential composition of 16 events
+//   2. per 1024-event tile, per-thread sequential composition of 4 events
 //      and a block scan of those: tile aggregates (segment flag, a, b),
 //   3. one block scans the tile aggregates (fixed order: deterministic),
 //   4. each thread composes its carry-in map, applies it to the group's
-//      initial factor, and then runs its 16 events sequentially with the
+//      initial factor, and then runs its 4 events sequentially with the
 //      exact update t1 = (1-alpha) c, t2 = alpha r, c = t1 + t2; it writes
 //      the trace and, at a group's last event, the group's final factor.
 // Every combine runs in a fixed order, so results are run-to-run identical.
@@ -22,7 +22,7 @@ namespace ds {
 namespace {
 
 constexpr int kT = 256;
-constexpr int kPer = 16;
+constexpr int kPer = 4;
 constexpr uint32_t kTile = kT * kPer;
 constexpr uint32_t kNoGroup = 0xFFFFFFFFu;
 
@@ -60,29 +60,55 @@ __device__ __forceinline__ uint32_t group_at(const Events &ev, uint32_t j)
     return e < ev.E ? ev.group[e] : kNoGroup;
 }
 
-// Aggregate of the (up to) 16 events of this thread.
-__device__ Map thread_aggregate(const Events &ev, uint32_t j0)
+// The (up to) kPer events of this thread: groups, and the affine map of each.
+struct Chunk {
+    uint32_t e[kPer], g[kPer];
+    double a[kPer], b[kPer];
+    uint32_t gprev, gnext;   // groups of the events just before and just after
+};
+
+__device__ __forceinline__ void load_chunk(const Events &ev, uint32_t j0, Chunk &c)
+{
+#pragma unroll
+    for (int k = 0; k < kPer; k++) {
+        uint32_t j = j0 + k;
+        uint32_t e = j < ev.E ? ev.sidx[j] : 0u;
+        c.e[k] = e < ev.E ? e : 0u;
+    }
+    c.gprev = j0 == 0 ? kNoGroup : (j0 - 1 < ev.E ? group_at(ev, j0 - 1) : kNoGroup);
+    c.gnext = j0 + kPer < ev.E ? group_at(ev, j0 + kPer) : kNoGroup;
+#pragma unroll
+    for (int k = 0; k < kPer; k++) {
+        uint32_t j = j0 + k;
+        uint32_t g = j < ev.E ? ev.group[c.e[k]] : kNoGroup;
+        double x = j < ev.E ? ev.est[c.e[k]] : 0.0;
+        uint32_t o = j < ev.E ? ev.obs[c.e[k]] : 0u;
+        c.g[k] = g;
+        if (g < ev.G && usable(x)) {
+            double r = (double)o / x;
+            c.a[k] = ev.oma;
+            c.b[k] = ev.alpha * r;
+        } else {
+            c.a[k] = 1.0;
+            c.b[k] = 0.0;
+        }
+    }
+}
+
+// Aggregate of this thread's events.
+__device__ __forceinline__ Map chunk_aggregate(const Events &ev, uint32_t j0, const Chunk &c)
 {
     Map acc = {0u, 1.0, 0.0};
-    uint32_t gprev = j0 == 0 ? kNoGroup : group_at(ev, j0 - 1);
+    uint32_t gprev = c.gprev;
+#pragma unroll
     for (int k = 0; k < kPer; k++) {
         uint32_t j = j0 + k;
         if (j >= ev.E) break;
-        uint32_t e = ev.sidx[j];
-        e = e < ev.E ? e : 0;
-        uint32_t g = ev.group[e];
         Map m;
-        m.f = (j == 0 || g != gprev) ? 1u : 0u;
-        gprev = g;
-        double x = ev.est[e];
-        if (g < ev.G && usable(x)) {
-            double r = (double)ev.obs[e] / x;
-            m.a = ev.oma;
-            m.b = ev.alpha * r;
-        } else {
-            m.a = 1.0;
-            m.b = 0.0;
-        }
+        m.f = (j == 0 || c.g[k] != gprev) ? 1u : 0u;
+        gprev = c.g[k];
+        m.a = c.a[k];
+        m.b = c.b[k];
         acc = combine(acc, m);
     }
     return acc;
@@ -119,7 +145,9 @@ __global__ __launch_bounds__(kT) void k_cal_reduce(Events ev, Map *__restrict__ 
     __shared__ double sa[kT], sb[kT];
     for (uint32_t g = blockIdx.x * kT + threadIdx.x; g < ev.G; g += gridDim.x * kT) c0[g] = state[g];
     const uint32_t j0 = blockIdx.x * kTile + threadIdx.x * kPer;
-    Map v = thread_aggregate(ev, j0);
+    Chunk ck;
+    load_chunk(ev, j0, ck);
+    Map v = chunk_aggregate(ev, j0, ck);
     v = block_scan(v, sf, sa, sb);
     if (threadIdx.x == kT - 1) tile_agg[blockIdx.x] = v;
 }
@@ -172,50 +200,42 @@ __global__ __launch_bounds__(kT) void k_cal_apply(Events ev, const Map *__restri
     __shared__ double sa[kT], sb[kT];
     const int t = threadIdx.x;
     const uint32_t j0 = blockIdx.x * kTile + t * kPer;
-    Map mine = thread_aggregate(ev, j0);
-    Map incl = block_scan(mine, sf, sa, sb);
+    Chunk ck;
+    load_chunk(ev, j0, ck);
+    Map mine = chunk_aggregate(ev, j0, ck);
+    block_scan(mine, sf, sa, sb);
     Map excl = {0u, 1.0, 0.0};
     if (t > 0) { excl.f = sf[t - 1]; excl.a = sa[t - 1]; excl.b = sb[t - 1]; }
     Map cin = combine(tile_carry[blockIdx.x], excl);
-    (void)incl;
     if (j0 >= ev.E) return;
 
-    uint32_t gprev = j0 == 0 ? kNoGroup : group_at(ev, j0 - 1);
-    uint32_t jend = j0 + kPer < ev.E ? j0 + kPer : ev.E;
-    uint32_t e = ev.sidx[j0];
-    e = e < ev.E ? e : 0;
-    uint32_t g = ev.group[e];
     double c;
-    if (g < ev.G) {
-        double base = c0[g];
-        // carry-in: the composite from this group's first event up to j0
-        double tt = cin.a * base;
-        c = tt + cin.b;
-    } else {
-        c = __builtin_nan("");
+    {
+        uint32_t g = ck.g[0];
+        if (g < ev.G) {
+            // carry-in: the composite from this group's first event up to j0
+            double tt = cin.a * c0[g];
+            c = tt + cin.b;
+        } else {
+            c = __builtin_nan("");
+        }
     }
-    for (uint32_t j = j0; j < jend; j++) {
-        bool start = (j == 0 || g != gprev);
-        if (start) c = g < ev.G ? c0[g] : __builtin_nan("");
-        double x = ev.est[e];
-        if (g < ev.G && usable(x)) {
-            double r = (double)ev.obs[e] / x;
-            double t1 = ev.oma * c;
-            double t2 = ev.alpha * r;
-            c = t1 + t2;
+    uint32_t gprev = ck.gprev;
+#pragma unroll
+    for (int k = 0; k < kPer; k++) {
+        uint32_t j = j0 + k;
+        if (j >= ev.E) break;
+        uint32_t g = ck.g[k];
+        if (j == 0 || g != gprev) c = g < ev.G ? c0[g] : __builtin_nan("");
+        if (ck.a[k] != 1.0 || ck.b[k] != 0.0) {
+            // the exact sequential update t1 = (1-alpha) c, t2 = alpha r
+            double t1 = ck.a[k] * c;
+            c = t1 + ck.b[k];
         }
-        if (trace) trace[e] = c;
-        // next event (possibly the first of the next thread)
-        uint32_t gn = kNoGroup, en = 0;
-        if (j + 1 < ev.E) {
-            en = ev.sidx[j + 1];
-            en = en < ev.E ? en : 0;
-            gn = ev.group[en];
-        }
+        if (trace) trace[ck.e[k]] = c;
+        uint32_t gn = (k + 1 < kPer) ? (j + 1 < ev.E ? ck.g[k + 1] : kNoGroup) : ck.gnext;
         if (g < ev.G && (j + 1 == ev.E || gn != g)) state[g] = c;
         gprev = g;
-        g = gn;
-        e = en;
     }
 }
 
@@ -240,7 +260,7 @@ uint32_t bits_for(uint32_t G)
 size_t cal_ws_bytes(uint64_t n, uint32_t n_groups)
 {
     uint64_t T = cdiv(n, kTile);
-    return sort_ws_bytes(n, bits_for(n_groups)) + align_up(n * 4, 256) +
+    return sort_ws_bytes(n, 1) + align_up(n * 4, 256) +
            align_up((uint64_t)n_groups * 8, 256) + 2 * align_up(T * sizeof(Map), 256);
 }
 
@@ -258,7 +278,7 @@ hipError_t cal_launch(const uint32_t *group, const double *est, const uint32_t *
     const uint32_t kb = bits_for(G);
     uint8_t *p = static_cast<uint8_t *>(ws);
     void *sort_ws = p;
-    p += sort_ws_bytes(n, kb);
+    p += sort_ws_bytes(n, 1);
     uint32_t *sidx = reinterpret_cast<uint32_t *>(p);
     p += align_up((uint64_t)n * 4, 256);
     double *c0 = reinterpret_cast<double *>(p);
@@ -268,11 +288,10 @@ hipError_t cal_launch(const uint32_t *group, const double *est, const uint32_t *
     Map *carry = reinterpret_cast<Map *>(p);
 
     SortInput in = {};
-    in.kind = SortKind::Group;
     in.n = n;
     in.group = group;
-    in.key_bits = kb;
-    hipError_t err = sort_launch(in, sidx, sort_ws, s);
+    SortJob job = {SortKind::Group, kb, nullptr, sidx};
+    hipError_t err = sort_launch(in, &job, 1, sort_ws, s);
     if (err != hipSuccess) return err;
 
     Events ev;

@@ -16,13 +16,13 @@
 // Layout of the work: the text is cut into equal byte ranges, one per wave;
 // each wave streams its range in rounds of 1 KiB (64 lanes x 16 bytes, 16-byte
 // loads, four rounds in flight) and classifies 4 bytes per 32-bit operation.
-// A round with no prompt boundary and no byte >= 0x80 takes a SWAR fast path;
-// other rounds resolve multi-byte separators and segment starts per lane with
-// 16-bit masks. Word starts are attributed to prompts through prefix sums:
+// A round with no prompt boundary and no UTF-8 lead byte takes a SWAR fast
+// path; other rounds check multi-byte separators at lead bytes and fold in
+// prompt starts. Carries between lanes move with DPP wave shifts. Word starts are attributed to prompts through prefix sums:
 // each prompt boundary receives the number of word starts in its wave's range
-// before it; a second kernel scans the per-wave totals and a third forms
-// counts[i] = P(offsets[i+1]) - P(offsets[i]). No atomics; results are exact
-// integers independent of scheduling.
+// before it, each wave its total; a second kernel forms counts[i] from the two
+// boundaries' local prefixes and the totals of the waves between them. No
+// atomics; results are exact integers independent of scheduling.
 #include "common.h"
 #include "kernels.h"
 
@@ -75,9 +75,16 @@ __device__ __forceinline__ uint32_t mb_space_len(uint32_t v)
     return 0;
 }
 
+typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+
+// 16 bytes at c (bytes >= B read as 0). The text is streamed once: the
+// full-chunk load is marked nontemporal.
 __device__ __forceinline__ uint4 load16(const uint8_t *t, uint64_t B, uint64_t c)
 {
-    if (c + 16 <= B) return *reinterpret_cast<const uint4 *>(t + c);
+    if (c + 16 <= B) {
+        v4u v = __builtin_nontemporal_load(reinterpret_cast<const v4u *>(t + c));
+        return make_uint4(v.x, v.y, v.z, v.w);
+    }
     uint32_t w[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
     for (int k = 0; k < 16; k++)
@@ -155,13 +162,33 @@ __device__ __forceinline__ void ensure_window(WaveState &st, const RangeCtx &rc,
     }
 }
 
+// bits 0..3 -> bits 7, 15, 23, 31
+__device__ __forceinline__ uint32_t expand4(uint32_t n)
+{
+    return ((n * 0x204081u) & 0x01010101u) << 7;
+}
+
+// Length (2 or 3) of the multi-byte separator starting at the low byte of v
+// (bytes little-endian), or 0; branch-free.
+__device__ __forceinline__ uint32_t mb_space_len_nb(uint32_t v)
+{
+    const uint32_t v2 = v & 0xFFFFu, v3 = v & 0xFFFFFFu, b2 = (v >> 16) & 0xFFu;
+    const bool two = (v2 == 0x85C2u) | (v2 == 0xA0C2u);
+    const bool e2 = (v2 == 0x80E2u) & ((b2 - 0x80u <= 0x0Au) | (b2 == 0xA8u) | (b2 == 0xA9u) | (b2 == 0xAFu));
+    const bool three = (v3 == 0x809AE1u) | (v3 == 0x9F81E2u) | (v3 == 0x8080E3u) | e2;
+    return two ? 2u : (three ? 3u : 0u);
+}
+
+// One 1 KiB round of a wave: lane i holds the 16 bytes at c = rb + 16 i.
+// Masks keep 0x80 per byte ("hb" form) as in the ASCII classification.
 __device__ __forceinline__ void process_round(WaveState &st, const RangeCtx &rc, const uint4 &d,
                                               uint32_t dn_top, uint64_t rb, int lane)
 {
     const uint64_t c = rb + 16u * (uint32_t)lane;
-    const uint32_t h0 = ascii_space_hb(d.x), h1 = ascii_space_hb(d.y);
-    const uint32_t h2 = ascii_space_hb(d.z), h3 = ascii_space_hb(d.w);
-    const uint32_t high = (d.x | d.y | d.z | d.w) & 0x80808080u;
+    uint32_t h0 = ascii_space_hb(d.x), h1 = ascii_space_hb(d.y);
+    uint32_t h2 = ascii_space_hb(d.z), h3 = ascii_space_hb(d.w);
+    const uint32_t l0 = lead_hb(d.x), l1 = lead_hb(d.y), l2 = lead_hb(d.z), l3 = lead_hb(d.w);
+    const bool anylead = __ballot((l0 | l1 | l2 | l3) != 0) != 0;
 
     const bool edge = rb < rc.ws_start || rb + kRound > rc.ws_end;
     const uint64_t lim = rb + kRound + 2;
@@ -169,17 +196,17 @@ __device__ __forceinline__ void process_round(WaveState &st, const RangeCtx &rc,
     const uint64_t nb = readlane64(st.win, (int)(st.s_ptr - st.wb));
     const bool bnd = nb < lim;
 
-    if (!edge && !bnd && st.spill == 0 && __ballot(high != 0) == 0) {
-        // fast path: ASCII only, no prompt boundary, every byte counted
-        uint32_t up = __shfl_up(h3, 1, 64);
-        uint32_t p0 = lane == 0 ? (st.ws_prev << 31) : up;
+    if (!edge && !bnd && st.spill == 0 && !anylead) {
+        // no prompt boundary, no multi-byte character starts here, every
+        // byte counted: whitespace is the ASCII set (continuation bytes of
+        // characters begun earlier are never whitespace on their own)
+        uint32_t p0 = wave_shr1(h3, st.ws_prev << 31);
         uint32_t s0 = ~h0 & __builtin_amdgcn_alignbyte(h0, p0, 3);
         uint32_t s1 = ~h1 & __builtin_amdgcn_alignbyte(h1, h0, 3);
         uint32_t s2 = ~h2 & __builtin_amdgcn_alignbyte(h2, h1, 3);
         uint32_t s3 = ~h3 & __builtin_amdgcn_alignbyte(h3, h2, 3);
         st.acc += __popc(s0) + __popc(s1) + __popc(s2) + __popc(s3);
-        st.ws_prev = readlane32(h3 >> 31, 63);
-        st.spill = 0;
+        st.ws_prev = readlane32(h3, 63) >> 31;
         return;
     }
 
@@ -203,53 +230,73 @@ __device__ __forceinline__ void process_round(WaveState &st, const RangeCtx &rc,
         }
     }
 
-    // whitespace bits of the 16 bytes, then multi-byte separators
-    uint32_t ws16 = compact16(h0, h1, h2, h3);
-    uint32_t lead = compact16(lead_hb(d.x), lead_hb(d.y), lead_hb(d.z), lead_hb(d.w));
-    uint32_t dn = __shfl_down(d.x, 1, 64);
-    if (lane == 63) dn = dn_top;
+    // multi-byte separators, checked at lead bytes; a separator must lie
+    // inside one prompt. cov: bytes covered, bits 16-17 spill to the next lane.
     uint32_t cov = 0;
-    while (__ballot(lead != 0)) {
-        if (lead) {
-            uint32_t j = (uint32_t)__ffs(lead) - 1;
-            lead &= lead - 1;
-            uint32_t L = mb_space_len(bytes_at(d, dn, j));
-            if (L) {
-                uint32_t inner = (bd >> (j + 1)) & ((1u << (L - 1)) - 1u);
-                if (!inner) cov |= ((1u << L) - 1u) << j;
+    if (anylead) {
+        uint32_t lead = compact16(l0, l1, l2, l3);
+        const uint32_t dn = wave_shl1(d.x, dn_top);
+        while (__ballot(lead != 0)) {
+            if (lead) {
+                uint32_t j = (uint32_t)__ffs(lead) - 1;
+                lead &= lead - 1;
+                uint32_t L = mb_space_len_nb(bytes_at(d, dn, j));
+                uint32_t inner = (bd >> (j + 1)) & ((1u << (L > 0 ? L - 1 : 0)) - 1u);
+                if (L && !inner) cov |= ((1u << L) - 1u) << j;
             }
         }
     }
-    uint32_t spill_out = cov >> 16;
-    uint32_t spill_in = __shfl_up(spill_out, 1, 64);
-    if (lane == 0) spill_in = st.spill;
-    ws16 |= (cov & 0xFFFFu) | spill_in;
-    uint32_t wsp = __shfl_up(ws16 >> 15, 1, 64) & 1u;
-    if (lane == 0) wsp = st.ws_prev;
+    const uint32_t spill_out = cov >> 16;
+    const uint32_t spill_in = wave_shr1(spill_out, st.spill);
+    const uint32_t extra = (cov & 0xFFFFu) | spill_in;
+    if (__ballot(extra != 0)) {
+        h0 |= expand4(extra & 0xFu);
+        h1 |= expand4((extra >> 4) & 0xFu);
+        h2 |= expand4((extra >> 8) & 0xFu);
+        h3 |= expand4((extra >> 12) & 0xFu);
+    }
+    st.spill = readlane32(spill_out, 63);
 
-    uint32_t valid = 0xFFFFu;
+    // word starts: not whitespace, and a prompt start or after whitespace
+    const uint32_t p0 = wave_shr1(h3, st.ws_prev << 31);
+    st.ws_prev = readlane32(h3, 63) >> 31;
+    uint32_t s0 = __builtin_amdgcn_alignbyte(h0, p0, 3);
+    uint32_t s1 = __builtin_amdgcn_alignbyte(h1, h0, 3);
+    uint32_t s2 = __builtin_amdgcn_alignbyte(h2, h1, 3);
+    uint32_t s3 = __builtin_amdgcn_alignbyte(h3, h2, 3);
+    if (bnd) {
+        s0 |= expand4(bd & 0xFu);
+        s1 |= expand4((bd >> 4) & 0xFu);
+        s2 |= expand4((bd >> 8) & 0xFu);
+        s3 |= expand4((bd >> 12) & 0xFu);
+    }
+    s0 &= ~h0;
+    s1 &= ~h1;
+    s2 &= ~h2;
+    s3 &= ~h3;
     if (edge) {
         int64_t a = (int64_t)rc.ws_start - (int64_t)c;
         int64_t b = (int64_t)rc.ws_end - (int64_t)c;
         a = a < 0 ? 0 : a;
         b = b > 16 ? 16 : b;
-        valid = b > a ? (((1u << (uint32_t)b) - 1u) & ~((1u << (uint32_t)a) - 1u)) : 0u;
+        uint32_t valid = b > a ? (((1u << (uint32_t)b) - 1u) & ~((1u << (uint32_t)a) - 1u)) : 0u;
+        s0 &= expand4(valid & 0xFu);
+        s1 &= expand4((valid >> 4) & 0xFu);
+        s2 &= expand4((valid >> 8) & 0xFu);
+        s3 &= expand4((valid >> 12) & 0xFu);
     }
-    uint32_t start = ~ws16 & ((ws16 << 1) | wsp | bd) & valid & 0xFFFFu;
-    uint32_t cnt = (uint32_t)__popc(start);
-    st.ws_prev = readlane32((ws16 >> 15) & 1u, 63);
-    st.spill = readlane32(spill_out, 63);
-
+    const uint32_t cnt = (uint32_t)(__popc(s0) + __popc(s1) + __popc(s2) + __popc(s3));
     if (!bnd) {
         st.acc += cnt;
         return;
     }
     // boundary round: exact prefix of word starts at every boundary it owns
-    st.running += wave_sum(st.acc);
+    st.running += readlane32(wave_incl_scan_dpp(st.acc), 63);
     st.acc = 0;
-    uint32_t incl = wave_incl_scan(cnt);
-    uint32_t excl = incl - cnt;
-    uint32_t tot = readlane32(incl, 63);
+    const uint32_t incl = wave_incl_scan_dpp(cnt);
+    const uint32_t excl = incl - cnt;
+    const uint32_t tot = readlane32(incl, 63);
+    const uint32_t start = compact16(s0, s1, s2, s3);
     const uint64_t rend = rb + kRound;
     uint32_t s = st.s_ptr;
     while (true) {
@@ -294,7 +341,7 @@ __global__ __launch_bounds__(kBlock) void k_char_main(const uint8_t *__restrict_
         return;
     }
     WaveState st;
-    const bool has_pre = rc.ws_start > 0;   // then ws_start >= Rw >= kRound
+    const bool has_pre = rc.ws_start > 0;   // then ws_start >= Rw >= 4 KiB
     st.s_ptr = lower_bound_wave(off, (uint64_t)N + 1, has_pre ? rc.ws_start - 16 : 0, lane);
     st.wb = st.s_ptr;
     st.win = win_load(off, N, st.wb, lane);
@@ -304,20 +351,69 @@ __global__ __launch_bounds__(kBlock) void k_char_main(const uint8_t *__restrict_
     st.spill = 0;
 
     const uint64_t load_end = rc.ws_end + 16;
-    for (uint64_t sb = has_pre ? rc.ws_start - kRound : rc.ws_start; sb < rc.ws_end;
-         sb += (uint64_t)kRound * kLoadRounds) {
+    const uint64_t sr_bytes = (uint64_t)kRound * kLoadRounds;
+    if (has_pre) {
+        // the 16 bytes before the range, in lane 63 of a round of its own:
+        // they carry the whitespace state of the byte before the range and
+        // any separator spilling into its first bytes (nothing is counted)
+        uint64_t rb = rc.ws_start - kRound;
+        uint4 dp = lane == 63 ? load16(text, B, rc.ws_start - 16) : make_uint4(0u, 0u, 0u, 0u);
+        uint32_t dn_top = load4(text, B, rc.ws_start);
+        process_round(st, rc, dp, dn_top, rb, lane);
+    }
+    for (uint64_t sb = rc.ws_start; sb < rc.ws_end; sb += sr_bytes) {
+        // whole: every chunk and the trailing dword lie inside the buffer
+        const bool whole = sb + sr_bytes + 4 <= B;
         uint4 d[kLoadRounds];
-#pragma unroll
-        for (uint32_t u = 0; u < kLoadRounds; u++) {
-            uint64_t rb = sb + (uint64_t)u * kRound;
-            uint64_t c = rb + 16u * (uint32_t)lane;
-            bool pre_only = rb + kRound <= rc.ws_start && lane < 63;
-            d[u] = (!pre_only && c < load_end && c < B) ? load16(text, B, c)
-                                                         : make_uint4(0u, 0u, 0u, 0u);
-        }
         uint32_t tail = 0;
-        uint64_t tpos = sb + (uint64_t)kRound * kLoadRounds;
-        if (tpos < load_end) tail = load4(text, B, tpos);
+        if (whole) {
+#pragma unroll
+            for (uint32_t u = 0; u < kLoadRounds; u++) {
+                v4u v = __builtin_nontemporal_load(
+                    reinterpret_cast<const v4u *>(text + sb + (uint64_t)u * kRound + 16u * (uint32_t)lane));
+                d[u] = make_uint4(v.x, v.y, v.z, v.w);
+            }
+            tail = *reinterpret_cast<const uint32_t *>(text + sb + sr_bytes);
+        } else {
+#pragma unroll
+            for (uint32_t u = 0; u < kLoadRounds; u++) {
+                uint64_t c = sb + (uint64_t)u * kRound + 16u * (uint32_t)lane;
+                d[u] = (c < load_end && c < B) ? load16(text, B, c) : make_uint4(0u, 0u, 0u, 0u);
+            }
+            if (sb + sr_bytes < load_end) tail = load4(text, B, sb + sr_bytes);
+        }
+        // fast super-round: all bytes counted, ASCII only, no prompt boundary
+        bool fast = whole && sb + sr_bytes <= rc.ws_end && st.spill == 0;
+        if (fast) {
+            ensure_window(st, rc, st.s_ptr, lane);
+            fast = readlane64(st.win, (int)(st.s_ptr - st.wb)) >= sb + sr_bytes + 2;
+        }
+        if (fast) {
+            uint32_t hi = 0;
+#pragma unroll
+            for (uint32_t u = 0; u < kLoadRounds; u++) hi |= d[u].x | d[u].y | d[u].z | d[u].w;
+            fast = __ballot((hi & 0x80808080u) != 0) == 0;
+        }
+        if (fast) {
+            uint32_t carry = st.ws_prev;
+            uint32_t acc = 0;
+#pragma unroll
+            for (uint32_t u = 0; u < kLoadRounds; u++) {
+                const uint32_t h0 = ascii_space_hb(d[u].x), h1 = ascii_space_hb(d[u].y);
+                const uint32_t h2 = ascii_space_hb(d[u].z), h3 = ascii_space_hb(d[u].w);
+                // lane i receives lane i-1's last dword; lane 0 the carried bit
+                uint32_t p0 = wave_shr1(h3, carry << 31);
+                uint32_t s0 = ~h0 & __builtin_amdgcn_alignbyte(h0, p0, 3);
+                uint32_t s1 = ~h1 & __builtin_amdgcn_alignbyte(h1, h0, 3);
+                uint32_t s2 = ~h2 & __builtin_amdgcn_alignbyte(h2, h1, 3);
+                uint32_t s3 = ~h3 & __builtin_amdgcn_alignbyte(h3, h2, 3);
+                acc += __popc(s0) + __popc(s1) + __popc(s2) + __popc(s3);
+                carry = readlane32(h3, 63) >> 31;
+            }
+            st.acc += acc;
+            st.ws_prev = carry;
+            continue;
+        }
 #pragma unroll
         for (uint32_t u = 0; u < kLoadRounds; u++) {
             uint64_t rb = sb + (uint64_t)u * kRound;
@@ -327,62 +423,39 @@ __global__ __launch_bounds__(kBlock) void k_char_main(const uint8_t *__restrict_
             process_round(st, rc, d[u], dn_top, rb, lane);
         }
     }
-    uint64_t total = st.running + wave_sum(st.acc);
+    uint64_t total = st.running + readlane32(wave_incl_scan_dpp(st.acc), 63);
     if (lane == 0) wavetot[w] = total;
 }
 
-// Exclusive scan of the per-wave totals (one block of 1024 threads).
-__global__ __launch_bounds__(1024) void k_char_scan(const uint64_t *__restrict__ wavetot,
-                                                    uint32_t nwaves, uint64_t *__restrict__ wavepre,
-                                                    uint64_t *__restrict__ total)
-{
-    __shared__ uint64_t part[1024];
-    const uint32_t t = threadIdx.x;
-    const uint32_t per = (nwaves + 1023) / 1024;
-    const uint32_t b = t * per;
-    uint64_t sum = 0;
-    for (uint32_t k = 0; k < per; k++)
-        if (b + k < nwaves) sum += wavetot[b + k];
-    part[t] = sum;
-    __syncthreads();
-    for (uint32_t d = 1; d < 1024; d <<= 1) {
-        uint64_t v = t >= d ? part[t - d] : 0;
-        __syncthreads();
-        part[t] += v;
-        __syncthreads();
-    }
-    uint64_t run = part[t] - sum;   // exclusive
-    for (uint32_t k = 0; k < per; k++) {
-        if (b + k < nwaves) {
-            wavepre[b + k] = run;
-            run += wavetot[b + k];
-        }
-    }
-    if (t == 1023) *total = part[1023];
-}
-
-__device__ __forceinline__ uint64_t prefix_at(uint64_t pos, uint64_t B, uint32_t rw_kib,
-                                              const uint64_t *wavepre, const uint32_t *ploc,
-                                              uint32_t i, uint64_t total)
-{
-    if (pos >= B) return total;
-    uint32_t w = (uint32_t)(pos >> 10) / rw_kib;
-    return wavepre[w] + ploc[i];
-}
-
+// counts[i] from the per-boundary local prefixes and the per-wave totals:
+// the word starts of [a, b) are the starts after a in a's wave, those of the
+// whole waves in between, and the starts before b in b's wave.
 __global__ __launch_bounds__(256) void k_char_fin(const uint64_t *__restrict__ off, uint32_t N,
-                                                  uint64_t B, uint32_t rw_kib,
-                                                  const uint64_t *__restrict__ wavepre,
+                                                  uint64_t B, uint32_t rw_kib, uint32_t nwaves,
+                                                  const uint64_t *__restrict__ wavetot,
                                                   const uint32_t *__restrict__ ploc,
-                                                  const uint64_t *__restrict__ total_p,
                                                   uint32_t *__restrict__ counts)
 {
-    const uint64_t total = *total_p;
     for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < N;
          i += (uint64_t)gridDim.x * blockDim.x) {
-        uint64_t a = prefix_at(off[i], B, rw_kib, wavepre, ploc, (uint32_t)i, total);
-        uint64_t b = prefix_at(off[i + 1], B, rw_kib, wavepre, ploc, (uint32_t)i + 1, total);
-        counts[i] = (uint32_t)(b - a);
+        uint64_t a = off[i], b = off[i + 1];
+        if (b <= a || a >= B) {
+            counts[i] = 0;
+            continue;
+        }
+        uint32_t wa = (uint32_t)(a >> 10) / rw_kib;
+        uint32_t wb;
+        uint64_t tail;
+        if (b >= B) {
+            wb = nwaves;
+            tail = 0;
+        } else {
+            wb = (uint32_t)(b >> 10) / rw_kib;
+            tail = ploc[i + 1];
+        }
+        uint64_t sum = tail;
+        for (uint32_t w = wa; w < wb && w < nwaves; w++) sum += wavetot[w];
+        counts[i] = (uint32_t)(sum - ploc[i]);
     }
 }
 
@@ -402,7 +475,7 @@ __global__ void k_char_validate(const uint64_t *__restrict__ off, uint32_t N, ui
 
 size_t char_ws_bytes(uint64_t n)
 {
-    return align_up((n + 1) * 4, 256) + 2 * align_up((uint64_t)kMaxWaves * 8, 256) + 256;
+    return align_up((n + 1) * 4, 256) + align_up((uint64_t)kMaxWaves * 8, 256);
 }
 
 hipError_t char_launch(const uint8_t *text, uint64_t B, const uint64_t *offsets, uint32_t n,
@@ -412,10 +485,6 @@ hipError_t char_launch(const uint8_t *text, uint64_t B, const uint64_t *offsets,
     uint32_t *ploc = reinterpret_cast<uint32_t *>(p);
     p += align_up(((uint64_t)n + 1) * 4, 256);
     uint64_t *wavetot = reinterpret_cast<uint64_t *>(p);
-    p += align_up((uint64_t)kMaxWaves * 8, 256);
-    uint64_t *wavepre = reinterpret_cast<uint64_t *>(p);
-    p += align_up((uint64_t)kMaxWaves * 8, 256);
-    uint64_t *total = reinterpret_cast<uint64_t *>(p);
 
     if (flag) {
         uint32_t blocks = (uint32_t)(cdiv(n, 256) < 1024 ? cdiv(n, 256) : 1024);
@@ -441,20 +510,18 @@ hipError_t char_launch(const uint8_t *text, uint64_t B, const uint64_t *offsets,
     }
     uint64_t target = (uint64_t)resident;
     if (target > kMaxWaves) target = kMaxWaves;
-    uint64_t Rw = align_up(cdiv(B ? B : 1, target), kRound);
-    if (Rw < 4 * kRound) Rw = 4 * kRound;
+    uint64_t Rw = align_up(cdiv(B ? B : 1, target), (uint64_t)kRound * kLoadRounds);
     uint32_t nwaves = (uint32_t)cdiv(B, Rw);
     if (nwaves > 0) {
         uint32_t blocks = (uint32_t)cdiv(nwaves, kBlock / 64);
         hipLaunchKernelGGL(k_char_main, dim3(blocks), dim3(kBlock), 0, s, text, B, offsets, n, Rw,
                            nwaves, ploc, wavetot);
     }
-    hipLaunchKernelGGL(k_char_scan, dim3(1), dim3(1024), 0, s, wavetot, nwaves, wavepre, total);
     uint64_t fb = cdiv(n, 256);
     uint32_t fblocks = (uint32_t)(fb < 4096 ? fb : 4096);
     if (fblocks)
         hipLaunchKernelGGL(k_char_fin, dim3(fblocks), dim3(256), 0, s, offsets, n, B,
-                           (uint32_t)(Rw >> 10), wavepre, ploc, total, counts);
+                           (uint32_t)(Rw >> 10), nwaves, wavetot, ploc, counts);
     return hipGetLastError();
 }
 

@@ -25,28 +25,34 @@ enum class SortKind : int {
     Group = 5      // key = group[j], val = j                  (calibration partition)
 };
 
+constexpr uint32_t kMaxSorts = 4;   // sorts of one batch (same length, same launches)
+
+// Inputs and parameters shared by the sorts of a batch.
 struct SortInput {
-    SortKind kind;
     uint32_t n;
     const double *arrival;
     const double *budget;
     const uint8_t *tier;
     const uint32_t *group;
     const uint32_t *fifo;      // sequence to reorder (Budget/Aging/Class/Tier)
-    double *key_out;           // optional per-request key (indexed by request)
     uint32_t n_tiers;
     uint32_t cls[16];          // Class: priority class of each tier
     double prio[16];           // Aging/Class keys
     uint32_t weight[16];       // Tier: weighted round robin
     double aging_rate, t_now, aging_floor;
-    uint32_t key_bits;         // number of significant key bits (<= 64)
 };
 
-size_t sort_ws_bytes(uint64_t n, uint32_t key_bits);
-// Stable sort of the produced pairs by key; writes the values, in key order,
-// to out (n entries). For SortKind::Tier the values are scattered to their
-// weighted-round-robin positions instead.
-hipError_t sort_launch(const SortInput &in, uint32_t *out, void *ws, hipStream_t s);
+struct SortJob {
+    SortKind kind;
+    uint32_t key_bits;         // significant key bits (<= 64)
+    double *key_out;           // optional per-request key (indexed by request)
+    uint32_t *out;             // n values in key order (Tier: at weighted positions)
+};
+
+size_t sort_ws_bytes(uint64_t n, uint32_t nsorts);
+// Stable sorts of the produced pairs by key, all jobs in the same launches.
+hipError_t sort_launch(const SortInput &in, const SortJob *jobs, uint32_t nsorts, void *ws,
+                       hipStream_t s);
 
 // ---- stage 2: calibrate -------------------------------------------------------
 size_t cal_ws_bytes(uint64_t n, uint32_t n_groups);
@@ -63,9 +69,9 @@ hipError_t score_launch(uint32_t n, const uint32_t *counts, const uint8_t *categ
                         double *budget, uint8_t *job_class, uint32_t *flag, hipStream_t s);
 
 // ---- stage 4: order ---------------------------------------------------------------
-size_t order_ws_bytes(uint64_t n);
+size_t order_ws_bytes(uint64_t n, uint32_t npolicies);
 struct OrderArgs {
-    int policy;
+    uint32_t mask;             // bit p: produce the order of policy p
     uint32_t n;
     const uint8_t *tier;
     const double *arrival;
@@ -75,8 +81,8 @@ struct OrderArgs {
     uint32_t weight[16];
     double prio[16];
     double aging_rate, t_now, aging_floor;
-    uint32_t *perm;
-    double *key;
+    uint32_t *perm[5];
+    double *key[5];
 };
 hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_t s);
 

@@ -1,4 +1,4 @@
-// Stage 4: dispatch order of one policy (Sec. "Scheduling Engine").
+// Stage 4: dispatch orders (Sec. "Scheduling Engine").
 //
 // Every policy ends ties in FIFO order, so each one is a stable reordering
 // of the FIFO sequence:
@@ -8,6 +8,8 @@
 //             its cyclic round-robin position (closed form of the round)
 //   SJF       stable radix sort of the FIFO sequence by budget
 //   Aging     stable radix sort of the FIFO sequence by the aged score
+// The FIFO sort runs first (unless the caller passes it in); the requested
+// policy sorts then run together in one batch of launches.
 #include <algorithm>
 
 #include "common.h"
@@ -28,10 +30,11 @@ __global__ void k_copy_fifo(const uint32_t *__restrict__ fifo, const double *__r
 __global__ void k_order_validate(OrderArgs a, uint32_t *__restrict__ flag)
 {
     uint32_t bad = 0;
+    const bool need_budget = (a.mask >> 3) & 1u;
     for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < a.n; i += gridDim.x * blockDim.x) {
         if (a.tier[i] >= a.n_tiers) bad = 1;
         if (isnan(a.arrival[i])) bad = 1;
-        if (a.policy == 3 && isnan(a.budget[i])) bad = 1;
+        if (need_budget && isnan(a.budget[i])) bad = 1;
         if (a.fifo_in) {
             // strictly increasing in (arrival, index) and in range: a permutation
             uint32_t f = a.fifo_in[i];
@@ -53,9 +56,10 @@ __global__ void k_order_validate(OrderArgs a, uint32_t *__restrict__ flag)
 
 }  // namespace
 
-size_t order_ws_bytes(uint64_t n)
+size_t order_ws_bytes(uint64_t n, uint32_t npolicies)
 {
-    return sort_ws_bytes(n, 64) + align_up(n * 4, 256);
+    uint32_t nsorts = npolicies < 1 ? 1 : (npolicies > kMaxSorts ? kMaxSorts : npolicies);
+    return align_up(n * 4, 256) + sort_ws_bytes(n, nsorts);
 }
 
 hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_t s)
@@ -67,11 +71,10 @@ hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_
         if (vb) hipLaunchKernelGGL(k_order_validate, dim3(vb), dim3(256), 0, s, a, flag);
         return hipGetLastError();
     }
-    if (n == 0) return hipSuccess;
+    if (n == 0 || a.mask == 0) return hipSuccess;
     uint8_t *p = static_cast<uint8_t *>(ws);
-    void *sort_ws = p;
-    p += sort_ws_bytes(n, 64);
     uint32_t *fifo_ws = reinterpret_cast<uint32_t *>(p);
+    void *sort_ws = p + align_up((uint64_t)n * 4, 256);
 
     SortInput in = {};
     in.n = n;
@@ -87,29 +90,26 @@ hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_
     in.t_now = a.t_now;
     in.aging_floor = a.aging_floor;
 
+    const bool want_fifo = a.mask & 1u;
     const uint32_t *fifo = a.fifo_in;
     hipError_t err;
     if (!fifo) {
-        uint32_t *target = a.policy == 0 ? a.perm : fifo_ws;
-        SortInput f = in;
-        f.kind = SortKind::Fifo;
-        f.key_bits = 64;
-        f.key_out = a.policy == 0 ? a.key : nullptr;
-        err = sort_launch(f, target, sort_ws, s);
+        SortJob job = {SortKind::Fifo, 64, want_fifo ? a.key[0] : nullptr,
+                       want_fifo ? a.perm[0] : fifo_ws};
+        err = sort_launch(in, &job, 1, sort_ws, s);
         if (err != hipSuccess) return err;
-        fifo = target;
-        if (a.policy == 0) return hipSuccess;
-    }
-    in.fifo = fifo;
-    in.key_out = a.key;
-    switch (a.policy) {
-    case 0: {
+        fifo = job.out;
+    } else if (want_fifo) {
         uint64_t nb = cdiv(n, 256);
         uint32_t blocks = (uint32_t)(nb < 4096 ? nb : 4096);
-        hipLaunchKernelGGL(k_copy_fifo, dim3(blocks), dim3(256), 0, s, fifo, a.arrival, n, a.perm, a.key);
-        return hipGetLastError();
+        hipLaunchKernelGGL(k_copy_fifo, dim3(blocks), dim3(256), 0, s, fifo, a.arrival, n,
+                           a.perm[0], a.key[0]);
     }
-    case 1: {
+    in.fifo = fifo;
+
+    SortJob jobs[kMaxSorts];
+    uint32_t nj = 0;
+    if (a.mask & (1u << 1)) {
         // priority classes: rank of each tier's priority among the distinct values
         double vals[16];
         for (uint32_t q = 0; q < a.n_tiers; q++) vals[q] = a.prio[q];
@@ -117,28 +117,17 @@ hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_
         uint32_t nd = (uint32_t)(std::unique(vals, vals + a.n_tiers) - vals);
         for (uint32_t q = 0; q < 16; q++) {
             uint32_t c = 0;
-            if (q < a.n_tiers) {
+            if (q < a.n_tiers)
                 while (c + 1 < nd && vals[c] < a.prio[q]) c++;
-            }
             in.cls[q] = c;
         }
-        in.kind = SortKind::Class;
-        in.key_bits = 8;
-        return sort_launch(in, a.perm, sort_ws, s);
+        jobs[nj++] = {SortKind::Class, 8, a.key[1], a.perm[1]};
     }
-    case 2:
-        in.kind = SortKind::Tier;
-        in.key_bits = 8;
-        return sort_launch(in, a.perm, sort_ws, s);
-    case 3:
-        in.kind = SortKind::Budget;
-        in.key_bits = 64;
-        return sort_launch(in, a.perm, sort_ws, s);
-    default:
-        in.kind = SortKind::Aging;
-        in.key_bits = 64;
-        return sort_launch(in, a.perm, sort_ws, s);
-    }
+    if (a.mask & (1u << 2)) jobs[nj++] = {SortKind::Tier, 8, a.key[2], a.perm[2]};
+    if (a.mask & (1u << 3)) jobs[nj++] = {SortKind::Budget, 64, a.key[3], a.perm[3]};
+    if (a.mask & (1u << 4)) jobs[nj++] = {SortKind::Aging, 64, a.key[4], a.perm[4]};
+    if (nj == 0) return hipGetLastError();
+    return sort_launch(in, jobs, nj, sort_ws, s);
 }
 
 __global__ void k_fill_u32(uint32_t *__restrict__ p, uint32_t v, uint64_t n)

@@ -1,20 +1,27 @@
-// Stable LSD radix sort of (key, value) pairs, 8-bit digits, one kernel per
-// digit pass with decoupled look-back between tiles.
+// Stable LSD radix sorts of (key, value) pairs, 8-bit digits, one kernel per
+// digit pass, with decoupled look-back between tiles. Several independent
+// sorts of the same length run in the same launches (grid.y = sort).
 //
 // Used for: the FIFO rank (key = arrival), SJF and Aging (key = budget or
-// aged score, sorting the FIFO sequence so that ties keep FIFO order), the
-// tier partitions of Priority and Weighted (one pass), and the group
-// partition of the calibration scan.
+// aged score over the FIFO sequence, so that ties keep FIFO order), the
+// one-pass partitions of Priority (priority class) and Weighted (tier, then
+// the closed-form round-robin position), and the group partition of the
+// calibration scan.
 //
-// Kernels of one sort:
-//   k_sort_zero  clears the digit histograms, tile tickets and look-back words
-//   k_sort_init  produces the pairs from the inputs, counts all passes' digits
-//   k_sort_plan  exclusive digit offsets; marks passes whose digit is the same
-//                for every key (they are skipped) and routes the buffers
-//   k_sort_pass  per 4096-key tile: wave-level match ranking (ballots over the
-//                digit bits), per-wave LDS counters, look-back over earlier
-//                tiles' per-digit counts, reorder through LDS, coalesced runs
-//                of global writes
+// Launches of one batch of sorts:
+//   k_sort_init  produces the pairs from the inputs, writes each block's digit
+//                histograms of every pass (no atomics), clears the tickets
+//                and look-back words of the passes
+//   k_sort_plan  one block per (pass, sort): sums the block histograms into
+//                exclusive digit offsets and marks a pass whose digit is the
+//                same for every key (it is skipped)
+//   k_sort_pass  one per digit pass: per tile of 256*R keys, wave ranking by
+//                ballots over the digit bits, per-wave LDS counters,
+//                look-back over earlier tiles' per-digit counts (windows of
+//                16 predecessors loaded at once, bounded wait), reorder
+//                through LDS, coalesced runs of global writes. The buffer a
+//                pass reads, and whether it is the last active pass, follow
+//                from the active flags.
 // Tiles take tickets from an atomic counter, so a tile only ever waits on
 // tiles that are already running.
 #include "common.h"
@@ -24,30 +31,42 @@ namespace ds {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kPer = 16;
-constexpr uint32_t kTile = kThreads * kPer;   // 4096 keys
 constexpr int kMaxPasses = 8;
 constexpr uint32_t kAgg = 1u << 30;
 constexpr uint32_t kPre = 2u << 30;
 constexpr uint32_t kValMask = (1u << 30) - 1u;
+constexpr uint32_t kSpinLimit = 1u << 22;   // bounded waits (never reached in normal runs)
+constexpr uint32_t kSmallN = 1u << 18;      // below: 1024-key tiles, above: 4096
+
+constexpr uint32_t kInitBlocks = 256;     // block histograms per sort (at most)
 
 struct SortCtl {
-    uint32_t hist[kMaxPasses][256];
     uint32_t excl[kMaxPasses][256];
     uint32_t ticket[kMaxPasses];
     uint32_t active[kMaxPasses];
-    uint32_t src[kMaxPasses];
-    int32_t last;
-    uint32_t pad[7];
+    uint32_t error;
+    uint32_t pad[15];
 };
 
-struct SortBufs {
+struct SortDesc {
+    SortKind kind;
+    uint32_t passes;
+    double *key_out;
+    uint32_t *out;
     SortCtl *ctl;
+    uint32_t *bhist;       // [init blocks][passes][256]
     uint64_t *key[2];
     uint32_t *val[2];
-    uint32_t *status;       // [passes][tiles][256]
-    uint32_t passes;
+    uint32_t *status;      // [passes][tiles][256]
+};
+
+struct SortBatch {
+    SortInput in;          // shared inputs and parameters
+    uint32_t n;
     uint32_t tiles;
+    uint32_t nsorts;
+    uint32_t init_blocks;
+    SortDesc s[kMaxSorts];
 };
 
 __host__ __device__ inline uint32_t n_passes(uint32_t key_bits)
@@ -56,28 +75,29 @@ __host__ __device__ inline uint32_t n_passes(uint32_t key_bits)
     return p == 0 ? 1 : (p > kMaxPasses ? kMaxPasses : p);
 }
 
-__device__ __forceinline__ void produce(const SortInput &in, uint32_t j, uint64_t &k, uint32_t &v)
+__device__ __forceinline__ void produce(const SortInput &in, SortKind kind, double *key_out,
+                                        uint32_t n, uint32_t j, uint64_t &k, uint32_t &v)
 {
-    switch (in.kind) {
+    switch (kind) {
     case SortKind::Fifo: {
         double a = in.arrival[j];
         k = ordered_bits(a);
         v = j;
-        if (in.key_out) in.key_out[j] = a;
+        if (key_out) key_out[j] = a;
         break;
     }
     case SortKind::Budget: {
         uint32_t i = in.fifo[j];
-        i = i < in.n ? i : 0;
+        i = i < n ? i : 0;
         double b = in.budget[i];
         k = ordered_bits(b);
         v = i;
-        if (in.key_out) in.key_out[i] = b;
+        if (key_out) key_out[i] = b;
         break;
     }
     case SortKind::Aging: {
         uint32_t i = in.fifo[j];
-        i = i < in.n ? i : 0;
+        i = i < n ? i : 0;
         uint32_t q = in.tier[i];
         q = q < 16 ? q : 15;
         double w = in.t_now - in.arrival[i];
@@ -87,22 +107,22 @@ __device__ __forceinline__ void produce(const SortInput &in, uint32_t j, uint64_
         if (e < in.aging_floor) e = in.aging_floor;
         k = ordered_bits(e);
         v = i;
-        if (in.key_out) in.key_out[i] = e;
+        if (key_out) key_out[i] = e;
         break;
     }
     case SortKind::Class: {
         uint32_t i = in.fifo[j];
-        i = i < in.n ? i : 0;
+        i = i < n ? i : 0;
         uint32_t q = in.tier[i];
         q = q < 16 ? q : 15;
         k = in.cls[q];
         v = i;
-        if (in.key_out) in.key_out[i] = in.prio[q];
+        if (key_out) key_out[i] = in.prio[q];
         break;
     }
     case SortKind::Tier: {
         uint32_t i = in.fifo[j];
-        i = i < in.n ? i : 0;
+        i = i < n ? i : 0;
         uint32_t q = in.tier[i];
         k = q < 16 ? q : 15;
         v = i;
@@ -113,36 +133,6 @@ __device__ __forceinline__ void produce(const SortInput &in, uint32_t j, uint64_
         v = j;
         break;
     }
-    }
-}
-
-__global__ void k_sort_zero(SortCtl *__restrict__ ctl, uint32_t *__restrict__ status, uint64_t words)
-{
-    uint64_t t = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
-    uint32_t *c = reinterpret_cast<uint32_t *>(ctl);
-    for (uint64_t i = t; i < sizeof(SortCtl) / 4; i += stride) c[i] = 0;
-    for (uint64_t i = t; i < words; i += stride) status[i] = 0;
-}
-
-__global__ __launch_bounds__(256) void k_sort_init(SortInput in, SortBufs sb)
-{
-    __shared__ uint32_t h[kMaxPasses][256];
-    const uint32_t P = sb.passes;
-    for (uint32_t i = threadIdx.x; i < P * 256; i += blockDim.x) (&h[0][0])[i] = 0;
-    __syncthreads();
-    for (uint32_t j = blockIdx.x * blockDim.x + threadIdx.x; j < in.n; j += gridDim.x * blockDim.x) {
-        uint64_t k;
-        uint32_t v;
-        produce(in, j, k, v);
-        sb.key[0][j] = k;
-        sb.val[0][j] = v;
-        for (uint32_t p = 0; p < P; p++) atomicAdd(&h[p][(k >> (8 * p)) & 255u], 1u);
-    }
-    __syncthreads();
-    for (uint32_t i = threadIdx.x; i < P * 256; i += blockDim.x) {
-        uint32_t c = (&h[0][0])[i];
-        if (c) atomicAdd(&sb.ctl->hist[i / 256][i % 256], c);
     }
 }
 
@@ -159,42 +149,101 @@ __device__ uint32_t block_excl_scan256(uint32_t x, uint32_t *tmp4)
     return off + incl - x;
 }
 
-__global__ __launch_bounds__(256) void k_sort_plan(SortBufs sb, uint32_t n)
+constexpr int kInitPer = 4;   // keys per thread per step of the init kernel
+
+__global__ __launch_bounds__(256) void k_sort_init(SortBatch b, uint64_t status_words)
 {
-    __shared__ uint32_t tmp4[4];
-    __shared__ uint32_t act[kMaxPasses];
-    const uint32_t d = threadIdx.x;
-    for (uint32_t p = 0; p < sb.passes; p++) {
-        uint32_t c = sb.ctl->hist[p][d];
-        int full = __syncthreads_or(c == n ? 1 : 0);
-        uint32_t e = block_excl_scan256(c, tmp4);
-        sb.ctl->excl[p][d] = e;
-        if (d == 0) act[p] = full ? 0u : 1u;
+    __shared__ uint32_t h[kMaxPasses][256];
+    const SortDesc &d = b.s[blockIdx.y];
+    const uint32_t P = d.passes;
+    const uint32_t n = b.n;
+    // clear this sort's tickets and look-back words (used by the passes)
+    {
+        uint64_t t = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+        uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+        if (t < kMaxPasses) d.ctl->ticket[t] = 0;
+        if (t == kMaxPasses) d.ctl->error = 0;
+        uint64_t words = (uint64_t)P * status_words;
+        for (uint64_t i = t; i < words; i += stride) d.status[i] = 0;
+    }
+    for (uint32_t i = threadIdx.x; i < P * 256; i += blockDim.x) (&h[0][0])[i] = 0;
+    __syncthreads();
+    const uint32_t step = gridDim.x * blockDim.x * kInitPer;
+    for (uint32_t j0 = blockIdx.x * blockDim.x * kInitPer; j0 < n; j0 += step) {
+        uint64_t k[kInitPer];
+        uint32_t v[kInitPer];
+        bool ok[kInitPer];
+#pragma unroll
+        for (int r = 0; r < kInitPer; r++) {
+            uint32_t j = j0 + (uint32_t)r * blockDim.x + threadIdx.x;
+            ok[r] = j < n;
+            k[r] = 0;
+            v[r] = 0;
+            if (ok[r]) produce(b.in, d.kind, d.key_out, n, j, k[r], v[r]);
+        }
+#pragma unroll
+        for (int r = 0; r < kInitPer; r++) {
+            uint32_t j = j0 + (uint32_t)r * blockDim.x + threadIdx.x;
+            if (ok[r]) {
+                d.key[0][j] = k[r];
+                d.val[0][j] = v[r];
+            }
+            const uint64_t act = __ballot(ok[r]);
+            for (uint32_t p = 0; p < P; p++) {
+                uint32_t dg = (uint32_t)(k[r] >> (8 * p)) & 255u;
+                // a digit shared by the whole wave (the common case for high
+                // digits) is counted with one atomic
+                uint32_t d0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)dg);
+                if (__ballot(ok[r] && dg != d0) == 0) {
+                    if (lane_id() == 0 && act) atomicAdd(&h[p][d0], (uint32_t)__popcll(act));
+                } else if (ok[r]) {
+                    atomicAdd(&h[p][dg], 1u);
+                }
+            }
+        }
     }
     __syncthreads();
-    if (d == 0) {
-        uint32_t cur = 0;
-        int32_t last = -1;
-        for (uint32_t p = 0; p < sb.passes; p++) {
-            sb.ctl->active[p] = act[p];
-            sb.ctl->src[p] = cur;
-            if (act[p]) { cur ^= 1u; last = (int32_t)p; }
-        }
-        sb.ctl->last = last;
+    uint32_t *bh = d.bhist + (uint64_t)blockIdx.x * P * 256u;
+    for (uint32_t i = threadIdx.x; i < P * 256; i += blockDim.x) bh[i] = (&h[0][0])[i];
+}
+
+// One block per (pass, sort): digit totals from the block histograms,
+// exclusive offsets, and whether the pass does anything.
+__global__ __launch_bounds__(256) void k_sort_plan(SortBatch b)
+{
+    __shared__ uint32_t tmp4[4];
+    const SortDesc &d = b.s[blockIdx.y];
+    const uint32_t p = blockIdx.x;
+    if (p >= d.passes) return;
+    const uint32_t t = threadIdx.x;
+    const uint32_t stride = d.passes * 256u;
+    // 16 independent loads in flight per step
+    uint32_t c = 0;
+    for (uint32_t blk0 = 0; blk0 < b.init_blocks; blk0 += 16) {
+        uint32_t x[16];
+#pragma unroll
+        for (uint32_t k = 0; k < 16; k++)
+            x[k] = blk0 + k < b.init_blocks ? d.bhist[(uint64_t)(blk0 + k) * stride + p * 256u + t] : 0u;
+#pragma unroll
+        for (uint32_t k = 0; k < 16; k++) c += x[k];
     }
+    int full = __syncthreads_or(c == b.n ? 1 : 0);
+    d.ctl->excl[p][t] = block_excl_scan256(c, tmp4);
+    if (t == 0) d.ctl->active[p] = full ? 0u : 1u;
 }
 
 // Weighted round robin position of the k-th (FIFO) request of tier q:
 // rounds before r = floor(k / w_q) dispatch sum_q' min(n_q', r w_q'); in
 // round r the tiers before q dispatch min(w_q', max(0, n_q' - r w_q')).
-__device__ __forceinline__ uint64_t wrr_pos(const SortInput &in, const uint32_t *cnt, uint32_t q,
-                                            uint64_t k, uint64_t &round)
+__device__ __forceinline__ uint64_t wrr_pos(const SortInput &in, const uint32_t *tstart, uint32_t n,
+                                            uint32_t q, uint64_t k, uint64_t &round)
 {
     uint64_t wq = in.weight[q] ? in.weight[q] : 1;
     uint64_t r = k / wq;
     uint64_t pos = k - r * wq;
     for (uint32_t t = 0; t < in.n_tiers; t++) {
-        uint64_t nt = cnt[t], wt = in.weight[t];
+        // requests of tier t: start of the next tier's range minus its own
+        uint64_t nt = (uint64_t)tstart[t + 1] - tstart[t], wt = in.weight[t];
         uint64_t full = r * wt;
         pos += nt < full ? nt : full;
         if (t < q) {
@@ -206,9 +255,49 @@ __device__ __forceinline__ uint64_t wrr_pos(const SortInput &in, const uint32_t 
     return pos;
 }
 
-__global__ __launch_bounds__(kThreads) void k_sort_pass(SortInput in, SortBufs sb, uint32_t p,
-                                                        uint32_t *__restrict__ out)
+// Sum of digit t's counts over the tiles before `tile` (decoupled look-back,
+// 16 predecessors loaded per window; the wait for an unpublished tile is
+// bounded and reported through err).
+__device__ uint32_t look_back(const uint32_t *st, uint32_t tile, uint32_t t, uint32_t *err)
 {
+    uint32_t prefix = 0;
+    int64_t j = (int64_t)tile - 1;
+    uint32_t spins = 0;
+    while (j >= 0) {
+        constexpr int kWin = 16;
+        uint32_t x[kWin];
+#pragma unroll
+        for (int k = 0; k < kWin; k++)
+            x[k] = (j - k >= 0) ? ld_relaxed(&st[(uint64_t)(j - k) * 256u + t]) : kPre;
+        bool done = false;
+        bool stop = false;
+        int used = 0;
+#pragma unroll
+        for (int k = 0; k < kWin; k++) {
+            if (done || stop || j - k < 0) continue;
+            if ((x[k] & ~kValMask) == 0) { stop = true; continue; }   // not published yet
+            prefix += x[k] & kValMask;
+            used = k + 1;
+            if ((x[k] & ~kValMask) == kPre) done = true;
+        }
+        if (done) break;
+        j -= used;
+        if (used == 0) {
+            __builtin_amdgcn_s_sleep(1);
+            if (++spins > kSpinLimit) {
+                atomicOr(err, 1u);
+                break;
+            }
+        }
+    }
+    return prefix;
+}
+
+template <int R>
+__global__ __launch_bounds__(kThreads) void k_sort_pass(SortBatch b, uint32_t p)
+{
+    constexpr uint32_t kTile = kThreads * R;
+    constexpr uint32_t kWaveKeys = kTile / 4;
     __shared__ uint32_t s_ticket;
     __shared__ uint32_t wcnt[4][256];
     __shared__ uint32_t texcl[256];
@@ -217,67 +306,83 @@ __global__ __launch_bounds__(kThreads) void k_sort_pass(SortInput in, SortBufs s
     __shared__ uint64_t lkey[kTile];
     __shared__ uint32_t lval[kTile];
 
-    const SortCtl *ctl = sb.ctl;
-    const uint32_t n = in.n;
-    if (!ctl->active[p]) {
+    const SortDesc &d = b.s[blockIdx.y];
+    if (p >= d.passes) return;
+    SortCtl *ctl = d.ctl;
+    const uint32_t n = b.n;
+    const uint32_t t = threadIdx.x;
+    // plan words first (independent loads, overlapping the ticket below):
+    // the pass reads the buffer written by the last active pass before it,
+    // and writes the output if no later pass is active
+    uint32_t act[kMaxPasses];
+#pragma unroll
+    for (uint32_t q = 0; q < kMaxPasses; q++) act[q] = q < d.passes ? ctl->active[q] : 0u;
+    const uint32_t dexcl = ctl->excl[p][t];
+    const uint32_t active = act[p];
+    uint32_t before = 0, after = 0;
+#pragma unroll
+    for (uint32_t q = 0; q < kMaxPasses; q++) {
+        if (q < p) before += act[q];
+        if (q > p) after += act[q];
+    }
+    const uint32_t srcb = before & 1u;
+    if (!active) {
         // a pass whose digit is constant is skipped; if no pass is active
         // the input order is the result (the last pass copies it out)
-        if (p + 1 == sb.passes && ctl->last < 0) {
+        if (p + 1 == d.passes && before == 0) {
             for (uint32_t j = blockIdx.x * blockDim.x + threadIdx.x; j < n; j += gridDim.x * blockDim.x) {
-                uint32_t val = sb.val[0][j];
-                out[j] = val;
-                if (in.kind == SortKind::Tier && in.key_out) {
+                uint32_t val = d.val[0][j];
+                d.out[j] = val;
+                if (d.kind == SortKind::Tier && d.key_out && val < n) {
                     // one non-empty tier: the k-th request is served in round k / w
-                    uint32_t q = (uint32_t)sb.key[0][j] & 15u;
-                    uint32_t wq = in.weight[q] ? in.weight[q] : 1u;
-                    if (val < n) in.key_out[val] = (double)(j / wq);
+                    uint32_t q = (uint32_t)d.key[0][j] & 15u;
+                    uint32_t wq = b.in.weight[q] ? b.in.weight[q] : 1u;
+                    d.key_out[val] = (double)(j / wq);
                 }
             }
         }
         return;
     }
-    const uint32_t t = threadIdx.x;
     const int w = (int)(t >> 6);
     const int lane = lane_id();
-    if (t == 0) s_ticket = atomicAdd(&sb.ctl->ticket[p], 1u);
+    if (t == 0) s_ticket = atomicAdd(&ctl->ticket[p], 1u);
     for (uint32_t i = t; i < 4 * 256; i += kThreads) (&wcnt[0][0])[i] = 0;
     __syncthreads();
     const uint32_t tile = s_ticket;
     const uint32_t base = tile * kTile;
     const uint32_t cnt = n - base < kTile ? n - base : kTile;
     const uint32_t shift = 8 * p;
-    const uint32_t srcb = ctl->src[p];
-    const uint64_t *ik = sb.key[srcb];
-    const uint32_t *iv = sb.val[srcb];
-    const bool last = (int32_t)p == ctl->last;
+    const uint64_t *ik = d.key[srcb];
+    const uint32_t *iv = d.val[srcb];
+    const bool last = after == 0;
 
-    uint64_t k[kPer];
-    uint32_t v[kPer];
-    uint32_t rk[kPer];
+    uint64_t k[R];
+    uint32_t v[R];
+    uint32_t rk[R];
 #pragma unroll
-    for (int r = 0; r < kPer; r++) {
-        uint32_t idx = (uint32_t)w * (kTile / 4) + (uint32_t)r * 64u + (uint32_t)lane;
+    for (int r = 0; r < R; r++) {
+        uint32_t idx = (uint32_t)w * kWaveKeys + (uint32_t)r * 64u + (uint32_t)lane;
         bool ok = idx < cnt;
         k[r] = ok ? ik[base + idx] : 0ull;
         v[r] = ok ? iv[base + idx] : 0u;
     }
     // stable rank within the wave, round by round (rounds are in index order)
 #pragma unroll
-    for (int r = 0; r < kPer; r++) {
-        uint32_t idx = (uint32_t)w * (kTile / 4) + (uint32_t)r * 64u + (uint32_t)lane;
+    for (int r = 0; r < R; r++) {
+        uint32_t idx = (uint32_t)w * kWaveKeys + (uint32_t)r * 64u + (uint32_t)lane;
         bool ok = idx < cnt;
-        uint32_t d = (uint32_t)(k[r] >> shift) & 255u;
+        uint32_t dg = (uint32_t)(k[r] >> shift) & 255u;
         uint64_t peers = __ballot(ok);
 #pragma unroll
-        for (int b = 0; b < 8; b++) {
-            bool bit = (d >> b) & 1u;
-            uint64_t bb = __ballot(bit);
-            peers &= bit ? bb : ~bb;
+        for (int bb = 0; bb < 8; bb++) {
+            bool bit = (dg >> bb) & 1u;
+            uint64_t m = __ballot(bit);
+            peers &= bit ? m : ~m;
         }
         uint32_t below = (uint32_t)__popcll(peers & lanemask_lt());
-        uint32_t old = ok ? wcnt[w][d] : 0u;
+        uint32_t old = ok ? wcnt[w][dg] : 0u;
         rk[r] = old + below;
-        if (ok && below == 0) wcnt[w][d] = old + (uint32_t)__popcll(peers);
+        if (ok && below == 0) wcnt[w][dg] = old + (uint32_t)__popcll(peers);
         __builtin_amdgcn_wave_barrier();
     }
     __syncthreads();
@@ -288,104 +393,123 @@ __global__ __launch_bounds__(kThreads) void k_sort_pass(SortInput in, SortBufs s
     wcnt[1][t] = c0;
     wcnt[2][t] = c0 + c1;
     wcnt[3][t] = c0 + c1 + c2;
+    // publish this tile's count first, then scan and look back
+    uint32_t *st = d.status + (uint64_t)p * b.tiles * 256u;
+    st_relaxed(&st[(uint64_t)tile * 256u + t], (tile == 0 ? kPre : kAgg) | tc);
     texcl[t] = block_excl_scan256(tc, tmp4);
-    // decoupled look-back over earlier tiles for digit t
-    uint32_t *st = sb.status + (uint64_t)p * sb.tiles * 256u;
     uint32_t prefix = 0;
-    if (tile == 0) {
-        st_relaxed(&st[t], kPre | tc);
-    } else {
-        st_relaxed(&st[(uint64_t)tile * 256u + t], kAgg | tc);
-        int64_t j = (int64_t)tile - 1;
-        while (true) {
-            uint32_t x = ld_relaxed(&st[(uint64_t)j * 256u + t]);
-            if ((x & ~kValMask) == 0) { __builtin_amdgcn_s_sleep(1); continue; }
-            prefix += x & kValMask;
-            if ((x & ~kValMask) == kPre) break;
-            j--;
-        }
+    if (tile > 0) {
+        prefix = look_back(st, tile, t, &ctl->error);
         st_relaxed(&st[(uint64_t)tile * 256u + t], kPre | (prefix + tc));
     }
-    gbase[t] = ctl->excl[p][t] + prefix;
+    gbase[t] = dexcl + prefix;
     __syncthreads();
     // reorder the tile through LDS by digit
 #pragma unroll
-    for (int r = 0; r < kPer; r++) {
-        uint32_t idx = (uint32_t)w * (kTile / 4) + (uint32_t)r * 64u + (uint32_t)lane;
+    for (int r = 0; r < R; r++) {
+        uint32_t idx = (uint32_t)w * kWaveKeys + (uint32_t)r * 64u + (uint32_t)lane;
         if (idx < cnt) {
-            uint32_t d = (uint32_t)(k[r] >> shift) & 255u;
-            uint32_t lp = texcl[d] + wcnt[w][d] + rk[r];
+            uint32_t dg = (uint32_t)(k[r] >> shift) & 255u;
+            uint32_t lp = texcl[dg] + wcnt[w][dg] + rk[r];
             lkey[lp] = k[r];
             lval[lp] = v[r];
         }
     }
     __syncthreads();
-    if (in.kind == SortKind::Tier) {
+    if (d.kind == SortKind::Tier) {
         // single pass: digit = tier; scatter to the weighted position
-        const uint32_t *tcount = ctl->hist[0];
+        const uint32_t *tstart = ctl->excl[0];
         for (uint32_t s = t; s < cnt; s += kThreads) {
             uint32_t q = (uint32_t)lkey[s] & 255u;
             uint32_t g = gbase[q] + s - texcl[q];
             uint64_t kq = g - ctl->excl[0][q];
             uint64_t rnd;
-            uint64_t pos = wrr_pos(in, tcount, q, kq, rnd);
+            uint64_t pos = wrr_pos(b.in, tstart, n, q, kq, rnd);
             uint32_t val = lval[s];
-            if (pos < n) out[pos] = val;   // always true when tiers are < n_tiers
-            if (in.key_out && val < n) in.key_out[val] = (double)rnd;
+            if (pos < n) d.out[pos] = val;   // always true when tiers are < n_tiers
+            if (d.key_out && val < n) d.key_out[val] = (double)rnd;
         }
         return;
     }
-    uint64_t *ok_ = sb.key[srcb ^ 1u];
-    uint32_t *ov = last ? out : sb.val[srcb ^ 1u];
+    uint64_t *okey = d.key[srcb ^ 1u];
+    uint32_t *ov = last ? d.out : d.val[srcb ^ 1u];
     for (uint32_t s = t; s < cnt; s += kThreads) {
         uint64_t kk = lkey[s];
-        uint32_t d = (uint32_t)(kk >> shift) & 255u;
-        uint32_t g = gbase[d] + s - texcl[d];
+        uint32_t dg = (uint32_t)(kk >> shift) & 255u;
+        uint32_t g = gbase[dg] + s - texcl[dg];
         ov[g] = lval[s];
-        if (!last) ok_[g] = kk;
+        if (!last) okey[g] = kk;
     }
 }
 
-void carve(void *ws, uint64_t n, uint32_t key_bits, SortBufs &b)
+uint32_t tile_keys(uint64_t n) { return n <= kSmallN ? kThreads * 4 : kThreads * 16; }
+
+uint64_t region_bytes(uint64_t n)
 {
-    uint8_t *p = static_cast<uint8_t *>(ws);
-    b.ctl = reinterpret_cast<SortCtl *>(p);
+    uint64_t tiles = cdiv(n, tile_keys(n));
+    return align_up(sizeof(SortCtl), 256) + align_up((uint64_t)kInitBlocks * kMaxPasses * 256 * 4, 256) +
+           2 * align_up(n * 8, 256) + 2 * align_up(n * 4, 256) +
+           align_up((uint64_t)kMaxPasses * tiles * 256 * 4, 256);
+}
+
+void carve(uint8_t *p, uint64_t n, SortDesc &d)
+{
+    d.ctl = reinterpret_cast<SortCtl *>(p);
     p += align_up(sizeof(SortCtl), 256);
+    d.bhist = reinterpret_cast<uint32_t *>(p);
+    p += align_up((uint64_t)kInitBlocks * kMaxPasses * 256 * 4, 256);
     for (int i = 0; i < 2; i++) {
-        b.key[i] = reinterpret_cast<uint64_t *>(p);
+        d.key[i] = reinterpret_cast<uint64_t *>(p);
         p += align_up(n * 8, 256);
     }
     for (int i = 0; i < 2; i++) {
-        b.val[i] = reinterpret_cast<uint32_t *>(p);
+        d.val[i] = reinterpret_cast<uint32_t *>(p);
         p += align_up(n * 4, 256);
     }
-    b.passes = n_passes(key_bits);
-    b.tiles = (uint32_t)cdiv(n, kTile);
-    b.status = reinterpret_cast<uint32_t *>(p);
+    d.status = reinterpret_cast<uint32_t *>(p);
 }
 
 }  // namespace
 
-size_t sort_ws_bytes(uint64_t n, uint32_t key_bits)
+size_t sort_ws_bytes(uint64_t n, uint32_t nsorts)
 {
-    uint64_t tiles = cdiv(n, kTile);
-    return align_up(sizeof(SortCtl), 256) + 2 * align_up(n * 8, 256) + 2 * align_up(n * 4, 256) +
-           align_up((uint64_t)n_passes(key_bits) * tiles * 256 * 4, 256);
+    return (size_t)nsorts * region_bytes(n);
 }
 
-hipError_t sort_launch(const SortInput &in, uint32_t *out, void *ws, hipStream_t s)
+hipError_t sort_launch(const SortInput &in, const SortJob *jobs, uint32_t nsorts, void *ws,
+                       hipStream_t s)
 {
-    if (in.n == 0) return hipSuccess;
-    SortBufs b;
-    carve(ws, in.n, in.key_bits, b);
-    uint64_t words = (uint64_t)b.passes * b.tiles * 256u;
-    uint32_t zb = (uint32_t)(cdiv(words, 256) < 1024 ? cdiv(words, 256) : 1024);
-    hipLaunchKernelGGL(k_sort_zero, dim3(zb ? zb : 1), dim3(256), 0, s, b.ctl, b.status, words);
-    uint32_t ib = (uint32_t)(cdiv(in.n, 256 * 8) < 1024 ? cdiv(in.n, 256 * 8) : 1024);
-    hipLaunchKernelGGL(k_sort_init, dim3(ib ? ib : 1), dim3(256), 0, s, in, b);
-    hipLaunchKernelGGL(k_sort_plan, dim3(1), dim3(256), 0, s, b, in.n);
-    for (uint32_t p = 0; p < b.passes; p++)
-        hipLaunchKernelGGL(k_sort_pass, dim3(b.tiles), dim3(kThreads), 0, s, in, b, p, out);
+    if (in.n == 0 || nsorts == 0) return hipSuccess;
+    if (nsorts > kMaxSorts) return hipErrorInvalidValue;
+    SortBatch b;
+    b.in = in;
+    b.n = in.n;
+    const uint32_t tk = tile_keys(in.n);
+    b.tiles = (uint32_t)cdiv(in.n, tk);
+    b.nsorts = nsorts;
+    uint32_t maxp = 0;
+    uint8_t *p = static_cast<uint8_t *>(ws);
+    for (uint32_t i = 0; i < nsorts; i++) {
+        SortDesc &d = b.s[i];
+        d.kind = jobs[i].kind;
+        d.passes = n_passes(jobs[i].key_bits);
+        d.key_out = jobs[i].key_out;
+        d.out = jobs[i].out;
+        carve(p, in.n, d);
+        p += region_bytes(in.n);
+        maxp = d.passes > maxp ? d.passes : maxp;
+    }
+    const uint64_t status_words = (uint64_t)b.tiles * 256u;
+    uint64_t ibw = cdiv(in.n, 256 * kInitPer);
+    b.init_blocks = (uint32_t)(ibw < kInitBlocks ? (ibw ? ibw : 1) : kInitBlocks);
+    hipLaunchKernelGGL(k_sort_init, dim3(b.init_blocks, nsorts), dim3(256), 0, s, b, status_words);
+    hipLaunchKernelGGL(k_sort_plan, dim3(maxp, nsorts), dim3(256), 0, s, b);
+    for (uint32_t pass = 0; pass < maxp; pass++) {
+        if (tk == kThreads * 4)
+            hipLaunchKernelGGL(k_sort_pass<4>, dim3(b.tiles, nsorts), dim3(kThreads), 0, s, b, pass);
+        else
+            hipLaunchKernelGGL(k_sort_pass<16>, dim3(b.tiles, nsorts), dim3(kThreads), 0, s, b, pass);
+    }
     return hipGetLastError();
 }
 

@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(HERE, "libdriftsched.so")
 
 FIFO, PRIORITY, WEIGHTED, SJF, AGING = 0, 1, 2, 3, 4
 POLICIES = {"fifo": FIFO, "priority": PRIORITY, "weighted": WEIGHTED, "sjf": SJF, "aging": AGING}
-OP_CHARACTERIZE, OP_CALIBRATE, OP_SCORE, OP_ORDER = 0, 1, 2, 3
+OP_CHARACTERIZE, OP_CALIBRATE, OP_SCORE, OP_ORDER, OP_ORDER_MULTI = 0, 1, 2, 3, 4
 DS_VALIDATE = 1
 MAX_TIERS = 16
 
@@ -53,7 +53,9 @@ def _load():
     lib.ds_score.argtypes = [u32, P, P, P, P, P, u32, P, u32, P, u32, ctypes.POINTER(ScoreParams),
                              P, P, P, P, P, sz, u32, P]
     lib.ds_order.argtypes = [i32, u32, P, P, P, P, ctypes.POINTER(OrderParams), P, P, P, sz, u32, P]
-    for f in (lib.ds_characterize, lib.ds_calibrate, lib.ds_score, lib.ds_order):
+    lib.ds_order_multi.argtypes = [u32, u32, P, P, P, P, ctypes.POINTER(OrderParams),
+                                   ctypes.POINTER(P), ctypes.POINTER(P), P, sz, u32, P]
+    for f in (lib.ds_characterize, lib.ds_calibrate, lib.ds_score, lib.ds_order, lib.ds_order_multi):
         f.restype = i32
     lib.ds_workspace_bytes.argtypes = [i32, u64, u32]
     lib.ds_workspace_bytes.restype = sz
@@ -223,3 +225,41 @@ def order(policy, tier, arrival, budget=None, fifo=None, params=None, perm=None,
                         ctypes.byref(params), _ptr(perm), _ptr(k), _ptr(ws), ws.numel(),
                         _flags(validate), _stream()))
     return perm, k
+
+
+def order_multi(policies, tier, arrival, budget=None, fifo=None, params=None, perms=None,
+                keys=False, ws=None, validate=False, **kw):
+    """Dispatch permutations of several policies in one call (FIFO computed
+    once, the policy sorts batched). Returns ({policy: perm}, {policy: key})."""
+    pols = [POLICIES[p] if isinstance(p, str) else int(p) for p in policies]
+    mask = 0
+    for p in pols:
+        mask |= 1 << p
+    _dev(tier, torch.uint8, "tier")
+    _dev(arrival, torch.float64, "arrival")
+    if budget is not None:
+        _dev(budget, torch.float64, "budget")
+    if fifo is not None:
+        _dev(fifo, torch.int32, "fifo")
+    n = tier.numel()
+    dev = tier.device
+    if params is None:
+        params = order_params(**kw)
+    out_p, out_k = {}, {}
+    pp = (ctypes.c_void_p * 5)()
+    kk = (ctypes.c_void_p * 5)()
+    for p in pols:
+        t = perms[p] if perms is not None and p in perms else torch.empty(n, dtype=torch.int32, device=dev)
+        _dev(t, torch.int32, "perm")
+        out_p[p] = t
+        pp[p] = t.data_ptr()
+        if keys:
+            k = torch.empty(n, dtype=torch.float64, device=dev)
+            out_k[p] = k
+            kk[p] = k.data_ptr()
+    if ws is None:
+        ws = workspace(OP_ORDER_MULTI, n, 0, dev)
+    _check(lib.ds_order_multi(mask, n, _ptr(tier), _ptr(arrival), _ptr(budget), _ptr(fifo),
+                              ctypes.byref(params), pp, kk if keys else None, _ptr(ws), ws.numel(),
+                              _flags(validate), _stream()))
+    return out_p, out_k

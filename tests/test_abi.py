@@ -25,7 +25,7 @@ def declared_functions():
 
 def test_exports_every_declared_symbol(ds):
     names = declared_functions()
-    assert names == ["ds_calibrate", "ds_characterize", "ds_order", "ds_score",
+    assert names == ["ds_calibrate", "ds_characterize", "ds_order", "ds_order_multi", "ds_score",
                      "ds_status_string", "ds_version", "ds_workspace_bytes"]
     for name in names:
         assert hasattr(ds.lib, name), name
@@ -40,7 +40,7 @@ def test_status_strings(ds):
 
 
 def test_workspace_sizes(ds):
-    for op in range(4):
+    for op in range(5):
         sizes = [ds.workspace_bytes(op, n, 64) for n in (0, 1, 4096, 65536, 1 << 20)]
         assert all(s >= 256 for s in sizes)
         assert sizes == sorted(sizes)
@@ -106,3 +106,20 @@ def test_order_host_errors(ds):
              NULL) == -3
     assert f(0, 10, FAKE, FAKE, NULL, NULL, ctypes.byref(p), FAKE, NULL, FAKE_WS, 64, 0, NULL) == -4
     assert f(0, 0, NULL, NULL, NULL, NULL, ctypes.byref(p), NULL, NULL, NULL, 0, 0, NULL) == 0
+
+
+def test_order_multi_host_errors(ds):
+    f = ds.lib.ds_order_multi
+    p = ds.order_params()
+    ws = 1 << 40
+    perms = (ctypes.c_void_p * 5)(0x1000, 0x1000, 0x1000, 0x1000, 0x1000)
+    nulls = (ctypes.c_void_p * 5)()
+    assert f(0, 10, FAKE, FAKE, FAKE, NULL, ctypes.byref(p), perms, NULL, FAKE_WS, ws, 0, NULL) == -2
+    assert f(0x20, 10, FAKE, FAKE, FAKE, NULL, ctypes.byref(p), perms, NULL, FAKE_WS, ws, 0, NULL) == -2
+    assert f(0x1F, 10, FAKE, FAKE, FAKE, NULL, ctypes.byref(p), NULL, NULL, FAKE_WS, ws, 0, NULL) == -1
+    assert f(0x03, 10, FAKE, FAKE, FAKE, NULL, ctypes.byref(p), nulls, NULL, FAKE_WS, ws, 0, NULL) == -1
+    assert f(0x08, 10, FAKE, FAKE, NULL, NULL, ctypes.byref(p), perms, NULL, FAKE_WS, ws, 0, NULL) == -1
+    need = ds.workspace_bytes(ds.OP_ORDER_MULTI, 10)
+    assert need > ds.workspace_bytes(ds.OP_ORDER, 10)
+    assert f(0x1F, 10, FAKE, FAKE, FAKE, NULL, ctypes.byref(p), perms, NULL, FAKE_WS, need - 1, 0,
+             NULL) == -4

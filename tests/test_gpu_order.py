@@ -123,6 +123,27 @@ def test_workloads(ds, oracle, name):
         assert np.array_equal(host(p1), host(p2))
 
 
+@pytest.mark.parametrize("name", ["batch4k", "batch64k", "chat1m"])
+def test_multi_equals_single(ds, oracle, name):
+    b = synth.generate(name, with_text=False)
+    rng = np.random.default_rng(1)
+    budget = np.round(rng.uniform(1, 3000, b.n), 2)
+    kw = dict(weights=tuple(int(x) for x in b.weights), tier_priority=tuple(b.tier_priority),
+              aging_rate=b.aging_rate, t_now=b.t_now, aging_floor=b.aging_floor)
+    tier, arr, bud = dev(b.tier), dev(b.arrival), dev(budget)
+    for pols in ([0, 1, 2, 3, 4], [1, 2, 3, 4], [3], [0, 4], [2, 1]):
+        perms, keys = ds.order_multi(pols, tier, arr, bud, keys=True, **kw)
+        for p in pols:
+            w_perm, w_key = oracle.order(p, b.tier, b.arrival, budget, **kw)
+            assert np.array_equal(host(perms[p], np.uint32), w_perm), (pols, p)
+            assert np.array_equal(host(keys[p]), w_key), (pols, p)
+    fifo, _ = ds.order(0, tier, arr, **kw)
+    perms, _ = ds.order_multi([0, 1, 2, 3, 4], tier, arr, bud, fifo=fifo, **kw)
+    assert np.array_equal(host(perms[0]), host(fifo))
+    w_perm, _ = oracle.order(4, b.tier, b.arrival, budget, **kw)
+    assert np.array_equal(host(perms[4], np.uint32), w_perm)
+
+
 @pytest.mark.parametrize("k", [1, 17, 40, 64])
 def test_drift_aging_ticks(ds, oracle, k):
     b = synth.generate("drift4m")
