@@ -321,15 +321,101 @@ __device__ __forceinline__ void process_round(WaveState &st, const RangeCtx &rc,
     st.running += tot;
 }
 
-__global__ __launch_bounds__(kBlock) void k_char_main(const uint8_t *__restrict__ text, uint64_t B,
+// Per-wave LDS of the super-round path: the super-round's bytes (plus the
+// next 16), the list of lead-byte offsets, and separator coverage per
+// (lane, round).
+constexpr uint32_t kSR = kRound * kLoadRounds;   // 4 KiB
+constexpr uint32_t kMaxLeads = 256;              // more leads: per-round path
+struct WaveLds {
+    uint32_t data[(kSR + 16) / 4];
+    uint16_t slot[kMaxLeads];
+    uint32_t cov[64 * kLoadRounds];              // [lane][round]
+};
+
+// Interleaved lead bits of one chunk: bit 8i + k <=> byte 4k + i.
+__device__ __forceinline__ uint32_t lead_bits(const uint4 &d)
+{
+    return (lead_hb(d.x) >> 7) | (lead_hb(d.y) >> 6) | (lead_hb(d.z) >> 5) | (lead_hb(d.w) >> 4);
+}
+
+__device__ __forceinline__ void wave_lds_fence()
+{
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+}
+
+// Multi-byte separators of one whole, boundary-free 4 KiB super-round, all
+// lanes cooperating: each lead byte is checked by one lane. Returns 0 (and
+// changes nothing) if the super-round holds more than kMaxLeads leads;
+// otherwise 1 if no separator was found, 2 if cov[u] (per lane: covered bytes
+// of its chunk in round u) or spill_next (bytes past the super-round's end)
+// were set. M: the lane's interleaved lead bits, two rounds per 32 bits.
+__device__ int superround_separators(WaveLds &L, const uint4 (&d)[kLoadRounds], uint32_t tail,
+                                     uint64_t M, uint32_t excl, uint32_t total, int lane,
+                                     uint32_t (&cov)[kLoadRounds], uint32_t &spill_next)
+{
+    if (total > kMaxLeads) return 0;
+    // stage the bytes and clear the coverage words
+#pragma unroll
+    for (uint32_t u = 0; u < kLoadRounds; u++)
+        *reinterpret_cast<uint4 *>(&L.data[(u * kRound + 16u * (uint32_t)lane) / 4]) = d[u];
+    if (lane == 0) *reinterpret_cast<uint4 *>(&L.data[kSR / 4]) = make_uint4(tail, 0u, 0u, 0u);
+    *reinterpret_cast<uint4 *>(&L.cov[4 * lane]) = make_uint4(0u, 0u, 0u, 0u);
+    // list the leads: byte offsets within the super-round
+    uint32_t r = excl;
+    while (__ballot(M != 0)) {
+        if (M) {
+            uint32_t lo = (uint32_t)M, hi = (uint32_t)(M >> 32);
+            uint32_t p = lo ? (uint32_t)__ffs(lo) - 1 : 32u + (uint32_t)__ffs(hi) - 1;
+            M &= M - 1;
+            uint32_t q = p & 31u;
+            uint32_t u = ((p >> 5) << 1) | ((q >> 2) & 1u);
+            uint32_t off = ((q & 3u) << 2) | (q >> 3);
+            L.slot[r++] = (uint16_t)(u * kRound + 16u * (uint32_t)lane + off);
+        }
+    }
+    wave_lds_fence();
+    // check them, one per lane per pass
+    bool any = false;
+    uint32_t sp = 0;
+    for (uint32_t base = 0; base < total; base += 64) {
+        uint32_t t = base + (uint32_t)lane;
+        uint32_t len = 0, pos = 0;
+        if (t < total) {
+            pos = L.slot[t];
+            uint32_t w0 = L.data[pos >> 2], w1 = L.data[(pos >> 2) + 1];
+            len = mb_space_len_nb(__builtin_amdgcn_alignbyte(w1, w0, pos & 3u));
+        }
+        if (__ballot(len != 0)) {
+            any = true;
+            for (uint32_t i = 0; i < len; i++) {
+                uint32_t b = pos + i;
+                if (b < kSR) atomicOr(&L.cov[4u * ((b >> 4) & 63u) + (b >> 10)], 1u << (b & 15u));
+                else sp |= 1u << (b - kSR);
+            }
+        }
+    }
+    if (!any) return 1;
+    spill_next = (__ballot(sp & 1u) ? 1u : 0u) | (__ballot(sp & 2u) ? 2u : 0u);
+    wave_lds_fence();
+    uint4 c4 = *reinterpret_cast<const uint4 *>(&L.cov[4 * lane]);
+    cov[0] = c4.x;
+    cov[1] = c4.y;
+    cov[2] = c4.z;
+    cov[3] = c4.w;
+    return 2;
+}
+
+__global__ __launch_bounds__(kBlock, 6) void k_char_main(const uint8_t *__restrict__ text, uint64_t B,
                                                       const uint64_t *__restrict__ off, uint32_t N,
                                                       uint64_t Rw, uint32_t nwaves,
                                                       uint32_t *__restrict__ ploc,
                                                       uint64_t *__restrict__ wavetot)
 {
+    __shared__ WaveLds lds_all[kBlock / 64];
     const int lane = lane_id();
     const uint32_t w = blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
     if (w >= nwaves) return;
+    WaveLds &lds = lds_all[threadIdx.x >> 6];
     RangeCtx rc;
     rc.off = off;
     rc.N = N;
@@ -382,37 +468,52 @@ __global__ __launch_bounds__(kBlock) void k_char_main(const uint8_t *__restrict_
             }
             if (sb + sr_bytes < load_end) tail = load4(text, B, sb + sr_bytes);
         }
-        // fast super-round: all bytes counted, ASCII only, no prompt boundary
+        // super-round path: all bytes counted, no prompt boundary, no
+        // separator carried in; multi-byte separators checked cooperatively
         bool fast = whole && sb + sr_bytes <= rc.ws_end && st.spill == 0;
         if (fast) {
             ensure_window(st, rc, st.s_ptr, lane);
             fast = readlane64(st.win, (int)(st.s_ptr - st.wb)) >= sb + sr_bytes + 2;
         }
         if (fast) {
-            uint32_t hi = 0;
-#pragma unroll
-            for (uint32_t u = 0; u < kLoadRounds; u++) hi |= d[u].x | d[u].y | d[u].z | d[u].w;
-            fast = __ballot((hi & 0x80808080u) != 0) == 0;
-        }
-        if (fast) {
-            uint32_t carry = st.ws_prev;
-            uint32_t acc = 0;
-#pragma unroll
-            for (uint32_t u = 0; u < kLoadRounds; u++) {
-                const uint32_t h0 = ascii_space_hb(d[u].x), h1 = ascii_space_hb(d[u].y);
-                const uint32_t h2 = ascii_space_hb(d[u].z), h3 = ascii_space_hb(d[u].w);
-                // lane i receives lane i-1's last dword; lane 0 the carried bit
-                uint32_t p0 = wave_shr1(h3, carry << 31);
-                uint32_t s0 = ~h0 & __builtin_amdgcn_alignbyte(h0, p0, 3);
-                uint32_t s1 = ~h1 & __builtin_amdgcn_alignbyte(h1, h0, 3);
-                uint32_t s2 = ~h2 & __builtin_amdgcn_alignbyte(h2, h1, 3);
-                uint32_t s3 = ~h3 & __builtin_amdgcn_alignbyte(h3, h2, 3);
-                acc += __popc(s0) + __popc(s1) + __popc(s2) + __popc(s3);
-                carry = readlane32(h3, 63) >> 31;
+            const uint64_t M = (uint64_t)(lead_bits(d[0]) | (lead_bits(d[1]) << 4)) |
+                               ((uint64_t)(lead_bits(d[2]) | (lead_bits(d[3]) << 4)) << 32);
+            const uint32_t nl = (uint32_t)__popcll(M);
+            uint32_t cov[kLoadRounds] = {0u, 0u, 0u, 0u};
+            uint32_t spill_next = 0;
+            int res = 1;
+            if (__ballot(nl != 0)) {
+                const uint32_t incl = wave_incl_scan_dpp(nl);
+                res = superround_separators(lds, d, tail, M, incl - nl, readlane32(incl, 63), lane,
+                                            cov, spill_next);
             }
-            st.acc += acc;
-            st.ws_prev = carry;
-            continue;
+            if (res != 0) {
+                uint32_t carry = st.ws_prev;
+                uint32_t acc = 0;
+#pragma unroll
+                for (uint32_t u = 0; u < kLoadRounds; u++) {
+                    uint32_t h0 = ascii_space_hb(d[u].x), h1 = ascii_space_hb(d[u].y);
+                    uint32_t h2 = ascii_space_hb(d[u].z), h3 = ascii_space_hb(d[u].w);
+                    if (res == 2) {
+                        h0 |= expand4(cov[u] & 0xFu);
+                        h1 |= expand4((cov[u] >> 4) & 0xFu);
+                        h2 |= expand4((cov[u] >> 8) & 0xFu);
+                        h3 |= expand4((cov[u] >> 12) & 0xFu);
+                    }
+                    // lane i receives lane i-1's last dword; lane 0 the carried bit
+                    uint32_t p0 = wave_shr1(h3, carry << 31);
+                    uint32_t s0 = ~h0 & __builtin_amdgcn_alignbyte(h0, p0, 3);
+                    uint32_t s1 = ~h1 & __builtin_amdgcn_alignbyte(h1, h0, 3);
+                    uint32_t s2 = ~h2 & __builtin_amdgcn_alignbyte(h2, h1, 3);
+                    uint32_t s3 = ~h3 & __builtin_amdgcn_alignbyte(h3, h2, 3);
+                    acc += __popc(s0) + __popc(s1) + __popc(s2) + __popc(s3);
+                    carry = readlane32(h3, 63) >> 31;
+                }
+                st.acc += acc;
+                st.ws_prev = carry;
+                st.spill = spill_next;
+                continue;
+            }
         }
 #pragma unroll
         for (uint32_t u = 0; u < kLoadRounds; u++) {

@@ -160,3 +160,33 @@ def test_validate_flag(ds):
         with pytest.raises(ds.DriftSchedError) as e:
             ds.characterize(text, dev(np.array(bad, np.uint64)), validate=True)
         assert e.value.status == -5
+
+
+@pytest.mark.parametrize("density", [0.002, 0.01, 0.05])
+def test_long_prompts_sparse_multibyte(ds, oracle, density):
+    # long prompts (no prompt boundary for many KiB) of ASCII words with
+    # multi-byte separators and look-alikes sprinkled at every byte offset,
+    # including across 1 KiB rounds and 4 KiB super-rounds
+    rng = random.Random(int(density * 1000))
+    seps = [c for c in SPACES if len(c.encode()) > 1]
+    prompts = []
+    for _ in range(12):
+        parts = []
+        size = 0
+        while size < 300_000:
+            x = rng.random()
+            if x < density:
+                t = rng.choice(seps)
+            elif x < 2 * density:
+                t = rng.choice(LOOKALIKES)
+            elif x < 0.15:
+                t = " "
+            else:
+                t = rng.choice("abcdefghij")
+            parts.append(t)
+            size += len(t.encode())
+        prompts.append("".join(parts).encode())
+    text, offsets = pack(prompts)
+    got = check(ds, oracle, text, offsets)
+    want = np.array([len(p.decode().split()) for p in prompts], dtype=np.uint32)
+    assert np.array_equal(got, want)
