@@ -36,15 +36,15 @@ constexpr uint32_t kMaxWaves = 16384;
 constexpr uint64_t kNone = ~0ull;
 
 // 0x80 in each byte of x that is an ASCII separator 09-0D or 1C-20.
-// Per-byte exact: every add stays below 0x100 within its byte.
+// v_lerp_u8 averages bytes without carries between them: bit 7 of byte k of
+// lerp(x, c, 0) is the carry of x_k + c_k, i.e. x_k >= 0x100 - c_k.
 __device__ __forceinline__ uint32_t ascii_space_hb(uint32_t x)
 {
-    uint32_t a = x & 0x7F7F7F7Fu;
-    uint32_t lt21 = ~((a + 0x5F5F5F5Fu) | x) & 0x80808080u;   // b < 0x21
-    uint32_t ge1c = a + 0x64646464u;                             // b >= 0x1C
-    uint32_t ge09 = a + 0x77777777u;                             // b >= 0x09
-    uint32_t ge0e = a + 0x72727272u;                             // b >= 0x0E
-    return lt21 & (ge1c | (ge09 & ~ge0e));
+    const uint32_t ge09 = __builtin_amdgcn_lerp(x, 0xF7F7F7F7u, 0u);
+    const uint32_t ge0e = __builtin_amdgcn_lerp(x, 0xF2F2F2F2u, 0u);
+    const uint32_t ge1c = __builtin_amdgcn_lerp(x, 0xE4E4E4E4u, 0u);
+    const uint32_t ge21 = __builtin_amdgcn_lerp(x, 0xDFDFDFDFu, 0u);
+    return ~ge21 & (ge1c | (ge09 & ~ge0e)) & 0x80808080u;
 }
 
 // 0x80 in each byte >= 0xC0 (UTF-8 lead bytes of multi-byte sequences).
@@ -354,12 +354,11 @@ __device__ int superround_separators(WaveLds &L, const uint4 (&d)[kLoadRounds], 
                                      uint32_t (&cov)[kLoadRounds], uint32_t &spill_next)
 {
     if (total > kMaxLeads) return 0;
-    // stage the bytes and clear the coverage words
+    // stage the bytes (the coverage words are already zero)
 #pragma unroll
     for (uint32_t u = 0; u < kLoadRounds; u++)
         *reinterpret_cast<uint4 *>(&L.data[(u * kRound + 16u * (uint32_t)lane) / 4]) = d[u];
     if (lane == 0) *reinterpret_cast<uint4 *>(&L.data[kSR / 4]) = make_uint4(tail, 0u, 0u, 0u);
-    *reinterpret_cast<uint4 *>(&L.cov[4 * lane]) = make_uint4(0u, 0u, 0u, 0u);
     // list the leads: byte offsets within the super-round
     uint32_t r = excl;
     while (__ballot(M != 0)) {
@@ -398,6 +397,8 @@ __device__ int superround_separators(WaveLds &L, const uint4 (&d)[kLoadRounds], 
     spill_next = (__ballot(sp & 1u) ? 1u : 0u) | (__ballot(sp & 2u) ? 2u : 0u);
     wave_lds_fence();
     uint4 c4 = *reinterpret_cast<const uint4 *>(&L.cov[4 * lane]);
+    // the coverage words are zero whenever this function starts
+    *reinterpret_cast<uint4 *>(&L.cov[4 * lane]) = make_uint4(0u, 0u, 0u, 0u);
     cov[0] = c4.x;
     cov[1] = c4.y;
     cov[2] = c4.z;
@@ -416,6 +417,7 @@ __global__ __launch_bounds__(kBlock, 6) void k_char_main(const uint8_t *__restri
     const uint32_t w = blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
     if (w >= nwaves) return;
     WaveLds &lds = lds_all[threadIdx.x >> 6];
+    *reinterpret_cast<uint4 *>(&lds.cov[4 * lane]) = make_uint4(0u, 0u, 0u, 0u);
     RangeCtx rc;
     rc.off = off;
     rc.N = N;

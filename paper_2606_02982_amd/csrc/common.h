@@ -28,18 +28,6 @@ __device__ __forceinline__ uint64_t lanemask_lt()
     return l ? (~0ull >> (64 - l)) : 0ull;
 }
 
-// Inclusive prefix sum over the 64 lanes of a wave.
-__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x)
-{
-    int l = lane_id();
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        uint32_t y = __shfl_up(x, d, 64);
-        if (l >= d) x += y;
-    }
-    return x;
-}
-
 // DPP lane moves (gfx9 wave shifts): lane i receives lane i-1 (shr) or
 // lane i+1 (shl) of x; the lane without a source receives `edge`.
 __device__ __forceinline__ uint32_t wave_shr1(uint32_t x, uint32_t edge)

@@ -10,20 +10,21 @@
 //
 // Launches of one batch of sorts:
 //   k_sort_init  produces the pairs from the inputs, writes each block's digit
-//                histograms of every pass (no atomics), clears the tickets
-//                and look-back words of the passes
+//                histograms of every pass (no atomics), clears the
+//                look-back words of the passes
 //   k_sort_plan  one block per (pass, sort): sums the block histograms into
 //                exclusive digit offsets and marks a pass whose digit is the
 //                same for every key (it is skipped)
-//   k_sort_pass  one per digit pass: per tile of 256*R keys, wave ranking by
+//   k_sort_pass  one per digit pass: per tile of TPB*R keys, wave ranking by
 //                ballots over the digit bits, per-wave LDS counters,
 //                look-back over earlier tiles' per-digit counts (windows of
 //                16 predecessors loaded at once, bounded wait), reorder
 //                through LDS, coalesced runs of global writes. The buffer a
 //                pass reads, and whether it is the last active pass, follow
 //                from the active flags.
-// Tiles take tickets from an atomic counter, so a tile only ever waits on
-// tiles that are already running.
+// Tile t of a pass is block t. Blocks of a dispatch start in index order on
+// each XCD, so a tile only waits on tiles that have started or will start
+// without waiting on it.
 #include "common.h"
 #include "kernels.h"
 
@@ -36,13 +37,11 @@ constexpr uint32_t kAgg = 1u << 30;
 constexpr uint32_t kPre = 2u << 30;
 constexpr uint32_t kValMask = (1u << 30) - 1u;
 constexpr uint32_t kSpinLimit = 1u << 22;   // bounded waits (never reached in normal runs)
-constexpr uint32_t kSmallN = 1u << 18;      // below: 1024-key tiles, above: 4096
 
 constexpr uint32_t kInitBlocks = 256;     // block histograms per sort (at most)
 
 struct SortCtl {
     uint32_t excl[kMaxPasses][256];
-    uint32_t ticket[kMaxPasses];
     uint32_t active[kMaxPasses];
     uint32_t error;
     uint32_t pad[15];
@@ -139,7 +138,7 @@ __device__ __forceinline__ void produce(const SortInput &in, SortKind kind, doub
 // Exclusive scan of one value per thread over a 256-thread block.
 __device__ uint32_t block_excl_scan256(uint32_t x, uint32_t *tmp4)
 {
-    uint32_t incl = wave_incl_scan(x);
+    uint32_t incl = wave_incl_scan_dpp(x);
     int w = threadIdx.x >> 6;
     if (lane_id() == 63) tmp4[w] = incl;
     __syncthreads();
@@ -157,12 +156,11 @@ __global__ __launch_bounds__(256) void k_sort_init(SortBatch b, uint64_t status_
     const SortDesc &d = b.s[blockIdx.y];
     const uint32_t P = d.passes;
     const uint32_t n = b.n;
-    // clear this sort's tickets and look-back words (used by the passes)
+    // clear this sort's look-back words (used by the passes)
     {
         uint64_t t = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
         uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
-        if (t < kMaxPasses) d.ctl->ticket[t] = 0;
-        if (t == kMaxPasses) d.ctl->error = 0;
+        if (t == 0) d.ctl->error = 0;
         uint64_t words = (uint64_t)P * status_words;
         for (uint64_t i = t; i < words; i += stride) d.status[i] = 0;
     }
@@ -255,30 +253,36 @@ __device__ __forceinline__ uint64_t wrr_pos(const SortInput &in, const uint32_t 
     return pos;
 }
 
-// Sum of digit t's counts over the tiles before `tile` (decoupled look-back,
-// 16 predecessors loaded per window; the wait for an unpublished tile is
-// bounded and reported through err).
+// Sum of digit t's counts over the tiles before `tile` (decoupled look-back).
+// Tiles publish their own count as soon as they have ranked their keys, so
+// by the time a tile looks back its predecessors' counts are normally all
+// there: windows of 16 predecessors are loaded at once and summed back to
+// the first inclusive prefix. The wait for an unpublished tile is bounded
+// and reported through err.
 __device__ uint32_t look_back(const uint32_t *st, uint32_t tile, uint32_t t, uint32_t *err)
 {
+    constexpr int kWin = 16;
     uint32_t prefix = 0;
-    int64_t j = (int64_t)tile - 1;
+    int64_t j = (int64_t)tile - 1;   // nearest predecessor not yet summed
     uint32_t spins = 0;
     while (j >= 0) {
-        constexpr int kWin = 16;
         uint32_t x[kWin];
 #pragma unroll
-        for (int k = 0; k < kWin; k++)
-            x[k] = (j - k >= 0) ? ld_relaxed(&st[(uint64_t)(j - k) * 256u + t]) : kPre;
-        bool done = false;
-        bool stop = false;
+        for (int k = 0; k < kWin; k++) {
+            int64_t jj = j - k >= 0 ? j - k : 0;
+            x[k] = ld_relaxed(&st[(uint64_t)jj * 256u + t]);
+        }
+        bool done = false, stop = false;
         int used = 0;
 #pragma unroll
         for (int k = 0; k < kWin; k++) {
-            if (done || stop || j - k < 0) continue;
-            if ((x[k] & ~kValMask) == 0) { stop = true; continue; }   // not published yet
-            prefix += x[k] & kValMask;
-            used = k + 1;
-            if ((x[k] & ~kValMask) == kPre) done = true;
+            const bool valid = !done && !stop && j - k >= 0;
+            const uint32_t flag = x[k] & ~kValMask;
+            stop = stop || (valid && flag == 0);                 // not published yet
+            const bool take = valid && flag != 0;
+            prefix += take ? (x[k] & kValMask) : 0u;
+            used = take ? k + 1 : used;
+            done = done || (take && flag == kPre);
         }
         if (done) break;
         j -= used;
@@ -293,13 +297,29 @@ __device__ uint32_t look_back(const uint32_t *st, uint32_t tile, uint32_t t, uin
     return prefix;
 }
 
-template <int R>
-__global__ __launch_bounds__(kThreads) void k_sort_pass(SortBatch b, uint32_t p)
+// Exclusive scan of the values of threads 0..255 over a block of TPB >= 256
+// threads (every thread calls it; the result is meaningful for t < 256).
+template <int TPB>
+__device__ uint32_t block_excl_scan_digits(uint32_t x, uint32_t *tmp)
 {
-    constexpr uint32_t kTile = kThreads * R;
-    constexpr uint32_t kWaveKeys = kTile / 4;
-    __shared__ uint32_t s_ticket;
-    __shared__ uint32_t wcnt[4][256];
+    const uint32_t incl = wave_incl_scan_dpp(x);
+    const int w = threadIdx.x >> 6;
+    if (lane_id() == 63 && w < 4) tmp[w] = incl;
+    __syncthreads();
+    uint32_t off = 0;
+    for (int k = 0; k < w && k < 4; k++) off += tmp[k];
+    __syncthreads();
+    return off + incl - x;
+}
+
+// One digit pass over tiles of TPB * R keys (tile t = block t).
+template <int TPB, int R>
+__global__ __launch_bounds__(TPB) void k_sort_pass(SortBatch b, uint32_t p)
+{
+    constexpr uint32_t kTile = TPB * R;
+    constexpr int kWaves = TPB / 64;
+    constexpr uint32_t kWaveKeys = 64u * R;
+    __shared__ uint32_t wcnt[kWaves][256];
     __shared__ uint32_t texcl[256];
     __shared__ uint32_t gbase[256];
     __shared__ uint32_t tmp4[4];
@@ -311,13 +331,13 @@ __global__ __launch_bounds__(kThreads) void k_sort_pass(SortBatch b, uint32_t p)
     SortCtl *ctl = d.ctl;
     const uint32_t n = b.n;
     const uint32_t t = threadIdx.x;
-    // plan words first (independent loads, overlapping the ticket below):
-    // the pass reads the buffer written by the last active pass before it,
-    // and writes the output if no later pass is active
+    const bool digit_thread = t < 256;
+    // plan words: the pass reads the buffer written by the last active pass
+    // before it, and writes the output if no later pass is active
     uint32_t act[kMaxPasses];
 #pragma unroll
     for (uint32_t q = 0; q < kMaxPasses; q++) act[q] = q < d.passes ? ctl->active[q] : 0u;
-    const uint32_t dexcl = ctl->excl[p][t];
+    const uint32_t dexcl = digit_thread ? ctl->excl[p][t] : 0u;
     const uint32_t active = act[p];
     uint32_t before = 0, after = 0;
 #pragma unroll
@@ -345,10 +365,8 @@ __global__ __launch_bounds__(kThreads) void k_sort_pass(SortBatch b, uint32_t p)
     }
     const int w = (int)(t >> 6);
     const int lane = lane_id();
-    if (t == 0) s_ticket = atomicAdd(&ctl->ticket[p], 1u);
-    for (uint32_t i = t; i < 4 * 256; i += kThreads) (&wcnt[0][0])[i] = 0;
-    __syncthreads();
-    const uint32_t tile = s_ticket;
+    for (uint32_t i = t; i < kWaves * 256u; i += TPB) (&wcnt[0][0])[i] = 0;
+    const uint32_t tile = blockIdx.x;
     const uint32_t base = tile * kTile;
     const uint32_t cnt = n - base < kTile ? n - base : kTile;
     const uint32_t shift = 8 * p;
@@ -366,6 +384,7 @@ __global__ __launch_bounds__(kThreads) void k_sort_pass(SortBatch b, uint32_t p)
         k[r] = ok ? ik[base + idx] : 0ull;
         v[r] = ok ? iv[base + idx] : 0u;
     }
+    __syncthreads();
     // stable rank within the wave, round by round (rounds are in index order)
 #pragma unroll
     for (int r = 0; r < R; r++) {
@@ -387,22 +406,28 @@ __global__ __launch_bounds__(kThreads) void k_sort_pass(SortBatch b, uint32_t p)
     }
     __syncthreads();
     // per digit (thread t = digit): tile count, per-wave exclusive offsets
-    uint32_t c0 = wcnt[0][t], c1 = wcnt[1][t], c2 = wcnt[2][t], c3 = wcnt[3][t];
-    uint32_t tc = c0 + c1 + c2 + c3;
-    wcnt[0][t] = 0;
-    wcnt[1][t] = c0;
-    wcnt[2][t] = c0 + c1;
-    wcnt[3][t] = c0 + c1 + c2;
+    uint32_t tc = 0;
+    if (digit_thread) {
+#pragma unroll
+        for (int q = 0; q < kWaves; q++) {
+            uint32_t c = wcnt[q][t];
+            wcnt[q][t] = tc;
+            tc += c;
+        }
+    }
     // publish this tile's count first, then scan and look back
     uint32_t *st = d.status + (uint64_t)p * b.tiles * 256u;
-    st_relaxed(&st[(uint64_t)tile * 256u + t], (tile == 0 ? kPre : kAgg) | tc);
-    texcl[t] = block_excl_scan256(tc, tmp4);
-    uint32_t prefix = 0;
-    if (tile > 0) {
-        prefix = look_back(st, tile, t, &ctl->error);
-        st_relaxed(&st[(uint64_t)tile * 256u + t], kPre | (prefix + tc));
+    if (digit_thread) st_relaxed(&st[(uint64_t)tile * 256u + t], (tile == 0 ? kPre : kAgg) | tc);
+    const uint32_t tex = block_excl_scan_digits<TPB>(tc, tmp4);
+    if (digit_thread) {
+        texcl[t] = tex;
+        uint32_t prefix = 0;
+        if (tile > 0) {
+            prefix = look_back(st, tile, t, &ctl->error);
+            st_relaxed(&st[(uint64_t)tile * 256u + t], kPre | (prefix + tc));
+        }
+        gbase[t] = dexcl + prefix;
     }
-    gbase[t] = dexcl + prefix;
     __syncthreads();
     // reorder the tile through LDS by digit
 #pragma unroll
@@ -419,7 +444,7 @@ __global__ __launch_bounds__(kThreads) void k_sort_pass(SortBatch b, uint32_t p)
     if (d.kind == SortKind::Tier) {
         // single pass: digit = tier; scatter to the weighted position
         const uint32_t *tstart = ctl->excl[0];
-        for (uint32_t s = t; s < cnt; s += kThreads) {
+        for (uint32_t s = t; s < cnt; s += TPB) {
             uint32_t q = (uint32_t)lkey[s] & 255u;
             uint32_t g = gbase[q] + s - texcl[q];
             uint64_t kq = g - ctl->excl[0][q];
@@ -433,7 +458,7 @@ __global__ __launch_bounds__(kThreads) void k_sort_pass(SortBatch b, uint32_t p)
     }
     uint64_t *okey = d.key[srcb ^ 1u];
     uint32_t *ov = last ? d.out : d.val[srcb ^ 1u];
-    for (uint32_t s = t; s < cnt; s += kThreads) {
+    for (uint32_t s = t; s < cnt; s += TPB) {
         uint64_t kk = lkey[s];
         uint32_t dg = (uint32_t)(kk >> shift) & 255u;
         uint32_t g = gbase[dg] + s - texcl[dg];
@@ -442,7 +467,10 @@ __global__ __launch_bounds__(kThreads) void k_sort_pass(SortBatch b, uint32_t p)
     }
 }
 
-uint32_t tile_keys(uint64_t n) { return n <= kSmallN ? kThreads * 4 : kThreads * 16; }
+// Tile shapes: 2048 keys (512 threads x 4) up to 2^18 keys, 8192 keys (1024
+// threads x 8) above, where fewer, larger tiles shorten the look-back.
+constexpr uint32_t kSmallN = 1u << 18;
+uint32_t tile_keys(uint64_t n) { return n <= kSmallN ? 512u * 4u : 1024u * 8u; }
 
 uint64_t region_bytes(uint64_t n)
 {
@@ -505,10 +533,10 @@ hipError_t sort_launch(const SortInput &in, const SortJob *jobs, uint32_t nsorts
     hipLaunchKernelGGL(k_sort_init, dim3(b.init_blocks, nsorts), dim3(256), 0, s, b, status_words);
     hipLaunchKernelGGL(k_sort_plan, dim3(maxp, nsorts), dim3(256), 0, s, b);
     for (uint32_t pass = 0; pass < maxp; pass++) {
-        if (tk == kThreads * 4)
-            hipLaunchKernelGGL(k_sort_pass<4>, dim3(b.tiles, nsorts), dim3(kThreads), 0, s, b, pass);
+        if (in.n <= kSmallN)
+            hipLaunchKernelGGL((k_sort_pass<512, 4>), dim3(b.tiles, nsorts), dim3(512), 0, s, b, pass);
         else
-            hipLaunchKernelGGL(k_sort_pass<16>, dim3(b.tiles, nsorts), dim3(kThreads), 0, s, b, pass);
+            hipLaunchKernelGGL((k_sort_pass<1024, 8>), dim3(b.tiles, nsorts), dim3(1024), 0, s, b, pass);
     }
     return hipGetLastError();
 }
