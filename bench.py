@@ -24,7 +24,9 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
-PROFILE = os.path.join(ROOT, "profiles", "pipeline_batch64k.md")
+# rocprofv3 summaries holding the measured HBM bytes of one characterize call
+PROFILES = {"batch64k": os.path.join(ROOT, "profiles", "pipeline_batch64k.md"),
+            "long16k": os.path.join(ROOT, "profiles", "characterize_long16k.md")}
 CHAR_SRC = os.path.join(ROOT, "paper_2606_02982_amd", "csrc", "characterize.hip")
 METRIC = "requests characterized+ordered/sec and achieved HBM GB/s (fraction of peak)"
 
@@ -83,12 +85,7 @@ def main():
         wl.name, N, B, gen_s), file=sys.stderr, flush=True)
 
     if args.copy_probe:
-        x = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
-        y = torch.empty_like(x)
-        for _ in range(3):
-            y.copy_(x)
-        torch.cuda.synchronize()
-        del x, y
+        copy_probe()
 
     # device-resident inputs
     text, offsets = to_dev(b.text), to_dev(b.offsets)
@@ -181,7 +178,7 @@ def main():
         "hbm_frac_step": round(total_gbs / HBM_PEAK_GBS, 4),
         "stages_ms": {"characterize": round(stage_ms[0], 4), "calibrate": round(stage_ms[1], 4),
                       "score": round(stage_ms[2], 4), "order_x5": round(stage_ms[3], 4)},
-        "roofline": {"kernel": "characterize (k_char_main + k_char_scan + k_char_fin)",
+        "roofline": {"kernel": "characterize (k_char_main + k_char_fin)",
                      "bound": "hbm", "achieved": round(char_gbs, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(char_gbs / HBM_PEAK_GBS, 4),
                      "algorithmic_bytes": int(char_bytes),
@@ -191,6 +188,17 @@ def main():
     print(json.dumps(out), flush=True)
 
 
+def copy_probe():
+    """A plain 1 GiB device copy: the reference reading of the memory counters."""
+    import torch
+    x = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    y = torch.empty_like(x)
+    for _ in range(3):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    del x, y
+
+
 def bench_characterize(args, wl):
     """Stage 1 alone on one workload: HBM roofline of the word counter."""
     import torch
@@ -198,6 +206,8 @@ def bench_characterize(args, wl):
     from paper_2606_02982_amd import synth
     b = synth.generate(wl)
     N, B = b.n, len(b.text)
+    if args.copy_probe:
+        copy_probe()
     text, offsets = to_dev(b.text), to_dev(b.offsets)
     counts = torch.empty(N, dtype=torch.int32, device="cuda")
     ws = ds.workspace(ds.OP_CHARACTERIZE, N)
@@ -216,6 +226,7 @@ def bench_characterize(args, wl):
     gbs = nbytes / (ms * 1e-3) / 1e9
     print(json.dumps({"metric": "characterize HBM GB/s", "value": round(gbs, 1), "unit": "GB/s",
                       "frac": round(gbs / HBM_PEAK_GBS, 4), "ms_per_call": round(ms, 4),
+                      "algorithmic_bytes": int(nbytes), "traffic": measured_traffic(wl.name),
                       "requests_per_s": round(N / (ms * 1e-3), 1), "steps": args.steps,
                       "config": {"workload": wl.name, "requests": N, "text_bytes": B,
                                  "nonascii_byte_frac": round(float((b.text >= 0x80).mean()), 4)}}),
@@ -224,18 +235,19 @@ def bench_characterize(args, wl):
 
 def measured_traffic(workload):
     """HBM bytes per characterize call from the committed rocprofv3 counter
-    summary, if it was taken on this workload with the current kernel source."""
+    summary of this workload, if it was taken with the current kernel source."""
     import hashlib
-    if workload != "batch64k" or not os.path.exists(PROFILE):
+    path = PROFILES.get(workload)
+    if path is None or not os.path.exists(path):
         return None
     vals = {}
-    for line in open(PROFILE):
+    for line in open(path):
         if ":" in line and line.split(":")[0].strip() in ("traffic_bytes_per_call",
                                                           "characterize_source_sha256_16"):
             k, v = line.split(":", 1)
             vals[k.strip()] = v.strip()
     sha = hashlib.sha256(open(CHAR_SRC, "rb").read()).hexdigest()[:16]
-    if vals.get("characterize_source_sha256_16") != sha:
+    if vals.get("characterize_source_sha256_16") != sha or "traffic_bytes_per_call" not in vals:
         return None
     return int(vals["traffic_bytes_per_call"])
 

@@ -13,14 +13,21 @@
 // sequences starts with a continuation byte, this equals decoding each prompt
 // on its own (undecodable bytes as ordinary characters) and splitting.
 //
-// Layout of the work: the text is cut into equal byte ranges, one per wave;
-// each wave streams its range in rounds of 1 KiB (64 lanes x 16 bytes, 16-byte
-// loads, four rounds in flight) and classifies 4 bytes per 32-bit operation.
-// A round with no prompt boundary and no UTF-8 lead byte takes a SWAR fast
-// path; other rounds check multi-byte separators at lead bytes and fold in
-// prompt starts. Carries between lanes move with DPP wave shifts. Word starts are attributed to prompts through prefix sums:
-// each prompt boundary receives the number of word starts in its wave's range
-// before it, each wave its total; a second kernel forms counts[i] from the two
+// Layout of the work: the text is cut into equal byte ranges, one per
+// resident wave; each wave streams its range in super-rounds of 4 KiB (four
+// 1 KiB rounds of 64 lanes x 16 bytes, all loads issued together) and
+// classifies 4 bytes per 32-bit operation (v_lerp_u8 thresholds). Carries
+// between lanes move with DPP wave shifts. A super-round takes one of three
+// paths:
+//   - no prompt boundary: ASCII classification, with the UTF-8 lead bytes
+//     listed in LDS and each checked for a multi-byte separator by one lane;
+//   - boundaries but no lead byte: ASCII classification, and per boundary a
+//     few lane reads and scalar operations give its exact prefix;
+//   - otherwise (and at the ends of a wave's range): round by round, with
+//     boundary bits per lane and separators checked at each lead byte.
+// Word starts are attributed to prompts through prefix sums: each prompt
+// boundary receives the number of word starts in its wave's range before it,
+// each wave its total; a second kernel forms counts[i] from the two
 // boundaries' local prefixes and the totals of the waves between them. No
 // atomics; results are exact integers independent of scheduling.
 #include "common.h"
@@ -406,7 +413,85 @@ __device__ int superround_separators(WaveLds &L, const uint4 (&d)[kLoadRounds], 
     return 2;
 }
 
-__global__ __launch_bounds__(kBlock, 6) void k_char_main(const uint8_t *__restrict__ text, uint64_t B,
+// Non-zero if any byte of the super-round is >= 0xC0 (a UTF-8 lead byte).
+__device__ __forceinline__ uint32_t lead_any(const uint4 (&d)[kLoadRounds])
+{
+    uint32_t a = 0;
+#pragma unroll
+    for (uint32_t u = 0; u < kLoadRounds; u++)
+        a |= __builtin_amdgcn_lerp(d[u].x, 0x40404040u, 0u) | __builtin_amdgcn_lerp(d[u].y, 0x40404040u, 0u) |
+             __builtin_amdgcn_lerp(d[u].z, 0x40404040u, 0u) | __builtin_amdgcn_lerp(d[u].w, 0x40404040u, 0u);
+    return a & 0x80808080u;
+}
+
+// A whole super-round with no UTF-8 lead byte that holds prompt boundaries
+// (the window lanes in bm, in position order). Word starts are those of the
+// plain path plus, at a boundary P whose bytes P and P-1 are both
+// non-whitespace, the start that the first character of a prompt always is.
+// Each boundary receives the exact number of starts in the wave's range
+// before it; per boundary only scalar work and lane reads.
+__device__ void boundary_superround(WaveState &st, const RangeCtx &rc, const uint4 (&d)[kLoadRounds],
+                                    uint64_t sb, uint64_t bm, int lane)
+{
+    uint64_t base = st.running + readlane32(wave_incl_scan_dpp(st.acc), 63);
+    st.acc = 0;
+    uint32_t carry = st.ws_prev;
+    uint64_t rem = bm;
+    uint32_t plv = 0;
+#pragma unroll
+    for (uint32_t u = 0; u < kLoadRounds; u++) {
+        const uint32_t h0 = ascii_space_hb(d[u].x), h1 = ascii_space_hb(d[u].y);
+        const uint32_t h2 = ascii_space_hb(d[u].z), h3 = ascii_space_hb(d[u].w);
+        // whitespace bits of each byte's predecessor
+        const uint32_t v0 = __builtin_amdgcn_alignbyte(h0, wave_shr1(h3, carry << 31), 3);
+        const uint32_t v1 = __builtin_amdgcn_alignbyte(h1, h0, 3);
+        const uint32_t v2 = __builtin_amdgcn_alignbyte(h2, h1, 3);
+        const uint32_t v3 = __builtin_amdgcn_alignbyte(h3, h2, 3);
+        const uint32_t s0 = ~h0 & v0, s1 = ~h1 & v1, s2 = ~h2 & v2, s3 = ~h3 & v3;
+        const uint32_t c = (uint32_t)(__popc(s0) + __popc(s1) + __popc(s2) + __popc(s3));
+        const uint32_t incl = wave_incl_scan_dpp(c);
+        carry = readlane32(h3, 63) >> 31;
+        const uint64_t rend = sb + (uint64_t)(u + 1) * kRound;
+        uint32_t fbr = 0, pend = 0;   // forced starts before P / at the last P
+        uint64_t lastP = kNone;
+        while (rem) {
+            const int j = __ffsll((unsigned long long)rem) - 1;
+            const uint64_t P = readlane64(st.win, j);
+            if (P >= rend) break;
+            rem &= rem - 1;
+            const uint32_t rel = (uint32_t)(P - (rend - kRound));
+            const int L = (int)(rel >> 4);
+            const uint32_t r = rel & 15u, k = r >> 2, sh = 8u * (r & 3u);
+            if (P != lastP) {
+                fbr += pend;
+                lastP = P;
+                uint32_t hk, vk;
+                if (k == 0) { hk = readlane32(h0, L); vk = readlane32(v0, L); }
+                else if (k == 1) { hk = readlane32(h1, L); vk = readlane32(v1, L); }
+                else if (k == 2) { hk = readlane32(h2, L); vk = readlane32(v2, L); }
+                else { hk = readlane32(h3, L); vk = readlane32(v3, L); }
+                pend = ((hk | vk) >> (sh + 7)) & 1u ? 0u : 1u;
+            }
+            const uint32_t e = L ? readlane32(incl, L - 1) : 0u;
+            const uint32_t low = (1u << sh) - 1u;
+            const uint32_t w0 = readlane32(s0, L), w1 = readlane32(s1, L);
+            const uint32_t w2 = readlane32(s2, L), w3 = readlane32(s3, L);
+            uint32_t part = (uint32_t)__popc(k == 0 ? (w0 & low) : w0);
+            part += k >= 1 ? (uint32_t)__popc(k == 1 ? (w1 & low) : w1) : 0u;
+            part += k >= 2 ? (uint32_t)__popc(k == 2 ? (w2 & low) : w2) : 0u;
+            part += k == 3 ? (uint32_t)__popc(w3 & low) : 0u;
+            const uint32_t val = (uint32_t)(base + fbr + e + part);
+            plv = lane == j ? val : plv;
+        }
+        base += readlane32(incl, 63) + fbr + pend;
+    }
+    if ((bm >> lane) & 1ull) rc.ploc[st.wb + (uint32_t)lane] = plv;
+    st.running = base;
+    st.ws_prev = carry;
+    st.s_ptr += (uint32_t)__popcll(bm);
+}
+
+__global__ __launch_bounds__(kBlock, 7) void k_char_main(const uint8_t *__restrict__ text, uint64_t B,
                                                       const uint64_t *__restrict__ off, uint32_t N,
                                                       uint64_t Rw, uint32_t nwaves,
                                                       uint32_t *__restrict__ ploc,
@@ -414,7 +499,8 @@ __global__ __launch_bounds__(kBlock, 6) void k_char_main(const uint8_t *__restri
 {
     __shared__ WaveLds lds_all[kBlock / 64];
     const int lane = lane_id();
-    const uint32_t w = blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
+    // the wave index, known to the compiler to be uniform across the wave
+    const uint32_t w = (uint32_t)__builtin_amdgcn_readfirstlane((int)(blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6)));
     if (w >= nwaves) return;
     WaveLds &lds = lds_all[threadIdx.x >> 6];
     *reinterpret_cast<uint4 *>(&lds.cov[4 * lane]) = make_uint4(0u, 0u, 0u, 0u);
@@ -470,12 +556,34 @@ __global__ __launch_bounds__(kBlock, 6) void k_char_main(const uint8_t *__restri
             }
             if (sb + sr_bytes < load_end) tail = load4(text, B, sb + sr_bytes);
         }
-        // super-round path: all bytes counted, no prompt boundary, no
-        // separator carried in; multi-byte separators checked cooperatively
-        bool fast = whole && sb + sr_bytes <= rc.ws_end && st.spill == 0;
-        if (fast) {
+        // Super-round paths (all bytes counted, no separator carried in):
+        // with no prompt boundary before sb + 4098, multi-byte separators
+        // are checked cooperatively; with boundaries but no UTF-8 lead
+        // byte, they are attributed per boundary. Otherwise: per round.
+        bool fast = false;
+        uint64_t bm = 0;   // window lanes holding this super-round's boundaries
+        if (whole && sb + sr_bytes <= rc.ws_end && st.spill == 0) {
             ensure_window(st, rc, st.s_ptr, lane);
-            fast = readlane64(st.win, (int)(st.s_ptr - st.wb)) >= sb + sr_bytes + 2;
+            uint32_t kk = st.s_ptr - st.wb;
+            uint64_t near = __ballot((uint32_t)lane >= kk && st.win < sb + sr_bytes + 2);
+            if ((near >> 63) & 1ull) {
+                // the window may end inside the super-round: restart it here
+                st.wb = st.s_ptr;
+                st.win = win_load(rc.off, rc.N, st.wb, lane);
+                kk = 0;
+                near = __ballot(st.win < sb + sr_bytes + 2);
+            }
+            if (!((near >> 63) & 1ull)) {
+                fast = near == 0;
+                bm = __ballot((uint32_t)lane >= kk && st.win < sb + sr_bytes);
+            }
+        }
+        if (bm) {
+            const uint32_t any = lead_any(d);
+            if (__ballot(any != 0) == 0) {
+                boundary_superround(st, rc, d, sb, bm, lane);
+                continue;
+            }
         }
         if (fast) {
             const uint64_t M = (uint64_t)(lead_bits(d[0]) | (lead_bits(d[1]) << 4)) |
@@ -595,8 +703,8 @@ hipError_t char_launch(const uint8_t *text, uint64_t B, const uint64_t *offsets,
         hipLaunchKernelGGL(k_char_validate, dim3(blocks), dim3(256), 0, s, offsets, n, B, flag);
         return hipGetLastError();
     }
-    // waves: ranges of whole KiB, at least 4 KiB each, at most kMaxWaves
-    // one wave range per resident wave: CUs x resident blocks per CU x 4
+    // one wave range per resident wave (CUs x resident waves per CU); ranges
+    // are whole 4 KiB super-rounds
     static int resident_cache[64];
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
