@@ -41,6 +41,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--stage", choices=["pipeline", "characterize"], default="pipeline",
                     help="characterize: time only stage 1 on --workload (any workload with text)")
+    ap.add_argument("--settle", type=float, default=0.5,
+                    help="seconds of untimed steps before the warmup steps (GPU clocks ramp "
+                         "up under sustained load; the timed steps measure the steady state)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="run a plain 1 GiB device copy first (to scale memory counters)")
     return ap.parse_args()
@@ -124,6 +127,7 @@ def main():
                        ws=ws[ds.OP_ORDER_MULTI])
         if ev: ev[4].record()
 
+    settle(step, args.settle)
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -166,6 +170,7 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "settle_s": args.settle,
         "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True,
         "scaling": "weak",
@@ -186,6 +191,16 @@ def main():
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
+
+
+def settle(fn, seconds):
+    """Untimed repetitions of fn for about `seconds` of wall time."""
+    import torch
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(8):
+            fn()
+        torch.cuda.synchronize()
 
 
 def copy_probe():
@@ -211,8 +226,10 @@ def bench_characterize(args, wl):
     text, offsets = to_dev(b.text), to_dev(b.offsets)
     counts = torch.empty(N, dtype=torch.int32, device="cuda")
     ws = ds.workspace(ds.OP_CHARACTERIZE, N)
+    call = lambda: ds.characterize(text, offsets, counts=counts, ws=ws)
+    settle(call, args.settle)
     for _ in range(args.warmup):
-        ds.characterize(text, offsets, counts=counts, ws=ws)
+        call()
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
     torch.cuda.synchronize()
     ev[0].record()
