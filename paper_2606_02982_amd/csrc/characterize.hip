@@ -332,17 +332,23 @@ __device__ __forceinline__ void process_round(WaveState &st, const RangeCtx &rc,
 // next 16), the list of lead-byte offsets, and separator coverage per
 // (lane, round).
 constexpr uint32_t kSR = kRound * kLoadRounds;   // 4 KiB
-constexpr uint32_t kMaxLeads = 256;              // more leads: per-round path
+constexpr uint32_t kMaxLeads = 224;              // more leads: per-round path
 struct WaveLds {
     uint32_t data[(kSR + 16) / 4];
     uint16_t slot[kMaxLeads];
-    uint32_t cov[64 * kLoadRounds];              // [lane][round]
+    uint32_t cov[32 * kLoadRounds];              // [lane pair][round], 16 bits per lane
 };
 
 // Interleaved lead bits of one chunk: bit 8i + k <=> byte 4k + i.
 __device__ __forceinline__ uint32_t lead_bits(const uint4 &d)
 {
-    return (lead_hb(d.x) >> 7) | (lead_hb(d.y) >> 6) | (lead_hb(d.z) >> 5) | (lead_hb(d.w) >> 4);
+    // bit 7 of each byte of lerp(x, 0x40.., 0): byte >= 0xC0
+    const uint32_t gx = __builtin_amdgcn_lerp(d.x, 0x40404040u, 0u);
+    const uint32_t gy = __builtin_amdgcn_lerp(d.y, 0x40404040u, 0u);
+    const uint32_t gz = __builtin_amdgcn_lerp(d.z, 0x40404040u, 0u);
+    const uint32_t gw = __builtin_amdgcn_lerp(d.w, 0x40404040u, 0u);
+    return ((gx >> 7) & 0x01010101u) | ((gy >> 6) & 0x02020202u) | ((gz >> 5) & 0x04040404u) |
+           ((gw >> 4) & 0x08080808u);
 }
 
 __device__ __forceinline__ void wave_lds_fence()
@@ -395,7 +401,8 @@ __device__ int superround_separators(WaveLds &L, const uint4 (&d)[kLoadRounds], 
             any = true;
             for (uint32_t i = 0; i < len; i++) {
                 uint32_t b = pos + i;
-                if (b < kSR) atomicOr(&L.cov[4u * ((b >> 4) & 63u) + (b >> 10)], 1u << (b & 15u));
+                const uint32_t bl = (b >> 4) & 63u;
+                if (b < kSR) atomicOr(&L.cov[4u * (bl >> 1) + (b >> 10)], 1u << ((b & 15u) + 16u * (bl & 1u)));
                 else sp |= 1u << (b - kSR);
             }
         }
@@ -403,24 +410,24 @@ __device__ int superround_separators(WaveLds &L, const uint4 (&d)[kLoadRounds], 
     if (!any) return 1;
     spill_next = (__ballot(sp & 1u) ? 1u : 0u) | (__ballot(sp & 2u) ? 2u : 0u);
     wave_lds_fence();
-    uint4 c4 = *reinterpret_cast<const uint4 *>(&L.cov[4 * lane]);
+    const uint4 c4 = *reinterpret_cast<const uint4 *>(&L.cov[4 * (lane >> 1)]);
+    const uint32_t hs = 16u * ((uint32_t)lane & 1u);
+    wave_lds_fence();
     // the coverage words are zero whenever this function starts
-    *reinterpret_cast<uint4 *>(&L.cov[4 * lane]) = make_uint4(0u, 0u, 0u, 0u);
-    cov[0] = c4.x;
-    cov[1] = c4.y;
-    cov[2] = c4.z;
-    cov[3] = c4.w;
+    *reinterpret_cast<uint4 *>(&L.cov[4 * (lane >> 1)]) = make_uint4(0u, 0u, 0u, 0u);
+    cov[0] = (c4.x >> hs) & 0xFFFFu;
+    cov[1] = (c4.y >> hs) & 0xFFFFu;
+    cov[2] = (c4.z >> hs) & 0xFFFFu;
+    cov[3] = (c4.w >> hs) & 0xFFFFu;
     return 2;
 }
 
-// Non-zero if any byte of the super-round is >= 0xC0 (a UTF-8 lead byte).
-__device__ __forceinline__ uint32_t lead_any(const uint4 (&d)[kLoadRounds])
+// Non-zero if any byte of the lane's 64 bytes has bit 7 set (not ASCII).
+__device__ __forceinline__ uint32_t high_any(const uint4 (&d)[kLoadRounds])
 {
     uint32_t a = 0;
 #pragma unroll
-    for (uint32_t u = 0; u < kLoadRounds; u++)
-        a |= __builtin_amdgcn_lerp(d[u].x, 0x40404040u, 0u) | __builtin_amdgcn_lerp(d[u].y, 0x40404040u, 0u) |
-             __builtin_amdgcn_lerp(d[u].z, 0x40404040u, 0u) | __builtin_amdgcn_lerp(d[u].w, 0x40404040u, 0u);
+    for (uint32_t u = 0; u < kLoadRounds; u++) a |= d[u].x | d[u].y | d[u].z | d[u].w;
     return a & 0x80808080u;
 }
 
@@ -503,7 +510,7 @@ __global__ __launch_bounds__(kBlock, 7) void k_char_main(const uint8_t *__restri
     const uint32_t w = (uint32_t)__builtin_amdgcn_readfirstlane((int)(blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6)));
     if (w >= nwaves) return;
     WaveLds &lds = lds_all[threadIdx.x >> 6];
-    *reinterpret_cast<uint4 *>(&lds.cov[4 * lane]) = make_uint4(0u, 0u, 0u, 0u);
+    if (lane < 32) *reinterpret_cast<uint4 *>(&lds.cov[4 * lane]) = make_uint4(0u, 0u, 0u, 0u);
     RangeCtx rc;
     rc.off = off;
     rc.N = N;
@@ -578,21 +585,25 @@ __global__ __launch_bounds__(kBlock, 7) void k_char_main(const uint8_t *__restri
                 bm = __ballot((uint32_t)lane >= kk && st.win < sb + sr_bytes);
             }
         }
-        if (bm) {
-            const uint32_t any = lead_any(d);
-            if (__ballot(any != 0) == 0) {
-                boundary_superround(st, rc, d, sb, bm, lane);
-                continue;
-            }
+        // lead bytes (>= 0xC0) of the super-round, listed only when some
+        // byte has bit 7 set
+        uint64_t M = 0;
+        bool leads = false;
+        if ((fast || bm) && __ballot(high_any(d) != 0)) {
+            M = (uint64_t)(lead_bits(d[0]) | (lead_bits(d[1]) << 4)) |
+                ((uint64_t)(lead_bits(d[2]) | (lead_bits(d[3]) << 4)) << 32);
+            leads = __ballot(M != 0) != 0;
+        }
+        if (bm && !leads) {
+            boundary_superround(st, rc, d, sb, bm, lane);
+            continue;
         }
         if (fast) {
-            const uint64_t M = (uint64_t)(lead_bits(d[0]) | (lead_bits(d[1]) << 4)) |
-                               ((uint64_t)(lead_bits(d[2]) | (lead_bits(d[3]) << 4)) << 32);
-            const uint32_t nl = (uint32_t)__popcll(M);
             uint32_t cov[kLoadRounds] = {0u, 0u, 0u, 0u};
             uint32_t spill_next = 0;
             int res = 1;
-            if (__ballot(nl != 0)) {
+            if (leads) {
+                const uint32_t nl = (uint32_t)__popcll(M);
                 const uint32_t incl = wave_incl_scan_dpp(nl);
                 res = superround_separators(lds, d, tail, M, incl - nl, readlane32(incl, 63), lane,
                                             cov, spill_next);
