@@ -27,6 +27,7 @@
 // without waiting on it.
 #include "common.h"
 #include "kernels.h"
+#include "keys.h"
 
 namespace ds {
 namespace {
@@ -72,67 +73,6 @@ __host__ __device__ inline uint32_t n_passes(uint32_t key_bits)
 {
     uint32_t p = (key_bits + 7) / 8;
     return p == 0 ? 1 : (p > kMaxPasses ? kMaxPasses : p);
-}
-
-__device__ __forceinline__ void produce(const SortInput &in, SortKind kind, double *key_out,
-                                        uint32_t n, uint32_t j, uint64_t &k, uint32_t &v)
-{
-    switch (kind) {
-    case SortKind::Fifo: {
-        double a = in.arrival[j];
-        k = ordered_bits(a);
-        v = j;
-        if (key_out) key_out[j] = a;
-        break;
-    }
-    case SortKind::Budget: {
-        uint32_t i = in.fifo[j];
-        i = i < n ? i : 0;
-        double b = in.budget[i];
-        k = ordered_bits(b);
-        v = i;
-        if (key_out) key_out[i] = b;
-        break;
-    }
-    case SortKind::Aging: {
-        uint32_t i = in.fifo[j];
-        i = i < n ? i : 0;
-        uint32_t q = in.tier[i];
-        q = q < 16 ? q : 15;
-        double w = in.t_now - in.arrival[i];
-        if (w < 0.0) w = 0.0;
-        double d = in.aging_rate * w;
-        double e = in.prio[q] - d;
-        if (e < in.aging_floor) e = in.aging_floor;
-        k = ordered_bits(e);
-        v = i;
-        if (key_out) key_out[i] = e;
-        break;
-    }
-    case SortKind::Class: {
-        uint32_t i = in.fifo[j];
-        i = i < n ? i : 0;
-        uint32_t q = in.tier[i];
-        q = q < 16 ? q : 15;
-        k = in.cls[q];
-        v = i;
-        if (key_out) key_out[i] = in.prio[q];
-        break;
-    }
-    case SortKind::Tier: {
-        uint32_t i = in.fifo[j];
-        i = i < n ? i : 0;
-        uint32_t q = in.tier[i];
-        k = q < 16 ? q : 15;
-        v = i;
-        break;
-    }
-    default: {   // Group
-        k = in.group[j];
-        v = j;
-        break;
-    }
-    }
 }
 
 // Exclusive scan of one value per thread over a 256-thread block.

@@ -54,7 +54,8 @@ def _batch(seed, n, q=None, tiers=3):
 
 
 @pytest.mark.parametrize("pol", POLICIES)
-@pytest.mark.parametrize("n", [1, 2, 63, 4095, 4096, 4097, 50000])
+@pytest.mark.parametrize("n", [1, 2, 63, 2047, 2048, 2049, 4095, 4096, 4097, 50000, 131071, 131072,
+                               131073])
 def test_sizes(ds, oracle, pol, n):
     tier, arr, bud = _batch(n, n)
     check(ds, oracle, pol, tier, arr, bud, t_now=10.0, aging_rate=0.1)
@@ -67,6 +68,26 @@ def test_many_ties(ds, oracle, pol):
     arr[:50] = 0.0
     arr[50:100] = -0.0
     check(ds, oracle, pol, tier, arr, bud, t_now=10.0, aging_rate=0.3)
+
+
+@pytest.mark.parametrize("pol", POLICIES)
+@pytest.mark.parametrize("pattern", ["sawtooth", "descending", "blocks"])
+def test_run_patterns(ds, oracle, pol, pattern):
+    # key layouts across the 2048-request runs of the run-merge sort: every
+    # run holding the same keys, runs in descending order, and a few long
+    # stretches of equal keys crossing run boundaries
+    n = 3 * 2048 * 5 + 77
+    j = np.arange(n)
+    if pattern == "sawtooth":
+        arr = (j % 2048) * 0.001
+    elif pattern == "descending":
+        arr = (n - j) * 0.001
+    else:
+        arr = np.floor(j / 5000.0) + np.where(j % 7 == 0, 0.5, 0.0)
+    rng = np.random.default_rng(n)
+    tier = rng.integers(0, 3, n).astype(np.uint8)
+    bud = np.where(j % 3 == 0, 100.0, np.round(rng.uniform(1, 3000, n), 1))
+    check(ds, oracle, pol, tier, arr, bud, t_now=float(arr.max()), aging_rate=0.05)
 
 
 @pytest.mark.parametrize("pol", POLICIES)
