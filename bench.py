@@ -39,8 +39,9 @@ def parse():
     ap.add_argument("--workload", default="batch64k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
-    ap.add_argument("--stage", choices=["pipeline", "characterize"], default="pipeline",
-                    help="characterize: time only stage 1 on --workload (any workload with text)")
+    ap.add_argument("--stage", choices=["pipeline", "characterize", "errors"], default="pipeline",
+                    help="characterize: time only stage 1 on --workload (any workload with text); "
+                         "errors: the estimation-error diagnostics on --workload's events")
     ap.add_argument("--settle", type=float, default=0.5,
                     help="seconds of untimed steps before the warmup steps (GPU clocks ramp "
                          "up under sustained load; the timed steps measure the steady state)")
@@ -76,6 +77,8 @@ def main():
     wl = synth.WORKLOADS[args.workload]
     if args.stage == "characterize":
         return bench_characterize(args, wl)
+    if args.stage == "errors":
+        return bench_errors(args, wl)
     if not wl.has_text or len(wl.policies) < 5:
         print("bench.py: the step needs a workload with text and all five policies", file=sys.stderr)
         sys.exit(2)
@@ -248,6 +251,54 @@ def bench_characterize(args, wl):
                       "config": {"workload": wl.name, "requests": N, "text_bytes": B,
                                  "nonascii_byte_frac": round(float((b.text >= 0x80).mean()), 4)}}),
           flush=True)
+
+
+def bench_errors(args, wl):
+    """The evaluation diagnostics on one workload's completion events: error
+    statistics with and without the calibrated factor, and the class histogram
+    of the batch (HBM-bound reductions)."""
+    import torch
+    from paper_2606_02982_amd import driftsched as ds
+    from paper_2606_02982_amd import synth
+    b = synth.generate(wl, with_text=False)
+    E, G = len(b.ev_group), b.n_groups
+    group, est, obs = to_dev(b.ev_group), to_dev(b.ev_est), to_dev(b.ev_obs)
+    state = torch.ones(G, dtype=torch.float64, device="cuda")
+    before = torch.empty(E, dtype=torch.float64, device="cuda")
+    ds.calibrate(group, est, obs, b.alphas[0], state, trace=False, trace_before=before)
+    cat = to_dev(b.category)
+    cls = to_dev(np.minimum(b.words % 3, 2).astype(np.uint8))   # any class values serve
+    out = torch.empty((G + 1, 4), dtype=torch.float64, device="cuda")
+    hist = torch.empty((len(b.t_base), 3), dtype=torch.int32, device="cuda")
+    ws = ds.workspace(ds.OP_ERROR_STATS, E, G)
+
+    def timed(fn):
+        settle(fn, args.settle)
+        for _ in range(args.warmup):
+            fn()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        torch.cuda.synchronize()
+        ev[0].record()
+        for _ in range(args.steps):
+            fn()
+        ev[1].record()
+        torch.cuda.synchronize()
+        return ev[0].elapsed_time(ev[1]) / args.steps
+
+    ms_off = timed(lambda: ds.error_stats(est, obs, group=group, n_groups=G, out=out, ws=ws))
+    ms_on = timed(lambda: ds.error_stats(est, obs, factor=before, group=group, n_groups=G, out=out,
+                                         ws=ws))
+    ms_hist = timed(lambda: ds.class_histogram(cat, cls, len(b.t_base), out=hist))
+    bytes_off = E * (8 + 4 + 4) + (G + 1) * 32
+    bytes_on = bytes_off + E * 8
+    bytes_hist = b.n * 2 + len(b.t_base) * 12
+    res = {"metric": "evaluation diagnostics HBM GB/s", "unit": "GB/s",
+           "config": {"workload": wl.name, "events": E, "groups": G, "requests": b.n},
+           "error_stats_bias_off": {"ms": round(ms_off, 4), "GBs": round(bytes_off / ms_off / 1e6, 1)},
+           "error_stats_bias_on": {"ms": round(ms_on, 4), "GBs": round(bytes_on / ms_on / 1e6, 1)},
+           "class_histogram": {"ms": round(ms_hist, 4), "GBs": round(bytes_hist / ms_hist / 1e6, 1)},
+           "peak": HBM_PEAK_GBS}
+    print(json.dumps(res), flush=True)
 
 
 def measured_traffic(workload):

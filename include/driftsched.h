@@ -14,6 +14,12 @@
  *   ds_score          calibrated output estimate, budget and runtime class
  *   ds_order          dispatch permutation for one policy
  *
+ * and, beside it, the diagnostics of the paper's evaluation:
+ *
+ *   ds_calibrate_ex     calibration with the factor before each event
+ *   ds_error_stats      MAE, RMSE and mean bias of estimates vs observed
+ *   ds_class_histogram  runtime classes per semantic category
+ *
  * Conventions shared by every entry point:
  *  - Array arguments are DEVICE pointers (memory from hipMalloc or any
  *    allocator of the same device, e.g. torch tensors); parameter structs
@@ -68,7 +74,9 @@ typedef enum {
     DS_OP_CALIBRATE = 1,
     DS_OP_SCORE = 2,
     DS_OP_ORDER = 3,
-    DS_OP_ORDER_MULTI = 4
+    DS_OP_ORDER_MULTI = 4,
+    DS_OP_ERROR_STATS = 5,
+    DS_OP_CLASS_HIST = 6
 } ds_op;
 
 /* flags */
@@ -76,6 +84,7 @@ typedef enum {
 
 #define DS_MAX_TIERS 16
 #define DS_MAX_ITEMS (1u << 30)   /* max events for ds_calibrate, requests for ds_order */
+#define DS_MAX_GROUPS (1u << 20)  /* max groups for ds_error_stats */
 
 typedef void *ds_stream;    /* hipStream_t */
 
@@ -233,6 +242,68 @@ ds_status ds_order_multi(uint32_t policy_mask, uint32_t n, const uint8_t *tier,
                          const ds_order_params *params, uint32_t *const *perms,
                          double *const *keys, void *ws, size_t ws_bytes, uint32_t flags,
                          ds_stream stream);
+
+/*
+ * ds_calibrate, and in addition trace_before[e]: the factor of e's group just
+ * before event e, i.e. the factor a request admitted at that point of the
+ * completion stream is scored with (the admission-time factor of Sec.
+ * "Runtime Calibration and Feedback Adaptation"). Either trace may be NULL.
+ * Same workspace (DS_OP_CALIBRATE), arguments and errors as ds_calibrate.
+ */
+ds_status ds_calibrate_ex(const uint32_t *group, const double *est, const uint32_t *observed,
+                          uint64_t n_events, double alpha, uint32_t n_groups,
+                          double *state, double *trace, double *trace_before,
+                          void *ws, size_t ws_bytes, uint32_t flags, ds_stream stream);
+
+/*
+ * Estimation error of token estimates against observed output lengths: the
+ * MAE, RMSE and mean bias of Sec. "Impact of Workload Characterization and
+ * Runtime Calibration" (tab:four_mode_token_error; their BIAS=OFF / BIAS=ON
+ * ratio per policy is tab:error_reduction).
+ *
+ * For every event e whose estimate x = est[e] * factor[e] (factor NULL: 1)
+ * is finite and > 0 (other events are skipped), d = x - observed[e]. For
+ * each group g < n_groups (the events with group[e] == g) and then for all
+ * events together, stats receives four doubles:
+ *     count, MAE = mean |d|, RMSE = sqrt(mean d^2), mean bias = mean(observed / x).
+ * A set without events gives count 0 and NaN for the three means.
+ *
+ *  est        device, n double: e.g. the B-free estimate (BIAS=OFF)
+ *  factor     device, n double, or NULL: multiplies est, e.g. trace_before
+ *             of ds_calibrate_ex for the admission-time calibrated estimate
+ *             (BIAS=ON)
+ *  observed   device, n uint32 (tokens)
+ *  group      device, n uint32, or NULL; contract: < n_groups
+ *  n_groups   number of groups; 0 exactly when group is NULL; <= DS_MAX_GROUPS
+ *  stats      device, 4 * (n_groups + 1) double; written
+ *  n          <= DS_MAX_ITEMS
+ *  ws         workspace of ds_workspace_bytes(DS_OP_ERROR_STATS, n, n_groups)
+ * Sums use floating-point atomic adds, so results vary between runs within
+ * the rounding of an n-term sum (relative error at most about n * 2^-53).
+ * Unlike the stages, n == 0 still writes stats (counts 0).
+ */
+ds_status ds_error_stats(uint64_t n, const double *est, const double *factor,
+                         const uint32_t *observed, const uint32_t *group, uint32_t n_groups,
+                         double *stats, void *ws, size_t ws_bytes, uint32_t flags,
+                         ds_stream stream);
+
+/*
+ * Runtime classes per semantic category (Eq. (4) classes against the
+ * categories of tab:workload_mapping): hist[c * 3 + k] = number of requests
+ * i with category[i] == c and job_class[i] == k.
+ *
+ *  category   device, n uint8; contract: < n_cat
+ *  n_cat      1..256
+ *  job_class  device, n uint8 (0 short, 1 medium, 2 long; e.g. from ds_score)
+ *  hist       device, 3 * n_cat uint32; written
+ *  ws         workspace of ds_workspace_bytes(DS_OP_CLASS_HIST, n, 0) bytes
+ *             (used by DS_VALIDATE only; may be NULL without that flag)
+ * Requests outside the contract are not counted (DS_VALIDATE reports them).
+ * n == 0 writes a zero histogram.
+ */
+ds_status ds_class_histogram(uint32_t n, const uint8_t *category, uint32_t n_cat,
+                             const uint8_t *job_class, uint32_t *hist,
+                             void *ws, size_t ws_bytes, uint32_t flags, ds_stream stream);
 
 /* Workspace size for op at size n (prompts, events or requests); n_groups
  * is used by DS_OP_CALIBRATE only. */

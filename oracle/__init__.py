@@ -53,6 +53,12 @@ def _load():
     lib.dsref_characterize.restype = i32
     lib.dsref_calibrate.argtypes = [P, P, P, u64, f64, u32, P, P]
     lib.dsref_calibrate.restype = i32
+    lib.dsref_calibrate_ex.argtypes = [P, P, P, u64, f64, u32, P, P, P]
+    lib.dsref_calibrate_ex.restype = i32
+    lib.dsref_error_stats.argtypes = [u64, P, P, P, P, u32, P]
+    lib.dsref_error_stats.restype = i32
+    lib.dsref_class_histogram.argtypes = [u64, P, u32, P, P]
+    lib.dsref_class_histogram.restype = i32
     lib.dsref_score.argtypes = [u64, P, P, P, P, P, u32, P, u32, P, u32,
                                 f64, f64, f64, P, P, P, P]
     lib.dsref_score.restype = i32
@@ -93,10 +99,12 @@ def characterize(text, offsets):
     return counts
 
 
-def calibrate(group, est, obs, alpha, state, with_trace=True):
+def calibrate(group, est, obs, alpha, state, with_trace=True, with_before=False):
     """Stage 2: EMA of Eq. (5) over ratios of Eq. (6), events in completion order.
 
-    Returns (state_out, trace or None); ``state`` is not modified.
+    Returns (state_out, trace or None), and trace_before (the factor of each
+    event's group just before it) as a third item when ``with_before``;
+    ``state`` is not modified.
     """
     group = _c(group, np.uint32)
     est = _c(est, np.float64)
@@ -104,11 +112,39 @@ def calibrate(group, est, obs, alpha, state, with_trace=True):
     st = np.array(state, dtype=np.float64, copy=True)
     n = len(group)
     trace = np.zeros(n, dtype=np.float64) if with_trace else None
-    rc = _load().dsref_calibrate(_ptr(group), _ptr(est), _ptr(obs), n, float(alpha),
-                                 len(st), _ptr(st), _ptr(trace))
+    before = np.zeros(n, dtype=np.float64) if with_before else None
+    rc = _load().dsref_calibrate_ex(_ptr(group), _ptr(est), _ptr(obs), n, float(alpha),
+                                    len(st), _ptr(st), _ptr(trace), _ptr(before))
     if rc != 0:
         raise ValueError("oracle calibrate: group index out of range")
-    return st, trace
+    return (st, trace, before) if with_before else (st, trace)
+
+
+def error_stats(est, obs, factor=None, group=None, n_groups=0):
+    """Estimation error per group and overall: array (n_groups + 1, 4) of
+    count, MAE, RMSE, mean bias (tab:four_mode_token_error)."""
+    est = _c(est, np.float64)
+    obs = _c(obs, np.uint32)
+    fac = None if factor is None else _c(factor, np.float64)
+    grp = None if group is None else _c(group, np.uint32)
+    out = np.zeros(4 * (n_groups + 1), dtype=np.float64)
+    rc = _load().dsref_error_stats(len(est), _ptr(est), _ptr(fac), _ptr(obs), _ptr(grp),
+                                   int(n_groups), _ptr(out))
+    if rc != 0:
+        raise ValueError("oracle error_stats: group index out of range")
+    return out.reshape(n_groups + 1, 4)
+
+
+def class_histogram(category, job_class, n_cat):
+    """Runtime classes per category: array (n_cat, 3) of counts."""
+    category = _c(category, np.uint8)
+    job_class = _c(job_class, np.uint8)
+    out = np.zeros(3 * n_cat, dtype=np.uint32)
+    rc = _load().dsref_class_histogram(len(category), _ptr(category), int(n_cat),
+                                       _ptr(job_class), _ptr(out))
+    if rc != 0:
+        raise ValueError("oracle class_histogram: category or class out of range")
+    return out.reshape(n_cat, 3)
 
 
 def score(counts, category, tenant, group, t_base, s_tenant, state,

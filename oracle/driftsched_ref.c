@@ -22,6 +22,14 @@
  *   dsref_score            Eq. (1), Eq. (2) in the order of Alg. 1, Eq. (4)
  *   dsref_order            FIFO, Priority, Weighted, SJF, Aging Priority
  *                          (Sec. "Scheduling Engine" and its subsections)
+ *   dsref_calibrate_ex     dsref_calibrate, also recording the factor each
+ *                          event's group had just before the event
+ *   dsref_error_stats      MAE, RMSE and mean bias of estimates against
+ *                          observed lengths (Sec. "Impact of Workload
+ *                          Characterization and Runtime Calibration",
+ *                          tab:four_mode_token_error, tab:error_reduction)
+ *   dsref_class_histogram  runtime classes (Eq. (4)) per semantic category
+ *                          (tab:workload_mapping)
  */
 #define _GNU_SOURCE
 #include <math.h>
@@ -154,15 +162,16 @@ int dsref_characterize(const uint8_t *text, uint64_t text_bytes,
  * and leaves B[g] unchanged. trace[e] (if trace is not NULL) is B[g] after
  * event e. Events whose group is >= n_groups are rejected (return -1).
  */
-int dsref_calibrate(const uint32_t *group, const double *est, const uint32_t *obs,
-                    uint64_t n_events, double alpha, uint32_t n_groups,
-                    double *state, double *trace)
+int dsref_calibrate_ex(const uint32_t *group, const double *est, const uint32_t *obs,
+                       uint64_t n_events, double alpha, uint32_t n_groups,
+                       double *state, double *trace, double *trace_before)
 {
     for (uint64_t e = 0; e < n_events; e++)
         if (group[e] >= n_groups) return -1;
     for (uint64_t e = 0; e < n_events; e++) {
         uint32_t g = group[e];
         double x = est[e];
+        if (trace_before) trace_before[e] = state[g];
         if (isfinite(x) && x > 0.0) {
             double r = (double)obs[e] / x;
             double t1 = (1.0 - alpha) * state[g];
@@ -170,6 +179,76 @@ int dsref_calibrate(const uint32_t *group, const double *est, const uint32_t *ob
             state[g] = t1 + t2;
         }
         if (trace) trace[e] = state[g];
+    }
+    return 0;
+}
+
+int dsref_calibrate(const uint32_t *group, const double *est, const uint32_t *obs,
+                    uint64_t n_events, double alpha, uint32_t n_groups,
+                    double *state, double *trace)
+{
+    return dsref_calibrate_ex(group, est, obs, n_events, alpha, n_groups, state, trace, NULL);
+}
+
+/*
+ * Estimation error (tab:four_mode_token_error). The estimate of event e is
+ * x = est[e] * factor[e] (factor NULL: est[e]); events whose x is not finite
+ * and positive are left out, as in the calibration update. With
+ * d = x - observed: MAE = mean |d|, RMSE = sqrt(mean d^2), mean bias =
+ * mean(observed / x), the ratio that the calibration factor tracks (Eq. (6)).
+ * stats[4 g .. 4 g + 3] = count, MAE, RMSE, mean bias of group g, and at
+ * g = n_groups the same over all events. Plain sums in event order.
+ */
+int dsref_error_stats(uint64_t n, const double *est, const double *factor, const uint32_t *obs,
+                      const uint32_t *group, uint32_t n_groups, double *stats)
+{
+    uint64_t slots = (uint64_t)n_groups + 1;
+    double *sum = calloc(4 * slots, sizeof(double));
+    if (!sum) return -2;
+    for (uint64_t e = 0; e < n; e++) {
+        if (group && group[e] >= n_groups) { free(sum); return -1; }
+    }
+    for (uint64_t e = 0; e < n; e++) {
+        double x = est[e];
+        if (factor) x = x * factor[e];
+        if (!(isfinite(x) && x > 0.0)) continue;
+        double o = (double)obs[e];
+        double d = x - o;
+        uint64_t idx[2];
+        int m = 0;
+        if (group) idx[m++] = group[e];
+        idx[m++] = n_groups;
+        for (int k = 0; k < m; k++) {
+            double *s = sum + 4 * idx[k];
+            s[0] += 1.0;
+            s[1] += fabs(d);
+            s[2] += d * d;
+            s[3] += o / x;
+        }
+    }
+    for (uint64_t g = 0; g < slots; g++) {
+        double *s = sum + 4 * g;
+        stats[4 * g] = s[0];
+        if (s[0] > 0.0) {
+            stats[4 * g + 1] = s[1] / s[0];
+            stats[4 * g + 2] = sqrt(s[2] / s[0]);
+            stats[4 * g + 3] = s[3] / s[0];
+        } else {
+            stats[4 * g + 1] = stats[4 * g + 2] = stats[4 * g + 3] = NAN;
+        }
+    }
+    free(sum);
+    return 0;
+}
+
+/* hist[c * 3 + k] = number of requests of category c in runtime class k. */
+int dsref_class_histogram(uint64_t n, const uint8_t *category, uint32_t n_cat,
+                          const uint8_t *job_class, uint32_t *hist)
+{
+    memset(hist, 0, (size_t)n_cat * 3 * sizeof(uint32_t));
+    for (uint64_t i = 0; i < n; i++) {
+        if (category[i] >= n_cat || job_class[i] > 2) return -1;
+        hist[category[i] * 3u + job_class[i]] += 1;
     }
     return 0;
 }

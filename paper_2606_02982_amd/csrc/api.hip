@@ -66,6 +66,8 @@ size_t ds_workspace_bytes(ds_op op, uint64_t n, uint32_t n_groups)
     case DS_OP_SCORE: return kFlagBytes;
     case DS_OP_ORDER: return kFlagBytes + order_ws_bytes(n, 1);
     case DS_OP_ORDER_MULTI: return kFlagBytes + order_ws_bytes(n, 4);
+    case DS_OP_ERROR_STATS: return kFlagBytes + err_ws_bytes(n, n_groups);
+    case DS_OP_CLASS_HIST: return kFlagBytes;
     }
     return 0;
 }
@@ -94,9 +96,10 @@ ds_status ds_characterize(const uint8_t *text, uint64_t text_bytes, const uint64
     });
 }
 
-ds_status ds_calibrate(const uint32_t *group, const double *est, const uint32_t *observed,
-                       uint64_t n_events, double alpha, uint32_t n_groups, double *state,
-                       double *trace, void *ws, size_t ws_bytes, uint32_t flags, ds_stream stream)
+ds_status ds_calibrate_ex(const uint32_t *group, const double *est, const uint32_t *observed,
+                          uint64_t n_events, double alpha, uint32_t n_groups, double *state,
+                          double *trace, double *trace_before, void *ws, size_t ws_bytes,
+                          uint32_t flags, ds_stream stream)
 {
     if (n_events > DS_MAX_ITEMS) return DS_ERR_SIZE;
     if (!(alpha >= 0.0 && alpha <= 1.0)) return DS_ERR_ARG;
@@ -104,15 +107,23 @@ ds_status ds_calibrate(const uint32_t *group, const double *est, const uint32_t 
     if (n_events == 0) return DS_OK;
     if (!group || !est || !observed || !state) return DS_ERR_NULL;
     if (!aligned(group, 4) || !aligned(est, 8) || !aligned(observed, 4) || !aligned(state, 8) ||
-        (trace && !aligned(trace, 8)))
+        (trace && !aligned(trace, 8)) || (trace_before && !aligned(trace_before, 8)))
         return DS_ERR_ALIGN;
     ds_status st = check_ws(ws, ws_bytes, ds_workspace_bytes(DS_OP_CALIBRATE, n_events, n_groups));
     if (st != DS_OK) return st;
     hipStream_t s = static_cast<hipStream_t>(stream);
     return run(ws, flags, s, [&](uint32_t *flag) {
         return cal_launch(group, est, observed, (uint32_t)n_events, alpha, n_groups, state, trace,
-                          after_flag(ws), flag, s);
+                          trace_before, after_flag(ws), flag, s);
     });
+}
+
+ds_status ds_calibrate(const uint32_t *group, const double *est, const uint32_t *observed,
+                       uint64_t n_events, double alpha, uint32_t n_groups, double *state,
+                       double *trace, void *ws, size_t ws_bytes, uint32_t flags, ds_stream stream)
+{
+    return ds_calibrate_ex(group, est, observed, n_events, alpha, n_groups, state, trace, nullptr,
+                           ws, ws_bytes, flags, stream);
 }
 
 ds_status ds_score(uint32_t n, const uint32_t *counts, const uint8_t *category,
@@ -229,6 +240,43 @@ ds_status ds_order_multi(uint32_t policy_mask, uint32_t n, const uint8_t *tier,
     if (!perms) return DS_ERR_NULL;
     return order_common(policy_mask, n, tier, arrival, budget, fifo_in, params, perms, keys, ws,
                         ws_bytes, DS_OP_ORDER_MULTI, flags, stream);
+}
+
+ds_status ds_error_stats(uint64_t n, const double *est, const double *factor,
+                         const uint32_t *observed, const uint32_t *group, uint32_t n_groups,
+                         double *stats, void *ws, size_t ws_bytes, uint32_t flags,
+                         ds_stream stream)
+{
+    if (n > DS_MAX_ITEMS) return DS_ERR_SIZE;
+    if ((group != nullptr) != (n_groups > 0)) return DS_ERR_ARG;
+    if (n_groups > DS_MAX_GROUPS) return DS_ERR_SIZE;
+    if (!stats || (n > 0 && (!est || !observed))) return DS_ERR_NULL;
+    if (!aligned(stats, 8) || (est && !aligned(est, 8)) || (factor && !aligned(factor, 8)) ||
+        (observed && !aligned(observed, 4)) || (group && !aligned(group, 4)))
+        return DS_ERR_ALIGN;
+    ds_status st = check_ws(ws, ws_bytes, ds_workspace_bytes(DS_OP_ERROR_STATS, n, n_groups));
+    if (st != DS_OK) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    return run(ws, flags, s, [&](uint32_t *flag) {
+        return err_launch(n, est, factor, observed, group, n_groups, stats, after_flag(ws), flag, s);
+    });
+}
+
+ds_status ds_class_histogram(uint32_t n, const uint8_t *category, uint32_t n_cat,
+                             const uint8_t *job_class, uint32_t *hist, void *ws, size_t ws_bytes,
+                             uint32_t flags, ds_stream stream)
+{
+    if (n_cat == 0 || n_cat > 256) return DS_ERR_ARG;
+    if (!hist || (n > 0 && (!category || !job_class))) return DS_ERR_NULL;
+    if (!aligned(hist, 4)) return DS_ERR_ALIGN;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (flags & DS_VALIDATE) {
+        ds_status st = check_ws(ws, ws_bytes, ds_workspace_bytes(DS_OP_CLASS_HIST, n, 0));
+        if (st != DS_OK) return st;
+    }
+    return run(ws, flags, s, [&](uint32_t *flag) {
+        return hist_launch(n, category, n_cat, job_class, hist, flag, s);
+    });
 }
 
 }  // extern "C"

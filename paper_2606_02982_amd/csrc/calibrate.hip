@@ -13,7 +13,8 @@
 //   4. each thread composes its carry-in map, applies it to the group's
 //      initial factor, and then runs its 4 events sequentially with the
 //      exact update t1 = (1-alpha) c, t2 = alpha r, c = t1 + t2; it writes
-//      the trace and, at a group's last event, the group's final factor.
+//      the factor before and after each event (the traces) and, at a
+//      group's last event, the group's final factor.
 // Every combine runs in a fixed order, so results are run-to-run identical.
 #include "common.h"
 #include "kernels.h"
@@ -194,7 +195,8 @@ __global__ __launch_bounds__(1024) void k_cal_scan(const Map *__restrict__ tile_
 __global__ __launch_bounds__(kT) void k_cal_apply(Events ev, const Map *__restrict__ tile_carry,
                                                   const double *__restrict__ c0,
                                                   double *__restrict__ state,
-                                                  double *__restrict__ trace)
+                                                  double *__restrict__ trace,
+                                                  double *__restrict__ trace_before)
 {
     __shared__ uint32_t sf[kT];
     __shared__ double sa[kT], sb[kT];
@@ -227,6 +229,7 @@ __global__ __launch_bounds__(kT) void k_cal_apply(Events ev, const Map *__restri
         if (j >= ev.E) break;
         uint32_t g = ck.g[k];
         if (j == 0 || g != gprev) c = g < ev.G ? c0[g] : __builtin_nan("");
+        if (trace_before) trace_before[ck.e[k]] = c;
         if (ck.a[k] != 1.0 || ck.b[k] != 0.0) {
             // the exact sequential update t1 = (1-alpha) c, t2 = alpha r
             double t1 = ck.a[k] * c;
@@ -265,8 +268,8 @@ size_t cal_ws_bytes(uint64_t n, uint32_t n_groups)
 }
 
 hipError_t cal_launch(const uint32_t *group, const double *est, const uint32_t *obs, uint32_t n,
-                      double alpha, uint32_t G, double *state, double *trace, void *ws,
-                      uint32_t *flag, hipStream_t s)
+                      double alpha, uint32_t G, double *state, double *trace, double *trace_before,
+                      void *ws, uint32_t *flag, hipStream_t s)
 {
     if (flag) {
         uint32_t vb = (uint32_t)(cdiv(n, 256) < 1024 ? cdiv(n, 256) : 1024);
@@ -306,7 +309,7 @@ hipError_t cal_launch(const uint32_t *group, const double *est, const uint32_t *
     hipLaunchKernelGGL(k_cal_reduce, dim3(T), dim3(kT), 0, s, ev, agg, (const double *)state, c0);
     hipLaunchKernelGGL(k_cal_scan, dim3(1), dim3(1024), 0, s, (const Map *)agg, T, carry);
     hipLaunchKernelGGL(k_cal_apply, dim3(T), dim3(kT), 0, s, ev, (const Map *)carry,
-                       (const double *)c0, state, trace);
+                       (const double *)c0, state, trace, trace_before);
     return hipGetLastError();
 }
 

@@ -58,7 +58,8 @@ hipError_t sort_launch(const SortInput &in, const SortJob *jobs, uint32_t nsorts
 size_t cal_ws_bytes(uint64_t n, uint32_t n_groups);
 hipError_t cal_launch(const uint32_t *group, const double *est, const uint32_t *obs,
                       uint32_t n, double alpha, uint32_t n_groups, double *state,
-                      double *trace, void *ws, uint32_t *flag, hipStream_t s);
+                      double *trace, double *trace_before, void *ws, uint32_t *flag,
+                      hipStream_t s);
 
 // ---- stage 3: score --------------------------------------------------------------
 hipError_t score_launch(uint32_t n, const uint32_t *counts, const uint8_t *category,
@@ -85,6 +86,14 @@ struct OrderArgs {
     double *key[5];
 };
 hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_t s);
+
+// ---- estimation error and class histogram ------------------------------------------
+size_t err_ws_bytes(uint64_t n, uint32_t n_groups);
+hipError_t err_launch(uint64_t n, const double *est, const double *factor, const uint32_t *obs,
+                      const uint32_t *group, uint32_t n_groups, double *stats, void *ws,
+                      uint32_t *flag, hipStream_t s);
+hipError_t hist_launch(uint32_t n, const uint8_t *category, uint32_t n_cat,
+                       const uint8_t *job_class, uint32_t *hist, uint32_t *flag, hipStream_t s);
 
 // ---- misc --------------------------------------------------------------------------
 hipError_t fill_u32(uint32_t *p, uint32_t v, uint64_t n, hipStream_t s);

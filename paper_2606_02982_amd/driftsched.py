@@ -20,6 +20,7 @@ LIB_PATH = os.path.join(HERE, "libdriftsched.so")
 FIFO, PRIORITY, WEIGHTED, SJF, AGING = 0, 1, 2, 3, 4
 POLICIES = {"fifo": FIFO, "priority": PRIORITY, "weighted": WEIGHTED, "sjf": SJF, "aging": AGING}
 OP_CHARACTERIZE, OP_CALIBRATE, OP_SCORE, OP_ORDER, OP_ORDER_MULTI = 0, 1, 2, 3, 4
+OP_ERROR_STATS, OP_CLASS_HIST = 5, 6
 DS_VALIDATE = 1
 MAX_TIERS = 16
 
@@ -50,12 +51,16 @@ def _load():
     sz = ctypes.c_size_t
     lib.ds_characterize.argtypes = [P, u64, P, u32, P, P, sz, u32, P]
     lib.ds_calibrate.argtypes = [P, P, P, u64, f64, u32, P, P, P, sz, u32, P]
+    lib.ds_calibrate_ex.argtypes = [P, P, P, u64, f64, u32, P, P, P, P, sz, u32, P]
+    lib.ds_error_stats.argtypes = [u64, P, P, P, P, u32, P, P, sz, u32, P]
+    lib.ds_class_histogram.argtypes = [u32, P, u32, P, P, P, sz, u32, P]
     lib.ds_score.argtypes = [u32, P, P, P, P, P, u32, P, u32, P, u32, ctypes.POINTER(ScoreParams),
                              P, P, P, P, P, sz, u32, P]
     lib.ds_order.argtypes = [i32, u32, P, P, P, P, ctypes.POINTER(OrderParams), P, P, P, sz, u32, P]
     lib.ds_order_multi.argtypes = [u32, u32, P, P, P, P, ctypes.POINTER(OrderParams),
                                    ctypes.POINTER(P), ctypes.POINTER(P), P, sz, u32, P]
-    for f in (lib.ds_characterize, lib.ds_calibrate, lib.ds_score, lib.ds_order, lib.ds_order_multi):
+    for f in (lib.ds_characterize, lib.ds_calibrate, lib.ds_calibrate_ex, lib.ds_score, lib.ds_order,
+              lib.ds_order_multi, lib.ds_error_stats, lib.ds_class_histogram):
         f.restype = i32
     lib.ds_workspace_bytes.argtypes = [i32, u64, u32]
     lib.ds_workspace_bytes.restype = sz
@@ -133,25 +138,75 @@ def characterize(text, offsets, counts=None, ws=None, validate=False):
     return counts
 
 
-def calibrate(group, est, observed, alpha, state, trace=True, ws=None, validate=False):
+def calibrate(group, est, observed, alpha, state, trace=True, ws=None, validate=False,
+              trace_before=None):
     """EMA calibration factors (Eq. 5/6). Updates ``state`` in place.
 
-    Returns (state, trace or None)."""
+    Returns (state, trace or None), and the factors before each event as a
+    third item when ``trace_before`` is True or a tensor."""
     _dev(group, torch.int32, "group")
     _dev(est, torch.float64, "est")
     _dev(observed, torch.int32, "observed")
     _dev(state, torch.float64, "state")
     n = group.numel()
-    tr = None
-    if trace is True:
-        tr = torch.empty(n, dtype=torch.float64, device=group.device)
-    elif trace is not None and trace is not False:
-        tr = _dev(trace, torch.float64, "trace")
+
+    def out_arg(x, name):
+        if x is True:
+            return torch.empty(n, dtype=torch.float64, device=group.device)
+        if x is None or x is False:
+            return None
+        return _dev(x, torch.float64, name)
+
+    tr = out_arg(trace, "trace")
+    tb = out_arg(trace_before, "trace_before")
     if ws is None:
         ws = workspace(OP_CALIBRATE, n, state.numel(), group.device)
-    _check(lib.ds_calibrate(_ptr(group), _ptr(est), _ptr(observed), n, float(alpha), state.numel(),
-                            _ptr(state), _ptr(tr), _ptr(ws), ws.numel(), _flags(validate), _stream()))
-    return state, tr
+    _check(lib.ds_calibrate_ex(_ptr(group), _ptr(est), _ptr(observed), n, float(alpha),
+                               state.numel(), _ptr(state), _ptr(tr), _ptr(tb), _ptr(ws), ws.numel(),
+                               _flags(validate), _stream()))
+    if trace_before is None or trace_before is False:
+        return state, tr
+    return state, tr, tb
+
+
+def error_stats(est, observed, factor=None, group=None, n_groups=0, out=None, ws=None,
+                validate=False):
+    """MAE, RMSE and mean bias of est * factor against observed, per group and
+    overall (tab:four_mode_token_error). Returns a (n_groups + 1, 4) float64
+    tensor: count, MAE, RMSE, mean bias; the last row covers all events."""
+    _dev(est, torch.float64, "est")
+    _dev(observed, torch.int32, "observed")
+    if factor is not None:
+        _dev(factor, torch.float64, "factor")
+    if group is not None:
+        _dev(group, torch.int32, "group")
+    n = est.numel()
+    dev = est.device
+    if out is None:
+        out = torch.empty((n_groups + 1, 4), dtype=torch.float64, device=dev)
+    _dev(out, torch.float64, "out")
+    if ws is None:
+        ws = workspace(OP_ERROR_STATS, n, n_groups, dev)
+    _check(lib.ds_error_stats(n, _ptr(est), _ptr(factor), _ptr(observed), _ptr(group), int(n_groups),
+                              _ptr(out), _ptr(ws), ws.numel(), _flags(validate), _stream()))
+    return out
+
+
+def class_histogram(category, job_class, n_cat, out=None, ws=None, validate=False):
+    """Requests per (category, runtime class): a (n_cat, 3) int32 tensor."""
+    _dev(category, torch.uint8, "category")
+    _dev(job_class, torch.uint8, "job_class")
+    n = category.numel()
+    dev = category.device
+    if out is None:
+        out = torch.empty((n_cat, 3), dtype=torch.int32, device=dev)
+    _dev(out, torch.int32, "out")
+    if ws is None and validate:
+        ws = workspace(OP_CLASS_HIST, n, 0, dev)
+    _check(lib.ds_class_histogram(n, _ptr(category), int(n_cat), _ptr(job_class), _ptr(out),
+                                  _ptr(ws), ws.numel() if ws is not None else 0, _flags(validate),
+                                  _stream()))
+    return out
 
 
 def score(counts, category, tenant, group, t_base, s_tenant, state, f_ref=1024.0,

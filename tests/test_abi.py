@@ -25,7 +25,8 @@ def declared_functions():
 
 def test_exports_every_declared_symbol(ds):
     names = declared_functions()
-    assert names == ["ds_calibrate", "ds_characterize", "ds_order", "ds_order_multi", "ds_score",
+    assert names == ["ds_calibrate", "ds_calibrate_ex", "ds_characterize", "ds_class_histogram",
+                     "ds_error_stats", "ds_order", "ds_order_multi", "ds_score",
                      "ds_status_string", "ds_version", "ds_workspace_bytes"]
     for name in names:
         assert hasattr(ds.lib, name), name
@@ -40,11 +41,14 @@ def test_status_strings(ds):
 
 
 def test_workspace_sizes(ds):
-    for op in range(5):
+    for op in range(7):
         sizes = [ds.workspace_bytes(op, n, 64) for n in (0, 1, 4096, 65536, 1 << 20)]
         assert all(s >= 256 for s in sizes)
         assert sizes == sorted(sizes)
     assert ds.workspace_bytes(ds.OP_SCORE, 1 << 20) == 256
+    assert ds.workspace_bytes(ds.OP_CLASS_HIST, 1 << 20) == 256
+    # error statistics: sums for every group and for all events
+    assert ds.workspace_bytes(ds.OP_ERROR_STATS, 10, 7) >= 256 + 4 * 8 * 8
 
 
 P = ctypes.c_void_p
@@ -123,3 +127,36 @@ def test_order_multi_host_errors(ds):
     assert need > ds.workspace_bytes(ds.OP_ORDER, 10)
     assert f(0x1F, 10, FAKE, FAKE, FAKE, NULL, ctypes.byref(p), perms, NULL, FAKE_WS, need - 1, 0,
              NULL) == -4
+
+
+def test_calibrate_ex_host_errors(ds):
+    f = ds.lib.ds_calibrate_ex
+    ws = 1 << 30
+    assert f(FAKE, FAKE, FAKE, 10, 1.5, 4, FAKE, NULL, NULL, FAKE_WS, ws, 0, NULL) == -2
+    assert f(FAKE, FAKE, FAKE, 10, 0.1, 4, FAKE, NULL, P(0x1004), FAKE_WS, ws, 0, NULL) == -7
+    assert f(FAKE, NULL, FAKE, 10, 0.1, 4, FAKE, NULL, FAKE, FAKE_WS, ws, 0, NULL) == -1
+    assert f(FAKE, FAKE, FAKE, 0, 0.1, 4, FAKE, NULL, NULL, NULL, 0, 0, NULL) == 0
+
+
+def test_error_stats_host_errors(ds):
+    f = ds.lib.ds_error_stats
+    ws = 1 << 30
+    # group and n_groups go together
+    assert f(10, FAKE, NULL, FAKE, FAKE, 0, FAKE, FAKE_WS, ws, 0, NULL) == -2
+    assert f(10, FAKE, NULL, FAKE, NULL, 3, FAKE, FAKE_WS, ws, 0, NULL) == -2
+    assert f(10, FAKE, NULL, FAKE, FAKE, (1 << 20) + 1, FAKE, FAKE_WS, ws, 0, NULL) == -3
+    assert f((1 << 30) + 1, FAKE, NULL, FAKE, NULL, 0, FAKE, FAKE_WS, ws, 0, NULL) == -3
+    assert f(10, NULL, NULL, FAKE, NULL, 0, FAKE, FAKE_WS, ws, 0, NULL) == -1
+    assert f(10, FAKE, NULL, FAKE, NULL, 0, NULL, FAKE_WS, ws, 0, NULL) == -1
+    assert f(10, P(0x1004), NULL, FAKE, NULL, 0, FAKE, FAKE_WS, ws, 0, NULL) == -7
+    assert f(10, FAKE, NULL, FAKE, FAKE, 5, FAKE, FAKE_WS, 64, 0, NULL) == -4
+
+
+def test_class_histogram_host_errors(ds):
+    f = ds.lib.ds_class_histogram
+    assert f(10, FAKE, 0, FAKE, FAKE, NULL, 0, 0, NULL) == -2
+    assert f(10, FAKE, 257, FAKE, FAKE, NULL, 0, 0, NULL) == -2
+    assert f(10, NULL, 4, FAKE, FAKE, NULL, 0, 0, NULL) == -1
+    assert f(10, FAKE, 4, FAKE, NULL, NULL, 0, 0, NULL) == -1
+    assert f(10, FAKE, 4, FAKE, P(0x1002), NULL, 0, 0, NULL) == -7
+    assert f(10, FAKE, 4, FAKE, FAKE, NULL, 0, 1, NULL) == -4     # DS_VALIDATE needs a workspace
