@@ -20,6 +20,11 @@
  *   ds_error_stats      MAE, RMSE and mean bias of estimates vs observed
  *   ds_class_histogram  runtime classes per semantic category
  *
+ * and the online loop that ties the stages together:
+ *
+ *   ds_simulate         dispatch ticks: order the pending set, dispatch a
+ *                       batch, feed its completions back into the factors
+ *
  * Conventions shared by every entry point:
  *  - Array arguments are DEVICE pointers (memory from hipMalloc or any
  *    allocator of the same device, e.g. torch tensors); parameter structs
@@ -76,7 +81,8 @@ typedef enum {
     DS_OP_ORDER = 3,
     DS_OP_ORDER_MULTI = 4,
     DS_OP_ERROR_STATS = 5,
-    DS_OP_CLASS_HIST = 6
+    DS_OP_CLASS_HIST = 6,
+    DS_OP_SIMULATE = 7
 } ds_op;
 
 /* flags */
@@ -85,6 +91,7 @@ typedef enum {
 #define DS_MAX_TIERS 16
 #define DS_MAX_ITEMS (1u << 30)   /* max events for ds_calibrate, requests for ds_order */
 #define DS_MAX_GROUPS (1u << 20)  /* max groups for ds_error_stats */
+#define DS_MAX_BATCH 1024         /* max requests per dispatch tick for ds_simulate */
 
 typedef void *ds_stream;    /* hipStream_t */
 
@@ -304,6 +311,62 @@ ds_status ds_error_stats(uint64_t n, const double *est, const double *factor,
 ds_status ds_class_histogram(uint32_t n, const uint8_t *category, uint32_t n_cat,
                              const uint8_t *job_class, uint32_t *hist,
                              void *ws, size_t ws_bytes, uint32_t flags, ds_stream stream);
+
+/* Parameters of the dispatch-tick loop. */
+typedef struct {
+    ds_policy policy;       /* dispatch policy of every tick */
+    uint32_t batch;         /* requests dispatched per tick: 1..DS_MAX_BATCH (32 in the paper) */
+    double alpha;           /* EMA weight of Eq. (5), in [0, 1] */
+    ds_score_params score;  /* budget and factor F of Eq. (1)/(2); the class bounds are unused */
+    ds_order_params order;  /* tiers, weights, priorities, aging; t_now is unused (tick k
+                               ages to tick_t[k]) */
+} ds_sim_params;
+
+/*
+ * Dispatch ticks of the online loop (Sec. "Experimental Configuration":
+ * dispatch in batches of 32; Sec. "Calibration and Evaluation Phases" and
+ * Sec. "Runtime Calibration and Feedback Adaptation": completed requests keep
+ * refining later estimates).
+ *
+ * At tick k the pending set is every request i with arrival[i] <= tick_t[k]
+ * that no earlier tick dispatched. It is ordered as ds_order orders it on
+ * those requests alone: SJF with the budgets ds_score gives with the factors
+ * as they stand, Aging with t_now = tick_t[k], Weighted with a fresh
+ * round-robin cycle over the pending tier queues; ties in FIFO order. The
+ * first min(batch, pending) requests are dispatched, then their completions
+ * update the factors as ds_calibrate does, in dispatch order: event
+ * (group[i], B-free estimate of request i as ds_score's est_base, observed[i]).
+ *
+ *  n          requests, <= DS_MAX_ITEMS
+ *  arrival    device, n double; contract: not NaN
+ *  tier       device, n uint8; contract: < params->order.n_tiers
+ *  counts     device, n uint32: input words (e.g. from ds_characterize)
+ *  category   device, n uint8; contract: < n_cat
+ *  tenant     device, n uint32; contract: < n_tenants
+ *  group      device, n uint32: calibration group; contract: < n_groups
+ *  observed   device, n uint32: output tokens the request turns out to have
+ *  t_base     device, n_cat double;  s_tenant: device, n_tenants double
+ *  n_groups   >= 1
+ *  tick_t     device, n_ticks double; contract: non-decreasing, not NaN
+ *  n_ticks    <= 2^31 - 1
+ *  state      device, n_groups double: factors before the first tick; updated in place
+ *  seq        device, n uint32: seq[d] = the request dispatched d-th;
+ *             0xFFFFFFFF past the last dispatch
+ *  tick_of    device, n int32: the tick that dispatched request i, -1 if none
+ *  n_dispatched  device, 1 uint32: number of requests dispatched
+ *  ws         workspace of ds_workspace_bytes(DS_OP_SIMULATE, n, 0) bytes
+ * One workgroup runs all ticks in one launch, so the call is meant for
+ * pending sets of up to about 10^5 requests; its time grows with the pending
+ * set times the number of ticks. n == 0 writes *n_dispatched = 0.
+ */
+ds_status ds_simulate(uint32_t n, const double *arrival, const uint8_t *tier,
+                      const uint32_t *counts, const uint8_t *category, const uint32_t *tenant,
+                      const uint32_t *group, const uint32_t *observed,
+                      const double *t_base, uint32_t n_cat, const double *s_tenant,
+                      uint32_t n_tenants, uint32_t n_groups,
+                      const double *tick_t, uint32_t n_ticks, const ds_sim_params *params,
+                      double *state, uint32_t *seq, int32_t *tick_of, uint32_t *n_dispatched,
+                      void *ws, size_t ws_bytes, uint32_t flags, ds_stream stream);
 
 /* Workspace size for op at size n (prompts, events or requests); n_groups
  * is used by DS_OP_CALIBRATE only. */

@@ -64,6 +64,10 @@ def _load():
     lib.dsref_score.restype = i32
     lib.dsref_order.argtypes = [i32, u32, P, P, P, u32, P, P, f64, f64, f64, P, P]
     lib.dsref_order.restype = i32
+    lib.dsref_simulate.argtypes = [i32, u32, P, P, P, P, P, P, P, P, u32, P, u32, u32,
+                                   f64, f64, f64, u32, P, P, f64, f64, f64, u32, P, u32, P,
+                                   P, P, P]
+    lib.dsref_simulate.restype = i32
     _lib = lib
     return lib
 
@@ -194,3 +198,44 @@ def order(policy, tier, arrival, budget=None, weights=(4, 2, 1),
     if rc != 0:
         raise ValueError("oracle order: bad tier, weight or policy")
     return perm, key
+
+
+def simulate(policy, arrival, tier, counts, category, tenant, group, observed, t_base,
+             s_tenant, state, tick_t, batch=32, alpha=0.1, weights=(4, 2, 1),
+             tier_priority=(0.0, 1.0, 2.0), aging_rate=0.01, aging_floor=0.0,
+             f_ref=1024.0, short_max=128.0, medium_max=512.0):
+    """Dispatch ticks of the online loop: order the pending set, dispatch a
+    batch, fold its completions into the factors (dsref_simulate).
+
+    Returns (seq[:n_dispatched], tick_of, state after the last tick).
+    """
+    arrival = _c(arrival, np.float64)
+    tier = _c(tier, np.uint8)
+    counts = _c(counts, np.uint32)
+    category = _c(category, np.uint8)
+    tenant = _c(tenant, np.uint32)
+    group = _c(group, np.uint32)
+    observed = _c(observed, np.uint32)
+    t_base = _c(t_base, np.float64)
+    s_tenant = _c(s_tenant, np.float64)
+    st = np.array(state, dtype=np.float64)
+    tick_t = _c(tick_t, np.float64)
+    w = _c(weights, np.uint32)
+    tp = _c(tier_priority, np.float64)
+    if len(w) != len(tp):
+        raise ValueError("weights and tier_priority must have one entry per tier")
+    n = len(arrival)
+    seq = np.zeros(n, np.uint32)
+    tick_of = np.zeros(n, np.int32)
+    nd = ctypes.c_uint32(0)
+    rc = _load().dsref_simulate(int(policy), n, _ptr(arrival), _ptr(tier), _ptr(counts),
+                                _ptr(category), _ptr(tenant), _ptr(group), _ptr(observed),
+                                _ptr(t_base), len(t_base), _ptr(s_tenant), len(s_tenant),
+                                len(st), float(f_ref), float(short_max), float(medium_max),
+                                len(w), _ptr(w), _ptr(tp), float(aging_rate),
+                                float(aging_floor), float(alpha), int(batch), _ptr(tick_t),
+                                len(tick_t), _ptr(st), _ptr(seq), _ptr(tick_of),
+                                ctypes.byref(nd))
+    if rc != 0:
+        raise ValueError("oracle simulate: bad index, weight, policy or batch")
+    return seq[:nd.value], tick_of, st

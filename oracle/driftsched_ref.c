@@ -30,6 +30,11 @@
  *                          tab:four_mode_token_error, tab:error_reduction)
  *   dsref_class_histogram  runtime classes (Eq. (4)) per semantic category
  *                          (tab:workload_mapping)
+ *   dsref_simulate         dispatch ticks of the online loop: order the
+ *                          pending set, dispatch a batch, feed its
+ *                          completions back (Sec. "Experimental
+ *                          Configuration", Sec. "Calibration and Evaluation
+ *                          Phases")
  */
 #define _GNU_SOURCE
 #include <math.h>
@@ -441,4 +446,100 @@ int dsref_order(int policy, uint32_t n, const uint8_t *tier, const double *arriv
         return 0;
     }
     return -1;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Dispatch ticks: the online loop                                           */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * The scheduler dispatches pending requests in batches (Sec. "Experimental
+ * Configuration": batch size 32) and keeps adapting its estimates as
+ * requests complete (Sec. "Calibration and Evaluation Phases"; Sec.
+ * "Runtime Calibration and Feedback Adaptation"). At tick k, with time
+ * tick_t[k]:
+ *   1. the pending set is every request with arrival <= tick_t[k] that has
+ *      not been dispatched, taken in index order;
+ *   2. it is ordered by dsref_order under the policy, on the pending
+ *      requests alone: SJF with budgets scored (dsref_score) from the
+ *      factors as they stand, Aging with t_now = tick_t[k], Weighted with a
+ *      fresh round-robin cycle over the pending tier queues;
+ *   3. the first min(batch, pending) requests of that order are dispatched;
+ *   4. their completions, in dispatch order, update the factors with
+ *      dsref_calibrate: group[i], the B-free estimate est_base[i] of
+ *      dsref_score, observed[i].
+ * seq[d] = the request dispatched d-th (0xFFFFFFFF past the last one),
+ * tick_of[i] = the tick that dispatched request i (-1 if none), and
+ * *n_dispatched the number dispatched. state (n_groups) is updated in place.
+ * Returns -1 on an out-of-range index, a zero weight or batch == 0.
+ */
+int dsref_simulate(int policy, uint32_t n, const double *arrival, const uint8_t *tier,
+                   const uint32_t *counts, const uint8_t *category, const uint32_t *tenant,
+                   const uint32_t *group, const uint32_t *observed,
+                   const double *t_base, uint32_t n_cat, const double *s_tenant,
+                   uint32_t n_tenants, uint32_t n_groups,
+                   double f_ref, double short_max, double medium_max,
+                   uint32_t n_tiers, const uint32_t *weight, const double *tier_priority,
+                   double aging_rate, double aging_floor, double alpha, uint32_t batch,
+                   const double *tick_t, uint32_t n_ticks, double *state,
+                   uint32_t *seq, int32_t *tick_of, uint32_t *n_dispatched)
+{
+    if (batch == 0) return -1;
+    uint32_t m = n ? n : 1;
+    double *est_base = (double *)malloc(sizeof(double) * m);
+    double *est = (double *)malloc(sizeof(double) * m);
+    double *budget = (double *)malloc(sizeof(double) * m);
+    uint8_t *cls = (uint8_t *)malloc(m);
+    uint8_t *done = (uint8_t *)calloc(m, 1);
+    uint32_t *pend = (uint32_t *)malloc(sizeof(uint32_t) * m);
+    uint8_t *p_tier = (uint8_t *)malloc(m);
+    double *p_arrival = (double *)malloc(sizeof(double) * m);
+    double *p_budget = (double *)malloc(sizeof(double) * m);
+    uint32_t *perm = (uint32_t *)malloc(sizeof(uint32_t) * m);
+    uint32_t *ev_group = (uint32_t *)malloc(sizeof(uint32_t) * m);
+    uint32_t *ev_obs = (uint32_t *)malloc(sizeof(uint32_t) * m);
+    double *ev_est = (double *)malloc(sizeof(double) * m);
+    int rc = dsref_score(n, counts, category, tenant, group, t_base, n_cat, s_tenant, n_tenants,
+                         state, n_groups, f_ref, short_max, medium_max, est_base, est, budget, cls);
+    for (uint32_t i = 0; i < n; i++) {
+        seq[i] = 0xFFFFFFFFu;
+        tick_of[i] = -1;
+    }
+    uint32_t total = 0;
+    for (uint32_t k = 0; rc == 0 && k < n_ticks; k++) {
+        double t = tick_t[k];
+        uint32_t np = 0;
+        for (uint32_t i = 0; i < n; i++)
+            if (arrival[i] <= t && !done[i]) pend[np++] = i;
+        if (policy == REF_SJF)
+            rc = dsref_score(n, counts, category, tenant, group, t_base, n_cat, s_tenant,
+                             n_tenants, state, n_groups, f_ref, short_max, medium_max, NULL, est,
+                             budget, cls);
+        for (uint32_t j = 0; j < np; j++) {
+            p_tier[j] = tier[pend[j]];
+            p_arrival[j] = arrival[pend[j]];
+            p_budget[j] = budget[pend[j]];
+        }
+        if (rc == 0)
+            rc = dsref_order(policy, np, p_tier, p_arrival, p_budget, n_tiers, weight,
+                             tier_priority, aging_rate, t, aging_floor, perm, NULL);
+        if (rc != 0) break;
+        uint32_t take = np < batch ? np : batch;
+        for (uint32_t j = 0; j < take; j++) {
+            uint32_t i = pend[perm[j]];
+            done[i] = 1;
+            seq[total++] = i;
+            tick_of[i] = (int32_t)k;
+            ev_group[j] = group[i];
+            ev_est[j] = est_base[i];
+            ev_obs[j] = observed[i];
+        }
+        /* their completions, in dispatch order */
+        rc = dsref_calibrate(ev_group, ev_est, ev_obs, take, alpha, n_groups, state, NULL);
+    }
+    *n_dispatched = total;
+    free(est_base); free(est); free(budget); free(cls); free(done); free(pend);
+    free(p_tier); free(p_arrival); free(p_budget); free(perm);
+    free(ev_group); free(ev_obs); free(ev_est);
+    return rc;
 }

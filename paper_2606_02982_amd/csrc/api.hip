@@ -68,6 +68,7 @@ size_t ds_workspace_bytes(ds_op op, uint64_t n, uint32_t n_groups)
     case DS_OP_ORDER_MULTI: return kFlagBytes + order_ws_bytes(n, 4);
     case DS_OP_ERROR_STATS: return kFlagBytes + err_ws_bytes(n, n_groups);
     case DS_OP_CLASS_HIST: return kFlagBytes;
+    case DS_OP_SIMULATE: return kFlagBytes + sim_ws_bytes(n);
     }
     return 0;
 }
@@ -277,6 +278,77 @@ ds_status ds_class_histogram(uint32_t n, const uint8_t *category, uint32_t n_cat
     return run(ws, flags, s, [&](uint32_t *flag) {
         return hist_launch(n, category, n_cat, job_class, hist, flag, s);
     });
+}
+
+ds_status ds_simulate(uint32_t n, const double *arrival, const uint8_t *tier,
+                      const uint32_t *counts, const uint8_t *category, const uint32_t *tenant,
+                      const uint32_t *group, const uint32_t *observed, const double *t_base,
+                      uint32_t n_cat, const double *s_tenant, uint32_t n_tenants,
+                      uint32_t n_groups, const double *tick_t, uint32_t n_ticks,
+                      const ds_sim_params *params, double *state, uint32_t *seq,
+                      int32_t *tick_of, uint32_t *n_dispatched, void *ws, size_t ws_bytes,
+                      uint32_t flags, ds_stream stream)
+{
+    if (!params) return DS_ERR_NULL;
+    const int policy = (int)params->policy;
+    if (policy < 0 || policy > 4) return DS_ERR_ARG;
+    if (params->batch < 1 || params->batch > DS_MAX_BATCH) return DS_ERR_ARG;
+    if (!(params->alpha >= 0.0 && params->alpha <= 1.0)) return DS_ERR_ARG;
+    if (!(params->score.f_ref > 0.0)) return DS_ERR_ARG;
+    ds_order_params op = params->order;
+    op.t_now = 0.0;   // each tick ages to its own time
+    ds_status st = check_order_params(&op, 1u << policy);
+    if (st != DS_OK) return st;
+    if (n_cat == 0 || n_cat > 256 || n_tenants == 0 || n_groups == 0) return DS_ERR_ARG;
+    if (n > DS_MAX_ITEMS) return DS_ERR_SIZE;
+    if (n_ticks > 0x7FFFFFFFu) return DS_ERR_SIZE;
+    if (!n_dispatched) return DS_ERR_NULL;
+    if (n > 0 && (!arrival || !tier || !counts || !category || !tenant || !group || !observed ||
+                  !t_base || !s_tenant || !state || !seq || !tick_of || (n_ticks && !tick_t)))
+        return DS_ERR_NULL;
+    if (!aligned(n_dispatched, 4) || (arrival && !aligned(arrival, 8)) ||
+        (counts && !aligned(counts, 4)) || (tenant && !aligned(tenant, 4)) ||
+        (group && !aligned(group, 4)) || (observed && !aligned(observed, 4)) ||
+        (t_base && !aligned(t_base, 8)) || (s_tenant && !aligned(s_tenant, 8)) ||
+        (state && !aligned(state, 8)) || (seq && !aligned(seq, 4)) ||
+        (tick_of && !aligned(tick_of, 4)) || (tick_t && !aligned(tick_t, 8)))
+        return DS_ERR_ALIGN;
+    st = check_ws(ws, ws_bytes, ds_workspace_bytes(DS_OP_SIMULATE, n, 0));
+    if (st != DS_OK) return st;
+    SimArgs a;
+    memset(&a, 0, sizeof(a));
+    a.n = n;
+    a.n_groups = n_groups;
+    a.policy = (uint32_t)policy;
+    a.batch = params->batch;
+    a.n_ticks = n_ticks;
+    a.tick_t = tick_t;
+    a.alpha = params->alpha;
+    a.arrival = arrival;
+    a.tier = tier;
+    a.counts = counts;
+    a.tenant = tenant;
+    a.group = group;
+    a.observed = observed;
+    a.category = category;
+    a.t_base = t_base;
+    a.s_tenant = s_tenant;
+    a.n_cat = n_cat;
+    a.n_tenants = n_tenants;
+    a.f_ref = params->score.f_ref;
+    a.n_tiers = params->order.n_tiers;
+    for (uint32_t q = 0; q < DS_MAX_TIERS; q++) {
+        a.weight[q] = q < a.n_tiers ? params->order.weight[q] : 1u;
+        a.prio[q] = q < a.n_tiers ? params->order.tier_priority[q] : 0.0;
+    }
+    a.aging_rate = params->order.aging_rate;
+    a.aging_floor = params->order.aging_floor;
+    a.state = state;
+    a.seq = seq;
+    a.tick_of = tick_of;
+    a.n_dispatched = n_dispatched;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    return run(ws, flags, s, [&](uint32_t *flag) { return sim_launch(a, after_flag(ws), flag, s); });
 }
 
 }  // extern "C"

@@ -95,6 +95,31 @@ hipError_t err_launch(uint64_t n, const double *est, const double *factor, const
 hipError_t hist_launch(uint32_t n, const uint8_t *category, uint32_t n_cat,
                        const uint8_t *job_class, uint32_t *hist, uint32_t *flag, hipStream_t s);
 
+// ---- dispatch-tick simulator --------------------------------------------------------
+struct SimArgs {
+    uint32_t n, n_groups, policy, batch, n_ticks;
+    const double *tick_t;      // device, n_ticks, non-decreasing
+    double alpha;
+    const double *arrival;
+    const uint8_t *tier;
+    const uint32_t *counts, *tenant, *group, *observed;
+    const uint8_t *category;
+    const double *t_base, *s_tenant;
+    uint32_t n_cat, n_tenants;
+    double f_ref;
+    uint32_t n_tiers;
+    uint32_t weight[16];
+    double prio[16];
+    double aging_rate, aging_floor;
+    double *state;
+    uint32_t *seq;
+    int32_t *tick_of;
+    uint32_t *n_dispatched;
+};
+constexpr uint32_t kSimMaxBatch = 1024;
+size_t sim_ws_bytes(uint64_t n);
+hipError_t sim_launch(const SimArgs &a, void *ws, uint32_t *flag, hipStream_t s);
+
 // ---- misc --------------------------------------------------------------------------
 hipError_t fill_u32(uint32_t *p, uint32_t v, uint64_t n, hipStream_t s);
 

@@ -20,9 +20,10 @@ LIB_PATH = os.path.join(HERE, "libdriftsched.so")
 FIFO, PRIORITY, WEIGHTED, SJF, AGING = 0, 1, 2, 3, 4
 POLICIES = {"fifo": FIFO, "priority": PRIORITY, "weighted": WEIGHTED, "sjf": SJF, "aging": AGING}
 OP_CHARACTERIZE, OP_CALIBRATE, OP_SCORE, OP_ORDER, OP_ORDER_MULTI = 0, 1, 2, 3, 4
-OP_ERROR_STATS, OP_CLASS_HIST = 5, 6
+OP_ERROR_STATS, OP_CLASS_HIST, OP_SIMULATE = 5, 6, 7
 DS_VALIDATE = 1
 MAX_TIERS = 16
+MAX_BATCH = 1024
 
 
 class DriftSchedError(RuntimeError):
@@ -42,6 +43,11 @@ class OrderParams(ctypes.Structure):
                 ("t_now", ctypes.c_double), ("aging_floor", ctypes.c_double)]
 
 
+class SimParams(ctypes.Structure):
+    _fields_ = [("policy", ctypes.c_int), ("batch", ctypes.c_uint32), ("alpha", ctypes.c_double),
+                ("score", ScoreParams), ("order", OrderParams)]
+
+
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError("libdriftsched.so is not built (run paper_2606_02982_amd.build.build())")
@@ -59,8 +65,10 @@ def _load():
     lib.ds_order.argtypes = [i32, u32, P, P, P, P, ctypes.POINTER(OrderParams), P, P, P, sz, u32, P]
     lib.ds_order_multi.argtypes = [u32, u32, P, P, P, P, ctypes.POINTER(OrderParams),
                                    ctypes.POINTER(P), ctypes.POINTER(P), P, sz, u32, P]
+    lib.ds_simulate.argtypes = [u32, P, P, P, P, P, P, P, P, u32, P, u32, u32, P, u32,
+                                ctypes.POINTER(SimParams), P, P, P, P, P, sz, u32, P]
     for f in (lib.ds_characterize, lib.ds_calibrate, lib.ds_calibrate_ex, lib.ds_score, lib.ds_order,
-              lib.ds_order_multi, lib.ds_error_stats, lib.ds_class_histogram):
+              lib.ds_order_multi, lib.ds_error_stats, lib.ds_class_histogram, lib.ds_simulate):
         f.restype = i32
     lib.ds_workspace_bytes.argtypes = [i32, u64, u32]
     lib.ds_workspace_bytes.restype = sz
@@ -318,3 +326,53 @@ def order_multi(policies, tier, arrival, budget=None, fifo=None, params=None, pe
                               ctypes.byref(params), pp, kk if keys else None, _ptr(ws), ws.numel(),
                               _flags(validate), _stream()))
     return out_p, out_k
+
+
+def sim_params(policy, batch=32, alpha=0.1, f_ref=1024.0, **order_kw):
+    """ds_sim_params for ``simulate`` (order_kw as ``order_params``)."""
+    if isinstance(policy, str):
+        policy = POLICIES[policy]
+    p = SimParams()
+    p.policy = int(policy)
+    p.batch = int(batch)
+    p.alpha = float(alpha)
+    p.score = ScoreParams(float(f_ref), 128.0, 512.0)
+    p.order = order_params(**order_kw)
+    return p
+
+
+def simulate(arrival, tier, counts, category, tenant, group, observed, t_base, s_tenant, state,
+             tick_t, params, out=None, ws=None, validate=False):
+    """Dispatch ticks of the online loop; ``state`` is updated in place.
+
+    Returns (seq, tick_of, n_dispatched): device tensors (int32 x2, and one
+    int32 element) without a host synchronisation.
+    """
+    _dev(arrival, torch.float64, "arrival")
+    _dev(tier, torch.uint8, "tier")
+    _dev(counts, torch.int32, "counts")
+    _dev(category, torch.uint8, "category")
+    _dev(tenant, torch.int32, "tenant")
+    _dev(group, torch.int32, "group")
+    _dev(observed, torch.int32, "observed")
+    _dev(t_base, torch.float64, "t_base")
+    _dev(s_tenant, torch.float64, "s_tenant")
+    _dev(state, torch.float64, "state")
+    _dev(tick_t, torch.float64, "tick_t")
+    n = arrival.numel()
+    dev = arrival.device
+    if out is None:
+        seq = torch.empty(n, dtype=torch.int32, device=dev)
+        tick_of = torch.empty(n, dtype=torch.int32, device=dev)
+        nd = torch.empty(1, dtype=torch.int32, device=dev)
+    else:
+        seq, tick_of, nd = out
+    if ws is None:
+        ws = workspace(OP_SIMULATE, n, 0, dev)
+    _check(lib.ds_simulate(n, _ptr(arrival), _ptr(tier), _ptr(counts), _ptr(category),
+                           _ptr(tenant), _ptr(group), _ptr(observed), _ptr(t_base),
+                           t_base.numel(), _ptr(s_tenant), s_tenant.numel(), state.numel(),
+                           _ptr(tick_t), tick_t.numel(), ctypes.byref(params), _ptr(state),
+                           _ptr(seq), _ptr(tick_of), _ptr(nd), _ptr(ws), ws.numel(),
+                           _flags(validate), _stream()))
+    return seq, tick_of, nd

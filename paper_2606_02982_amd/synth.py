@@ -238,6 +238,10 @@ def generate(wl, n=None, with_text=True):
     out["ev_group"] = tenant[ev_req].astype(np.uint32)
     out["ev_est"] = nominal
     out["ev_obs"] = obs
+    # the same observed lengths per request, in batch order
+    observed = np.empty(n, dtype=np.uint32)
+    observed[ev_req] = obs
+    out["observed"] = observed
 
     if wl.has_text and with_text:
         text, offsets = make_text(words, wl.seed, wl.nonascii_p)
@@ -251,6 +255,16 @@ def generate(wl, n=None, with_text=True):
         # set is a prefix
         out["tick_n"] = np.searchsorted(arrival_sorted, t, side="right").astype(np.int64)
     return out
+
+
+def sim_ticks(arrival, batch=32, dt=0.01, extra=16):
+    """Dispatch tick times dt, 2 dt, ...: one tick per `dt` seconds (the
+    batch wait), enough of them to dispatch every request in batches of
+    `batch` once all have arrived, plus `extra`."""
+    n = len(arrival)
+    amax = float(np.max(arrival)) if n else 0.0
+    k = max(int(np.ceil(amax / dt)), -(-n // batch)) + extra
+    return dt * np.arange(1, k + 1, dtype=np.float64)
 
 
 def text_bytes_estimate(wl):

@@ -27,7 +27,7 @@ def test_exports_every_declared_symbol(ds):
     names = declared_functions()
     assert names == ["ds_calibrate", "ds_calibrate_ex", "ds_characterize", "ds_class_histogram",
                      "ds_error_stats", "ds_order", "ds_order_multi", "ds_score",
-                     "ds_status_string", "ds_version", "ds_workspace_bytes"]
+                     "ds_simulate", "ds_status_string", "ds_version", "ds_workspace_bytes"]
     for name in names:
         assert hasattr(ds.lib, name), name
 
@@ -41,7 +41,7 @@ def test_status_strings(ds):
 
 
 def test_workspace_sizes(ds):
-    for op in range(7):
+    for op in range(8):
         sizes = [ds.workspace_bytes(op, n, 64) for n in (0, 1, 4096, 65536, 1 << 20)]
         assert all(s >= 256 for s in sizes)
         assert sizes == sorted(sizes)
@@ -160,3 +160,38 @@ def test_class_histogram_host_errors(ds):
     assert f(10, FAKE, 4, FAKE, NULL, NULL, 0, 0, NULL) == -1
     assert f(10, FAKE, 4, FAKE, P(0x1002), NULL, 0, 0, NULL) == -7
     assert f(10, FAKE, 4, FAKE, FAKE, NULL, 0, 1, NULL) == -4     # DS_VALIDATE needs a workspace
+
+
+def test_simulate_host_errors(ds):
+    f = ds.lib.ds_simulate
+    ws = 1 << 40
+
+    # every call below must fail a host check (none may reach a launch)
+    def call(params, n=10, n_cat=4, n_tenants=2, n_groups=3, tick_t=FAKE, n_ticks=5, seq=FAKE,
+             nd=FAKE, wsb=ws, arrival=FAKE):
+        st = f(n, arrival, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, n_cat, FAKE, n_tenants,
+               n_groups, tick_t, n_ticks, ctypes.byref(params) if params is not None else None,
+               FAKE, seq, FAKE, nd, FAKE_WS, wsb, 0, NULL)
+        assert st != 0
+        return st
+
+    ok = ds.sim_params("sjf")
+    assert call(None) == -1
+    assert call(ds.sim_params(5)) == -2
+    assert call(ds.sim_params("fifo", batch=0)) == -2
+    assert call(ds.sim_params("fifo", batch=1025)) == -2
+    assert call(ds.sim_params("fifo", alpha=1.5)) == -2
+    assert call(ds.sim_params("fifo", f_ref=0.0)) == -2
+    assert call(ds.sim_params("weighted", weights=(1, 0, 1))) == -2
+    assert call(ds.sim_params("aging", aging_rate=-1.0)) == -2
+    assert call(ds.sim_params("fifo", n_tiers=0)) == -2
+    assert call(ok, n_cat=0) == -2 and call(ok, n_cat=257) == -2
+    assert call(ok, n_tenants=0) == -2 and call(ok, n_groups=0) == -2
+    assert call(ok, n=(1 << 30) + 1) == -3
+    assert call(ok, n_ticks=1 << 31) == -3
+    assert call(ok, nd=NULL) == -1 and call(ok, seq=NULL) == -1
+    assert call(ok, tick_t=NULL) == -1
+    assert call(ok, arrival=P(0x1004)) == -7
+    assert call(ok, wsb=ds.workspace_bytes(ds.OP_SIMULATE, 10) - 1) == -4
+    # t_now is not used: each tick ages to its own time
+    assert call(ds.sim_params("aging", t_now=float("nan")), wsb=64) == -4

@@ -1,0 +1,198 @@
+"""The dispatch-tick loop on the GPU against the oracle.
+
+The dispatch sequence, the tick of every request and the dispatch count are
+compared exactly. The factors are compared exactly too: both sides apply the
+EMA updates of each group one after another in dispatch order with the same
+operations (no fused multiply-add), and SJF's budgets, which decide the
+order, come from them.
+"""
+import numpy as np
+import pytest
+
+from paper_2606_02982_amd import synth
+from tests.gpu_util import dev, host
+
+pytestmark = pytest.mark.gpu
+
+FIFO, PRIORITY, WEIGHTED, SJF, AGING = 0, 1, 2, 3, 4
+ALL = [FIFO, PRIORITY, WEIGHTED, SJF, AGING]
+
+
+@pytest.fixture(scope="module")
+def ds():
+    from paper_2606_02982_amd import driftsched
+    return driftsched
+
+
+def run_gpu(ds, policy, arrival, tier, counts, category, tenant, group, observed, t_base,
+            s_tenant, state, ticks, batch=32, alpha=0.1, weights=(4, 2, 1),
+            tier_priority=(0.0, 1.0, 2.0), aging_rate=0.01, aging_floor=0.0, validate=False):
+    """(seq, n_dispatched, tick_of, state) from ds_simulate."""
+    arrival = np.asarray(arrival, np.float64)
+    print("simulate policy=%d n=%d ticks=%d batch=%d" % (policy, len(arrival), len(ticks), batch),
+          flush=True)
+    p = ds.sim_params(policy, batch=batch, alpha=alpha, n_tiers=len(weights), weights=weights,
+                      tier_priority=tier_priority, aging_rate=aging_rate, aging_floor=aging_floor)
+    st = dev(np.asarray(state, np.float64).copy())
+    seq, tick_of, nd = ds.simulate(dev(arrival), dev(np.asarray(tier, np.uint8)),
+                                   dev(np.asarray(counts, np.uint32)),
+                                   dev(np.asarray(category, np.uint8)),
+                                   dev(np.asarray(tenant, np.uint32)),
+                                   dev(np.asarray(group, np.uint32)),
+                                   dev(np.asarray(observed, np.uint32)),
+                                   dev(np.asarray(t_base, np.float64)),
+                                   dev(np.asarray(s_tenant, np.float64)), st,
+                                   dev(np.asarray(ticks, np.float64)), p, validate=validate)
+    return host(seq, np.uint32), int(host(nd)[0]), host(tick_of), host(st)
+
+
+def both(ds, oracle, policy, arrival, tier, counts, category, tenant, group, observed, t_base,
+         s_tenant, state, ticks, batch=32, alpha=0.1, weights=(4, 2, 1),
+         tier_priority=(0.0, 1.0, 2.0), aging_rate=0.01, aging_floor=0.0, validate=False):
+    w_seq, w_tick, w_state = oracle.simulate(policy, arrival, tier, counts, category, tenant,
+                                             group, observed, t_base, s_tenant, state, ticks,
+                                             batch=batch, alpha=alpha, weights=weights,
+                                             tier_priority=tier_priority, aging_rate=aging_rate,
+                                             aging_floor=aging_floor)
+    seq, nd, tick_of, got = run_gpu(ds, policy, arrival, tier, counts, category, tenant, group,
+                                    observed, t_base, s_tenant, state, ticks, batch, alpha,
+                                    weights, tier_priority, aging_rate, aging_floor, validate)
+    assert nd == len(w_seq), "dispatched %d, oracle %d" % (nd, len(w_seq))
+    if nd:
+        bad = np.flatnonzero(seq[:nd] != w_seq)
+        assert bad.size == 0, "first difference at dispatch %d: %d vs %d" % (
+            bad[0], seq[bad[0]], w_seq[bad[0]])
+    assert np.all(seq[nd:] == 0xFFFFFFFF)
+    assert np.array_equal(tick_of, w_tick)
+    assert np.array_equal(got, w_state), "factors differ: max |d| %g" % np.abs(got - w_state).max()
+    return seq[:nd], tick_of, got
+
+
+def random_inputs(seed, n, G=5, n_cat=4, n_ten=6, tiers=3, round_arrival=1):
+    rng = np.random.default_rng(seed)
+    return dict(
+        arrival=np.round(rng.uniform(0, 10, n), round_arrival),
+        tier=rng.integers(0, tiers, n).astype(np.uint8),
+        counts=rng.integers(0, 3000, n).astype(np.uint32),
+        category=rng.integers(0, n_cat, n).astype(np.uint8),
+        tenant=rng.integers(0, n_ten, n).astype(np.uint32),
+        group=rng.integers(0, G, n).astype(np.uint32),
+        observed=rng.integers(0, 4000, n).astype(np.uint32),
+        t_base=np.array([50.0, 100.0, 300.0, 800.0])[:n_cat],
+        s_tenant=np.linspace(0.5, 1.5, n_ten),
+        state=rng.uniform(0.8, 1.2, G))
+
+
+@pytest.mark.parametrize("policy", ALL)
+@pytest.mark.parametrize("n,batch", [(1, 32), (400, 1), (400, 4), (400, 32), (5000, 32),
+                                     (5000, 7), (3000, 1024)])
+def test_random(ds, oracle, policy, n, batch):
+    x = random_inputs(n + batch, n)
+    ticks = np.concatenate([[0.0, 0.0], np.linspace(0.25, 12.0, 60)])
+    both(ds, oracle, policy, ticks=ticks, batch=batch, alpha=0.2, weights=(3, 2, 1),
+         aging_rate=0.3, **x)
+
+
+@pytest.mark.parametrize("policy", ALL)
+def test_large_pending_set(ds, oracle, policy):
+    # a queue of up to 20,000 requests: the SJF/Aging select works over the
+    # whole list in global memory before its bucket fits in LDS
+    x = random_inputs(7, 20000, G=64, round_arrival=3)
+    ticks = np.repeat([2.0, 6.0, 10.0, 10.0], [3, 3, 3, 20])
+    both(ds, oracle, policy, ticks=ticks, batch=1000, alpha=0.05, aging_rate=0.05, **x)
+
+
+@pytest.mark.parametrize("policy", [SJF, AGING, PRIORITY])
+def test_all_keys_equal(ds, oracle, policy):
+    # every key equal (one budget; every aged score clamped to the floor;
+    # one tier): the order is FIFO, found by the select on list positions,
+    # with more tied candidates than fit in LDS
+    n = 12000
+    rng = np.random.default_rng(1)
+    arrival = np.round(rng.uniform(0, 1, n), 2)
+    z8, z32 = np.zeros(n, np.uint8), np.zeros(n, np.uint32)
+    tier = np.full(n, 1, np.uint8)
+    seq, _, _ = both(ds, oracle, policy, arrival, tier, z32, z8, z32, z32, z32 + 100, [64.0],
+                     [1.0], [1.0], ticks=[5.0, 5.0, 6.0], batch=1000, alpha=0.0,
+                     aging_rate=10.0, aging_floor=0.0)
+    assert np.array_equal(seq, np.lexsort((np.arange(n), arrival))[:3000])
+
+
+def test_hand_cases(ds, oracle):
+    # SJF rescored from the updated factor (see the oracle's pins)
+    z = np.zeros(4, np.uint32)
+    seq, tick_of, st = both(ds, oracle, SJF, np.zeros(4), np.zeros(4, np.uint8), z,
+                            np.zeros(4, np.uint8), z, [0, 0, 1, 1], [400, 400, 150, 150], [100.0],
+                            [1.0], [1.0, 1.5], [1.0, 2.0, 3.0], batch=1, alpha=0.5)
+    assert seq.tolist() == [0, 2, 3] and tick_of.tolist() == [0, -1, 1, 2]
+    assert st.tolist() == [2.5, 1.5]
+    # Aging to the tick's time
+    z = np.zeros(2, np.uint32)
+    for t, want in [(2.0, [1]), (9.0, [0])]:
+        seq, _, _ = both(ds, oracle, AGING, [0.0, 1.0], [2, 1], z, np.zeros(2, np.uint8), z, z,
+                         [100, 100], [100.0], [1.0], [1.0], [t], batch=1, aging_rate=0.25)
+        assert seq.tolist() == want
+    # the Weighted cycle restarts at every tick
+    z = np.zeros(6, np.uint32)
+    seq, tick_of, _ = both(ds, oracle, WEIGHTED, np.arange(6) * 0.01, [0, 0, 0, 0, 1, 1], z,
+                           np.zeros(6, np.uint8), z, z, z + 100, [100.0], [1.0], [1.0],
+                           [1.0, 2.0, 3.0], batch=2, weights=(2, 1), tier_priority=(0.0, 1.0))
+    assert seq.tolist() == [0, 1, 2, 3, 4, 5] and tick_of.tolist() == [0, 0, 1, 1, 2, 2]
+
+
+def test_sixteen_tiers_and_shared_priorities(ds, oracle):
+    x = random_inputs(3, 6000, tiers=16)
+    w = tuple(range(1, 17))
+    prio = tuple(float(q % 5) for q in range(16))       # classes shared by several tiers
+    ticks = np.linspace(0.5, 10.0, 30)
+    for pol in (PRIORITY, WEIGHTED, AGING):
+        both(ds, oracle, pol, ticks=ticks, batch=64, weights=w, tier_priority=prio,
+             aging_rate=0.2, aging_floor=-1e300, **x)
+
+
+def test_empty(ds, oracle):
+    e32, e8 = np.zeros(0, np.uint32), np.zeros(0, np.uint8)
+    both(ds, oracle, SJF, np.zeros(0), e8, e32, e8, e32, e32, e32, [1.0], [1.0], [1.0], [1.0])
+    x = random_inputs(2, 50)
+    both(ds, oracle, FIFO, ticks=np.zeros(0), **x)
+    both(ds, oracle, FIFO, ticks=[-1.0, -1.0], **x)      # before every arrival
+
+
+def test_validate(ds, oracle):
+    x = random_inputs(4, 300)
+    ticks = np.linspace(1, 10, 10)
+    both(ds, oracle, SJF, ticks=ticks, validate=True, **x)
+    cases = [("tier", 3), ("category", 4), ("tenant", 6), ("group", 5), ("arrival", np.nan)]
+    for field, bad in cases:
+        y = dict(x)
+        y[field] = x[field].copy()
+        y[field][17] = bad
+        with pytest.raises(ds.DriftSchedError) as e:
+            run_gpu(ds, SJF, ticks=ticks, validate=True, **y)
+        assert e.value.status == -5, field
+    for t in (ticks[::-1].copy(), np.array([1.0, np.nan, 3.0])):
+        with pytest.raises(ds.DriftSchedError) as e:
+            run_gpu(ds, FIFO, ticks=t, validate=True, **x)
+        assert e.value.status == -5
+
+
+def test_repeatable(ds):
+    x = random_inputs(9, 8000, G=16)
+    ticks = np.linspace(0.5, 10.0, 40)
+    a = run_gpu(ds, SJF, ticks=ticks, batch=100, **x)
+    b = run_gpu(ds, SJF, ticks=ticks, batch=100, **x)
+    for u, v in zip(a, b):
+        assert np.array_equal(u, v)
+
+
+@pytest.mark.parametrize("policy", ALL)
+def test_synthetic_workload(ds, oracle, policy):
+    # the 65,536-request workload: 10 ms ticks of 32 against 5,000
+    # arrivals/s, 2,064 ticks, every request dispatched
+    b = synth.generate("batch64k", with_text=False)
+    ticks = synth.sim_ticks(b.arrival)
+    seq, _, _ = both(ds, oracle, policy, b.arrival, b.tier, b.words, b.category, b.tenant,
+                     b.group, b.observed, b.t_base, b.s_tenant, np.ones(b.n_groups), ticks,
+                     batch=32, alpha=0.1, weights=tuple(b.weights),
+                     tier_priority=tuple(b.tier_priority), aging_rate=b.aging_rate)
+    assert len(seq) == b.n
