@@ -39,9 +39,12 @@ def parse():
     ap.add_argument("--workload", default="batch64k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
-    ap.add_argument("--stage", choices=["pipeline", "characterize", "errors"], default="pipeline",
+    ap.add_argument("--stage", choices=["pipeline", "characterize", "errors", "drift", "simulate"],
+                    default="pipeline",
                     help="characterize: time only stage 1 on --workload (any workload with text); "
-                         "errors: the estimation-error diagnostics on --workload's events")
+                         "errors: the estimation-error diagnostics on --workload's events; "
+                         "drift: calibration at each alpha and the Aging re-sorts at every tick "
+                         "(drift4m); simulate: the dispatch-tick loop on --workload, per policy")
     ap.add_argument("--settle", type=float, default=0.5,
                     help="seconds of untimed steps before the warmup steps (GPU clocks ramp "
                          "up under sustained load; the timed steps measure the steady state)")
@@ -79,6 +82,10 @@ def main():
         return bench_characterize(args, wl)
     if args.stage == "errors":
         return bench_errors(args, wl)
+    if args.stage == "drift":
+        return bench_drift(args, synth.WORKLOADS["drift4m"] if args.workload == "batch64k" else wl)
+    if args.stage == "simulate":
+        return bench_simulate(args, wl)
     if not wl.has_text or len(wl.policies) < 5:
         print("bench.py: the step needs a workload with text and all five policies", file=sys.stderr)
         sys.exit(2)
@@ -298,6 +305,153 @@ def bench_errors(args, wl):
            "error_stats_bias_on": {"ms": round(ms_on, 4), "GBs": round(bytes_on / ms_on / 1e6, 1)},
            "class_histogram": {"ms": round(ms_hist, 4), "GBs": round(bytes_hist / ms_hist / 1e6, 1)},
            "peak": HBM_PEAK_GBS}
+    print(json.dumps(res), flush=True)
+
+
+def timed_ms(fn, args):
+    """Mean milliseconds per call of fn over args.steps calls after the settle
+    and warmup calls (HIP events on torch's current stream, where the library
+    launches)."""
+    import torch
+    settle(fn, args.settle)
+    for _ in range(args.warmup):
+        fn()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    torch.cuda.synchronize()
+    ev[0].record()
+    for _ in range(args.steps):
+        fn()
+    ev[1].record()
+    torch.cuda.synchronize()
+    return ev[0].elapsed_time(ev[1]) / args.steps
+
+
+def bench_drift(args, wl):
+    """The drift workload: 4,194,304 completion events over 4,096 tenants
+    folded into the calibration factors at each alpha (events/s), and the
+    Aging order of the pending set recomputed at each of the 64 ticks (keys
+    re-sorted/s). Requests are stored in arrival order, so the pending set of
+    tick k is the first n_k requests and its FIFO order is the first n_k
+    entries of the whole set's FIFO order."""
+    import torch
+    import oracle
+    from paper_2606_02982_amd import driftsched as ds
+    from paper_2606_02982_amd import synth
+    b = synth.generate(wl)
+    E, G = len(b.ev_group), b.n_groups
+    group, est, obs = to_dev(b.ev_group), to_dev(b.ev_est), to_dev(b.ev_obs)
+    state = torch.ones(G, dtype=torch.float64, device="cuda")
+    trace = torch.empty(E, dtype=torch.float64, device="cuda")
+    ws_cal = ds.workspace(ds.OP_CALIBRATE, E, G)
+    res = {"metric": "drift workload: calibration events/s and Aging keys re-sorted/s",
+           "config": {"workload": wl.name, "events": E, "groups": G, "ticks": len(b.tick_t),
+                      "keys_over_ticks": int(b.tick_n.sum()), "alphas": list(wl.alphas)},
+           "steps": args.steps, "peak_GBs": HBM_PEAK_GBS}
+    cal_bytes = E * (4 + 8 + 4) + E * 8 + 16 * G
+    for alpha in wl.alphas:
+        def cal():
+            ds.calibrate(group, est, obs, alpha, state, trace=trace, ws=ws_cal)
+        ms = timed_ms(cal, args)
+        # parity of the final factors after one call from 1.0
+        state.fill_(1.0)
+        cal()
+        want, _ = oracle.calibrate(b.ev_group, b.ev_est, b.ev_obs, alpha, np.ones(G))
+        got = state.cpu().numpy()
+        assert np.all(np.abs(got - want) <= 1e-12 * np.abs(want)), "calibration mismatch"
+        res["calibrate_alpha_%g" % alpha] = {
+            "ms": round(ms, 4), "events_per_s": round(E / (ms * 1e-3), 1),
+            "GBs": round(cal_bytes / (ms * 1e-3) / 1e9, 1)}
+
+    tier, arrival = to_dev(b.tier), to_dev(b.arrival)
+    N = b.n
+    fifo_full, _ = ds.order(ds.FIFO, tier, arrival)
+    perm = torch.empty(N, dtype=torch.int32, device="cuda")
+    perm_fifo = torch.empty(N, dtype=torch.int32, device="cuda")
+    ws_o = ds.workspace(ds.OP_ORDER_MULTI, N)
+    kw = dict(weights=tuple(int(w) for w in b.weights), tier_priority=tuple(b.tier_priority),
+              aging_rate=b.aging_rate, aging_floor=b.aging_floor)
+    ticks = [(int(nk), ds.order_params(t_now=float(t), **kw)) for nk, t in zip(b.tick_n, b.tick_t)]
+    total = int(b.tick_n.sum())
+
+    def aging_ticks():
+        for nk, p in ticks:
+            ds.order(ds.AGING, tier[:nk], arrival[:nk], fifo=fifo_full[:nk], params=p,
+                     perm=perm[:nk], ws=ws_o)
+
+    def aging_ticks_with_fifo():
+        for nk, p in ticks:
+            ds.order_multi((ds.FIFO, ds.AGING), tier[:nk], arrival[:nk], params=p,
+                           perms={ds.FIFO: perm_fifo[:nk], ds.AGING: perm[:nk]}, ws=ws_o)
+
+    steps = max(1, args.steps // 10)
+    a2 = argparse.Namespace(**dict(vars(args), steps=steps, warmup=1))
+    ms = timed_ms(aging_ticks, a2)
+    ms_f = timed_ms(aging_ticks_with_fifo, a2)
+    # parity of the first tick's order
+    n1, p1 = ticks[0]
+    got, _ = ds.order(ds.AGING, tier[:n1], arrival[:n1], fifo=fifo_full[:n1], params=p1)
+    want, _ = oracle.order(4, b.tier[:n1], b.arrival[:n1], None, t_now=float(b.tick_t[0]), **kw)
+    assert np.array_equal(got.cpu().numpy().view(np.uint32), want), "aging order mismatch"
+    res["aging_64_ticks"] = {"ms": round(ms, 4), "keys_per_s": round(total / (ms * 1e-3), 1),
+                             "ms_with_fifo_sort": round(ms_f, 4),
+                             "keys_per_s_with_fifo_sort": round(total / (ms_f * 1e-3), 1),
+                             "GBs": round(13 * total / (ms * 1e-3) / 1e9, 1)}
+    if not args.no_cpu_baseline:
+        t0 = time.perf_counter()
+        oracle.calibrate(b.ev_group, b.ev_est, b.ev_obs, wl.alphas[0], np.ones(G))
+        cal_s = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        done = 0
+        for k, (nk, p) in enumerate(ticks):
+            oracle.order(4, b.tier[:nk], b.arrival[:nk], None, t_now=float(b.tick_t[k]), **kw)
+            done += nk
+            if time.perf_counter() - t0 > args.cpu_seconds:
+                break
+        ag_s = time.perf_counter() - t0
+        res["cpu_baseline"] = {"calibrate_events_per_s": round(E / cal_s, 1),
+                               "aging_keys_per_s": round(done / ag_s, 1), "cores": 1,
+                               "kind": "oracle",
+                               "sample": "one calibration pass over all events; Aging orders "
+                                         "of the first %d ticks (%d keys, %.1f s)" % (k + 1, done, ag_s)}
+    print(json.dumps(res), flush=True)
+
+
+def bench_simulate(args, wl):
+    """The dispatch-tick loop over one workload's requests for each policy:
+    10 ms ticks dispatching batches of 32, completions folded into the
+    factors between ticks. Reports ticks/s and requests dispatched/s."""
+    import torch
+    from paper_2606_02982_amd import driftsched as ds
+    from paper_2606_02982_amd import synth
+    b = synth.generate(wl, with_text=False)
+    ticks = synth.sim_ticks(b.arrival)
+    d = {k: to_dev(getattr(b, k)) for k in ("arrival", "tier", "words", "category", "tenant",
+                                            "group", "observed", "t_base", "s_tenant")}
+    tick_t = to_dev(ticks)
+    state = torch.ones(b.n_groups, dtype=torch.float64, device="cuda")
+    N = b.n
+    out = (torch.empty(N, dtype=torch.int32, device="cuda"),
+           torch.empty(N, dtype=torch.int32, device="cuda"),
+           torch.empty(1, dtype=torch.int32, device="cuda"))
+    ws = ds.workspace(ds.OP_SIMULATE, N)
+    res = {"metric": "dispatch-tick loop: ticks/s and requests dispatched/s",
+           "config": {"workload": wl.name, "requests": N, "ticks": len(ticks), "batch": 32,
+                      "tick_s": 0.01}, "policies": {}}
+    steps = max(1, args.steps // 10)
+    a2 = argparse.Namespace(**dict(vars(args), steps=steps, warmup=1, settle=0.0))
+    for name, pol in ds.POLICIES.items():
+        p = ds.sim_params(pol, batch=32, alpha=b.alphas[0], weights=tuple(int(w) for w in b.weights),
+                          tier_priority=tuple(b.tier_priority), aging_rate=b.aging_rate)
+
+        def run():
+            state.fill_(1.0)
+            ds.simulate(d["arrival"], d["tier"], d["words"], d["category"], d["tenant"], d["group"],
+                        d["observed"], d["t_base"], d["s_tenant"], state, tick_t, p, out=out, ws=ws)
+        ms = timed_ms(run, a2)
+        nd = int(out[2].cpu()[0])
+        res["policies"][name] = {"ms": round(ms, 3), "ticks_per_s": round(len(ticks) / (ms * 1e-3), 1),
+                                 "dispatched": nd,
+                                 "requests_per_s": round(nd / (ms * 1e-3), 1)}
     print(json.dumps(res), flush=True)
 
 

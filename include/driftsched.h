@@ -87,6 +87,9 @@ typedef enum {
 
 /* flags */
 #define DS_VALIDATE 1u      /* check device data, wait, and report DS_ERR_DATA */
+#define DS_SERIAL_SORT 2u   /* ds_order, ds_order_multi: up to 2^18 requests, run the
+                               single-workgroup sort that is otherwise the fallback of
+                               an overflowing sample-sort bucket (diagnostic; slow) */
 
 #define DS_MAX_TIERS 16
 #define DS_MAX_ITEMS (1u << 30)   /* max events for ds_calibrate, requests for ds_order */

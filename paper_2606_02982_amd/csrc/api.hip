@@ -209,6 +209,7 @@ static ds_status order_common(uint32_t mask, uint32_t n, const uint8_t *tier,
     a.aging_rate = params->aging_rate;
     a.t_now = params->t_now;
     a.aging_floor = params->aging_floor;
+    a.serial_sort = (flags & DS_SERIAL_SORT) != 0;
     for (int p = 0; p < 5; p++) {
         a.perm[p] = ((mask >> p) & 1u) ? perms[p] : nullptr;
         a.key[p] = ((mask >> p) & 1u) && keys ? keys[p] : nullptr;

@@ -54,6 +54,14 @@ size_t sort_ws_bytes(uint64_t n, uint32_t nsorts);
 hipError_t sort_launch(const SortInput &in, const SortJob *jobs, uint32_t nsorts, void *ws,
                        hipStream_t s);
 
+// Sample sort of (64-bit key, position) pairs in three launches, for Fifo,
+// Budget and Aging jobs of at most kSsMaxN keys; `serial` sorts in one
+// workgroup instead (the path taken when a bucket overflows).
+constexpr uint32_t kSsMaxN = 1u << 18;
+size_t ssort_ws_bytes(uint64_t n, uint32_t nsorts);   // 0 above kSsMaxN
+hipError_t ssort_launch(const SortInput &in, const SortJob *jobs, uint32_t nsorts, bool serial,
+                        void *ws, hipStream_t s);
+
 // ---- stage 2: calibrate -------------------------------------------------------
 size_t cal_ws_bytes(uint64_t n, uint32_t n_groups);
 hipError_t cal_launch(const uint32_t *group, const double *est, const uint32_t *obs,
@@ -84,6 +92,7 @@ struct OrderArgs {
     double aging_rate, t_now, aging_floor;
     uint32_t *perm[5];
     double *key[5];
+    bool serial_sort;          // sample-sort path: sort in one workgroup
 };
 hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_t s);
 

@@ -9,7 +9,10 @@
 //   SJF       stable radix sort of the FIFO sequence by budget
 //   Aging     stable radix sort of the FIFO sequence by the aged score
 // The FIFO sort runs first (unless the caller passes it in); the requested
-// policy sorts then run together in one batch of launches.
+// policy sorts then run together in one batch of launches. Up to kSsMaxN
+// requests the 64-bit-key sorts (FIFO, SJF, Aging) are sample sorts of three
+// launches, and the one-pass partitions (Priority, Weighted) a batch of their
+// own.
 #include <algorithm>
 
 #include "common.h"
@@ -59,7 +62,10 @@ __global__ void k_order_validate(OrderArgs a, uint32_t *__restrict__ flag)
 size_t order_ws_bytes(uint64_t n, uint32_t npolicies)
 {
     uint32_t nsorts = npolicies < 1 ? 1 : (npolicies > kMaxSorts ? kMaxSorts : npolicies);
-    return align_up(n * 4, 256) + sort_ws_bytes(n, nsorts);
+    // the FIFO sort and the policy sorts run one after another on the stream
+    // and share the sort workspace
+    const size_t radix = sort_ws_bytes(n, nsorts), sample = ssort_ws_bytes(n, nsorts);
+    return align_up(n * 4, 256) + (radix > sample ? radix : sample);
 }
 
 hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_t s)
@@ -93,10 +99,12 @@ hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_
     const bool want_fifo = a.mask & 1u;
     const uint32_t *fifo = a.fifo_in;
     hipError_t err;
+    const bool sample = n <= kSsMaxN;
     if (!fifo) {
         SortJob job = {SortKind::Fifo, 64, want_fifo ? a.key[0] : nullptr,
                        want_fifo ? a.perm[0] : fifo_ws};
-        err = sort_launch(in, &job, 1, sort_ws, s);
+        err = sample ? ssort_launch(in, &job, 1, a.serial_sort, sort_ws, s)
+                     : sort_launch(in, &job, 1, sort_ws, s);
         if (err != hipSuccess) return err;
         fifo = job.out;
     } else if (want_fifo) {
@@ -127,7 +135,21 @@ hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_
     if (a.mask & (1u << 3)) jobs[nj++] = {SortKind::Budget, 64, a.key[3], a.perm[3]};
     if (a.mask & (1u << 4)) jobs[nj++] = {SortKind::Aging, 64, a.key[4], a.perm[4]};
     if (nj == 0) return hipGetLastError();
-    return sort_launch(in, jobs, nj, sort_ws, s);
+    if (!sample) return sort_launch(in, jobs, nj, sort_ws, s);
+    SortJob part[kMaxSorts], keyed[kMaxSorts];
+    uint32_t np = 0, nk = 0;
+    for (uint32_t i = 0; i < nj; i++) {
+        if (jobs[i].kind == SortKind::Budget || jobs[i].kind == SortKind::Aging)
+            keyed[nk++] = jobs[i];
+        else
+            part[np++] = jobs[i];
+    }
+    if (np) {
+        err = sort_launch(in, part, np, sort_ws, s);
+        if (err != hipSuccess) return err;
+    }
+    if (nk) return ssort_launch(in, keyed, nk, a.serial_sort, sort_ws, s);
+    return hipGetLastError();
 }
 
 __global__ void k_fill_u32(uint32_t *__restrict__ p, uint32_t v, uint64_t n)

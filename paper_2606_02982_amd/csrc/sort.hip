@@ -28,17 +28,13 @@
 #include "common.h"
 #include "kernels.h"
 #include "keys.h"
+#include "lookback.h"
 
 namespace ds {
 namespace {
 
 constexpr int kThreads = 256;
 constexpr int kMaxPasses = 8;
-constexpr uint32_t kAgg = 1u << 30;
-constexpr uint32_t kPre = 2u << 30;
-constexpr uint32_t kValMask = (1u << 30) - 1u;
-constexpr uint32_t kSpinLimit = 1u << 22;   // bounded waits (never reached in normal runs)
-
 constexpr uint32_t kInitBlocks = 256;     // block histograms per sort (at most)
 
 struct SortCtl {
@@ -193,65 +189,6 @@ __device__ __forceinline__ uint64_t wrr_pos(const SortInput &in, const uint32_t 
     return pos;
 }
 
-// Sum of digit t's counts over the tiles before `tile` (decoupled look-back).
-// Tiles publish their own count as soon as they have ranked their keys, so
-// by the time a tile looks back its predecessors' counts are normally all
-// there: windows of 16 predecessors are loaded at once and summed back to
-// the first inclusive prefix. The wait for an unpublished tile is bounded
-// and reported through err.
-__device__ uint32_t look_back(const uint32_t *st, uint32_t tile, uint32_t t, uint32_t *err)
-{
-    constexpr int kWin = 16;
-    uint32_t prefix = 0;
-    int64_t j = (int64_t)tile - 1;   // nearest predecessor not yet summed
-    uint32_t spins = 0;
-    while (j >= 0) {
-        uint32_t x[kWin];
-#pragma unroll
-        for (int k = 0; k < kWin; k++) {
-            int64_t jj = j - k >= 0 ? j - k : 0;
-            x[k] = ld_relaxed(&st[(uint64_t)jj * 256u + t]);
-        }
-        bool done = false, stop = false;
-        int used = 0;
-#pragma unroll
-        for (int k = 0; k < kWin; k++) {
-            const bool valid = !done && !stop && j - k >= 0;
-            const uint32_t flag = x[k] & ~kValMask;
-            stop = stop || (valid && flag == 0);                 // not published yet
-            const bool take = valid && flag != 0;
-            prefix += take ? (x[k] & kValMask) : 0u;
-            used = take ? k + 1 : used;
-            done = done || (take && flag == kPre);
-        }
-        if (done) break;
-        j -= used;
-        if (used == 0) {
-            __builtin_amdgcn_s_sleep(1);
-            if (++spins > kSpinLimit) {
-                atomicOr(err, 1u);
-                break;
-            }
-        }
-    }
-    return prefix;
-}
-
-// Exclusive scan of the values of threads 0..255 over a block of TPB >= 256
-// threads (every thread calls it; the result is meaningful for t < 256).
-template <int TPB>
-__device__ uint32_t block_excl_scan_digits(uint32_t x, uint32_t *tmp)
-{
-    const uint32_t incl = wave_incl_scan_dpp(x);
-    const int w = threadIdx.x >> 6;
-    if (lane_id() == 63 && w < 4) tmp[w] = incl;
-    __syncthreads();
-    uint32_t off = 0;
-    for (int k = 0; k < w && k < 4; k++) off += tmp[k];
-    __syncthreads();
-    return off + incl - x;
-}
-
 // One digit pass over tiles of TPB * R keys (tile t = block t).
 template <int TPB, int R>
 __global__ __launch_bounds__(TPB) void k_sort_pass(SortBatch b, uint32_t p)
@@ -348,11 +285,13 @@ __global__ __launch_bounds__(TPB) void k_sort_pass(SortBatch b, uint32_t p)
     // per digit (thread t = digit): tile count, per-wave exclusive offsets
     uint32_t tc = 0;
     if (digit_thread) {
+        uint32_t c[kWaves];
+#pragma unroll
+        for (int q = 0; q < kWaves; q++) c[q] = wcnt[q][t];
 #pragma unroll
         for (int q = 0; q < kWaves; q++) {
-            uint32_t c = wcnt[q][t];
             wcnt[q][t] = tc;
-            tc += c;
+            tc += c[q];
         }
     }
     // publish this tile's count first, then scan and look back

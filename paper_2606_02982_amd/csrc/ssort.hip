@@ -1,0 +1,685 @@
+// Sample sort of (64-bit key, position) pairs for batches of up to 2^18
+// requests, where the dispatch orders are latency-bound: three launches per
+// batch of sorts instead of one launch per 8-bit digit.
+//
+// Every sort orders positions j = 0..n-1 of a sequence by (key_j, j); its
+// output is the value of each position in that order (j itself for the FIFO
+// sort, the j-th request of the FIFO sequence for SJF and Aging). Since the
+// pairs are distinct, the result is the unique stable order whatever the
+// intermediate arrangement.
+//
+//   k_ss_sample   produces S <= 2048 pairs at stratified random positions;
+//                 each of S/8 blocks stages all of them in LDS and finds the
+//                 rank of 8 of them by counting the smaller ones, and stores
+//                 each at its rank: the sorted sample, of which every
+//                 (S/B)-th pair is one of B - 1 splitters. Also clears the
+//                 look-back words and the overflow flag.
+//   k_ss_scatter  per tile of 2048 positions: produces the pairs (and the
+//                 per-request key output), finds each pair's bucket by binary
+//                 search over the splitters, ranks the tile by bucket (wave
+//                 ballots), takes the bucket prefix of earlier tiles by
+//                 decoupled look-back and writes each key with its output
+//                 value into the bucket's fixed-capacity region, so that a
+//                 bucket holds its pairs in position order.
+//   k_ss_bucket   one block per bucket: loads the bucket into registers and
+//                 LDS and runs stable LSD passes over the key bytes that vary
+//                 inside the bucket (position order breaks the remaining
+//                 ties), then writes the values at the bucket's offset (the
+//                 sizes of the buckets before it).
+// A bucket that outgrows its region (only for inputs arranged against the
+// sampling) sets the overflow flag; k_ss_bucket then sorts the whole
+// sequence in one workgroup with the same LSD passes over global memory.
+#include "common.h"
+#include "kernels.h"
+#include "keys.h"
+#include "lookback.h"
+
+namespace ds {
+namespace {
+
+constexpr uint32_t kSamples = 2048;      // pairs sampled per sort
+constexpr uint32_t kCap = 4096;          // pairs per bucket region
+constexpr uint32_t kMaxBuckets = 256;
+constexpr uint32_t kBucketAvg = 256;     // target pairs per bucket
+constexpr int kScTPB = 512, kScR = 4;    // scatter tile: 2048 positions
+constexpr uint32_t kScTile = kScTPB * kScR;
+constexpr int kBkTPB = 512, kBkR = kCap / kBkTPB;
+constexpr int kSmpTPB = 256;            // k_ss_sample: threads per block,
+constexpr uint32_t kSmpThr = 32;         // threads per sample ranked,
+constexpr uint32_t kSmpPerBlock = kSmpTPB / kSmpThr;   // samples ranked per block
+
+struct SsCtl {
+    uint32_t overflow;
+    uint32_t pad[63];
+};
+
+struct SsDesc {
+    SortKind kind;
+    double *key_out;
+    uint32_t *out;
+    SsCtl *ctl;
+    uint64_t *smp_k;       // [kSamples] the sample in sorted order
+    uint32_t *smp_j;
+    uint32_t *status;      // [tiles][256] look-back words
+    uint64_t *bkey;        // [buckets][kCap] bucket regions: keys and output values
+    uint32_t *bj;
+    uint64_t *fkey[2];     // [n] x 2: single-workgroup sort
+    uint32_t *fj[2];
+};
+
+struct SsBatch {
+    SortInput in;
+    uint32_t n;
+    uint32_t tiles;        // scatter tiles
+    uint32_t nb;           // buckets, 1..kMaxBuckets
+    uint32_t ns;           // samples, 1..kSamples
+    uint32_t serial;       // sort in one workgroup regardless of the buckets
+    SsDesc s[kMaxSorts];
+};
+
+// Value emitted for position j: the FIFO sort reorders the requests
+// themselves; SJF and Aging reorder the FIFO sequence.
+__device__ __forceinline__ uint32_t value_of(const SortInput &in, SortKind kind, uint32_t n, uint32_t j)
+{
+    if (kind == SortKind::Fifo) return j;
+    const uint32_t i = in.fifo[j < n ? j : 0];
+    return i < n ? i : 0u;
+}
+
+// Position of sample s: uniform in the s-th of S equal strata of [0, n)
+// (a fixed integer hash picks the offset), so that sampling does not lock
+// onto periodic arrangements of the input.
+// (32-bit arithmetic: s n < 2^29 for n <= 2^18 and s < 2048.)
+__device__ __forceinline__ uint32_t sample_pos(uint32_t s, uint32_t n, uint32_t S)
+{
+    const uint32_t lo = s * n / S, hi = (s + 1) * n / S;
+    uint32_t h = s * 0x9E3779B1u + 0x7F4A7C15u;
+    h ^= h >> 15;
+    h *= 0x85EBCA77u;
+    h ^= h >> 13;
+    return lo + h % (hi - lo);   // hi > lo since S <= n
+}
+
+__device__ __forceinline__ bool pair_less(uint64_t ka, uint32_t ja, uint64_t kb, uint32_t jb)
+{
+    return ka < kb || (ka == kb && ja < jb);
+}
+
+template <SortKind K>
+__device__ __forceinline__ void sample_body(const SsBatch &b, const SsDesc &d, uint64_t *sk, uint32_t *sj)
+{
+    const uint32_t t = threadIdx.x, n = b.n, S = b.ns;
+    const uint32_t stride = gridDim.x * kSmpTPB;
+    for (uint32_t i = blockIdx.x * kSmpTPB + t; i < b.tiles * 256u; i += stride) d.status[i] = 0;
+    if (blockIdx.x == 0 && t == 0) d.ctl->overflow = b.serial;
+    {
+        // all gathers in flight before the first LDS store
+        constexpr int kPer = kSamples / kSmpTPB;
+        double kv[kPer];
+        uint32_t j[kPer];
+#pragma unroll
+        for (int r = 0; r < kPer; r++) {
+            const uint32_t s = (uint32_t)r * kSmpTPB + t;
+            j[r] = s < S ? sample_pos(s, n, S) : 0u;
+            uint32_t v;
+            kv[r] = primary_key<K>(b.in, n, j[r], v);
+        }
+#pragma unroll
+        for (int r = 0; r < kPer; r++) {
+            // unused slots hold the largest pair, below no sample
+            const uint32_t s = (uint32_t)r * kSmpTPB + t;
+            sk[s] = s < S ? ordered_bits(kv[r]) : ~0ull;
+            sj[s] = s < S ? j[r] : ~0u;
+        }
+    }
+    __syncthreads();
+    // kSmpThr threads per sample: thread q of sample s counts the samples
+    // u = q, q + kSmpThr, ... below s (neighbouring lanes read neighbouring
+    // words); the partial counts are added by shuffles
+    const uint32_t s = blockIdx.x * kSmpPerBlock + t / kSmpThr, q = t % kSmpThr;
+    uint32_t below = 0;
+    {
+        const uint32_t sc = s < S ? s : 0u;
+        const uint64_t ks = sk[sc];
+        const uint32_t js = sj[sc];
+        uint32_t part[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+        for (uint32_t u0 = 0; u0 < kSamples; u0 += 8 * kSmpThr) {
+            uint64_t ku[8];
+            uint32_t ju[8];
+#pragma unroll
+            for (uint32_t e = 0; e < 8; e++) {
+                ku[e] = sk[u0 + e * kSmpThr + q];
+                ju[e] = sj[u0 + e * kSmpThr + q];
+            }
+#pragma unroll
+            for (uint32_t e = 0; e < 8; e++) part[e] += pair_less(ku[e], ju[e], ks, js) ? 1u : 0u;
+        }
+#pragma unroll
+        for (uint32_t e = 0; e < 8; e++) below += part[e];
+    }
+#pragma unroll
+    for (int m = kSmpThr / 2; m >= 1; m >>= 1) below += (uint32_t)__shfl_xor((int)below, m, 64);
+    if (s < S && q == 0) {
+        d.smp_k[below] = sk[s];
+        d.smp_j[below] = sj[s];
+    }
+}
+
+__global__ __launch_bounds__(kSmpTPB) void k_ss_sample(SsBatch b)
+{
+    __shared__ uint64_t sk[kSamples];
+    __shared__ uint32_t sj[kSamples];
+    const SsDesc &d = b.s[blockIdx.y];
+    switch (d.kind) {
+    case SortKind::Fifo: sample_body<SortKind::Fifo>(b, d, sk, sj); break;
+    case SortKind::Budget: sample_body<SortKind::Budget>(b, d, sk, sj); break;
+    default: sample_body<SortKind::Aging>(b, d, sk, sj); break;
+    }
+}
+
+// The pairs of this thread's kScR positions of the tile (loads first, then
+// the per-request key output).
+template <SortKind K>
+__device__ __forceinline__ void scatter_keys(const SsBatch &b, const SsDesc &d, uint32_t base, uint32_t cnt,
+                                             uint64_t *k, uint32_t *jj, uint32_t *vv)
+{
+    const uint32_t n = b.n;
+    const int w = (int)(threadIdx.x >> 6), lane = lane_id();
+    double kv[kScR];
+#pragma unroll
+    for (int r = 0; r < kScR; r++) {
+        const uint32_t idx = (uint32_t)w * (64u * kScR) + (uint32_t)r * 64u + (uint32_t)lane;
+        jj[r] = base + idx;
+        vv[r] = 0;
+        kv[r] = idx < cnt ? primary_key<K>(b.in, n, base + idx, vv[r]) : 0.0;
+    }
+#pragma unroll
+    for (int r = 0; r < kScR; r++) {
+        const uint32_t idx = (uint32_t)w * (64u * kScR) + (uint32_t)r * 64u + (uint32_t)lane;
+        k[r] = ordered_bits(kv[r]);
+        if (d.key_out && idx < cnt) d.key_out[K == SortKind::Fifo ? base + idx : vv[r]] = kv[r];
+    }
+}
+
+__global__ __launch_bounds__(kScTPB) void k_ss_scatter(SsBatch b)
+{
+    constexpr int kWaves = kScTPB / 64;
+    constexpr uint32_t kWaveKeys = 64u * kScR;
+    __shared__ uint64_t s_sk[kMaxBuckets];
+    __shared__ uint32_t s_sj[kMaxBuckets];
+    __shared__ uint32_t wcnt[kWaves][256];
+    __shared__ uint32_t texcl[256];
+    __shared__ uint32_t gbase[256];
+    __shared__ uint32_t tmp4[4];
+    __shared__ uint64_t lkey[kScTile];
+    __shared__ uint32_t lj[kScTile];
+    __shared__ uint8_t lb[kScTile];
+
+    const SsDesc &d = b.s[blockIdx.y];
+    const uint32_t t = threadIdx.x, n = b.n, nsp = b.nb - 1;
+    const int w = (int)(t >> 6), lane = lane_id();
+    const uint32_t tile = blockIdx.x, base = tile * kScTile;
+    const uint32_t cnt = n - base < kScTile ? n - base : kScTile;
+    const bool digit_thread = t < 256;
+
+    uint64_t k[kScR];
+    uint32_t jj[kScR], vv[kScR], bk[kScR], rk[kScR];
+    switch (d.kind) {
+    case SortKind::Fifo: scatter_keys<SortKind::Fifo>(b, d, base, cnt, k, jj, vv); break;
+    case SortKind::Budget: scatter_keys<SortKind::Budget>(b, d, base, cnt, k, jj, vv); break;
+    default: scatter_keys<SortKind::Aging>(b, d, base, cnt, k, jj, vv); break;
+    }
+    // splitter i is the sample of rank floor((i + 1) S / B)
+    for (uint32_t i = t; i < nsp; i += kScTPB) {
+        const uint32_t r = (i + 1) * b.ns / b.nb;   // < ns; (i + 1) ns < 2^19
+        s_sk[i] = d.smp_k[r];
+        s_sj[i] = d.smp_j[r];
+    }
+    for (uint32_t i = t; i < kWaves * 256u; i += kScTPB) (&wcnt[0][0])[i] = 0;
+    __syncthreads();   // splitters and counters ready
+    // bucket = number of splitters <= (key, j) (fixed-step binary search)
+    uint32_t top = 1;
+    while (top <= nsp) top <<= 1;
+    // (the rounds' searches advance together, so that their LDS reads overlap)
+#pragma unroll
+    for (int r = 0; r < kScR; r++) bk[r] = 0;
+    for (uint32_t step = top >> 1; step > 0; step >>= 1) {
+        uint64_t sk_[kScR];
+        uint32_t sj_[kScR];
+#pragma unroll
+        for (int r = 0; r < kScR; r++) {
+            const uint32_t c = bk[r] + step;   // candidate count: splitter c - 1 <= pair?
+            const uint32_t ci = c <= nsp ? c - 1 : 0u;
+            sk_[r] = s_sk[ci];
+            sj_[r] = s_sj[ci];
+        }
+#pragma unroll
+        for (int r = 0; r < kScR; r++) {
+            const uint32_t c = bk[r] + step;
+            if (c <= nsp && !pair_less(k[r], jj[r], sk_[r], sj_[r])) bk[r] = c;
+        }
+    }
+    // stable rank within the wave by bucket, round by round
+#pragma unroll
+    for (int r = 0; r < kScR; r++) {
+        const uint32_t idx = (uint32_t)w * kWaveKeys + (uint32_t)r * 64u + (uint32_t)lane;
+        const bool ok = idx < cnt;
+        const uint32_t dg = bk[r];
+        const uint64_t peers = digit_peers(dg, ok);
+        const uint32_t below = (uint32_t)__popcll(peers & lanemask_lt());
+        const uint32_t old = ok ? wcnt[w][dg] : 0u;
+        rk[r] = old + below;
+        if (ok && below == 0) wcnt[w][dg] = old + (uint32_t)__popcll(peers);
+        __builtin_amdgcn_wave_barrier();
+    }
+    __syncthreads();
+    uint32_t tc = 0;
+    if (digit_thread) {
+        uint32_t c[kWaves];
+#pragma unroll
+        for (int q = 0; q < kWaves; q++) c[q] = wcnt[q][t];
+#pragma unroll
+        for (int q = 0; q < kWaves; q++) {
+            wcnt[q][t] = tc;
+            tc += c[q];
+        }
+    }
+    uint32_t *st = d.status;
+    if (digit_thread) st_relaxed(&st[(uint64_t)tile * 256u + t], (tile == 0 ? kPre : kAgg) | tc);
+    const uint32_t tex = block_excl_scan_digits<kScTPB>(tc, tmp4);
+    if (digit_thread) {
+        texcl[t] = tex;
+        uint32_t prefix = 0;
+        if (tile > 0) {
+            prefix = look_back(st, tile, t, &d.ctl->overflow);
+            st_relaxed(&st[(uint64_t)tile * 256u + t], kPre | (prefix + tc));
+        }
+        gbase[t] = prefix;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < kScR; r++) {
+        const uint32_t idx = (uint32_t)w * kWaveKeys + (uint32_t)r * 64u + (uint32_t)lane;
+        if (idx < cnt) {
+            const uint32_t dg = bk[r];
+            const uint32_t lp = texcl[dg] + wcnt[w][dg] + rk[r];
+            lkey[lp] = k[r];
+            lj[lp] = vv[r];
+            lb[lp] = (uint8_t)dg;
+        }
+    }
+    __syncthreads();
+    bool over = false;
+    for (uint32_t s = t; s < cnt; s += kScTPB) {
+        const uint32_t dg = lb[s];
+        const uint32_t g = gbase[dg] + s - texcl[dg];
+        if (g < kCap) {
+            d.bkey[(uint64_t)dg * kCap + g] = lkey[s];
+            d.bj[(uint64_t)dg * kCap + g] = lj[s];
+        } else {
+            over = true;
+        }
+    }
+    if (over) atomicOr(&d.ctl->overflow, 1u);
+}
+
+// LDS scratch of the bucket sort (also used by the single-workgroup sort).
+struct BkShared {
+    uint32_t wcnt[2][kBkTPB / 64][256];   // per-wave digit counters, two passes' worth
+    uint32_t texcl[256];
+    uint32_t dcnt[256];
+    uint32_t offs[256];
+    uint32_t tmp4[4];
+    uint64_t red[kBkTPB / 64];
+    uint32_t redu[kBkTPB / 64];
+    uint64_t key0;
+    uint64_t lkey[kCap];
+    uint32_t lj[kCap];
+};
+
+// One stable LSD pass on byte p of the keys of m pairs held R_eff per thread
+// (wave-major positions w * 64 R_eff + r * 64 + lane): returns each pair's
+// place in the pass order through pos, leaves the digits' exclusive starts in
+// sh.texcl and, for thread t < 256, digit t's count in tc. Counters buffer
+// `cur` must be zero on entry; buffer cur ^ 1 is cleared for the next pass.
+// Ends with a barrier; the caller's reads of pos-ordered data need another.
+__device__ __forceinline__ void lds_rank(BkShared &sh, uint32_t cur, const uint64_t *k, uint32_t reff,
+                                         uint32_t m, uint32_t p, uint32_t *pos, uint32_t &tc)
+{
+    constexpr int kWaves = kBkTPB / 64;
+    const uint32_t t = threadIdx.x;
+    const int w = (int)(t >> 6), lane = lane_id();
+    const uint32_t wk = 64u * reff;
+    uint32_t (*wc)[256] = sh.wcnt[cur];
+    uint32_t rk[kBkR];
+#pragma unroll
+    for (int r = 0; r < kBkR; r++) {
+        rk[r] = 0;
+        if ((uint32_t)r < reff) {
+            const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
+            const bool ok = idx < m;
+            const uint32_t dg = (uint32_t)(k[r] >> (8 * p)) & 255u;
+            const uint64_t peers = digit_peers(dg, ok);
+            const uint32_t below = (uint32_t)__popcll(peers & lanemask_lt());
+            const uint32_t old = ok ? wc[w][dg] : 0u;
+            rk[r] = old + below;
+            if (ok && below == 0) wc[w][dg] = old + (uint32_t)__popcll(peers);
+            __builtin_amdgcn_wave_barrier();
+        }
+    }
+    for (uint32_t i = t; i < kWaves * 256u; i += kBkTPB) (&sh.wcnt[cur ^ 1u][0][0])[i] = 0;
+    __syncthreads();
+    // wave 0: digits 4 l .. 4 l + 3 per lane l: per-wave exclusive offsets,
+    // digit totals and their exclusive scan
+    if (w == 0) {
+        uint32_t c[4][kWaves], tot[4];
+#pragma unroll
+        for (int e = 0; e < 4; e++)
+#pragma unroll
+            for (int q = 0; q < kWaves; q++) c[e][q] = wc[q][4u * (uint32_t)lane + (uint32_t)e];
+#pragma unroll
+        for (int e = 0; e < 4; e++) {
+            const uint32_t dgt = 4u * (uint32_t)lane + (uint32_t)e;
+            uint32_t acc = 0;
+#pragma unroll
+            for (int q = 0; q < kWaves; q++) {
+                wc[q][dgt] = acc;
+                acc += c[e][q];
+            }
+            tot[e] = acc;
+        }
+        const uint32_t sum = tot[0] + tot[1] + tot[2] + tot[3];
+        uint32_t ex = wave_incl_scan_dpp(sum) - sum;
+#pragma unroll
+        for (int e = 0; e < 4; e++) {
+            const uint32_t dgt = 4u * (uint32_t)lane + (uint32_t)e;
+            sh.texcl[dgt] = ex;
+            sh.dcnt[dgt] = tot[e];
+            ex += tot[e];
+        }
+    }
+    __syncthreads();
+    tc = t < 256 ? sh.dcnt[t] : 0u;
+#pragma unroll
+    for (int r = 0; r < kBkR; r++) {
+        if ((uint32_t)r < reff) {
+            const uint32_t dg = (uint32_t)(k[r] >> (8 * p)) & 255u;
+            pos[r] = sh.texcl[dg] + wc[w][dg] + rk[r];
+        }
+    }
+}
+
+// The whole sequence sorted by one workgroup: LSD passes over global
+// ping-pong buffers, in chunks of kCap pairs taken in order.
+__device__ void serial_sort(const SsBatch &b, const SsDesc &d, BkShared &sh)
+{
+    const uint32_t n = b.n, t = threadIdx.x;
+    const int w = (int)(t >> 6), lane = lane_id();
+    for (uint32_t i = t; i < 2u * (kBkTPB / 64) * 256u; i += kBkTPB) (&sh.wcnt[0][0][0])[i] = 0;
+    uint32_t cur = 0;
+    for (uint32_t j = t; j < n; j += kBkTPB) {
+        uint64_t k;
+        uint32_t v;
+        produce(b.in, d.kind, nullptr, n, j, k, v);
+        d.fkey[0][j] = k;
+        d.fj[0][j] = j;
+    }
+    __syncthreads();
+    uint32_t src = 0;
+    for (uint32_t p = 0; p < 8; p++) {
+        // digit histogram; a pass whose digit is the same for all keys is skipped
+        if (t < 256) sh.offs[t] = 0;
+        __syncthreads();
+        for (uint32_t j = t; j < n; j += kBkTPB)
+            atomicAdd(&sh.offs[(uint32_t)(d.fkey[src][j] >> (8 * p)) & 255u], 1u);
+        __syncthreads();
+        const uint32_t h = t < 256 ? sh.offs[t] : 0u;
+        const int constant = __syncthreads_or(t < 256 && h == n);
+        if (constant) continue;
+        const uint32_t ex = block_excl_scan_digits<kBkTPB>(h, sh.tmp4);
+        if (t < 256) sh.offs[t] = ex;
+        __syncthreads();
+        for (uint32_t c0 = 0; c0 < n; c0 += kCap) {
+            const uint32_t m = n - c0 < kCap ? n - c0 : kCap;
+            const uint32_t reff = (m + kBkTPB - 1) / kBkTPB;
+            const uint32_t wk = 64u * reff;
+            uint64_t k[kBkR];
+            uint32_t jv[kBkR], pos[kBkR];
+#pragma unroll
+            for (int r = 0; r < kBkR; r++) {
+                const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
+                k[r] = 0;
+                jv[r] = 0;
+                if ((uint32_t)r < reff && idx < m) {
+                    k[r] = d.fkey[src][c0 + idx];
+                    jv[r] = d.fj[src][c0 + idx];
+                }
+            }
+            uint32_t tc;
+            lds_rank(sh, cur, k, reff, m, p, pos, tc);
+            cur ^= 1u;
+#pragma unroll
+            for (int r = 0; r < kBkR; r++) {
+                const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
+                if ((uint32_t)r < reff && idx < m) {
+                    const uint32_t dg = (uint32_t)(k[r] >> (8 * p)) & 255u;
+                    // rank in the chunk minus the chunk's digit start, plus
+                    // the digit's running offset
+                    const uint32_t g = sh.offs[dg] + pos[r] - sh.texcl[dg];
+                    d.fkey[src ^ 1u][g] = k[r];
+                    d.fj[src ^ 1u][g] = jv[r];
+                }
+            }
+            __syncthreads();
+            if (t < 256) sh.offs[t] += tc;
+            __syncthreads();
+        }
+        src ^= 1u;
+    }
+    for (uint32_t i = t; i < n; i += kBkTPB) d.out[i] = value_of(b.in, d.kind, n, d.fj[src][i]);
+}
+
+__global__ __launch_bounds__(kBkTPB) void k_ss_bucket(SsBatch b)
+{
+    constexpr int kWaves = kBkTPB / 64;
+    __shared__ BkShared sh;
+    const SsDesc &d = b.s[blockIdx.y];
+    const uint32_t t = threadIdx.x, bkt = blockIdx.x, n = b.n;
+    const int w = (int)(t >> 6), lane = lane_id();
+    if (ld_relaxed(&d.ctl->overflow)) {
+        if (bkt == 0) serial_sort(b, d, sh);
+        return;
+    }
+    for (uint32_t i = t; i < 2u * kWaves * 256u; i += kBkTPB) (&sh.wcnt[0][0][0])[i] = 0;
+    const uint64_t *src_k = d.bkey + (uint64_t)bkt * kCap;
+    const uint32_t *src_j = d.bj + (uint64_t)bkt * kCap;
+    // the first kBkTPB slots are loaded before the size is known (a bucket
+    // of at most kBkTPB pairs, the common case, needs no other load)
+    const uint64_t k0 = src_k[t];
+    const uint32_t j0 = src_j[t];
+    // bucket sizes: the last tile's inclusive prefixes
+    const uint32_t *last = d.status + (uint64_t)(b.tiles - 1) * 256u;
+    const uint32_t c = t < b.nb ? (last[t] & kValMask) : 0u;
+    uint32_t before = wave_sum(t < bkt ? c : 0u);
+    if (lane == 0) sh.redu[w] = before;
+    if (t == bkt) sh.offs[0] = c;
+    if (t == 0) sh.key0 = k0;   // slot 0: the reference for the varying key bytes
+    __syncthreads();
+    uint32_t off = 0;
+#pragma unroll
+    for (int q = 0; q < kWaves; q++) off += sh.redu[q];
+    const uint32_t m = sh.offs[0];   // <= kCap: no region overflowed
+    if (m <= kBkTPB) {
+        // rank by counting: the rank of slot x is the number of slots u with
+        // (key_u, u) < (key_x, x) (slot order is position order). Slots up to
+        // a multiple of 16 are padded with the largest key, below nothing.
+        const uint32_t mp = (m + 15u) & ~15u;
+        for (uint32_t i = t; i < mp; i += kBkTPB) {
+            sh.lkey[i] = i < m ? k0 : ~0ull;
+            sh.lj[i] = j0;
+        }
+        __syncthreads();
+        // two threads per slot for buckets of up to 256 pairs, else one
+        const uint32_t G = m <= kBkTPB / 2 ? 2u : 1u;
+        const uint32_t x = G == 2 ? t >> 1 : t, h = G == 2 ? (t & 1u) : 0u;
+        const uint32_t xc = x < m ? x : 0u;
+        const uint64_t kx = sh.lkey[xc];
+        uint32_t part[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+        for (uint32_t u0 = h; u0 < mp; u0 += 8u * G) {
+            uint64_t ku[8];
+#pragma unroll
+            for (uint32_t e = 0; e < 8; e++) ku[e] = sh.lkey[u0 + e * G];
+#pragma unroll
+            for (uint32_t e = 0; e < 8; e++) {
+                const uint32_t u = u0 + e * G;
+                part[e] += (ku[e] < kx || (ku[e] == kx && u < xc)) ? 1u : 0u;
+            }
+        }
+        uint32_t rank = 0;
+#pragma unroll
+        for (uint32_t e = 0; e < 8; e++) rank += part[e];
+        if (G == 2) rank += (uint32_t)__shfl_xor((int)rank, 1, 64);
+        if (x < m && h == 0 && off + rank < n) d.out[off + rank] = sh.lj[x];
+        return;
+    }
+
+    const uint32_t reff = (m + kBkTPB - 1) / kBkTPB;
+    const uint32_t wk = 64u * reff;
+
+    uint64_t k[kBkR];
+    uint32_t jv[kBkR], pos[kBkR];
+    const uint64_t key0 = sh.key0;
+    uint64_t diff = 0;
+#pragma unroll
+    for (int r = 0; r < kBkR; r++) {
+        const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
+        k[r] = 0;
+        jv[r] = 0;
+        if ((uint32_t)r < reff && idx < m) {
+            if (reff == 1) {
+                k[r] = k0;
+                jv[r] = j0;
+            } else {
+                k[r] = src_k[idx];
+                jv[r] = src_j[idx];
+            }
+            diff |= k[r] ^ key0;
+        }
+    }
+    // key bytes that vary inside the bucket
+#pragma unroll
+    for (int s = 32; s >= 1; s >>= 1) {
+        const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)diff, s, 64);
+        const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(diff >> 32), s, 64);
+        diff |= ((uint64_t)hi << 32) | lo;
+    }
+    if (lane == 0) sh.red[w] = diff;
+    __syncthreads();
+    diff = 0;
+#pragma unroll
+    for (int q = 0; q < kWaves; q++) diff |= sh.red[q];
+
+    uint32_t cur = 0;
+    for (uint32_t p = 0; p < 8; p++) {
+        if (((diff >> (8 * p)) & 255u) == 0) continue;   // uniform
+        uint32_t tc;
+        lds_rank(sh, cur, k, reff, m, p, pos, tc);
+        cur ^= 1u;
+#pragma unroll
+        for (int r = 0; r < kBkR; r++) {
+            const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
+            if ((uint32_t)r < reff && idx < m) {
+                sh.lkey[pos[r]] = k[r];
+                sh.lj[pos[r]] = jv[r];
+            }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int r = 0; r < kBkR; r++) {
+            const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
+            if ((uint32_t)r < reff && idx < m) {
+                k[r] = sh.lkey[idx];
+                jv[r] = sh.lj[idx];
+            }
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < kBkR; r++) {
+        const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
+        if ((uint32_t)r < reff && idx < m && off + idx < n) d.out[off + idx] = jv[r];
+    }
+}
+
+uint32_t n_buckets(uint64_t n)
+{
+    const uint64_t b = cdiv(n, kBucketAvg);
+    return (uint32_t)(b < 1 ? 1 : (b > kMaxBuckets ? kMaxBuckets : b));
+}
+
+uint64_t region_bytes(uint64_t n)
+{
+    const uint64_t tiles = cdiv(n, kScTile);
+    const uint64_t nb = n_buckets(n);
+    return align_up(sizeof(SsCtl), 256) + align_up(kSamples * 8, 256) + align_up(kSamples * 4, 256) +
+           align_up(tiles * 256 * 4, 256) + align_up(nb * kCap * 8, 256) + align_up(nb * kCap * 4, 256) +
+           2 * align_up(n * 8, 256) + 2 * align_up(n * 4, 256);
+}
+
+void carve(uint8_t *p, uint64_t n, SsDesc &d)
+{
+    const uint64_t tiles = cdiv(n, kScTile);
+    const uint64_t nb = n_buckets(n);
+    auto take = [&](uint64_t bytes) {
+        uint8_t *q = p;
+        p += align_up(bytes, 256);
+        return q;
+    };
+    d.ctl = reinterpret_cast<SsCtl *>(take(sizeof(SsCtl)));
+    d.smp_k = reinterpret_cast<uint64_t *>(take(kSamples * 8));
+    d.smp_j = reinterpret_cast<uint32_t *>(take(kSamples * 4));
+    d.status = reinterpret_cast<uint32_t *>(take(tiles * 256 * 4));
+    d.bkey = reinterpret_cast<uint64_t *>(take(nb * kCap * 8));
+    d.bj = reinterpret_cast<uint32_t *>(take(nb * kCap * 4));
+    for (int i = 0; i < 2; i++) d.fkey[i] = reinterpret_cast<uint64_t *>(take(n * 8));
+    for (int i = 0; i < 2; i++) d.fj[i] = reinterpret_cast<uint32_t *>(take(n * 4));
+}
+
+}  // namespace
+
+size_t ssort_ws_bytes(uint64_t n, uint32_t nsorts)
+{
+    return n <= kSsMaxN ? (size_t)nsorts * region_bytes(n) : 0;
+}
+
+hipError_t ssort_launch(const SortInput &in, const SortJob *jobs, uint32_t nsorts, bool serial,
+                        void *ws, hipStream_t s)
+{
+    if (in.n == 0 || nsorts == 0) return hipSuccess;
+    if (nsorts > kMaxSorts || in.n > kSsMaxN) return hipErrorInvalidValue;
+    SsBatch b;
+    b.in = in;
+    b.n = in.n;
+    b.tiles = (uint32_t)cdiv(in.n, kScTile);
+    b.nb = n_buckets(in.n);
+    b.ns = in.n < kSamples ? in.n : kSamples;
+    b.serial = serial ? 1u : 0u;
+    uint8_t *p = static_cast<uint8_t *>(ws);
+    for (uint32_t i = 0; i < nsorts; i++) {
+        SsDesc &d = b.s[i];
+        if (jobs[i].kind != SortKind::Fifo && jobs[i].kind != SortKind::Budget &&
+            jobs[i].kind != SortKind::Aging)
+            return hipErrorInvalidValue;
+        d.kind = jobs[i].kind;
+        d.key_out = jobs[i].key_out;
+        d.out = jobs[i].out;
+        carve(p, in.n, d);
+        p += region_bytes(in.n);
+    }
+    hipLaunchKernelGGL(k_ss_sample, dim3((uint32_t)cdiv(b.ns, kSmpPerBlock), nsorts), dim3(kSmpTPB), 0,
+                       s, b);
+    hipLaunchKernelGGL(k_ss_scatter, dim3(b.tiles, nsorts), dim3(kScTPB), 0, s, b);
+    hipLaunchKernelGGL(k_ss_bucket, dim3(b.nb, nsorts), dim3(kBkTPB), 0, s, b);
+    return hipGetLastError();
+}
+
+}  // namespace ds

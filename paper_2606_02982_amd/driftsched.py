@@ -22,6 +22,7 @@ POLICIES = {"fifo": FIFO, "priority": PRIORITY, "weighted": WEIGHTED, "sjf": SJF
 OP_CHARACTERIZE, OP_CALIBRATE, OP_SCORE, OP_ORDER, OP_ORDER_MULTI = 0, 1, 2, 3, 4
 OP_ERROR_STATS, OP_CLASS_HIST, OP_SIMULATE = 5, 6, 7
 DS_VALIDATE = 1
+DS_SERIAL_SORT = 2
 MAX_TIERS = 16
 MAX_BATCH = 1024
 
@@ -261,8 +262,11 @@ def order_params(n_tiers=3, weights=(4, 2, 1), tier_priority=(0.0, 1.0, 2.0), ag
 
 
 def order(policy, tier, arrival, budget=None, fifo=None, params=None, perm=None, key=False,
-          ws=None, validate=False, **kw):
-    """Dispatch permutation of one policy. Returns (perm, key or None)."""
+          ws=None, validate=False, serial_sort=False, **kw):
+    """Dispatch permutation of one policy. Returns (perm, key or None).
+
+    ``serial_sort`` sets DS_SERIAL_SORT (the single-workgroup sort; a
+    diagnostic)."""
     if isinstance(policy, str):
         policy = POLICIES[policy]
     _dev(tier, torch.uint8, "tier")
@@ -284,14 +288,15 @@ def order(policy, tier, arrival, budget=None, fifo=None, params=None, perm=None,
         k = _dev(key, torch.float64, "key")
     if ws is None:
         ws = workspace(OP_ORDER, n, 0, dev)
+    flags = _flags(validate) | (DS_SERIAL_SORT if serial_sort else 0)
     _check(lib.ds_order(int(policy), n, _ptr(tier), _ptr(arrival), _ptr(budget), _ptr(fifo),
                         ctypes.byref(params), _ptr(perm), _ptr(k), _ptr(ws), ws.numel(),
-                        _flags(validate), _stream()))
+                        flags, _stream()))
     return perm, k
 
 
 def order_multi(policies, tier, arrival, budget=None, fifo=None, params=None, perms=None,
-                keys=False, ws=None, validate=False, **kw):
+                keys=False, ws=None, validate=False, serial_sort=False, **kw):
     """Dispatch permutations of several policies in one call (FIFO computed
     once, the policy sorts batched). Returns ({policy: perm}, {policy: key})."""
     pols = [POLICIES[p] if isinstance(p, str) else int(p) for p in policies]
@@ -322,9 +327,10 @@ def order_multi(policies, tier, arrival, budget=None, fifo=None, params=None, pe
             kk[p] = k.data_ptr()
     if ws is None:
         ws = workspace(OP_ORDER_MULTI, n, 0, dev)
+    flags = _flags(validate) | (DS_SERIAL_SORT if serial_sort else 0)
     _check(lib.ds_order_multi(mask, n, _ptr(tier), _ptr(arrival), _ptr(budget), _ptr(fifo),
                               ctypes.byref(params), pp, kk if keys else None, _ptr(ws), ws.numel(),
-                              _flags(validate), _stream()))
+                              flags, _stream()))
     return out_p, out_k
 
 

@@ -23,6 +23,7 @@ def ds():
 
 def run(ds, pol, tier, arr, bud=None, fifo=None, **kw):
     n_tiers = kw.pop("n_tiers", 3)
+    print("order policy=%d n=%d serial=%s" % (pol, len(arr), kw.get("serial_sort", False)), flush=True)
     perm, key = ds.order(pol, dev(np.asarray(tier, np.uint8)), dev(np.asarray(arr, np.float64)),
                          None if bud is None else dev(np.asarray(bud, np.float64)),
                          fifo=fifo, key=True, n_tiers=n_tiers, **kw)
@@ -59,6 +60,33 @@ def _batch(seed, n, q=None, tiers=3):
 def test_sizes(ds, oracle, pol, n):
     tier, arr, bud = _batch(n, n)
     check(ds, oracle, pol, tier, arr, bud, t_now=10.0, aging_rate=0.1)
+
+
+@pytest.mark.parametrize("pol", POLICIES)
+@pytest.mark.parametrize("n", [262143, 262144, 262145])
+def test_sizes_at_the_sample_sort_limit(ds, oracle, pol, n):
+    # up to 2^18 requests the 64-bit-key orders are sample sorts; above, radix sorts
+    tier, arr, bud = _batch(n, n, q=1e-4)
+    check(ds, oracle, pol, tier, arr, bud, t_now=10.0, aging_rate=0.1)
+
+
+@pytest.mark.parametrize("pol", [0, 3, 4])
+@pytest.mark.parametrize("n", [1, 2, 700, 5000, 70001])
+def test_serial_sort(ds, oracle, pol, n):
+    # the single-workgroup sort that takes over when a bucket overflows
+    tier, arr, bud = _batch(n + 5, n, q=0.01)
+    check(ds, oracle, pol, tier, arr, bud, t_now=10.0, aging_rate=0.1, serial_sort=True)
+
+
+@pytest.mark.parametrize("pol", [0, 3, 4])
+def test_skewed_keys(ds, oracle, pol):
+    # 99% of the keys equal, the rest spread over many binades of both signs
+    n = 100000
+    rng = np.random.default_rng(11)
+    arr = np.where(rng.random(n) < 0.99, 5.0, rng.uniform(-1e6, 1e6, n) * 10.0 ** rng.integers(-30, 30, n))
+    bud = np.where(rng.random(n) < 0.99, 100.0, rng.standard_cauchy(n))
+    tier = rng.integers(0, 3, n).astype(np.uint8)
+    check(ds, oracle, pol, tier, arr, bud, t_now=6.0, aging_rate=0.5, aging_floor=-np.inf)
 
 
 @pytest.mark.parametrize("pol", POLICIES)
