@@ -8,7 +8,8 @@
 // pairs are distinct, the result is the unique stable order whatever the
 // intermediate arrangement.
 //
-//   k_ss_sample   produces S <= 2048 pairs at stratified random positions;
+//   k_ss_sample   produces S pairs (1024 up to 2^17 keys, else 2048) at
+//                 stratified random positions;
 //                 each of S/8 blocks stages all of them in LDS and finds the
 //                 rank of 8 of them by counting the smaller ones, and stores
 //                 each at its rank: the sorted sample, of which every
@@ -21,11 +22,12 @@
 //                 decoupled look-back and writes each key with its output
 //                 value into the bucket's fixed-capacity region, so that a
 //                 bucket holds its pairs in position order.
-//   k_ss_bucket   one block per bucket: loads the bucket into registers and
-//                 LDS and runs stable LSD passes over the key bytes that vary
-//                 inside the bucket (position order breaks the remaining
-//                 ties), then writes the values at the bucket's offset (the
-//                 sizes of the buckets before it).
+//   k_ss_bucket   one block per bucket (its offset: the sizes of the
+//                 buckets before it): bins the pairs into 2048 intervals of
+//                 the bucket's key range (an LDS histogram and its scan), and
+//                 ranks each pair inside its bin by (key, position) by
+//                 counting; a bucket with a bin of more than 64 pairs runs
+//                 stable LSD passes over its varying key bytes instead.
 // A bucket that outgrows its region (only for inputs arranged against the
 // sampling) sets the overflow flag; k_ss_bucket then sorts the whole
 // sequence in one workgroup with the same LSD passes over global memory.
@@ -37,13 +39,15 @@
 namespace ds {
 namespace {
 
-constexpr uint32_t kSamples = 2048;      // pairs sampled per sort
+constexpr uint32_t kSamples = 2048;      // pairs sampled per sort (at most)
 constexpr uint32_t kCap = 4096;          // pairs per bucket region
 constexpr uint32_t kMaxBuckets = 256;
 constexpr uint32_t kBucketAvg = 256;     // target pairs per bucket
 constexpr int kScTPB = 512, kScR = 4;    // scatter tile: 2048 positions
 constexpr uint32_t kScTile = kScTPB * kScR;
 constexpr int kBkTPB = 512, kBkR = kCap / kBkTPB;
+constexpr uint32_t kBinBits = 11, kBins = 1u << kBinBits;   // in-bucket bins
+constexpr uint32_t kBinMax = 64;         // larger bins: LSD passes instead
 constexpr int kSmpTPB = 256;            // k_ss_sample: threads per block,
 constexpr uint32_t kSmpThr = 32;         // threads per sample ranked,
 constexpr uint32_t kSmpPerBlock = kSmpTPB / kSmpThr;   // samples ranked per block
@@ -100,6 +104,20 @@ __device__ __forceinline__ uint32_t sample_pos(uint32_t s, uint32_t n, uint32_t 
     return lo + h % (hi - lo);   // hi > lo since S <= n
 }
 
+// The double whose ordered_bits is k (+0.0 for the key of both zeros).
+__device__ __forceinline__ double from_ordered(uint64_t k)
+{
+    const uint64_t u = (k >> 63) ? (k & 0x7FFFFFFFFFFFFFFFull) : ~k;
+    return __longlong_as_double((long long)u);
+}
+
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t x, int m)
+{
+    const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)x, m, 64);
+    const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(x >> 32), m, 64);
+    return ((uint64_t)hi << 32) | lo;
+}
+
 __device__ __forceinline__ bool pair_less(uint64_t ka, uint32_t ja, uint64_t kb, uint32_t jb)
 {
     return ka < kb || (ka == kb && ja < jb);
@@ -143,7 +161,8 @@ __device__ __forceinline__ void sample_body(const SsBatch &b, const SsDesc &d, u
         const uint64_t ks = sk[sc];
         const uint32_t js = sj[sc];
         uint32_t part[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-        for (uint32_t u0 = 0; u0 < kSamples; u0 += 8 * kSmpThr) {
+        const uint32_t Sp = (S + 8 * kSmpThr - 1) / (8 * kSmpThr) * (8 * kSmpThr);   // <= kSamples
+        for (uint32_t u0 = 0; u0 < Sp; u0 += 8 * kSmpThr) {
             uint64_t ku[8];
             uint32_t ju[8];
 #pragma unroll
@@ -205,7 +224,7 @@ __global__ __launch_bounds__(kScTPB) void k_ss_scatter(SsBatch b)
 {
     constexpr int kWaves = kScTPB / 64;
     constexpr uint32_t kWaveKeys = 64u * kScR;
-    __shared__ uint64_t s_sk[kMaxBuckets];
+    __shared__ uint64_t s_sk[kMaxBuckets];   // [1, 2^hgt): the search tree
     __shared__ uint32_t s_sj[kMaxBuckets];
     __shared__ uint32_t wcnt[kWaves][256];
     __shared__ uint32_t texcl[256];
@@ -229,36 +248,48 @@ __global__ __launch_bounds__(kScTPB) void k_ss_scatter(SsBatch b)
     case SortKind::Budget: scatter_keys<SortKind::Budget>(b, d, base, cnt, k, jj, vv); break;
     default: scatter_keys<SortKind::Aging>(b, d, base, cnt, k, jj, vv); break;
     }
-    // splitter i is the sample of rank floor((i + 1) S / B)
-    for (uint32_t i = t; i < nsp; i += kScTPB) {
-        const uint32_t r = (i + 1) * b.ns / b.nb;   // < ns; (i + 1) ns < 2^19
-        s_sk[i] = d.smp_k[r];
-        s_sj[i] = d.smp_j[r];
+    // splitters in breadth-first (Eytzinger) order of a complete search tree
+    // of height hgt: node e (1-based) holds the splitter of in-order index
+    // (2 p + 1) 2^(hgt - d - 1) - 1 (d = depth of e, p = e - 2^d); splitter i
+    // is the sample of rank floor((i + 1) S / B), and in-order indices from
+    // B - 1 on are padded with the largest pair. The first levels of every
+    // search then read the same few LDS words in all lanes.
+    uint32_t hgt = 0;
+    while ((1u << hgt) < b.nb) hgt++;
+    for (uint32_t e = t + 1; e < (1u << hgt); e += kScTPB) {
+        const uint32_t dpt = 31u - (uint32_t)__clz((int)e), pp = e - (1u << dpt);
+        const uint32_t i = (2u * pp + 1u) * (1u << (hgt - dpt - 1u)) - 1u;
+        uint64_t kk = ~0ull;
+        uint32_t jv = ~0u;
+        if (i < nsp) {
+            const uint32_t r = (i + 1) * b.ns / b.nb;   // < ns; (i + 1) ns < 2^19
+            kk = d.smp_k[r];
+            jv = d.smp_j[r];
+        }
+        s_sk[e] = kk;
+        s_sj[e] = jv;
     }
     for (uint32_t i = t; i < kWaves * 256u; i += kScTPB) (&wcnt[0][0])[i] = 0;
     __syncthreads();   // splitters and counters ready
-    // bucket = number of splitters <= (key, j) (fixed-step binary search)
-    uint32_t top = 1;
-    while (top <= nsp) top <<= 1;
-    // (the rounds' searches advance together, so that their LDS reads overlap)
+    // bucket = number of splitters <= (key, j): hgt steps down the tree
+    // (the rounds advance together, so that their LDS reads overlap)
+    uint32_t node[kScR];
 #pragma unroll
-    for (int r = 0; r < kScR; r++) bk[r] = 0;
-    for (uint32_t step = top >> 1; step > 0; step >>= 1) {
+    for (int r = 0; r < kScR; r++) node[r] = 1;
+    for (uint32_t lvl = 0; lvl < hgt; lvl++) {
         uint64_t sk_[kScR];
         uint32_t sj_[kScR];
 #pragma unroll
         for (int r = 0; r < kScR; r++) {
-            const uint32_t c = bk[r] + step;   // candidate count: splitter c - 1 <= pair?
-            const uint32_t ci = c <= nsp ? c - 1 : 0u;
-            sk_[r] = s_sk[ci];
-            sj_[r] = s_sj[ci];
+            sk_[r] = s_sk[node[r]];
+            sj_[r] = s_sj[node[r]];
         }
 #pragma unroll
-        for (int r = 0; r < kScR; r++) {
-            const uint32_t c = bk[r] + step;
-            if (c <= nsp && !pair_less(k[r], jj[r], sk_[r], sj_[r])) bk[r] = c;
-        }
+        for (int r = 0; r < kScR; r++)
+            node[r] = 2u * node[r] + (pair_less(k[r], jj[r], sk_[r], sj_[r]) ? 0u : 1u);
     }
+#pragma unroll
+    for (int r = 0; r < kScR; r++) bk[r] = node[r] - (1u << hgt);
     // stable rank within the wave by bucket, round by round
 #pragma unroll
     for (int r = 0; r < kScR; r++) {
@@ -332,9 +363,13 @@ struct BkShared {
     uint32_t tmp4[4];
     uint64_t red[kBkTPB / 64];
     uint32_t redu[kBkTPB / 64];
-    uint64_t key0;
+    uint32_t wsum[kBkTPB / 64];
+    uint32_t wmax[kBkTPB / 64];
+    uint64_t kmin[kBkTPB / 64], kmax[kBkTPB / 64];
+    uint32_t bin[kBins + 1];              // bin histogram, then bin starts
     uint64_t lkey[kCap];
     uint32_t lj[kCap];
+    uint16_t lslot[kCap];
 };
 
 // One stable LSD pass on byte p of the keys of m pairs held R_eff per thread
@@ -503,53 +538,17 @@ __global__ __launch_bounds__(kBkTPB) void k_ss_bucket(SsBatch b)
     uint32_t before = wave_sum(t < bkt ? c : 0u);
     if (lane == 0) sh.redu[w] = before;
     if (t == bkt) sh.offs[0] = c;
-    if (t == 0) sh.key0 = k0;   // slot 0: the reference for the varying key bytes
     __syncthreads();
     uint32_t off = 0;
 #pragma unroll
     for (int q = 0; q < kWaves; q++) off += sh.redu[q];
     const uint32_t m = sh.offs[0];   // <= kCap: no region overflowed
-    if (m <= kBkTPB) {
-        // rank by counting: the rank of slot x is the number of slots u with
-        // (key_u, u) < (key_x, x) (slot order is position order). Slots up to
-        // a multiple of 16 are padded with the largest key, below nothing.
-        const uint32_t mp = (m + 15u) & ~15u;
-        for (uint32_t i = t; i < mp; i += kBkTPB) {
-            sh.lkey[i] = i < m ? k0 : ~0ull;
-            sh.lj[i] = j0;
-        }
-        __syncthreads();
-        // two threads per slot for buckets of up to 256 pairs, else one
-        const uint32_t G = m <= kBkTPB / 2 ? 2u : 1u;
-        const uint32_t x = G == 2 ? t >> 1 : t, h = G == 2 ? (t & 1u) : 0u;
-        const uint32_t xc = x < m ? x : 0u;
-        const uint64_t kx = sh.lkey[xc];
-        uint32_t part[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-        for (uint32_t u0 = h; u0 < mp; u0 += 8u * G) {
-            uint64_t ku[8];
-#pragma unroll
-            for (uint32_t e = 0; e < 8; e++) ku[e] = sh.lkey[u0 + e * G];
-#pragma unroll
-            for (uint32_t e = 0; e < 8; e++) {
-                const uint32_t u = u0 + e * G;
-                part[e] += (ku[e] < kx || (ku[e] == kx && u < xc)) ? 1u : 0u;
-            }
-        }
-        uint32_t rank = 0;
-#pragma unroll
-        for (uint32_t e = 0; e < 8; e++) rank += part[e];
-        if (G == 2) rank += (uint32_t)__shfl_xor((int)rank, 1, 64);
-        if (x < m && h == 0 && off + rank < n) d.out[off + rank] = sh.lj[x];
-        return;
-    }
-
     const uint32_t reff = (m + kBkTPB - 1) / kBkTPB;
     const uint32_t wk = 64u * reff;
 
     uint64_t k[kBkR];
     uint32_t jv[kBkR], pos[kBkR];
-    const uint64_t key0 = sh.key0;
-    uint64_t diff = 0;
+    uint64_t kmn = ~0ull, kmx = 0;
 #pragma unroll
     for (int r = 0; r < kBkR; r++) {
         const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
@@ -563,22 +562,126 @@ __global__ __launch_bounds__(kBkTPB) void k_ss_bucket(SsBatch b)
                 k[r] = src_k[idx];
                 jv[r] = src_j[idx];
             }
-            diff |= k[r] ^ key0;
+            kmn = k[r] < kmn ? k[r] : kmn;
+            kmx = k[r] > kmx ? k[r] : kmx;
         }
     }
-    // key bytes that vary inside the bucket
+    // key range of the bucket
 #pragma unroll
-    for (int s = 32; s >= 1; s >>= 1) {
-        const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)diff, s, 64);
-        const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(diff >> 32), s, 64);
-        diff |= ((uint64_t)hi << 32) | lo;
+    for (int sft = 32; sft >= 1; sft >>= 1) {
+        const uint64_t a = shfl_xor_u64(kmn, sft), c2 = shfl_xor_u64(kmx, sft);
+        kmn = a < kmn ? a : kmn;
+        kmx = c2 > kmx ? c2 : kmx;
     }
-    if (lane == 0) sh.red[w] = diff;
+    if (lane == 0) {
+        sh.kmin[w] = kmn;
+        sh.kmax[w] = kmx;
+    }
+    for (uint32_t i = t; i <= kBins; i += kBkTPB) sh.bin[i] = 0;
     __syncthreads();
-    diff = 0;
 #pragma unroll
-    for (int q = 0; q < kWaves; q++) diff |= sh.red[q];
-
+    for (int q = 0; q < kWaves; q++) {
+        kmn = sh.kmin[q] < kmn ? sh.kmin[q] : kmn;
+        kmx = sh.kmax[q] > kmx ? sh.kmax[q] : kmx;
+    }
+    if (kmn >= kmx) {
+        // one key (or an empty bucket): position order is the order
+#pragma unroll
+        for (int r = 0; r < kBkR; r++) {
+            const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
+            if ((uint32_t)r < reff && idx < m && off + idx < n) d.out[off + idx] = jv[r];
+        }
+        return;
+    }
+    // bins, monotone in the key: for a finite range, kBins equal intervals
+    // of the key's value ((x - xmin) * (kBins / (xmax - xmin)), each step
+    // rounded and monotone); otherwise the kBinBits bits of key - kmin below
+    // its highest varying bit. rank = bin start + rank inside the bin by
+    // (key, slot), the slot being the position order.
+    const int hb = 63 - __clzll((long long)(kmn ^ kmx));
+    const uint32_t shift = hb >= (int)kBinBits ? (uint32_t)hb - (kBinBits - 1u) : 0u;
+    const double xmn = from_ordered(kmn), xmx = from_ordered(kmx);
+    const double span = xmx - xmn;
+    const bool linear = isfinite(span) && span > 0.0 && isfinite((double)kBins / span);
+    const double scale = linear ? (double)kBins / span : 0.0;
+    uint32_t dg[kBkR], bs[kBkR];
+#pragma unroll
+    for (int r = 0; r < kBkR; r++) {
+        const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
+        dg[r] = 0;
+        bs[r] = 0;
+        if ((uint32_t)r < reff && idx < m) {
+            if (linear) {
+                const double f = (from_ordered(k[r]) - xmn) * scale;   // in [0, kBins]
+                const uint32_t q = f < (double)kBins ? (uint32_t)f : kBins - 1u;
+                dg[r] = q;
+            } else {
+                dg[r] = (uint32_t)((k[r] - kmn) >> shift);   // < kBins
+            }
+            bs[r] = atomicAdd(&sh.bin[dg[r]], 1u);
+        }
+    }
+    __syncthreads();
+    // bin starts: thread t owns bins 4t .. 4t + 3
+    {
+        uint32_t hv[4], sum = 0, mx = 0;
+#pragma unroll
+        for (int e = 0; e < 4; e++) {
+            hv[e] = sh.bin[4 * t + e];
+            sum += hv[e];
+            mx = hv[e] > mx ? hv[e] : mx;
+        }
+        const uint32_t incl = wave_incl_scan_dpp(sum);
+#pragma unroll
+        for (int sft = 32; sft >= 1; sft >>= 1) {
+            const uint32_t o = (uint32_t)__shfl_xor((int)mx, sft, 64);
+            mx = o > mx ? o : mx;
+        }
+        if (lane == 63) sh.wsum[w] = incl;
+        if (lane == 0) sh.wmax[w] = mx;
+        __syncthreads();
+        uint32_t ex = incl - sum;
+        for (int q = 0; q < w; q++) ex += sh.wsum[q];
+#pragma unroll
+        for (int e = 0; e < 4; e++) {
+            sh.bin[4 * t + e] = ex;
+            ex += hv[e];
+        }
+        if (t == 0) sh.bin[kBins] = m;
+    }
+    uint32_t maxbin = 0;
+#pragma unroll
+    for (int q = 0; q < kWaves; q++) maxbin = sh.wmax[q] > maxbin ? sh.wmax[q] : maxbin;
+    __syncthreads();
+    if (maxbin <= kBinMax) {
+#pragma unroll
+        for (int r = 0; r < kBkR; r++) {
+            const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
+            if ((uint32_t)r < reff && idx < m) {
+                const uint32_t q = sh.bin[dg[r]] + bs[r];
+                sh.lkey[q] = k[r];
+                sh.lslot[q] = (uint16_t)idx;
+            }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int r = 0; r < kBkR; r++) {
+            const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
+            if ((uint32_t)r < reff && idx < m) {
+                const uint32_t s0 = sh.bin[dg[r]], s1 = sh.bin[dg[r] + 1];
+                uint32_t rank = s0;
+                for (uint32_t u = s0; u < s1; u++) {
+                    const uint64_t ku = sh.lkey[u];
+                    rank += (ku < k[r] || (ku == k[r] && sh.lslot[u] < idx)) ? 1u : 0u;
+                }
+                if (off + rank < n) d.out[off + rank] = jv[r];
+            }
+        }
+        return;
+    }
+    // crowded bins (many equal or near-equal keys): stable LSD passes over
+    // the key bytes up to the highest varying bit
+    const uint64_t diff = hb == 63 ? ~0ull : ((1ull << (hb + 1)) - 1ull);
     uint32_t cur = 0;
     for (uint32_t p = 0; p < 8; p++) {
         if (((diff >> (8 * p)) & 255u) == 0) continue;   // uniform
@@ -661,7 +764,10 @@ hipError_t ssort_launch(const SortInput &in, const SortJob *jobs, uint32_t nsort
     b.n = in.n;
     b.tiles = (uint32_t)cdiv(in.n, kScTile);
     b.nb = n_buckets(in.n);
-    b.ns = in.n < kSamples ? in.n : kSamples;
+    // 1024 samples (4 per bucket) up to 2^17 keys, 2048 above, where the
+    // average bucket is a quarter of the region capacity
+    const uint32_t smax = in.n <= (1u << 17) ? kSamples / 2 : kSamples;
+    b.ns = in.n < smax ? in.n : smax;
     b.serial = serial ? 1u : 0u;
     uint8_t *p = static_cast<uint8_t *>(ws);
     for (uint32_t i = 0; i < nsorts; i++) {
