@@ -59,8 +59,28 @@ hipError_t sort_launch(const SortInput &in, const SortJob *jobs, uint32_t nsorts
 // workgroup instead (the path taken when a bucket overflows).
 constexpr uint32_t kSsMaxN = 1u << 18;
 size_t ssort_ws_bytes(uint64_t n, uint32_t nsorts);   // 0 above kSsMaxN
+// Side work of the first launch of a sample sort, for the partitions that
+// follow in the same call: clear `clear_words` words, and write per-block
+// tier counts (ssort_sample_blocks(n) x 16) to tier_part if not NULL.
+struct SsSide {
+    uint32_t *clear;
+    uint32_t clear_words;
+    uint32_t *tier_part;
+};
+uint32_t ssort_sample_blocks(uint64_t n);
 hipError_t ssort_launch(const SortInput &in, const SortJob *jobs, uint32_t nsorts, bool serial,
-                        void *ws, hipStream_t s);
+                        void *ws, hipStream_t s, const SsSide *side = nullptr);
+
+// One-pass Priority (Class) and Weighted (Tier) orders of at most kSsMaxN
+// requests over the FIFO sequence in.fifo. status: part_ws_bytes(n) bytes of
+// zeroed words per job; tier_part: nparts x 16 tier counts of slices of the
+// batch (from the FIFO sort's first launch, or part_prepare).
+size_t part_ws_bytes(uint64_t n);          // one job's look-back words
+hipError_t part_launch(const SortInput &in, const SortJob *jobs, uint32_t njobs, uint32_t *status,
+                       uint32_t *error, const uint32_t *tier_part, uint32_t nparts, hipStream_t s);
+// The same side work without a FIFO sort: clear and tier counts.
+hipError_t part_prepare(const SortInput &in, uint32_t *clear, uint32_t clear_words,
+                        uint32_t *tier_part, uint32_t nparts, hipStream_t s);
 
 // ---- stage 2: calibrate -------------------------------------------------------
 size_t cal_ws_bytes(uint64_t n, uint32_t n_groups);

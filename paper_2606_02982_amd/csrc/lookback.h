@@ -14,12 +14,13 @@ constexpr uint32_t kPre = 2u << 30;          // the word holds the inclusive pre
 constexpr uint32_t kValMask = (1u << 30) - 1u;
 constexpr uint32_t kSpinLimit = 1u << 22;    // bounded waits (never reached in normal runs)
 
-// Sum of digit t's counts over the tiles before `tile`. Tiles publish their
-// own count as soon as they have ranked their keys, so by the time a tile
-// looks back its predecessors' counts are normally all there: windows of 16
-// predecessors are loaded at once and summed back to the first inclusive
-// prefix. The wait for an unpublished tile is bounded and reported through
-// err.
+// Sum of digit t's counts over the tiles before `tile` (tile j's words at
+// st[j * kStride + digit]). Tiles publish their own count as soon as they
+// have ranked their keys, so by the time a tile looks back its predecessors'
+// counts are normally all there: windows of 16 predecessors are loaded at
+// once and summed back to the first inclusive prefix. The wait for an
+// unpublished tile is bounded and reported through err.
+template <uint32_t kStride = 256>
 __device__ inline uint32_t look_back(const uint32_t *st, uint32_t tile, uint32_t t, uint32_t *err)
 {
     constexpr int kWin = 16;
@@ -31,7 +32,7 @@ __device__ inline uint32_t look_back(const uint32_t *st, uint32_t tile, uint32_t
 #pragma unroll
         for (int k = 0; k < kWin; k++) {
             int64_t jj = j - k >= 0 ? j - k : 0;
-            x[k] = ld_relaxed(&st[(uint64_t)jj * 256u + t]);
+            x[k] = ld_relaxed(&st[(uint64_t)jj * kStride + t]);
         }
         bool done = false, stop = false;
         int used = 0;

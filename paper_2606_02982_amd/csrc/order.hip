@@ -59,13 +59,20 @@ __global__ void k_order_validate(OrderArgs a, uint32_t *__restrict__ flag)
 
 }  // namespace
 
+// Up to kSsMaxN requests: the look-back words of the two partitions, an
+// error word, and the tier counts of the slices of the batch.
+static size_t part_region_bytes(uint64_t n)
+{
+    return n <= kSsMaxN ? 2 * part_ws_bytes(n) + 256 + align_up((uint64_t)ssort_sample_blocks(n) * 64, 256) : 0;
+}
+
 size_t order_ws_bytes(uint64_t n, uint32_t npolicies)
 {
     uint32_t nsorts = npolicies < 1 ? 1 : (npolicies > kMaxSorts ? kMaxSorts : npolicies);
     // the FIFO sort and the policy sorts run one after another on the stream
     // and share the sort workspace
     const size_t radix = sort_ws_bytes(n, nsorts), sample = ssort_ws_bytes(n, nsorts);
-    return align_up(n * 4, 256) + (radix > sample ? radix : sample);
+    return align_up(n * 4, 256) + part_region_bytes(n) + (radix > sample ? radix : sample);
 }
 
 hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_t s)
@@ -78,9 +85,11 @@ hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_
         return hipGetLastError();
     }
     if (n == 0 || a.mask == 0) return hipSuccess;
+    // workspace: FIFO permutation, partition look-back words, sort workspace
     uint8_t *p = static_cast<uint8_t *>(ws);
     uint32_t *fifo_ws = reinterpret_cast<uint32_t *>(p);
-    void *sort_ws = p + align_up((uint64_t)n * 4, 256);
+    uint8_t *part_ws = p + align_up((uint64_t)n * 4, 256);
+    void *sort_ws = part_ws + part_region_bytes(n);
 
     SortInput in = {};
     in.n = n;
@@ -100,18 +109,32 @@ hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_
     const uint32_t *fifo = a.fifo_in;
     hipError_t err;
     const bool sample = n <= kSsMaxN;
+    const bool parts = sample && (a.mask & 6u);   // Priority or Weighted by the one-pass partition
+    // partition region: look-back words of two jobs, error word, tier counts
+    uint32_t *pstatus = reinterpret_cast<uint32_t *>(part_ws);
+    uint32_t *perror = reinterpret_cast<uint32_t *>(part_ws + 2 * part_ws_bytes(n));
+    uint32_t *tier_part = reinterpret_cast<uint32_t *>(part_ws + 2 * part_ws_bytes(n) + 256);
+    const uint32_t nparts = sample ? ssort_sample_blocks(n) : 0u;
+    const uint32_t clear_words = (uint32_t)(2 * part_ws_bytes(n) / 4 + 1);
     if (!fifo) {
         SortJob job = {SortKind::Fifo, 64, want_fifo ? a.key[0] : nullptr,
                        want_fifo ? a.perm[0] : fifo_ws};
-        err = sample ? ssort_launch(in, &job, 1, a.serial_sort, sort_ws, s)
+        const SsSide side = {pstatus, clear_words, tier_part};
+        err = sample ? ssort_launch(in, &job, 1, a.serial_sort, sort_ws, s, parts ? &side : nullptr)
                      : sort_launch(in, &job, 1, sort_ws, s);
         if (err != hipSuccess) return err;
         fifo = job.out;
-    } else if (want_fifo) {
-        uint64_t nb = cdiv(n, 256);
-        uint32_t blocks = (uint32_t)(nb < 4096 ? nb : 4096);
-        hipLaunchKernelGGL(k_copy_fifo, dim3(blocks), dim3(256), 0, s, fifo, a.arrival, n,
-                           a.perm[0], a.key[0]);
+    } else {
+        if (want_fifo) {
+            uint64_t nb = cdiv(n, 256);
+            uint32_t blocks = (uint32_t)(nb < 4096 ? nb : 4096);
+            hipLaunchKernelGGL(k_copy_fifo, dim3(blocks), dim3(256), 0, s, fifo, a.arrival, n,
+                               a.perm[0], a.key[0]);
+        }
+        if (parts) {
+            err = part_prepare(in, pstatus, clear_words, tier_part, nparts, s);
+            if (err != hipSuccess) return err;
+        }
     }
     in.fifo = fifo;
 
@@ -145,7 +168,7 @@ hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_
             part[np++] = jobs[i];
     }
     if (np) {
-        err = sort_launch(in, part, np, sort_ws, s);
+        err = part_launch(in, part, np, pstatus, perror, tier_part, nparts, s);
         if (err != hipSuccess) return err;
     }
     if (nk) return ssort_launch(in, keyed, nk, a.serial_sort, sort_ws, s);

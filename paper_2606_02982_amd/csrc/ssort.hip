@@ -35,6 +35,7 @@
 #include "kernels.h"
 #include "keys.h"
 #include "lookback.h"
+#include "tiercount.h"
 
 namespace ds {
 namespace {
@@ -78,6 +79,7 @@ struct SsBatch {
     uint32_t nb;           // buckets, 1..kMaxBuckets
     uint32_t ns;           // samples, 1..kSamples
     uint32_t serial;       // sort in one workgroup regardless of the buckets
+    SsSide side;           // work of a later launch done by k_ss_sample of sort 0
     SsDesc s[kMaxSorts];
 };
 
@@ -130,6 +132,13 @@ __device__ __forceinline__ void sample_body(const SsBatch &b, const SsDesc &d, u
     const uint32_t stride = gridDim.x * kSmpTPB;
     for (uint32_t i = blockIdx.x * kSmpTPB + t; i < b.tiles * 256u; i += stride) d.status[i] = 0;
     if (blockIdx.x == 0 && t == 0) d.ctl->overflow = b.serial;
+    if (blockIdx.y == 0) {
+        for (uint32_t i = blockIdx.x * kSmpTPB + t; i < b.side.clear_words; i += stride) b.side.clear[i] = 0;
+        if (b.side.tier_part)
+            tier_partial<kSmpTPB>(b.in.tier, n, blockIdx.x, gridDim.x, b.side.tier_part,
+                                  reinterpret_cast<uint32_t *>(sk));
+        __syncthreads();   // sk is reused below
+    }
     {
         // all gathers in flight before the first LDS store
         constexpr int kPer = kSamples / kSmpTPB;
@@ -365,7 +374,7 @@ struct BkShared {
     uint32_t redu[kBkTPB / 64];
     uint32_t wsum[kBkTPB / 64];
     uint32_t wmax[kBkTPB / 64];
-    uint64_t kmin[kBkTPB / 64], kmax[kBkTPB / 64];
+    uint64_t kmin[kBkTPB / 64], kmax[kBkTPB / 64], kmin2[kBkTPB / 64];
     uint32_t bin[kBins + 1];              // bin histogram, then bin starts
     uint64_t lkey[kCap];
     uint32_t lj[kCap];
@@ -593,14 +602,75 @@ __global__ __launch_bounds__(kBkTPB) void k_ss_bucket(SsBatch b)
         }
         return;
     }
-    // bins, monotone in the key: for a finite range, kBins equal intervals
-    // of the key's value ((x - xmin) * (kBins / (xmax - xmin)), each step
-    // rounded and monotone); otherwise the kBinBits bits of key - kmin below
-    // its highest varying bit. rank = bin start + rank inside the bin by
-    // (key, slot), the slot being the position order.
-    const int hb = 63 - __clzll((long long)(kmn ^ kmx));
+    // Pairs with the bucket's smallest key (the common heavy tie: aged
+    // scores clamped to the floor) come first, in position order: their rank
+    // is the number of such pairs at lower slots, from ballots. The others
+    // go to bins, monotone in the key, over the range [x2, xmax] of the keys
+    // above the minimum: for a finite range, kBins equal intervals
+    // ((x - x2) * (kBins / (xmax - x2)), each step rounded, so monotone);
+    // otherwise the kBinBits bits of key - key2 below its highest varying
+    // bit. Their rank = pairs at the minimum + bin start + rank inside the
+    // bin by (key, slot), the slot being the position order.
+    uint32_t lowrank[kBkR], hirank[kBkR];
+    uint32_t nlow;
+    uint64_t kmn2 = ~0ull;   // smallest key above the minimum
+    {
+        uint32_t run = 0, runh = 0;
+#pragma unroll
+        for (int r = 0; r < kBkR; r++) {
+            const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
+            const bool valid = (uint32_t)r < reff && idx < m;
+            const bool low = valid && k[r] == kmn;
+            const uint64_t bl = __ballot(low), bh = __ballot(valid && !low);
+            lowrank[r] = run + (uint32_t)__popcll(bl & lanemask_lt());
+            hirank[r] = runh + (uint32_t)__popcll(bh & lanemask_lt());
+            run += (uint32_t)__popcll(bl);
+            runh += (uint32_t)__popcll(bh);
+            if (valid && !low && k[r] < kmn2) kmn2 = k[r];
+        }
+#pragma unroll
+        for (int sft = 32; sft >= 1; sft >>= 1) {
+            const uint64_t a = shfl_xor_u64(kmn2, sft);
+            kmn2 = a < kmn2 ? a : kmn2;
+        }
+        if (lane == 0) {
+            sh.wsum[w] = run;
+            sh.wmax[w] = runh;
+            sh.kmin2[w] = kmn2;
+        }
+        __syncthreads();
+        uint32_t before_w = 0, before_h = 0;
+        nlow = 0;
+#pragma unroll
+        for (int q = 0; q < kWaves; q++) {
+            before_w += q < w ? sh.wsum[q] : 0u;
+            before_h += q < w ? sh.wmax[q] : 0u;
+            nlow += sh.wsum[q];
+            kmn2 = sh.kmin2[q] < kmn2 ? sh.kmin2[q] : kmn2;
+        }
+#pragma unroll
+        for (int r = 0; r < kBkR; r++) {
+            lowrank[r] += before_w;
+            hirank[r] += before_h;
+        }
+        __syncthreads();   // sh.wsum, sh.wmax are reused by the bin scan
+    }
+    if (kmn2 >= kmx) {
+        // two distinct keys: each in position order
+#pragma unroll
+        for (int r = 0; r < kBkR; r++) {
+            const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
+            if ((uint32_t)r < reff && idx < m) {
+                const uint32_t rank = k[r] == kmn ? lowrank[r] : nlow + hirank[r];
+                if (off + rank < n) d.out[off + rank] = jv[r];
+            }
+        }
+        return;
+    }
+    // bins over [kmn2, kmx] for the pairs above the minimum
+    const int hb = 63 - __clzll((long long)(kmn2 ^ kmx));
     const uint32_t shift = hb >= (int)kBinBits ? (uint32_t)hb - (kBinBits - 1u) : 0u;
-    const double xmn = from_ordered(kmn), xmx = from_ordered(kmx);
+    const double xmn = from_ordered(kmn2), xmx = from_ordered(kmx);
     const double span = xmx - xmn;
     const bool linear = isfinite(span) && span > 0.0 && isfinite((double)kBins / span);
     const double scale = linear ? (double)kBins / span : 0.0;
@@ -610,13 +680,13 @@ __global__ __launch_bounds__(kBkTPB) void k_ss_bucket(SsBatch b)
         const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
         dg[r] = 0;
         bs[r] = 0;
-        if ((uint32_t)r < reff && idx < m) {
+        if ((uint32_t)r < reff && idx < m && k[r] != kmn) {
             if (linear) {
                 const double f = (from_ordered(k[r]) - xmn) * scale;   // in [0, kBins]
                 const uint32_t q = f < (double)kBins ? (uint32_t)f : kBins - 1u;
                 dg[r] = q;
             } else {
-                dg[r] = (uint32_t)((k[r] - kmn) >> shift);   // < kBins
+                dg[r] = (uint32_t)((k[r] - kmn2) >> shift);   // < kBins
             }
             bs[r] = atomicAdd(&sh.bin[dg[r]], 1u);
         }
@@ -647,7 +717,7 @@ __global__ __launch_bounds__(kBkTPB) void k_ss_bucket(SsBatch b)
             sh.bin[4 * t + e] = ex;
             ex += hv[e];
         }
-        if (t == 0) sh.bin[kBins] = m;
+        if (t == 0) sh.bin[kBins] = m - nlow;
     }
     uint32_t maxbin = 0;
 #pragma unroll
@@ -657,7 +727,7 @@ __global__ __launch_bounds__(kBkTPB) void k_ss_bucket(SsBatch b)
 #pragma unroll
         for (int r = 0; r < kBkR; r++) {
             const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
-            if ((uint32_t)r < reff && idx < m) {
+            if ((uint32_t)r < reff && idx < m && k[r] != kmn) {
                 const uint32_t q = sh.bin[dg[r]] + bs[r];
                 sh.lkey[q] = k[r];
                 sh.lslot[q] = (uint16_t)idx;
@@ -668,11 +738,14 @@ __global__ __launch_bounds__(kBkTPB) void k_ss_bucket(SsBatch b)
         for (int r = 0; r < kBkR; r++) {
             const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
             if ((uint32_t)r < reff && idx < m) {
-                const uint32_t s0 = sh.bin[dg[r]], s1 = sh.bin[dg[r] + 1];
-                uint32_t rank = s0;
-                for (uint32_t u = s0; u < s1; u++) {
-                    const uint64_t ku = sh.lkey[u];
-                    rank += (ku < k[r] || (ku == k[r] && sh.lslot[u] < idx)) ? 1u : 0u;
+                uint32_t rank = lowrank[r];
+                if (k[r] != kmn) {
+                    const uint32_t s0 = sh.bin[dg[r]], s1 = sh.bin[dg[r] + 1];
+                    rank = nlow + s0;
+                    for (uint32_t u = s0; u < s1; u++) {
+                        const uint64_t ku = sh.lkey[u];
+                        rank += (ku < k[r] || (ku == k[r] && sh.lslot[u] < idx)) ? 1u : 0u;
+                    }
                 }
                 if (off + rank < n) d.out[off + rank] = jv[r];
             }
@@ -680,8 +753,10 @@ __global__ __launch_bounds__(kBkTPB) void k_ss_bucket(SsBatch b)
         return;
     }
     // crowded bins (many equal or near-equal keys): stable LSD passes over
-    // the key bytes up to the highest varying bit
-    const uint64_t diff = hb == 63 ? ~0ull : ((1ull << (hb + 1)) - 1ull);
+    // all the pairs, on the key bytes up to the highest bit that varies in
+    // the bucket (minimum included)
+    const int hba = 63 - __clzll((long long)(kmn ^ kmx));
+    const uint64_t diff = hba == 63 ? ~0ull : ((1ull << (hba + 1)) - 1ull);
     uint32_t cur = 0;
     for (uint32_t p = 0; p < 8; p++) {
         if (((diff >> (8 * p)) & 255u) == 0) continue;   // uniform
@@ -754,8 +829,15 @@ size_t ssort_ws_bytes(uint64_t n, uint32_t nsorts)
     return n <= kSsMaxN ? (size_t)nsorts * region_bytes(n) : 0;
 }
 
+uint32_t ssort_sample_blocks(uint64_t n)
+{
+    const uint64_t smax = n <= (1u << 17) ? kSamples / 2 : kSamples;
+    const uint64_t ns = n < smax ? n : smax;
+    return (uint32_t)cdiv(ns ? ns : 1, kSmpPerBlock);
+}
+
 hipError_t ssort_launch(const SortInput &in, const SortJob *jobs, uint32_t nsorts, bool serial,
-                        void *ws, hipStream_t s)
+                        void *ws, hipStream_t s, const SsSide *side)
 {
     if (in.n == 0 || nsorts == 0) return hipSuccess;
     if (nsorts > kMaxSorts || in.n > kSsMaxN) return hipErrorInvalidValue;
@@ -769,6 +851,7 @@ hipError_t ssort_launch(const SortInput &in, const SortJob *jobs, uint32_t nsort
     const uint32_t smax = in.n <= (1u << 17) ? kSamples / 2 : kSamples;
     b.ns = in.n < smax ? in.n : smax;
     b.serial = serial ? 1u : 0u;
+    b.side = side ? *side : SsSide{nullptr, 0u, nullptr};
     uint8_t *p = static_cast<uint8_t *>(ws);
     for (uint32_t i = 0; i < nsorts; i++) {
         SsDesc &d = b.s[i];
@@ -781,8 +864,7 @@ hipError_t ssort_launch(const SortInput &in, const SortJob *jobs, uint32_t nsort
         carve(p, in.n, d);
         p += region_bytes(in.n);
     }
-    hipLaunchKernelGGL(k_ss_sample, dim3((uint32_t)cdiv(b.ns, kSmpPerBlock), nsorts), dim3(kSmpTPB), 0,
-                       s, b);
+    hipLaunchKernelGGL(k_ss_sample, dim3(ssort_sample_blocks(in.n), nsorts), dim3(kSmpTPB), 0, s, b);
     hipLaunchKernelGGL(k_ss_scatter, dim3(b.tiles, nsorts), dim3(kScTPB), 0, s, b);
     hipLaunchKernelGGL(k_ss_bucket, dim3(b.nb, nsorts), dim3(kBkTPB), 0, s, b);
     return hipGetLastError();
