@@ -1,0 +1,465 @@
+// Stage 2 for up to kCalGroupsLds groups: Eq. (5) with the ratio of Eq. (6)
+// (Sec. "Runtime Calibration and Feedback Adaptation") without a global
+// partition of the events by group, so that every access is coalesced.
+//
+// The events, in completion order, are cut into C chunks of L events (L a
+// multiple of 2048). With M(c, g) the composition of the affine maps
+// x -> (1 - alpha) x + alpha r of group g's events in chunk c (in order):
+//   k_calc_agg    per chunk (one block): each 2048-event sub-tile is sorted
+//                 by group in LDS (stable LSD passes, wave ballots), scanned
+//                 as a segmented scan of maps, and each group's part is
+//                 composed into that group's map in LDS; the chunk writes
+//                 M(c, g) for every group (or "no usable event").
+//   k_calc_scan   per group (one wave): the group's factor before chunk c is
+//                 M(c-1, g) o ... o M(0, g) applied to its initial factor
+//                 (the maps composed per lane, then a wave scan); writes those
+//                 carries and the final factor.
+//   k_calc_apply  per chunk: the same sub-tile sort and scan; every event
+//                 then runs the exact update t1 = (1 - alpha) c, t2 =
+//                 alpha r, c = t1 + t2 from its carried factor, in order, and
+//                 the traces are staged in LDS and written in event order.
+// Results match the sequential recurrence up to the rounding of the
+// composed maps (a few ulps; the contract is 1e-12 relative).
+#include "common.h"
+#include "kernels.h"
+
+namespace ds {
+namespace {
+
+constexpr int kT = 512;                  // threads per block
+constexpr int kE = 4;                    // events per thread per sub-tile
+constexpr uint32_t kSub = kT * kE;       // events per sub-tile
+constexpr int kW = kT / 64;
+constexpr uint32_t kG = kCalGroupsLds;   // groups held in LDS
+constexpr uint32_t kMaxTable = 1u << 20; // C x G entries at most (C >= 1)
+constexpr uint32_t kMaxChunks = 512;
+
+struct CalArgs {
+    const uint32_t *group;
+    const double *est;
+    const uint32_t *obs;
+    uint32_t E, G;
+    double alpha, oma;       // alpha and 1 - alpha
+    uint32_t C;              // chunks
+    uint32_t L;              // events per chunk
+    uint32_t passes;         // 8-bit LSD passes over the group key (key < 2^(8 passes))
+    double *aggA, *aggB;     // [C][G]: M(c, g) = x -> A x + B; A < 0: no usable event
+    double *carry;           // [C][G]: factor of g before chunk c
+    double *state;           // [G] in: before all events, out: after
+    double *trace, *trace_before;
+};
+
+// A composed affine map: x -> a x + b, f = a segment starts inside,
+// u = some usable event inside.
+struct Map {
+    uint32_t f, u;
+    double a, b;
+};
+
+// x then y
+__device__ __forceinline__ Map combine(const Map &x, const Map &y)
+{
+    if (y.f) return y;
+    Map r;
+    r.f = x.f;
+    r.u = x.u | y.u;
+    r.a = y.a * x.a;
+    const double t = y.a * x.b;
+    r.b = t + y.b;
+    return r;
+}
+
+__device__ __forceinline__ double shfl_up_d(double x, int d)
+{
+    const long long v = __double_as_longlong(x);
+    const int lo = __shfl_up((int)(uint32_t)v, d, 64), hi = __shfl_up((int)(uint32_t)(v >> 32), d, 64);
+    return __longlong_as_double((long long)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo));
+}
+
+__device__ __forceinline__ Map shfl_up_map(const Map &m, int d)
+{
+    Map r;
+    r.f = (uint32_t)__shfl_up((int)m.f, d, 64);
+    r.u = (uint32_t)__shfl_up((int)m.u, d, 64);
+    r.a = shfl_up_d(m.a, d);
+    r.b = shfl_up_d(m.b, d);
+    return r;
+}
+
+// Inclusive scan of one map per lane over the wave (fixed order).
+__device__ __forceinline__ Map wave_scan(Map v)
+{
+    const int lane = lane_id();
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const Map o = shfl_up_map(v, d);
+        if (lane >= d) v = combine(o, v);
+    }
+    return v;
+}
+
+struct SubShared {
+    uint32_t wcnt[kW][256];
+    uint32_t texcl[256];
+    Map wagg[kW];
+    uint16_t key[kSub];      // group (G for an event outside the groups)
+    uint16_t slot[kSub];     // position in the sub-tile
+    double b[kSub];          // alpha * r, or 0; reused for trace staging once read
+    uint8_t ok[kSub];        // usable
+};
+
+// The sub-tile starting at event s0 (m <= kSub events, m > 0), sorted by
+// group and scanned. On return (after a barrier that follows every thread's
+// reads of sh.b, sh.slot and sh.ok), thread t holds sorted positions 4t ..
+// 4t+3: key, slot, b, usable and the segment-start flags; and, when its first
+// position continues a segment that starts at p < 4t, `excl`, the
+// composition of the maps of positions p .. 4t-1. sh.key keeps the sorted
+// keys.
+struct Sub {
+    uint32_t key[kE], slot[kE], ok[kE], flag[kE];
+    double b[kE];
+    Map excl;
+};
+
+__device__ void load_sort_scan(const CalArgs &a, uint32_t s0, uint32_t m, SubShared &sh, Sub &out)
+{
+    const uint32_t t = threadIdx.x;
+    const int w = (int)(t >> 6), lane = lane_id();
+    // wave-major slots: wave w holds slots [64 kE w, 64 kE (w + 1)), round r
+    // the 64 slots from 64 kE w + 64 r; every load is coalesced
+    uint32_t key[kE], slot[kE], ok[kE];
+    double b[kE];
+#pragma unroll
+    for (int r = 0; r < kE; r++) {
+        const uint32_t sl = (uint32_t)w * (64u * kE) + (uint32_t)r * 64u + (uint32_t)lane;
+        slot[r] = sl;
+        key[r] = 0;
+        ok[r] = 0;
+        b[r] = 0.0;
+        if (sl < m) {
+            const uint32_t e = s0 + sl;
+            const uint32_t g = a.group[e];
+            const double x = a.est[e];
+            const uint32_t o = a.obs[e];
+            key[r] = g < a.G ? g : a.G;
+            if (g < a.G && isfinite(x) && x > 0.0) {
+                const double ratio = (double)o / x;
+                b[r] = a.alpha * ratio;
+                ok[r] = 1;
+            }
+        }
+    }
+    // stable LSD passes over the key (8 bits each); positions in LDS
+    for (uint32_t p = 0; p < a.passes; p++) {
+        for (uint32_t i = t; i < kW * 256u; i += kT) (&sh.wcnt[0][0])[i] = 0;
+        __syncthreads();
+        uint32_t rk[kE];
+#pragma unroll
+        for (int r = 0; r < kE; r++) {
+            const uint32_t sl = (uint32_t)w * (64u * kE) + (uint32_t)r * 64u + (uint32_t)lane;
+            const bool v = sl < m;
+            const uint32_t dg = (key[r] >> (8 * p)) & 255u;
+            uint64_t peers = __ballot(v);
+#pragma unroll
+            for (int bb = 0; bb < 8; bb++) {
+                const bool bit = (dg >> bb) & 1u;
+                const uint64_t mk = __ballot(bit);
+                peers &= bit ? mk : ~mk;
+            }
+            const uint32_t below = (uint32_t)__popcll(peers & lanemask_lt());
+            const uint32_t old = v ? sh.wcnt[w][dg] : 0u;
+            rk[r] = old + below;
+            if (v && below == 0) sh.wcnt[w][dg] = old + (uint32_t)__popcll(peers);
+            __builtin_amdgcn_wave_barrier();
+        }
+        __syncthreads();
+        if (w == 0) {
+            // digits 4 l .. 4 l + 3: per-wave exclusive offsets and digit starts
+            uint32_t c[4][kW], tot[4];
+#pragma unroll
+            for (int e = 0; e < 4; e++)
+#pragma unroll
+                for (int q = 0; q < kW; q++) c[e][q] = sh.wcnt[q][4 * lane + e];
+#pragma unroll
+            for (int e = 0; e < 4; e++) {
+                uint32_t acc = 0;
+#pragma unroll
+                for (int q = 0; q < kW; q++) {
+                    sh.wcnt[q][4 * lane + e] = acc;
+                    acc += c[e][q];
+                }
+                tot[e] = acc;
+            }
+            const uint32_t sum = tot[0] + tot[1] + tot[2] + tot[3];
+            uint32_t ex = wave_incl_scan_dpp(sum) - sum;
+#pragma unroll
+            for (int e = 0; e < 4; e++) {
+                sh.texcl[4 * lane + e] = ex;
+                ex += tot[e];
+            }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int r = 0; r < kE; r++) {
+            const uint32_t sl = (uint32_t)w * (64u * kE) + (uint32_t)r * 64u + (uint32_t)lane;
+            if (sl < m) {
+                const uint32_t dg = (key[r] >> (8 * p)) & 255u;
+                const uint32_t q = sh.texcl[dg] + sh.wcnt[w][dg] + rk[r];
+                sh.key[q] = (uint16_t)key[r];
+                sh.slot[q] = (uint16_t)slot[r];
+                sh.b[q] = b[r];
+                sh.ok[q] = (uint8_t)ok[r];
+            }
+        }
+        __syncthreads();
+        if (p + 1 < a.passes) {
+#pragma unroll
+            for (int r = 0; r < kE; r++) {
+                const uint32_t sl = (uint32_t)w * (64u * kE) + (uint32_t)r * 64u + (uint32_t)lane;
+                if (sl < m) {
+                    key[r] = sh.key[sl];
+                    slot[r] = sh.slot[sl];
+                    b[r] = sh.b[sl];
+                    ok[r] = sh.ok[sl];
+                }
+            }
+            __syncthreads();
+        }
+    }
+    // thread t takes sorted positions kE t .. kE t + kE - 1
+    Map agg = {0u, 0u, 1.0, 0.0};
+#pragma unroll
+    for (int e = 0; e < kE; e++) {
+        const uint32_t i = t * kE + (uint32_t)e;
+        out.key[e] = kG;   // past the end: no group
+        out.slot[e] = 0;
+        out.ok[e] = 0;
+        out.flag[e] = 0;
+        out.b[e] = 0.0;
+        if (i < m) {
+            out.key[e] = sh.key[i];
+            out.slot[e] = sh.slot[i];
+            out.ok[e] = sh.ok[i];
+            out.b[e] = sh.b[i];
+            out.flag[e] = (i == 0 || sh.key[i - 1] != sh.key[i]) ? 1u : 0u;
+            Map mp;
+            mp.f = out.flag[e];
+            mp.u = out.ok[e];
+            mp.a = out.ok[e] ? a.oma : 1.0;
+            mp.b = out.ok[e] ? out.b[e] : 0.0;
+            agg = (e == 0) ? mp : combine(agg, mp);
+        }
+    }
+    // exclusive scan of the threads' maps: wave scan, then the waves before
+    const Map incl = wave_scan(agg);
+    if (lane == 63) sh.wagg[w] = incl;
+    __syncthreads();
+    Map before = {1u, 0u, 1.0, 0.0};   // nothing before
+    for (int q = 0; q < w; q++) before = (q == 0) ? sh.wagg[0] : combine(before, sh.wagg[q]);
+    Map ex = shfl_up_map(incl, 1);
+    if (lane == 0) ex = before;
+    else if (w > 0) ex = combine(before, ex);
+    if (t == 0) ex = Map{1u, 0u, 1.0, 0.0};
+    out.excl = ex;
+}
+
+__global__ __launch_bounds__(kT) void k_calc_agg(CalArgs a)
+{
+    __shared__ SubShared sh;
+    __shared__ double sA[kG], sB[kG];   // the chunk's map per group so far (A < 0: none)
+    const uint32_t t = threadIdx.x, c = blockIdx.x;
+    for (uint32_t g = t; g < a.G; g += kT) {
+        sA[g] = -1.0;
+        sB[g] = 0.0;
+    }
+    const uint64_t c0 = (uint64_t)c * a.L;
+    const uint64_t c1 = c0 + a.L < a.E ? c0 + a.L : a.E;
+    for (uint64_t s0 = c0; s0 < c1; s0 += kSub) {
+        const uint32_t m = (uint32_t)(c1 - s0 < kSub ? c1 - s0 : kSub);
+        Sub sub;
+        load_sort_scan(a, (uint32_t)s0, m, sh, sub);   // (its first barrier orders the sA/sB writes)
+        // the segment of each group in this sub-tile, composed into the
+        // group's map at the segment's last position (one thread per group)
+        Map run = sub.excl;
+#pragma unroll
+        for (int e = 0; e < kE; e++) {
+            const uint32_t i = t * kE + (uint32_t)e;
+            if (i >= m) break;
+            Map mp;
+            mp.f = sub.flag[e];
+            mp.u = sub.ok[e];
+            mp.a = sub.ok[e] ? a.oma : 1.0;
+            mp.b = sub.ok[e] ? sub.b[e] : 0.0;
+            run = mp.f ? mp : combine(run, mp);
+            const bool last = (i + 1 == m) || (e + 1 < kE ? sub.flag[e + 1] != 0u : sh.key[i + 1] != sh.key[i]);
+            const uint32_t g = sub.key[e];
+            if (last && g < a.G && run.u) {
+                const double pa = sA[g];
+                if (pa < 0.0) {
+                    sA[g] = run.a;
+                    sB[g] = run.b;
+                } else {
+                    // the chunk so far, then this segment
+                    sA[g] = run.a * pa;
+                    const double tt = run.a * sB[g];
+                    sB[g] = tt + run.b;
+                }
+            }
+        }
+        __syncthreads();
+    }
+    for (uint32_t g = t; g < a.G; g += kT) {
+        a.aggA[(uint64_t)c * a.G + g] = sA[g];
+        a.aggB[(uint64_t)c * a.G + g] = sB[g];
+    }
+}
+
+// One wave per group: carries before every chunk, and the final factor.
+__global__ __launch_bounds__(256) void k_calc_scan(CalArgs a)
+{
+    const uint32_t g = blockIdx.x * 4u + (threadIdx.x >> 6);
+    const int lane = lane_id();
+    if (g >= a.G) return;
+    const uint32_t per = (a.C + 63u) / 64u;
+    const uint32_t cb = (uint32_t)lane * per, ce = cb + per < a.C ? cb + per : a.C;
+    Map agg = {0u, 0u, 1.0, 0.0};
+    for (uint32_t c = cb; c < ce; c++) {
+        const double A = a.aggA[(uint64_t)c * a.G + g], B = a.aggB[(uint64_t)c * a.G + g];
+        if (A >= 0.0) agg = combine(agg, Map{0u, 1u, A, B});
+    }
+    const Map incl = wave_scan(agg);
+    Map ex = shfl_up_map(incl, 1);
+    if (lane == 0) ex = Map{0u, 0u, 1.0, 0.0};
+    const double v0 = a.state[g];
+    double v = v0;
+    if (ex.u) {
+        const double tt = ex.a * v0;
+        v = tt + ex.b;
+    }
+    for (uint32_t c = cb; c < ce; c++) {
+        a.carry[(uint64_t)c * a.G + g] = v;
+        const double A = a.aggA[(uint64_t)c * a.G + g], B = a.aggB[(uint64_t)c * a.G + g];
+        if (A >= 0.0) {
+            const double tt = A * v;
+            v = tt + B;
+        }
+    }
+    // the lane holding the last chunk writes the factor after all events
+    // (a group without usable events keeps its factor untouched)
+    const bool touched = __ballot(incl.u != 0u) != 0ull;
+    if (ce == a.C && cb < ce && touched) a.state[g] = v;
+}
+
+__global__ __launch_bounds__(kT) void k_calc_apply(CalArgs a)
+{
+    __shared__ SubShared sh;
+    __shared__ double trb[kSub];   // trace_before staging (the trace goes to sh.b)
+    __shared__ double sv[kG];      // each group's factor at the current point of the chunk
+    const uint32_t t = threadIdx.x, c = blockIdx.x;
+    for (uint32_t g = t; g < a.G; g += kT) sv[g] = a.carry[(uint64_t)c * a.G + g];
+    const uint64_t c0 = (uint64_t)c * a.L;
+    const uint64_t c1 = c0 + a.L < a.E ? c0 + a.L : a.E;
+    const double nan = __builtin_nan("");
+    double *tr = sh.b;
+    for (uint64_t s0 = c0; s0 < c1; s0 += kSub) {
+        const uint32_t m = (uint32_t)(c1 - s0 < kSub ? c1 - s0 : kSub);
+        Sub sub;
+        load_sort_scan(a, (uint32_t)s0, m, sh, sub);
+        // the factor before this thread's first position: the group's factor
+        // at the sub-tile start, through the earlier positions of its
+        // segment (their composed map, if any of them is usable)
+        double cv;
+        {
+            const uint32_t g0 = sub.key[0];
+            const double base = g0 < a.G ? sv[g0] : nan;
+            cv = base;
+            if (!sub.flag[0] && sub.excl.u) {
+                const double tt = sub.excl.a * base;
+                cv = tt + sub.excl.b;
+            }
+        }
+        double after[kE];
+#pragma unroll
+        for (int e = 0; e < kE; e++) {
+            const uint32_t i = t * kE + (uint32_t)e;
+            after[e] = cv;
+            if (i >= m) continue;
+            const uint32_t g = sub.key[e];
+            if (sub.flag[e]) cv = g < a.G ? sv[g] : nan;
+            trb[sub.slot[e]] = cv;
+            if (sub.ok[e]) {
+                // the exact sequential update
+                const double t1 = a.oma * cv;
+                cv = t1 + sub.b[e];
+            }
+            tr[sub.slot[e]] = cv;
+            after[e] = cv;
+        }
+        __syncthreads();   // every read of sv above precedes the updates below
+#pragma unroll
+        for (int e = 0; e < kE; e++) {
+            const uint32_t i = t * kE + (uint32_t)e;
+            if (i >= m) break;
+            const bool last = (i + 1 == m) || (e + 1 < kE ? sub.flag[e + 1] != 0u : sh.key[i + 1] != sh.key[i]);
+            const uint32_t g = sub.key[e];
+            if (last && g < a.G) sv[g] = after[e];
+        }
+        // the traces in event order
+        for (uint32_t i = t; i < m; i += kT) {
+            if (a.trace) a.trace[s0 + i] = tr[i];
+            if (a.trace_before) a.trace_before[s0 + i] = trb[i];
+        }
+        __syncthreads();
+    }
+}
+
+uint32_t sub_per_chunk(uint64_t E, uint32_t G)
+{
+    uint64_t cmax = kMaxTable / (G ? G : 1);
+    cmax = cmax < kMaxChunks ? cmax : kMaxChunks;
+    cmax = cmax ? cmax : 1;
+    const uint64_t subs = cdiv(E, kSub);
+    return (uint32_t)(cdiv(subs, cmax) ? cdiv(subs, cmax) : 1);
+}
+
+}  // namespace
+
+size_t calc_ws_bytes(uint64_t n, uint32_t G)
+{
+    const uint64_t L = (uint64_t)kSub * sub_per_chunk(n, G);
+    const uint64_t C = cdiv(n ? n : 1, L);
+    return 3 * align_up(C * G * 8, 256);
+}
+
+hipError_t calc_launch(const uint32_t *group, const double *est, const uint32_t *obs, uint32_t n,
+                       double alpha, uint32_t G, double *state, double *trace, double *trace_before,
+                       void *ws, hipStream_t s)
+{
+    if (n == 0) return hipSuccess;
+    if (G == 0 || G > kG) return hipErrorInvalidValue;
+    CalArgs a;
+    a.group = group;
+    a.est = est;
+    a.obs = obs;
+    a.E = n;
+    a.G = G;
+    a.alpha = alpha;
+    a.oma = 1.0 - alpha;
+    a.L = kSub * sub_per_chunk(n, G);
+    a.C = (uint32_t)cdiv(n, a.L);
+    a.passes = G < 256 ? 1u : 2u;   // keys 0..G fit in 8 or 16 bits
+    uint8_t *p = static_cast<uint8_t *>(ws);
+    const uint64_t tb = align_up((uint64_t)a.C * G * 8, 256);
+    a.aggA = reinterpret_cast<double *>(p);
+    a.aggB = reinterpret_cast<double *>(p + tb);
+    a.carry = reinterpret_cast<double *>(p + 2 * tb);
+    a.state = state;
+    a.trace = trace;
+    a.trace_before = trace_before;
+    hipLaunchKernelGGL(k_calc_agg, dim3(a.C), dim3(kT), 0, s, a);
+    hipLaunchKernelGGL(k_calc_scan, dim3((G + 3) / 4), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(k_calc_apply, dim3(a.C), dim3(kT), 0, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace ds

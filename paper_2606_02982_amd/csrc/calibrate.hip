@@ -1,5 +1,6 @@
 // Stage 2: EMA calibration factors, Eq. (5) with the ratio of Eq. (6), over
-// completion events in completion order, per calibration group.
+// completion events in completion order, per calibration group. This file
+// serves more than kCalGroupsLds groups; up to that, calchunk.hip.
 //
 // The recurrence c <- (1 - alpha) c + alpha r is, per group, a composition
 // of affine maps x -> a x + b (a = 1 - alpha, b = alpha * obs / est; the
@@ -262,6 +263,7 @@ uint32_t bits_for(uint32_t G)
 
 size_t cal_ws_bytes(uint64_t n, uint32_t n_groups)
 {
+    if (n_groups <= kCalGroupsLds) return calc_ws_bytes(n, n_groups);
     uint64_t T = cdiv(n, kTile);
     return sort_ws_bytes(n, 1) + align_up(n * 4, 256) +
            align_up((uint64_t)n_groups * 8, 256) + 2 * align_up(T * sizeof(Map), 256);
@@ -277,6 +279,7 @@ hipError_t cal_launch(const uint32_t *group, const double *est, const uint32_t *
         return hipGetLastError();
     }
     if (n == 0) return hipSuccess;
+    if (G <= kCalGroupsLds) return calc_launch(group, est, obs, n, alpha, G, state, trace, trace_before, ws, s);
     const uint32_t T = (uint32_t)cdiv(n, kTile);
     const uint32_t kb = bits_for(G);
     uint8_t *p = static_cast<uint8_t *>(ws);

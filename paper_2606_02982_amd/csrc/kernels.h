@@ -83,6 +83,12 @@ hipError_t part_prepare(const SortInput &in, uint32_t *clear, uint32_t clear_wor
                         uint32_t *tier_part, uint32_t nparts, hipStream_t s);
 
 // ---- stage 2: calibrate -------------------------------------------------------
+// Up to kCalGroupsLds groups: chunked scan without a global partition.
+constexpr uint32_t kCalGroupsLds = 4096;
+size_t calc_ws_bytes(uint64_t n, uint32_t n_groups);
+hipError_t calc_launch(const uint32_t *group, const double *est, const uint32_t *obs, uint32_t n,
+                       double alpha, uint32_t n_groups, double *state, double *trace,
+                       double *trace_before, void *ws, hipStream_t s);
 size_t cal_ws_bytes(uint64_t n, uint32_t n_groups);
 hipError_t cal_launch(const uint32_t *group, const double *est, const uint32_t *obs,
                       uint32_t n, double alpha, uint32_t n_groups, double *state,

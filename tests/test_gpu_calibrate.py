@@ -58,7 +58,11 @@ def test_drift_events(ds, oracle, alpha):
 
 
 @pytest.mark.parametrize("E,G", [(1, 1), (5, 3), (4095, 1), (4097, 2), (100000, 1),
-                                 (70000, 70000), (30000, 65536), (9000, 300)])
+                                 (70000, 70000), (30000, 65536), (9000, 300),
+                                 # one or two LDS sort passes, chunked or partitioned
+                                 (12000, 255), (12000, 256), (50000, 4096), (50000, 4097),
+                                 # several 4096-event sub-tiles per chunk, ragged tail
+                                 (1310720 + 777, 4096), (700001, 1000)])
 def test_shapes(ds, oracle, E, G):
     rng = np.random.default_rng(E + G)
     g = rng.integers(0, G, E).astype(np.uint32)
@@ -95,6 +99,20 @@ def test_resume_equals_one_call(ds, oracle):
 def test_groups_without_events_unchanged(ds):
     st, _ = run(ds, [3, 3, 5], [10.0, 10.0, 10.0], [20, 20, 20], 0.5, [7.0] * 8)
     assert st[0] == 7.0 and st[7] == 7.0 and st[3] != 7.0
+
+
+def test_groups_with_only_skipped_events_unchanged(ds, oracle):
+    # a factor with no usable event is not touched at all (-0.0 stays -0.0,
+    # NaN stays NaN), as in the sequential loop; traces repeat it
+    g = np.array([0, 1, 0, 2, 1], np.uint32)
+    est = np.array([0.0, np.nan, -1.0, 4.0, np.inf])
+    obs = np.array([5, 5, 5, 8, 5], np.uint32)
+    st0 = np.array([-0.0, np.nan, 1.0])
+    st, tr = run(ds, g, est, obs, 0.5, st0)
+    w_st, w_tr = oracle.calibrate(g, est, obs, 0.5, st0)
+    assert np.signbit(st[0]) and st[0] == 0.0 and np.isnan(st[1]) and st[2] == w_st[2] == 1.5
+    assert np.signbit(tr[0]) and np.signbit(tr[2]) and np.isnan(tr[1]) and np.isnan(tr[4])
+    assert np.array_equal(np.signbit(tr), np.signbit(w_tr))
 
 
 def test_deterministic(ds):
