@@ -10,6 +10,9 @@ prompts (the synthetic batch64k workload).
 Prints one JSON line: whole-step throughput in requests/s, the roofline of
 the dominant stage (characterize, HBM-bound) from HIP events on the stream it
 runs on, and the single-threaded CPU oracle's throughput on a bounded sample.
+By default the timed steps are replays of one step captured in a HIP graph
+(the same launches; stage times and the eager step time come from eager
+steps run first).
 """
 import argparse
 import json
@@ -50,6 +53,9 @@ def parse():
                          "up under sustained load; the timed steps measure the steady state)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="run a plain 1 GiB device copy first (to scale memory counters)")
+    ap.add_argument("--no-graph", dest="graph", action="store_false",
+                    help="time eager launches instead of replays of one step captured in a HIP "
+                         "graph (the same kernels; the graph shortens the gaps between them)")
     return ap.parse_args()
 
 
@@ -149,6 +155,35 @@ def main():
         step(evs[k])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    ms_eager = wall * 1e3 / args.steps
+
+    if args.graph:
+        # the whole step (every launch of the four stages) captured once in a
+        # HIP graph and replayed; the stage times stay those of the eager
+        # steps above, the step time is the replays'. The replays' outputs
+        # must equal the eager step's.
+        # (the factors keep folding the same events step after step, so the
+        # budgets and the SJF order may move by rounding; the others may not)
+        eager = [perms[i].clone() for i in (0, 1, 2, 4)] + [counts.clone()]
+        g = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step()
+            torch.cuda.synchronize()
+            with torch.cuda.graph(g, stream=side):
+                step()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        settle(g.replay, args.settle)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for k in range(args.steps):
+            g.replay()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        for a, b_ in zip(eager, [perms[i] for i in (0, 1, 2, 4)] + [counts]):
+            assert torch.equal(a, b_), "graph replay differs from the eager step"
 
     stage_ms = np.zeros(4)
     for e in evs:
@@ -181,6 +216,8 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "settle_s": args.settle,
+        "graph": bool(args.graph),
+        "ms_per_step_eager": round(ms_eager, 4),
         "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True,
         "scaling": "weak",

@@ -35,6 +35,10 @@ struct SortInput {
     const uint8_t *tier;
     const uint32_t *group;
     const uint32_t *fifo;      // sequence to reorder (Budget/Aging/Class/Tier)
+    // optional copies in FIFO order (entry j belongs to request fifo[j]),
+    // read instead of gathering through fifo: tier, budget, arrival
+    const uint8_t *ftier;
+    const double *fbudget, *farr;
     uint32_t n_tiers;
     uint32_t cls[16];          // Class: priority class of each tier
     double prio[16];           // Aging/Class keys
@@ -62,14 +66,21 @@ size_t ssort_ws_bytes(uint64_t n, uint32_t nsorts);   // 0 above kSsMaxN
 // Side work of the first launch of a sample sort, for the partitions that
 // follow in the same call: clear `clear_words` words, and write per-block
 // tier counts (ssort_sample_blocks(n) x 16) to tier_part if not NULL.
+// A FIFO sort can also write, at each FIFO position, the request's tier,
+// budget and arrival (NULL pointers: not wanted).
 struct SsSide {
     uint32_t *clear;
     uint32_t clear_words;
     uint32_t *tier_part;
+    uint8_t *ftier;
+    double *fbudget, *farr;
 };
+struct PartBatch;
 uint32_t ssort_sample_blocks(uint64_t n);
+// part: Priority/Weighted tiles run in the sampling launch (may be NULL).
 hipError_t ssort_launch(const SortInput &in, const SortJob *jobs, uint32_t nsorts, bool serial,
-                        void *ws, hipStream_t s, const SsSide *side = nullptr);
+                        void *ws, hipStream_t s, const SsSide *side = nullptr,
+                        const PartBatch *part = nullptr);
 
 // One-pass Priority (Class) and Weighted (Tier) orders of at most kSsMaxN
 // requests over the FIFO sequence in.fifo. status: part_ws_bytes(n) bytes of

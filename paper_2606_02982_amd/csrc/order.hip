@@ -17,6 +17,7 @@
 
 #include "common.h"
 #include "kernels.h"
+#include "partbody.h"
 
 namespace ds {
 namespace {
@@ -60,10 +61,13 @@ __global__ void k_order_validate(OrderArgs a, uint32_t *__restrict__ flag)
 }  // namespace
 
 // Up to kSsMaxN requests: the look-back words of the two partitions, an
-// error word, and the tier counts of the slices of the batch.
+// error word, the tier counts of the slices of the batch, and the tiers,
+// budgets and arrivals in FIFO order.
 static size_t part_region_bytes(uint64_t n)
 {
-    return n <= kSsMaxN ? 2 * part_ws_bytes(n) + 256 + align_up((uint64_t)ssort_sample_blocks(n) * 64, 256) : 0;
+    return n <= kSsMaxN ? 2 * part_ws_bytes(n) + 256 + align_up((uint64_t)ssort_sample_blocks(n) * 64, 256) +
+                              align_up(n, 256) + 2 * align_up(n * 8, 256)
+                        : 0;
 }
 
 size_t order_ws_bytes(uint64_t n, uint32_t npolicies)
@@ -116,14 +120,33 @@ hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_
     uint32_t *tier_part = reinterpret_cast<uint32_t *>(part_ws + 2 * part_ws_bytes(n) + 256);
     const uint32_t nparts = sample ? ssort_sample_blocks(n) : 0u;
     const uint32_t clear_words = (uint32_t)(2 * part_ws_bytes(n) / 4 + 1);
+    uint8_t *fcopy = part_ws + 2 * part_ws_bytes(n) + 256 + align_up((uint64_t)nparts * 64, 256);
+    uint8_t *ftier = fcopy;
+    double *fbudget = reinterpret_cast<double *>(fcopy + align_up(n, 256));
+    double *farr = reinterpret_cast<double *>(fcopy + align_up(n, 256) + align_up((uint64_t)n * 8, 256));
     if (!fifo) {
         SortJob job = {SortKind::Fifo, 64, want_fifo ? a.key[0] : nullptr,
                        want_fifo ? a.perm[0] : fifo_ws};
-        const SsSide side = {pstatus, clear_words, tier_part};
-        err = sample ? ssort_launch(in, &job, 1, a.serial_sort, sort_ws, s, parts ? &side : nullptr)
+        // the policies after the FIFO sort read tiers, budgets and arrivals
+        // in FIFO order, written by its last launch
+        SsSide side = {nullptr, 0u, nullptr, nullptr, nullptr, nullptr};
+        if (sample) {
+            if (parts) {
+                side.clear = pstatus;
+                side.clear_words = clear_words;
+                side.tier_part = tier_part;
+            }
+            if (a.mask & 0x16u) side.ftier = ftier;                       // Priority, Weighted, Aging
+            if ((a.mask & (1u << 3)) && a.budget) side.fbudget = fbudget;  // SJF
+            if (a.mask & (1u << 4)) side.farr = farr;                      // Aging
+        }
+        err = sample ? ssort_launch(in, &job, 1, a.serial_sort, sort_ws, s, &side)
                      : sort_launch(in, &job, 1, sort_ws, s);
         if (err != hipSuccess) return err;
         fifo = job.out;
+        in.ftier = side.ftier;
+        in.fbudget = side.fbudget;
+        in.farr = side.farr;
     } else {
         if (want_fifo) {
             uint64_t nb = cdiv(n, 256);
@@ -167,11 +190,12 @@ hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_
         else
             part[np++] = jobs[i];
     }
-    if (np) {
-        err = part_launch(in, part, np, pstatus, perror, tier_part, nparts, s);
-        if (err != hipSuccess) return err;
+    if (nk) {
+        // SJF/Aging sampling and the Priority/Weighted tiles share a launch
+        const PartBatch pb = part_batch(in, part, np, pstatus, perror, tier_part, nparts);
+        return ssort_launch(in, keyed, nk, a.serial_sort, sort_ws, s, nullptr, np ? &pb : nullptr);
     }
-    if (nk) return ssort_launch(in, keyed, nk, a.serial_sort, sort_ws, s);
+    if (np) return part_launch(in, part, np, pstatus, perror, tier_part, nparts, s);
     return hipGetLastError();
 }
 

@@ -31,10 +31,13 @@
 // A bucket that outgrows its region (only for inputs arranged against the
 // sampling) sets the overflow flag; k_ss_bucket then sorts the whole
 // sequence in one workgroup with the same LSD passes over global memory.
+#include <string.h>
+
 #include "common.h"
 #include "kernels.h"
 #include "keys.h"
 #include "lookback.h"
+#include "partbody.h"
 #include "tiercount.h"
 
 namespace ds {
@@ -79,7 +82,10 @@ struct SsBatch {
     uint32_t nb;           // buckets, 1..kMaxBuckets
     uint32_t ns;           // samples, 1..kSamples
     uint32_t serial;       // sort in one workgroup regardless of the buckets
-    SsSide side;           // work of a later launch done by k_ss_sample of sort 0
+    uint32_t nsorts;       // sorts of the batch (grid rows 0 .. nsorts - 1)
+    uint32_t nsb;          // blocks of k_ss_sample per sort
+    SsSide side;           // side work for the launches after this sort
+    PartBatch part;        // Priority/Weighted tiles run by k_ss_sample (rows nsorts ..)
     SsDesc s[kMaxSorts];
 };
 
@@ -129,13 +135,13 @@ template <SortKind K>
 __device__ __forceinline__ void sample_body(const SsBatch &b, const SsDesc &d, uint64_t *sk, uint32_t *sj)
 {
     const uint32_t t = threadIdx.x, n = b.n, S = b.ns;
-    const uint32_t stride = gridDim.x * kSmpTPB;
+    const uint32_t stride = b.nsb * kSmpTPB;
     for (uint32_t i = blockIdx.x * kSmpTPB + t; i < b.tiles * 256u; i += stride) d.status[i] = 0;
     if (blockIdx.x == 0 && t == 0) d.ctl->overflow = b.serial;
     if (blockIdx.y == 0) {
         for (uint32_t i = blockIdx.x * kSmpTPB + t; i < b.side.clear_words; i += stride) b.side.clear[i] = 0;
         if (b.side.tier_part)
-            tier_partial<kSmpTPB>(b.in.tier, n, blockIdx.x, gridDim.x, b.side.tier_part,
+            tier_partial<kSmpTPB>(b.in.tier, n, blockIdx.x, b.nsb, b.side.tier_part,
                                   reinterpret_cast<uint32_t *>(sk));
         __syncthreads();   // sk is reused below
     }
@@ -197,6 +203,14 @@ __global__ __launch_bounds__(kSmpTPB) void k_ss_sample(SsBatch b)
 {
     __shared__ uint64_t sk[kSamples];
     __shared__ uint32_t sj[kSamples];
+    if (blockIdx.y >= b.nsorts) {
+        // a Priority/Weighted tile; these rows come after every sampling
+        // block in dispatch order, so their look-back waits only on tiles
+        // dispatched before them
+        if (blockIdx.x < b.part.tiles) part_body<kSmpTPB>(b.part, blockIdx.y - b.nsorts, blockIdx.x);
+        return;
+    }
+    if (blockIdx.x >= b.nsb) return;
     const SsDesc &d = b.s[blockIdx.y];
     switch (d.kind) {
     case SortKind::Fifo: sample_body<SortKind::Fifo>(b, d, sk, sj); break;
@@ -363,6 +377,20 @@ __global__ __launch_bounds__(kScTPB) void k_ss_scatter(SsBatch b)
     if (over) atomicOr(&d.ctl->overflow, 1u);
 }
 
+// Output position pos of a sort holds val; the FIFO sort can also write the
+// request's tier, budget and arrival at pos (the copies in FIFO order that
+// the sorts after it read instead of gathering).
+__device__ __forceinline__ void emit(const SsBatch &b, const SsDesc &d, uint32_t pos, uint32_t val)
+{
+    d.out[pos] = val;
+    if (d.kind == SortKind::Fifo) {
+        const uint32_t i = val < b.n ? val : 0u;
+        if (b.side.ftier) b.side.ftier[pos] = b.in.tier[i];
+        if (b.side.fbudget) b.side.fbudget[pos] = b.in.budget[i];
+        if (b.side.farr) b.side.farr[pos] = b.in.arrival[i];
+    }
+}
+
 // LDS scratch of the bucket sort (also used by the single-workgroup sort).
 struct BkShared {
     uint32_t wcnt[2][kBkTPB / 64][256];   // per-wave digit counters, two passes' worth
@@ -520,7 +548,7 @@ __device__ void serial_sort(const SsBatch &b, const SsDesc &d, BkShared &sh)
         }
         src ^= 1u;
     }
-    for (uint32_t i = t; i < n; i += kBkTPB) d.out[i] = value_of(b.in, d.kind, n, d.fj[src][i]);
+    for (uint32_t i = t; i < n; i += kBkTPB) emit(b, d, i, value_of(b.in, d.kind, n, d.fj[src][i]));
 }
 
 __global__ __launch_bounds__(kBkTPB) void k_ss_bucket(SsBatch b)
@@ -598,7 +626,7 @@ __global__ __launch_bounds__(kBkTPB) void k_ss_bucket(SsBatch b)
 #pragma unroll
         for (int r = 0; r < kBkR; r++) {
             const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
-            if ((uint32_t)r < reff && idx < m && off + idx < n) d.out[off + idx] = jv[r];
+            if ((uint32_t)r < reff && idx < m && off + idx < n) emit(b, d, off + idx, jv[r]);
         }
         return;
     }
@@ -662,7 +690,7 @@ __global__ __launch_bounds__(kBkTPB) void k_ss_bucket(SsBatch b)
             const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
             if ((uint32_t)r < reff && idx < m) {
                 const uint32_t rank = k[r] == kmn ? lowrank[r] : nlow + hirank[r];
-                if (off + rank < n) d.out[off + rank] = jv[r];
+                if (off + rank < n) emit(b, d, off + rank, jv[r]);
             }
         }
         return;
@@ -747,7 +775,7 @@ __global__ __launch_bounds__(kBkTPB) void k_ss_bucket(SsBatch b)
                         rank += (ku < k[r] || (ku == k[r] && sh.lslot[u] < idx)) ? 1u : 0u;
                     }
                 }
-                if (off + rank < n) d.out[off + rank] = jv[r];
+                if (off + rank < n) emit(b, d, off + rank, jv[r]);
             }
         }
         return;
@@ -784,7 +812,7 @@ __global__ __launch_bounds__(kBkTPB) void k_ss_bucket(SsBatch b)
 #pragma unroll
     for (int r = 0; r < kBkR; r++) {
         const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
-        if ((uint32_t)r < reff && idx < m && off + idx < n) d.out[off + idx] = jv[r];
+        if ((uint32_t)r < reff && idx < m && off + idx < n) emit(b, d, off + idx, jv[r]);
     }
 }
 
@@ -837,7 +865,7 @@ uint32_t ssort_sample_blocks(uint64_t n)
 }
 
 hipError_t ssort_launch(const SortInput &in, const SortJob *jobs, uint32_t nsorts, bool serial,
-                        void *ws, hipStream_t s, const SsSide *side)
+                        void *ws, hipStream_t s, const SsSide *side, const PartBatch *part)
 {
     if (in.n == 0 || nsorts == 0) return hipSuccess;
     if (nsorts > kMaxSorts || in.n > kSsMaxN) return hipErrorInvalidValue;
@@ -851,7 +879,14 @@ hipError_t ssort_launch(const SortInput &in, const SortJob *jobs, uint32_t nsort
     const uint32_t smax = in.n <= (1u << 17) ? kSamples / 2 : kSamples;
     b.ns = in.n < smax ? in.n : smax;
     b.serial = serial ? 1u : 0u;
-    b.side = side ? *side : SsSide{nullptr, 0u, nullptr};
+    b.side = side ? *side : SsSide{nullptr, 0u, nullptr, nullptr, nullptr, nullptr};
+    b.nsorts = nsorts;
+    b.nsb = ssort_sample_blocks(in.n);
+    if (part) {
+        b.part = *part;
+    } else {
+        memset(&b.part, 0, sizeof(b.part));
+    }
     uint8_t *p = static_cast<uint8_t *>(ws);
     for (uint32_t i = 0; i < nsorts; i++) {
         SsDesc &d = b.s[i];
@@ -864,7 +899,8 @@ hipError_t ssort_launch(const SortInput &in, const SortJob *jobs, uint32_t nsort
         carve(p, in.n, d);
         p += region_bytes(in.n);
     }
-    hipLaunchKernelGGL(k_ss_sample, dim3(ssort_sample_blocks(in.n), nsorts), dim3(kSmpTPB), 0, s, b);
+    const uint32_t gx = b.part.njobs && b.part.tiles > b.nsb ? b.part.tiles : b.nsb;
+    hipLaunchKernelGGL(k_ss_sample, dim3(gx, nsorts + b.part.njobs), dim3(kSmpTPB), 0, s, b);
     hipLaunchKernelGGL(k_ss_scatter, dim3(b.tiles, nsorts), dim3(kScTPB), 0, s, b);
     hipLaunchKernelGGL(k_ss_bucket, dim3(b.nb, nsorts), dim3(kBkTPB), 0, s, b);
     return hipGetLastError();

@@ -1,0 +1,86 @@
+"""The whole admission step captured in a HIP graph and replayed.
+
+Every launch of the library goes on the caller's stream and none is a
+memset, so a step can be captured once and replayed. Each replay must give
+the eager step's results exactly: replays are interleaved with eager work
+and synchronisations, and every replay is checked.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2606_02982_amd import synth
+from tests.gpu_util import dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def ds():
+    from paper_2606_02982_amd import driftsched
+    return driftsched
+
+
+def test_step_graph_replays_equal_eager(ds):
+    b = synth.generate("batch4k")
+    N = b.n
+    text, offsets = dev(b.text), dev(b.offsets)
+    ev_group, ev_est, ev_obs = dev(b.ev_group), dev(b.ev_est), dev(b.ev_obs)
+    category, tenant, group = dev(b.category), dev(b.tenant), dev(b.group)
+    t_base, s_tenant = dev(b.t_base), dev(b.s_tenant)
+    tier, arrival = dev(b.tier), dev(b.arrival)
+    params = ds.order_params(weights=tuple(int(w) for w in b.weights),
+                             tier_priority=tuple(b.tier_priority), aging_rate=b.aging_rate,
+                             t_now=b.t_now, aging_floor=b.aging_floor)
+    ws = {op: ds.workspace(op, N, b.n_groups) for op in range(5)}
+
+    def buffers():
+        return dict(counts=torch.empty(N, dtype=torch.int32, device="cuda"),
+                    state=torch.ones(b.n_groups, dtype=torch.float64, device="cuda"),
+                    trace=torch.empty(N, dtype=torch.float64, device="cuda"),
+                    sc=tuple(torch.empty(N, dtype=torch.float64, device="cuda") for _ in range(3)) +
+                    (torch.empty(N, dtype=torch.uint8, device="cuda"),),
+                    perms={p: torch.empty(N, dtype=torch.int32, device="cuda") for p in range(5)})
+
+    def step(o):
+        o["state"].fill_(1.0)   # a fill kernel, not a memset
+        ds.characterize(text, offsets, counts=o["counts"], ws=ws[ds.OP_CHARACTERIZE])
+        ds.calibrate(ev_group, ev_est, ev_obs, b.alphas[0], o["state"], trace=o["trace"],
+                     ws=ws[ds.OP_CALIBRATE])
+        ds.score(o["counts"], category, tenant, group, t_base, s_tenant, o["state"], out=o["sc"])
+        ds.order_multi((0, 1, 2, 3, 4), tier, arrival, o["sc"][2], params=params, perms=o["perms"],
+                       ws=ws[ds.OP_ORDER_MULTI])
+
+    def snapshot(o):
+        out = [o["counts"], o["state"], o["trace"]] + list(o["sc"]) + [o["perms"][p] for p in range(5)]
+        return [t.cpu().clone() for t in out]
+
+    ref = buffers()
+    step(ref)
+    torch.cuda.synchronize()
+    want = snapshot(ref)
+
+    out = buffers()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step(out)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=side):
+            step(out)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    scratch = buffers()
+    for rep in range(4):
+        for t in [out["counts"], out["trace"]] + list(out["sc"][:3]) + list(out["perms"].values()):
+            t.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        got = snapshot(out)
+        for i, (a, w) in enumerate(zip(got, want)):
+            assert torch.equal(a, w), "replay %d: output %d differs" % (rep, i)
+        step(scratch)   # eager work between the replays
+        torch.cuda.synchronize()
+    assert np.array_equal(want[0].numpy().view(np.uint32), b.words)
