@@ -10,9 +10,12 @@ prompts (the synthetic batch64k workload).
 Prints one JSON line: whole-step throughput in requests/s, the roofline of
 the dominant stage (characterize, HBM-bound) from HIP events on the stream it
 runs on, and the single-threaded CPU oracle's throughput on a bounded sample.
-By default the timed steps are replays of one step captured in a HIP graph
-(the same launches; stage times and the eager step time come from eager
-steps run first).
+The timed steps are eager launches on one stream (stage times come from
+steps with events between the stages, run first); --graph times replays of
+one step captured in a HIP graph instead (the same launches, measured a few
+percent slower than eager launches here). --schedule overlap runs the stages along their
+dependencies on two streams instead (calibrate and the FIFO, Priority,
+Weighted and Aging orders beside characterize; score and SJF after both).
 """
 import argparse
 import json
@@ -53,9 +56,13 @@ def parse():
                          "up under sustained load; the timed steps measure the steady state)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="run a plain 1 GiB device copy first (to scale memory counters)")
-    ap.add_argument("--no-graph", dest="graph", action="store_false",
-                    help="time eager launches instead of replays of one step captured in a HIP "
-                         "graph (the same kernels; the graph shortens the gaps between them)")
+    ap.add_argument("--schedule", choices=["serial", "overlap"], default="serial",
+                    help="overlap: stages that do not depend on each other run on two streams "
+                         "(calibrate and the budget-free orders beside characterize); serial: "
+                         "the four stages one after another on one stream")
+    ap.add_argument("--graph", action="store_true",
+                    help="time replays of one step captured in a HIP graph instead of eager "
+                         "launches (the same kernels)")
     return ap.parse_args()
 
 
@@ -131,31 +138,64 @@ def main():
     torch.cuda.synchronize()
 
     def step(ev=None):
+        """The four stages one after another on the current stream."""
         if ev: ev[0].record()
         ds.characterize(text, offsets, counts=counts, ws=ws[ds.OP_CHARACTERIZE])
         if ev: ev[1].record()
         ds.calibrate(ev_group, ev_est, ev_obs, alpha, state, trace=trace, ws=ws[ds.OP_CALIBRATE])
         if ev: ev[2].record()
-        budget = sc_out[2]
         ds.score(counts, category, tenant, group, t_base, s_tenant, state, out=sc_out)
         if ev: ev[3].record()
-        ds.order_multi(ALL, tier, arrival, budget, params=params, perms=perm_map,
+        ds.order_multi(ALL, tier, arrival, sc_out[2], params=params, perms=perm_map,
                        ws=ws[ds.OP_ORDER_MULTI])
         if ev: ev[4].record()
 
-    settle(step, args.settle)
+    # The same work along the stages' dependencies: calibrate reads only the
+    # completion events, and FIFO, Priority, Weighted and Aging only tiers and
+    # arrivals, so they run on a second stream beside characterize; score
+    # joins both, and SJF (budget-keyed) reuses the FIFO permutation.
+    aux = torch.cuda.Stream()
+    ws_aux = ds.workspace(ds.OP_ORDER_MULTI, N, b.n_groups)
+    budget = sc_out[2]
+
+    def step_overlap():
+        main_s = torch.cuda.current_stream()
+        aux.wait_stream(main_s)
+        with torch.cuda.stream(aux):
+            ds.calibrate(ev_group, ev_est, ev_obs, alpha, state, trace=trace,
+                         ws=ws[ds.OP_CALIBRATE])
+            ds.order_multi((0, 1, 2, 4), tier, arrival, params=params, perms=perm_map, ws=ws_aux)
+        ds.characterize(text, offsets, counts=counts, ws=ws[ds.OP_CHARACTERIZE])
+        main_s.wait_stream(aux)
+        ds.score(counts, category, tenant, group, t_base, s_tenant, state, out=sc_out)
+        ds.order_multi((3,), tier, arrival, budget, fifo=perms[0], params=params, perms=perm_map,
+                       ws=ws[ds.OP_ORDER_MULTI])
+
+    run = step if args.schedule == "serial" else step_overlap
+
+    settle(run, args.settle)
+    for _ in range(args.warmup):
+        run()
+    torch.cuda.synchronize()
+
+    # stage times: serial steps with events between the stages
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
     for k in range(args.steps):
         step(evs[k])
     torch.cuda.synchronize()
+    serial_out = [perms[i].clone() for i in (0, 1, 2, 4)] + [counts.clone()]
+    # eager step time of the timed schedule
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        run()
+    torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_eager = wall * 1e3 / args.steps
+    for a, b_ in zip(serial_out, [perms[i] for i in (0, 1, 2, 4)] + [counts]):
+        assert torch.equal(a, b_), "the %s schedule differs from the serial step" % args.schedule
 
     if args.graph:
         # the whole step (every launch of the four stages) captured once in a
@@ -166,14 +206,14 @@ def main():
         # budgets and the SJF order may move by rounding; the others may not)
         eager = [perms[i].clone() for i in (0, 1, 2, 4)] + [counts.clone()]
         g = torch.cuda.CUDAGraph()
-        side = torch.cuda.Stream()
-        side.wait_stream(torch.cuda.current_stream())
-        with torch.cuda.stream(side):
-            step()
+        cap = torch.cuda.Stream()
+        cap.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(cap):
+            run()
             torch.cuda.synchronize()
-            with torch.cuda.graph(g, stream=side):
-                step()
-        torch.cuda.current_stream().wait_stream(side)
+            with torch.cuda.graph(g, stream=cap):
+                run()
+        torch.cuda.current_stream().wait_stream(cap)
         torch.cuda.synchronize()
         settle(g.replay, args.settle)
         torch.cuda.synchronize()
@@ -217,6 +257,7 @@ def main():
         "warmup": args.warmup,
         "settle_s": args.settle,
         "graph": bool(args.graph),
+        "schedule": args.schedule,
         "ms_per_step_eager": round(ms_eager, 4),
         "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True,

@@ -39,7 +39,11 @@ namespace {
 constexpr uint32_t kRound = 1024;        // bytes per wave per round
 constexpr uint32_t kLoadRounds = 4;      // rounds loaded together
 constexpr uint32_t kBlock = 256;         // 4 independent waves per block
-constexpr uint32_t kMaxWaves = 16384;
+// Each wave takes one contiguous range of the buffer. Four ranges per
+// resident wave slot: waves that start late (their slot held by an earlier
+// wave or by another stream's kernel) leave a short tail, not a long one.
+constexpr uint32_t kRangesPerSlot = 4;
+constexpr uint32_t kMaxWaves = 32768;
 constexpr uint64_t kNone = ~0ull;
 
 // 0x80 in each byte of x that is an ASCII separator 09-0D or 1C-20.
@@ -66,20 +70,6 @@ __device__ __forceinline__ uint32_t compact4(uint32_t hb)
 __device__ __forceinline__ uint32_t compact16(uint32_t a, uint32_t b, uint32_t c, uint32_t d)
 {
     return compact4(a) | (compact4(b) << 4) | (compact4(c) << 8) | (compact4(d) << 12);
-}
-
-// Length (2 or 3) of a multi-byte separator whose bytes are the low bytes of
-// v (little-endian), or 0.
-__device__ __forceinline__ uint32_t mb_space_len(uint32_t v)
-{
-    uint32_t v2 = v & 0xFFFFu, v3 = v & 0xFFFFFFu;
-    if (v2 == 0x85C2u || v2 == 0xA0C2u) return 2;                   // U+0085, U+00A0
-    if (v3 == 0x809AE1u || v3 == 0x9F81E2u || v3 == 0x8080E3u) return 3;  // U+1680, U+205F, U+3000
-    if (v2 == 0x80E2u) {                                             // U+2000..200A, 2028, 2029, 202F
-        uint32_t b2 = (v >> 16) & 0xFFu;
-        if (b2 - 0x80u <= 0x0Au || b2 == 0xA8u || b2 == 0xA9u || b2 == 0xAFu) return 3;
-    }
-    return 0;
 }
 
 typedef unsigned int v4u __attribute__((ext_vector_type(4)));
@@ -730,7 +720,7 @@ hipError_t char_launch(const uint8_t *text, uint64_t B, const uint64_t *offsets,
         resident = (n_cu > 0 ? n_cu : 1) * (per_cu > 0 ? per_cu : 1) * (int)(kBlock / 64);
         if (dev >= 0 && dev < 64) resident_cache[dev] = resident;
     }
-    uint64_t target = (uint64_t)resident;
+    uint64_t target = (uint64_t)resident * kRangesPerSlot;
     if (target > kMaxWaves) target = kMaxWaves;
     uint64_t Rw = align_up(cdiv(B ? B : 1, target), (uint64_t)kRound * kLoadRounds);
     uint32_t nwaves = (uint32_t)cdiv(B, Rw);

@@ -21,7 +21,8 @@ def ds():
     return driftsched
 
 
-def test_step_graph_replays_equal_eager(ds):
+@pytest.mark.parametrize("schedule", ["serial", "overlap"])
+def test_step_graph_replays_equal_eager(ds, schedule):
     b = synth.generate("batch4k")
     N = b.n
     text, offsets = dev(b.text), dev(b.offsets)
@@ -42,7 +43,10 @@ def test_step_graph_replays_equal_eager(ds):
                     (torch.empty(N, dtype=torch.uint8, device="cuda"),),
                     perms={p: torch.empty(N, dtype=torch.int32, device="cuda") for p in range(5)})
 
-    def step(o):
+    aux = torch.cuda.Stream()
+    ws_aux = ds.workspace(ds.OP_ORDER_MULTI, N, b.n_groups)
+
+    def serial(o):
         o["state"].fill_(1.0)   # a fill kernel, not a memset
         ds.characterize(text, offsets, counts=o["counts"], ws=ws[ds.OP_CHARACTERIZE])
         ds.calibrate(ev_group, ev_est, ev_obs, b.alphas[0], o["state"], trace=o["trace"],
@@ -51,12 +55,30 @@ def test_step_graph_replays_equal_eager(ds):
         ds.order_multi((0, 1, 2, 3, 4), tier, arrival, o["sc"][2], params=params, perms=o["perms"],
                        ws=ws[ds.OP_ORDER_MULTI])
 
+    def overlap(o):
+        # calibrate and the budget-free orders on a second stream beside
+        # characterize; score and SJF after the join
+        o["state"].fill_(1.0)
+        main_s = torch.cuda.current_stream()
+        aux.wait_stream(main_s)
+        with torch.cuda.stream(aux):
+            ds.calibrate(ev_group, ev_est, ev_obs, b.alphas[0], o["state"], trace=o["trace"],
+                         ws=ws[ds.OP_CALIBRATE])
+            ds.order_multi((0, 1, 2, 4), tier, arrival, params=params, perms=o["perms"], ws=ws_aux)
+        ds.characterize(text, offsets, counts=o["counts"], ws=ws[ds.OP_CHARACTERIZE])
+        main_s.wait_stream(aux)
+        ds.score(o["counts"], category, tenant, group, t_base, s_tenant, o["state"], out=o["sc"])
+        ds.order_multi((3,), tier, arrival, o["sc"][2], fifo=o["perms"][0], params=params,
+                       perms=o["perms"], ws=ws[ds.OP_ORDER_MULTI])
+
+    step = serial if schedule == "serial" else overlap
+
     def snapshot(o):
         out = [o["counts"], o["state"], o["trace"]] + list(o["sc"]) + [o["perms"][p] for p in range(5)]
         return [t.cpu().clone() for t in out]
 
     ref = buffers()
-    step(ref)
+    serial(ref)
     torch.cuda.synchronize()
     want = snapshot(ref)
 
