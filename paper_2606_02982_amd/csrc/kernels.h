@@ -34,11 +34,7 @@ struct SortInput {
     const double *budget;
     const uint8_t *tier;
     const uint32_t *group;
-    const uint32_t *fifo;      // sequence to reorder (Budget/Aging/Class/Tier)
-    // optional copies in FIFO order (entry j belongs to request fifo[j]),
-    // read instead of gathering through fifo: tier, budget, arrival
-    const uint8_t *ftier;
-    const double *fbudget, *farr;
+    const uint32_t *fifo;      // LSD sorts: sequence to reorder (Budget/Aging/Class/Tier)
     uint32_t n_tiers;
     uint32_t cls[16];          // Class: priority class of each tier
     double prio[16];           // Aging/Class keys
@@ -58,40 +54,16 @@ size_t sort_ws_bytes(uint64_t n, uint32_t nsorts);
 hipError_t sort_launch(const SortInput &in, const SortJob *jobs, uint32_t nsorts, void *ws,
                        hipStream_t s);
 
-// Sample sort of (64-bit key, position) pairs in three launches, for Fifo,
-// Budget and Aging jobs of at most kSsMaxN keys; `serial` sorts in one
-// workgroup instead (the path taken when a bucket overflows).
+// The dispatch orders of at most kSsMaxN requests: a batch of up to
+// kSsMaxSorts sample sorts (Fifo, Class, Tier, Budget, Aging; at most one of
+// each) by composite keys, in three launches; none needs the FIFO order as an
+// input. `serial` sorts in one workgroup instead (the path taken when a
+// bucket overflows).
 constexpr uint32_t kSsMaxN = 1u << 18;
+constexpr uint32_t kSsMaxSorts = 5;
 size_t ssort_ws_bytes(uint64_t n, uint32_t nsorts);   // 0 above kSsMaxN
-// Side work of the first launch of a sample sort, for the partitions that
-// follow in the same call: clear `clear_words` words, and write per-block
-// tier counts (ssort_sample_blocks(n) x 16) to tier_part if not NULL.
-// A FIFO sort can also write, at each FIFO position, the request's tier,
-// budget and arrival (NULL pointers: not wanted).
-struct SsSide {
-    uint32_t *clear;
-    uint32_t clear_words;
-    uint32_t *tier_part;
-    uint8_t *ftier;
-    double *fbudget, *farr;
-};
-struct PartBatch;
-uint32_t ssort_sample_blocks(uint64_t n);
-// part: Priority/Weighted tiles run in the sampling launch (may be NULL).
 hipError_t ssort_launch(const SortInput &in, const SortJob *jobs, uint32_t nsorts, bool serial,
-                        void *ws, hipStream_t s, const SsSide *side = nullptr,
-                        const PartBatch *part = nullptr);
-
-// One-pass Priority (Class) and Weighted (Tier) orders of at most kSsMaxN
-// requests over the FIFO sequence in.fifo. status: part_ws_bytes(n) bytes of
-// zeroed words per job; tier_part: nparts x 16 tier counts of slices of the
-// batch (from the FIFO sort's first launch, or part_prepare).
-size_t part_ws_bytes(uint64_t n);          // one job's look-back words
-hipError_t part_launch(const SortInput &in, const SortJob *jobs, uint32_t njobs, uint32_t *status,
-                       uint32_t *error, const uint32_t *tier_part, uint32_t nparts, hipStream_t s);
-// The same side work without a FIFO sort: clear and tier counts.
-hipError_t part_prepare(const SortInput &in, uint32_t *clear, uint32_t clear_words,
-                        uint32_t *tier_part, uint32_t nparts, hipStream_t s);
+                        void *ws, hipStream_t s);
 
 // ---- stage 2: calibrate -------------------------------------------------------
 // Up to kCalGroupsLds groups: chunked scan without a global partition.

@@ -77,34 +77,4 @@ __device__ __forceinline__ void produce(const SortInput &in, SortKind kind, doub
     }
 }
 
-// The primary key of position j as a double, and its value, for the sorts
-// with floating-point keys (Fifo, Budget, Aging); the same operations as
-// produce(), reading the FIFO-ordered copies when present. Only loads: a
-// caller that unrolls several positions gets all their loads in flight
-// before the first use.
-template <SortKind K>
-__device__ __forceinline__ double primary_key(const SortInput &in, uint32_t n, uint32_t j, uint32_t &v)
-{
-    if constexpr (K == SortKind::Fifo) {
-        v = j;
-        return in.arrival[j];
-    } else {
-        uint32_t i = in.fifo[j];
-        i = i < n ? i : 0;
-        v = i;
-        if constexpr (K == SortKind::Budget) {
-            return in.fbudget ? in.fbudget[j] : in.budget[i];
-        } else {
-            uint32_t q = in.ftier ? in.ftier[j] : in.tier[i];
-            q = q < 16 ? q : 15;
-            double w = in.t_now - (in.farr ? in.farr[j] : in.arrival[i]);
-            if (w < 0.0) w = 0.0;
-            double d = in.aging_rate * w;
-            double e = in.prio[q] - d;
-            if (e < in.aging_floor) e = in.aging_floor;
-            return e;
-        }
-    }
-}
-
 }  // namespace ds

@@ -2,22 +2,21 @@
 //
 // Every policy ends ties in FIFO order, so each one is a stable reordering
 // of the FIFO sequence:
-//   FIFO      radix sort of (arrival, index)
+//   FIFO      order of (arrival, index)
 //   Priority  stable partition of the FIFO sequence by priority class
 //   Weighted  stable partition by tier, then each request goes straight to
 //             its cyclic round-robin position (closed form of the round)
-//   SJF       stable radix sort of the FIFO sequence by budget
-//   Aging     stable radix sort of the FIFO sequence by the aged score
-// The FIFO sort runs first (unless the caller passes it in); the requested
-// policy sorts then run together in one batch of launches. Up to kSsMaxN
-// requests the 64-bit-key sorts (FIFO, SJF, Aging) are sample sorts of three
-// launches, and the one-pass partitions (Priority, Weighted) a batch of their
-// own.
+//   SJF       stable sort of the FIFO sequence by budget
+//   Aging     stable sort of the FIFO sequence by the aged score
+// Up to kSsMaxN requests every requested policy is a sample sort by the
+// composite key (policy key, arrival, index), all of them in the same three
+// launches. Above that, the FIFO permutation is sorted first (unless the
+// caller passes it in) and the other policies are LSD radix sorts of the
+// FIFO sequence, batched in one set of launches.
 #include <algorithm>
 
 #include "common.h"
 #include "kernels.h"
-#include "partbody.h"
 
 namespace ds {
 namespace {
@@ -60,23 +59,18 @@ __global__ void k_order_validate(OrderArgs a, uint32_t *__restrict__ flag)
 
 }  // namespace
 
-// Up to kSsMaxN requests: the look-back words of the two partitions, an
-// error word, the tier counts of the slices of the batch, and the tiers,
-// budgets and arrivals in FIFO order.
-static size_t part_region_bytes(uint64_t n)
-{
-    return n <= kSsMaxN ? 2 * part_ws_bytes(n) + 256 + align_up((uint64_t)ssort_sample_blocks(n) * 64, 256) +
-                              align_up(n, 256) + 2 * align_up(n * 8, 256)
-                        : 0;
-}
-
 size_t order_ws_bytes(uint64_t n, uint32_t npolicies)
 {
-    uint32_t nsorts = npolicies < 1 ? 1 : (npolicies > kMaxSorts ? kMaxSorts : npolicies);
-    // the FIFO sort and the policy sorts run one after another on the stream
-    // and share the sort workspace
-    const size_t radix = sort_ws_bytes(n, nsorts), sample = ssort_ws_bytes(n, nsorts);
-    return align_up(n * 4, 256) + part_region_bytes(n) + (radix > sample ? radix : sample);
+    // sample sorts: the FIFO sort and each policy's; radix sorts: the FIFO
+    // permutation, then the policy sorts (sharing the sort workspace with the
+    // FIFO sort, which runs before them on the stream)
+    const uint32_t np = npolicies < 1 ? 1 : npolicies;
+    const uint32_t nss = np + 1 > kSsMaxSorts ? kSsMaxSorts : np + 1;
+    const uint32_t nrs = np > kMaxSorts ? kMaxSorts : np;
+    const size_t sample = ssort_ws_bytes(n < kSsMaxN ? n : kSsMaxN, nss);
+    const size_t radix = align_up(n * 4, 256) + sort_ws_bytes(n, nrs);
+    // the larger of the two keeps the size non-decreasing in n
+    return n <= kSsMaxN ? sample : (radix > sample ? radix : sample);
 }
 
 hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_t s)
@@ -89,11 +83,6 @@ hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_
         return hipGetLastError();
     }
     if (n == 0 || a.mask == 0) return hipSuccess;
-    // workspace: FIFO permutation, partition look-back words, sort workspace
-    uint8_t *p = static_cast<uint8_t *>(ws);
-    uint32_t *fifo_ws = reinterpret_cast<uint32_t *>(p);
-    uint8_t *part_ws = p + align_up((uint64_t)n * 4, 256);
-    void *sort_ws = part_ws + part_region_bytes(n);
 
     SortInput in = {};
     in.n = n;
@@ -108,61 +97,6 @@ hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_
     in.aging_rate = a.aging_rate;
     in.t_now = a.t_now;
     in.aging_floor = a.aging_floor;
-
-    const bool want_fifo = a.mask & 1u;
-    const uint32_t *fifo = a.fifo_in;
-    hipError_t err;
-    const bool sample = n <= kSsMaxN;
-    const bool parts = sample && (a.mask & 6u);   // Priority or Weighted by the one-pass partition
-    // partition region: look-back words of two jobs, error word, tier counts
-    uint32_t *pstatus = reinterpret_cast<uint32_t *>(part_ws);
-    uint32_t *perror = reinterpret_cast<uint32_t *>(part_ws + 2 * part_ws_bytes(n));
-    uint32_t *tier_part = reinterpret_cast<uint32_t *>(part_ws + 2 * part_ws_bytes(n) + 256);
-    const uint32_t nparts = sample ? ssort_sample_blocks(n) : 0u;
-    const uint32_t clear_words = (uint32_t)(2 * part_ws_bytes(n) / 4 + 1);
-    uint8_t *fcopy = part_ws + 2 * part_ws_bytes(n) + 256 + align_up((uint64_t)nparts * 64, 256);
-    uint8_t *ftier = fcopy;
-    double *fbudget = reinterpret_cast<double *>(fcopy + align_up(n, 256));
-    double *farr = reinterpret_cast<double *>(fcopy + align_up(n, 256) + align_up((uint64_t)n * 8, 256));
-    if (!fifo) {
-        SortJob job = {SortKind::Fifo, 64, want_fifo ? a.key[0] : nullptr,
-                       want_fifo ? a.perm[0] : fifo_ws};
-        // the policies after the FIFO sort read tiers, budgets and arrivals
-        // in FIFO order, written by its last launch
-        SsSide side = {nullptr, 0u, nullptr, nullptr, nullptr, nullptr};
-        if (sample) {
-            if (parts) {
-                side.clear = pstatus;
-                side.clear_words = clear_words;
-                side.tier_part = tier_part;
-            }
-            if (a.mask & 0x16u) side.ftier = ftier;                       // Priority, Weighted, Aging
-            if ((a.mask & (1u << 3)) && a.budget) side.fbudget = fbudget;  // SJF
-            if (a.mask & (1u << 4)) side.farr = farr;                      // Aging
-        }
-        err = sample ? ssort_launch(in, &job, 1, a.serial_sort, sort_ws, s, &side)
-                     : sort_launch(in, &job, 1, sort_ws, s);
-        if (err != hipSuccess) return err;
-        fifo = job.out;
-        in.ftier = side.ftier;
-        in.fbudget = side.fbudget;
-        in.farr = side.farr;
-    } else {
-        if (want_fifo) {
-            uint64_t nb = cdiv(n, 256);
-            uint32_t blocks = (uint32_t)(nb < 4096 ? nb : 4096);
-            hipLaunchKernelGGL(k_copy_fifo, dim3(blocks), dim3(256), 0, s, fifo, a.arrival, n,
-                               a.perm[0], a.key[0]);
-        }
-        if (parts) {
-            err = part_prepare(in, pstatus, clear_words, tier_part, nparts, s);
-            if (err != hipSuccess) return err;
-        }
-    }
-    in.fifo = fifo;
-
-    SortJob jobs[kMaxSorts];
-    uint32_t nj = 0;
     if (a.mask & (1u << 1)) {
         // priority classes: rank of each tier's priority among the distinct values
         double vals[16];
@@ -175,28 +109,49 @@ hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_
                 while (c + 1 < nd && vals[c] < a.prio[q]) c++;
             in.cls[q] = c;
         }
-        jobs[nj++] = {SortKind::Class, 8, a.key[1], a.perm[1]};
     }
-    if (a.mask & (1u << 2)) jobs[nj++] = {SortKind::Tier, 8, a.key[2], a.perm[2]};
+    const bool want_fifo = a.mask & 1u;
+    // the policy sorts, in the order of their grid rows
+    SortJob jobs[kSsMaxSorts];
+    uint32_t nj = 0;
+    // (the sample sorts' rows are dispatched in this order: the cheaper
+    // partitions last, where a second round of blocks may start)
     if (a.mask & (1u << 3)) jobs[nj++] = {SortKind::Budget, 64, a.key[3], a.perm[3]};
     if (a.mask & (1u << 4)) jobs[nj++] = {SortKind::Aging, 64, a.key[4], a.perm[4]};
+    if (a.mask & (1u << 1)) jobs[nj++] = {SortKind::Class, 8, a.key[1], a.perm[1]};
+    if (a.mask & (1u << 2)) jobs[nj++] = {SortKind::Tier, 8, a.key[2], a.perm[2]};
+
+    if (want_fifo && a.fifo_in) {
+        uint64_t nb = cdiv(n, 256);
+        uint32_t blocks = (uint32_t)(nb < 4096 ? nb : 4096);
+        hipLaunchKernelGGL(k_copy_fifo, dim3(blocks), dim3(256), 0, s, a.fifo_in, a.arrival, n, a.perm[0],
+                           a.key[0]);
+    }
+    if (n <= kSsMaxN) {
+        // one batch of sample sorts; the FIFO order is not an input of the
+        // others, so a given fifo_in only saves the FIFO sort itself
+        SortJob all[kSsMaxSorts];
+        uint32_t na = 0;
+        if (want_fifo && !a.fifo_in) all[na++] = {SortKind::Fifo, 64, a.key[0], a.perm[0]};
+        for (uint32_t i = 0; i < nj; i++) all[na++] = jobs[i];
+        if (na == 0) return hipGetLastError();
+        return ssort_launch(in, all, na, a.serial_sort, ws, s);
+    }
+
+    // radix sorts: the FIFO permutation first, then the policies over it
+    uint8_t *p = static_cast<uint8_t *>(ws);
+    uint32_t *fifo_ws = reinterpret_cast<uint32_t *>(p);
+    void *sort_ws = p + align_up((uint64_t)n * 4, 256);
+    const uint32_t *fifo = a.fifo_in;
+    if (!fifo) {
+        SortJob job = {SortKind::Fifo, 64, want_fifo ? a.key[0] : nullptr, want_fifo ? a.perm[0] : fifo_ws};
+        hipError_t err = sort_launch(in, &job, 1, sort_ws, s);
+        if (err != hipSuccess) return err;
+        fifo = job.out;
+    }
+    in.fifo = fifo;
     if (nj == 0) return hipGetLastError();
-    if (!sample) return sort_launch(in, jobs, nj, sort_ws, s);
-    SortJob part[kMaxSorts], keyed[kMaxSorts];
-    uint32_t np = 0, nk = 0;
-    for (uint32_t i = 0; i < nj; i++) {
-        if (jobs[i].kind == SortKind::Budget || jobs[i].kind == SortKind::Aging)
-            keyed[nk++] = jobs[i];
-        else
-            part[np++] = jobs[i];
-    }
-    if (nk) {
-        // SJF/Aging sampling and the Priority/Weighted tiles share a launch
-        const PartBatch pb = part_batch(in, part, np, pstatus, perror, tier_part, nparts);
-        return ssort_launch(in, keyed, nk, a.serial_sort, sort_ws, s, nullptr, np ? &pb : nullptr);
-    }
-    if (np) return part_launch(in, part, np, pstatus, perror, tier_part, nparts, s);
-    return hipGetLastError();
+    return sort_launch(in, jobs, nj, sort_ws, s);
 }
 
 __global__ void k_fill_u32(uint32_t *__restrict__ p, uint32_t v, uint64_t n)

@@ -1,60 +1,72 @@
-// Sample sort of (64-bit key, position) pairs for batches of up to 2^18
-// requests, where the dispatch orders are latency-bound: three launches per
-// batch of sorts instead of one launch per 8-bit digit.
+// Dispatch orders of up to 2^18 requests as one batch of sample sorts
+// (Sec. "Scheduling Engine"): three launches for any set of policies.
 //
-// Every sort orders positions j = 0..n-1 of a sequence by (key_j, j); its
-// output is the value of each position in that order (j itself for the FIFO
-// sort, the j-th request of the FIFO sequence for SJF and Aging). Since the
-// pairs are distinct, the result is the unique stable order whatever the
-// intermediate arrangement.
+// Every policy ends ties in FIFO order, and FIFO order is the order of
+// (arrival, index). So each policy's order is the order of the requests by a
+// composite key (k1, k2, i): k1 the policy's own key, k2 the arrival, i the
+// request index, compared in that order. No policy needs the FIFO
+// permutation as an input, and all of them sort side by side:
+//   Fifo    k1 = arrival (no k2)
+//   Class   k1 = priority class of the tier                (Priority)
+//   Tier    k1 = tier; the sorted position p of a request gives its rank
+//           k = p - (requests of lower tiers) within its tier in FIFO order,
+//           and the request goes to the round-robin position of that rank
+//           (Weighted):
+//           sum_t' min(n_t', r w_t') + sum_{t' < t} min(w_t', max(0, n_t' - r w_t'))
+//           + (k - r w_t),  r = floor(k / w_t)
+//   Budget  k1 = budget                                     (SJF)
+//   Aging   k1 = aged score max(floor, p - rate * max(0, t_now - arrival))
+// Keys are doubles compared through ordered_bits (so -0.0 ties with +0.0).
 //
-//   k_ss_sample   produces S pairs (1024 up to 2^17 keys, else 2048) at
-//                 stratified random positions;
-//                 each of S/8 blocks stages all of them in LDS and finds the
-//                 rank of 8 of them by counting the smaller ones, and stores
-//                 each at its rank: the sorted sample, of which every
-//                 (S/B)-th pair is one of B - 1 splitters. Also clears the
-//                 look-back words and the overflow flag.
-//   k_ss_scatter  per tile of 2048 positions: produces the pairs (and the
-//                 per-request key output), finds each pair's bucket by binary
-//                 search over the splitters, ranks the tile by bucket (wave
-//                 ballots), takes the bucket prefix of earlier tiles by
-//                 decoupled look-back and writes each key with its output
-//                 value into the bucket's fixed-capacity region, so that a
-//                 bucket holds its pairs in position order.
-//   k_ss_bucket   one block per bucket (its offset: the sizes of the
-//                 buckets before it): bins the pairs into 2048 intervals of
-//                 the bucket's key range (an LDS histogram and its scan), and
-//                 ranks each pair inside its bin by (key, position) by
-//                 counting; a bucket with a bin of more than 64 pairs runs
-//                 stable LSD passes over its varying key bytes instead.
+//   k_ss_sample   S triples (1024 up to 2^17 requests, else 2048) at
+//                 stratified random positions; each of S/8 blocks stages all
+//                 of them in LDS, finds the rank of 8 of them by counting the
+//                 smaller ones and stores each at its rank: the sorted
+//                 sample, of which every (S/B)-th triple is one of B - 1
+//                 splitters. Also clears the look-back words and the overflow
+//                 flag, and counts the tiers of slices of the batch.
+//   k_ss_scatter  per tile of 2048 requests: makes the keys (and the
+//                 per-request key output), finds each request's bucket by
+//                 descending a search tree of the splitters, ranks the tile
+//                 by bucket (wave ballots), takes the bucket's count over
+//                 earlier tiles by decoupled look-back and writes the keys
+//                 and index into the bucket's fixed-capacity region, so that
+//                 a bucket holds its requests in index order.
+//   k_ss_bucket   one block per bucket (its offset: the sizes of the buckets
+//                 before it). A rank pass orders the bucket by one 64-bit key,
+//                 stably in the current order: by bins over the key range and
+//                 counting inside a bin, or stable LSD passes when a bin is
+//                 crowded. Two-key sorts take a pass by k2, then one by k1
+//                 (skipped when k1 is the same for the whole bucket), which
+//                 together order by (k1, k2, index).
 // A bucket that outgrows its region (only for inputs arranged against the
-// sampling) sets the overflow flag; k_ss_bucket then sorts the whole
-// sequence in one workgroup with the same LSD passes over global memory.
+// sampling) sets the overflow flag; k_ss_bucket then sorts the whole batch
+// in one workgroup with LSD passes over global memory.
 #include <string.h>
+
+#include <type_traits>
 
 #include "common.h"
 #include "kernels.h"
-#include "keys.h"
 #include "lookback.h"
-#include "partbody.h"
 #include "tiercount.h"
 
 namespace ds {
 namespace {
 
-constexpr uint32_t kSamples = 2048;      // pairs sampled per sort (at most)
-constexpr uint32_t kCap = 4096;          // pairs per bucket region
+constexpr uint32_t kSamples = 2048;      // triples sampled per sort (at most)
+constexpr uint32_t kCap = 4096;          // requests per bucket region
 constexpr uint32_t kMaxBuckets = 256;
-constexpr uint32_t kBucketAvg = 256;     // target pairs per bucket
-constexpr int kScTPB = 512, kScR = 4;    // scatter tile: 2048 positions
+constexpr uint32_t kBucketAvg = 1024;    // target requests per bucket
+constexpr int kScTPB = 512, kScR = 4;    // scatter tile: 2048 requests
 constexpr uint32_t kScTile = kScTPB * kScR;
 constexpr int kBkTPB = 512, kBkR = kCap / kBkTPB;
 constexpr uint32_t kBinBits = 11, kBins = 1u << kBinBits;   // in-bucket bins
 constexpr uint32_t kBinMax = 64;         // larger bins: LSD passes instead
-constexpr int kSmpTPB = 256;            // k_ss_sample: threads per block,
+constexpr int kSmpTPB = 256;             // k_ss_sample: threads per block,
 constexpr uint32_t kSmpThr = 32;         // threads per sample ranked,
 constexpr uint32_t kSmpPerBlock = kSmpTPB / kSmpThr;   // samples ranked per block
+constexpr uint32_t kQ = kTierCounts;     // tiers
 
 struct SsCtl {
     uint32_t overflow;
@@ -63,15 +75,20 @@ struct SsCtl {
 
 struct SsDesc {
     SortKind kind;
+    uint32_t two;          // k2 (the arrival) is part of the key
     double *key_out;
     uint32_t *out;
     SsCtl *ctl;
-    uint64_t *smp_k;       // [kSamples] the sample in sorted order
+    uint64_t *smp_k1;      // [kSamples] the sample in sorted order
+    uint64_t *smp_k2;
     uint32_t *smp_j;
     uint32_t *status;      // [tiles][256] look-back words
-    uint64_t *bkey;        // [buckets][kCap] bucket regions: keys and output values
+    uint64_t *bk1;         // [buckets][kCap] bucket regions
+    uint64_t *bk2;
     uint32_t *bj;
-    uint64_t *fkey[2];     // [n] x 2: single-workgroup sort
+    uint32_t *tot;         // [kQ] requests per tier (Tier sorts)
+    uint64_t *fk1[2];      // [n] x 2: single-workgroup sort
+    uint64_t *fk2[2];
     uint32_t *fj[2];
 };
 
@@ -82,21 +99,11 @@ struct SsBatch {
     uint32_t nb;           // buckets, 1..kMaxBuckets
     uint32_t ns;           // samples, 1..kSamples
     uint32_t serial;       // sort in one workgroup regardless of the buckets
-    uint32_t nsorts;       // sorts of the batch (grid rows 0 .. nsorts - 1)
+    uint32_t nsorts;       // sorts of the batch (grid rows)
     uint32_t nsb;          // blocks of k_ss_sample per sort
-    SsSide side;           // side work for the launches after this sort
-    PartBatch part;        // Priority/Weighted tiles run by k_ss_sample (rows nsorts ..)
-    SsDesc s[kMaxSorts];
+    uint32_t *tier_part;   // [nsb][kQ] tier counts of slices (a Tier sort is in the batch)
+    SsDesc s[kSsMaxSorts];
 };
-
-// Value emitted for position j: the FIFO sort reorders the requests
-// themselves; SJF and Aging reorder the FIFO sequence.
-__device__ __forceinline__ uint32_t value_of(const SortInput &in, SortKind kind, uint32_t n, uint32_t j)
-{
-    if (kind == SortKind::Fifo) return j;
-    const uint32_t i = in.fifo[j < n ? j : 0];
-    return i < n ? i : 0u;
-}
 
 // Position of sample s: uniform in the s-th of S equal strata of [0, n)
 // (a fixed integer hash picks the offset), so that sampling does not lock
@@ -126,43 +133,97 @@ __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t x, int m)
     return ((uint64_t)hi << 32) | lo;
 }
 
-__device__ __forceinline__ bool pair_less(uint64_t ka, uint32_t ja, uint64_t kb, uint32_t jb)
+__device__ __forceinline__ bool key_less(uint64_t a1, uint64_t a2, uint32_t ja, uint64_t b1, uint64_t b2,
+                                         uint32_t jb)
 {
-    return ka < kb || (ka == kb && ja < jb);
+    return a1 < b1 || (a1 == b1 && (a2 < b2 || (a2 == b2 && ja < jb)));
 }
 
+// The sort key (k1, k2) of request i, and the per-request key output (the
+// policy's primary key; the Weighted round number is written later). The
+// aged score rounds each operation separately (no fused multiply-add). Only
+// loads and arithmetic: a caller that unrolls several requests gets all
+// their loads in flight before the first use.
 template <SortKind K>
-__device__ __forceinline__ void sample_body(const SsBatch &b, const SsDesc &d, uint64_t *sk, uint32_t *sj)
+__device__ __forceinline__ void ss_key(const SortInput &in, uint32_t i, uint64_t &k1, uint64_t &k2, double &kv)
+{
+    const double a = in.arrival[i];
+    if constexpr (K == SortKind::Fifo) {
+        kv = a;
+        k1 = ordered_bits(a);
+        k2 = 0;
+    } else if constexpr (K == SortKind::Budget) {
+        kv = in.budget[i];
+        k1 = ordered_bits(kv);
+        k2 = ordered_bits(a);
+    } else {
+        uint32_t q = in.tier[i];
+        q = q < kQ ? q : kQ - 1u;
+        k2 = ordered_bits(a);
+        if constexpr (K == SortKind::Aging) {
+            double w = in.t_now - a;
+            if (w < 0.0) w = 0.0;
+            const double d = in.aging_rate * w;
+            double e = in.prio[q] - d;
+            if (e < in.aging_floor) e = in.aging_floor;
+            kv = e;
+            k1 = ordered_bits(e);
+        } else if constexpr (K == SortKind::Class) {
+            kv = in.prio[q];
+            k1 = ordered_bits((double)in.cls[q]);
+        } else {   // Tier
+            kv = 0.0;
+            k1 = ordered_bits((double)q);
+        }
+    }
+}
+
+// Run `body` with the sort kind as a compile-time constant.
+template <typename F>
+__device__ __forceinline__ void with_kind(SortKind kind, F &&body)
+{
+    switch (kind) {
+    case SortKind::Fifo: body(std::integral_constant<SortKind, SortKind::Fifo>()); break;
+    case SortKind::Class: body(std::integral_constant<SortKind, SortKind::Class>()); break;
+    case SortKind::Tier: body(std::integral_constant<SortKind, SortKind::Tier>()); break;
+    case SortKind::Budget: body(std::integral_constant<SortKind, SortKind::Budget>()); break;
+    default: body(std::integral_constant<SortKind, SortKind::Aging>()); break;
+    }
+}
+
+struct SmpShared {
+    uint64_t k1[kSamples];
+    uint64_t k2[kSamples];
+    uint32_t j[kSamples];
+    uint32_t tw[(kSmpTPB / 64) * kQ];
+};
+
+template <SortKind K>
+__device__ __forceinline__ void sample_body(const SsBatch &b, const SsDesc &d, SmpShared &sh)
 {
     const uint32_t t = threadIdx.x, n = b.n, S = b.ns;
     const uint32_t stride = b.nsb * kSmpTPB;
     for (uint32_t i = blockIdx.x * kSmpTPB + t; i < b.tiles * 256u; i += stride) d.status[i] = 0;
     if (blockIdx.x == 0 && t == 0) d.ctl->overflow = b.serial;
-    if (blockIdx.y == 0) {
-        for (uint32_t i = blockIdx.x * kSmpTPB + t; i < b.side.clear_words; i += stride) b.side.clear[i] = 0;
-        if (b.side.tier_part)
-            tier_partial<kSmpTPB>(b.in.tier, n, blockIdx.x, b.nsb, b.side.tier_part,
-                                  reinterpret_cast<uint32_t *>(sk));
-        __syncthreads();   // sk is reused below
-    }
     {
-        // all gathers in flight before the first LDS store
+        // all loads in flight before the first LDS store
         constexpr int kPer = kSamples / kSmpTPB;
-        double kv[kPer];
+        uint64_t k1[kPer], k2[kPer];
         uint32_t j[kPer];
 #pragma unroll
         for (int r = 0; r < kPer; r++) {
             const uint32_t s = (uint32_t)r * kSmpTPB + t;
             j[r] = s < S ? sample_pos(s, n, S) : 0u;
-            uint32_t v;
-            kv[r] = primary_key<K>(b.in, n, j[r], v);
+            double kv;
+            ss_key<K>(b.in, j[r], k1[r], k2[r], kv);
         }
 #pragma unroll
         for (int r = 0; r < kPer; r++) {
-            // unused slots hold the largest pair, below no sample
+            // unused slots hold the largest triple, below no sample
             const uint32_t s = (uint32_t)r * kSmpTPB + t;
-            sk[s] = s < S ? ordered_bits(kv[r]) : ~0ull;
-            sj[s] = s < S ? j[r] : ~0u;
+            sh.k1[s] = s < S ? k1[r] : ~0ull;
+            sh.k2[s] = s < S ? k2[r] : ~0ull;
+            sh.j[s] = s < S ? j[r] : ~0u;
         }
     }
     __syncthreads();
@@ -173,20 +234,21 @@ __device__ __forceinline__ void sample_body(const SsBatch &b, const SsDesc &d, u
     uint32_t below = 0;
     {
         const uint32_t sc = s < S ? s : 0u;
-        const uint64_t ks = sk[sc];
-        const uint32_t js = sj[sc];
+        const uint64_t a1 = sh.k1[sc], a2 = sh.k2[sc];
+        const uint32_t ja = sh.j[sc];
         uint32_t part[8] = {0, 0, 0, 0, 0, 0, 0, 0};
         const uint32_t Sp = (S + 8 * kSmpThr - 1) / (8 * kSmpThr) * (8 * kSmpThr);   // <= kSamples
         for (uint32_t u0 = 0; u0 < Sp; u0 += 8 * kSmpThr) {
-            uint64_t ku[8];
+            uint64_t u1[8], u2[8];
             uint32_t ju[8];
 #pragma unroll
             for (uint32_t e = 0; e < 8; e++) {
-                ku[e] = sk[u0 + e * kSmpThr + q];
-                ju[e] = sj[u0 + e * kSmpThr + q];
+                u1[e] = sh.k1[u0 + e * kSmpThr + q];
+                u2[e] = sh.k2[u0 + e * kSmpThr + q];
+                ju[e] = sh.j[u0 + e * kSmpThr + q];
             }
 #pragma unroll
-            for (uint32_t e = 0; e < 8; e++) part[e] += pair_less(ku[e], ju[e], ks, js) ? 1u : 0u;
+            for (uint32_t e = 0; e < 8; e++) part[e] += key_less(u1[e], u2[e], ju[e], a1, a2, ja) ? 1u : 0u;
         }
 #pragma unroll
         for (uint32_t e = 0; e < 8; e++) below += part[e];
@@ -194,52 +256,41 @@ __device__ __forceinline__ void sample_body(const SsBatch &b, const SsDesc &d, u
 #pragma unroll
     for (int m = kSmpThr / 2; m >= 1; m >>= 1) below += (uint32_t)__shfl_xor((int)below, m, 64);
     if (s < S && q == 0) {
-        d.smp_k[below] = sk[s];
-        d.smp_j[below] = sj[s];
+        d.smp_k1[below] = sh.k1[s];
+        d.smp_k2[below] = sh.k2[s];
+        d.smp_j[below] = sh.j[s];
     }
 }
 
 __global__ __launch_bounds__(kSmpTPB) void k_ss_sample(SsBatch b)
 {
-    __shared__ uint64_t sk[kSamples];
-    __shared__ uint32_t sj[kSamples];
-    if (blockIdx.y >= b.nsorts) {
-        // a Priority/Weighted tile; these rows come after every sampling
-        // block in dispatch order, so their look-back waits only on tiles
-        // dispatched before them
-        if (blockIdx.x < b.part.tiles) part_body<kSmpTPB>(b.part, blockIdx.y - b.nsorts, blockIdx.x);
-        return;
-    }
-    if (blockIdx.x >= b.nsb) return;
+    __shared__ SmpShared sh;
+    if (blockIdx.y == 0 && b.tier_part)
+        tier_partial<kSmpTPB>(b.in.tier, b.n, blockIdx.x, b.nsb, b.tier_part, sh.tw);
     const SsDesc &d = b.s[blockIdx.y];
-    switch (d.kind) {
-    case SortKind::Fifo: sample_body<SortKind::Fifo>(b, d, sk, sj); break;
-    case SortKind::Budget: sample_body<SortKind::Budget>(b, d, sk, sj); break;
-    default: sample_body<SortKind::Aging>(b, d, sk, sj); break;
-    }
+    with_kind(d.kind, [&](auto K) { sample_body<decltype(K)::value>(b, d, sh); });
 }
 
-// The pairs of this thread's kScR positions of the tile (loads first, then
-// the per-request key output).
+// The keys of this thread's kScR requests of the tile (loads first, then the
+// per-request key output).
 template <SortKind K>
 __device__ __forceinline__ void scatter_keys(const SsBatch &b, const SsDesc &d, uint32_t base, uint32_t cnt,
-                                             uint64_t *k, uint32_t *jj, uint32_t *vv)
+                                             uint64_t *k1, uint64_t *k2, uint32_t *jj)
 {
-    const uint32_t n = b.n;
     const int w = (int)(threadIdx.x >> 6), lane = lane_id();
     double kv[kScR];
 #pragma unroll
     for (int r = 0; r < kScR; r++) {
         const uint32_t idx = (uint32_t)w * (64u * kScR) + (uint32_t)r * 64u + (uint32_t)lane;
-        jj[r] = base + idx;
-        vv[r] = 0;
-        kv[r] = idx < cnt ? primary_key<K>(b.in, n, base + idx, vv[r]) : 0.0;
+        jj[r] = base + (idx < cnt ? idx : 0u);
+        ss_key<K>(b.in, jj[r], k1[r], k2[r], kv[r]);
     }
+    if (K != SortKind::Tier && d.key_out) {
 #pragma unroll
-    for (int r = 0; r < kScR; r++) {
-        const uint32_t idx = (uint32_t)w * (64u * kScR) + (uint32_t)r * 64u + (uint32_t)lane;
-        k[r] = ordered_bits(kv[r]);
-        if (d.key_out && idx < cnt) d.key_out[K == SortKind::Fifo ? base + idx : vv[r]] = kv[r];
+        for (int r = 0; r < kScR; r++) {
+            const uint32_t idx = (uint32_t)w * (64u * kScR) + (uint32_t)r * 64u + (uint32_t)lane;
+            if (idx < cnt) d.key_out[base + idx] = kv[r];
+        }
     }
 }
 
@@ -247,13 +298,15 @@ __global__ __launch_bounds__(kScTPB) void k_ss_scatter(SsBatch b)
 {
     constexpr int kWaves = kScTPB / 64;
     constexpr uint32_t kWaveKeys = 64u * kScR;
-    __shared__ uint64_t s_sk[kMaxBuckets];   // [1, 2^hgt): the search tree
-    __shared__ uint32_t s_sj[kMaxBuckets];
+    __shared__ uint64_t s_k1[kMaxBuckets];   // [1, 2^hgt): the search tree
+    __shared__ uint64_t s_k2[kMaxBuckets];
+    __shared__ uint32_t s_j[kMaxBuckets];
     __shared__ uint32_t wcnt[kWaves][256];
     __shared__ uint32_t texcl[256];
     __shared__ uint32_t gbase[256];
     __shared__ uint32_t tmp4[4];
-    __shared__ uint64_t lkey[kScTile];
+    __shared__ uint64_t lk1[kScTile];
+    __shared__ uint64_t lk2[kScTile];
     __shared__ uint32_t lj[kScTile];
     __shared__ uint8_t lb[kScTile];
 
@@ -264,52 +317,51 @@ __global__ __launch_bounds__(kScTPB) void k_ss_scatter(SsBatch b)
     const uint32_t cnt = n - base < kScTile ? n - base : kScTile;
     const bool digit_thread = t < 256;
 
-    uint64_t k[kScR];
-    uint32_t jj[kScR], vv[kScR], bk[kScR], rk[kScR];
-    switch (d.kind) {
-    case SortKind::Fifo: scatter_keys<SortKind::Fifo>(b, d, base, cnt, k, jj, vv); break;
-    case SortKind::Budget: scatter_keys<SortKind::Budget>(b, d, base, cnt, k, jj, vv); break;
-    default: scatter_keys<SortKind::Aging>(b, d, base, cnt, k, jj, vv); break;
-    }
+    uint64_t k1[kScR], k2[kScR];
+    uint32_t jj[kScR], bk[kScR], rk[kScR];
+    with_kind(d.kind, [&](auto K) { scatter_keys<decltype(K)::value>(b, d, base, cnt, k1, k2, jj); });
     // splitters in breadth-first (Eytzinger) order of a complete search tree
     // of height hgt: node e (1-based) holds the splitter of in-order index
     // (2 p + 1) 2^(hgt - d - 1) - 1 (d = depth of e, p = e - 2^d); splitter i
     // is the sample of rank floor((i + 1) S / B), and in-order indices from
-    // B - 1 on are padded with the largest pair. The first levels of every
+    // B - 1 on are padded with the largest triple. The first levels of every
     // search then read the same few LDS words in all lanes.
     uint32_t hgt = 0;
     while ((1u << hgt) < b.nb) hgt++;
     for (uint32_t e = t + 1; e < (1u << hgt); e += kScTPB) {
         const uint32_t dpt = 31u - (uint32_t)__clz((int)e), pp = e - (1u << dpt);
         const uint32_t i = (2u * pp + 1u) * (1u << (hgt - dpt - 1u)) - 1u;
-        uint64_t kk = ~0ull;
+        uint64_t a1 = ~0ull, a2 = ~0ull;
         uint32_t jv = ~0u;
         if (i < nsp) {
             const uint32_t r = (i + 1) * b.ns / b.nb;   // < ns; (i + 1) ns < 2^19
-            kk = d.smp_k[r];
+            a1 = d.smp_k1[r];
+            a2 = d.smp_k2[r];
             jv = d.smp_j[r];
         }
-        s_sk[e] = kk;
-        s_sj[e] = jv;
+        s_k1[e] = a1;
+        s_k2[e] = a2;
+        s_j[e] = jv;
     }
     for (uint32_t i = t; i < kWaves * 256u; i += kScTPB) (&wcnt[0][0])[i] = 0;
     __syncthreads();   // splitters and counters ready
-    // bucket = number of splitters <= (key, j): hgt steps down the tree
+    // bucket = number of splitters <= (k1, k2, i): hgt steps down the tree
     // (the rounds advance together, so that their LDS reads overlap)
     uint32_t node[kScR];
 #pragma unroll
     for (int r = 0; r < kScR; r++) node[r] = 1;
     for (uint32_t lvl = 0; lvl < hgt; lvl++) {
-        uint64_t sk_[kScR];
-        uint32_t sj_[kScR];
+        uint64_t a1[kScR], a2[kScR];
+        uint32_t aj[kScR];
 #pragma unroll
         for (int r = 0; r < kScR; r++) {
-            sk_[r] = s_sk[node[r]];
-            sj_[r] = s_sj[node[r]];
+            a1[r] = s_k1[node[r]];
+            a2[r] = s_k2[node[r]];
+            aj[r] = s_j[node[r]];
         }
 #pragma unroll
         for (int r = 0; r < kScR; r++)
-            node[r] = 2u * node[r] + (pair_less(k[r], jj[r], sk_[r], sj_[r]) ? 0u : 1u);
+            node[r] = 2u * node[r] + (key_less(k1[r], k2[r], jj[r], a1[r], a2[r], aj[r]) ? 0u : 1u);
     }
 #pragma unroll
     for (int r = 0; r < kScR; r++) bk[r] = node[r] - (1u << hgt);
@@ -357,8 +409,9 @@ __global__ __launch_bounds__(kScTPB) void k_ss_scatter(SsBatch b)
         if (idx < cnt) {
             const uint32_t dg = bk[r];
             const uint32_t lp = texcl[dg] + wcnt[w][dg] + rk[r];
-            lkey[lp] = k[r];
-            lj[lp] = vv[r];
+            lk1[lp] = k1[r];
+            lk2[lp] = k2[r];
+            lj[lp] = jj[r];
             lb[lp] = (uint8_t)dg;
         }
     }
@@ -368,53 +421,96 @@ __global__ __launch_bounds__(kScTPB) void k_ss_scatter(SsBatch b)
         const uint32_t dg = lb[s];
         const uint32_t g = gbase[dg] + s - texcl[dg];
         if (g < kCap) {
-            d.bkey[(uint64_t)dg * kCap + g] = lkey[s];
-            d.bj[(uint64_t)dg * kCap + g] = lj[s];
+            const uint64_t o = (uint64_t)dg * kCap + g;
+            d.bk1[o] = lk1[s];
+            if (d.two) d.bk2[o] = lk2[s];
+            d.bj[o] = lj[s];
         } else {
             over = true;
         }
     }
     if (over) atomicOr(&d.ctl->overflow, 1u);
-}
-
-// Output position pos of a sort holds val; the FIFO sort can also write the
-// request's tier, budget and arrival at pos (the copies in FIFO order that
-// the sorts after it read instead of gathering).
-__device__ __forceinline__ void emit(const SsBatch &b, const SsDesc &d, uint32_t pos, uint32_t val)
-{
-    d.out[pos] = val;
-    if (d.kind == SortKind::Fifo) {
-        const uint32_t i = val < b.n ? val : 0u;
-        if (b.side.ftier) b.side.ftier[pos] = b.in.tier[i];
-        if (b.side.fbudget) b.side.fbudget[pos] = b.in.budget[i];
-        if (b.side.farr) b.side.farr[pos] = b.in.arrival[i];
+    if (d.kind == SortKind::Tier && tile == 0) {
+        // requests per tier (for the round-robin positions): the sum of the
+        // slices' counts, after this tile's look-back word is out
+        __syncthreads();
+        if (t < kQ) texcl[t] = 0;
+        __syncthreads();
+        for (uint32_t i = t; i < b.nsb * kQ; i += kScTPB) {
+            const uint32_t c = b.tier_part[i];
+            if (c) atomicAdd(&texcl[i % kQ], c);
+        }
+        __syncthreads();
+        if (t < kQ) d.tot[t] = texcl[t];
     }
 }
 
+// Requests per tier and the first sorted position of each tier, for the
+// round-robin positions of a Tier sort.
+struct TierTable {
+    uint32_t tot[kQ];
+    uint32_t start[kQ];
+};
+
+// Output position pos of the sorted sequence holds request j: the request
+// goes there, or, for Weighted, to the round-robin position of its rank
+// within its tier.
+__device__ __forceinline__ void emit(const SsBatch &b, const SsDesc &d, const TierTable &tt, uint32_t pos,
+                                     uint32_t j)
+{
+    if (d.kind != SortKind::Tier) {
+        d.out[pos] = j;
+        return;
+    }
+    const SortInput &in = b.in;
+    uint32_t q = in.tier[j];
+    q = q < kQ ? q : kQ - 1u;
+    const uint32_t k = pos - tt.start[q];   // rank within the tier
+    const uint32_t wq = in.weight[q] ? in.weight[q] : 1u;
+    const uint32_t rnd = k / wq;
+    uint64_t p = k - rnd * wq;
+    for (uint32_t u = 0; u < in.n_tiers; u++) {
+        const uint64_t nt = tt.tot[u], wt = in.weight[u], full = (uint64_t)rnd * wt;
+        p += nt < full ? nt : full;
+        if (u < q) {
+            const uint64_t left = nt > full ? nt - full : 0u;
+            p += left < wt ? left : wt;
+        }
+    }
+    if (p < b.n) d.out[p] = j;   // always, for tiers < n_tiers
+    if (d.key_out) d.key_out[j] = (double)rnd;
+}
+
 // LDS scratch of the bucket sort (also used by the single-workgroup sort).
+// The bin histogram and the LSD digit counters are never live together and
+// share their words, so that two blocks fit a CU.
 struct BkShared {
-    uint32_t wcnt[2][kBkTPB / 64][256];   // per-wave digit counters, two passes' worth
+    union {
+        uint32_t bin[kBins + 1];              // bin histogram, then bin starts
+        uint32_t wcnt[2][kBkTPB / 64][256];   // per-wave digit counters, two passes' worth
+    };
     uint32_t texcl[256];
     uint32_t dcnt[256];
     uint32_t offs[256];
     uint32_t tmp4[4];
-    uint64_t red[kBkTPB / 64];
     uint32_t redu[kBkTPB / 64];
     uint32_t wsum[kBkTPB / 64];
     uint32_t wmax[kBkTPB / 64];
     uint64_t kmin[kBkTPB / 64], kmax[kBkTPB / 64], kmin2[kBkTPB / 64];
-    uint32_t bin[kBins + 1];              // bin histogram, then bin starts
+    uint64_t kmin1[kBkTPB / 64], kmax1[kBkTPB / 64];
+    TierTable tt;
     uint64_t lkey[kCap];
     uint32_t lj[kCap];
     uint16_t lslot[kCap];
 };
 
-// One stable LSD pass on byte p of the keys of m pairs held R_eff per thread
-// (wave-major positions w * 64 R_eff + r * 64 + lane): returns each pair's
-// place in the pass order through pos, leaves the digits' exclusive starts in
-// sh.texcl and, for thread t < 256, digit t's count in tc. Counters buffer
-// `cur` must be zero on entry; buffer cur ^ 1 is cleared for the next pass.
-// Ends with a barrier; the caller's reads of pos-ordered data need another.
+// One stable LSD pass on byte p of the keys of m entries held R_eff per
+// thread (wave-major positions w * 64 R_eff + r * 64 + lane): returns each
+// entry's place in the pass order through pos, leaves the digits' exclusive
+// starts in sh.texcl and, for thread t < 256, digit t's count in tc. Counters
+// buffer `cur` must be zero on entry; buffer cur ^ 1 is cleared for the next
+// pass. Ends with a barrier; the caller's reads of pos-ordered data need
+// another.
 __device__ __forceinline__ void lds_rank(BkShared &sh, uint32_t cur, const uint64_t *k, uint32_t reff,
                                          uint32_t m, uint32_t p, uint32_t *pos, uint32_t &tc)
 {
@@ -481,179 +577,104 @@ __device__ __forceinline__ void lds_rank(BkShared &sh, uint32_t cur, const uint6
     }
 }
 
-// The whole sequence sorted by one workgroup: LSD passes over global
-// ping-pong buffers, in chunks of kCap pairs taken in order.
-__device__ void serial_sort(const SsBatch &b, const SsDesc &d, BkShared &sh)
-{
-    const uint32_t n = b.n, t = threadIdx.x;
-    const int w = (int)(t >> 6), lane = lane_id();
-    for (uint32_t i = t; i < 2u * (kBkTPB / 64) * 256u; i += kBkTPB) (&sh.wcnt[0][0][0])[i] = 0;
-    uint32_t cur = 0;
-    for (uint32_t j = t; j < n; j += kBkTPB) {
-        uint64_t k;
-        uint32_t v;
-        produce(b.in, d.kind, nullptr, n, j, k, v);
-        d.fkey[0][j] = k;
-        d.fj[0][j] = j;
-    }
-    __syncthreads();
-    uint32_t src = 0;
-    for (uint32_t p = 0; p < 8; p++) {
-        // digit histogram; a pass whose digit is the same for all keys is skipped
-        if (t < 256) sh.offs[t] = 0;
-        __syncthreads();
-        for (uint32_t j = t; j < n; j += kBkTPB)
-            atomicAdd(&sh.offs[(uint32_t)(d.fkey[src][j] >> (8 * p)) & 255u], 1u);
-        __syncthreads();
-        const uint32_t h = t < 256 ? sh.offs[t] : 0u;
-        const int constant = __syncthreads_or(t < 256 && h == n);
-        if (constant) continue;
-        const uint32_t ex = block_excl_scan_digits<kBkTPB>(h, sh.tmp4);
-        if (t < 256) sh.offs[t] = ex;
-        __syncthreads();
-        for (uint32_t c0 = 0; c0 < n; c0 += kCap) {
-            const uint32_t m = n - c0 < kCap ? n - c0 : kCap;
-            const uint32_t reff = (m + kBkTPB - 1) / kBkTPB;
-            const uint32_t wk = 64u * reff;
-            uint64_t k[kBkR];
-            uint32_t jv[kBkR], pos[kBkR];
-#pragma unroll
-            for (int r = 0; r < kBkR; r++) {
-                const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
-                k[r] = 0;
-                jv[r] = 0;
-                if ((uint32_t)r < reff && idx < m) {
-                    k[r] = d.fkey[src][c0 + idx];
-                    jv[r] = d.fj[src][c0 + idx];
-                }
-            }
-            uint32_t tc;
-            lds_rank(sh, cur, k, reff, m, p, pos, tc);
-            cur ^= 1u;
-#pragma unroll
-            for (int r = 0; r < kBkR; r++) {
-                const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
-                if ((uint32_t)r < reff && idx < m) {
-                    const uint32_t dg = (uint32_t)(k[r] >> (8 * p)) & 255u;
-                    // rank in the chunk minus the chunk's digit start, plus
-                    // the digit's running offset
-                    const uint32_t g = sh.offs[dg] + pos[r] - sh.texcl[dg];
-                    d.fkey[src ^ 1u][g] = k[r];
-                    d.fj[src ^ 1u][g] = jv[r];
-                }
-            }
-            __syncthreads();
-            if (t < 256) sh.offs[t] += tc;
-            __syncthreads();
-        }
-        src ^= 1u;
-    }
-    for (uint32_t i = t; i < n; i += kBkTPB) emit(b, d, i, value_of(b.in, d.kind, n, d.fj[src][i]));
-}
-
-__global__ __launch_bounds__(kBkTPB) void k_ss_bucket(SsBatch b)
+// Key ranges of the m entries of a bucket: of k, and of k2 when given
+// (every thread gets them). Ends with a barrier.
+__device__ __forceinline__ void block_range(BkShared &sh, const uint64_t *k, const uint64_t *k2, uint32_t reff,
+                                            uint32_t m, uint64_t &kmn, uint64_t &kmx, uint64_t &kmn2,
+                                            uint64_t &kmx2)
 {
     constexpr int kWaves = kBkTPB / 64;
-    __shared__ BkShared sh;
-    const SsDesc &d = b.s[blockIdx.y];
-    const uint32_t t = threadIdx.x, bkt = blockIdx.x, n = b.n;
-    const int w = (int)(t >> 6), lane = lane_id();
-    if (ld_relaxed(&d.ctl->overflow)) {
-        if (bkt == 0) serial_sort(b, d, sh);
-        return;
-    }
-    for (uint32_t i = t; i < 2u * kWaves * 256u; i += kBkTPB) (&sh.wcnt[0][0][0])[i] = 0;
-    const uint64_t *src_k = d.bkey + (uint64_t)bkt * kCap;
-    const uint32_t *src_j = d.bj + (uint64_t)bkt * kCap;
-    // the first kBkTPB slots are loaded before the size is known (a bucket
-    // of at most kBkTPB pairs, the common case, needs no other load)
-    const uint64_t k0 = src_k[t];
-    const uint32_t j0 = src_j[t];
-    // bucket sizes: the last tile's inclusive prefixes
-    const uint32_t *last = d.status + (uint64_t)(b.tiles - 1) * 256u;
-    const uint32_t c = t < b.nb ? (last[t] & kValMask) : 0u;
-    uint32_t before = wave_sum(t < bkt ? c : 0u);
-    if (lane == 0) sh.redu[w] = before;
-    if (t == bkt) sh.offs[0] = c;
-    __syncthreads();
-    uint32_t off = 0;
-#pragma unroll
-    for (int q = 0; q < kWaves; q++) off += sh.redu[q];
-    const uint32_t m = sh.offs[0];   // <= kCap: no region overflowed
-    const uint32_t reff = (m + kBkTPB - 1) / kBkTPB;
+    const int w = (int)(threadIdx.x >> 6), lane = lane_id();
     const uint32_t wk = 64u * reff;
-
-    uint64_t k[kBkR];
-    uint32_t jv[kBkR], pos[kBkR];
-    uint64_t kmn = ~0ull, kmx = 0;
+    kmn = ~0ull;
+    kmx = 0;
+    kmn2 = ~0ull;
+    kmx2 = 0;
 #pragma unroll
     for (int r = 0; r < kBkR; r++) {
         const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
-        k[r] = 0;
-        jv[r] = 0;
         if ((uint32_t)r < reff && idx < m) {
-            if (reff == 1) {
-                k[r] = k0;
-                jv[r] = j0;
-            } else {
-                k[r] = src_k[idx];
-                jv[r] = src_j[idx];
-            }
             kmn = k[r] < kmn ? k[r] : kmn;
             kmx = k[r] > kmx ? k[r] : kmx;
+            if (k2) {
+                kmn2 = k2[r] < kmn2 ? k2[r] : kmn2;
+                kmx2 = k2[r] > kmx2 ? k2[r] : kmx2;
+            }
         }
     }
-    // key range of the bucket
 #pragma unroll
     for (int sft = 32; sft >= 1; sft >>= 1) {
-        const uint64_t a = shfl_xor_u64(kmn, sft), c2 = shfl_xor_u64(kmx, sft);
+        uint64_t a = shfl_xor_u64(kmn, sft), c2 = shfl_xor_u64(kmx, sft);
         kmn = a < kmn ? a : kmn;
         kmx = c2 > kmx ? c2 : kmx;
+        if (k2) {
+            a = shfl_xor_u64(kmn2, sft);
+            c2 = shfl_xor_u64(kmx2, sft);
+            kmn2 = a < kmn2 ? a : kmn2;
+            kmx2 = c2 > kmx2 ? c2 : kmx2;
+        }
     }
     if (lane == 0) {
         sh.kmin[w] = kmn;
         sh.kmax[w] = kmx;
+        sh.kmin1[w] = kmn2;
+        sh.kmax1[w] = kmx2;
     }
-    for (uint32_t i = t; i <= kBins; i += kBkTPB) sh.bin[i] = 0;
     __syncthreads();
 #pragma unroll
     for (int q = 0; q < kWaves; q++) {
         kmn = sh.kmin[q] < kmn ? sh.kmin[q] : kmn;
         kmx = sh.kmax[q] > kmx ? sh.kmax[q] : kmx;
+        kmn2 = sh.kmin1[q] < kmn2 ? sh.kmin1[q] : kmn2;
+        kmx2 = sh.kmax1[q] > kmx2 ? sh.kmax1[q] : kmx2;
     }
+}
+
+// Rank pass: the place rank[r] of each of the m entries (entry idx =
+// w * 64 R_eff + r * 64 + lane) in the order of key k, ties in entry order;
+// kmn, kmx: the keys' range. Every thread of the block calls it; sh.bin,
+// sh.lkey, sh.lj and sh.lslot are used, and k is left in an unspecified
+// order.
+//
+// Entries with the smallest key (the common heavy tie: aged scores clamped to
+// the floor, or the lowest class of a bucket) come first, in entry order:
+// their rank is the number of such entries before them, from ballots. The
+// others go to bins, monotone in the key, over the range [x2, xmax] of the
+// keys above the minimum: for a finite range, kBins equal intervals
+// ((x - x2) * (kBins / (xmax - x2)), each step rounded, so monotone);
+// otherwise the kBinBits bits of key - key2 below its highest varying bit.
+// Their rank = entries at the minimum + bin start + rank inside the bin by
+// (key, entry). A bin of more than kBinMax entries sends the whole bucket
+// through stable LSD passes on the key bytes that vary in it instead.
+__device__ __forceinline__ void rank_pass(BkShared &sh, uint64_t *k, uint32_t reff, uint32_t m, uint64_t kmn, uint64_t kmx,
+                          uint32_t *rank)
+{
+    constexpr int kWaves = kBkTPB / 64;
+    const uint32_t t = threadIdx.x;
+    const int w = (int)(t >> 6), lane = lane_id();
+    const uint32_t wk = 64u * reff;
     if (kmn >= kmx) {
-        // one key (or an empty bucket): position order is the order
+        // one key (or no entry): entry order is the order
 #pragma unroll
-        for (int r = 0; r < kBkR; r++) {
-            const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
-            if ((uint32_t)r < reff && idx < m && off + idx < n) emit(b, d, off + idx, jv[r]);
-        }
+        for (int r = 0; r < kBkR; r++) rank[r] = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
         return;
     }
-    // Pairs with the bucket's smallest key (the common heavy tie: aged
-    // scores clamped to the floor) come first, in position order: their rank
-    // is the number of such pairs at lower slots, from ballots. The others
-    // go to bins, monotone in the key, over the range [x2, xmax] of the keys
-    // above the minimum: for a finite range, kBins equal intervals
-    // ((x - x2) * (kBins / (xmax - x2)), each step rounded, so monotone);
-    // otherwise the kBinBits bits of key - key2 below its highest varying
-    // bit. Their rank = pairs at the minimum + bin start + rank inside the
-    // bin by (key, slot), the slot being the position order.
-    uint32_t lowrank[kBkR], hirank[kBkR];
+    for (uint32_t i = t; i <= kBins; i += kBkTPB) sh.bin[i] = 0;
+    // rank[r] first holds the number of minimum-key entries before entry r
+    // (its rank if it has the minimum key; the valid entries are a prefix,
+    // so entry idx has idx - rank[r] entries above the minimum before it)
     uint32_t nlow;
     uint64_t kmn2 = ~0ull;   // smallest key above the minimum
     {
-        uint32_t run = 0, runh = 0;
+        uint32_t run = 0;
 #pragma unroll
         for (int r = 0; r < kBkR; r++) {
             const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
             const bool valid = (uint32_t)r < reff && idx < m;
             const bool low = valid && k[r] == kmn;
-            const uint64_t bl = __ballot(low), bh = __ballot(valid && !low);
-            lowrank[r] = run + (uint32_t)__popcll(bl & lanemask_lt());
-            hirank[r] = runh + (uint32_t)__popcll(bh & lanemask_lt());
+            const uint64_t bl = __ballot(low);
+            rank[r] = run + (uint32_t)__popcll(bl & lanemask_lt());
             run += (uint32_t)__popcll(bl);
-            runh += (uint32_t)__popcll(bh);
             if (valid && !low && k[r] < kmn2) kmn2 = k[r];
         }
 #pragma unroll
@@ -663,60 +684,52 @@ __global__ __launch_bounds__(kBkTPB) void k_ss_bucket(SsBatch b)
         }
         if (lane == 0) {
             sh.wsum[w] = run;
-            sh.wmax[w] = runh;
             sh.kmin2[w] = kmn2;
         }
         __syncthreads();
-        uint32_t before_w = 0, before_h = 0;
+        uint32_t before_w = 0;
         nlow = 0;
 #pragma unroll
         for (int q = 0; q < kWaves; q++) {
             before_w += q < w ? sh.wsum[q] : 0u;
-            before_h += q < w ? sh.wmax[q] : 0u;
             nlow += sh.wsum[q];
             kmn2 = sh.kmin2[q] < kmn2 ? sh.kmin2[q] : kmn2;
         }
 #pragma unroll
-        for (int r = 0; r < kBkR; r++) {
-            lowrank[r] += before_w;
-            hirank[r] += before_h;
-        }
-        __syncthreads();   // sh.wsum, sh.wmax are reused by the bin scan
+        for (int r = 0; r < kBkR; r++) rank[r] += before_w;
+        __syncthreads();   // sh.wsum is reused by the bin scan
     }
     if (kmn2 >= kmx) {
-        // two distinct keys: each in position order
+        // two distinct keys: each in entry order
 #pragma unroll
         for (int r = 0; r < kBkR; r++) {
             const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
-            if ((uint32_t)r < reff && idx < m) {
-                const uint32_t rank = k[r] == kmn ? lowrank[r] : nlow + hirank[r];
-                if (off + rank < n) emit(b, d, off + rank, jv[r]);
-            }
+            if (k[r] != kmn) rank[r] = nlow + (idx - rank[r]);
         }
         return;
     }
-    // bins over [kmn2, kmx] for the pairs above the minimum
+    // bins over [kmn2, kmx] for the entries above the minimum
     const int hb = 63 - __clzll((long long)(kmn2 ^ kmx));
     const uint32_t shift = hb >= (int)kBinBits ? (uint32_t)hb - (kBinBits - 1u) : 0u;
     const double xmn = from_ordered(kmn2), xmx = from_ordered(kmx);
     const double span = xmx - xmn;
     const bool linear = isfinite(span) && span > 0.0 && isfinite((double)kBins / span);
     const double scale = linear ? (double)kBins / span : 0.0;
-    uint32_t dg[kBkR], bs[kBkR];
+    // bin (low kBinBits bits) and slot in the bin (above them) of each entry
+    uint32_t db[kBkR];
 #pragma unroll
     for (int r = 0; r < kBkR; r++) {
         const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
-        dg[r] = 0;
-        bs[r] = 0;
+        db[r] = 0;
         if ((uint32_t)r < reff && idx < m && k[r] != kmn) {
+            uint32_t q;
             if (linear) {
                 const double f = (from_ordered(k[r]) - xmn) * scale;   // in [0, kBins]
-                const uint32_t q = f < (double)kBins ? (uint32_t)f : kBins - 1u;
-                dg[r] = q;
+                q = f < (double)kBins ? (uint32_t)f : kBins - 1u;
             } else {
-                dg[r] = (uint32_t)((k[r] - kmn2) >> shift);   // < kBins
+                q = (uint32_t)((k[r] - kmn2) >> shift);   // < kBins
             }
-            bs[r] = atomicAdd(&sh.bin[dg[r]], 1u);
+            db[r] = q | (atomicAdd(&sh.bin[q], 1u) << kBinBits);
         }
     }
     __syncthreads();
@@ -756,7 +769,7 @@ __global__ __launch_bounds__(kBkTPB) void k_ss_bucket(SsBatch b)
         for (int r = 0; r < kBkR; r++) {
             const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
             if ((uint32_t)r < reff && idx < m && k[r] != kmn) {
-                const uint32_t q = sh.bin[dg[r]] + bs[r];
+                const uint32_t q = sh.bin[db[r] & (kBins - 1u)] + (db[r] >> kBinBits);
                 sh.lkey[q] = k[r];
                 sh.lslot[q] = (uint16_t)idx;
             }
@@ -765,38 +778,44 @@ __global__ __launch_bounds__(kBkTPB) void k_ss_bucket(SsBatch b)
 #pragma unroll
         for (int r = 0; r < kBkR; r++) {
             const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
-            if ((uint32_t)r < reff && idx < m) {
-                uint32_t rank = lowrank[r];
-                if (k[r] != kmn) {
-                    const uint32_t s0 = sh.bin[dg[r]], s1 = sh.bin[dg[r] + 1];
-                    rank = nlow + s0;
-                    for (uint32_t u = s0; u < s1; u++) {
-                        const uint64_t ku = sh.lkey[u];
-                        rank += (ku < k[r] || (ku == k[r] && sh.lslot[u] < idx)) ? 1u : 0u;
-                    }
+            if ((uint32_t)r < reff && idx < m && k[r] != kmn) {
+                const uint32_t bn = db[r] & (kBins - 1u);
+                const uint32_t s0 = sh.bin[bn], s1 = sh.bin[bn + 1];
+                uint32_t rk = nlow + s0;
+                for (uint32_t u = s0; u < s1; u++) {
+                    const uint64_t ku = sh.lkey[u];
+                    rk += (ku < k[r] || (ku == k[r] && sh.lslot[u] < idx)) ? 1u : 0u;
                 }
-                if (off + rank < n) emit(b, d, off + rank, jv[r]);
+                rank[r] = rk;
             }
         }
+        __syncthreads();   // sh.lkey, sh.lslot are free again
         return;
     }
     // crowded bins (many equal or near-equal keys): stable LSD passes over
-    // all the pairs, on the key bytes up to the highest bit that varies in
-    // the bucket (minimum included)
+    // all the entries, on the key bytes up to the highest bit that varies in
+    // the bucket (minimum included); the entries carry their index along,
+    // and the final order gives each its rank
     const int hba = 63 - __clzll((long long)(kmn ^ kmx));
     const uint64_t diff = hba == 63 ? ~0ull : ((1ull << (hba + 1)) - 1ull);
+    for (uint32_t i = t; i < 2u * kWaves * 256u; i += kBkTPB) (&sh.wcnt[0][0][0])[i] = 0;
+    uint64_t *kk = k;
+    uint32_t slot[kBkR], pos[kBkR];
+#pragma unroll
+    for (int r = 0; r < kBkR; r++) slot[r] = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
+    __syncthreads();
     uint32_t cur = 0;
     for (uint32_t p = 0; p < 8; p++) {
         if (((diff >> (8 * p)) & 255u) == 0) continue;   // uniform
         uint32_t tc;
-        lds_rank(sh, cur, k, reff, m, p, pos, tc);
+        lds_rank(sh, cur, kk, reff, m, p, pos, tc);
         cur ^= 1u;
 #pragma unroll
         for (int r = 0; r < kBkR; r++) {
             const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
             if ((uint32_t)r < reff && idx < m) {
-                sh.lkey[pos[r]] = k[r];
-                sh.lj[pos[r]] = jv[r];
+                sh.lkey[pos[r]] = kk[r];
+                sh.lj[pos[r]] = slot[r];
             }
         }
         __syncthreads();
@@ -804,15 +823,227 @@ __global__ __launch_bounds__(kBkTPB) void k_ss_bucket(SsBatch b)
         for (int r = 0; r < kBkR; r++) {
             const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
             if ((uint32_t)r < reff && idx < m) {
-                k[r] = sh.lkey[idx];
-                jv[r] = sh.lj[idx];
+                kk[r] = sh.lkey[idx];
+                slot[r] = sh.lj[idx];
             }
         }
+        __syncthreads();
+    }
+    // entry slot[r] is now at place idx
+#pragma unroll
+    for (int r = 0; r < kBkR; r++) {
+        const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
+        if ((uint32_t)r < reff && idx < m) sh.lslot[slot[r]] = (uint16_t)idx;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < kBkR; r++) {
+        const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
+        rank[r] = (uint32_t)r < reff && idx < m ? sh.lslot[idx] : 0u;
+    }
+    __syncthreads();
+}
+
+// Requests per tier and each tier's first sorted position, into sh.tt.
+__device__ __forceinline__ void load_tiers(const SsBatch &b, const SsDesc &d, BkShared &sh)
+{
+    if (threadIdx.x < kQ) sh.tt.tot[threadIdx.x] = d.tot[threadIdx.x];
+    __syncthreads();
+    if (threadIdx.x < kQ) {
+        uint32_t s = 0;
+        for (uint32_t q = 0; q < threadIdx.x; q++) s += sh.tt.tot[q];
+        sh.tt.start[threadIdx.x] = s;
+    }
+    __syncthreads();
+}
+
+// The whole batch sorted by one workgroup: stable LSD passes over global
+// ping-pong buffers, in chunks of kCap entries taken in order; by k2 first
+// (two-key sorts), then by k1.
+__device__ __forceinline__ void serial_sort(const SsBatch &b, const SsDesc &d, BkShared &sh)
+{
+    const uint32_t n = b.n, t = threadIdx.x;
+    const int w = (int)(t >> 6), lane = lane_id();
+    for (uint32_t i = t; i < 2u * (kBkTPB / 64) * 256u; i += kBkTPB) (&sh.wcnt[0][0][0])[i] = 0;
+    uint32_t cur = 0;
+    for (uint32_t j = t; j < n; j += kBkTPB) {
+        uint64_t k1, k2;
+        double kv;
+        with_kind(d.kind, [&](auto K) { ss_key<decltype(K)::value>(b.in, j, k1, k2, kv); });
+        d.fk1[0][j] = k1;
+        d.fk2[0][j] = k2;
+        d.fj[0][j] = j;
+        if (d.key_out && d.kind != SortKind::Tier) d.key_out[j] = kv;
+    }
+    if (d.kind == SortKind::Tier) load_tiers(b, d, sh);
+    __syncthreads();
+    uint32_t src = 0;
+    for (uint32_t pass = 0; pass < 16; pass++) {
+        // bytes 0..7 of k2, then of k1; a pass whose digit is the same for
+        // all keys is skipped
+        const bool on_k1 = pass >= 8;
+        const uint32_t p = pass & 7u;
+        if (!on_k1 && !d.two) continue;
+        const uint64_t *ksrc = on_k1 ? d.fk1[src] : d.fk2[src];
+        if (t < 256) sh.offs[t] = 0;
+        __syncthreads();
+        for (uint32_t j = t; j < n; j += kBkTPB) atomicAdd(&sh.offs[(uint32_t)(ksrc[j] >> (8 * p)) & 255u], 1u);
+        __syncthreads();
+        const uint32_t h = t < 256 ? sh.offs[t] : 0u;
+        const int constant = __syncthreads_or(t < 256 && h == n);
+        if (constant) continue;
+        const uint32_t ex = block_excl_scan_digits<kBkTPB>(h, sh.tmp4);
+        if (t < 256) sh.offs[t] = ex;
+        __syncthreads();
+        for (uint32_t c0 = 0; c0 < n; c0 += kCap) {
+            const uint32_t m = n - c0 < kCap ? n - c0 : kCap;
+            const uint32_t reff = (m + kBkTPB - 1) / kBkTPB;
+            const uint32_t wk = 64u * reff;
+            uint64_t k[kBkR];
+            uint32_t pos[kBkR];
+#pragma unroll
+            for (int r = 0; r < kBkR; r++) {
+                const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
+                k[r] = (uint32_t)r < reff && idx < m ? ksrc[c0 + idx] : 0ull;
+            }
+            uint32_t tc;
+            lds_rank(sh, cur, k, reff, m, p, pos, tc);
+            cur ^= 1u;
+#pragma unroll
+            for (int r = 0; r < kBkR; r++) {
+                const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
+                if ((uint32_t)r < reff && idx < m) {
+                    const uint32_t dg = (uint32_t)(k[r] >> (8 * p)) & 255u;
+                    // rank in the chunk minus the chunk's digit start, plus
+                    // the digit's running offset
+                    const uint32_t g = sh.offs[dg] + pos[r] - sh.texcl[dg];
+                    d.fk1[src ^ 1u][g] = d.fk1[src][c0 + idx];
+                    d.fk2[src ^ 1u][g] = d.fk2[src][c0 + idx];
+                    d.fj[src ^ 1u][g] = d.fj[src][c0 + idx];
+                }
+            }
+            __syncthreads();
+            if (t < 256) sh.offs[t] += tc;
+            __syncthreads();
+        }
+        src ^= 1u;
+    }
+    for (uint32_t i = t; i < n; i += kBkTPB) {
+        const uint32_t j = d.fj[src][i];
+        emit(b, d, sh.tt, i, j < n ? j : 0u);
+    }
+}
+
+__global__ __launch_bounds__(kBkTPB) void k_ss_bucket(SsBatch b)
+{
+    constexpr int kWaves = kBkTPB / 64;
+    __shared__ BkShared sh;
+    const SsDesc &d = b.s[blockIdx.y];
+    const uint32_t t = threadIdx.x, bkt = blockIdx.x, n = b.n;
+    const int w = (int)(t >> 6), lane = lane_id();
+    if (ld_relaxed(&d.ctl->overflow)) {
+        if (bkt == 0) serial_sort(b, d, sh);
+        return;
+    }
+    const uint64_t *src1 = d.bk1 + (uint64_t)bkt * kCap;
+    const uint64_t *src2 = d.bk2 + (uint64_t)bkt * kCap;
+    const uint32_t *srcj = d.bj + (uint64_t)bkt * kCap;
+    const bool two = d.two != 0;
+    // the first kBkTPB slots are loaded before the size is known (a bucket
+    // of at most kBkTPB requests, the common case, needs no other load)
+    const uint64_t a0 = src1[t];
+    const uint64_t b0 = two ? src2[t] : 0ull;
+    const uint32_t j0 = srcj[t];
+    // bucket sizes: the last tile's inclusive prefixes
+    const uint32_t *last = d.status + (uint64_t)(b.tiles - 1) * 256u;
+    const uint32_t c = t < b.nb ? (last[t] & kValMask) : 0u;
+    const uint32_t before = wave_sum(t < bkt ? c : 0u);
+    if (lane == 0) sh.redu[w] = before;
+    if (t == bkt) sh.offs[0] = c;
+    if (d.kind == SortKind::Tier && t < kQ) sh.tt.tot[t] = d.tot[t];
+    __syncthreads();
+    uint32_t off = 0;
+#pragma unroll
+    for (int q = 0; q < kWaves; q++) off += sh.redu[q];
+    const uint32_t m = sh.offs[0];   // <= kCap: no region overflowed
+    const uint32_t reff = (m + kBkTPB - 1) / kBkTPB;
+    const uint32_t wk = 64u * reff;
+    if (d.kind == SortKind::Tier && t < kQ) {
+        uint32_t s = 0;
+        for (uint32_t q = 0; q < t; q++) s += sh.tt.tot[q];
+        sh.tt.start[t] = s;   // read after the barriers below
+    }
+
+    // the entries: index order within the bucket
+    uint64_t k[kBkR];
+    uint32_t jv[kBkR], rank[kBkR];
+    if (two) {
+        // by arrival first (ties: index order, which is entry order), then
+        // stably by k1, with the entries laid out in arrival order
+        uint64_t mn1, mx1, mn2, mx2;
+        {
+            uint64_t k1[kBkR];
+#pragma unroll
+            for (int r = 0; r < kBkR; r++) {
+                const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
+                k1[r] = 0;
+                k[r] = 0;
+                if ((uint32_t)r < reff && idx < m) {
+                    k1[r] = reff == 1 ? a0 : src1[idx];
+                    k[r] = reff == 1 ? b0 : src2[idx];
+                }
+            }
+            block_range(sh, k, k1, reff, m, mn2, mx2, mn1, mx1);
+        }
+        rank_pass(sh, k, reff, m, mn2, mx2, rank);
+        if (mn1 < mx1) {
+#pragma unroll
+            for (int r = 0; r < kBkR; r++) {
+                const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
+                if ((uint32_t)r < reff && idx < m) {
+                    sh.lkey[rank[r]] = reff == 1 ? a0 : src1[idx];
+                    sh.lj[rank[r]] = reff == 1 ? j0 : srcj[idx];
+                }
+            }
+            __syncthreads();
+#pragma unroll
+            for (int r = 0; r < kBkR; r++) {
+                const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
+                k[r] = 0;
+                jv[r] = 0;
+                if ((uint32_t)r < reff && idx < m) {
+                    k[r] = sh.lkey[idx];
+                    jv[r] = sh.lj[idx];
+                }
+            }
+            __syncthreads();
+            rank_pass(sh, k, reff, m, mn1, mx1, rank);
+        } else {
+#pragma unroll
+            for (int r = 0; r < kBkR; r++) {
+                const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
+                jv[r] = (uint32_t)r < reff && idx < m ? (reff == 1 ? j0 : srcj[idx]) : 0u;
+            }
+        }
+    } else {
+#pragma unroll
+        for (int r = 0; r < kBkR; r++) {
+            const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
+            k[r] = 0;
+            jv[r] = 0;
+            if ((uint32_t)r < reff && idx < m) {
+                k[r] = reff == 1 ? a0 : src1[idx];
+                jv[r] = reff == 1 ? j0 : srcj[idx];
+            }
+        }
+        uint64_t mn1, mx1, u0, u1;
+        block_range(sh, k, nullptr, reff, m, mn1, mx1, u0, u1);
+        rank_pass(sh, k, reff, m, mn1, mx1, rank);
     }
 #pragma unroll
     for (int r = 0; r < kBkR; r++) {
         const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
-        if ((uint32_t)r < reff && idx < m && off + idx < n) emit(b, d, off + idx, jv[r]);
+        if ((uint32_t)r < reff && idx < m && off + rank[r] < n) emit(b, d, sh.tt, off + rank[r], jv[r]);
     }
 }
 
@@ -822,13 +1053,28 @@ uint32_t n_buckets(uint64_t n)
     return (uint32_t)(b < 1 ? 1 : (b > kMaxBuckets ? kMaxBuckets : b));
 }
 
+uint32_t n_samples(uint64_t n)
+{
+    // 1024 samples (16 per bucket up to 2^16 requests, 8 up to 2^17), 2048
+    // above (8 per bucket); the average bucket is at most a quarter of the
+    // region capacity
+    const uint64_t smax = n <= (1u << 17) ? kSamples / 2 : kSamples;
+    return (uint32_t)(n < smax ? n : smax);
+}
+
+uint32_t sample_blocks(uint64_t n)
+{
+    const uint32_t ns = n_samples(n);
+    return (uint32_t)cdiv(ns ? ns : 1, kSmpPerBlock);
+}
+
 uint64_t region_bytes(uint64_t n)
 {
     const uint64_t tiles = cdiv(n, kScTile);
     const uint64_t nb = n_buckets(n);
-    return align_up(sizeof(SsCtl), 256) + align_up(kSamples * 8, 256) + align_up(kSamples * 4, 256) +
-           align_up(tiles * 256 * 4, 256) + align_up(nb * kCap * 8, 256) + align_up(nb * kCap * 4, 256) +
-           2 * align_up(n * 8, 256) + 2 * align_up(n * 4, 256);
+    return align_up(sizeof(SsCtl), 256) + 2 * align_up(kSamples * 8, 256) + align_up(kSamples * 4, 256) +
+           align_up(tiles * 256 * 4, 256) + 2 * align_up(nb * kCap * 8, 256) + align_up(nb * kCap * 4, 256) +
+           align_up(kQ * 4, 256) + 4 * align_up(n * 8, 256) + 2 * align_up(n * 4, 256);
 }
 
 void carve(uint8_t *p, uint64_t n, SsDesc &d)
@@ -841,66 +1087,61 @@ void carve(uint8_t *p, uint64_t n, SsDesc &d)
         return q;
     };
     d.ctl = reinterpret_cast<SsCtl *>(take(sizeof(SsCtl)));
-    d.smp_k = reinterpret_cast<uint64_t *>(take(kSamples * 8));
+    d.smp_k1 = reinterpret_cast<uint64_t *>(take(kSamples * 8));
+    d.smp_k2 = reinterpret_cast<uint64_t *>(take(kSamples * 8));
     d.smp_j = reinterpret_cast<uint32_t *>(take(kSamples * 4));
     d.status = reinterpret_cast<uint32_t *>(take(tiles * 256 * 4));
-    d.bkey = reinterpret_cast<uint64_t *>(take(nb * kCap * 8));
+    d.bk1 = reinterpret_cast<uint64_t *>(take(nb * kCap * 8));
+    d.bk2 = reinterpret_cast<uint64_t *>(take(nb * kCap * 8));
     d.bj = reinterpret_cast<uint32_t *>(take(nb * kCap * 4));
-    for (int i = 0; i < 2; i++) d.fkey[i] = reinterpret_cast<uint64_t *>(take(n * 8));
+    d.tot = reinterpret_cast<uint32_t *>(take(kQ * 4));
+    for (int i = 0; i < 2; i++) d.fk1[i] = reinterpret_cast<uint64_t *>(take(n * 8));
+    for (int i = 0; i < 2; i++) d.fk2[i] = reinterpret_cast<uint64_t *>(take(n * 8));
     for (int i = 0; i < 2; i++) d.fj[i] = reinterpret_cast<uint32_t *>(take(n * 4));
 }
+
+uint64_t tier_part_bytes(uint64_t n) { return align_up((uint64_t)sample_blocks(n) * kQ * 4, 256); }
 
 }  // namespace
 
 size_t ssort_ws_bytes(uint64_t n, uint32_t nsorts)
 {
-    return n <= kSsMaxN ? (size_t)nsorts * region_bytes(n) : 0;
+    return n <= kSsMaxN ? (size_t)(tier_part_bytes(n) + (uint64_t)nsorts * region_bytes(n)) : 0;
 }
 
-uint32_t ssort_sample_blocks(uint64_t n)
-{
-    const uint64_t smax = n <= (1u << 17) ? kSamples / 2 : kSamples;
-    const uint64_t ns = n < smax ? n : smax;
-    return (uint32_t)cdiv(ns ? ns : 1, kSmpPerBlock);
-}
-
-hipError_t ssort_launch(const SortInput &in, const SortJob *jobs, uint32_t nsorts, bool serial,
-                        void *ws, hipStream_t s, const SsSide *side, const PartBatch *part)
+hipError_t ssort_launch(const SortInput &in, const SortJob *jobs, uint32_t nsorts, bool serial, void *ws,
+                        hipStream_t s)
 {
     if (in.n == 0 || nsorts == 0) return hipSuccess;
-    if (nsorts > kMaxSorts || in.n > kSsMaxN) return hipErrorInvalidValue;
+    if (nsorts > kSsMaxSorts || in.n > kSsMaxN) return hipErrorInvalidValue;
     SsBatch b;
+    memset(&b, 0, sizeof(b));
     b.in = in;
     b.n = in.n;
     b.tiles = (uint32_t)cdiv(in.n, kScTile);
     b.nb = n_buckets(in.n);
-    // 1024 samples (4 per bucket) up to 2^17 keys, 2048 above, where the
-    // average bucket is a quarter of the region capacity
-    const uint32_t smax = in.n <= (1u << 17) ? kSamples / 2 : kSamples;
-    b.ns = in.n < smax ? in.n : smax;
+    b.ns = n_samples(in.n);
     b.serial = serial ? 1u : 0u;
-    b.side = side ? *side : SsSide{nullptr, 0u, nullptr, nullptr, nullptr, nullptr};
     b.nsorts = nsorts;
-    b.nsb = ssort_sample_blocks(in.n);
-    if (part) {
-        b.part = *part;
-    } else {
-        memset(&b.part, 0, sizeof(b.part));
-    }
+    b.nsb = sample_blocks(in.n);
     uint8_t *p = static_cast<uint8_t *>(ws);
+    uint32_t *tier_part = reinterpret_cast<uint32_t *>(p);
+    p += tier_part_bytes(in.n);
     for (uint32_t i = 0; i < nsorts; i++) {
         SsDesc &d = b.s[i];
-        if (jobs[i].kind != SortKind::Fifo && jobs[i].kind != SortKind::Budget &&
-            jobs[i].kind != SortKind::Aging)
+        const SortKind k = jobs[i].kind;
+        if (k != SortKind::Fifo && k != SortKind::Class && k != SortKind::Tier && k != SortKind::Budget &&
+            k != SortKind::Aging)
             return hipErrorInvalidValue;
-        d.kind = jobs[i].kind;
+        if (k == SortKind::Tier) b.tier_part = tier_part;
+        d.kind = k;
+        d.two = k != SortKind::Fifo;
         d.key_out = jobs[i].key_out;
         d.out = jobs[i].out;
         carve(p, in.n, d);
         p += region_bytes(in.n);
     }
-    const uint32_t gx = b.part.njobs && b.part.tiles > b.nsb ? b.part.tiles : b.nsb;
-    hipLaunchKernelGGL(k_ss_sample, dim3(gx, nsorts + b.part.njobs), dim3(kSmpTPB), 0, s, b);
+    hipLaunchKernelGGL(k_ss_sample, dim3(b.nsb, nsorts), dim3(kSmpTPB), 0, s, b);
     hipLaunchKernelGGL(k_ss_scatter, dim3(b.tiles, nsorts), dim3(kScTPB), 0, s, b);
     hipLaunchKernelGGL(k_ss_bucket, dim3(b.nb, nsorts), dim3(kBkTPB), 0, s, b);
     return hipGetLastError();
