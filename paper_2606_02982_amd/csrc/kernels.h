@@ -55,15 +55,21 @@ hipError_t sort_launch(const SortInput &in, const SortJob *jobs, uint32_t nsorts
                        hipStream_t s);
 
 // The dispatch orders of at most kSsMaxN requests: a batch of up to
-// kSsMaxSorts sample sorts (Fifo, Class, Tier, Budget, Aging; at most one of
-// each) by composite keys, in three launches; none needs the FIFO order as an
-// input. `serial` sorts in one workgroup instead (the path taken when a
-// bucket overflows).
+// kSsMaxSorts sample sorts (Fifo, Budget, Aging; at most one of each) by
+// composite keys, in three launches; none needs the FIFO order as an input.
+// The Fifo job also places the Priority (perm[0]) and Weighted (perm[1])
+// orders given in parts (NULL entries: not wanted; the Fifo job's own out
+// may then be NULL). `serial` sorts in one workgroup instead (the path taken
+// when a bucket overflows).
 constexpr uint32_t kSsMaxN = 1u << 18;
-constexpr uint32_t kSsMaxSorts = 5;
+constexpr uint32_t kSsMaxSorts = 3;
+struct SsPartitions {
+    uint32_t *perm[2];
+    double *key[2];
+};
 size_t ssort_ws_bytes(uint64_t n, uint32_t nsorts);   // 0 above kSsMaxN
 hipError_t ssort_launch(const SortInput &in, const SortJob *jobs, uint32_t nsorts, bool serial,
-                        void *ws, hipStream_t s);
+                        void *ws, hipStream_t s, const SsPartitions *parts = nullptr);
 
 // ---- stage 2: calibrate -------------------------------------------------------
 // Up to kCalGroupsLds groups: chunked scan without a global partition.

@@ -8,9 +8,10 @@
 //             its cyclic round-robin position (closed form of the round)
 //   SJF       stable sort of the FIFO sequence by budget
 //   Aging     stable sort of the FIFO sequence by the aged score
-// Up to kSsMaxN requests every requested policy is a sample sort by the
-// composite key (policy key, arrival, index), all of them in the same three
-// launches. Above that, the FIFO permutation is sorted first (unless the
+// Up to kSsMaxN requests FIFO, SJF and Aging are sample sorts by the
+// composite key (policy key, arrival, index), all in the same three
+// launches, and the FIFO sort's last launch also places Priority and
+// Weighted. Above that, the FIFO permutation is sorted first (unless the
 // caller passes it in) and the other policies are LSD radix sorts of the
 // FIFO sequence, batched in one set of launches.
 #include <algorithm>
@@ -111,16 +112,6 @@ hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_
         }
     }
     const bool want_fifo = a.mask & 1u;
-    // the policy sorts, in the order of their grid rows
-    SortJob jobs[kSsMaxSorts];
-    uint32_t nj = 0;
-    // (the sample sorts' rows are dispatched in this order: the cheaper
-    // partitions last, where a second round of blocks may start)
-    if (a.mask & (1u << 3)) jobs[nj++] = {SortKind::Budget, 64, a.key[3], a.perm[3]};
-    if (a.mask & (1u << 4)) jobs[nj++] = {SortKind::Aging, 64, a.key[4], a.perm[4]};
-    if (a.mask & (1u << 1)) jobs[nj++] = {SortKind::Class, 8, a.key[1], a.perm[1]};
-    if (a.mask & (1u << 2)) jobs[nj++] = {SortKind::Tier, 8, a.key[2], a.perm[2]};
-
     if (want_fifo && a.fifo_in) {
         uint64_t nb = cdiv(n, 256);
         uint32_t blocks = (uint32_t)(nb < 4096 ? nb : 4096);
@@ -128,15 +119,34 @@ hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_
                            a.key[0]);
     }
     if (n <= kSsMaxN) {
-        // one batch of sample sorts; the FIFO order is not an input of the
-        // others, so a given fifo_in only saves the FIFO sort itself
+        // one batch of sample sorts: FIFO (carrying Priority and Weighted),
+        // SJF, Aging; a given fifo_in only saves the FIFO sort when neither
+        // partition is wanted
+        const bool parts = a.mask & 6u;
+        SsPartitions pw = {{nullptr, nullptr}, {nullptr, nullptr}};
+        for (int e = 0; e < 2; e++)
+            if (a.mask & (2u << e)) {
+                pw.perm[e] = a.perm[1 + e];
+                pw.key[e] = a.key[1 + e];
+            }
         SortJob all[kSsMaxSorts];
         uint32_t na = 0;
-        if (want_fifo && !a.fifo_in) all[na++] = {SortKind::Fifo, 64, a.key[0], a.perm[0]};
-        for (uint32_t i = 0; i < nj; i++) all[na++] = jobs[i];
+        const bool fifo_out = want_fifo && !a.fifo_in;
+        if (fifo_out || parts)
+            all[na++] = {SortKind::Fifo, 64, fifo_out ? a.key[0] : nullptr, fifo_out ? a.perm[0] : nullptr};
+        if (a.mask & (1u << 3)) all[na++] = {SortKind::Budget, 64, a.key[3], a.perm[3]};
+        if (a.mask & (1u << 4)) all[na++] = {SortKind::Aging, 64, a.key[4], a.perm[4]};
         if (na == 0) return hipGetLastError();
-        return ssort_launch(in, all, na, a.serial_sort, ws, s);
+        return ssort_launch(in, all, na, a.serial_sort, ws, s, parts ? &pw : nullptr);
     }
+
+    // the policy sorts over the FIFO sequence
+    SortJob jobs[kMaxSorts];
+    uint32_t nj = 0;
+    if (a.mask & (1u << 1)) jobs[nj++] = {SortKind::Class, 8, a.key[1], a.perm[1]};
+    if (a.mask & (1u << 2)) jobs[nj++] = {SortKind::Tier, 8, a.key[2], a.perm[2]};
+    if (a.mask & (1u << 3)) jobs[nj++] = {SortKind::Budget, 64, a.key[3], a.perm[3]};
+    if (a.mask & (1u << 4)) jobs[nj++] = {SortKind::Aging, 64, a.key[4], a.perm[4]};
 
     // radix sorts: the FIFO permutation first, then the policies over it
     uint8_t *p = static_cast<uint8_t *>(ws);

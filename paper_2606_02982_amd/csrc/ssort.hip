@@ -2,21 +2,24 @@
 // (Sec. "Scheduling Engine"): three launches for any set of policies.
 //
 // Every policy ends ties in FIFO order, and FIFO order is the order of
-// (arrival, index). So each policy's order is the order of the requests by a
-// composite key (k1, k2, i): k1 the policy's own key, k2 the arrival, i the
-// request index, compared in that order. No policy needs the FIFO
-// permutation as an input, and all of them sort side by side:
+// (arrival, index). So SJF and Aging order the requests by a composite key
+// (k1, k2, i): k1 the policy's own key, k2 the arrival, i the request index,
+// compared in that order; neither needs the FIFO permutation as an input,
+// and they sort side by side with the FIFO sort:
 //   Fifo    k1 = arrival (no k2)
-//   Class   k1 = priority class of the tier                (Priority)
-//   Tier    k1 = tier; the sorted position p of a request gives its rank
-//           k = p - (requests of lower tiers) within its tier in FIFO order,
-//           and the request goes to the round-robin position of that rank
-//           (Weighted):
-//           sum_t' min(n_t', r w_t') + sum_{t' < t} min(w_t', max(0, n_t' - r w_t'))
-//           + (k - r w_t),  r = floor(k / w_t)
 //   Budget  k1 = budget                                     (SJF)
 //   Aging   k1 = aged score max(floor, p - rate * max(0, t_now - arrival))
 // Keys are doubles compared through ordered_bits (so -0.0 ties with +0.0).
+// Priority and Weighted are stable partitions of the FIFO sequence by a
+// digit of at most 4 bits (the priority class of the tier, or the tier).
+// The FIFO row's bucket blocks place them: a bucket holds a contiguous run
+// of the FIFO sequence, so a request's rank among its digit's requests is
+// the count over earlier buckets (decoupled look-back over the buckets'
+// digit counts) plus its rank in the bucket. Priority puts it at its class's
+// first position plus that rank; Weighted at the round-robin position of
+// the k-th request of tier t:
+//   sum_t' min(n_t', r w_t') + sum_{t' < t} min(w_t', max(0, n_t' - r w_t'))
+//   + (k - r w_t),  r = floor(k / w_t).
 //
 //   k_ss_sample   S triples (1024 up to 2^17 requests, else 2048) at
 //                 stratified random positions; each of S/8 blocks stages all
@@ -62,7 +65,8 @@ constexpr int kScTPB = 512, kScR = 4;    // scatter tile: 2048 requests
 constexpr uint32_t kScTile = kScTPB * kScR;
 constexpr int kBkTPB = 512, kBkR = kCap / kBkTPB;
 constexpr uint32_t kBinBits = 11, kBins = 1u << kBinBits;   // in-bucket bins
-constexpr uint32_t kBinMax = 64;         // larger bins: LSD passes instead
+constexpr uint32_t kBinMax = 128;        // larger bins: LSD passes instead
+constexpr uint32_t kBinMax2 = 32;        // the same for a pass by two keys
 constexpr int kSmpTPB = 256;             // k_ss_sample: threads per block,
 constexpr uint32_t kSmpThr = 32;         // threads per sample ranked,
 constexpr uint32_t kSmpPerBlock = kSmpTPB / kSmpThr;   // samples ranked per block
@@ -70,7 +74,8 @@ constexpr uint32_t kQ = kTierCounts;     // tiers
 
 struct SsCtl {
     uint32_t overflow;
-    uint32_t pad[63];
+    uint32_t lb_err;       // a bounded look-back wait over the buckets ran out
+    uint32_t pad[62];
 };
 
 struct SsDesc {
@@ -86,7 +91,10 @@ struct SsDesc {
     uint64_t *bk1;         // [buckets][kCap] bucket regions
     uint64_t *bk2;
     uint32_t *bj;
-    uint32_t *tot;         // [kQ] requests per tier (Tier sorts)
+    uint32_t *tot;         // [kQ] requests per tier (FIFO row with partitions)
+    uint32_t *bstat;       // [buckets][2 kQ] look-back words of the digit counts
+    uint32_t *pw_out[2];   // FIFO row: Priority and Weighted orders (or NULL)
+    double *pw_key[2];
     uint64_t *fk1[2];      // [n] x 2: single-workgroup sort
     uint64_t *fk2[2];
     uint32_t *fj[2];
@@ -101,7 +109,7 @@ struct SsBatch {
     uint32_t serial;       // sort in one workgroup regardless of the buckets
     uint32_t nsorts;       // sorts of the batch (grid rows)
     uint32_t nsb;          // blocks of k_ss_sample per sort
-    uint32_t *tier_part;   // [nsb][kQ] tier counts of slices (a Tier sort is in the batch)
+    uint32_t *tier_part;   // [nsb][kQ] tier counts of slices (when the partitions are wanted)
     SsDesc s[kSsMaxSorts];
 };
 
@@ -140,7 +148,7 @@ __device__ __forceinline__ bool key_less(uint64_t a1, uint64_t a2, uint32_t ja, 
 }
 
 // The sort key (k1, k2) of request i, and the per-request key output (the
-// policy's primary key; the Weighted round number is written later). The
+// policy's primary key). The
 // aged score rounds each operation separately (no fused multiply-add). Only
 // loads and arithmetic: a caller that unrolls several requests gets all
 // their loads in flight before the first use.
@@ -156,25 +164,17 @@ __device__ __forceinline__ void ss_key(const SortInput &in, uint32_t i, uint64_t
         kv = in.budget[i];
         k1 = ordered_bits(kv);
         k2 = ordered_bits(a);
-    } else {
+    } else {   // Aging
         uint32_t q = in.tier[i];
         q = q < kQ ? q : kQ - 1u;
         k2 = ordered_bits(a);
-        if constexpr (K == SortKind::Aging) {
-            double w = in.t_now - a;
-            if (w < 0.0) w = 0.0;
-            const double d = in.aging_rate * w;
-            double e = in.prio[q] - d;
-            if (e < in.aging_floor) e = in.aging_floor;
-            kv = e;
-            k1 = ordered_bits(e);
-        } else if constexpr (K == SortKind::Class) {
-            kv = in.prio[q];
-            k1 = ordered_bits((double)in.cls[q]);
-        } else {   // Tier
-            kv = 0.0;
-            k1 = ordered_bits((double)q);
-        }
+        double w = in.t_now - a;
+        if (w < 0.0) w = 0.0;
+        const double d = in.aging_rate * w;
+        double e = in.prio[q] - d;
+        if (e < in.aging_floor) e = in.aging_floor;
+        kv = e;
+        k1 = ordered_bits(e);
     }
 }
 
@@ -184,8 +184,6 @@ __device__ __forceinline__ void with_kind(SortKind kind, F &&body)
 {
     switch (kind) {
     case SortKind::Fifo: body(std::integral_constant<SortKind, SortKind::Fifo>()); break;
-    case SortKind::Class: body(std::integral_constant<SortKind, SortKind::Class>()); break;
-    case SortKind::Tier: body(std::integral_constant<SortKind, SortKind::Tier>()); break;
     case SortKind::Budget: body(std::integral_constant<SortKind, SortKind::Budget>()); break;
     default: body(std::integral_constant<SortKind, SortKind::Aging>()); break;
     }
@@ -204,7 +202,12 @@ __device__ __forceinline__ void sample_body(const SsBatch &b, const SsDesc &d, S
     const uint32_t t = threadIdx.x, n = b.n, S = b.ns;
     const uint32_t stride = b.nsb * kSmpTPB;
     for (uint32_t i = blockIdx.x * kSmpTPB + t; i < b.tiles * 256u; i += stride) d.status[i] = 0;
-    if (blockIdx.x == 0 && t == 0) d.ctl->overflow = b.serial;
+    if (d.pw_out[0] || d.pw_out[1])
+        for (uint32_t i = blockIdx.x * kSmpTPB + t; i < b.nb * 2u * kQ; i += stride) d.bstat[i] = 0;
+    if (blockIdx.x == 0 && t == 0) {
+        d.ctl->overflow = b.serial;
+        d.ctl->lb_err = 0;
+    }
     {
         // all loads in flight before the first LDS store
         constexpr int kPer = kSamples / kSmpTPB;
@@ -285,7 +288,7 @@ __device__ __forceinline__ void scatter_keys(const SsBatch &b, const SsDesc &d, 
         jj[r] = base + (idx < cnt ? idx : 0u);
         ss_key<K>(b.in, jj[r], k1[r], k2[r], kv[r]);
     }
-    if (K != SortKind::Tier && d.key_out) {
+    if (d.key_out) {
 #pragma unroll
         for (int r = 0; r < kScR; r++) {
             const uint32_t idx = (uint32_t)w * (64u * kScR) + (uint32_t)r * 64u + (uint32_t)lane;
@@ -430,7 +433,7 @@ __global__ __launch_bounds__(kScTPB) void k_ss_scatter(SsBatch b)
         }
     }
     if (over) atomicOr(&d.ctl->overflow, 1u);
-    if (d.kind == SortKind::Tier && tile == 0) {
+    if ((d.pw_out[0] || d.pw_out[1]) && tile == 0) {
         // requests per tier (for the round-robin positions): the sum of the
         // slices' counts, after this tile's look-back word is out
         __syncthreads();
@@ -445,40 +448,56 @@ __global__ __launch_bounds__(kScTPB) void k_ss_scatter(SsBatch b)
     }
 }
 
-// Requests per tier and the first sorted position of each tier, for the
-// round-robin positions of a Tier sort.
-struct TierTable {
+// Priority and Weighted: requests per tier, each class's first position,
+// and the digit counts (classes 0..15, then tiers 16..31).
+struct PwTable {
+    double prio[kQ];                 // per tier: priority, class, weight (copies of
+    uint32_t cls[kQ];                // the launch parameters, indexed per lane)
+    uint32_t weight[kQ];
     uint32_t tot[kQ];
-    uint32_t start[kQ];
+    uint32_t cstart[kQ];
+    uint32_t cnt[2 * kQ];            // this bucket's (or chunk's) digit counts
+    uint32_t pre[2 * kQ];            // the digits' counts before it
+    uint32_t wd[kBkTPB / 64][2 * kQ];   // per-wave digit counters
 };
 
-// Output position pos of the sorted sequence holds request j: the request
-// goes there, or, for Weighted, to the round-robin position of its rank
-// within its tier.
-__device__ __forceinline__ void emit(const SsBatch &b, const SsDesc &d, const TierTable &tt, uint32_t pos,
-                                     uint32_t j)
+// The round-robin position of the k-th request (in FIFO order) of tier q,
+// and its round.
+__device__ __forceinline__ uint64_t weighted_pos(const PwTable &pt, uint32_t n_tiers, uint32_t q, uint32_t k,
+                                                 uint32_t &rnd)
 {
-    if (d.kind != SortKind::Tier) {
-        d.out[pos] = j;
-        return;
-    }
-    const SortInput &in = b.in;
-    uint32_t q = in.tier[j];
-    q = q < kQ ? q : kQ - 1u;
-    const uint32_t k = pos - tt.start[q];   // rank within the tier
-    const uint32_t wq = in.weight[q] ? in.weight[q] : 1u;
-    const uint32_t rnd = k / wq;
+    const uint32_t wq = pt.weight[q] ? pt.weight[q] : 1u;
+    rnd = k / wq;
     uint64_t p = k - rnd * wq;
-    for (uint32_t u = 0; u < in.n_tiers; u++) {
-        const uint64_t nt = tt.tot[u], wt = in.weight[u], full = (uint64_t)rnd * wt;
+    for (uint32_t u = 0; u < n_tiers; u++) {
+        const uint64_t nt = pt.tot[u], wt = pt.weight[u], full = (uint64_t)rnd * wt;
         p += nt < full ? nt : full;
         if (u < q) {
             const uint64_t left = nt > full ? nt - full : 0u;
             p += left < wt ? left : wt;
         }
     }
-    if (p < b.n) d.out[p] = j;   // always, for tiers < n_tiers
-    if (d.key_out) d.key_out[j] = (double)rnd;
+    return p;
+}
+
+// Requests at FIFO positions in a run: their Priority and Weighted places.
+// qd: tier (clamped), j: request, rc/rt: rank among the run's requests of
+// the same class/tier before it, pre: counts of the digits before the run.
+__device__ __forceinline__ void pw_place(const SsBatch &b, const SsDesc &d, const PwTable &pt, uint32_t q,
+                                         uint32_t j, uint32_t kc, uint32_t kt)
+{
+    if (d.pw_out[0]) {
+        const uint32_t c = pt.cls[q];
+        const uint64_t pos = (uint64_t)pt.cstart[c] + kc;
+        if (pos < b.n) d.pw_out[0][pos] = j;   // always, for tiers < n_tiers
+        if (d.pw_key[0]) d.pw_key[0][j] = pt.prio[q];
+    }
+    if (d.pw_out[1]) {
+        uint32_t rnd;
+        const uint64_t pos = weighted_pos(pt, b.in.n_tiers < kQ ? b.in.n_tiers : kQ, q, kt, rnd);
+        if (pos < b.n) d.pw_out[1][pos] = j;
+        if (d.pw_key[1]) d.pw_key[1][j] = (double)rnd;
+    }
 }
 
 // LDS scratch of the bucket sort (also used by the single-workgroup sort).
@@ -498,10 +517,12 @@ struct BkShared {
     uint32_t wmax[kBkTPB / 64];
     uint64_t kmin[kBkTPB / 64], kmax[kBkTPB / 64], kmin2[kBkTPB / 64];
     uint64_t kmin1[kBkTPB / 64], kmax1[kBkTPB / 64];
-    TierTable tt;
+    PwTable pt;
     uint64_t lkey[kCap];
-    uint32_t lj[kCap];
+    uint64_t lkey2[kCap];
+    uint32_t lj[kCap + 1];
     uint16_t lslot[kCap];
+    uint8_t lq[kCap];
 };
 
 // One stable LSD pass on byte p of the keys of m entries held R_eff per
@@ -630,11 +651,32 @@ __device__ __forceinline__ void block_range(BkShared &sh, const uint64_t *k, con
     }
 }
 
+// Exclusive scan of one value per thread over the block (every thread
+// calls it; sh.wsum is used). Ends with a barrier.
+__device__ __forceinline__ uint32_t block_excl_scan(BkShared &sh, uint32_t x)
+{
+    const int w = (int)(threadIdx.x >> 6);
+    const uint32_t incl = wave_incl_scan_dpp(x);
+    if (lane_id() == 63) sh.wsum[w] = incl;
+    __syncthreads();
+    uint32_t off = 0;
+    for (int q = 0; q < w; q++) off += sh.wsum[q];
+    __syncthreads();
+    return off + incl - x;
+}
+
 // Rank pass: the place rank[r] of each of the m entries (entry idx =
 // w * 64 R_eff + r * 64 + lane) in the order of key k, ties in entry order;
 // kmn, kmx: the keys' range. Every thread of the block calls it; sh.bin,
 // sh.lkey, sh.lj and sh.lslot are used, and k is left in an unspecified
 // order.
+//
+// With k2 (not NULL) it ranks by (k, k2, entry) in one pass if it can: all
+// entries (the smallest key included) go to the bins, and when no bin holds
+// more than kBinMax2 of them each is ranked by counting inside its bin by
+// (k, k2, entry). Otherwise it returns false without ranks, k unchanged
+// (the caller then ranks by k2 and by k in two passes). The outcome is the
+// same in every thread.
 //
 // Entries with the smallest key (the common heavy tie: aged scores clamped to
 // the floor, or the lowest class of a bucket) come first, in entry order:
@@ -646,8 +688,8 @@ __device__ __forceinline__ void block_range(BkShared &sh, const uint64_t *k, con
 // Their rank = entries at the minimum + bin start + rank inside the bin by
 // (key, entry). A bin of more than kBinMax entries sends the whole bucket
 // through stable LSD passes on the key bytes that vary in it instead.
-__device__ __forceinline__ void rank_pass(BkShared &sh, uint64_t *k, uint32_t reff, uint32_t m, uint64_t kmn, uint64_t kmx,
-                          uint32_t *rank)
+__device__ __forceinline__ bool rank_pass(BkShared &sh, uint64_t *k, const uint64_t *k2, uint32_t reff, uint32_t m,
+                                          uint64_t kmn, uint64_t kmx, uint32_t *rank)
 {
     constexpr int kWaves = kBkTPB / 64;
     const uint32_t t = threadIdx.x;
@@ -657,18 +699,21 @@ __device__ __forceinline__ void rank_pass(BkShared &sh, uint64_t *k, uint32_t re
         // one key (or no entry): entry order is the order
 #pragma unroll
         for (int r = 0; r < kBkR; r++) rank[r] = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
-        return;
+        return !k2;   // one key: the order is by k2 alone
     }
     for (uint32_t i = t; i <= kBins; i += kBkTPB) sh.bin[i] = 0;
+    // excl: the minimum-key entries are ranked apart (one key only).
     // rank[r] first holds the number of minimum-key entries before entry r
     // (its rank if it has the minimum key; the valid entries are a prefix,
     // so entry idx has idx - rank[r] entries above the minimum before it)
-    uint32_t nlow;
-    uint64_t kmn2 = ~0ull;   // smallest key above the minimum
-    {
+    const bool excl = !k2;
+    uint32_t nlow = 0;
+    uint64_t kmn2 = excl ? ~0ull : kmn;   // smallest key of the binned entries
+    if (excl) {
         uint32_t run = 0;
 #pragma unroll
         for (int r = 0; r < kBkR; r++) {
+            if ((uint32_t)r >= reff) break;
             const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
             const bool valid = (uint32_t)r < reff && idx < m;
             const bool low = valid && k[r] == kmn;
@@ -706,9 +751,9 @@ __device__ __forceinline__ void rank_pass(BkShared &sh, uint64_t *k, uint32_t re
             const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
             if (k[r] != kmn) rank[r] = nlow + (idx - rank[r]);
         }
-        return;
+        return true;
     }
-    // bins over [kmn2, kmx] for the entries above the minimum
+    // bins over [kmn2, kmx] for the binned entries
     const int hb = 63 - __clzll((long long)(kmn2 ^ kmx));
     const uint32_t shift = hb >= (int)kBinBits ? (uint32_t)hb - (kBinBits - 1u) : 0u;
     const double xmn = from_ordered(kmn2), xmx = from_ordered(kmx);
@@ -721,7 +766,7 @@ __device__ __forceinline__ void rank_pass(BkShared &sh, uint64_t *k, uint32_t re
     for (int r = 0; r < kBkR; r++) {
         const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
         db[r] = 0;
-        if ((uint32_t)r < reff && idx < m && k[r] != kmn) {
+        if ((uint32_t)r < reff && idx < m && (!excl || k[r] != kmn)) {
             uint32_t q;
             if (linear) {
                 const double f = (from_ordered(k[r]) - xmn) * scale;   // in [0, kBins]
@@ -764,13 +809,14 @@ __device__ __forceinline__ void rank_pass(BkShared &sh, uint64_t *k, uint32_t re
 #pragma unroll
     for (int q = 0; q < kWaves; q++) maxbin = sh.wmax[q] > maxbin ? sh.wmax[q] : maxbin;
     __syncthreads();
-    if (maxbin <= kBinMax) {
+    if (maxbin <= (excl ? kBinMax : kBinMax2)) {
 #pragma unroll
         for (int r = 0; r < kBkR; r++) {
             const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
-            if ((uint32_t)r < reff && idx < m && k[r] != kmn) {
+            if ((uint32_t)r < reff && idx < m && (!excl || k[r] != kmn)) {
                 const uint32_t q = sh.bin[db[r] & (kBins - 1u)] + (db[r] >> kBinBits);
                 sh.lkey[q] = k[r];
+                if (k2) sh.lkey2[q] = k2[r];
                 sh.lslot[q] = (uint16_t)idx;
             }
         }
@@ -778,20 +824,108 @@ __device__ __forceinline__ void rank_pass(BkShared &sh, uint64_t *k, uint32_t re
 #pragma unroll
         for (int r = 0; r < kBkR; r++) {
             const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
-            if ((uint32_t)r < reff && idx < m && k[r] != kmn) {
+            if ((uint32_t)r < reff && idx < m && (!excl || k[r] != kmn)) {
                 const uint32_t bn = db[r] & (kBins - 1u);
                 const uint32_t s0 = sh.bin[bn], s1 = sh.bin[bn + 1];
                 uint32_t rk = nlow + s0;
-                for (uint32_t u = s0; u < s1; u++) {
-                    const uint64_t ku = sh.lkey[u];
-                    rk += (ku < k[r] || (ku == k[r] && sh.lslot[u] < idx)) ? 1u : 0u;
+                if (k2) {
+                    for (uint32_t u = s0; u < s1; u++) {
+                        const uint64_t ku = sh.lkey[u], k2u = sh.lkey2[u];
+                        rk += key_less(ku, k2u, sh.lslot[u], k[r], k2[r], idx) ? 1u : 0u;
+                    }
+                } else {
+                    for (uint32_t u = s0; u < s1; u++) {
+                        const uint64_t ku = sh.lkey[u];
+                        rk += (ku < k[r] || (ku == k[r] && sh.lslot[u] < idx)) ? 1u : 0u;
+                    }
                 }
                 rank[r] = rk;
             }
         }
-        __syncthreads();   // sh.lkey, sh.lslot are free again
-        return;
+        __syncthreads();   // sh.lkey, sh.lkey2, sh.lslot are free again
+        return true;
     }
+    if (linear) {
+        // crowded bins (keys in clusters with gaps between them, which the
+        // equal-width bins spread over): bin b of c_b entries is cut into c_b
+        // equal sub-intervals, one sub-bin each, by the fraction of the key
+        // inside the bin (the same rounded operations, so monotone). The
+        // sub-bins of bin b start at the bin's start; their counts and starts
+        // use sh.lj.
+        const uint32_t nb2 = m - nlow;   // sub-bins, one per binned entry
+        for (uint32_t i = t; i <= nb2; i += kBkTPB) sh.lj[i] = 0;
+        __syncthreads();
+#pragma unroll
+        for (int r = 0; r < kBkR; r++) {
+            const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
+            if ((uint32_t)r < reff && idx < m && (!excl || k[r] != kmn)) {
+                const uint32_t bn = db[r] & (kBins - 1u);
+                const uint32_t s0 = sh.bin[bn], cb = sh.bin[bn + 1] - s0;
+                const double f = (from_ordered(k[r]) - xmn) * scale - (double)bn;   // in [0, 1)
+                uint32_t sub = f > 0.0 ? (uint32_t)(f * (double)cb) : 0u;
+                sub = sub < cb ? sub : cb - 1u;
+                const uint32_t sb = s0 + sub;
+                db[r] = sb | (atomicAdd(&sh.lj[sb], 1u) << 12);
+            }
+        }
+        __syncthreads();
+        // sub-bin starts: thread t scans sub-bins 8t .. 8t + 7
+        uint32_t hv[kCap / kBkTPB], sum = 0, mx = 0;
+#pragma unroll
+        for (int e = 0; e < (int)(kCap / kBkTPB); e++) {
+            const uint32_t i = (uint32_t)t * (kCap / kBkTPB) + (uint32_t)e;
+            hv[e] = i < nb2 ? sh.lj[i] : 0u;
+            sum += hv[e];
+            mx = hv[e] > mx ? hv[e] : mx;
+        }
+#pragma unroll
+        for (int sft = 32; sft >= 1; sft >>= 1) {
+            const uint32_t o = (uint32_t)__shfl_xor((int)mx, sft, 64);
+            mx = o > mx ? o : mx;
+        }
+        if (lane == 0) sh.wmax[w] = mx;
+        uint32_t ex = block_excl_scan(sh, sum);
+#pragma unroll
+        for (int e = 0; e < (int)(kCap / kBkTPB); e++) {
+            const uint32_t i = (uint32_t)t * (kCap / kBkTPB) + (uint32_t)e;
+            if (i < nb2) sh.lj[i] = ex;
+            ex += hv[e];
+        }
+        if (t == 0) sh.lj[nb2] = nb2;
+        uint32_t maxsub = 0;
+#pragma unroll
+        for (int q = 0; q < kWaves; q++) maxsub = sh.wmax[q] > maxsub ? sh.wmax[q] : maxsub;
+        __syncthreads();
+        if (maxsub <= (excl ? kBinMax : kBinMax2)) {
+#pragma unroll
+            for (int r = 0; r < kBkR; r++) {
+                const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
+                if ((uint32_t)r < reff && idx < m && (!excl || k[r] != kmn)) {
+                    const uint32_t q = sh.lj[db[r] & 4095u] + (db[r] >> 12);
+                    sh.lkey[q] = k[r];
+                    sh.lkey2[q] = k2 ? k2[r] : 0ull;
+                    sh.lslot[q] = (uint16_t)idx;
+                }
+            }
+            __syncthreads();
+#pragma unroll
+            for (int r = 0; r < kBkR; r++) {
+                const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
+                if ((uint32_t)r < reff && idx < m && (!excl || k[r] != kmn)) {
+                    const uint32_t sb = db[r] & 4095u;
+                    const uint32_t s0 = sh.lj[sb], s1 = sh.lj[sb + 1];
+                    const uint64_t e2 = k2 ? k2[r] : 0ull;
+                    uint32_t rk = nlow + s0;
+                    for (uint32_t u = s0; u < s1; u++)
+                        rk += key_less(sh.lkey[u], sh.lkey2[u], sh.lslot[u], k[r], e2, idx) ? 1u : 0u;
+                    rank[r] = rk;
+                }
+            }
+            __syncthreads();
+            return true;
+        }
+    }
+    if (k2) return false;
     // crowded bins (many equal or near-equal keys): stable LSD passes over
     // all the entries, on the key bytes up to the highest bit that varies in
     // the bucket (minimum included); the entries carry their index along,
@@ -842,17 +976,77 @@ __device__ __forceinline__ void rank_pass(BkShared &sh, uint64_t *k, uint32_t re
         rank[r] = (uint32_t)r < reff && idx < m ? sh.lslot[idx] : 0u;
     }
     __syncthreads();
+    return true;
 }
 
-// Requests per tier and each tier's first sorted position, into sh.tt.
-__device__ __forceinline__ void load_tiers(const SsBatch &b, const SsDesc &d, BkShared &sh)
+// Requests per tier and each class's first position, into sh.pt; clears the
+// digit counters. Every thread calls it.
+__device__ __forceinline__ void load_pw(const SsBatch &b, const SsDesc &d, BkShared &sh)
 {
-    if (threadIdx.x < kQ) sh.tt.tot[threadIdx.x] = d.tot[threadIdx.x];
+    const uint32_t t = threadIdx.x;
+    if (t < kQ) {
+        sh.pt.tot[t] = d.tot[t];
+        sh.pt.prio[t] = b.in.prio[t];
+        sh.pt.cls[t] = b.in.cls[t];
+        sh.pt.weight[t] = b.in.weight[t];
+    }
+    if (t < 2 * kQ) sh.pt.cnt[t] = 0;
+    for (uint32_t i = t; i < (kBkTPB / 64) * 2 * kQ; i += kBkTPB) (&sh.pt.wd[0][0])[i] = 0;
     __syncthreads();
-    if (threadIdx.x < kQ) {
+    if (t < kQ) {
         uint32_t s = 0;
-        for (uint32_t q = 0; q < threadIdx.x; q++) s += sh.tt.tot[q];
-        sh.tt.start[threadIdx.x] = s;
+        for (uint32_t q = 0; q < b.in.n_tiers && q < kQ; q++) s += sh.pt.cls[q] < t ? sh.pt.tot[q] : 0u;
+        sh.pt.cstart[t] = s;
+    }
+}
+
+// Stable ranks of this thread's entries (wave-major, entry idx =
+// w * 64 R_eff + r * 64 + lane, valid below m) among the entries of the
+// same class (rc) and of the same tier (rt) of the run, from ballots and
+// the per-wave counters sh.pt.wd (zero on entry; afterwards each wave's
+// exclusive start per digit). Ends with a barrier.
+__device__ __forceinline__ void pw_rank(const SsBatch &b, BkShared &sh, const uint32_t *q, uint32_t reff, uint32_t m,
+                                        uint32_t *rc, uint32_t *rt)
+{
+    constexpr int kWaves = kBkTPB / 64;
+    const uint32_t t = threadIdx.x;
+    const int w = (int)(t >> 6), lane = lane_id();
+    const uint32_t wk = 64u * reff;
+#pragma unroll
+    for (int r = 0; r < kBkR; r++) {
+        rc[r] = 0;
+        rt[r] = 0;
+        if ((uint32_t)r < reff) {
+            const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
+            const bool ok = idx < m;
+            const uint32_t dc = sh.pt.cls[q[r]], dt = q[r];
+            uint64_t pc = __ballot(ok), pt = pc;
+#pragma unroll
+            for (int bb = 0; bb < 4; bb++) {
+                const bool xc = (dc >> bb) & 1u, xt = (dt >> bb) & 1u;
+                const uint64_t mc = __ballot(xc), mt = __ballot(xt);
+                pc &= xc ? mc : ~mc;
+                pt &= xt ? mt : ~mt;
+            }
+            const uint32_t bc = (uint32_t)__popcll(pc & lanemask_lt()), bt = (uint32_t)__popcll(pt & lanemask_lt());
+            const uint32_t oc = ok ? sh.pt.wd[w][dc] : 0u, ot = ok ? sh.pt.wd[w][kQ + dt] : 0u;
+            rc[r] = oc + bc;
+            rt[r] = ot + bt;
+            if (ok && bc == 0) sh.pt.wd[w][dc] = oc + (uint32_t)__popcll(pc);
+            if (ok && bt == 0) sh.pt.wd[w][kQ + dt] = ot + (uint32_t)__popcll(pt);
+            __builtin_amdgcn_wave_barrier();
+        }
+    }
+    __syncthreads();
+    if (t < 2 * kQ) {
+        uint32_t acc = 0;
+#pragma unroll
+        for (int v = 0; v < kWaves; v++) {
+            const uint32_t c = sh.pt.wd[v][t];
+            sh.pt.wd[v][t] = acc;
+            acc += c;
+        }
+        sh.pt.cnt[t] = acc;   // the run's digit counts
     }
     __syncthreads();
 }
@@ -873,9 +1067,8 @@ __device__ __forceinline__ void serial_sort(const SsBatch &b, const SsDesc &d, B
         d.fk1[0][j] = k1;
         d.fk2[0][j] = k2;
         d.fj[0][j] = j;
-        if (d.key_out && d.kind != SortKind::Tier) d.key_out[j] = kv;
+        if (d.key_out) d.key_out[j] = kv;
     }
-    if (d.kind == SortKind::Tier) load_tiers(b, d, sh);
     __syncthreads();
     uint32_t src = 0;
     for (uint32_t pass = 0; pass < 16; pass++) {
@@ -928,9 +1121,36 @@ __device__ __forceinline__ void serial_sort(const SsBatch &b, const SsDesc &d, B
         }
         src ^= 1u;
     }
-    for (uint32_t i = t; i < n; i += kBkTPB) {
-        const uint32_t j = d.fj[src][i];
-        emit(b, d, sh.tt, i, j < n ? j : 0u);
+    if (d.out)
+        for (uint32_t i = t; i < n; i += kBkTPB) d.out[i] = d.fj[src][i];
+    if (!d.pw_out[0] && !d.pw_out[1]) return;
+    // Priority and Weighted over the FIFO sequence, a chunk of kBkTPB
+    // positions at a time (one per thread), with running digit counts
+    load_pw(b, d, sh);
+    if (t < 2 * kQ) sh.pt.pre[t] = 0;
+    __syncthreads();
+    for (uint32_t c0 = 0; c0 < n; c0 += kBkTPB) {
+        const uint32_t m = n - c0 < kBkTPB ? n - c0 : kBkTPB;
+        uint32_t q[kBkR], rc[kBkR], rt[kBkR];
+        uint32_t j = 0;
+#pragma unroll
+        for (int r = 0; r < kBkR; r++) q[r] = 0;
+        if (t < m) {
+            j = d.fj[src][c0 + t];
+            j = j < n ? j : 0u;
+            const uint32_t qq = b.in.tier[j];
+            q[0] = qq < kQ ? qq : kQ - 1u;
+        }
+        pw_rank(b, sh, q, 1u, m, rc, rt);
+        if (t < m) {
+            const uint32_t c = sh.pt.cls[q[0]];
+            pw_place(b, d, sh.pt, q[0], j, sh.pt.pre[c] + sh.pt.wd[w][c] + rc[0],
+                     sh.pt.pre[kQ + q[0]] + sh.pt.wd[w][kQ + q[0]] + rt[0]);
+        }
+        __syncthreads();
+        if (t < 2 * kQ) sh.pt.pre[t] += sh.pt.cnt[t];
+        for (uint32_t i = t; i < (kBkTPB / 64) * 2 * kQ; i += kBkTPB) (&sh.pt.wd[0][0])[i] = 0;
+        __syncthreads();
     }
 }
 
@@ -960,7 +1180,6 @@ __global__ __launch_bounds__(kBkTPB) void k_ss_bucket(SsBatch b)
     const uint32_t before = wave_sum(t < bkt ? c : 0u);
     if (lane == 0) sh.redu[w] = before;
     if (t == bkt) sh.offs[0] = c;
-    if (d.kind == SortKind::Tier && t < kQ) sh.tt.tot[t] = d.tot[t];
     __syncthreads();
     uint32_t off = 0;
 #pragma unroll
@@ -968,82 +1187,129 @@ __global__ __launch_bounds__(kBkTPB) void k_ss_bucket(SsBatch b)
     const uint32_t m = sh.offs[0];   // <= kCap: no region overflowed
     const uint32_t reff = (m + kBkTPB - 1) / kBkTPB;
     const uint32_t wk = 64u * reff;
-    if (d.kind == SortKind::Tier && t < kQ) {
-        uint32_t s = 0;
-        for (uint32_t q = 0; q < t; q++) s += sh.tt.tot[q];
-        sh.tt.start[t] = s;   // read after the barriers below
-    }
 
-    // the entries: index order within the bucket
-    uint64_t k[kBkR];
-    uint32_t jv[kBkR], rank[kBkR];
-    if (two) {
-        // by arrival first (ties: index order, which is entry order), then
-        // stably by k1, with the entries laid out in arrival order
-        uint64_t mn1, mx1, mn2, mx2;
-        {
-            uint64_t k1[kBkR];
-#pragma unroll
-            for (int r = 0; r < kBkR; r++) {
-                const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
-                k1[r] = 0;
-                k[r] = 0;
-                if ((uint32_t)r < reff && idx < m) {
-                    k1[r] = reff == 1 ? a0 : src1[idx];
-                    k[r] = reff == 1 ? b0 : src2[idx];
-                }
-            }
-            block_range(sh, k, k1, reff, m, mn2, mx2, mn1, mx1);
-        }
-        rank_pass(sh, k, reff, m, mn2, mx2, rank);
-        if (mn1 < mx1) {
-#pragma unroll
-            for (int r = 0; r < kBkR; r++) {
-                const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
-                if ((uint32_t)r < reff && idx < m) {
-                    sh.lkey[rank[r]] = reff == 1 ? a0 : src1[idx];
-                    sh.lj[rank[r]] = reff == 1 ? j0 : srcj[idx];
-                }
-            }
-            __syncthreads();
-#pragma unroll
-            for (int r = 0; r < kBkR; r++) {
-                const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
-                k[r] = 0;
-                jv[r] = 0;
-                if ((uint32_t)r < reff && idx < m) {
-                    k[r] = sh.lkey[idx];
-                    jv[r] = sh.lj[idx];
-                }
-            }
-            __syncthreads();
-            rank_pass(sh, k, reff, m, mn1, mx1, rank);
-        } else {
-#pragma unroll
-            for (int r = 0; r < kBkR; r++) {
-                const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
-                jv[r] = (uint32_t)r < reff && idx < m ? (reff == 1 ? j0 : srcj[idx]) : 0u;
-            }
-        }
-    } else {
-#pragma unroll
-        for (int r = 0; r < kBkR; r++) {
-            const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
-            k[r] = 0;
-            jv[r] = 0;
-            if ((uint32_t)r < reff && idx < m) {
-                k[r] = reff == 1 ? a0 : src1[idx];
-                jv[r] = reff == 1 ? j0 : srcj[idx];
-            }
-        }
-        uint64_t mn1, mx1, u0, u1;
-        block_range(sh, k, nullptr, reff, m, mn1, mx1, u0, u1);
-        rank_pass(sh, k, reff, m, mn1, mx1, rank);
-    }
+    // the entries (index order within the bucket) and the keys' ranges
+    const bool pw = d.pw_out[0] || d.pw_out[1];   // FIFO row with the partitions
+    if (pw) load_pw(b, d, sh);
+    uint64_t k[kBkR], k2[kBkR];
+    uint32_t jv[kBkR], rank[kBkR], q[kBkR];
 #pragma unroll
     for (int r = 0; r < kBkR; r++) {
         const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
-        if ((uint32_t)r < reff && idx < m && off + rank[r] < n) emit(b, d, sh.tt, off + rank[r], jv[r]);
+        k[r] = 0;
+        k2[r] = 0;
+        jv[r] = 0;
+        q[r] = 0;
+        if ((uint32_t)r < reff && idx < m) {
+            k[r] = reff == 1 ? a0 : src1[idx];
+            if (two) k2[r] = reff == 1 ? b0 : src2[idx];
+            jv[r] = reff == 1 ? j0 : srcj[idx];
+        }
+    }
+    if (pw) {
+        // the bucket's digit counts (order-free), published before its own
+        // ranking so that later buckets need not wait for it
+#pragma unroll
+        for (int r = 0; r < kBkR; r++) {
+            const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
+            if ((uint32_t)r < reff && idx < m) {
+                const uint32_t qq = b.in.tier[jv[r]];
+                q[r] = qq < kQ ? qq : kQ - 1u;
+                atomicAdd(&sh.pt.cnt[sh.pt.cls[q[r]]], 1u);
+                atomicAdd(&sh.pt.cnt[kQ + q[r]], 1u);
+            }
+        }
+    }
+    uint64_t mn1, mx1, mn2, mx2;
+    block_range(sh, k, two ? k2 : nullptr, reff, m, mn1, mx1, mn2, mx2);
+    if (pw && t < 2 * kQ)
+        st_relaxed(&d.bstat[(uint64_t)bkt * 2 * kQ + t], (bkt == 0 ? kPre : kAgg) | sh.pt.cnt[t]);
+    // Two-key sorts: one pass by (k1, k2, index) where the bucket allows
+    // it. Otherwise stable passes: by arrival (ties: index order, which is
+    // entry order), then by k1 with the entries laid out in arrival order
+    // (skipped when the bucket holds one k1). FIFO: one pass by arrival.
+    const bool both = two && mn1 < mx1;
+    bool done = both && rank_pass(sh, k, k2, reff, m, mn1, mx1, rank);
+    if (!done) {
+        const uint32_t npass = both ? 2u : 1u;
+        for (uint32_t ps = 0; ps < npass; ps++) {
+            uint64_t lo = mn1, hi = mx1;
+            if (ps == 0 && two) {
+#pragma unroll
+                for (int r = 0; r < kBkR; r++) k[r] = k2[r];
+                lo = mn2;
+                hi = mx2;
+            }
+            if (ps == 1) {
+#pragma unroll
+                for (int r = 0; r < kBkR; r++) {
+                    const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
+                    if ((uint32_t)r < reff && idx < m) {
+                        sh.lkey[rank[r]] = reff == 1 ? a0 : src1[idx];
+                        sh.lj[rank[r]] = jv[r];
+                    }
+                }
+                __syncthreads();
+#pragma unroll
+                for (int r = 0; r < kBkR; r++) {
+                    const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
+                    k[r] = 0;
+                    jv[r] = 0;
+                    if ((uint32_t)r < reff && idx < m) {
+                        k[r] = sh.lkey[idx];
+                        jv[r] = sh.lj[idx];
+                    }
+                }
+                __syncthreads();
+            }
+            rank_pass(sh, k, nullptr, reff, m, lo, hi, rank);
+        }
+    }
+    if (pw) {
+        // the bucket's requests in FIFO order, and the digits' counts over
+        // the buckets before it
+#pragma unroll
+        for (int r = 0; r < kBkR; r++) {
+            const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
+            if ((uint32_t)r < reff && idx < m) {
+                sh.lq[rank[r]] = (uint8_t)q[r];
+                sh.lj[rank[r]] = jv[r];
+            }
+        }
+        if (t < 2 * kQ) {
+            uint32_t pre = 0;
+            if (bkt > 0) {
+                pre = look_back<2 * kQ>(d.bstat, bkt, t, &d.ctl->lb_err);
+                st_relaxed(&d.bstat[(uint64_t)bkt * 2 * kQ + t], kPre | (pre + sh.pt.cnt[t]));
+            }
+            sh.pt.pre[t] = pre;
+        }
+        __syncthreads();
+        uint32_t jf[kBkR], rc[kBkR], rt[kBkR];
+#pragma unroll
+        for (int r = 0; r < kBkR; r++) {
+            const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
+            const bool ok = (uint32_t)r < reff && idx < m;
+            q[r] = ok ? sh.lq[idx] : 0u;
+            jf[r] = ok ? sh.lj[idx] : 0u;
+        }
+        pw_rank(b, sh, q, reff, m, rc, rt);
+#pragma unroll
+        for (int r = 0; r < kBkR; r++) {
+            const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
+            if ((uint32_t)r < reff && idx < m) {
+                const uint32_t c = sh.pt.cls[q[r]];
+                pw_place(b, d, sh.pt, q[r], jf[r], sh.pt.pre[c] + sh.pt.wd[w][c] + rc[r],
+                         sh.pt.pre[kQ + q[r]] + sh.pt.wd[w][kQ + q[r]] + rt[r]);
+            }
+        }
+    }
+    if (d.out) {
+#pragma unroll
+        for (int r = 0; r < kBkR; r++) {
+            const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
+            if ((uint32_t)r < reff && idx < m && off + rank[r] < n) d.out[off + rank[r]] = jv[r];
+        }
     }
 }
 
@@ -1074,7 +1340,8 @@ uint64_t region_bytes(uint64_t n)
     const uint64_t nb = n_buckets(n);
     return align_up(sizeof(SsCtl), 256) + 2 * align_up(kSamples * 8, 256) + align_up(kSamples * 4, 256) +
            align_up(tiles * 256 * 4, 256) + 2 * align_up(nb * kCap * 8, 256) + align_up(nb * kCap * 4, 256) +
-           align_up(kQ * 4, 256) + 4 * align_up(n * 8, 256) + 2 * align_up(n * 4, 256);
+           align_up(kQ * 4, 256) + align_up(nb * 2 * kQ * 4, 256) + 4 * align_up(n * 8, 256) +
+           2 * align_up(n * 4, 256);
 }
 
 void carve(uint8_t *p, uint64_t n, SsDesc &d)
@@ -1095,6 +1362,7 @@ void carve(uint8_t *p, uint64_t n, SsDesc &d)
     d.bk2 = reinterpret_cast<uint64_t *>(take(nb * kCap * 8));
     d.bj = reinterpret_cast<uint32_t *>(take(nb * kCap * 4));
     d.tot = reinterpret_cast<uint32_t *>(take(kQ * 4));
+    d.bstat = reinterpret_cast<uint32_t *>(take(nb * 2 * kQ * 4));
     for (int i = 0; i < 2; i++) d.fk1[i] = reinterpret_cast<uint64_t *>(take(n * 8));
     for (int i = 0; i < 2; i++) d.fk2[i] = reinterpret_cast<uint64_t *>(take(n * 8));
     for (int i = 0; i < 2; i++) d.fj[i] = reinterpret_cast<uint32_t *>(take(n * 4));
@@ -1110,7 +1378,7 @@ size_t ssort_ws_bytes(uint64_t n, uint32_t nsorts)
 }
 
 hipError_t ssort_launch(const SortInput &in, const SortJob *jobs, uint32_t nsorts, bool serial, void *ws,
-                        hipStream_t s)
+                        hipStream_t s, const SsPartitions *parts)
 {
     if (in.n == 0 || nsorts == 0) return hipSuccess;
     if (nsorts > kSsMaxSorts || in.n > kSsMaxN) return hipErrorInvalidValue;
@@ -1130,11 +1398,15 @@ hipError_t ssort_launch(const SortInput &in, const SortJob *jobs, uint32_t nsort
     for (uint32_t i = 0; i < nsorts; i++) {
         SsDesc &d = b.s[i];
         const SortKind k = jobs[i].kind;
-        if (k != SortKind::Fifo && k != SortKind::Class && k != SortKind::Tier && k != SortKind::Budget &&
-            k != SortKind::Aging)
-            return hipErrorInvalidValue;
-        if (k == SortKind::Tier) b.tier_part = tier_part;
+        if (k != SortKind::Fifo && k != SortKind::Budget && k != SortKind::Aging) return hipErrorInvalidValue;
         d.kind = k;
+        if (k == SortKind::Fifo && parts && (parts->perm[0] || parts->perm[1])) {
+            b.tier_part = tier_part;
+            for (int e = 0; e < 2; e++) {
+                d.pw_out[e] = parts->perm[e];
+                d.pw_key[e] = parts->perm[e] ? parts->key[e] : nullptr;
+            }
+        }
         d.two = k != SortKind::Fifo;
         d.key_out = jobs[i].key_out;
         d.out = jobs[i].out;

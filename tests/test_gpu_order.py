@@ -70,10 +70,11 @@ def test_sizes_at_the_sample_sort_limit(ds, oracle, pol, n):
     check(ds, oracle, pol, tier, arr, bud, t_now=10.0, aging_rate=0.1)
 
 
-@pytest.mark.parametrize("pol", [0, 3, 4])
+@pytest.mark.parametrize("pol", POLICIES)
 @pytest.mark.parametrize("n", [1, 2, 700, 5000, 70001])
 def test_serial_sort(ds, oracle, pol, n):
     # the single-workgroup sort that takes over when a bucket overflows
+    # (Priority and Weighted are then placed by chunks of its FIFO order)
     tier, arr, bud = _batch(n + 5, n, q=0.01)
     check(ds, oracle, pol, tier, arr, bud, t_now=10.0, aging_rate=0.1, serial_sort=True)
 
@@ -101,9 +102,9 @@ def test_many_ties(ds, oracle, pol):
 @pytest.mark.parametrize("pol", POLICIES)
 @pytest.mark.parametrize("pattern", ["sawtooth", "descending", "blocks"])
 def test_run_patterns(ds, oracle, pol, pattern):
-    # key layouts across the 2048-request runs of the run-merge sort: every
-    # run holding the same keys, runs in descending order, and a few long
-    # stretches of equal keys crossing run boundaries
+    # key layouts across 2048-request tiles: every tile holding the same
+    # keys, tiles in descending order, and a few long stretches of equal
+    # keys crossing tile boundaries
     n = 3 * 2048 * 5 + 77
     j = np.arange(n)
     if pattern == "sawtooth":
@@ -116,6 +117,30 @@ def test_run_patterns(ds, oracle, pol, pattern):
     tier = rng.integers(0, 3, n).astype(np.uint8)
     bud = np.where(j % 3 == 0, 100.0, np.round(rng.uniform(1, 3000, n), 1))
     check(ds, oracle, pol, tier, arr, bud, t_now=float(arr.max()), aging_rate=0.05)
+
+
+@pytest.mark.parametrize("pol", POLICIES)
+@pytest.mark.parametrize("pattern", ["bands", "duplicates", "gapped"])
+def test_clustered_keys(ds, oracle, pol, pattern):
+    # keys in tight clusters with wide gaps between them, so that a bucket
+    # holding the end of one cluster and the start of the next has most of
+    # its keys in a few of its equal-width bins (split further by the
+    # entries' place in the bin); exact duplicates, which no split separates
+    # (two passes: by arrival, then by the key); and gapped arrivals for the
+    # one-key FIFO sort
+    n = 65536 + 123
+    rng = np.random.default_rng(n + len(pattern))
+    tier = rng.integers(0, 3, n).astype(np.uint8)
+    if pattern == "bands":
+        bud = rng.choice([100.0, 5000.0, 1e6], n) + rng.uniform(0.0, 0.5, n)
+        arr = rng.choice([0.0, 50.0], n) + rng.uniform(0.0, 1e-3, n)
+    elif pattern == "duplicates":
+        bud = rng.choice([100.0, 100.5, 5000.0], n)
+        arr = np.round(rng.uniform(0.0, 10.0, n) / 0.5) * 0.5
+    else:
+        arr = np.where(rng.random(n) < 0.9, rng.uniform(0.0, 1e-3, n), rng.uniform(1e3, 1e3 + 1.0, n))
+        bud = np.round(np.exp(rng.normal(6.0, 1.0, n)), 2)
+    check(ds, oracle, pol, tier, arr, bud, t_now=float(arr.max()), aging_rate=0.01)
 
 
 @pytest.mark.parametrize("pol", POLICIES)
