@@ -18,6 +18,10 @@
 //                 then runs the exact update t1 = (1 - alpha) c, t2 =
 //                 alpha r, c = t1 + t2 from its carried factor, in order, and
 //                 the traces are staged in LDS and written in event order.
+// When the table of chunk maps is small (C x G <= kSmallTable), k_calc_scan
+// is left out: each k_calc_apply block applies the maps of the chunks before
+// it to the initial factors itself (k_calc_agg keeps a copy of them), and
+// the last chunk's block writes the final factors.
 // Results match the sequential recurrence up to the rounding of the
 // composed maps (a few ulps; the contract is 1e-12 relative).
 #include "common.h"
@@ -33,6 +37,8 @@ constexpr int kW = kT / 64;
 constexpr uint32_t kG = kCalGroupsLds;   // groups held in LDS
 constexpr uint32_t kMaxTable = 1u << 20; // C x G entries at most (C >= 1)
 constexpr uint32_t kMaxChunks = 512;
+constexpr uint32_t kSmallTable = 16384;  // C x G up to which the carries are formed in k_calc_apply
+constexpr uint32_t kCarryR = 4;          // chunk maps per thread held in registers for the carry
 
 struct CalArgs {
     const uint32_t *group;
@@ -45,6 +51,8 @@ struct CalArgs {
     uint32_t passes;         // 8-bit LSD passes over the group key (key < 2^(8 passes))
     double *aggA, *aggB;     // [C][G]: M(c, g) = x -> A x + B; A < 0: no usable event
     double *carry;           // [C][G]: factor of g before chunk c
+    double *s0;              // [G] the initial factors (small tables: no k_calc_scan)
+    uint32_t small;          // C x G <= kSmallTable
     double *state;           // [G] in: before all events, out: after
     double *trace, *trace_before;
 };
@@ -73,6 +81,13 @@ __device__ __forceinline__ double shfl_up_d(double x, int d)
 {
     const long long v = __double_as_longlong(x);
     const int lo = __shfl_up((int)(uint32_t)v, d, 64), hi = __shfl_up((int)(uint32_t)(v >> 32), d, 64);
+    return __longlong_as_double((long long)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo));
+}
+
+__device__ __forceinline__ double shfl_down_d(double x, int d)
+{
+    const long long v = __double_as_longlong(x);
+    const int lo = __shfl_down((int)(uint32_t)v, d, 64), hi = __shfl_down((int)(uint32_t)(v >> 32), d, 64);
     return __longlong_as_double((long long)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo));
 }
 
@@ -271,6 +286,7 @@ __global__ __launch_bounds__(kT) void k_calc_agg(CalArgs a)
     for (uint32_t g = t; g < a.G; g += kT) {
         sA[g] = -1.0;
         sB[g] = 0.0;
+        if (a.small && c == 0) a.s0[g] = a.state[g];
     }
     const uint64_t c0 = (uint64_t)c * a.L;
     const uint64_t c1 = c0 + a.L < a.E ? c0 + a.L : a.E;
@@ -355,8 +371,49 @@ __global__ __launch_bounds__(kT) void k_calc_apply(CalArgs a)
     __shared__ SubShared sh;
     __shared__ double trb[kSub];   // trace_before staging (the trace goes to sh.b)
     __shared__ double sv[kG];      // each group's factor at the current point of the chunk
+    __shared__ uint8_t su[kG];     // small tables: the group has a usable event so far
     const uint32_t t = threadIdx.x, c = blockIdx.x;
-    for (uint32_t g = t; g < a.G; g += kT) sv[g] = a.carry[(uint64_t)c * a.G + g];
+    // small tables: the carry is the maps of the chunks before this one,
+    // composed in order (tpg threads per group, each over a contiguous range
+    // of at most kCarryR chunks, then an ordered tree of shuffles), applied
+    // to the initial factor; a chunk without usable events of the group
+    // leaves it untouched. The maps are loaded before the first sub-tile's
+    // events and composed after them, so that both loads are in flight
+    // together.
+    uint32_t tpg = 1;
+    while (tpg < 64 && tpg * 2 * a.G <= (uint32_t)kT) tpg *= 2;
+    const bool quick = a.small && a.G <= (uint32_t)kT / tpg && c <= tpg * kCarryR;
+    double cA[kCarryR], cB[kCarryR];
+    if (quick) {
+        const uint32_t g = t / tpg, p = t % tpg, jb = p * c / tpg, je = (p + 1) * c / tpg;
+#pragma unroll
+        for (int r = 0; r < (int)kCarryR; r++) {
+            const uint32_t j = jb + (uint32_t)r;
+            cA[r] = -1.0;
+            cB[r] = 0.0;
+            if (g < a.G && j < je) {
+                cA[r] = a.aggA[(uint64_t)j * a.G + g];
+                cB[r] = a.aggB[(uint64_t)j * a.G + g];
+            }
+        }
+    } else if (a.small) {
+        for (uint32_t g = t; g < a.G; g += kT) {
+            double v = a.s0[g];
+            bool u = false;
+            for (uint32_t j = 0; j < c; j++) {
+                const double A = a.aggA[(uint64_t)j * a.G + g], B = a.aggB[(uint64_t)j * a.G + g];
+                if (A >= 0.0) {
+                    const double tt = A * v;
+                    v = tt + B;
+                    u = true;
+                }
+            }
+            sv[g] = v;
+            su[g] = (uint8_t)u;
+        }
+    } else {
+        for (uint32_t g = t; g < a.G; g += kT) sv[g] = a.carry[(uint64_t)c * a.G + g];
+    }
     const uint64_t c0 = (uint64_t)c * a.L;
     const uint64_t c1 = c0 + a.L < a.E ? c0 + a.L : a.E;
     const double nan = __builtin_nan("");
@@ -365,6 +422,31 @@ __global__ __launch_bounds__(kT) void k_calc_apply(CalArgs a)
         const uint32_t m = (uint32_t)(c1 - s0 < kSub ? c1 - s0 : kSub);
         Sub sub;
         load_sort_scan(a, (uint32_t)s0, m, sh, sub);
+        if (quick && s0 == c0) {
+            const uint32_t g = t / tpg, p = t % tpg;
+            Map mp = {0u, 0u, 1.0, 0.0};
+#pragma unroll
+            for (int r = 0; r < (int)kCarryR; r++)
+                if (cA[r] >= 0.0) mp = combine(mp, Map{0u, 1u, cA[r], cB[r]});
+            for (uint32_t d = 1; d < tpg; d <<= 1) {
+                Map o;
+                o.f = 0u;
+                o.u = (uint32_t)__shfl_down((int)mp.u, (int)d, 64);
+                o.a = shfl_down_d(mp.a, (int)d);
+                o.b = shfl_down_d(mp.b, (int)d);
+                if (p % (2 * d) == 0) mp = combine(mp, o);
+            }
+            if (g < a.G && p == 0) {
+                double v = a.s0[g];
+                if (mp.u) {
+                    const double tt = mp.a * v;
+                    v = tt + mp.b;
+                }
+                sv[g] = v;
+                su[g] = (uint8_t)mp.u;
+            }
+            __syncthreads();
+        }
         // the factor before this thread's first position: the group's factor
         // at the sub-tile start, through the earlier positions of its
         // segment (their composed map, if any of them is usable)
@@ -387,6 +469,7 @@ __global__ __launch_bounds__(kT) void k_calc_apply(CalArgs a)
             const uint32_t g = sub.key[e];
             if (sub.flag[e]) cv = g < a.G ? sv[g] : nan;
             trb[sub.slot[e]] = cv;
+            if (a.small && sub.ok[e]) su[g] = 1;
             if (sub.ok[e]) {
                 // the exact sequential update
                 const double t1 = a.oma * cv;
@@ -411,6 +494,12 @@ __global__ __launch_bounds__(kT) void k_calc_apply(CalArgs a)
         }
         __syncthreads();
     }
+    if (a.small && c + 1 == a.C) {
+        // the factors after all events: the groups with a usable event in
+        // some chunk (the others keep theirs untouched)
+        for (uint32_t g = t; g < a.G; g += kT)
+            if (su[g]) a.state[g] = sv[g];
+    }
 }
 
 uint32_t sub_per_chunk(uint64_t E, uint32_t G)
@@ -428,7 +517,7 @@ size_t calc_ws_bytes(uint64_t n, uint32_t G)
 {
     const uint64_t L = (uint64_t)kSub * sub_per_chunk(n, G);
     const uint64_t C = cdiv(n ? n : 1, L);
-    return 3 * align_up(C * G * 8, 256);
+    return 3 * align_up(C * G * 8, 256) + align_up((uint64_t)G * 8, 256);
 }
 
 hipError_t calc_launch(const uint32_t *group, const double *est, const uint32_t *obs, uint32_t n,
@@ -453,11 +542,13 @@ hipError_t calc_launch(const uint32_t *group, const double *est, const uint32_t 
     a.aggA = reinterpret_cast<double *>(p);
     a.aggB = reinterpret_cast<double *>(p + tb);
     a.carry = reinterpret_cast<double *>(p + 2 * tb);
+    a.s0 = reinterpret_cast<double *>(p + 3 * tb);
+    a.small = (uint64_t)a.C * G <= kSmallTable ? 1u : 0u;
     a.state = state;
     a.trace = trace;
     a.trace_before = trace_before;
     hipLaunchKernelGGL(k_calc_agg, dim3(a.C), dim3(kT), 0, s, a);
-    hipLaunchKernelGGL(k_calc_scan, dim3((G + 3) / 4), dim3(256), 0, s, a);
+    if (!a.small) hipLaunchKernelGGL(k_calc_scan, dim3((G + 3) / 4), dim3(256), 0, s, a);
     hipLaunchKernelGGL(k_calc_apply, dim3(a.C), dim3(kT), 0, s, a);
     return hipGetLastError();
 }
