@@ -3,9 +3,9 @@
 // partition of the events by group, so that every access is coalesced.
 //
 // The events, in completion order, are cut into C chunks of L events (L a
-// multiple of 2048). With M(c, g) the composition of the affine maps
+// multiple of the sub-tile). With M(c, g) the composition of the affine maps
 // x -> (1 - alpha) x + alpha r of group g's events in chunk c (in order):
-//   k_calc_agg    per chunk (one block): each 2048-event sub-tile is sorted
+//   k_calc_agg    per chunk (one block): each sub-tile (512 or 2048 events) is sorted
 //                 by group in LDS (stable LSD passes, wave ballots), scanned
 //                 as a segmented scan of maps, and each group's part is
 //                 composed into that group's map in LDS; the chunk writes
@@ -31,8 +31,9 @@ namespace ds {
 namespace {
 
 constexpr int kT = 512;                  // threads per block
-constexpr int kE = 4;                    // events per thread per sub-tile
-constexpr uint32_t kSub = kT * kE;       // events per sub-tile
+// events per thread per sub-tile (kE) is a template parameter: 1 for the
+// small tables (more, shorter blocks), 4 otherwise; kSub = kT * kE events
+// per sub-tile
 constexpr int kW = kT / 64;
 constexpr uint32_t kG = kCalGroupsLds;   // groups held in LDS
 constexpr uint32_t kMaxTable = 1u << 20; // C x G entries at most (C >= 1)
@@ -113,7 +114,9 @@ __device__ __forceinline__ Map wave_scan(Map v)
     return v;
 }
 
+template <int kE>
 struct SubShared {
+    static constexpr uint32_t kSub = kT * kE;
     uint32_t wcnt[kW][256];
     uint32_t texcl[256];
     Map wagg[kW];
@@ -130,13 +133,15 @@ struct SubShared {
 // position continues a segment that starts at p < 4t, `excl`, the
 // composition of the maps of positions p .. 4t-1. sh.key keeps the sorted
 // keys.
+template <int kE>
 struct Sub {
     uint32_t key[kE], slot[kE], ok[kE], flag[kE];
     double b[kE];
     Map excl;
 };
 
-__device__ void load_sort_scan(const CalArgs &a, uint32_t s0, uint32_t m, SubShared &sh, Sub &out)
+template <int kE>
+__device__ void load_sort_scan(const CalArgs &a, uint32_t s0, uint32_t m, SubShared<kE> &sh, Sub<kE> &out)
 {
     const uint32_t t = threadIdx.x;
     const int w = (int)(t >> 6), lane = lane_id();
@@ -278,9 +283,11 @@ __device__ void load_sort_scan(const CalArgs &a, uint32_t s0, uint32_t m, SubSha
     out.excl = ex;
 }
 
+template <int kE>
 __global__ __launch_bounds__(kT) void k_calc_agg(CalArgs a)
 {
-    __shared__ SubShared sh;
+    constexpr uint32_t kSub = kT * kE;
+    __shared__ SubShared<kE> sh;
     __shared__ double sA[kG], sB[kG];   // the chunk's map per group so far (A < 0: none)
     const uint32_t t = threadIdx.x, c = blockIdx.x;
     for (uint32_t g = t; g < a.G; g += kT) {
@@ -292,8 +299,8 @@ __global__ __launch_bounds__(kT) void k_calc_agg(CalArgs a)
     const uint64_t c1 = c0 + a.L < a.E ? c0 + a.L : a.E;
     for (uint64_t s0 = c0; s0 < c1; s0 += kSub) {
         const uint32_t m = (uint32_t)(c1 - s0 < kSub ? c1 - s0 : kSub);
-        Sub sub;
-        load_sort_scan(a, (uint32_t)s0, m, sh, sub);   // (its first barrier orders the sA/sB writes)
+        Sub<kE> sub;
+        load_sort_scan<kE>(a, (uint32_t)s0, m, sh, sub);   // (its first barrier orders the sA/sB writes)
         // the segment of each group in this sub-tile, composed into the
         // group's map at the segment's last position (one thread per group)
         Map run = sub.excl;
@@ -366,26 +373,29 @@ __global__ __launch_bounds__(256) void k_calc_scan(CalArgs a)
     if (ce == a.C && cb < ce && touched) a.state[g] = v;
 }
 
+template <int kE>
 __global__ __launch_bounds__(kT) void k_calc_apply(CalArgs a)
 {
-    __shared__ SubShared sh;
+    constexpr uint32_t kSub = kT * kE;
+    __shared__ SubShared<kE> sh;
     __shared__ double trb[kSub];   // trace_before staging (the trace goes to sh.b)
     __shared__ double sv[kG];      // each group's factor at the current point of the chunk
     __shared__ uint8_t su[kG];     // small tables: the group has a usable event so far
     const uint32_t t = threadIdx.x, c = blockIdx.x;
     // small tables: the carry is the maps of the chunks before this one,
     // composed in order (tpg threads per group, each over a contiguous range
-    // of at most kCarryR chunks, then an ordered tree of shuffles), applied
-    // to the initial factor; a chunk without usable events of the group
-    // leaves it untouched. The maps are loaded before the first sub-tile's
-    // events and composed after them, so that both loads are in flight
-    // together.
+    // of chunks, kCarryR maps loaded at a time, then an ordered tree of
+    // shuffles), applied to the initial factor; a chunk without usable
+    // events of the group leaves it untouched. The first kCarryR maps are
+    // loaded before the first sub-tile's events and composed after them, so
+    // that both loads are in flight together.
     uint32_t tpg = 1;
     while (tpg < 64 && tpg * 2 * a.G <= (uint32_t)kT) tpg *= 2;
-    const bool quick = a.small && a.G <= (uint32_t)kT / tpg && c <= tpg * kCarryR;
+    const bool quick = a.small && a.G <= (uint32_t)kT / tpg;
     double cA[kCarryR], cB[kCarryR];
+    const uint32_t cjb = (t % tpg) * c / tpg, cje = (t % tpg + 1) * c / tpg;
     if (quick) {
-        const uint32_t g = t / tpg, p = t % tpg, jb = p * c / tpg, je = (p + 1) * c / tpg;
+        const uint32_t g = t / tpg, jb = cjb, je = cje;
 #pragma unroll
         for (int r = 0; r < (int)kCarryR; r++) {
             const uint32_t j = jb + (uint32_t)r;
@@ -420,14 +430,29 @@ __global__ __launch_bounds__(kT) void k_calc_apply(CalArgs a)
     double *tr = sh.b;
     for (uint64_t s0 = c0; s0 < c1; s0 += kSub) {
         const uint32_t m = (uint32_t)(c1 - s0 < kSub ? c1 - s0 : kSub);
-        Sub sub;
-        load_sort_scan(a, (uint32_t)s0, m, sh, sub);
+        Sub<kE> sub;
+        load_sort_scan<kE>(a, (uint32_t)s0, m, sh, sub);
         if (quick && s0 == c0) {
             const uint32_t g = t / tpg, p = t % tpg;
             Map mp = {0u, 0u, 1.0, 0.0};
 #pragma unroll
             for (int r = 0; r < (int)kCarryR; r++)
                 if (cA[r] >= 0.0) mp = combine(mp, Map{0u, 1u, cA[r], cB[r]});
+            for (uint32_t j0 = cjb + kCarryR; j0 < cje; j0 += kCarryR) {
+#pragma unroll
+                for (int r = 0; r < (int)kCarryR; r++) {
+                    const uint32_t j = j0 + (uint32_t)r;
+                    cA[r] = -1.0;
+                    cB[r] = 0.0;
+                    if (g < a.G && j < cje) {
+                        cA[r] = a.aggA[(uint64_t)j * a.G + g];
+                        cB[r] = a.aggB[(uint64_t)j * a.G + g];
+                    }
+                }
+#pragma unroll
+                for (int r = 0; r < (int)kCarryR; r++)
+                    if (cA[r] >= 0.0) mp = combine(mp, Map{0u, 1u, cA[r], cB[r]});
+            }
             for (uint32_t d = 1; d < tpg; d <<= 1) {
                 Map o;
                 o.f = 0u;
@@ -502,7 +527,7 @@ __global__ __launch_bounds__(kT) void k_calc_apply(CalArgs a)
     }
 }
 
-uint32_t sub_per_chunk(uint64_t E, uint32_t G)
+uint32_t sub_per_chunk(uint64_t E, uint32_t G, uint32_t kSub)
 {
     uint64_t cmax = kMaxTable / (G ? G : 1);
     cmax = cmax < kMaxChunks ? cmax : kMaxChunks;
@@ -513,10 +538,21 @@ uint32_t sub_per_chunk(uint64_t E, uint32_t G)
 
 }  // namespace
 
+// Chunking for kE events per thread: events per chunk and chunks.
+static void chunking(uint64_t n, uint32_t G, uint32_t e, uint32_t &L, uint32_t &C)
+{
+    const uint32_t sub = kT * e;
+    L = sub * sub_per_chunk(n, G, sub);
+    C = (uint32_t)cdiv(n ? n : 1, L);
+}
+
 size_t calc_ws_bytes(uint64_t n, uint32_t G)
 {
-    const uint64_t L = (uint64_t)kSub * sub_per_chunk(n, G);
-    const uint64_t C = cdiv(n ? n : 1, L);
+    // the larger of the two chunkings' tables
+    uint32_t L1, C1, L4, C4;
+    chunking(n, G, 1, L1, C1);
+    chunking(n, G, 4, L4, C4);
+    const uint64_t C = C1 > C4 ? C1 : C4;
     return 3 * align_up(C * G * 8, 256) + align_up((uint64_t)G * 8, 256);
 }
 
@@ -534,8 +570,11 @@ hipError_t calc_launch(const uint32_t *group, const double *est, const uint32_t 
     a.G = G;
     a.alpha = alpha;
     a.oma = 1.0 - alpha;
-    a.L = kSub * sub_per_chunk(n, G);
-    a.C = (uint32_t)cdiv(n, a.L);
+    // sub-tiles of 512 events when the table of chunk maps stays small (the
+    // carries are then formed in k_calc_apply), else of 2048
+    chunking(n, G, 1, a.L, a.C);
+    a.small = (uint64_t)a.C * G <= kSmallTable ? 1u : 0u;
+    if (!a.small) chunking(n, G, 4, a.L, a.C);
     a.passes = G < 256 ? 1u : 2u;   // keys 0..G fit in 8 or 16 bits
     uint8_t *p = static_cast<uint8_t *>(ws);
     const uint64_t tb = align_up((uint64_t)a.C * G * 8, 256);
@@ -543,13 +582,17 @@ hipError_t calc_launch(const uint32_t *group, const double *est, const uint32_t 
     a.aggB = reinterpret_cast<double *>(p + tb);
     a.carry = reinterpret_cast<double *>(p + 2 * tb);
     a.s0 = reinterpret_cast<double *>(p + 3 * tb);
-    a.small = (uint64_t)a.C * G <= kSmallTable ? 1u : 0u;
     a.state = state;
     a.trace = trace;
     a.trace_before = trace_before;
-    hipLaunchKernelGGL(k_calc_agg, dim3(a.C), dim3(kT), 0, s, a);
-    if (!a.small) hipLaunchKernelGGL(k_calc_scan, dim3((G + 3) / 4), dim3(256), 0, s, a);
-    hipLaunchKernelGGL(k_calc_apply, dim3(a.C), dim3(kT), 0, s, a);
+    if (a.small) {
+        hipLaunchKernelGGL(k_calc_agg<1>, dim3(a.C), dim3(kT), 0, s, a);
+        hipLaunchKernelGGL(k_calc_apply<1>, dim3(a.C), dim3(kT), 0, s, a);
+    } else {
+        hipLaunchKernelGGL(k_calc_agg<4>, dim3(a.C), dim3(kT), 0, s, a);
+        hipLaunchKernelGGL(k_calc_scan, dim3((G + 3) / 4), dim3(256), 0, s, a);
+        hipLaunchKernelGGL(k_calc_apply<4>, dim3(a.C), dim3(kT), 0, s, a);
+    }
     return hipGetLastError();
 }
 
