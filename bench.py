@@ -1,21 +1,24 @@
 """Benchmark of the DriftSched admission hot path on one MI355X.
 
 One step = the whole hot path over one batch already resident in HBM:
-characterize (word counts of every prompt), calibrate (EMA factors from the
-batch's completion events), score (budgets and classes), and the dispatch
-orders of all five policies (FIFO first; the other four reuse its
-permutation). Default workload: 65,536 requests, 64 tenants, 32-2,048-word
-prompts (the synthetic batch64k workload).
+calibrate (EMA factors from the batch's completion events), characterize
+and score (word counts of every prompt, then budgets and classes, fused in
+one call: ds_characterize_score; --separate makes them the two calls), and
+the dispatch orders of all five policies (one batch of sample sorts).
+Default workload: 65,536 requests, 64 tenants, 32-2,048-word prompts (the
+synthetic batch64k workload).
 
 Prints one JSON line: whole-step throughput in requests/s, the roofline of
-the dominant stage (characterize, HBM-bound) from HIP events on the stream it
-runs on, and the single-threaded CPU oracle's throughput on a bounded sample.
+the dominant stage (characterize + score, HBM-bound) from HIP events on the
+stream it runs on, and the single-threaded CPU oracle's throughput on a
+bounded sample.
 The timed steps are eager launches on one stream (stage times come from
 steps with events between the stages, run first); --graph times replays of
 one step captured in a HIP graph instead (the same launches, measured a few
-percent slower than eager launches here). --schedule overlap runs the stages along their
-dependencies on two streams instead (calibrate and the FIFO, Priority,
-Weighted and Aging orders beside characterize; score and SJF after both).
+percent slower than eager launches here). --schedule overlap runs the
+stages along their dependencies on two streams instead (the FIFO, Priority,
+Weighted and Aging orders beside calibrate and characterize + score; SJF
+after both).
 """
 import argparse
 import json
@@ -60,6 +63,9 @@ def parse():
                     help="overlap: stages that do not depend on each other run on two streams "
                          "(calibrate and the budget-free orders beside characterize); serial: "
                          "the four stages one after another on one stream")
+    ap.add_argument("--separate", action="store_true",
+                    help="stages 1 and 3 as the two calls ds_characterize and ds_score instead of "
+                         "the fused ds_characterize_score (the same results)")
     ap.add_argument("--graph", action="store_true",
                     help="time replays of one step captured in a HIP graph instead of eager "
                          "launches (the same kernels)")
@@ -137,23 +143,32 @@ def main():
     alpha = b.alphas[0]
     torch.cuda.synchronize()
 
+    def char_score():
+        """Stages 1 and 3: one fused call, or the two calls (--separate)."""
+        if args.separate:
+            ds.characterize(text, offsets, counts=counts, ws=ws[ds.OP_CHARACTERIZE])
+            ds.score(counts, category, tenant, group, t_base, s_tenant, state, out=sc_out)
+        else:
+            ds.characterize_score(text, offsets, category, tenant, group, t_base, s_tenant, state,
+                                  counts=counts, out=sc_out, ws=ws[ds.OP_CHARACTERIZE])
+
     def step(ev=None):
-        """The four stages one after another on the current stream."""
+        """The stages one after another on the current stream: calibrate
+        (its factors are final before scoring), characterize + score, the
+        five orders."""
         if ev: ev[0].record()
-        ds.characterize(text, offsets, counts=counts, ws=ws[ds.OP_CHARACTERIZE])
-        if ev: ev[1].record()
         ds.calibrate(ev_group, ev_est, ev_obs, alpha, state, trace=trace, ws=ws[ds.OP_CALIBRATE])
+        if ev: ev[1].record()
+        char_score()
         if ev: ev[2].record()
-        ds.score(counts, category, tenant, group, t_base, s_tenant, state, out=sc_out)
-        if ev: ev[3].record()
         ds.order_multi(ALL, tier, arrival, sc_out[2], params=params, perms=perm_map,
                        ws=ws[ds.OP_ORDER_MULTI])
-        if ev: ev[4].record()
+        if ev: ev[3].record()
 
-    # The same work along the stages' dependencies: calibrate reads only the
-    # completion events, and FIFO, Priority, Weighted and Aging only tiers and
-    # arrivals, so they run on a second stream beside characterize; score
-    # joins both, and SJF (budget-keyed) reuses the FIFO permutation.
+    # The same work along the stages' dependencies: FIFO, Priority, Weighted
+    # and Aging read only tiers and arrivals, so they run on a second stream
+    # beside calibrate and characterize + score; SJF (budget-keyed) follows
+    # both and reuses the FIFO permutation.
     aux = torch.cuda.Stream()
     ws_aux = ds.workspace(ds.OP_ORDER_MULTI, N, b.n_groups)
     budget = sc_out[2]
@@ -162,12 +177,10 @@ def main():
         main_s = torch.cuda.current_stream()
         aux.wait_stream(main_s)
         with torch.cuda.stream(aux):
-            ds.calibrate(ev_group, ev_est, ev_obs, alpha, state, trace=trace,
-                         ws=ws[ds.OP_CALIBRATE])
             ds.order_multi((0, 1, 2, 4), tier, arrival, params=params, perms=perm_map, ws=ws_aux)
-        ds.characterize(text, offsets, counts=counts, ws=ws[ds.OP_CHARACTERIZE])
+        ds.calibrate(ev_group, ev_est, ev_obs, alpha, state, trace=trace, ws=ws[ds.OP_CALIBRATE])
+        char_score()
         main_s.wait_stream(aux)
-        ds.score(counts, category, tenant, group, t_base, s_tenant, state, out=sc_out)
         ds.order_multi((3,), tier, arrival, budget, fifo=perms[0], params=params, perms=perm_map,
                        ws=ws[ds.OP_ORDER_MULTI])
 
@@ -179,7 +192,7 @@ def main():
     torch.cuda.synchronize()
 
     # stage times: serial steps with events between the stages
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -225,9 +238,9 @@ def main():
         for a, b_ in zip(eager, [perms[i] for i in (0, 1, 2, 4)] + [counts]):
             assert torch.equal(a, b_), "graph replay differs from the eager step"
 
-    stage_ms = np.zeros(4)
+    stage_ms = np.zeros(3)
     for e in evs:
-        for s in range(4):
+        for s in range(3):
             stage_ms[s] += e[s].elapsed_time(e[s + 1])
     stage_ms /= args.steps
     ms_per_step = wall * 1e3 / args.steps
@@ -236,9 +249,12 @@ def main():
     # algorithmic bytes (what the method must move) per stage
     char_bytes = B + 8 * (N + 1) + 4 * N
     cal_bytes = 16 * N + 8 * N + 16 * b.n_groups
-    score_bytes = (4 + 1 + 4 + 4) * N + (8 + 8 + 8 + 1) * N
+    # score: category, tenant, group read; est_base, est, budget, class
+    # written (the two separate calls read the counts back as well)
+    score_bytes = (1 + 4 + 4) * N + (8 + 8 + 8 + 1) * N + (4 * N if args.separate else 0)
     order_bytes = (12 + 13 + 13 + 20 + 13) * N
-    char_gbs = char_bytes / (stage_ms[0] * 1e-3) / 1e9
+    cs_bytes = char_bytes + score_bytes
+    char_gbs = cs_bytes / (stage_ms[1] * 1e-3) / 1e9
     total_gbs = (char_bytes + cal_bytes + score_bytes + order_bytes) / (ms_per_step * 1e-3) / 1e9
 
     # sanity: the counts of the last step equal the generator's word counts
@@ -269,12 +285,14 @@ def main():
                    "events": N, "policies": 5, "description": wl.note},
         "hbm_gbs_step": round(total_gbs, 1),
         "hbm_frac_step": round(total_gbs / HBM_PEAK_GBS, 4),
-        "stages_ms": {"characterize": round(stage_ms[0], 4), "calibrate": round(stage_ms[1], 4),
-                      "score": round(stage_ms[2], 4), "order_x5": round(stage_ms[3], 4)},
-        "roofline": {"kernel": "characterize (k_char_main + k_char_fin)",
+        "stages_ms": {"calibrate": round(stage_ms[0], 4), "characterize_score": round(stage_ms[1], 4),
+                      "order_x5": round(stage_ms[2], 4)},
+        "fused_characterize_score": not args.separate,
+        "roofline": {"kernel": "characterize + score (k_char_main + k_char_fin)" if not args.separate
+                     else "characterize + score (k_char_main + k_char_fin, k_score)",
                      "bound": "hbm", "achieved": round(char_gbs, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(char_gbs / HBM_PEAK_GBS, 4),
-                     "algorithmic_bytes": int(char_bytes),
+                     "algorithmic_bytes": int(cs_bytes),
                      "traffic": measured_traffic(wl.name)},
         "cpu_baseline": cpu,
     }

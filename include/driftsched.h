@@ -138,6 +138,25 @@ ds_status ds_characterize(const uint8_t *text, uint64_t text_bytes,
                           void *ws, size_t ws_bytes, uint32_t flags, ds_stream stream);
 
 /*
+ * Stages 1 and 3 in one pass: the results of ds_characterize followed by
+ * ds_score on its counts, bit for bit, with each request scored as soon as
+ * its count is known (no second launch, no second read of the counts).
+ * Arguments as in those two calls (the counts are written as by
+ * ds_characterize; state, if calibrated in the same step, must be final
+ * before this call). Workspace: ds_workspace_bytes(DS_OP_CHARACTERIZE, n, 0).
+ * Errors: those of either call; with DS_VALIDATE both calls' checks run.
+ */
+ds_status ds_characterize_score(const uint8_t *text, uint64_t text_bytes,
+                                const uint64_t *offsets, uint32_t n, uint32_t *counts,
+                                const uint8_t *category, const uint32_t *tenant,
+                                const uint32_t *group, const double *t_base, uint32_t n_cat,
+                                const double *s_tenant, uint32_t n_tenants,
+                                const double *state, uint32_t n_groups,
+                                const ds_score_params *params, double *est_base, double *est,
+                                double *budget, uint8_t *job_class, void *ws, size_t ws_bytes,
+                                uint32_t flags, ds_stream stream);
+
+/*
  * Stage 2: calibration factors, Eq. (5) with the ratio of Eq. (6)
  * (Sec. "Runtime Calibration and Feedback Adaptation").
  *

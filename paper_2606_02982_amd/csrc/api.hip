@@ -158,6 +158,47 @@ ds_status ds_score(uint32_t n, const uint32_t *counts, const uint8_t *category,
     });
 }
 
+ds_status ds_characterize_score(const uint8_t *text, uint64_t text_bytes, const uint64_t *offsets,
+                                uint32_t n, uint32_t *counts, const uint8_t *category,
+                                const uint32_t *tenant, const uint32_t *group, const double *t_base,
+                                uint32_t n_cat, const double *s_tenant, uint32_t n_tenants,
+                                const double *state, uint32_t n_groups, const ds_score_params *params,
+                                double *est_base, double *est, double *budget, uint8_t *job_class,
+                                void *ws, size_t ws_bytes, uint32_t flags, ds_stream stream)
+{
+    // the checks of ds_characterize and of ds_score
+    if (n == 0xFFFFFFFFu) return DS_ERR_SIZE;
+    if (!params) return DS_ERR_NULL;
+    if (!(params->f_ref > 0.0) || isnan(params->short_max) || isnan(params->medium_max))
+        return DS_ERR_ARG;
+    if (n_cat == 0 || n_tenants == 0 || n_groups == 0) return DS_ERR_ARG;
+    if (n == 0) return DS_OK;
+    if (!offsets || !counts || (text_bytes > 0 && !text)) return DS_ERR_NULL;
+    if (!category || !tenant || !group || !t_base || !s_tenant || !state || !est || !budget || !job_class)
+        return DS_ERR_NULL;
+    if (text && !aligned(text, 16)) return DS_ERR_ALIGN;
+    if (!aligned(offsets, 8) || !aligned(counts, 4)) return DS_ERR_ALIGN;
+    if (!aligned(tenant, 4) || !aligned(group, 4) || !aligned(t_base, 8) || !aligned(s_tenant, 8) ||
+        !aligned(state, 8) || !aligned(est, 8) || !aligned(budget, 8) || (est_base && !aligned(est_base, 8)))
+        return DS_ERR_ALIGN;
+    if (text_bytes >= (1ull << 46)) return DS_ERR_SIZE;
+    ds_status st = check_ws(ws, ws_bytes, ds_workspace_bytes(DS_OP_CHARACTERIZE, n, 0));
+    if (st != DS_OK) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    ScoreArgs sc = {n, counts, category, tenant, group, t_base, n_cat, s_tenant, n_tenants, state, n_groups,
+                    params->f_ref, params->short_max, params->medium_max, est_base, est, budget, job_class};
+    return run(ws, flags, s, [&](uint32_t *flag) {
+        if (flag) {
+            hipError_t e = char_launch(text, text_bytes, offsets, n, counts, after_flag(ws), flag, s);
+            if (e != hipSuccess) return e;
+            return score_launch(n, counts, category, tenant, group, t_base, n_cat, s_tenant, n_tenants, state,
+                                n_groups, params->f_ref, params->short_max, params->medium_max, est_base, est,
+                                budget, job_class, flag, s);
+        }
+        return char_launch(text, text_bytes, offsets, n, counts, after_flag(ws), nullptr, s, &sc);
+    });
+}
+
 static ds_status check_order_params(const ds_order_params *params, uint32_t mask)
 {
     if (!params) return DS_ERR_NULL;

@@ -32,6 +32,7 @@
 // atomics; results are exact integers independent of scheduling.
 #include "common.h"
 #include "kernels.h"
+#include "scoremath.h"
 
 namespace ds {
 namespace {
@@ -642,17 +643,21 @@ __global__ __launch_bounds__(kBlock, 7) void k_char_main(const uint8_t *__restri
 // counts[i] from the per-boundary local prefixes and the per-wave totals:
 // the word starts of [a, b) are the starts after a in a's wave, those of the
 // whole waves in between, and the starts before b in b's wave.
+// Per prompt: the word count from the waves' totals and the boundary
+// positions; with sc.n != 0 the request is also scored (stage 3) from that
+// count.
 __global__ __launch_bounds__(256) void k_char_fin(const uint64_t *__restrict__ off, uint32_t N,
                                                   uint64_t B, uint32_t rw_kib, uint32_t nwaves,
                                                   const uint64_t *__restrict__ wavetot,
                                                   const uint32_t *__restrict__ ploc,
-                                                  uint32_t *__restrict__ counts)
+                                                  uint32_t *__restrict__ counts, ScoreArgs sc)
 {
     for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < N;
          i += (uint64_t)gridDim.x * blockDim.x) {
         uint64_t a = off[i], b = off[i + 1];
         if (b <= a || a >= B) {
             counts[i] = 0;
+            if (sc.n) score_one(sc, (uint32_t)i, 0u);
             continue;
         }
         uint32_t wa = (uint32_t)(a >> 10) / rw_kib;
@@ -667,7 +672,9 @@ __global__ __launch_bounds__(256) void k_char_fin(const uint64_t *__restrict__ o
         }
         uint64_t sum = tail;
         for (uint32_t w = wa; w < wb && w < nwaves; w++) sum += wavetot[w];
-        counts[i] = (uint32_t)(sum - ploc[i]);
+        const uint32_t cnt = (uint32_t)(sum - ploc[i]);
+        counts[i] = cnt;
+        if (sc.n) score_one(sc, (uint32_t)i, cnt);
     }
 }
 
@@ -691,7 +698,7 @@ size_t char_ws_bytes(uint64_t n)
 }
 
 hipError_t char_launch(const uint8_t *text, uint64_t B, const uint64_t *offsets, uint32_t n,
-                       uint32_t *counts, void *ws, uint32_t *flag, hipStream_t s)
+                       uint32_t *counts, void *ws, uint32_t *flag, hipStream_t s, const ScoreArgs *score)
 {
     uint8_t *p = static_cast<uint8_t *>(ws);
     uint32_t *ploc = reinterpret_cast<uint32_t *>(p);
@@ -733,7 +740,8 @@ hipError_t char_launch(const uint8_t *text, uint64_t B, const uint64_t *offsets,
     uint32_t fblocks = (uint32_t)(fb < 4096 ? fb : 4096);
     if (fblocks)
         hipLaunchKernelGGL(k_char_fin, dim3(fblocks), dim3(256), 0, s, offsets, n, B,
-                           (uint32_t)(Rw >> 10), nwaves, wavetot, ploc, counts);
+                           (uint32_t)(Rw >> 10), nwaves, wavetot, ploc, counts,
+                           score ? *score : ScoreArgs{});
     return hipGetLastError();
 }
 

@@ -7,12 +7,32 @@
 
 namespace ds {
 
+// ---- stage 3 arguments (also taken by the fused stage 1 + 3) ------------------
+struct ScoreArgs {
+    uint32_t n;
+    const uint32_t *counts;
+    const uint8_t *category;
+    const uint32_t *tenant;
+    const uint32_t *group;
+    const double *t_base;
+    uint32_t n_cat;
+    const double *s_tenant;
+    uint32_t n_tenants;
+    const double *state;
+    uint32_t n_groups;
+    double f_ref, short_max, medium_max;
+    double *est_base, *est, *budget;
+    uint8_t *job_class;
+};
+
 // ---- stage 1: characterize -------------------------------------------------
 size_t char_ws_bytes(uint64_t n);
-// flag: device word set non-zero by the validation kernel (NULL: no checks)
+// flag: device word set non-zero by the validation kernel (NULL: no checks).
+// score (or NULL): also score each request as its count is written, with
+// these arguments (their counts pointer is not used).
 hipError_t char_launch(const uint8_t *text, uint64_t text_bytes, const uint64_t *offsets,
                        uint32_t n, uint32_t *counts, void *ws, uint32_t *flag,
-                       hipStream_t s);
+                       hipStream_t s, const ScoreArgs *score = nullptr);
 
 // ---- radix sort machinery ----------------------------------------------------
 // Producers of (key, value) pairs for the sorts used by calibrate and order.

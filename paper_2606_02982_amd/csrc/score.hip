@@ -1,59 +1,17 @@
-// Stage 3: calibrated output estimate, token budget and runtime class.
-//
-// Eq. (2) in the order Alg. 1 gathers its factors (T_base, then B_runtime,
-// then S_tenant, then F_input), Eq. (1) T_budget = T_input + estimate, and
-// the class thresholds of Eq. (4). Elementwise; the library is built with
-// -ffp-contract=off, so every product and sum is rounded separately.
+// Stage 3: calibrated output estimate, token budget and runtime class
+// (Eq. (2), Eq. (1), Eq. (4); the per-request arithmetic is score_one).
+// Elementwise.
 #include "common.h"
 #include "kernels.h"
+#include "scoremath.h"
 
 namespace ds {
 namespace {
 
-struct ScoreArgs {
-    uint32_t n;
-    const uint32_t *counts;
-    const uint8_t *category;
-    const uint32_t *tenant;
-    const uint32_t *group;
-    const double *t_base;
-    uint32_t n_cat;
-    const double *s_tenant;
-    uint32_t n_tenants;
-    const double *state;
-    uint32_t n_groups;
-    double f_ref, short_max, medium_max;
-    double *est_base, *est, *budget;
-    uint8_t *job_class;
-};
-
 __global__ __launch_bounds__(256) void k_score(ScoreArgs a)
 {
-    const double nan = __builtin_nan("");
-    for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < a.n; i += gridDim.x * blockDim.x) {
-        const uint32_t cat = a.category[i], ten = a.tenant[i], g = a.group[i];
-        const double words = (double)a.counts[i];
-        const bool ok = cat < a.n_cat && ten < a.n_tenants && g < a.n_groups;
-        const double tb = ok ? a.t_base[cat] : nan;
-        const double s = ok ? a.s_tenant[ten] : nan;
-        const double b = ok ? a.state[g] : nan;
-        const double F = 1.0 + words / a.f_ref;
-        double e = tb * b;
-        e = e * s;
-        e = e * F;
-        if (a.est_base) {
-            double e0 = tb * s;
-            e0 = e0 * F;
-            a.est_base[i] = e0;
-        }
-        a.est[i] = e;
-        const double total = words + e;
-        a.budget[i] = total;
-        uint8_t c = 2;
-        if (total <= a.short_max) c = 0;
-        else if (total <= a.medium_max) c = 1;
-        a.job_class[i] = c;
-    }
+    for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < a.n; i += gridDim.x * blockDim.x)
+        score_one(a, i, a.counts[i]);
 }
 
 __global__ void k_score_validate(ScoreArgs a, uint32_t *__restrict__ flag)

@@ -63,6 +63,8 @@ def _load():
     lib.ds_class_histogram.argtypes = [u32, P, u32, P, P, P, sz, u32, P]
     lib.ds_score.argtypes = [u32, P, P, P, P, P, u32, P, u32, P, u32, ctypes.POINTER(ScoreParams),
                              P, P, P, P, P, sz, u32, P]
+    lib.ds_characterize_score.argtypes = [P, u64, P, u32, P, P, P, P, P, u32, P, u32, P, u32,
+                                          ctypes.POINTER(ScoreParams), P, P, P, P, P, sz, u32, P]
     lib.ds_order.argtypes = [i32, u32, P, P, P, P, ctypes.POINTER(OrderParams), P, P, P, sz, u32, P]
     lib.ds_order_multi.argtypes = [u32, u32, P, P, P, P, ctypes.POINTER(OrderParams),
                                    ctypes.POINTER(P), ctypes.POINTER(P), P, sz, u32, P]
@@ -246,6 +248,39 @@ def score(counts, category, tenant, group, t_base, s_tenant, state, f_ref=1024.0
                         ctypes.byref(p), _ptr(est_base), _ptr(est), _ptr(budget), _ptr(cls),
                         _ptr(ws), ws.numel() if ws is not None else 0, _flags(validate), _stream()))
     return est_base, est, budget, cls
+
+
+def characterize_score(text, offsets, category, tenant, group, t_base, s_tenant, state,
+                       f_ref=1024.0, short_max=128.0, medium_max=512.0, want_est_base=True,
+                       counts=None, out=None, ws=None, validate=False):
+    """``characterize`` then ``score`` on its counts, in one pass (the same
+    results). Returns (counts, (est_base, est, budget, class))."""
+    _dev(text, torch.uint8, "text")
+    _dev(offsets, torch.int64, "offsets")
+    for t, dt, name in ((category, torch.uint8, "category"), (tenant, torch.int32, "tenant"),
+                        (group, torch.int32, "group"), (t_base, torch.float64, "t_base"),
+                        (s_tenant, torch.float64, "s_tenant"), (state, torch.float64, "state")):
+        _dev(t, dt, name)
+    n = offsets.numel() - 1
+    dev = offsets.device
+    if counts is None:
+        counts = torch.empty(max(n, 0), dtype=torch.int32, device=dev)
+    _dev(counts, torch.int32, "counts")
+    if out is None:
+        m = max(n, 0)
+        est_base = torch.empty(m, dtype=torch.float64, device=dev) if want_est_base else None
+        out = (est_base, torch.empty(m, dtype=torch.float64, device=dev),
+               torch.empty(m, dtype=torch.float64, device=dev), torch.empty(m, dtype=torch.uint8, device=dev))
+    est_base, est, budget, cls = out
+    if ws is None:
+        ws = workspace(OP_CHARACTERIZE, n, 0, dev)
+    p = ScoreParams(float(f_ref), float(short_max), float(medium_max))
+    _check(lib.ds_characterize_score(_ptr(text) if text.numel() else None, text.numel(), _ptr(offsets), n,
+                                     _ptr(counts), _ptr(category), _ptr(tenant), _ptr(group), _ptr(t_base),
+                                     t_base.numel(), _ptr(s_tenant), s_tenant.numel(), _ptr(state),
+                                     state.numel(), ctypes.byref(p), _ptr(est_base), _ptr(est), _ptr(budget),
+                                     _ptr(cls), _ptr(ws), ws.numel(), _flags(validate), _stream()))
+    return counts, out
 
 
 def order_params(n_tiers=3, weights=(4, 2, 1), tier_priority=(0.0, 1.0, 2.0), aging_rate=0.01,

@@ -25,8 +25,8 @@ def declared_functions():
 
 def test_exports_every_declared_symbol(ds):
     names = declared_functions()
-    assert names == ["ds_calibrate", "ds_calibrate_ex", "ds_characterize", "ds_class_histogram",
-                     "ds_error_stats", "ds_order", "ds_order_multi", "ds_score",
+    assert names == ["ds_calibrate", "ds_calibrate_ex", "ds_characterize", "ds_characterize_score",
+                     "ds_class_histogram", "ds_error_stats", "ds_order", "ds_order_multi", "ds_score",
                      "ds_simulate", "ds_status_string", "ds_version", "ds_workspace_bytes"]
     for name in names:
         assert hasattr(ds.lib, name), name
@@ -195,3 +195,23 @@ def test_simulate_host_errors(ds):
     assert call(ok, wsb=ds.workspace_bytes(ds.OP_SIMULATE, 10) - 1) == -4
     # t_now is not used: each tick ages to its own time
     assert call(ds.sim_params("aging", t_now=float("nan")), wsb=64) == -4
+
+
+def test_characterize_score_host_errors(ds):
+    f = ds.lib.ds_characterize_score
+    good = ds.ScoreParams(1024.0, 128.0, 512.0)
+    bad = ds.ScoreParams(0.0, 128.0, 512.0)
+    # category, tenant, group, t_base, n_cat, s_tenant, n_tenants, state, n_groups
+    sc = [FAKE, FAKE, FAKE, FAKE, 4, FAKE, 3, FAKE, 3]
+    outs = [NULL, FAKE, FAKE, FAKE]   # est_base, est, budget, class
+    ws = 1 << 30
+    assert f(FAKE, 16, FAKE, 4, FAKE, *sc, ctypes.byref(bad), *outs, FAKE_WS, ws, 0, NULL) == -2
+    assert f(FAKE, 16, FAKE, 4, FAKE, *sc, None, *outs, FAKE_WS, ws, 0, NULL) == -1
+    assert f(FAKE, 16, NULL, 4, FAKE, *sc, ctypes.byref(good), *outs, FAKE_WS, ws, 0, NULL) == -1
+    assert f(FAKE, 16, FAKE, 4, FAKE, NULL, *sc[1:], ctypes.byref(good), *outs, FAKE_WS, ws, 0, NULL) == -1
+    assert f(FAKE, 16, FAKE, 4, FAKE, *sc[:4], 0, *sc[5:], ctypes.byref(good), *outs, FAKE_WS, ws, 0,
+             NULL) == -2
+    assert f(P(0x1001), 16, FAKE, 4, FAKE, *sc, ctypes.byref(good), *outs, FAKE_WS, ws, 0, NULL) == -7
+    assert f(FAKE, 16, FAKE, 4, FAKE, *sc, ctypes.byref(good), *outs, FAKE_WS, 16, 0, NULL) == -4
+    assert f(FAKE, 16, FAKE, 0xFFFFFFFF, FAKE, *sc, ctypes.byref(good), *outs, FAKE_WS, ws, 0, NULL) == -3
+    assert f(NULL, 0, NULL, 0, NULL, *sc, ctypes.byref(good), *outs, NULL, 0, 0, NULL) == 0
