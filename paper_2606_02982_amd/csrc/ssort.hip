@@ -743,6 +743,8 @@ __device__ __forceinline__ bool rank_pass(BkShared &sh, uint64_t *k, const uint6
 #pragma unroll
         for (int r = 0; r < kBkR; r++) rank[r] += before_w;
         __syncthreads();   // sh.wsum is reused by the bin scan
+    } else {
+        __syncthreads();   // the bins are zero before any count goes in
     }
     if (kmn2 >= kmx) {
         // two distinct keys: each in entry order
@@ -1221,7 +1223,12 @@ __global__ __launch_bounds__(kBkTPB) void k_ss_bucket(SsBatch b)
         }
     }
     uint64_t mn1, mx1, mn2, mx2;
-    block_range(sh, k, two ? k2 : nullptr, reff, m, mn1, mx1, mn2, mx2);
+    // (two calls, so that k2 is never behind a pointer chosen at run time,
+    // which would move the array out of registers)
+    if (two)
+        block_range(sh, k, k2, reff, m, mn1, mx1, mn2, mx2);
+    else
+        block_range(sh, k, nullptr, reff, m, mn1, mx1, mn2, mx2);
     if (pw && t < 2 * kQ)
         st_relaxed(&d.bstat[(uint64_t)bkt * 2 * kQ + t], (bkt == 0 ? kPre : kAgg) | sh.pt.cnt[t]);
     // Two-key sorts: one pass by (k1, k2, index) where the bucket allows
