@@ -22,6 +22,7 @@ _LIB_PATH = os.path.join(_HERE, "liboracle.so")
 _lib = None
 
 FIFO, PRIORITY, WEIGHTED, SJF, AGING = 0, 1, 2, 3, 4
+WEIGHTED_SMOOTH = 5   # the smooth weighted round robin reading of Weighted
 
 
 def build(force=True):

@@ -314,7 +314,8 @@ int dsref_score(uint64_t n, const uint32_t *counts, const uint8_t *category,
 /* Dispatch orders                                                           */
 /* ------------------------------------------------------------------------ */
 
-enum { REF_FIFO = 0, REF_PRIORITY = 1, REF_WEIGHTED = 2, REF_SJF = 3, REF_AGING = 4 };
+enum { REF_FIFO = 0, REF_PRIORITY = 1, REF_WEIGHTED = 2, REF_SJF = 3, REF_AGING = 4,
+       REF_WEIGHTED_SMOOTH = 5 };
 
 /* Sort context: primary key (may be NULL), then arrival, then index. */
 struct sort_ctx {
@@ -368,6 +369,16 @@ static void sort_requests(uint32_t *perm, uint32_t n, const double *primary,
  *            lower first, where p = tier_priority[tier] and a = arrival:
  *            waiting lowers the score (Sec. "Aging Priority Scheduling").
  *            key = e.
+ *  Weighted, smooth (policy 5; a reading of the same section: the paper
+ *            fixes the ratio and the cyclic dispatch, not how the tiers
+ *            interleave inside a cycle): the smooth weighted round robin.
+ *            Every queue holds a credit, 0 at the start. Before each
+ *            dispatch every non-empty queue's credit grows by its weight;
+ *            the queue with the largest credit (the lowest tier on ties)
+ *            dispatches its head and gives up the sum of the weights of the
+ *            non-empty queues. A queue that runs empty leaves with its
+ *            credit. key = floor(k / weight) for the k-th request of its
+ *            tier, as for Weighted.
  * Returns -1 on a tier >= n_tiers, a zero weight or an unknown policy.
  */
 int dsref_order(int policy, uint32_t n, const uint8_t *tier, const double *arrival,
@@ -410,7 +421,7 @@ int dsref_order(int policy, uint32_t n, const uint8_t *tier, const double *arriv
         free(e);
         return 0;
     }
-    if (policy == REF_WEIGHTED) {
+    if (policy == REF_WEIGHTED || policy == REF_WEIGHTED_SMOOTH) {
         for (uint32_t q = 0; q < n_tiers; q++)
             if (weight[q] == 0) return -1;
         /* tier queues in FIFO order */
@@ -428,6 +439,28 @@ int dsref_order(int policy, uint32_t n, const uint8_t *tier, const double *arriv
         }
         memset(head, 0, sizeof(uint32_t) * n_tiers);
         uint32_t pos = 0;
+        if (policy == REF_WEIGHTED_SMOOTH) {
+            long long *credit = (long long *)calloc(n_tiers, sizeof(long long));
+            while (pos < n) {
+                long long total = 0;
+                for (uint32_t q = 0; q < n_tiers; q++)
+                    if (head[q] < len[q]) total += weight[q];
+                int best = -1;
+                for (uint32_t q = 0; q < n_tiers; q++) {
+                    if (head[q] >= len[q]) continue;
+                    credit[q] += weight[q];
+                    if (best < 0 || credit[q] > credit[best]) best = (int)q;
+                }
+                credit[best] -= total;
+                uint32_t i = queue[start[best] + head[best]];
+                perm[pos++] = i;
+                if (key) key[i] = (double)(head[best] / weight[best]);
+                head[best]++;
+            }
+            free(credit);
+            free(fifo); free(len); free(start); free(head); free(queue);
+            return 0;
+        }
         double round = 0.0;
         while (pos < n) {
             for (uint32_t q = 0; q < n_tiers; q++) {
