@@ -376,9 +376,10 @@ static void sort_requests(uint32_t *perm, uint32_t n, const double *primary,
  *            dispatch every non-empty queue's credit grows by its weight;
  *            the queue with the largest credit (the lowest tier on ties)
  *            dispatches its head and gives up the sum of the weights of the
- *            non-empty queues. A queue that runs empty leaves with its
- *            credit. key = floor(k / weight) for the k-th request of its
- *            tier, as for Weighted.
+ *            non-empty queues. When a queue runs empty it leaves and a new
+ *            cycle begins over the queues left: every credit returns to 0.
+ *            key = floor(k / weight) for the k-th request of its tier, as
+ *            for Weighted.
  * Returns -1 on a tier >= n_tiers, a zero weight or an unknown policy.
  */
 int dsref_order(int policy, uint32_t n, const uint8_t *tier, const double *arrival,
@@ -456,6 +457,8 @@ int dsref_order(int policy, uint32_t n, const uint8_t *tier, const double *arriv
                 perm[pos++] = i;
                 if (key) key[i] = (double)(head[best] / weight[best]);
                 head[best]++;
+                if (head[best] == len[best])   /* a new cycle over the queues left */
+                    memset(credit, 0, sizeof(long long) * n_tiers);
             }
             free(credit);
             free(fifo); free(len); free(start); free(head); free(queue);
