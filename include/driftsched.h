@@ -113,7 +113,14 @@ typedef struct {
     double aging_rate;                   /* DS_AGING: priority units per second, >= 0 */
     double t_now;                        /* DS_AGING: current time (same clock as arrival) */
     double aging_floor;                  /* DS_AGING: lower clamp of the aged score (may be -inf) */
+    uint32_t weighted_mode;              /* DS_WEIGHTED: DS_WRR_BLOCKED or DS_WRR_SMOOTH */
 } ds_order_params;
+
+/* ds_order_params.weighted_mode: how the tiers interleave inside a cycle */
+#define DS_WRR_BLOCKED 0u                /* each tier's share of a round in one block */
+#define DS_WRR_SMOOTH 1u                 /* smooth interleaving; weights sum to at most
+                                            DS_WRR_MAX_WEIGHT_SUM */
+#define DS_WRR_MAX_WEIGHT_SUM 1024u
 
 /*
  * Stage 1: whitespace-proxy word counts (Sec. "Workload Characterization and
@@ -225,10 +232,20 @@ ds_status ds_score(uint32_t n, const uint32_t *counts, const uint8_t *category,
  *  DS_FIFO      key (arrival, index)                   (Sec. "FIFO Scheduling")
  *  DS_PRIORITY  key (tier_priority[tier], FIFO rank): the exact order of the
  *               score priority * 10^12 + arrival       (Sec. "Priority Scheduling")
- *  DS_WEIGHTED  blocked cyclic round robin: round r serves, for q = 0, 1, ...,
- *               the requests of tier q with FIFO rank within the tier in
- *               [r w_q, (r+1) w_q); empty queues are passed over
- *                                                      (Sec. "Weighted Scheduling")
+ *  DS_WEIGHTED  cyclic weighted round robin over the tier queues (Sec.
+ *               "Weighted Scheduling"). The paper fixes the ratio w_q and the
+ *               cyclic service; params->weighted_mode picks how the tiers
+ *               interleave inside a cycle:
+ *               DS_WRR_BLOCKED  round r serves, for q = 0, 1, ..., the
+ *                 requests of tier q with FIFO rank within the tier in
+ *                 [r w_q, (r+1) w_q); empty queues are passed over
+ *               DS_WRR_SMOOTH  before each dispatch every non-empty queue's
+ *                 credit grows by w_q; the largest credit (lowest tier on
+ *                 ties) is served and gives up W, the sum of the non-empty
+ *                 queues' weights; credits start at 0, and when a queue runs
+ *                 empty a new cycle begins over the rest with every credit
+ *                 at 0. W <= DS_WRR_MAX_WEIGHT_SUM (else DS_ERR_ARG)
+ *               key: floor(k / w_q) for the k-th request of tier q in both modes
  *  DS_SJF       key (budget, FIFO rank)                (Sec. "Shortest-Job-First Scheduling")
  *  DS_AGING     key (e, FIFO rank), e = max(aging_floor,
  *               tier_priority[tier] - aging_rate * max(0, t_now - arrival))

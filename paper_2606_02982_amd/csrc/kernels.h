@@ -46,6 +46,7 @@ enum class SortKind : int {
 };
 
 constexpr uint32_t kMaxSorts = 4;   // sorts of one batch (same length, same launches)
+constexpr uint32_t kWrrMaxWeightSum = 1024;   // smooth round robin: largest sum of the weights
 
 // Inputs and parameters shared by the sorts of a batch.
 struct SortInput {
@@ -59,6 +60,7 @@ struct SortInput {
     uint32_t cls[16];          // Class: priority class of each tier
     double prio[16];           // Aging/Class keys
     uint32_t weight[16];       // Tier: weighted round robin
+    uint32_t wrr_smooth;       // Tier: the smooth interleaving (weights sum <= kWrrMaxWeightSum)
     double aging_rate, t_now, aging_floor;
 };
 
@@ -123,6 +125,7 @@ struct OrderArgs {
     const uint32_t *fifo_in;
     uint32_t n_tiers;
     uint32_t weight[16];
+    uint32_t wrr_smooth;       // Weighted: smooth interleaving
     double prio[16];
     double aging_rate, t_now, aging_floor;
     uint32_t *perm[5];
@@ -153,6 +156,7 @@ struct SimArgs {
     double f_ref;
     uint32_t n_tiers;
     uint32_t weight[16];
+    uint32_t wrr_smooth;       // Weighted: smooth interleaving
     double prio[16];
     double aging_rate, aging_floor;
     double *state;

@@ -5,7 +5,8 @@
 //   FIFO      order of (arrival, index)
 //   Priority  stable partition of the FIFO sequence by priority class
 //   Weighted  stable partition by tier, then each request goes straight to
-//             its cyclic round-robin position (closed form of the round)
+//             its cyclic round-robin position (closed form of the round, or
+//             of the smooth interleaving's period table)
 //   SJF       stable sort of the FIFO sequence by budget
 //   Aging     stable sort of the FIFO sequence by the aged score
 // Up to kSsMaxN requests FIFO, SJF and Aging are sample sorts by the
@@ -95,6 +96,7 @@ hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_
         in.prio[q] = a.prio[q];
         in.weight[q] = a.weight[q];
     }
+    in.wrr_smooth = a.wrr_smooth;
     in.aging_rate = a.aging_rate;
     in.t_now = a.t_now;
     in.aging_floor = a.aging_floor;

@@ -8,7 +8,7 @@
 // that has not been dispatched. It is ordered by the policy (ties in FIFO
 // order) with the factors as they stand: SJF scores budgets (Eq. (1), (2))
 // from the current factors, Aging ages to t_k, Weighted starts a fresh
-// round-robin cycle over the pending tier queues. The first min(batch,
+// round-robin cycle over the pending tier queues (blocked or smooth). The first min(batch,
 // pending) requests are dispatched, and their completions (observed length
 // against the B-free admission estimate) update the factors in dispatch
 // order before the next tick.
@@ -32,6 +32,7 @@
 //     sequential evaluation.
 #include "common.h"
 #include "kernels.h"
+#include "wrrplan.h"
 
 namespace ds {
 namespace {
@@ -74,6 +75,7 @@ struct EngineArgs {
     const Aux *aux;
     const uint8_t *val;
     uint32_t weight[kMaxQ];
+    uint32_t wrr_smooth;       // Weighted: smooth interleaving
     double alpha, aging_rate, aging_floor;
     double *state;
     uint32_t *list[2];
@@ -294,6 +296,27 @@ __global__ __launch_bounds__(kTPB) void k_sim_engine(EngineArgs a)
         // 3. list positions of the first m requests of the order
         if (policy == kFifo) {
             if (tid < m) s_selpos[tid] = tid;
+        } else if (policy == kWeighted && a.wrr_smooth) {
+            // the first m dispatches of a fresh smooth cycle, one per step,
+            // by one wave (lane q = tier q); a queue running empty starts a
+            // new cycle over the rest
+            if (w == 0) {
+                const uint32_t len = lane < nq ? s_cnt[lane] : 0u;
+                const uint32_t wq = lane < nq ? s_wt[lane] : 0u;
+                uint32_t served = 0;
+                int32_t credit = 0;
+                uint32_t W = wave_sum(len ? wq : 0u);
+                for (uint32_t pos = 0; pos < m; pos++) {
+                    const int b = wrr_pick(credit, served < len, wq, W);
+                    const bool mine = lane == (uint32_t)b;
+                    if (mine) s_selpos[pos] = s_big.first[lane][served];   // served < m <= batch
+                    served += mine ? 1u : 0u;
+                    if (__ballot(mine && served == len) != 0ull) {
+                        credit = 0;
+                        W = wave_sum(served < len ? wq : 0u);
+                    }
+                }
+            }
         } else if (queued) {
             for (uint32_t p = tid; p < nq * batch; p += kTPB) {
                 const uint32_t q = p / batch, r = p - q * batch;
@@ -608,6 +631,7 @@ hipError_t sim_launch(const SimArgs &a, void *ws, uint32_t *flag, hipStream_t s)
     ea.aux = aux;
     ea.val = val;
     for (uint32_t q = 0; q < kMaxQ; q++) ea.weight[q] = q < a.n_tiers && a.weight[q] ? a.weight[q] : 1u;
+    ea.wrr_smooth = a.wrr_smooth;
     ea.alpha = a.alpha;
     ea.aging_rate = a.aging_rate;
     ea.aging_floor = a.aging_floor;

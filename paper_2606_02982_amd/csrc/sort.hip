@@ -29,6 +29,7 @@
 #include "kernels.h"
 #include "keys.h"
 #include "lookback.h"
+#include "wrrplan.h"
 
 namespace ds {
 namespace {
@@ -54,6 +55,7 @@ struct SortDesc {
     uint64_t *key[2];
     uint32_t *val[2];
     uint32_t *status;      // [passes][tiles][256]
+    WrrPlan *plan;         // Tier, smooth round robin: the period table (built by k_sort_plan)
 };
 
 struct SortBatch {
@@ -164,6 +166,13 @@ __global__ __launch_bounds__(256) void k_sort_plan(SortBatch b)
     int full = __syncthreads_or(c == b.n ? 1 : 0);
     d.ctl->excl[p][t] = block_excl_scan256(c, tmp4);
     if (t == 0) d.ctl->active[p] = full ? 0u : 1u;
+    if (d.kind == SortKind::Tier && b.in.wrr_smooth && t < 64) {
+        // the smooth interleaving's period table (digit t = tier t)
+        __shared__ uint16_t per[kWrrMaxWeightSum];
+        const uint32_t nq = b.in.n_tiers < kWrrTiers ? b.in.n_tiers : kWrrTiers;
+        const bool tl = t < nq;
+        wrr_plan_build(tl ? c : 0u, tl ? b.in.weight[t] : 0u, per, d.plan);
+    }
 }
 
 // Weighted round robin position of the k-th (FIFO) request of tier q:
@@ -323,12 +332,28 @@ __global__ __launch_bounds__(TPB) void k_sort_pass(SortBatch b, uint32_t p)
     if (d.kind == SortKind::Tier) {
         // single pass: digit = tier; scatter to the weighted position
         const uint32_t *tstart = ctl->excl[0];
+        WrrPlanHead &wh = *reinterpret_cast<WrrPlanHead *>(&wcnt[0][0]);   // the counters are done
+        static_assert(sizeof(WrrPlanHead) <= sizeof(wcnt), "plan header fits the counters");
+        const bool smooth = b.in.wrr_smooth != 0;
+        if (smooth) {
+            __syncthreads();
+            for (uint32_t i = t; i < sizeof(WrrPlanHead) / 4; i += TPB)
+                reinterpret_cast<uint32_t *>(&wh)[i] = reinterpret_cast<const uint32_t *>(&d.plan->h)[i];
+            __syncthreads();
+        }
         for (uint32_t s = t; s < cnt; s += TPB) {
             uint32_t q = (uint32_t)lkey[s] & 255u;
             uint32_t g = gbase[q] + s - texcl[q];
             uint64_t kq = g - ctl->excl[0][q];
             uint64_t rnd;
-            uint64_t pos = wrr_pos(b.in, tstart, n, q, kq, rnd);
+            uint64_t pos;
+            if (smooth) {
+                uint32_t r32;
+                pos = wrr_smooth_pos(wh, d.plan->off, b.in.weight[q & 15u], q & 15u, (uint32_t)kq, r32);
+                rnd = r32;
+            } else {
+                pos = wrr_pos(b.in, tstart, n, q, kq, rnd);
+            }
             uint32_t val = lval[s];
             if (pos < n) d.out[pos] = val;   // always true when tiers are < n_tiers
             if (d.key_out && val < n) d.key_out[val] = (double)rnd;
@@ -356,7 +381,7 @@ uint64_t region_bytes(uint64_t n)
     uint64_t tiles = cdiv(n, tile_keys(n));
     return align_up(sizeof(SortCtl), 256) + align_up((uint64_t)kInitBlocks * kMaxPasses * 256 * 4, 256) +
            2 * align_up(n * 8, 256) + 2 * align_up(n * 4, 256) +
-           align_up((uint64_t)kMaxPasses * tiles * 256 * 4, 256);
+           align_up((uint64_t)kMaxPasses * tiles * 256 * 4, 256) + align_up(sizeof(WrrPlan), 256);
 }
 
 void carve(uint8_t *p, uint64_t n, SortDesc &d)
@@ -374,6 +399,8 @@ void carve(uint8_t *p, uint64_t n, SortDesc &d)
         p += align_up(n * 4, 256);
     }
     d.status = reinterpret_cast<uint32_t *>(p);
+    p += align_up((uint64_t)kMaxPasses * cdiv(n, tile_keys(n)) * 256 * 4, 256);
+    d.plan = reinterpret_cast<WrrPlan *>(p);
 }
 
 }  // namespace

@@ -53,6 +53,7 @@
 #include "kernels.h"
 #include "lookback.h"
 #include "tiercount.h"
+#include "wrrplan.h"
 
 namespace ds {
 namespace {
@@ -110,6 +111,7 @@ struct SsBatch {
     uint32_t nsorts;       // sorts of the batch (grid rows)
     uint32_t nsb;          // blocks of k_ss_sample per sort
     uint32_t *tier_part;   // [nsb][kQ] tier counts of slices (when the partitions are wanted)
+    WrrPlan *plan;         // smooth round robin: the period table (built by the scatter)
     SsDesc s[kSsMaxSorts];
 };
 
@@ -445,6 +447,14 @@ __global__ __launch_bounds__(kScTPB) void k_ss_scatter(SsBatch b)
         }
         __syncthreads();
         if (t < kQ) d.tot[t] = texcl[t];
+        if (d.pw_out[1] && b.in.wrr_smooth && w == 0) {
+            // the smooth interleaving's period table, by one wave (the
+            // tile's keys are out, so lj serves as its scratch)
+            const uint32_t nq = b.in.n_tiers < kQ ? b.in.n_tiers : kQ;
+            const bool tl = (uint32_t)lane < nq;
+            wrr_plan_build(tl ? texcl[lane] : 0u, tl ? b.in.weight[lane] : 0u, reinterpret_cast<uint16_t *>(lj),
+                           b.plan);
+        }
     }
 }
 
@@ -459,6 +469,7 @@ struct PwTable {
     uint32_t cnt[2 * kQ];            // this bucket's (or chunk's) digit counts
     uint32_t pre[2 * kQ];            // the digits' counts before it
     uint32_t wd[kBkTPB / 64][2 * kQ];   // per-wave digit counters
+    WrrPlanHead wh;                  // smooth round robin: the phases of the period table
 };
 
 // The round-robin position of the k-th request (in FIFO order) of tier q,
@@ -494,7 +505,8 @@ __device__ __forceinline__ void pw_place(const SsBatch &b, const SsDesc &d, cons
     }
     if (d.pw_out[1]) {
         uint32_t rnd;
-        const uint64_t pos = weighted_pos(pt, b.in.n_tiers < kQ ? b.in.n_tiers : kQ, q, kt, rnd);
+        const uint64_t pos = b.in.wrr_smooth ? wrr_smooth_pos(pt.wh, b.plan->off, pt.weight[q], q, kt, rnd)
+                                             : weighted_pos(pt, b.in.n_tiers < kQ ? b.in.n_tiers : kQ, q, kt, rnd);
         if (pos < b.n) d.pw_out[1][pos] = j;
         if (d.pw_key[1]) d.pw_key[1][j] = (double)rnd;
     }
@@ -994,6 +1006,9 @@ __device__ __forceinline__ void load_pw(const SsBatch &b, const SsDesc &d, BkSha
     }
     if (t < 2 * kQ) sh.pt.cnt[t] = 0;
     for (uint32_t i = t; i < (kBkTPB / 64) * 2 * kQ; i += kBkTPB) (&sh.pt.wd[0][0])[i] = 0;
+    if (d.pw_out[1] && b.in.wrr_smooth)
+        for (uint32_t i = t; i < sizeof(WrrPlanHead) / 4; i += kBkTPB)
+            reinterpret_cast<uint32_t *>(&sh.pt.wh)[i] = reinterpret_cast<const uint32_t *>(&b.plan->h)[i];
     __syncthreads();
     if (t < kQ) {
         uint32_t s = 0;
@@ -1381,7 +1396,9 @@ uint64_t tier_part_bytes(uint64_t n) { return align_up((uint64_t)sample_blocks(n
 
 size_t ssort_ws_bytes(uint64_t n, uint32_t nsorts)
 {
-    return n <= kSsMaxN ? (size_t)(tier_part_bytes(n) + (uint64_t)nsorts * region_bytes(n)) : 0;
+    return n <= kSsMaxN ? (size_t)(tier_part_bytes(n) + align_up(sizeof(WrrPlan), 256) +
+                                   (uint64_t)nsorts * region_bytes(n))
+                        : 0;
 }
 
 hipError_t ssort_launch(const SortInput &in, const SortJob *jobs, uint32_t nsorts, bool serial, void *ws,
@@ -1402,6 +1419,8 @@ hipError_t ssort_launch(const SortInput &in, const SortJob *jobs, uint32_t nsort
     uint8_t *p = static_cast<uint8_t *>(ws);
     uint32_t *tier_part = reinterpret_cast<uint32_t *>(p);
     p += tier_part_bytes(in.n);
+    b.plan = reinterpret_cast<WrrPlan *>(p);
+    p += align_up(sizeof(WrrPlan), 256);
     for (uint32_t i = 0; i < nsorts; i++) {
         SsDesc &d = b.s[i];
         const SortKind k = jobs[i].kind;

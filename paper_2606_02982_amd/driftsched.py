@@ -24,6 +24,8 @@ OP_ERROR_STATS, OP_CLASS_HIST, OP_SIMULATE = 5, 6, 7
 DS_VALIDATE = 1
 DS_SERIAL_SORT = 2
 MAX_TIERS = 16
+WRR_BLOCKED, WRR_SMOOTH = 0, 1   # ds_order_params.weighted_mode
+WRR_MAX_WEIGHT_SUM = 1024
 MAX_BATCH = 1024
 
 
@@ -41,7 +43,8 @@ class ScoreParams(ctypes.Structure):
 class OrderParams(ctypes.Structure):
     _fields_ = [("n_tiers", ctypes.c_uint32), ("weight", ctypes.c_uint32 * MAX_TIERS),
                 ("tier_priority", ctypes.c_double * MAX_TIERS), ("aging_rate", ctypes.c_double),
-                ("t_now", ctypes.c_double), ("aging_floor", ctypes.c_double)]
+                ("t_now", ctypes.c_double), ("aging_floor", ctypes.c_double),
+                ("weighted_mode", ctypes.c_uint32)]
 
 
 class SimParams(ctypes.Structure):
@@ -284,7 +287,11 @@ def characterize_score(text, offsets, category, tenant, group, t_base, s_tenant,
 
 
 def order_params(n_tiers=3, weights=(4, 2, 1), tier_priority=(0.0, 1.0, 2.0), aging_rate=0.01,
-                 t_now=0.0, aging_floor=0.0):
+                 t_now=0.0, aging_floor=0.0, weighted_mode=WRR_BLOCKED):
+    """ds_order_params. weighted_mode: WRR_BLOCKED or WRR_SMOOTH (or their
+    names "blocked", "smooth")."""
+    if isinstance(weighted_mode, str):
+        weighted_mode = {"blocked": WRR_BLOCKED, "smooth": WRR_SMOOTH}[weighted_mode]
     p = OrderParams()
     p.n_tiers = int(n_tiers)
     for q in range(MAX_TIERS):
@@ -293,6 +300,7 @@ def order_params(n_tiers=3, weights=(4, 2, 1), tier_priority=(0.0, 1.0, 2.0), ag
     p.aging_rate = float(aging_rate)
     p.t_now = float(t_now)
     p.aging_floor = float(aging_floor)
+    p.weighted_mode = int(weighted_mode)
     return p
 
 
