@@ -23,6 +23,7 @@ _lib = None
 
 FIFO, PRIORITY, WEIGHTED, SJF, AGING = 0, 1, 2, 3, 4
 WEIGHTED_SMOOTH = 5   # the smooth weighted round robin reading of Weighted
+WEIGHTED_STRIDE = 6   # the stride scheduling reading of Weighted
 
 
 def build(force=True):

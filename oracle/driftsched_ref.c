@@ -315,7 +315,7 @@ int dsref_score(uint64_t n, const uint32_t *counts, const uint8_t *category,
 /* ------------------------------------------------------------------------ */
 
 enum { REF_FIFO = 0, REF_PRIORITY = 1, REF_WEIGHTED = 2, REF_SJF = 3, REF_AGING = 4,
-       REF_WEIGHTED_SMOOTH = 5 };
+       REF_WEIGHTED_SMOOTH = 5, REF_WEIGHTED_STRIDE = 6 };
 
 /* Sort context: primary key (may be NULL), then arrival, then index. */
 struct sort_ctx {
@@ -380,6 +380,13 @@ static void sort_requests(uint32_t *perm, uint32_t n, const double *primary,
  *            cycle begins over the queues left: every credit returns to 0.
  *            key = floor(k / weight) for the k-th request of its tier, as
  *            for Weighted.
+ *  Weighted, stride (policy 6; another reading of the same section):
+ *            stride scheduling. Queue q advances its pass by the stride
+ *            1 / weight[q], starting from one stride; the non-empty queue
+ *            with the smallest pass (the lowest tier on ties) dispatches its
+ *            head and advances. Passes are compared exactly, as the
+ *            fractions they are (no fixed-point stride). key as for
+ *            Weighted.
  * Returns -1 on a tier >= n_tiers, a zero weight or an unknown policy.
  */
 int dsref_order(int policy, uint32_t n, const uint8_t *tier, const double *arrival,
@@ -422,7 +429,7 @@ int dsref_order(int policy, uint32_t n, const uint8_t *tier, const double *arriv
         free(e);
         return 0;
     }
-    if (policy == REF_WEIGHTED || policy == REF_WEIGHTED_SMOOTH) {
+    if (policy == REF_WEIGHTED || policy == REF_WEIGHTED_SMOOTH || policy == REF_WEIGHTED_STRIDE) {
         for (uint32_t q = 0; q < n_tiers; q++)
             if (weight[q] == 0) return -1;
         /* tier queues in FIFO order */
@@ -461,6 +468,25 @@ int dsref_order(int policy, uint32_t n, const uint8_t *tier, const double *arriv
                     memset(credit, 0, sizeof(long long) * n_tiers);
             }
             free(credit);
+            free(fifo); free(len); free(start); free(head); free(queue);
+            return 0;
+        }
+        if (policy == REF_WEIGHTED_STRIDE) {
+            while (pos < n) {
+                /* the pass of queue q is (head[q] + 1) / weight[q]: compare
+                   a / w_a < b / w_b as a w_b < b w_a (below 2^62) */
+                int best = -1;
+                for (uint32_t q = 0; q < n_tiers; q++) {
+                    if (head[q] >= len[q]) continue;
+                    if (best < 0 || (uint64_t)(head[q] + 1) * weight[best] <
+                                        (uint64_t)(head[best] + 1) * weight[q])
+                        best = (int)q;
+                }
+                uint32_t i = queue[start[best] + head[best]];
+                perm[pos++] = i;
+                if (key) key[i] = (double)(head[best] / weight[best]);
+                head[best]++;
+            }
             free(fifo); free(len); free(start); free(head); free(queue);
             return 0;
         }
