@@ -113,13 +113,14 @@ typedef struct {
     double aging_rate;                   /* DS_AGING: priority units per second, >= 0 */
     double t_now;                        /* DS_AGING: current time (same clock as arrival) */
     double aging_floor;                  /* DS_AGING: lower clamp of the aged score (may be -inf) */
-    uint32_t weighted_mode;              /* DS_WEIGHTED: DS_WRR_BLOCKED or DS_WRR_SMOOTH */
+    uint32_t weighted_mode;              /* DS_WEIGHTED: DS_WRR_BLOCKED, _SMOOTH or _STRIDE */
 } ds_order_params;
 
 /* ds_order_params.weighted_mode: how the tiers interleave inside a cycle */
 #define DS_WRR_BLOCKED 0u                /* each tier's share of a round in one block */
 #define DS_WRR_SMOOTH 1u                 /* smooth interleaving; weights sum to at most
                                             DS_WRR_MAX_WEIGHT_SUM */
+#define DS_WRR_STRIDE 2u                 /* stride scheduling */
 #define DS_WRR_MAX_WEIGHT_SUM 1024u
 
 /*
@@ -245,7 +246,10 @@ ds_status ds_score(uint32_t n, const uint32_t *counts, const uint8_t *category,
  *                 queues' weights; credits start at 0, and when a queue runs
  *                 empty a new cycle begins over the rest with every credit
  *                 at 0. W <= DS_WRR_MAX_WEIGHT_SUM (else DS_ERR_ARG)
- *               key: floor(k / w_q) for the k-th request of tier q in both modes
+ *               DS_WRR_STRIDE  stride scheduling: the k-th request of tier q
+ *                 (FIFO rank within the tier) has pass (k+1) / w_q, compared
+ *                 exactly; smaller pass first, equal passes by lower tier
+ *               key: floor(k / w_q) for the k-th request of tier q in every mode
  *  DS_SJF       key (budget, FIFO rank)                (Sec. "Shortest-Job-First Scheduling")
  *  DS_AGING     key (e, FIFO rank), e = max(aging_floor,
  *               tier_priority[tier] - aging_rate * max(0, t_now - arrival))

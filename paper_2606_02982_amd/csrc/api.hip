@@ -8,6 +8,9 @@
 #include "kernels.h"
 
 static_assert(DS_WRR_MAX_WEIGHT_SUM == ds::kWrrMaxWeightSum, "smooth round robin weight bound");
+static_assert(DS_WRR_BLOCKED == ds::kWrrBlocked && DS_WRR_SMOOTH == ds::kWrrSmooth &&
+                  DS_WRR_STRIDE == ds::kWrrStride,
+              "weighted modes");
 
 using namespace ds;
 
@@ -212,7 +215,7 @@ static ds_status check_order_params(const ds_order_params *params, uint32_t mask
         wsum += params->weight[q];
     }
     if (mask & (1u << DS_WEIGHTED)) {
-        if (params->weighted_mode > DS_WRR_SMOOTH) return DS_ERR_ARG;
+        if (params->weighted_mode > DS_WRR_STRIDE) return DS_ERR_ARG;
         if (params->weighted_mode == DS_WRR_SMOOTH && wsum > DS_WRR_MAX_WEIGHT_SUM) return DS_ERR_ARG;
     }
     if ((mask & (1u << DS_AGING)) &&
@@ -258,7 +261,7 @@ static ds_status order_common(uint32_t mask, uint32_t n, const uint8_t *tier,
     a.aging_rate = params->aging_rate;
     a.t_now = params->t_now;
     a.aging_floor = params->aging_floor;
-    a.wrr_smooth = (mask & (1u << DS_WEIGHTED)) && params->weighted_mode == DS_WRR_SMOOTH ? 1u : 0u;
+    a.wrr_mode = (mask & (1u << DS_WEIGHTED)) ? params->weighted_mode : kWrrBlocked;
     a.serial_sort = (flags & DS_SERIAL_SORT) != 0;
     for (int p = 0; p < 5; p++) {
         a.perm[p] = ((mask >> p) & 1u) ? perms[p] : nullptr;
@@ -392,7 +395,7 @@ ds_status ds_simulate(uint32_t n, const double *arrival, const uint8_t *tier,
         a.weight[q] = q < a.n_tiers ? params->order.weight[q] : 1u;
         a.prio[q] = q < a.n_tiers ? params->order.tier_priority[q] : 0.0;
     }
-    a.wrr_smooth = policy == DS_WEIGHTED && params->order.weighted_mode == DS_WRR_SMOOTH ? 1u : 0u;
+    a.wrr_mode = policy == DS_WEIGHTED ? params->order.weighted_mode : kWrrBlocked;
     a.aging_rate = params->order.aging_rate;
     a.aging_floor = params->order.aging_floor;
     a.state = state;

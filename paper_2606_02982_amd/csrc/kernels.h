@@ -47,6 +47,8 @@ enum class SortKind : int {
 
 constexpr uint32_t kMaxSorts = 4;   // sorts of one batch (same length, same launches)
 constexpr uint32_t kWrrMaxWeightSum = 1024;   // smooth round robin: largest sum of the weights
+// How Weighted interleaves the tiers inside a cycle (the ABI's weighted_mode).
+enum : uint32_t { kWrrBlocked = 0, kWrrSmooth = 1, kWrrStride = 2 };
 
 // Inputs and parameters shared by the sorts of a batch.
 struct SortInput {
@@ -60,7 +62,7 @@ struct SortInput {
     uint32_t cls[16];          // Class: priority class of each tier
     double prio[16];           // Aging/Class keys
     uint32_t weight[16];       // Tier: weighted round robin
-    uint32_t wrr_smooth;       // Tier: the smooth interleaving (weights sum <= kWrrMaxWeightSum)
+    uint32_t wrr_mode;         // Tier: kWrrBlocked, kWrrSmooth (weights sum <= kWrrMaxWeightSum), kWrrStride
     double aging_rate, t_now, aging_floor;
 };
 
@@ -125,7 +127,7 @@ struct OrderArgs {
     const uint32_t *fifo_in;
     uint32_t n_tiers;
     uint32_t weight[16];
-    uint32_t wrr_smooth;       // Weighted: smooth interleaving
+    uint32_t wrr_mode;         // Weighted: kWrrBlocked, kWrrSmooth or kWrrStride
     double prio[16];
     double aging_rate, t_now, aging_floor;
     uint32_t *perm[5];
@@ -156,7 +158,7 @@ struct SimArgs {
     double f_ref;
     uint32_t n_tiers;
     uint32_t weight[16];
-    uint32_t wrr_smooth;       // Weighted: smooth interleaving
+    uint32_t wrr_mode;         // Weighted: kWrrBlocked, kWrrSmooth or kWrrStride
     double prio[16];
     double aging_rate, aging_floor;
     double *state;

@@ -96,7 +96,7 @@ hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_
         in.prio[q] = a.prio[q];
         in.weight[q] = a.weight[q];
     }
-    in.wrr_smooth = a.wrr_smooth;
+    in.wrr_mode = a.wrr_mode;
     in.aging_rate = a.aging_rate;
     in.t_now = a.t_now;
     in.aging_floor = a.aging_floor;

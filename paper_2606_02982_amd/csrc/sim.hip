@@ -75,7 +75,7 @@ struct EngineArgs {
     const Aux *aux;
     const uint8_t *val;
     uint32_t weight[kMaxQ];
-    uint32_t wrr_smooth;       // Weighted: smooth interleaving
+    uint32_t wrr_mode;         // Weighted: kWrrBlocked, kWrrSmooth or kWrrStride
     double alpha, aging_rate, aging_floor;
     double *state;
     uint32_t *list[2];
@@ -296,7 +296,7 @@ __global__ __launch_bounds__(kTPB) void k_sim_engine(EngineArgs a)
         // 3. list positions of the first m requests of the order
         if (policy == kFifo) {
             if (tid < m) s_selpos[tid] = tid;
-        } else if (policy == kWeighted && a.wrr_smooth) {
+        } else if (policy == kWeighted && a.wrr_mode == kWrrSmooth) {
             // the first m dispatches of a fresh smooth cycle, one per step,
             // by one wave (lane q = tier q); a queue running empty starts a
             // new cycle over the rest
@@ -325,6 +325,8 @@ __global__ __launch_bounds__(kTPB) void k_sim_engine(EngineArgs a)
                 if (policy == kPriority) {
                     pos = r;
                     for (uint32_t u = 0; u < q; u++) pos += s_cnt[u];
+                } else if (a.wrr_mode == kWrrStride) {
+                    pos = wrr_stride_pos(q, r, s_wt, nq, [&](uint32_t u) { return s_cnt[u]; });
                 } else {
                     pos = wrr_place(q, r, s_cnt, s_wt, nq);
                 }
@@ -631,7 +633,7 @@ hipError_t sim_launch(const SimArgs &a, void *ws, uint32_t *flag, hipStream_t s)
     ea.aux = aux;
     ea.val = val;
     for (uint32_t q = 0; q < kMaxQ; q++) ea.weight[q] = q < a.n_tiers && a.weight[q] ? a.weight[q] : 1u;
-    ea.wrr_smooth = a.wrr_smooth;
+    ea.wrr_mode = a.wrr_mode;
     ea.alpha = a.alpha;
     ea.aging_rate = a.aging_rate;
     ea.aging_floor = a.aging_floor;

@@ -166,7 +166,7 @@ __global__ __launch_bounds__(256) void k_sort_plan(SortBatch b)
     int full = __syncthreads_or(c == b.n ? 1 : 0);
     d.ctl->excl[p][t] = block_excl_scan256(c, tmp4);
     if (t == 0) d.ctl->active[p] = full ? 0u : 1u;
-    if (d.kind == SortKind::Tier && b.in.wrr_smooth && t < 64) {
+    if (d.kind == SortKind::Tier && b.in.wrr_mode == kWrrSmooth && t < 64) {
         // the smooth interleaving's period table (digit t = tier t)
         __shared__ uint16_t per[kWrrMaxWeightSum];
         const uint32_t nq = b.in.n_tiers < kWrrTiers ? b.in.n_tiers : kWrrTiers;
@@ -334,7 +334,7 @@ __global__ __launch_bounds__(TPB) void k_sort_pass(SortBatch b, uint32_t p)
         const uint32_t *tstart = ctl->excl[0];
         WrrPlanHead &wh = *reinterpret_cast<WrrPlanHead *>(&wcnt[0][0]);   // the counters are done
         static_assert(sizeof(WrrPlanHead) <= sizeof(wcnt), "plan header fits the counters");
-        const bool smooth = b.in.wrr_smooth != 0;
+        const bool smooth = b.in.wrr_mode == kWrrSmooth;
         if (smooth) {
             __syncthreads();
             for (uint32_t i = t; i < sizeof(WrrPlanHead) / 4; i += TPB)
@@ -351,6 +351,11 @@ __global__ __launch_bounds__(TPB) void k_sort_pass(SortBatch b, uint32_t p)
                 uint32_t r32;
                 pos = wrr_smooth_pos(wh, d.plan->off, b.in.weight[q & 15u], q & 15u, (uint32_t)kq, r32);
                 rnd = r32;
+            } else if (b.in.wrr_mode == kWrrStride) {
+                const uint32_t qc = q & 15u, wq = b.in.weight[qc] ? b.in.weight[qc] : 1u;
+                rnd = kq / wq;
+                pos = wrr_stride_pos(qc, kq, b.in.weight, b.in.n_tiers < 16u ? b.in.n_tiers : 16u,
+                                     [&](uint32_t u) { return tstart[u + 1] - tstart[u]; });
             } else {
                 pos = wrr_pos(b.in, tstart, n, q, kq, rnd);
             }

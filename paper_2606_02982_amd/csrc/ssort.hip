@@ -447,7 +447,7 @@ __global__ __launch_bounds__(kScTPB) void k_ss_scatter(SsBatch b)
         }
         __syncthreads();
         if (t < kQ) d.tot[t] = texcl[t];
-        if (d.pw_out[1] && b.in.wrr_smooth && w == 0) {
+        if (d.pw_out[1] && b.in.wrr_mode == kWrrSmooth && w == 0) {
             // the smooth interleaving's period table, by one wave (the
             // tile's keys are out, so lj serves as its scratch)
             const uint32_t nq = b.in.n_tiers < kQ ? b.in.n_tiers : kQ;
@@ -505,8 +505,16 @@ __device__ __forceinline__ void pw_place(const SsBatch &b, const SsDesc &d, cons
     }
     if (d.pw_out[1]) {
         uint32_t rnd;
-        const uint64_t pos = b.in.wrr_smooth ? wrr_smooth_pos(pt.wh, b.plan->off, pt.weight[q], q, kt, rnd)
-                                             : weighted_pos(pt, b.in.n_tiers < kQ ? b.in.n_tiers : kQ, q, kt, rnd);
+        const uint32_t nq = b.in.n_tiers < kQ ? b.in.n_tiers : kQ;
+        uint64_t pos;
+        if (b.in.wrr_mode == kWrrSmooth) {
+            pos = wrr_smooth_pos(pt.wh, b.plan->off, pt.weight[q], q, kt, rnd);
+        } else if (b.in.wrr_mode == kWrrStride) {
+            rnd = kt / (pt.weight[q] ? pt.weight[q] : 1u);
+            pos = wrr_stride_pos(q, kt, pt.weight, nq, [&](uint32_t u) { return pt.tot[u]; });
+        } else {
+            pos = weighted_pos(pt, nq, q, kt, rnd);
+        }
         if (pos < b.n) d.pw_out[1][pos] = j;
         if (d.pw_key[1]) d.pw_key[1][j] = (double)rnd;
     }
@@ -1006,7 +1014,7 @@ __device__ __forceinline__ void load_pw(const SsBatch &b, const SsDesc &d, BkSha
     }
     if (t < 2 * kQ) sh.pt.cnt[t] = 0;
     for (uint32_t i = t; i < (kBkTPB / 64) * 2 * kQ; i += kBkTPB) (&sh.pt.wd[0][0])[i] = 0;
-    if (d.pw_out[1] && b.in.wrr_smooth)
+    if (d.pw_out[1] && b.in.wrr_mode == kWrrSmooth)
         for (uint32_t i = t; i < sizeof(WrrPlanHead) / 4; i += kBkTPB)
             reinterpret_cast<uint32_t *>(&sh.pt.wh)[i] = reinterpret_cast<const uint32_t *>(&b.plan->h)[i];
     __syncthreads();

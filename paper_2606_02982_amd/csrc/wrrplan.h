@@ -139,4 +139,27 @@ __device__ __forceinline__ uint64_t wrr_smooth_pos(const WrrPlanHead &head, cons
     return (uint64_t)head.start[ph] + (uint64_t)(i / wq) * head.W[ph] + off[head.offbase[ph][q] + i % wq];
 }
 
+// Stride scheduling, another reading of the same section: queue q's pass
+// starts at its stride 1 / w_q and grows by it per dispatch; the smallest
+// pass (the lowest tier on ties) is served. The k-th request (FIFO order)
+// of tier q runs at pass (k + 1) / w_q, so its place is k plus, for every
+// other tier t, the requests of t with a smaller pass, or an equal one when
+// t < q: min(n_t, floor((k + 1) w_t / w_q)) for t < q and
+// min(n_t, floor(((k + 1) w_t - 1) / w_q)) for t > q. cnt(t) = n_t; weights
+// >= 1 below nq (the products stay below 2^62).
+template <typename Cnt>
+__device__ __forceinline__ uint64_t wrr_stride_pos(uint32_t q, uint64_t k, const uint32_t *w, uint32_t nq, Cnt cnt)
+{
+    const uint64_t wq = w[q] ? w[q] : 1u, k1 = k + 1u;
+    uint64_t pos = k;
+    for (uint32_t t = 0; t < nq; t++) {
+        if (t == q) continue;
+        const uint64_t x = k1 * (w[t] ? w[t] : 1u);
+        const uint64_t c = (t < q ? x : x - 1u) / wq;
+        const uint64_t nt = cnt(t);
+        pos += c < nt ? c : nt;
+    }
+    return pos;
+}
+
 }  // namespace ds

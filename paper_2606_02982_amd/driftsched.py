@@ -24,7 +24,7 @@ OP_ERROR_STATS, OP_CLASS_HIST, OP_SIMULATE = 5, 6, 7
 DS_VALIDATE = 1
 DS_SERIAL_SORT = 2
 MAX_TIERS = 16
-WRR_BLOCKED, WRR_SMOOTH = 0, 1   # ds_order_params.weighted_mode
+WRR_BLOCKED, WRR_SMOOTH, WRR_STRIDE = 0, 1, 2   # ds_order_params.weighted_mode
 WRR_MAX_WEIGHT_SUM = 1024
 MAX_BATCH = 1024
 
@@ -288,10 +288,10 @@ def characterize_score(text, offsets, category, tenant, group, t_base, s_tenant,
 
 def order_params(n_tiers=3, weights=(4, 2, 1), tier_priority=(0.0, 1.0, 2.0), aging_rate=0.01,
                  t_now=0.0, aging_floor=0.0, weighted_mode=WRR_BLOCKED):
-    """ds_order_params. weighted_mode: WRR_BLOCKED or WRR_SMOOTH (or their
-    names "blocked", "smooth")."""
+    """ds_order_params. weighted_mode: WRR_BLOCKED, WRR_SMOOTH or WRR_STRIDE
+    (or their names "blocked", "smooth", "stride")."""
     if isinstance(weighted_mode, str):
-        weighted_mode = {"blocked": WRR_BLOCKED, "smooth": WRR_SMOOTH}[weighted_mode]
+        weighted_mode = {"blocked": WRR_BLOCKED, "smooth": WRR_SMOOTH, "stride": WRR_STRIDE}[weighted_mode]
     p = OrderParams()
     p.n_tiers = int(n_tiers)
     for q in range(MAX_TIERS):

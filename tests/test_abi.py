@@ -106,8 +106,10 @@ def test_order_host_errors(ds):
     q = ds.order_params(aging_rate=-1.0)
     assert f(4, 10, FAKE, FAKE, FAKE, NULL, ctypes.byref(q), FAKE, NULL, FAKE_WS, ws, 0, NULL) == -2
     # the smooth interleaving: a known mode, weights summing to at most 1024
-    q = ds.order_params(weighted_mode=2)
+    q = ds.order_params(weighted_mode=3)
     assert f(2, 10, FAKE, FAKE, FAKE, NULL, ctypes.byref(q), FAKE, NULL, FAKE_WS, ws, 0, NULL) == -2
+    q = ds.order_params(weights=(4000, 1, 1), weighted_mode="stride")    # no bound for stride
+    assert f(2, 10, FAKE, FAKE, FAKE, NULL, ctypes.byref(q), FAKE, NULL, FAKE_WS, 64, 0, NULL) == -4
     q = ds.order_params(weights=(1000, 24, 1), weighted_mode="smooth")
     assert f(2, 10, FAKE, FAKE, FAKE, NULL, ctypes.byref(q), FAKE, NULL, FAKE_WS, ws, 0, NULL) == -2
     q = ds.order_params(weights=(1000, 23, 1), weighted_mode="smooth")   # sum 1024: accepted
@@ -194,7 +196,7 @@ def test_simulate_host_errors(ds):
     assert call(ds.sim_params("fifo", alpha=1.5)) == -2
     assert call(ds.sim_params("fifo", f_ref=0.0)) == -2
     assert call(ds.sim_params("weighted", weights=(1, 0, 1))) == -2
-    assert call(ds.sim_params("weighted", weighted_mode=2)) == -2
+    assert call(ds.sim_params("weighted", weighted_mode=3)) == -2
     assert call(ds.sim_params("weighted", weights=(1020, 4, 1), weighted_mode="smooth")) == -2
     assert call(ds.sim_params("aging", aging_rate=-1.0)) == -2
     assert call(ds.sim_params("fifo", n_tiers=0)) == -2
