@@ -66,6 +66,9 @@ def parse():
     ap.add_argument("--separate", action="store_true",
                     help="stages 1 and 3 as the two calls ds_characterize and ds_score instead of "
                          "the fused ds_characterize_score (the same results)")
+    ap.add_argument("--weighted-mode", choices=["blocked", "smooth", "stride"], default="blocked",
+                    help="how Weighted interleaves the tiers inside a cycle (ds_order_params."
+                         "weighted_mode); the workloads' reading is blocked")
     ap.add_argument("--graph", action="store_true",
                     help="time replays of one step captured in a HIP graph instead of eager "
                          "launches (the same kernels)")
@@ -136,7 +139,7 @@ def main():
     perms = [torch.empty(N, dtype=torch.int32, device="cuda") for _ in range(5)]
     params = ds.order_params(weights=tuple(int(w) for w in b.weights),
                              tier_priority=tuple(b.tier_priority), aging_rate=b.aging_rate,
-                             t_now=b.t_now, aging_floor=b.aging_floor)
+                             t_now=b.t_now, aging_floor=b.aging_floor, weighted_mode=args.weighted_mode)
     ws = {op: ds.workspace(op, N, b.n_groups) for op in range(5)}
     ALL = (0, 1, 2, 3, 4)
     perm_map = dict(enumerate(perms))
@@ -262,7 +265,7 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(b, args.cpu_seconds)
+        cpu = cpu_baseline(b, args.cpu_seconds, args.weighted_mode)
 
     out = {
         "metric": METRIC,
@@ -288,6 +291,7 @@ def main():
         "stages_ms": {"calibrate": round(stage_ms[0], 4), "characterize_score": round(stage_ms[1], 4),
                       "order_x5": round(stage_ms[2], 4)},
         "fused_characterize_score": not args.separate,
+        "weighted_mode": args.weighted_mode,
         "roofline": {"kernel": "characterize + score (k_char_main + k_char_fin)" if not args.separate
                      else "characterize + score (k_char_main + k_char_fin, k_score)",
                      "bound": "hbm", "achieved": round(char_gbs, 1), "peak": HBM_PEAK_GBS,
@@ -570,7 +574,7 @@ def measured_traffic(workload):
     return int(vals["traffic_bytes_per_call"])
 
 
-def cpu_baseline(b, budget_s):
+def cpu_baseline(b, budget_s, weighted_mode="blocked"):
     """The oracle as it stands, single-threaded, on the same step."""
     import oracle
     N = b.n
@@ -584,7 +588,8 @@ def cpu_baseline(b, budget_s):
         state, _ = oracle.calibrate(b.ev_group, b.ev_est, b.ev_obs, b.alphas[0], state)
         _, _, budget, _ = oracle.score(counts, b.category, b.tenant, b.group, b.t_base,
                                        b.s_tenant, state)
-        for pol in range(5):
+        weighted = {"blocked": 2, "smooth": oracle.WEIGHTED_SMOOTH, "stride": oracle.WEIGHTED_STRIDE}
+        for pol in (0, 1, weighted[weighted_mode], 3, 4):
             oracle.order(pol, b.tier, b.arrival, budget, **kw)
         reps += 1
         el = time.perf_counter() - t0

@@ -37,41 +37,66 @@ struct WrrPlan {
     uint16_t off[kWrrMaxOffsets];              // dispatch offsets inside a period, ascending per tier
 };
 
-__device__ __forceinline__ int32_t wave_max_i32(int32_t x)
+// Reductions over the 16 lanes of each DPP row (the tiers are lanes 0..15,
+// row 0): rotations by 8, 4, 2, 1 within the row; every lane of a row ends
+// with its row's result.
+template <int kRor>
+__device__ __forceinline__ uint32_t row_ror(uint32_t x)
 {
-#pragma unroll
-    for (int d = 32; d >= 1; d >>= 1) {
-        const int32_t o = __shfl_xor(x, d, 64);
-        x = o > x ? o : x;
-    }
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x120 + kRor, 0xF, 0xF, false);
+}
+
+__device__ __forceinline__ int32_t row_max_i32(int32_t x)
+{
+    int32_t o;
+    o = (int32_t)row_ror<8>((uint32_t)x); x = o > x ? o : x;
+    o = (int32_t)row_ror<4>((uint32_t)x); x = o > x ? o : x;
+    o = (int32_t)row_ror<2>((uint32_t)x); x = o > x ? o : x;
+    o = (int32_t)row_ror<1>((uint32_t)x); x = o > x ? o : x;
     return x;
 }
 
-__device__ __forceinline__ uint64_t wave_min_u64(uint64_t x)
+__device__ __forceinline__ uint32_t row_sum_u32(uint32_t x)
 {
-#pragma unroll
-    for (int d = 32; d >= 1; d >>= 1) {
-        const uint64_t o = (uint64_t)__shfl_xor((long long)x, d, 64);
-        x = o < x ? o : x;
-    }
+    x += row_ror<8>(x);
+    x += row_ror<4>(x);
+    x += row_ror<2>(x);
+    x += row_ror<1>(x);
     return x;
 }
 
-// One dispatch of the smooth rule over the wave's lanes (lane q = tier q):
-// returns the served lane. total: the sum of the active lanes' weights.
+template <int kRor>
+__device__ __forceinline__ uint64_t row_ror64(uint64_t x)
+{
+    return ((uint64_t)row_ror<kRor>((uint32_t)(x >> 32)) << 32) | row_ror<kRor>((uint32_t)x);
+}
+
+__device__ __forceinline__ uint64_t row_min_u64(uint64_t x)
+{
+    uint64_t o;
+    o = row_ror64<8>(x); x = o < x ? o : x;
+    o = row_ror64<4>(x); x = o < x ? o : x;
+    o = row_ror64<2>(x); x = o < x ? o : x;
+    o = row_ror64<1>(x); x = o < x ? o : x;
+    return x;
+}
+
+// One dispatch of the smooth rule over the wave's lanes (lane q = tier q;
+// only lanes 0..15 may be active): returns the served lane. total: the sum
+// of the active lanes' weights.
 __device__ __forceinline__ int wrr_pick(int32_t &credit, bool active, uint32_t wq, uint32_t total)
 {
     if (active) credit += (int32_t)wq;
     const int32_t key = active ? credit : INT32_MIN;
-    const int32_t mx = wave_max_i32(key);
+    const int32_t mx = row_max_i32(key);   // row 0's maximum in lanes 0..15
     const int best = __ffsll((unsigned long long)__ballot(active && key == mx)) - 1;   // lowest tier
     if (lane_id() == best) credit -= (int32_t)total;
     return best;
 }
 
 // The plan for queue lengths len and weights wq held by lane q = tier q of
-// one wave (lanes of absent tiers pass len = 0; weights >= 1 for tiers with
-// requests, their sum <= kWrrMaxWeightSum). per: LDS scratch of
+// one wave (lanes of absent tiers, and every lane from 16 on, pass len = 0;
+// weights >= 1 for tiers with requests, their sum <= kWrrMaxWeightSum). per: LDS scratch of
 // kWrrMaxWeightSum entries. The plan goes to global memory, for later
 // launches.
 __device__ inline void wrr_plan_build(uint32_t len, uint32_t wq, uint16_t *per, WrrPlan *plan)
@@ -81,7 +106,7 @@ __device__ inline void wrr_plan_build(uint32_t len, uint32_t wq, uint16_t *per, 
     uint32_t used = 0, pos = 0, ph = 0, offcur = 0;
     while (__ballot(active) != 0ull) {
         const uint32_t mine = active ? wq : 0u;
-        const uint32_t W = wave_sum(mine);
+        const uint32_t W = readlane32(row_sum_u32(mine), 0);   // row 0 holds every active lane
         const uint32_t base = wave_incl_scan_dpp(mine) - mine;   // this tier's offsets in the period
         if (lane == 0) {
             plan->h.start[ph] = pos;
@@ -110,7 +135,7 @@ __device__ inline void wrr_plan_build(uint32_t len, uint32_t wq, uint16_t *per, 
             const uint32_t rem = len - used;   // >= 1
             Tq = (uint64_t)((rem - 1u) / wq) * W + per[base + (rem - 1u) % wq] + 1u;
         }
-        const uint64_t T = wave_min_u64(Tq);   // <= the requests left
+        const uint64_t T = readlane64(row_min_u64(Tq), 0);   // <= the requests left
         // each tier's dispatches among those T
         const uint32_t part = (uint32_t)(T % W);
         uint32_t inpart = 0;
