@@ -26,10 +26,11 @@
 //                 of them in LDS, finds the rank of 8 of them by counting the
 //                 smaller ones and stores each at its rank: the sorted
 //                 sample, of which every (S/B)-th triple is one of B - 1
-//                 splitters. Also clears the look-back words and the overflow
-//                 flag, and counts the tiers of slices of the batch.
+//                 splitters. Also clears the look-back words, the overflow
+//                 flag and the tier totals.
 //   k_ss_scatter  per tile of 2048 requests: makes the keys (and the
-//                 per-request key output), finds each request's bucket by
+//                 per-request key output; the FIFO row adds its tier counts
+//                 to the totals), finds each request's bucket by
 //                 descending a search tree of the splitters, ranks the tile
 //                 by bucket (wave ballots), takes the bucket's count over
 //                 earlier tiles by decoupled look-back and writes the keys
@@ -52,7 +53,6 @@
 #include "common.h"
 #include "kernels.h"
 #include "lookback.h"
-#include "tiercount.h"
 #include "wrrplan.h"
 
 namespace ds {
@@ -71,12 +71,13 @@ constexpr uint32_t kBinMax2 = 32;        // the same for a pass by two keys
 constexpr int kSmpTPB = 256;             // k_ss_sample: threads per block,
 constexpr uint32_t kSmpThr = 32;         // threads per sample ranked,
 constexpr uint32_t kSmpPerBlock = kSmpTPB / kSmpThr;   // samples ranked per block
-constexpr uint32_t kQ = kTierCounts;     // tiers
+constexpr uint32_t kQ = 16;              // tiers (a larger tier value counts as the last)
 
 struct SsCtl {
     uint32_t overflow;
     uint32_t lb_err;       // a bounded look-back wait over the buckets ran out
-    uint32_t pad[62];
+    uint32_t tiles_done;   // FIFO row, smooth round robin: scatter tiles whose tier counts are in
+    uint32_t pad[61];
 };
 
 struct SsDesc {
@@ -92,7 +93,7 @@ struct SsDesc {
     uint64_t *bk1;         // [buckets][kCap] bucket regions
     uint64_t *bk2;
     uint32_t *bj;
-    uint32_t *tot;         // [kQ] requests per tier (FIFO row with partitions)
+    uint32_t *tot;         // [kQ] requests per tier (FIFO row with partitions; added up by the scatter tiles)
     uint32_t *bstat;       // [buckets][2 kQ] look-back words of the digit counts
     uint32_t *pw_out[2];   // FIFO row: Priority and Weighted orders (or NULL)
     double *pw_key[2];
@@ -110,7 +111,6 @@ struct SsBatch {
     uint32_t serial;       // sort in one workgroup regardless of the buckets
     uint32_t nsorts;       // sorts of the batch (grid rows)
     uint32_t nsb;          // blocks of k_ss_sample per sort
-    uint32_t *tier_part;   // [nsb][kQ] tier counts of slices (when the partitions are wanted)
     WrrPlan *plan;         // smooth round robin: the period table (built by the scatter)
     SsDesc s[kSsMaxSorts];
 };
@@ -195,7 +195,6 @@ struct SmpShared {
     uint64_t k1[kSamples];
     uint64_t k2[kSamples];
     uint32_t j[kSamples];
-    uint32_t tw[(kSmpTPB / 64) * kQ];
 };
 
 template <SortKind K>
@@ -209,7 +208,9 @@ __device__ __forceinline__ void sample_body(const SsBatch &b, const SsDesc &d, S
     if (blockIdx.x == 0 && t == 0) {
         d.ctl->overflow = b.serial;
         d.ctl->lb_err = 0;
+        d.ctl->tiles_done = 0;
     }
+    if (blockIdx.x == 0 && t < kQ && (d.pw_out[0] || d.pw_out[1])) d.tot[t] = 0;
     {
         // all loads in flight before the first LDS store
         constexpr int kPer = kSamples / kSmpTPB;
@@ -270,8 +271,6 @@ __device__ __forceinline__ void sample_body(const SsBatch &b, const SsDesc &d, S
 __global__ __launch_bounds__(kSmpTPB) void k_ss_sample(SsBatch b)
 {
     __shared__ SmpShared sh;
-    if (blockIdx.y == 0 && b.tier_part)
-        tier_partial<kSmpTPB>(b.in.tier, b.n, blockIdx.x, b.nsb, b.tier_part, sh.tw);
     const SsDesc &d = b.s[blockIdx.y];
     with_kind(d.kind, [&](auto K) { sample_body<decltype(K)::value>(b, d, sh); });
 }
@@ -314,6 +313,8 @@ __global__ __launch_bounds__(kScTPB) void k_ss_scatter(SsBatch b)
     __shared__ uint64_t lk2[kScTile];
     __shared__ uint32_t lj[kScTile];
     __shared__ uint8_t lb[kScTile];
+    __shared__ uint32_t s_tq[kQ];
+    __shared__ uint32_t s_last;
 
     const SsDesc &d = b.s[blockIdx.y];
     const uint32_t t = threadIdx.x, n = b.n, nsp = b.nb - 1;
@@ -321,10 +322,19 @@ __global__ __launch_bounds__(kScTPB) void k_ss_scatter(SsBatch b)
     const uint32_t tile = blockIdx.x, base = tile * kScTile;
     const uint32_t cnt = n - base < kScTile ? n - base : kScTile;
     const bool digit_thread = t < 256;
+    const bool pw = d.pw_out[0] || d.pw_out[1];   // FIFO row with the partitions: count the tiers
 
     uint64_t k1[kScR], k2[kScR];
-    uint32_t jj[kScR], bk[kScR], rk[kScR];
+    uint32_t jj[kScR], bk[kScR], rk[kScR], tq[kScR];
     with_kind(d.kind, [&](auto K) { scatter_keys<decltype(K)::value>(b, d, base, cnt, k1, k2, jj); });
+    if (pw) {
+#pragma unroll
+        for (int r = 0; r < kScR; r++) {
+            const uint32_t idx = (uint32_t)w * kWaveKeys + (uint32_t)r * 64u + (uint32_t)lane;
+            tq[r] = idx < cnt ? b.in.tier[base + idx] : kQ;   // kQ: no request
+        }
+        if (t < kQ) s_tq[t] = 0;
+    }
     // splitters in breadth-first (Eytzinger) order of a complete search tree
     // of height hgt: node e (1-based) holds the splitter of in-order index
     // (2 p + 1) 2^(hgt - d - 1) - 1 (d = depth of e, p = e - 2^d); splitter i
@@ -350,6 +360,11 @@ __global__ __launch_bounds__(kScTPB) void k_ss_scatter(SsBatch b)
     }
     for (uint32_t i = t; i < kWaves * 256u; i += kScTPB) (&wcnt[0][0])[i] = 0;
     __syncthreads();   // splitters and counters ready
+    if (pw) {
+#pragma unroll
+        for (int r = 0; r < kScR; r++)
+            if (tq[r] != kQ) atomicAdd(&s_tq[tq[r] < kQ ? tq[r] : kQ - 1u], 1u);
+    }
     // bucket = number of splitters <= (k1, k2, i): hgt steps down the tree
     // (the rounds advance together, so that their LDS reads overlap)
     uint32_t node[kScR];
@@ -395,6 +410,8 @@ __global__ __launch_bounds__(kScTPB) void k_ss_scatter(SsBatch b)
             tc += c[q];
         }
     }
+    // the tile's requests per tier join the row's totals (read by the bucket launch)
+    if (pw && t < kQ && s_tq[t]) atomicAdd(&d.tot[t], s_tq[t]);
     uint32_t *st = d.status;
     if (digit_thread) st_relaxed(&st[(uint64_t)tile * 256u + t], (tile == 0 ? kPre : kAgg) | tc);
     const uint32_t tex = block_excl_scan_digits<kScTPB>(tc, tmp4);
@@ -435,25 +452,20 @@ __global__ __launch_bounds__(kScTPB) void k_ss_scatter(SsBatch b)
         }
     }
     if (over) atomicOr(&d.ctl->overflow, 1u);
-    if ((d.pw_out[0] || d.pw_out[1]) && tile == 0) {
-        // requests per tier (for the round-robin positions): the sum of the
-        // slices' counts, after this tile's look-back word is out
+    if (pw && d.pw_out[1] && b.in.wrr_mode == kWrrSmooth) {
+        // the smooth interleaving's period table needs every tile's tier
+        // counts: the last tile to be done builds it, with one wave (its
+        // keys are out, so lj serves as scratch)
+        if (t < kQ) __threadfence();   // this tile's counts are in before its ticket
         __syncthreads();
-        if (t < kQ) texcl[t] = 0;
+        if (t == 0) s_last = atomicAdd(&d.ctl->tiles_done, 1u) == b.tiles - 1u ? 1u : 0u;
         __syncthreads();
-        for (uint32_t i = t; i < b.nsb * kQ; i += kScTPB) {
-            const uint32_t c = b.tier_part[i];
-            if (c) atomicAdd(&texcl[i % kQ], c);
-        }
-        __syncthreads();
-        if (t < kQ) d.tot[t] = texcl[t];
-        if (d.pw_out[1] && b.in.wrr_mode == kWrrSmooth && w == 0) {
-            // the smooth interleaving's period table, by one wave (the
-            // tile's keys are out, so lj serves as its scratch)
+        if (s_last && w == 0) {
+            __threadfence();
             const uint32_t nq = b.in.n_tiers < kQ ? b.in.n_tiers : kQ;
             const bool tl = (uint32_t)lane < nq;
-            wrr_plan_build(tl ? texcl[lane] : 0u, tl ? b.in.weight[lane] : 0u, reinterpret_cast<uint16_t *>(lj),
-                           b.plan);
+            wrr_plan_build(tl ? ld_relaxed(&d.tot[lane]) : 0u, tl ? b.in.weight[lane] : 0u,
+                           reinterpret_cast<uint16_t *>(lj), b.plan);
         }
     }
 }
@@ -1398,13 +1410,12 @@ void carve(uint8_t *p, uint64_t n, SsDesc &d)
     for (int i = 0; i < 2; i++) d.fj[i] = reinterpret_cast<uint32_t *>(take(n * 4));
 }
 
-uint64_t tier_part_bytes(uint64_t n) { return align_up((uint64_t)sample_blocks(n) * kQ * 4, 256); }
 
 }  // namespace
 
 size_t ssort_ws_bytes(uint64_t n, uint32_t nsorts)
 {
-    return n <= kSsMaxN ? (size_t)(tier_part_bytes(n) + align_up(sizeof(WrrPlan), 256) +
+    return n <= kSsMaxN ? (size_t)(align_up(sizeof(WrrPlan), 256) +
                                    (uint64_t)nsorts * region_bytes(n))
                         : 0;
 }
@@ -1425,8 +1436,6 @@ hipError_t ssort_launch(const SortInput &in, const SortJob *jobs, uint32_t nsort
     b.nsorts = nsorts;
     b.nsb = sample_blocks(in.n);
     uint8_t *p = static_cast<uint8_t *>(ws);
-    uint32_t *tier_part = reinterpret_cast<uint32_t *>(p);
-    p += tier_part_bytes(in.n);
     b.plan = reinterpret_cast<WrrPlan *>(p);
     p += align_up(sizeof(WrrPlan), 256);
     for (uint32_t i = 0; i < nsorts; i++) {
@@ -1435,7 +1444,6 @@ hipError_t ssort_launch(const SortInput &in, const SortJob *jobs, uint32_t nsort
         if (k != SortKind::Fifo && k != SortKind::Budget && k != SortKind::Aging) return hipErrorInvalidValue;
         d.kind = k;
         if (k == SortKind::Fifo && parts && (parts->perm[0] || parts->perm[1])) {
-            b.tier_part = tier_part;
             for (int e = 0; e < 2; e++) {
                 d.pw_out[e] = parts->perm[e];
                 d.pw_key[e] = parts->perm[e] ? parts->key[e] : nullptr;
