@@ -73,22 +73,14 @@ __host__ __device__ inline uint32_t n_passes(uint32_t key_bits)
     return p == 0 ? 1 : (p > kMaxPasses ? kMaxPasses : p);
 }
 
-// Exclusive scan of one value per thread over a 256-thread block.
-__device__ uint32_t block_excl_scan256(uint32_t x, uint32_t *tmp4)
-{
-    uint32_t incl = wave_incl_scan_dpp(x);
-    int w = threadIdx.x >> 6;
-    if (lane_id() == 63) tmp4[w] = incl;
-    __syncthreads();
-    uint32_t off = 0;
-    for (int k = 0; k < w; k++) off += tmp4[k];
-    __syncthreads();
-    return off + incl - x;
-}
+constexpr int kInitPer = 4;        // keys per thread per step of the init kernel
+constexpr int kPlanTPB = 1024;     // threads per plan block: four per digit
 
-constexpr int kInitPer = 4;   // keys per thread per step of the init kernel
-
-__global__ __launch_bounds__(256) void k_sort_init(SortBatch b, uint64_t status_words)
+// TPB: 1024 threads for batches of one or two sorts, 512 for more, so that
+// the init blocks of a batch (at most kInitBlocks per sort) are resident at
+// once.
+template <int TPB>
+__global__ __launch_bounds__(TPB) void k_sort_init(SortBatch b, uint64_t status_words)
 {
     __shared__ uint32_t h[kMaxPasses][256];
     const SortDesc &d = b.s[blockIdx.y];
@@ -144,27 +136,50 @@ __global__ __launch_bounds__(256) void k_sort_init(SortBatch b, uint64_t status_
 }
 
 // One block per (pass, sort): digit totals from the block histograms,
-// exclusive offsets, and whether the pass does anything.
-__global__ __launch_bounds__(256) void k_sort_plan(SortBatch b)
+// exclusive offsets, and whether the pass does anything. Four threads per
+// digit each add up every fourth block histogram, 32 loads in flight at a
+// time.
+__global__ __launch_bounds__(kPlanTPB) void k_sort_plan(SortBatch b)
 {
+    constexpr uint32_t kParts = kPlanTPB / 256, kBatch = 32;
+    __shared__ uint32_t part[kParts][256];
     __shared__ uint32_t tmp4[4];
     const SortDesc &d = b.s[blockIdx.y];
     const uint32_t p = blockIdx.x;
     if (p >= d.passes) return;
-    const uint32_t t = threadIdx.x;
+    const uint32_t t = threadIdx.x, dig = t & 255u, q = t >> 8;
     const uint32_t stride = d.passes * 256u;
-    // 16 independent loads in flight per step
     uint32_t c = 0;
-    for (uint32_t blk0 = 0; blk0 < b.init_blocks; blk0 += 16) {
-        uint32_t x[16];
+    for (uint32_t i0 = 0; i0 * kParts < b.init_blocks; i0 += kBatch) {
+        uint32_t x[kBatch];
 #pragma unroll
-        for (uint32_t k = 0; k < 16; k++)
-            x[k] = blk0 + k < b.init_blocks ? d.bhist[(uint64_t)(blk0 + k) * stride + p * 256u + t] : 0u;
+        for (uint32_t k = 0; k < kBatch; k++) {
+            const uint32_t blk = q + kParts * (i0 + k);
+            x[k] = blk < b.init_blocks ? d.bhist[(uint64_t)blk * stride + p * 256u + dig] : 0u;
+        }
 #pragma unroll
-        for (uint32_t k = 0; k < 16; k++) c += x[k];
+        for (uint32_t k = 0; k < kBatch; k++) c += x[k];
     }
-    int full = __syncthreads_or(c == b.n ? 1 : 0);
-    d.ctl->excl[p][t] = block_excl_scan256(c, tmp4);
+    part[q][dig] = c;
+    __syncthreads();
+    c = 0;
+    if (t < 256) {
+#pragma unroll
+        for (uint32_t k = 0; k < kParts; k++) c += part[k][t];
+    }
+    const int full = __syncthreads_or(t < 256 && c == b.n ? 1 : 0);
+    // exclusive scan of the 256 digit totals (waves 0..3)
+    uint32_t incl = 0;
+    if (t < 256) {
+        incl = wave_incl_scan_dpp(c);
+        if (lane_id() == 63) tmp4[t >> 6] = incl;
+    }
+    __syncthreads();
+    if (t < 256) {
+        uint32_t off = 0;
+        for (uint32_t k = 0; k < (t >> 6); k++) off += tmp4[k];
+        d.ctl->excl[p][t] = off + incl - c;
+    }
     if (t == 0) d.ctl->active[p] = full ? 0u : 1u;
     if (d.kind == SortKind::Tier && b.in.wrr_mode == kWrrSmooth && t < 64) {
         // the smooth interleaving's period table (digit t = tier t)
@@ -376,10 +391,12 @@ __global__ __launch_bounds__(TPB) void k_sort_pass(SortBatch b, uint32_t p)
     }
 }
 
-// Tile shapes: 2048 keys (512 threads x 4) up to 2^18 keys, 8192 keys (1024
-// threads x 8) above, where fewer, larger tiles shorten the look-back.
+// Tile shapes: 2048 keys (512 threads x 4) up to 2^18 keys, 4096 keys (512
+// threads x 8) above: larger tiles shorten the look-back, and at 2^20 keys
+// 4096-key tiles still give every CU a tile of each sort (8192-key tiles
+// left half of them idle).
 constexpr uint32_t kSmallN = 1u << 18;
-uint32_t tile_keys(uint64_t n) { return n <= kSmallN ? 512u * 4u : 1024u * 8u; }
+uint32_t tile_keys(uint64_t n) { return n <= kSmallN ? 512u * 4u : 512u * 8u; }
 
 uint64_t region_bytes(uint64_t n)
 {
@@ -439,15 +456,20 @@ hipError_t sort_launch(const SortInput &in, const SortJob *jobs, uint32_t nsorts
         maxp = d.passes > maxp ? d.passes : maxp;
     }
     const uint64_t status_words = (uint64_t)b.tiles * 256u;
-    uint64_t ibw = cdiv(in.n, 256 * kInitPer);
+    const bool wide = nsorts <= 2;
+    const uint32_t itpb = wide ? 1024u : 512u;
+    uint64_t ibw = cdiv(in.n, (uint64_t)itpb * kInitPer);
     b.init_blocks = (uint32_t)(ibw < kInitBlocks ? (ibw ? ibw : 1) : kInitBlocks);
-    hipLaunchKernelGGL(k_sort_init, dim3(b.init_blocks, nsorts), dim3(256), 0, s, b, status_words);
-    hipLaunchKernelGGL(k_sort_plan, dim3(maxp, nsorts), dim3(256), 0, s, b);
+    if (wide)
+        hipLaunchKernelGGL(k_sort_init<1024>, dim3(b.init_blocks, nsorts), dim3(1024), 0, s, b, status_words);
+    else
+        hipLaunchKernelGGL(k_sort_init<512>, dim3(b.init_blocks, nsorts), dim3(512), 0, s, b, status_words);
+    hipLaunchKernelGGL(k_sort_plan, dim3(maxp, nsorts), dim3(kPlanTPB), 0, s, b);
     for (uint32_t pass = 0; pass < maxp; pass++) {
         if (in.n <= kSmallN)
             hipLaunchKernelGGL((k_sort_pass<512, 4>), dim3(b.tiles, nsorts), dim3(512), 0, s, b, pass);
         else
-            hipLaunchKernelGGL((k_sort_pass<1024, 8>), dim3(b.tiles, nsorts), dim3(1024), 0, s, b, pass);
+            hipLaunchKernelGGL((k_sort_pass<512, 8>), dim3(b.tiles, nsorts), dim3(512), 0, s, b, pass);
     }
     return hipGetLastError();
 }
