@@ -106,3 +106,43 @@ def test_step_graph_replays_equal_eager(ds, schedule):
         step(scratch)   # eager work between the replays
         torch.cuda.synchronize()
     assert np.array_equal(want[0].numpy().view(np.uint32), b.words)
+
+
+@pytest.mark.parametrize("mode", ["smooth", "stride"])
+@pytest.mark.parametrize("n", [65536, 300000])
+def test_order_modes_graph_replays(ds, mode, n):
+    # the smooth table is built by the last scatter tile to finish (a ticket
+    # cleared by the sample launch) or by the plan block: every replay must
+    # give the eager orders
+    rng = np.random.default_rng(n)
+    tier = dev(rng.integers(0, 4, n).astype(np.uint8))
+    arrival = dev(np.round(rng.uniform(0, 50, n), 3))
+    budget = dev(np.round(rng.uniform(1, 3000, n), 1))
+    params = ds.order_params(n_tiers=4, weights=(5, 3, 2, 1), tier_priority=(0.0, 1.0, 2.0, 3.0),
+                             aging_rate=0.01, t_now=50.0, weighted_mode=mode)
+    ws = ds.workspace(ds.OP_ORDER_MULTI, n, 0)
+    print("graph order_multi mode=%s n=%d" % (mode, n), flush=True)
+    want, _ = ds.order_multi((0, 1, 2, 3, 4), tier, arrival, budget, params=params, ws=ws)
+    torch.cuda.synchronize()
+    want = {p: t.cpu().clone() for p, t in want.items()}
+    perms = {p: torch.empty(n, dtype=torch.int32, device="cuda") for p in range(5)}
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        ds.order_multi((0, 1, 2, 3, 4), tier, arrival, budget, params=params, perms=perms, ws=ws)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=side):
+            ds.order_multi((0, 1, 2, 3, 4), tier, arrival, budget, params=params, perms=perms, ws=ws)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        for t in perms.values():
+            t.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for p in range(5):
+            assert torch.equal(perms[p].cpu(), want[p]), "replay %d policy %d" % (rep, p)
+        ds.order_multi((2,), tier, arrival, budget, params=params, ws=ws)   # eager work between replays
+        torch.cuda.synchronize()
