@@ -72,6 +72,11 @@ constexpr int kSmpTPB = 256;             // k_ss_sample: threads per block,
 constexpr uint32_t kSmpThr = 32;         // threads per sample ranked,
 constexpr uint32_t kSmpPerBlock = kSmpTPB / kSmpThr;   // samples ranked per block
 constexpr uint32_t kQ = 16;              // tiers (a larger tier value counts as the last)
+// FIFO row with the partitions: a bucket entry's index carries its request's
+// tier in the top byte (written by the scatter, which loads the tiers
+// anyway), so that the bucket blocks need not gather them
+constexpr uint32_t kIdxBits = 24, kIdxMask = (1u << kIdxBits) - 1u;
+static_assert(kSsMaxN <= (1u << kIdxBits), "request index and tier share a word");
 
 struct SsCtl {
     uint32_t overflow;
@@ -433,7 +438,7 @@ __global__ __launch_bounds__(kScTPB) void k_ss_scatter(SsBatch b)
             const uint32_t lp = texcl[dg] + wcnt[w][dg] + rk[r];
             lk1[lp] = k1[r];
             lk2[lp] = k2[r];
-            lj[lp] = jj[r];
+            lj[lp] = pw ? jj[r] | (tq[r] << kIdxBits) : jj[r];   // tq[r] < 256 here
             lb[lp] = (uint8_t)dg;
         }
     }
@@ -1250,7 +1255,8 @@ __global__ __launch_bounds__(kBkTPB) void k_ss_bucket(SsBatch b)
         for (int r = 0; r < kBkR; r++) {
             const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
             if ((uint32_t)r < reff && idx < m) {
-                const uint32_t qq = b.in.tier[jv[r]];
+                const uint32_t qq = jv[r] >> kIdxBits;   // the tier, packed by the scatter
+                jv[r] &= kIdxMask;
                 q[r] = qq < kQ ? qq : kQ - 1u;
                 atomicAdd(&sh.pt.cnt[sh.pt.cls[q[r]]], 1u);
                 atomicAdd(&sh.pt.cnt[kQ + q[r]], 1u);
