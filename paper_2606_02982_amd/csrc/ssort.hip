@@ -1211,17 +1211,34 @@ __global__ __launch_bounds__(kBkTPB) void k_ss_bucket(SsBatch b)
     const uint64_t *src2 = d.bk2 + (uint64_t)bkt * kCap;
     const uint32_t *srcj = d.bj + (uint64_t)bkt * kCap;
     const bool two = d.two != 0;
-    // the first kBkTPB slots are loaded before the size is known (a bucket
-    // of at most kBkTPB requests, the common case, needs no other load)
-    const uint64_t a0 = src1[t];
-    const uint64_t b0 = two ? src2[t] : 0ull;
-    const uint32_t j0 = srcj[t];
+    // the first kPreSlots slots are loaded before the size is known, four
+    // per thread, and staged in LDS, from where each thread takes its entries
+    // in the layout the size gives (a bucket of at most kPreSlots requests,
+    // twice the average, needs no other global load)
+    constexpr uint32_t kPreR = 4, kPreSlots = kPreR * kBkTPB;
+    static_assert(kPreSlots <= kCap, "staged slots lie in the region");
+    uint64_t pa[kPreR], pb[kPreR];
+    uint32_t pj[kPreR];
+#pragma unroll
+    for (uint32_t i = 0; i < kPreR; i++) {
+        const uint32_t s = t + i * kBkTPB;
+        pa[i] = src1[s];
+        pb[i] = two ? src2[s] : 0ull;
+        pj[i] = srcj[s];
+    }
     // bucket sizes: the last tile's inclusive prefixes
     const uint32_t *last = d.status + (uint64_t)(b.tiles - 1) * 256u;
     const uint32_t c = t < b.nb ? (last[t] & kValMask) : 0u;
     const uint32_t before = wave_sum(t < bkt ? c : 0u);
     if (lane == 0) sh.redu[w] = before;
     if (t == bkt) sh.offs[0] = c;
+#pragma unroll
+    for (uint32_t i = 0; i < kPreR; i++) {
+        const uint32_t s = t + i * kBkTPB;
+        sh.lkey[s] = pa[i];
+        if (two) sh.lkey2[s] = pb[i];
+        sh.lj[s] = pj[i];
+    }
     __syncthreads();
     uint32_t off = 0;
 #pragma unroll
@@ -1243,9 +1260,15 @@ __global__ __launch_bounds__(kBkTPB) void k_ss_bucket(SsBatch b)
         jv[r] = 0;
         q[r] = 0;
         if ((uint32_t)r < reff && idx < m) {
-            k[r] = reff == 1 ? a0 : src1[idx];
-            if (two) k2[r] = reff == 1 ? b0 : src2[idx];
-            jv[r] = reff == 1 ? j0 : srcj[idx];
+            if (idx < kPreSlots) {
+                k[r] = sh.lkey[idx];
+                if (two) k2[r] = sh.lkey2[idx];
+                jv[r] = sh.lj[idx];
+            } else {
+                k[r] = src1[idx];
+                if (two) k2[r] = src2[idx];
+                jv[r] = srcj[idx];
+            }
         }
     }
     if (pw) {
@@ -1293,7 +1316,7 @@ __global__ __launch_bounds__(kBkTPB) void k_ss_bucket(SsBatch b)
                 for (int r = 0; r < kBkR; r++) {
                     const uint32_t idx = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
                     if ((uint32_t)r < reff && idx < m) {
-                        sh.lkey[rank[r]] = reff == 1 ? a0 : src1[idx];
+                        sh.lkey[rank[r]] = src1[idx];
                         sh.lj[rank[r]] = jv[r];
                     }
                 }
