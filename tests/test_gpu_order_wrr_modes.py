@@ -71,6 +71,21 @@ def test_weight_sum_at_the_bound(ds, oracle):
     check(ds, oracle, mode, np.zeros(3000, np.uint8), arr[:3000], (1000, 23, 1))
 
 
+@pytest.mark.parametrize("n", [50000, 300000])
+def test_largest_table(ds, oracle, n):
+    # 16 tiers with weights summing to 1024 and 16 different queue lengths,
+    # so that queues run out at up to 16 points: up to 16 phases of the
+    # table, each with a 1024-dispatch period
+    rng = np.random.default_rng(n + 11)
+    w = [int(x) for x in rng.multinomial(1024 - 16, [1 / 16] * 16) + 1]
+    share = np.arange(1, 17, dtype=np.float64)
+    rng.shuffle(share)
+    tier = rng.choice(16, n, p=share / share.sum()).astype(np.uint8)
+    arr = np.round(rng.uniform(0, 20, n), 4)
+    assert sum(w) == 1024 and len(np.unique(np.bincount(tier, minlength=16))) == 16
+    check(ds, oracle, "smooth", tier, arr, tuple(w))
+
+
 @pytest.mark.parametrize("n", [5000, 300000])
 @pytest.mark.parametrize("mode", MODES)
 def test_uneven_queues(ds, oracle, mode, n):
