@@ -1295,12 +1295,14 @@ __global__ __launch_bounds__(kBkTPB) void k_ss_bucket(SsBatch b)
         block_range(sh, k, nullptr, reff, m, mn1, mx1, mn2, mx2);
     if (pw && t < 2 * kQ)
         st_relaxed(&d.bstat[(uint64_t)bkt * 2 * kQ + t], (bkt == 0 ? kPre : kAgg) | sh.pt.cnt[t]);
-    // Two-key sorts: one pass by (k1, k2, index) where the bucket allows
-    // it. Otherwise stable passes: by arrival (ties: index order, which is
-    // entry order), then by k1 with the entries laid out in arrival order
-    // (skipped when the bucket holds one k1). FIFO: one pass by arrival.
+    // One pass by (k1, k2, index) where the bucket allows it; FIFO takes it
+    // too, with k2 = 0 (every entry binned, no separate pass for the ties
+    // at the minimum). Otherwise stable passes: by arrival (ties: index
+    // order, which is entry order), then by k1 with the entries laid out in
+    // arrival order (skipped when the bucket holds one k1); FIFO: one pass
+    // by arrival.
     const bool both = two && mn1 < mx1;
-    bool done = both && rank_pass(sh, k, k2, reff, m, mn1, mx1, rank);
+    bool done = (both || (!two && mn1 < mx1)) && rank_pass(sh, k, k2, reff, m, mn1, mx1, rank);
     if (!done) {
         const uint32_t npass = both ? 2u : 1u;
         for (uint32_t ps = 0; ps < npass; ps++) {
