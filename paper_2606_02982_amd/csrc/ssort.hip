@@ -62,6 +62,7 @@ constexpr uint32_t kSamples = 2048;      // triples sampled per sort (at most)
 constexpr uint32_t kCap = 4096;          // requests per bucket region
 constexpr uint32_t kMaxBuckets = 256;
 constexpr uint32_t kBucketAvg = 1024;    // target requests per bucket
+constexpr uint32_t kBucketAvgFifo = 512; // the same for the FIFO row, which does the most per bucket
 constexpr int kScTPB = 512, kScR = 4;    // scatter tile: 2048 requests
 constexpr uint32_t kScTile = kScTPB * kScR;
 constexpr int kBkTPB = 512, kBkR = kCap / kBkTPB;
@@ -87,6 +88,7 @@ struct SsCtl {
 
 struct SsDesc {
     SortKind kind;
+    uint32_t nb;           // buckets of this row, 1..kMaxBuckets
     uint32_t two;          // k2 (the arrival) is part of the key
     double *key_out;
     uint32_t *out;
@@ -111,7 +113,7 @@ struct SsBatch {
     SortInput in;
     uint32_t n;
     uint32_t tiles;        // scatter tiles
-    uint32_t nb;           // buckets, 1..kMaxBuckets
+    uint32_t nb;           // the most buckets of a row (grid width of the bucket launch)
     uint32_t ns;           // samples, 1..kSamples
     uint32_t serial;       // sort in one workgroup regardless of the buckets
     uint32_t nsorts;       // sorts of the batch (grid rows)
@@ -209,7 +211,7 @@ __device__ __forceinline__ void sample_body(const SsBatch &b, const SsDesc &d, S
     const uint32_t stride = b.nsb * kSmpTPB;
     for (uint32_t i = blockIdx.x * kSmpTPB + t; i < b.tiles * 256u; i += stride) d.status[i] = 0;
     if (d.pw_out[0] || d.pw_out[1])
-        for (uint32_t i = blockIdx.x * kSmpTPB + t; i < b.nb * 2u * kQ; i += stride) d.bstat[i] = 0;
+        for (uint32_t i = blockIdx.x * kSmpTPB + t; i < d.nb * 2u * kQ; i += stride) d.bstat[i] = 0;
     if (blockIdx.x == 0 && t == 0) {
         d.ctl->overflow = b.serial;
         d.ctl->lb_err = 0;
@@ -322,7 +324,7 @@ __global__ __launch_bounds__(kScTPB) void k_ss_scatter(SsBatch b)
     __shared__ uint32_t s_last;
 
     const SsDesc &d = b.s[blockIdx.y];
-    const uint32_t t = threadIdx.x, n = b.n, nsp = b.nb - 1;
+    const uint32_t t = threadIdx.x, n = b.n, nsp = d.nb - 1;
     const int w = (int)(t >> 6), lane = lane_id();
     const uint32_t tile = blockIdx.x, base = tile * kScTile;
     const uint32_t cnt = n - base < kScTile ? n - base : kScTile;
@@ -347,14 +349,14 @@ __global__ __launch_bounds__(kScTPB) void k_ss_scatter(SsBatch b)
     // B - 1 on are padded with the largest triple. The first levels of every
     // search then read the same few LDS words in all lanes.
     uint32_t hgt = 0;
-    while ((1u << hgt) < b.nb) hgt++;
+    while ((1u << hgt) < d.nb) hgt++;
     for (uint32_t e = t + 1; e < (1u << hgt); e += kScTPB) {
         const uint32_t dpt = 31u - (uint32_t)__clz((int)e), pp = e - (1u << dpt);
         const uint32_t i = (2u * pp + 1u) * (1u << (hgt - dpt - 1u)) - 1u;
         uint64_t a1 = ~0ull, a2 = ~0ull;
         uint32_t jv = ~0u;
         if (i < nsp) {
-            const uint32_t r = (i + 1) * b.ns / b.nb;   // < ns; (i + 1) ns < 2^19
+            const uint32_t r = (i + 1) * b.ns / d.nb;   // < ns; (i + 1) ns < 2^19
             a1 = d.smp_k1[r];
             a2 = d.smp_k2[r];
             jv = d.smp_j[r];
@@ -1207,6 +1209,7 @@ __global__ __launch_bounds__(kBkTPB) void k_ss_bucket(SsBatch b)
         if (bkt == 0) serial_sort(b, d, sh);
         return;
     }
+    if (bkt >= d.nb) return;   // a row with fewer buckets than the grid is wide
     const uint64_t *src1 = d.bk1 + (uint64_t)bkt * kCap;
     const uint64_t *src2 = d.bk2 + (uint64_t)bkt * kCap;
     const uint32_t *srcj = d.bj + (uint64_t)bkt * kCap;
@@ -1228,7 +1231,7 @@ __global__ __launch_bounds__(kBkTPB) void k_ss_bucket(SsBatch b)
     }
     // bucket sizes: the last tile's inclusive prefixes
     const uint32_t *last = d.status + (uint64_t)(b.tiles - 1) * 256u;
-    const uint32_t c = t < b.nb ? (last[t] & kValMask) : 0u;
+    const uint32_t c = t < d.nb ? (last[t] & kValMask) : 0u;
     const uint32_t before = wave_sum(t < bkt ? c : 0u);
     if (lane == 0) sh.redu[w] = before;
     if (t == bkt) sh.offs[0] = c;
@@ -1386,17 +1389,17 @@ __global__ __launch_bounds__(kBkTPB) void k_ss_bucket(SsBatch b)
     }
 }
 
-uint32_t n_buckets(uint64_t n)
+uint32_t n_buckets(uint64_t n, uint32_t avg = kBucketAvg)
 {
-    const uint64_t b = cdiv(n, kBucketAvg);
+    const uint64_t b = cdiv(n, avg);
     return (uint32_t)(b < 1 ? 1 : (b > kMaxBuckets ? kMaxBuckets : b));
 }
 
 uint32_t n_samples(uint64_t n)
 {
-    // 1024 samples (16 per bucket up to 2^16 requests, 8 up to 2^17), 2048
-    // above (8 per bucket); the average bucket is at most a quarter of the
-    // region capacity
+    // 1024 samples up to 2^17 requests, 2048 above: 8 to 16 per bucket of
+    // the SJF and Aging rows (an average bucket of at most a quarter of the
+    // region), 4 to 8 per bucket of the FIFO row (at most an eighth)
     const uint64_t smax = n <= (1u << 17) ? kSamples / 2 : kSamples;
     return (uint32_t)(n < smax ? n : smax);
 }
@@ -1410,7 +1413,7 @@ uint32_t sample_blocks(uint64_t n)
 uint64_t region_bytes(uint64_t n)
 {
     const uint64_t tiles = cdiv(n, kScTile);
-    const uint64_t nb = n_buckets(n);
+    const uint64_t nb = n_buckets(n, kBucketAvgFifo);   // every row's regions hold the most buckets
     return align_up(sizeof(SsCtl), 256) + 2 * align_up(kSamples * 8, 256) + align_up(kSamples * 4, 256) +
            align_up(tiles * 256 * 4, 256) + 2 * align_up(nb * kCap * 8, 256) + align_up(nb * kCap * 4, 256) +
            align_up(kQ * 4, 256) + align_up(nb * 2 * kQ * 4, 256) + 4 * align_up(n * 8, 256) +
@@ -1420,7 +1423,7 @@ uint64_t region_bytes(uint64_t n)
 void carve(uint8_t *p, uint64_t n, SsDesc &d)
 {
     const uint64_t tiles = cdiv(n, kScTile);
-    const uint64_t nb = n_buckets(n);
+    const uint64_t nb = n_buckets(n, kBucketAvgFifo);
     auto take = [&](uint64_t bytes) {
         uint8_t *q = p;
         p += align_up(bytes, 256);
@@ -1461,7 +1464,7 @@ hipError_t ssort_launch(const SortInput &in, const SortJob *jobs, uint32_t nsort
     b.in = in;
     b.n = in.n;
     b.tiles = (uint32_t)cdiv(in.n, kScTile);
-    b.nb = n_buckets(in.n);
+    b.nb = 1;
     b.ns = n_samples(in.n);
     b.serial = serial ? 1u : 0u;
     b.nsorts = nsorts;
@@ -1474,6 +1477,8 @@ hipError_t ssort_launch(const SortInput &in, const SortJob *jobs, uint32_t nsort
         const SortKind k = jobs[i].kind;
         if (k != SortKind::Fifo && k != SortKind::Budget && k != SortKind::Aging) return hipErrorInvalidValue;
         d.kind = k;
+        d.nb = n_buckets(in.n, k == SortKind::Fifo ? kBucketAvgFifo : kBucketAvg);
+        b.nb = d.nb > b.nb ? d.nb : b.nb;
         if (k == SortKind::Fifo && parts && (parts->perm[0] || parts->perm[1])) {
             for (int e = 0; e < 2; e++) {
                 d.pw_out[e] = parts->perm[e];
