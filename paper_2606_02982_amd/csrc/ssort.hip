@@ -728,7 +728,7 @@ __device__ __forceinline__ uint32_t block_excl_scan(BkShared &sh, uint32_t x)
 // (key, entry). A bin of more than kBinMax entries sends the whole bucket
 // through stable LSD passes on the key bytes that vary in it instead.
 __device__ __forceinline__ bool rank_pass(BkShared &sh, uint64_t *k, const uint64_t *k2, uint32_t reff, uint32_t m,
-                                          uint64_t kmn, uint64_t kmx, uint32_t *rank)
+                                          uint64_t kmn, uint64_t kmx, uint32_t *rank, bool bins_zero = false)
 {
     constexpr int kWaves = kBkTPB / 64;
     const uint32_t t = threadIdx.x;
@@ -740,7 +740,8 @@ __device__ __forceinline__ bool rank_pass(BkShared &sh, uint64_t *k, const uint6
         for (int r = 0; r < kBkR; r++) rank[r] = (uint32_t)w * wk + (uint32_t)r * 64u + (uint32_t)lane;
         return !k2;   // one key: the order is by k2 alone
     }
-    for (uint32_t i = t; i <= kBins; i += kBkTPB) sh.bin[i] = 0;
+    if (!bins_zero)
+        for (uint32_t i = t; i <= kBins; i += kBkTPB) sh.bin[i] = 0;
     // excl: the minimum-key entries are ranked apart (one key only).
     // rank[r] first holds the number of minimum-key entries before entry r
     // (its rank if it has the minimum key; the valid entries are a prefix,
@@ -782,7 +783,7 @@ __device__ __forceinline__ bool rank_pass(BkShared &sh, uint64_t *k, const uint6
 #pragma unroll
         for (int r = 0; r < kBkR; r++) rank[r] += before_w;
         __syncthreads();   // sh.wsum is reused by the bin scan
-    } else {
+    } else if (!bins_zero) {
         __syncthreads();   // the bins are zero before any count goes in
     }
     if (kmn2 >= kmx) {
@@ -1021,8 +1022,9 @@ __device__ __forceinline__ bool rank_pass(BkShared &sh, uint64_t *k, const uint6
 }
 
 // Requests per tier and each class's first position, into sh.pt; clears the
-// digit counters. Every thread calls it.
-__device__ __forceinline__ void load_pw(const SsBatch &b, const SsDesc &d, BkShared &sh)
+// digit counters. Every thread calls pw_params, then (after a barrier)
+// pw_starts; load_pw does both.
+__device__ __forceinline__ void pw_params(const SsBatch &b, const SsDesc &d, BkShared &sh)
 {
     const uint32_t t = threadIdx.x;
     if (t < kQ) {
@@ -1036,12 +1038,23 @@ __device__ __forceinline__ void load_pw(const SsBatch &b, const SsDesc &d, BkSha
     if (d.pw_out[1] && b.in.wrr_mode == kWrrSmooth)
         for (uint32_t i = t; i < sizeof(WrrPlanHead) / 4; i += kBkTPB)
             reinterpret_cast<uint32_t *>(&sh.pt.wh)[i] = reinterpret_cast<const uint32_t *>(&b.plan->h)[i];
-    __syncthreads();
+}
+
+__device__ __forceinline__ void pw_starts(const SsBatch &b, BkShared &sh)
+{
+    const uint32_t t = threadIdx.x;
     if (t < kQ) {
         uint32_t s = 0;
         for (uint32_t q = 0; q < b.in.n_tiers && q < kQ; q++) s += sh.pt.cls[q] < t ? sh.pt.tot[q] : 0u;
         sh.pt.cstart[t] = s;
     }
+}
+
+__device__ __forceinline__ void load_pw(const SsBatch &b, const SsDesc &d, BkShared &sh)
+{
+    pw_params(b, d, sh);
+    __syncthreads();
+    pw_starts(b, sh);
 }
 
 // Stable ranks of this thread's entries (wave-major, entry idx =
@@ -1210,6 +1223,7 @@ __global__ __launch_bounds__(kBkTPB) void k_ss_bucket(SsBatch b)
         return;
     }
     if (bkt >= d.nb) return;   // a row with fewer buckets than the grid is wide
+    const bool pw = d.pw_out[0] || d.pw_out[1];   // FIFO row with the partitions
     const uint64_t *src1 = d.bk1 + (uint64_t)bkt * kCap;
     const uint64_t *src2 = d.bk2 + (uint64_t)bkt * kCap;
     const uint32_t *srcj = d.bj + (uint64_t)bkt * kCap;
@@ -1229,6 +1243,10 @@ __global__ __launch_bounds__(kBkTPB) void k_ss_bucket(SsBatch b)
         pb[i] = two ? src2[s] : 0ull;
         pj[i] = srcj[s];
     }
+    // the partitions' parameters (their loads in flight with the slots'),
+    // and the bins of the first rank pass cleared, before the size barrier
+    if (pw) pw_params(b, d, sh);
+    for (uint32_t i = t; i <= kBins; i += kBkTPB) sh.bin[i] = 0;
     // bucket sizes: the last tile's inclusive prefixes
     const uint32_t *last = d.status + (uint64_t)(b.tiles - 1) * 256u;
     const uint32_t c = t < d.nb ? (last[t] & kValMask) : 0u;
@@ -1251,8 +1269,7 @@ __global__ __launch_bounds__(kBkTPB) void k_ss_bucket(SsBatch b)
     const uint32_t wk = 64u * reff;
 
     // the entries (index order within the bucket) and the keys' ranges
-    const bool pw = d.pw_out[0] || d.pw_out[1];   // FIFO row with the partitions
-    if (pw) load_pw(b, d, sh);
+    if (pw) pw_starts(b, sh);
     uint64_t k[kBkR], k2[kBkR];
     uint32_t jv[kBkR], rank[kBkR], q[kBkR];
 #pragma unroll
@@ -1305,7 +1322,7 @@ __global__ __launch_bounds__(kBkTPB) void k_ss_bucket(SsBatch b)
     // arrival order (skipped when the bucket holds one k1); FIFO: one pass
     // by arrival.
     const bool both = two && mn1 < mx1;
-    bool done = (both || (!two && mn1 < mx1)) && rank_pass(sh, k, k2, reff, m, mn1, mx1, rank);
+    bool done = (both || (!two && mn1 < mx1)) && rank_pass(sh, k, k2, reff, m, mn1, mx1, rank, true);
     if (!done) {
         const uint32_t npass = both ? 2u : 1u;
         for (uint32_t ps = 0; ps < npass; ps++) {
