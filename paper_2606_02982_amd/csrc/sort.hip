@@ -5,8 +5,9 @@
 // Used for: the FIFO rank (key = arrival), SJF and Aging (key = budget or
 // aged score over the FIFO sequence, so that ties keep FIFO order), the
 // one-pass partitions of Priority (priority class) and Weighted (tier, then
-// the closed-form round-robin position), and the group partition of the
-// calibration scan.
+// the round-robin position: a closed form for the blocked and stride
+// interleavings, the period table built by k_sort_plan for the smooth one),
+// and the group partition of the calibration scan.
 //
 // Launches of one batch of sorts:
 //   k_sort_init  produces the pairs from the inputs, writes each block's digit

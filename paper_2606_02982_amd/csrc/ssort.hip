@@ -17,9 +17,12 @@
 // the count over earlier buckets (decoupled look-back over the buckets'
 // digit counts) plus its rank in the bucket. Priority puts it at its class's
 // first position plus that rank; Weighted at the round-robin position of
-// the k-th request of tier t:
+// the k-th request of tier t, blocked:
 //   sum_t' min(n_t', r w_t') + sum_{t' < t} min(w_t', max(0, n_t' - r w_t'))
-//   + (k - r w_t),  r = floor(k / w_t).
+//   + (k - r w_t),  r = floor(k / w_t);
+// smooth: from the period table of the smooth interleaving (wrrplan.h),
+// built by the FIFO row's last scatter tile; stride: from the closed form
+// of the passes (k + 1) / w_t.
 //
 //   k_ss_sample   S triples (1024 up to 2^17 requests, else 2048) at
 //                 stratified random positions; each of S/8 blocks stages all
