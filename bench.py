@@ -48,9 +48,11 @@ def parse():
     ap.add_argument("--workload", default="batch64k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
-    ap.add_argument("--stage", choices=["pipeline", "characterize", "errors", "drift", "simulate"],
+    ap.add_argument("--stage", choices=["pipeline", "characterize", "errors", "drift", "simulate", "split"],
                     default="pipeline",
                     help="characterize: time only stage 1 on --workload (any workload with text); "
+                         "split: Python len(p.split()) per prompt of batch4k on one host core, "
+                         "the reference point of the paper's tokenizer-overhead table (no GPU); "
                          "errors: the estimation-error diagnostics on --workload's events; "
                          "drift: calibration at each alpha and the Aging re-sorts at every tick "
                          "(drift4m); simulate: the dispatch-tick loop on --workload, per policy")
@@ -85,8 +87,40 @@ def to_dev(a):
     return torch.from_numpy(a).cuda()
 
 
+def bench_split(wl):
+    """Python's len(p.split()) on each prompt, one host core: the split() column
+    of the paper's tokenizer-overhead comparison, on synthetic prompts."""
+    from paper_2606_02982_amd import synth
+    b = synth.generate(wl.name)
+    prompts = [bytes(b.text[b.offsets[i]:b.offsets[i + 1]]).decode("utf-8", "surrogateescape")
+               for i in range(b.n)]
+    nbytes = int(b.offsets[-1])
+    best = None
+    for _ in range(3):
+        t0 = time.perf_counter()
+        counts = [len(p.split()) for p in prompts]
+        el = time.perf_counter() - t0
+        best = el if best is None or el < best else best
+    assert counts == [int(x) for x in b.words], "split() disagrees with the generator's word counts"
+    model = ""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    print(json.dumps({"metric": "python str.split() per prompt (one host core)", "workload": wl.name,
+                      "prompts": b.n, "text_bytes": nbytes, "us_per_prompt": round(best / b.n * 1e6, 3),
+                      "MB_per_s": round(nbytes / best / 1e6, 1), "reps": 3, "timing": "best of 3",
+                      "host_cores": os.cpu_count(), "cpu_model": model}), flush=True)
+
+
 def main():
     args = parse()
+    if args.stage == "split":
+        from paper_2606_02982_amd import synth
+        return bench_split(synth.WORKLOADS["batch4k"])
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py: this build runs the admission hot path on one GPU; --gpus %d is not "
