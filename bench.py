@@ -48,10 +48,13 @@ def parse():
     ap.add_argument("--workload", default="batch64k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
-    ap.add_argument("--stage", choices=["pipeline", "characterize", "errors", "drift", "simulate", "split"],
+    ap.add_argument("--stage", choices=["pipeline", "characterize", "errors", "drift", "simulate", "split",
+                                        "ceiling"],
                     default="pipeline",
                     help="characterize: time only stage 1 on --workload (any workload with text); "
                          "split: Python len(p.split()) per prompt of batch4k on one host core, "
+                         "ceiling: the read side of characterize alone over --workload's text size "
+                         "(ds_read_bandwidth: the practical read rate of its access pattern); "
                          "the reference point of the paper's tokenizer-overhead table (no GPU); "
                          "errors: the estimation-error diagnostics on --workload's events; "
                          "drift: calibration at each alpha and the Aging re-sorts at every tick "
@@ -116,6 +119,35 @@ def bench_split(wl):
                       "host_cores": os.cpu_count(), "cpu_model": model}), flush=True)
 
 
+def bench_ceiling(args, wl):
+    """ds_read_bandwidth over a buffer of the workload's text size: the same
+    wave ranges and loads as characterize, without the classification."""
+    import torch
+    from paper_2606_02982_amd import driftsched as ds
+    from paper_2606_02982_amd import synth
+    nbytes = synth.generate(wl.name).offsets[-1] // 16 * 16
+    buf = torch.randint(0, 256, (int(nbytes),), dtype=torch.uint8, device="cuda")
+    out = torch.empty(1, dtype=torch.int32, device="cuda")
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < args.settle:
+        ds.read_bandwidth(buf, out)
+        torch.cuda.synchronize()
+    for _ in range(args.warmup):
+        ds.read_bandwidth(buf, out)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(args.steps):
+        ds.read_bandwidth(buf, out)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    print(json.dumps({"metric": "read side of characterize alone (ds_read_bandwidth) GB/s", "value": round(gbs, 1),
+                      "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4), "ms_per_call": round(ms, 4),
+                      "bytes": int(nbytes), "steps": args.steps, "config": {"workload": wl.name}}), flush=True)
+
+
 def main():
     args = parse()
     if args.stage == "split":
@@ -136,6 +168,8 @@ def main():
     wl = synth.WORKLOADS[args.workload]
     if args.stage == "characterize":
         return bench_characterize(args, wl)
+    if args.stage == "ceiling":
+        return bench_ceiling(args, wl)
     if args.stage == "errors":
         return bench_errors(args, wl)
     if args.stage == "drift":

@@ -25,6 +25,10 @@
  *   ds_simulate         dispatch ticks: order the pending set, dispatch a
  *                       batch, feed its completions back into the factors
  *
+ * and one measurement aid:
+ *
+ *   ds_read_bandwidth   the read side of ds_characterize alone
+ *
  * Conventions shared by every entry point:
  *  - Array arguments are DEVICE pointers (memory from hipMalloc or any
  *    allocator of the same device, e.g. torch tensors); parameter structs
@@ -410,6 +414,22 @@ ds_status ds_simulate(uint32_t n, const double *arrival, const uint8_t *tier,
                       const double *tick_t, uint32_t n_ticks, const ds_sim_params *params,
                       double *state, uint32_t *seq, int32_t *tick_of, uint32_t *n_dispatched,
                       void *ws, size_t ws_bytes, uint32_t flags, ds_stream stream);
+
+/*
+ * Measurement aid: the practical HBM read rate of ds_characterize's access
+ * pattern. Streams `bytes` of buf with the same wave ranges and 16-byte
+ * nontemporal loads as the characterize kernel, with no classification. Each
+ * wave writes the XOR of its words to a word of its own in xor_out, so the
+ * XOR of the DS_READ_BW_WORDS words written there is the XOR of all the
+ * buffer's 32-bit (little-endian) words, and no load can be dropped.
+ *
+ *  buf      device, 16-byte aligned (else DS_ERR_ALIGN); may be NULL if bytes == 0
+ *  bytes    a multiple of 16 (else DS_ERR_ARG)
+ *  xor_out  device, DS_READ_BW_WORDS uint32, 4-byte aligned; written
+ * No workspace; asynchronous on stream.
+ */
+#define DS_READ_BW_WORDS 32768
+ds_status ds_read_bandwidth(const void *buf, uint64_t bytes, uint32_t *xor_out, ds_stream stream);
 
 /* Workspace size for op at size n (prompts, events or requests); n_groups
  * is used by DS_OP_CALIBRATE only. */

@@ -8,6 +8,7 @@
 #include "kernels.h"
 
 static_assert(DS_WRR_MAX_WEIGHT_SUM == ds::kWrrMaxWeightSum, "smooth round robin weight bound");
+static_assert(DS_READ_BW_WORDS == ds::kReadBwWords, "read-rate output words");
 static_assert(DS_WRR_BLOCKED == ds::kWrrBlocked && DS_WRR_SMOOTH == ds::kWrrSmooth &&
                   DS_WRR_STRIDE == ds::kWrrStride,
               "weighted modes");
@@ -404,6 +405,15 @@ ds_status ds_simulate(uint32_t n, const double *arrival, const uint8_t *tier,
     a.n_dispatched = n_dispatched;
     hipStream_t s = static_cast<hipStream_t>(stream);
     return run(ws, flags, s, [&](uint32_t *flag) { return sim_launch(a, after_flag(ws), flag, s); });
+}
+
+ds_status ds_read_bandwidth(const void *buf, uint64_t bytes, uint32_t *xor_out, ds_stream stream)
+{
+    if (bytes % 16 != 0) return DS_ERR_ARG;
+    if (!xor_out || (bytes && !buf)) return DS_ERR_NULL;
+    if (!aligned(xor_out, 4) || (buf && !aligned(buf, 16))) return DS_ERR_ALIGN;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    return hip_status(readbw_launch(buf, bytes, xor_out, s));
 }
 
 }  // extern "C"

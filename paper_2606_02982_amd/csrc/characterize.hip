@@ -690,6 +690,59 @@ __global__ void k_char_validate(const uint64_t *__restrict__ off, uint32_t N, ui
     if (bad) atomicOr(flag, 1u);
 }
 
+// The read side of k_char_main alone: the same wave ranges and 16-byte
+// nontemporal loads, four rounds in flight per wave, and no classification;
+// each wave's XOR of its words goes to sink[w], so that no load is dropped.
+// B is a multiple of 16.
+__global__ __launch_bounds__(kBlock) void k_read_stream(const uint8_t *__restrict__ p, uint64_t B, uint64_t Rw,
+                                                      uint32_t nwaves, uint32_t *__restrict__ sink)
+{
+    const uint32_t w = (uint32_t)__builtin_amdgcn_readfirstlane((int)(blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6)));
+    if (w >= nwaves) return;
+    const int lane = lane_id();
+    const uint64_t b = (uint64_t)w * Rw, e = b + Rw < B ? b + Rw : B;
+    uint32_t acc = 0;
+    for (uint64_t sb = b; sb < e; sb += (uint64_t)kRound * kLoadRounds) {
+        v4u d[kLoadRounds];
+#pragma unroll
+        for (uint32_t u = 0; u < kLoadRounds; u++) {
+            const uint64_t c = sb + (uint64_t)u * kRound + 16u * (uint32_t)lane;   // c < e: c + 16 <= e
+            d[u] = c < e ? __builtin_nontemporal_load(reinterpret_cast<const v4u *>(p + c)) : v4u{0u, 0u, 0u, 0u};
+        }
+#pragma unroll
+        for (uint32_t u = 0; u < kLoadRounds; u++) acc ^= d[u].x ^ d[u].y ^ d[u].z ^ d[u].w;
+    }
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) acc ^= (uint32_t)__shfl_xor((int)acc, m, 64);
+    if (lane == 0) sink[w] = acc;
+}
+
+// Wave ranges of k_char_main for B bytes: one per resident wave slot (CUs x
+// resident waves of k_char_main per CU) times kRangesPerSlot, whole 4 KiB
+// super-rounds.
+hipError_t char_waves(uint64_t B, uint64_t &Rw, uint32_t &nwaves)
+{
+    static int resident_cache[64];
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    int resident = dev >= 0 && dev < 64 ? resident_cache[dev] : 0;
+    if (resident == 0) {
+        int n_cu = 0, per_cu = 0;
+        e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
+        if (e != hipSuccess) return e;
+        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_char_main, kBlock, 0);
+        if (e != hipSuccess) return e;
+        resident = (n_cu > 0 ? n_cu : 1) * (per_cu > 0 ? per_cu : 1) * (int)(kBlock / 64);
+        if (dev >= 0 && dev < 64) resident_cache[dev] = resident;
+    }
+    uint64_t target = (uint64_t)resident * kRangesPerSlot;
+    if (target > kMaxWaves) target = kMaxWaves;
+    Rw = align_up(cdiv(B ? B : 1, target), (uint64_t)kRound * kLoadRounds);
+    nwaves = (uint32_t)cdiv(B, Rw);
+    return hipSuccess;
+}
+
 }  // namespace
 
 size_t char_ws_bytes(uint64_t n)
@@ -711,26 +764,10 @@ hipError_t char_launch(const uint8_t *text, uint64_t B, const uint64_t *offsets,
         hipLaunchKernelGGL(k_char_validate, dim3(blocks), dim3(256), 0, s, offsets, n, B, flag);
         return hipGetLastError();
     }
-    // one wave range per resident wave (CUs x resident waves per CU); ranges
-    // are whole 4 KiB super-rounds
-    static int resident_cache[64];
-    int dev = 0;
-    hipError_t e = hipGetDevice(&dev);
+    uint64_t Rw = 0;
+    uint32_t nwaves = 0;
+    hipError_t e = char_waves(B, Rw, nwaves);
     if (e != hipSuccess) return e;
-    int resident = dev >= 0 && dev < 64 ? resident_cache[dev] : 0;
-    if (resident == 0) {
-        int n_cu = 0, per_cu = 0;
-        e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
-        if (e != hipSuccess) return e;
-        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_char_main, kBlock, 0);
-        if (e != hipSuccess) return e;
-        resident = (n_cu > 0 ? n_cu : 1) * (per_cu > 0 ? per_cu : 1) * (int)(kBlock / 64);
-        if (dev >= 0 && dev < 64) resident_cache[dev] = resident;
-    }
-    uint64_t target = (uint64_t)resident * kRangesPerSlot;
-    if (target > kMaxWaves) target = kMaxWaves;
-    uint64_t Rw = align_up(cdiv(B ? B : 1, target), (uint64_t)kRound * kLoadRounds);
-    uint32_t nwaves = (uint32_t)cdiv(B, Rw);
     if (nwaves > 0) {
         uint32_t blocks = (uint32_t)cdiv(nwaves, kBlock / 64);
         hipLaunchKernelGGL(k_char_main, dim3(blocks), dim3(kBlock), 0, s, text, B, offsets, n, Rw,
@@ -742,6 +779,21 @@ hipError_t char_launch(const uint8_t *text, uint64_t B, const uint64_t *offsets,
         hipLaunchKernelGGL(k_char_fin, dim3(fblocks), dim3(256), 0, s, offsets, n, B,
                            (uint32_t)(Rw >> 10), nwaves, wavetot, ploc, counts,
                            score ? *score : ScoreArgs{});
+    return hipGetLastError();
+}
+
+hipError_t readbw_launch(const void *buf, uint64_t bytes, uint32_t *xor_out, hipStream_t s)
+{
+    hipError_t e = fill_u32(xor_out, 0u, kReadBwWords, s);   // a fill kernel, not a memset
+    if (e != hipSuccess || bytes == 0) return e;
+    uint64_t Rw = 0;
+    uint32_t nwaves = 0;
+    e = char_waves(bytes, Rw, nwaves);
+    if (e != hipSuccess) return e;
+    static_assert(kMaxWaves <= kReadBwWords, "a word per wave");
+    const uint32_t blocks = (uint32_t)cdiv(nwaves, kBlock / 64);
+    hipLaunchKernelGGL(k_read_stream, dim3(blocks), dim3(kBlock), 0, s, static_cast<const uint8_t *>(buf), bytes, Rw,
+                       nwaves, xor_out);
     return hipGetLastError();
 }
 

@@ -172,5 +172,9 @@ hipError_t sim_launch(const SimArgs &a, void *ws, uint32_t *flag, hipStream_t s)
 
 // ---- misc --------------------------------------------------------------------------
 hipError_t fill_u32(uint32_t *p, uint32_t v, uint64_t n, hipStream_t s);
+// The read side of characterize alone (bytes a multiple of 16): the XOR of
+// the kReadBwWords words of xor_out = the XOR of the buffer's 32-bit words.
+constexpr uint32_t kReadBwWords = 32768;   // one per wave (at most this many waves)
+hipError_t readbw_launch(const void *buf, uint64_t bytes, uint32_t *xor_out, hipStream_t s);
 
 }  // namespace ds

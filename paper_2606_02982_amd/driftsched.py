@@ -64,6 +64,7 @@ def _load():
     lib.ds_calibrate_ex.argtypes = [P, P, P, u64, f64, u32, P, P, P, P, sz, u32, P]
     lib.ds_error_stats.argtypes = [u64, P, P, P, P, u32, P, P, sz, u32, P]
     lib.ds_class_histogram.argtypes = [u32, P, u32, P, P, P, sz, u32, P]
+    lib.ds_read_bandwidth.argtypes = [P, u64, P, P]
     lib.ds_score.argtypes = [u32, P, P, P, P, P, u32, P, u32, P, u32, ctypes.POINTER(ScoreParams),
                              P, P, P, P, P, sz, u32, P]
     lib.ds_characterize_score.argtypes = [P, u64, P, u32, P, P, P, P, P, u32, P, u32, P, u32,
@@ -203,6 +204,23 @@ def error_stats(est, observed, factor=None, group=None, n_groups=0, out=None, ws
         ws = workspace(OP_ERROR_STATS, n, n_groups, dev)
     _check(lib.ds_error_stats(n, _ptr(est), _ptr(factor), _ptr(observed), _ptr(group), int(n_groups),
                               _ptr(out), _ptr(ws), ws.numel(), _flags(validate), _stream()))
+    return out
+
+
+READ_BW_WORDS = 32768
+
+
+def read_bandwidth(buf, out=None):
+    """The read side of characterize alone over a contiguous device tensor
+    (its size a multiple of 16 bytes). Returns an int32 tensor of
+    READ_BW_WORDS words whose XOR is the XOR of the buffer's 32-bit words."""
+    if not buf.is_cuda or not buf.is_contiguous():
+        raise ValueError("buf must be a contiguous device tensor")
+    if out is None:
+        out = torch.empty(READ_BW_WORDS, dtype=torch.int32, device=buf.device)
+    _dev(out, torch.int32, "out")
+    nbytes = buf.numel() * buf.element_size()
+    _check(lib.ds_read_bandwidth(_ptr(buf) if nbytes else None, nbytes, _ptr(out), _stream()))
     return out
 
 

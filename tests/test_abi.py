@@ -26,8 +26,9 @@ def declared_functions():
 def test_exports_every_declared_symbol(ds):
     names = declared_functions()
     assert names == ["ds_calibrate", "ds_calibrate_ex", "ds_characterize", "ds_characterize_score",
-                     "ds_class_histogram", "ds_error_stats", "ds_order", "ds_order_multi", "ds_score",
-                     "ds_simulate", "ds_status_string", "ds_version", "ds_workspace_bytes"]
+                     "ds_class_histogram", "ds_error_stats", "ds_order", "ds_order_multi",
+                     "ds_read_bandwidth", "ds_score", "ds_simulate", "ds_status_string", "ds_version",
+                     "ds_workspace_bytes"]
     for name in names:
         assert hasattr(ds.lib, name), name
 
@@ -230,3 +231,12 @@ def test_characterize_score_host_errors(ds):
     assert f(FAKE, 16, FAKE, 4, FAKE, *sc, ctypes.byref(good), *outs, FAKE_WS, 16, 0, NULL) == -4
     assert f(FAKE, 16, FAKE, 0xFFFFFFFF, FAKE, *sc, ctypes.byref(good), *outs, FAKE_WS, ws, 0, NULL) == -3
     assert f(NULL, 0, NULL, 0, NULL, *sc, ctypes.byref(good), *outs, NULL, 0, 0, NULL) == 0
+
+
+def test_read_bandwidth_host_errors(ds):
+    f = ds.lib.ds_read_bandwidth
+    assert f(FAKE, 17, FAKE, NULL) == -2      # not a multiple of 16
+    assert f(NULL, 32, FAKE, NULL) == -1
+    assert f(FAKE, 32, NULL, NULL) == -1
+    assert f(P(0x1008), 32, FAKE, NULL) == -7  # not 16-byte aligned
+    assert f(FAKE, 32, P(0x1002), NULL) == -7

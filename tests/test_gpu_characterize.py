@@ -190,3 +190,16 @@ def test_long_prompts_sparse_multibyte(ds, oracle, density):
     got = check(ds, oracle, text, offsets)
     want = np.array([len(p.decode().split()) for p in prompts], dtype=np.uint32)
     assert np.array_equal(got, want)
+
+
+@pytest.mark.parametrize("nbytes", [0, 16, 4096 + 16, (10 << 20) + 48, 64 << 20])
+def test_read_bandwidth_xor(nbytes):
+    # the measurement aid reads every byte: the XOR of the buffer's words
+    from paper_2606_02982_amd import driftsched as ds
+    rng = np.random.default_rng(nbytes)
+    host_buf = rng.integers(0, 256, nbytes, dtype=np.uint8)
+    print("read_bandwidth bytes=%d" % nbytes, flush=True)
+    out = host(ds.read_bandwidth(dev(host_buf)), np.uint32)
+    assert out.size == ds.READ_BW_WORDS
+    want = np.bitwise_xor.reduce(host_buf.view(np.uint32)) if nbytes else np.uint32(0)
+    assert np.bitwise_xor.reduce(out) == np.uint32(want)
