@@ -331,6 +331,21 @@ def main():
     # sanity: the counts of the last step equal the generator's word counts
     assert np.array_equal(counts.cpu().numpy().view(np.uint32), b.words), "counts mismatch"
 
+    # the practical read ceiling of characterize's access pattern, after the
+    # timed region: its read side alone over the same text buffer
+    rb = (int(text.numel()) // 16) * 16
+    rbuf, rout = text[:rb], torch.empty(ds.READ_BW_WORDS, dtype=torch.int32, device="cuda")
+    for _ in range(5):
+        ds.read_bandwidth(rbuf, rout)
+    r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    r0.record()
+    for _ in range(20):
+        ds.read_bandwidth(rbuf, rout)
+    r1.record()
+    torch.cuda.synchronize()
+    ceil_gbs = rb / (r0.elapsed_time(r1) / 20 * 1e-3) / 1e9
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(b, args.cpu_seconds, args.weighted_mode)
@@ -367,6 +382,9 @@ def main():
                      "algorithmic_bytes": int(cs_bytes),
                      "traffic": measured_traffic(wl.name)},
         "cpu_baseline": cpu,
+        "read_ceiling": {"kernel": "ds_read_bandwidth (characterize's waves and loads, no classification)",
+                         "achieved": round(ceil_gbs, 1), "unit": "GB/s", "frac": round(ceil_gbs / HBM_PEAK_GBS, 4),
+                         "characterize_score_of_ceiling": round(char_gbs / ceil_gbs, 4)},
     }
     print(json.dumps(out), flush=True)
 
