@@ -242,3 +242,31 @@ def test_validate_flag(ds):
     good = dev(np.array([1, 0, 2], np.uint32))
     p, _ = ds.order(1, tier, arr, fifo=good, validate=True)
     assert list(host(p)) == [0, 1, 2]
+
+
+@pytest.mark.parametrize("pol", POLICIES)
+@pytest.mark.parametrize("n", [700, 4096])
+def test_small_batch_crowded_keys(ds, oracle, pol, n):
+    # small batches (a few buckets per row): three budget values and coarse
+    # arrivals crowd the bins, so the two-key rows take the two-pass fallback
+    rng = np.random.default_rng(n + 31 * pol)
+    tier = rng.integers(0, 3, n).astype(np.uint8)
+    arr = np.round(rng.uniform(0.0, 10.0, n) * 2.0) / 2.0
+    bud = rng.choice([100.0, 200.0, 300.0], n)
+    check(ds, oracle, pol, tier, arr, bud, t_now=10.0, aging_rate=0.3)
+
+
+@pytest.mark.parametrize("n", [1, 33, 2048, 4096])
+def test_small_batch_multi(ds, oracle, n):
+    # the five orders of one call at batch sizes of one to four buckets
+    rng = np.random.default_rng(n)
+    tier = rng.integers(0, 4, n).astype(np.uint8)
+    arr = np.round(rng.uniform(0.0, 5.0, n), 2)
+    bud = np.round(rng.uniform(1.0, 3000.0, n), 1)
+    kw = dict(weights=(3, 1, 2, 5), tier_priority=(1.0, 0.0, 1.0, 2.0), aging_rate=0.05, t_now=5.0)
+    print("small-batch order_multi n=%d" % n, flush=True)
+    perms, keys = ds.order_multi((0, 1, 2, 3, 4), dev(tier), dev(arr), dev(bud), keys=True, n_tiers=4, **kw)
+    for p in range(5):
+        w_perm, w_key = oracle.order(p, tier, arr, bud, **kw)
+        assert np.array_equal(host(perms[p], np.uint32), w_perm), "policy %d" % p
+        assert np.array_equal(host(keys[p]), w_key), "policy %d" % p
