@@ -240,3 +240,31 @@ def test_read_bandwidth_host_errors(ds):
     assert f(FAKE, 32, NULL, NULL) == -1
     assert f(P(0x1008), 32, FAKE, NULL) == -7  # not 16-byte aligned
     assert f(FAKE, 32, P(0x1002), NULL) == -7
+
+
+def test_param_struct_layouts_match_the_header(ds, tmp_path):
+    # the binding's ctypes structures have the C header's sizes and field
+    # offsets (gcc compiles a program that prints them)
+    import shutil
+    import subprocess
+    if shutil.which("gcc") is None:
+        pytest.skip("gcc not available")
+    structs = {"ds_score_params": ds.ScoreParams, "ds_order_params": ds.OrderParams,
+               "ds_sim_params": ds.SimParams}
+    lines = ["#include <stddef.h>", "#include <stdio.h>", '#include "driftsched.h"', "int main(void) {"]
+    for cname, cls in structs.items():
+        lines.append('printf("%s %%zu\\n", sizeof(%s));' % (cname, cname))
+        for fname, _ in cls._fields_:
+            lines.append('printf("%s.%s %%zu\\n", offsetof(%s, %s));' % (cname, fname, cname, fname))
+    lines += ["return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    inc = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include")
+    subprocess.run(["gcc", "-std=c99", "-I", inc, str(src), "-o", str(exe)], check=True)
+    got = dict(line.split() for line in subprocess.run([str(exe)], check=True, capture_output=True,
+                                                        text=True).stdout.splitlines())
+    for cname, cls in structs.items():
+        assert int(got[cname]) == ctypes.sizeof(cls), cname
+        for fname, _ in cls._fields_:
+            assert int(got["%s.%s" % (cname, fname)]) == getattr(cls, fname).offset, (cname, fname)
