@@ -627,7 +627,8 @@ def bench_simulate(args, wl):
     a2 = argparse.Namespace(**dict(vars(args), steps=steps, warmup=1, settle=0.0))
     for name, pol in ds.POLICIES.items():
         p = ds.sim_params(pol, batch=32, alpha=b.alphas[0], weights=tuple(int(w) for w in b.weights),
-                          tier_priority=tuple(b.tier_priority), aging_rate=b.aging_rate)
+                          tier_priority=tuple(b.tier_priority), aging_rate=b.aging_rate,
+                          weighted_mode=args.weighted_mode)
 
         def run():
             state.fill_(1.0)
