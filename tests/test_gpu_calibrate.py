@@ -7,7 +7,7 @@ calibration contract states (1e-12 relative, per event and final state).
 import numpy as np
 import pytest
 
-from paper_2606_02982_amd import synth
+from tests import wl
 from tests.gpu_util import dev, host, rel_close
 
 pytestmark = pytest.mark.gpu
@@ -47,13 +47,13 @@ def test_dyadic_exact(ds):
 
 @pytest.mark.parametrize("name", ["batch4k", "batch64k", "chat1m", "long16k"])
 def test_workload_events(ds, oracle, name):
-    b = synth.generate(name, with_text=False)
+    b = wl.load(name, with_text=False)
     check(ds, oracle, b.ev_group, b.ev_est, b.ev_obs, b.alphas[0], np.ones(b.n_groups))
 
 
 @pytest.mark.parametrize("alpha", [0.05, 0.2])
 def test_drift_events(ds, oracle, alpha):
-    b = synth.generate("drift4m")
+    b = wl.load("drift4m")
     check(ds, oracle, b.ev_group, b.ev_est, b.ev_obs, alpha, np.ones(b.n_groups))
 
 
@@ -87,7 +87,7 @@ def test_skipped_events_and_extreme_alpha(ds, oracle):
 
 
 def test_resume_equals_one_call(ds, oracle):
-    b = synth.generate("batch64k", with_text=False)
+    b = wl.load("batch64k", with_text=False)
     g, e, o = b.ev_group, b.ev_est, b.ev_obs
     st1, tr1 = run(ds, g[:20000], e[:20000], o[:20000], 0.1, np.ones(b.n_groups))
     st2, tr2 = run(ds, g[20000:], e[20000:], o[20000:], 0.1, st1)
@@ -116,7 +116,7 @@ def test_groups_with_only_skipped_events_unchanged(ds, oracle):
 
 
 def test_deterministic(ds):
-    b = synth.generate("chat1m", with_text=False)
+    b = wl.load("chat1m", with_text=False)
     a = run(ds, b.ev_group, b.ev_est, b.ev_obs, 0.1, np.ones(b.n_groups))
     c = run(ds, b.ev_group, b.ev_est, b.ev_obs, 0.1, np.ones(b.n_groups))
     assert np.array_equal(a[0], c[0]) and np.array_equal(a[1], c[1])

@@ -10,7 +10,8 @@ import random
 import numpy as np
 import pytest
 
-from paper_2606_02982_amd import synth
+import workloads as synth
+from tests import wl
 from tests.gpu_util import dev, host, pack
 
 pytestmark = pytest.mark.gpu
@@ -138,13 +139,13 @@ def test_empty_text(ds, oracle):
 
 @pytest.mark.parametrize("name", ["batch4k", "batch64k", "chat1m", "long16k"])
 def test_workloads_full_size(ds, oracle, name):
-    b = synth.generate(name)
+    b = wl.load(name)
     got = check(ds, oracle, b.text, b.offsets)
     assert np.array_equal(got, b.words)
 
 
 def test_deterministic(ds):
-    b = synth.generate("batch4k")
+    b = wl.load("batch4k")
     t, o = dev(b.text), dev(b.offsets)
     a1 = host(ds.characterize(t, o))
     a2 = host(ds.characterize(t, o))

@@ -11,7 +11,7 @@ corresponding bound on the means; counts are exact.
 import numpy as np
 import pytest
 
-from paper_2606_02982_amd import synth
+from tests import wl
 from tests.gpu_util import dev, host, rel_close
 
 pytestmark = pytest.mark.gpu
@@ -73,7 +73,7 @@ def test_random(ds, oracle, n, G):
 def test_bias_off_on(ds, oracle, name):
     # BIAS=OFF: the B-free estimate; BIAS=ON: scored with the factor each
     # event's group had before it (calibrate's trace_before)
-    b = synth.generate(name, with_text=False)
+    b = wl.load(name, with_text=False)
     alpha = b.alphas[0]
     st0 = np.ones(b.n_groups)
     w_st, w_tr, w_before = oracle.calibrate(b.ev_group, b.ev_est, b.ev_obs, alpha, st0,
@@ -110,7 +110,7 @@ def test_class_histogram(ds, oracle, n, C):
 
 
 def test_class_histogram_of_scores(ds, oracle):
-    b = synth.generate("batch64k", with_text=False)
+    b = wl.load("batch64k", with_text=False)
     _, _, _, cls = oracle.score(b.words, b.category, b.tenant, b.group, b.t_base, b.s_tenant,
                                 np.ones(b.n_groups))
     got = host(ds.class_histogram(dev(b.category), dev(cls), len(b.t_base)), np.int32)

@@ -4,7 +4,7 @@ import numpy as np
 import pytest
 import torch
 
-from paper_2606_02982_amd import synth
+from tests import wl
 from tests.gpu_util import dev, host
 
 pytestmark = pytest.mark.gpu
@@ -29,7 +29,7 @@ def separate_and_fused(ds, text, offsets, cat, ten, grp, tb, s, state, **kw):
 
 @pytest.mark.parametrize("name", ["batch4k", "batch64k"])
 def test_workload_equals_separate_calls(ds, oracle, name):
-    b = synth.generate(name)
+    b = wl.load(name)
     print("fused characterize+score %s n=%d" % (name, b.n), flush=True)
     st, _ = oracle.calibrate(b.ev_group, b.ev_est, b.ev_obs, 0.1, np.ones(b.n_groups), False)
     sep, fused = separate_and_fused(ds, b.text, b.offsets, b.category, b.tenant, b.group, b.t_base,
@@ -58,7 +58,7 @@ def test_edge_prompts_and_no_est_base(ds, oracle):
 
 
 def test_validate_rejects_bad_group(ds):
-    b = synth.generate("batch4k")
+    b = wl.load("batch4k")
     grp = np.asarray(b.group, np.uint32).copy()
     grp[7] = b.n_groups   # out of range
     args = [dev(np.asarray(b.category, np.uint8)), dev(np.asarray(b.tenant, np.uint32)), dev(grp),

@@ -9,7 +9,7 @@ import numpy as np
 import pytest
 import torch
 
-from paper_2606_02982_amd import synth
+from tests import wl
 from tests.gpu_util import dev
 
 pytestmark = pytest.mark.gpu
@@ -23,7 +23,7 @@ def ds():
 
 @pytest.mark.parametrize("schedule", ["serial", "overlap"])
 def test_step_graph_replays_equal_eager(ds, schedule):
-    b = synth.generate("batch4k")
+    b = wl.load("batch4k")
     N = b.n
     text, offsets = dev(b.text), dev(b.offsets)
     ev_group, ev_est, ev_obs = dev(b.ev_group), dev(b.ev_est), dev(b.ev_obs)

@@ -7,8 +7,9 @@ bit-identical here because both sides receive the same budget array).
 """
 import numpy as np
 import pytest
+import torch
 
-from paper_2606_02982_amd import synth
+from tests import wl
 from tests.gpu_util import dev, host
 
 pytestmark = pytest.mark.gpu
@@ -181,7 +182,7 @@ def test_aging_parameters(ds, oracle, floor, rate):
 
 @pytest.mark.parametrize("name", ["batch4k", "batch64k", "chat1m"])
 def test_workloads(ds, oracle, name):
-    b = synth.generate(name, with_text=False)
+    b = wl.load(name, with_text=False)
     st, _ = oracle.calibrate(b.ev_group, b.ev_est, b.ev_obs, 0.1, np.ones(b.n_groups), False)
     _, _, budget, _ = oracle.score(b.words, b.category, b.tenant, b.group, b.t_base, b.s_tenant, st)
     kw = dict(weights=tuple(int(x) for x in b.weights), tier_priority=tuple(b.tier_priority),
@@ -199,7 +200,7 @@ def test_workloads(ds, oracle, name):
 
 @pytest.mark.parametrize("name", ["batch4k", "batch64k", "chat1m"])
 def test_multi_equals_single(ds, oracle, name):
-    b = synth.generate(name, with_text=False)
+    b = wl.load(name, with_text=False)
     rng = np.random.default_rng(1)
     budget = np.round(rng.uniform(1, 3000, b.n), 2)
     kw = dict(weights=tuple(int(x) for x in b.weights), tier_priority=tuple(b.tier_priority),
@@ -218,14 +219,25 @@ def test_multi_equals_single(ds, oracle, name):
     assert np.array_equal(host(perms[4], np.uint32), w_perm)
 
 
-@pytest.mark.parametrize("k", [1, 17, 40, 64])
-def test_drift_aging_ticks(ds, oracle, k):
-    b = synth.generate("drift4m")
-    n = int(b.tick_n[k - 1])
-    t = float(b.tick_t[k - 1])
-    kw = dict(tier_priority=tuple(b.tier_priority), aging_rate=b.aging_rate, t_now=t,
-              aging_floor=b.aging_floor)
-    check(ds, oracle, 4, b.tier[:n], b.arrival[:n], None, **kw)
+def test_drift_aging_all_ticks(ds, oracle):
+    """Every one of the drift workload's 64 Aging re-sorts (pending prefix of
+    tick k aged to t_k), as the benchmark runs them: one FIFO order of the
+    whole set, whose first n_k entries are each tick's FIFO order."""
+    b = wl.load("drift4m")
+    tier, arr = dev(b.tier), dev(b.arrival)
+    fifo, _ = ds.order(0, tier, arr)
+    perm = torch.empty(b.n, dtype=torch.int32, device="cuda")
+    for k in range(len(b.tick_t)):
+        n = int(b.tick_n[k])
+        t = float(b.tick_t[k])
+        kw = dict(tier_priority=tuple(b.tier_priority), aging_rate=b.aging_rate, t_now=t,
+                  aging_floor=b.aging_floor)
+        print("drift tick %d: %d pending" % (k + 1, n), flush=True)
+        got, key = ds.order(4, tier[:n], arr[:n], fifo=fifo[:n], perm=perm[:n], key=True,
+                            params=ds.order_params(**kw))
+        w_perm, w_key = oracle.order(4, b.tier[:n], b.arrival[:n], None, **kw)
+        assert np.array_equal(host(got, np.uint32), w_perm), "tick %d" % (k + 1)
+        assert np.array_equal(host(key), w_key), "tick %d keys" % (k + 1)
 
 
 def test_validate_flag(ds):

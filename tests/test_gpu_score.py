@@ -3,7 +3,7 @@ and classes given the same word counts and calibration factors."""
 import numpy as np
 import pytest
 
-from paper_2606_02982_amd import synth
+from tests import wl
 from tests.gpu_util import dev, host
 
 pytestmark = pytest.mark.gpu
@@ -25,7 +25,7 @@ def run(ds, counts, cat, ten, grp, tb, s, state, **kw):
 
 @pytest.mark.parametrize("name", ["batch4k", "batch64k", "chat1m"])
 def test_workload_bitwise(ds, oracle, name):
-    b = synth.generate(name, with_text=False)
+    b = wl.load(name, with_text=False)
     st, _ = oracle.calibrate(b.ev_group, b.ev_est, b.ev_obs, 0.1, np.ones(b.n_groups), False)
     want = oracle.score(b.words, b.category, b.tenant, b.group, b.t_base, b.s_tenant, st)
     got = run(ds, b.words, b.category, b.tenant, b.group, b.t_base, b.s_tenant, st)

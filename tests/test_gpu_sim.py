@@ -9,7 +9,8 @@ order, come from them.
 import numpy as np
 import pytest
 
-from paper_2606_02982_amd import synth
+import workloads as synth
+from tests import wl
 from tests.gpu_util import dev, host
 
 pytestmark = pytest.mark.gpu
@@ -189,7 +190,7 @@ def test_repeatable(ds):
 def test_synthetic_workload(ds, oracle, policy):
     # the 65,536-request workload: 10 ms ticks of 32 against 5,000
     # arrivals/s, 2,064 ticks, every request dispatched
-    b = synth.generate("batch64k", with_text=False)
+    b = wl.load("batch64k", with_text=False)
     ticks = synth.sim_ticks(b.arrival)
     seq, _, _ = both(ds, oracle, policy, b.arrival, b.tier, b.words, b.category, b.tenant,
                      b.group, b.observed, b.t_base, b.s_tenant, np.ones(b.n_groups), ticks,

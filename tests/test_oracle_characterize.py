@@ -11,7 +11,7 @@ import random
 import numpy as np
 import pytest
 
-from paper_2606_02982_amd import synth
+from tests import wl
 
 
 def _pack(prompts):
@@ -135,7 +135,7 @@ def test_fuzz_arbitrary_bytes(oracle):
 @pytest.mark.parametrize("name,n", [("batch4k", None), ("long16k", 64)])
 def test_generator_word_counts(oracle, name, n):
     # the generator records how many words it wrote into each prompt
-    b = synth.generate(name, n=n)
+    b = wl.load(name, n=n)
     got = oracle.characterize(b.text, b.offsets)
     assert np.array_equal(got, b.words)
 

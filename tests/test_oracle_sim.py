@@ -10,7 +10,8 @@ Aging to the tick's time, and the Weighted cycle restarted at every tick.
 import numpy as np
 import pytest
 
-from paper_2606_02982_amd import synth
+import workloads as synth
+from tests import wl
 
 FIFO, PRIORITY, WEIGHTED, SJF, AGING = 0, 1, 2, 3, 4
 
@@ -201,7 +202,7 @@ def test_rejects_bad_input(oracle):
 def test_synthetic_workload_drains(oracle):
     # a reduced copy of the 65,536-request workload: 10 ms ticks of 32
     # against 5,000 arrivals/s build a queue, and the schedule drains it
-    b = synth.generate("batch64k", n=3000, with_text=False)
+    b = wl.load("batch64k", n=3000, with_text=False)
     ticks = synth.sim_ticks(b.arrival)
     for pol in (FIFO, SJF):
         seq, tick_of, st = oracle.simulate(pol, b.arrival, b.tier, b.words, b.category, b.tenant,

@@ -1,9 +1,16 @@
 """Seeded synthetic workloads for the DriftSched admission hot path.
 
-This module only makes inputs. It holds none of the four stages' arithmetic
-(no word counting, no calibration update, no budget or class, no policy key
-or ordering); both the HIP path and the CPU oracle receive the arrays it
-returns unchanged.
+A module of its own, outside the HIP package and outside the oracle: it only
+makes inputs, and both sides receive the arrays it returns unchanged. It holds
+none of the four stages' arithmetic: no word counting, no budget estimate
+(the product of the baseline, the tenant scaling and the prompt-complexity
+factor), no calibration update, no class, no policy key or ordering.
+
+The workloads define each request's observed output length as its B-free
+admission estimate times a log-normal drift ratio. That estimate is the score
+stage's output, so this module draws the ratios only; ``complete()`` turns an
+estimate computed elsewhere (by the CPU oracle in the tests, by the library's
+own score call during benchmark set-up) into the completion events.
 
 The paper's own prompt corpus (about 1,180 prompts in four semantic
 categories, three tenant tiers) is not available; these generators stand in
@@ -80,7 +87,6 @@ WORKLOADS = {
         note="1,048,576 short chat requests, 1,024 tenants, 8-256 words"),
     "long16k": Workload(
         "long16k", 16384, (8192, 32768), 16, 0.25, 0.3, nonascii_p=0.02696, seed=3,
-        policies=(),
         note="16,384 long-context prompts of 8,192-32,768 words, ~5% non-ASCII bytes"),
     "drift4m": Workload(
         "drift4m", 4194304, (8, 256), 4096, 0.0, 0.3, alphas=(0.05, 0.2), seed=4,
@@ -152,28 +158,17 @@ def make_text(words, seed, nonascii_p=0.0):
     return text, offsets
 
 
-def _synthetic_observed(t_base_cat, s_ten, words, ratio):
-    """Synthetic model of the serving engine's output length.
-
-    The workloads define the observed output of a request as its B-free
-    admission estimate times a log-normal drift ratio, rounded half to even.
-    This is input synthesis: the estimate handed to the calibration stage as
-    part of each completion event is this same value, and no expected result
-    of any stage is derived from it.
-    """
-    nominal = t_base_cat * s_ten * (1.0 + words / F_REF)
-    obs = np.rint(nominal * ratio)
-    obs = np.clip(obs, 0, 2**32 - 1).astype(np.uint32)
-    return nominal, obs
-
-
 def generate(wl, n=None, with_text=True):
     """Arrays for workload ``wl`` (a Workload or its name).
 
     ``n`` overrides the request count (for reduced test cases) keeping every
     other parameter. Arrays are in batch order: the batch lists the requests
     in a seeded random permutation of arrival order, so that FIFO is a real
-    sort. Completion events are the same requests in arrival order.
+    sort. Completion events are the same requests in arrival order:
+    ``ev_req[e]`` is the batch index of event e's request, ``ev_group[e]`` its
+    calibration group and ``ev_ratio[e]`` the drift ratio of its observed
+    length. The events' estimates and observed lengths are added by
+    ``complete()``.
     """
     if isinstance(wl, str):
         wl = WORKLOADS[wl]
@@ -232,16 +227,9 @@ def generate(wl, n=None, with_text=True):
         ratio_ev = ratio[by_arrival]
     else:
         ratio_ev = ratio_by_rank
-    ev_req = by_arrival
-    nominal, obs = _synthetic_observed(t_base[category[ev_req]], s_tenant[tenant[ev_req]],
-                                       words[ev_req].astype(np.float64), ratio_ev)
-    out["ev_group"] = tenant[ev_req].astype(np.uint32)
-    out["ev_est"] = nominal
-    out["ev_obs"] = obs
-    # the same observed lengths per request, in batch order
-    observed = np.empty(n, dtype=np.uint32)
-    observed[ev_req] = obs
-    out["observed"] = observed
+    out["ev_req"] = by_arrival
+    out["ev_group"] = tenant[by_arrival].astype(np.uint32)
+    out["ev_ratio"] = ratio_ev
 
     if wl.has_text and with_text:
         text, offsets = make_text(words, wl.seed, wl.nonascii_p)
@@ -255,6 +243,29 @@ def generate(wl, n=None, with_text=True):
         # set is a prefix
         out["tick_n"] = np.searchsorted(arrival_sorted, t, side="right").astype(np.int64)
     return out
+
+
+def complete(b, est_base):
+    """Completion events of batch ``b`` given each request's B-free admission
+    estimate ``est_base`` (float64, batch order; computed by a score call).
+
+    Adds ``ev_est`` (the estimate the event carries), ``ev_obs`` (observed
+    output tokens: the estimate times the event's drift ratio, rounded half to
+    even, clipped to uint32) and ``observed`` (the same lengths per request,
+    batch order), and returns ``b``. This is the serving engine's synthetic
+    output model, not a stage of the method.
+    """
+    est_base = np.ascontiguousarray(est_base, dtype=np.float64)
+    if est_base.shape != (b.n,):
+        raise ValueError("est_base must hold one estimate per request")
+    ev_est = est_base[b.ev_req]
+    obs = np.clip(np.rint(ev_est * b.ev_ratio), 0, 2**32 - 1).astype(np.uint32)
+    observed = np.empty(b.n, dtype=np.uint32)
+    observed[b.ev_req] = obs
+    b["ev_est"] = ev_est
+    b["ev_obs"] = obs
+    b["observed"] = observed
+    return b
 
 
 def sim_ticks(arrival, batch=32, dt=0.01, extra=16):
