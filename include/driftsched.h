@@ -67,7 +67,9 @@ typedef enum {
     DS_ERR_WORKSPACE = -4,  /* workspace NULL, misaligned or smaller than required */
     DS_ERR_DATA = -5,       /* DS_VALIDATE found device data breaking the contract */
     DS_ERR_HIP = -6,        /* the HIP runtime reported an error */
-    DS_ERR_ALIGN = -7       /* an array pointer is not aligned as required */
+    DS_ERR_ALIGN = -7,      /* an array pointer is not aligned as required */
+    DS_ERR_WAIT = -8        /* a bounded device-side wait ran out (DS_VALIDATE): the
+                               call's results are invalid */
 } ds_status;
 
 typedef enum {
@@ -94,6 +96,24 @@ typedef enum {
 #define DS_SERIAL_SORT 2u   /* ds_order, ds_order_multi: up to 2^18 requests, run the
                                single-workgroup sort that is otherwise the fallback of
                                an overflowing sample-sort bucket (diagnostic; slow) */
+#define DS_NO_WAIT 4u       /* diagnostic of the error path below: every bounded
+                               device-side wait gives up at once, as if it had run out */
+
+/*
+ * Bounded waits. The sorts behind ds_order, ds_order_multi, ds_calibrate
+ * (above 4096 groups) and ds_simulate split their work into tiles that wait,
+ * each for at most about 0.2 s, on counts published by tiles of smaller
+ * index (decoupled look-back). In normal operation no wait runs out (a tile
+ * waits only on tiles that have already started). If one does:
+ *  - in a sample-sort scatter (up to 2^18 requests), the call finishes on
+ *    the single-workgroup path instead, with exact results;
+ *  - anywhere else the results are invalid, and the call's status word is
+ *    set: the uint32 at byte DS_WS_STATUS_OFFSET of the workspace, zeroed by
+ *    the call's first kernel. With DS_VALIDATE the call waits for its work
+ *    and returns DS_ERR_WAIT; without it, the word is left for the caller
+ *    (read it after the stream has completed the call).
+ */
+#define DS_WS_STATUS_OFFSET 4
 
 #define DS_MAX_TIERS 16
 #define DS_MAX_ITEMS (1u << 30)   /* max events for ds_calibrate, requests for ds_order */

@@ -43,6 +43,32 @@ ds_status run(void *ws, uint32_t flags, hipStream_t s, F &&enqueue)
 
 void *after_flag(void *ws) { return static_cast<uint8_t *>(ws) + kFlagBytes; }
 
+// The calls whose kernels wait on each other (the look-backs of the sorts)
+// keep a status word in the workspace, at byte DS_WS_STATUS_OFFSET: the
+// call's first kernel zeroes it and a wait that runs out sets it. With
+// DS_VALIDATE the call waits for the work and returns DS_ERR_WAIT if it is
+// set; without, the word is left for the caller to read.
+WaitCfg wait_cfg(void *ws, uint32_t flags)
+{
+    WaitCfg w;
+    w.status = reinterpret_cast<uint32_t *>(static_cast<uint8_t *>(ws) + DS_WS_STATUS_OFFSET);
+    w.no_wait = (flags & DS_NO_WAIT) != 0;
+    w.clear = true;
+    return w;
+}
+
+template <typename F>
+ds_status run_waits(void *ws, uint32_t flags, hipStream_t s, F &&enqueue)
+{
+    ds_status st = run(ws, flags, s, enqueue);
+    if (st != DS_OK || !(flags & DS_VALIDATE)) return st;
+    uint32_t host = 0;
+    hipError_t e = hipMemcpyAsync(&host, wait_cfg(ws, flags).status, 4, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return DS_ERR_HIP;
+    return host ? DS_ERR_WAIT : DS_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -60,6 +86,7 @@ const char *ds_status_string(ds_status st)
     case DS_ERR_DATA: return "device data violate the call's contract";
     case DS_ERR_HIP: return "HIP runtime error";
     case DS_ERR_ALIGN: return "array pointer misaligned";
+    case DS_ERR_WAIT: return "a bounded device-side wait ran out: the results are invalid";
     }
     return "unknown status";
 }
@@ -119,9 +146,9 @@ ds_status ds_calibrate_ex(const uint32_t *group, const double *est, const uint32
     ds_status st = check_ws(ws, ws_bytes, ds_workspace_bytes(DS_OP_CALIBRATE, n_events, n_groups));
     if (st != DS_OK) return st;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    return run(ws, flags, s, [&](uint32_t *flag) {
+    return run_waits(ws, flags, s, [&](uint32_t *flag) {
         return cal_launch(group, est, observed, (uint32_t)n_events, alpha, n_groups, state, trace,
-                          trace_before, after_flag(ws), flag, s);
+                          trace_before, after_flag(ws), flag, s, wait_cfg(ws, flags));
     });
 }
 
@@ -164,13 +191,16 @@ ds_status ds_score(uint32_t n, const uint32_t *counts, const uint8_t *category,
     });
 }
 
-ds_status ds_characterize_score(const uint8_t *text, uint64_t text_bytes, const uint64_t *offsets,
-                                uint32_t n, uint32_t *counts, const uint8_t *category,
-                                const uint32_t *tenant, const uint32_t *group, const double *t_base,
-                                uint32_t n_cat, const double *s_tenant, uint32_t n_tenants,
-                                const double *state, uint32_t n_groups, const ds_score_params *params,
-                                double *est_base, double *est, double *budget, uint8_t *job_class,
-                                void *ws, size_t ws_bytes, uint32_t flags, ds_stream stream)
+// The checks and launches of ds_characterize_score on a workspace of at
+// least ds_workspace_bytes(DS_OP_CHARACTERIZE, n, 0) bytes (checked by the
+// caller).
+static ds_status char_score_checks(const uint8_t *text, uint64_t text_bytes, const uint64_t *offsets,
+                                   uint32_t n, uint32_t *counts, const uint8_t *category,
+                                   const uint32_t *tenant, const uint32_t *group, const double *t_base,
+                                   uint32_t n_cat, const double *s_tenant, uint32_t n_tenants,
+                                   const double *state, uint32_t n_groups,
+                                   const ds_score_params *params, double *est_base, double *est,
+                                   double *budget, uint8_t *job_class)
 {
     // the checks of ds_characterize and of ds_score
     if (n == 0xFFFFFFFFu) return DS_ERR_SIZE;
@@ -188,9 +218,18 @@ ds_status ds_characterize_score(const uint8_t *text, uint64_t text_bytes, const 
         !aligned(state, 8) || !aligned(est, 8) || !aligned(budget, 8) || (est_base && !aligned(est_base, 8)))
         return DS_ERR_ALIGN;
     if (text_bytes >= (1ull << 46)) return DS_ERR_SIZE;
-    ds_status st = check_ws(ws, ws_bytes, ds_workspace_bytes(DS_OP_CHARACTERIZE, n, 0));
-    if (st != DS_OK) return st;
-    hipStream_t s = static_cast<hipStream_t>(stream);
+    return DS_OK;
+}
+
+static ds_status char_score_enqueue(const uint8_t *text, uint64_t text_bytes, const uint64_t *offsets,
+                                    uint32_t n, uint32_t *counts, const uint8_t *category,
+                                    const uint32_t *tenant, const uint32_t *group, const double *t_base,
+                                    uint32_t n_cat, const double *s_tenant, uint32_t n_tenants,
+                                    const double *state, uint32_t n_groups,
+                                    const ds_score_params *params, double *est_base, double *est,
+                                    double *budget, uint8_t *job_class, void *ws, uint32_t flags,
+                                    hipStream_t s)
+{
     ScoreArgs sc = {n, counts, category, tenant, group, t_base, n_cat, s_tenant, n_tenants, state, n_groups,
                     params->f_ref, params->short_max, params->medium_max, est_base, est, budget, job_class};
     return run(ws, flags, s, [&](uint32_t *flag) {
@@ -203,6 +242,25 @@ ds_status ds_characterize_score(const uint8_t *text, uint64_t text_bytes, const 
         }
         return char_launch(text, text_bytes, offsets, n, counts, after_flag(ws), nullptr, s, &sc);
     });
+}
+
+ds_status ds_characterize_score(const uint8_t *text, uint64_t text_bytes, const uint64_t *offsets,
+                                uint32_t n, uint32_t *counts, const uint8_t *category,
+                                const uint32_t *tenant, const uint32_t *group, const double *t_base,
+                                uint32_t n_cat, const double *s_tenant, uint32_t n_tenants,
+                                const double *state, uint32_t n_groups, const ds_score_params *params,
+                                double *est_base, double *est, double *budget, uint8_t *job_class,
+                                void *ws, size_t ws_bytes, uint32_t flags, ds_stream stream)
+{
+    ds_status st = char_score_checks(text, text_bytes, offsets, n, counts, category, tenant, group, t_base,
+                                     n_cat, s_tenant, n_tenants, state, n_groups, params, est_base, est,
+                                     budget, job_class);
+    if (st != DS_OK || n == 0) return st;
+    st = check_ws(ws, ws_bytes, ds_workspace_bytes(DS_OP_CHARACTERIZE, n, 0));
+    if (st != DS_OK) return st;
+    return char_score_enqueue(text, text_bytes, offsets, n, counts, category, tenant, group, t_base, n_cat,
+                              s_tenant, n_tenants, state, n_groups, params, est_base, est, budget,
+                              job_class, ws, flags, static_cast<hipStream_t>(stream));
 }
 
 static ds_status check_order_params(const ds_order_params *params, uint32_t mask)
@@ -269,7 +327,9 @@ static ds_status order_common(uint32_t mask, uint32_t n, const uint8_t *tier,
         a.key[p] = ((mask >> p) & 1u) && keys ? keys[p] : nullptr;
     }
     hipStream_t s = static_cast<hipStream_t>(stream);
-    return run(ws, flags, s, [&](uint32_t *flag) { return order_launch(a, after_flag(ws), flag, s); });
+    return run_waits(ws, flags, s, [&](uint32_t *flag) {
+        return order_launch(a, after_flag(ws), flag, s, wait_cfg(ws, flags));
+    });
 }
 
 ds_status ds_order(ds_policy policy, uint32_t n, const uint8_t *tier, const double *arrival,
@@ -404,7 +464,9 @@ ds_status ds_simulate(uint32_t n, const double *arrival, const uint8_t *tier,
     a.tick_of = tick_of;
     a.n_dispatched = n_dispatched;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    return run(ws, flags, s, [&](uint32_t *flag) { return sim_launch(a, after_flag(ws), flag, s); });
+    return run_waits(ws, flags, s, [&](uint32_t *flag) {
+        return sim_launch(a, after_flag(ws), flag, s, wait_cfg(ws, flags));
+    });
 }
 
 ds_status ds_read_bandwidth(const void *buf, uint64_t bytes, uint32_t *xor_out, ds_stream stream)

@@ -56,6 +56,7 @@ struct CalArgs {
     uint32_t small;          // C x G <= kSmallTable
     double *state;           // [G] in: before all events, out: after
     double *trace, *trace_before;
+    uint32_t *wait_status;   // or NULL: zeroed by k_calc_agg (this path has no waits)
 };
 
 // A composed affine map: x -> a x + b, f = a segment starts inside,
@@ -290,6 +291,7 @@ __global__ __launch_bounds__(kT) void k_calc_agg(CalArgs a)
     __shared__ SubShared<kE> sh;
     __shared__ double sA[kG], sB[kG];   // the chunk's map per group so far (A < 0: none)
     const uint32_t t = threadIdx.x, c = blockIdx.x;
+    if (a.wait_status && c == 0 && t == 0) *a.wait_status = 0;
     for (uint32_t g = t; g < a.G; g += kT) {
         sA[g] = -1.0;
         sB[g] = 0.0;
@@ -558,7 +560,7 @@ size_t calc_ws_bytes(uint64_t n, uint32_t G)
 
 hipError_t calc_launch(const uint32_t *group, const double *est, const uint32_t *obs, uint32_t n,
                        double alpha, uint32_t G, double *state, double *trace, double *trace_before,
-                       void *ws, hipStream_t s)
+                       void *ws, hipStream_t s, uint32_t *wait_status)
 {
     if (n == 0) return hipSuccess;
     if (G == 0 || G > kG) return hipErrorInvalidValue;
@@ -585,6 +587,7 @@ hipError_t calc_launch(const uint32_t *group, const double *est, const uint32_t 
     a.state = state;
     a.trace = trace;
     a.trace_before = trace_before;
+    a.wait_status = wait_status;
     if (a.small) {
         hipLaunchKernelGGL(k_calc_agg<1>, dim3(a.C), dim3(kT), 0, s, a);
         hipLaunchKernelGGL(k_calc_apply<1>, dim3(a.C), dim3(kT), 0, s, a);

@@ -271,7 +271,7 @@ size_t cal_ws_bytes(uint64_t n, uint32_t n_groups)
 
 hipError_t cal_launch(const uint32_t *group, const double *est, const uint32_t *obs, uint32_t n,
                       double alpha, uint32_t G, double *state, double *trace, double *trace_before,
-                      void *ws, uint32_t *flag, hipStream_t s)
+                      void *ws, uint32_t *flag, hipStream_t s, WaitCfg wait)
 {
     if (flag) {
         uint32_t vb = (uint32_t)(cdiv(n, 256) < 1024 ? cdiv(n, 256) : 1024);
@@ -279,7 +279,9 @@ hipError_t cal_launch(const uint32_t *group, const double *est, const uint32_t *
         return hipGetLastError();
     }
     if (n == 0) return hipSuccess;
-    if (G <= kCalGroupsLds) return calc_launch(group, est, obs, n, alpha, G, state, trace, trace_before, ws, s);
+    if (G <= kCalGroupsLds)
+        return calc_launch(group, est, obs, n, alpha, G, state, trace, trace_before, ws, s,
+                           wait.clear ? wait.status : nullptr);
     const uint32_t T = (uint32_t)cdiv(n, kTile);
     const uint32_t kb = bits_for(G);
     uint8_t *p = static_cast<uint8_t *>(ws);
@@ -296,6 +298,7 @@ hipError_t cal_launch(const uint32_t *group, const double *est, const uint32_t *
     SortInput in = {};
     in.n = n;
     in.group = group;
+    in.wait = wait;
     SortJob job = {SortKind::Group, kb, nullptr, sidx};
     hipError_t err = sort_launch(in, &job, 1, sort_ws, s);
     if (err != hipSuccess) return err;

@@ -50,6 +50,18 @@ constexpr uint32_t kWrrMaxWeightSum = 1024;   // smooth round robin: largest sum
 // How Weighted interleaves the tiers inside a cycle (the ABI's weighted_mode).
 enum : uint32_t { kWrrBlocked = 0, kWrrSmooth = 1, kWrrStride = 2 };
 
+// Bounded device-side waits (the look-backs of the sorts). A wait that runs
+// out sets *status (a word of the caller's workspace) non-zero, or, in a
+// sample-sort scatter, sends the sort to its single-workgroup path. `clear`:
+// this launch is the call's first to touch *status and zeroes it first.
+// no_wait: every wait gives up at once (a diagnostic of the error path).
+// A zero-initialised WaitCfg means: bounded waits, errors kept internal.
+struct WaitCfg {
+    uint32_t *status;
+    bool no_wait;
+    bool clear;
+};
+
 // Inputs and parameters shared by the sorts of a batch.
 struct SortInput {
     uint32_t n;
@@ -64,6 +76,7 @@ struct SortInput {
     uint32_t weight[16];       // Tier: weighted round robin
     uint32_t wrr_mode;         // Tier: kWrrBlocked, kWrrSmooth (weights sum <= kWrrMaxWeightSum), kWrrStride
     double aging_rate, t_now, aging_floor;
+    WaitCfg wait;
 };
 
 struct SortJob {
@@ -99,14 +112,16 @@ hipError_t ssort_launch(const SortInput &in, const SortJob *jobs, uint32_t nsort
 // Up to kCalGroupsLds groups: chunked scan without a global partition.
 constexpr uint32_t kCalGroupsLds = 4096;
 size_t calc_ws_bytes(uint64_t n, uint32_t n_groups);
+// wait_status (may be NULL): zeroed by the first kernel (no waits here).
 hipError_t calc_launch(const uint32_t *group, const double *est, const uint32_t *obs, uint32_t n,
                        double alpha, uint32_t n_groups, double *state, double *trace,
-                       double *trace_before, void *ws, hipStream_t s);
+                       double *trace_before, void *ws, hipStream_t s,
+                       uint32_t *wait_status = nullptr);
 size_t cal_ws_bytes(uint64_t n, uint32_t n_groups);
 hipError_t cal_launch(const uint32_t *group, const double *est, const uint32_t *obs,
                       uint32_t n, double alpha, uint32_t n_groups, double *state,
                       double *trace, double *trace_before, void *ws, uint32_t *flag,
-                      hipStream_t s);
+                      hipStream_t s, WaitCfg wait = {});
 
 // ---- stage 3: score --------------------------------------------------------------
 hipError_t score_launch(uint32_t n, const uint32_t *counts, const uint8_t *category,
@@ -134,7 +149,8 @@ struct OrderArgs {
     double *key[5];
     bool serial_sort;          // sample-sort path: sort in one workgroup
 };
-hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_t s);
+hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_t s,
+                        WaitCfg wait = {});
 
 // ---- estimation error and class histogram ------------------------------------------
 size_t err_ws_bytes(uint64_t n, uint32_t n_groups);
@@ -168,7 +184,8 @@ struct SimArgs {
 };
 constexpr uint32_t kSimMaxBatch = 1024;
 size_t sim_ws_bytes(uint64_t n);
-hipError_t sim_launch(const SimArgs &a, void *ws, uint32_t *flag, hipStream_t s);
+hipError_t sim_launch(const SimArgs &a, void *ws, uint32_t *flag, hipStream_t s,
+                      WaitCfg wait = {});
 
 // ---- misc --------------------------------------------------------------------------
 hipError_t fill_u32(uint32_t *p, uint32_t v, uint64_t n, hipStream_t s);

@@ -12,18 +12,26 @@ namespace ds {
 constexpr uint32_t kAgg = 1u << 30;          // the word holds this tile's count only
 constexpr uint32_t kPre = 2u << 30;          // the word holds the inclusive prefix
 constexpr uint32_t kValMask = (1u << 30) - 1u;
-constexpr uint32_t kSpinLimit = 1u << 22;    // bounded waits (never reached in normal runs)
+constexpr uint32_t kSpinLimit = 1u << 22;    // bounded waits (never reached in normal runs:
+                                             // about 0.2 s of sleeps)
 
 // Sum of digit t's counts over the tiles before `tile` (tile j's words at
 // st[j * kStride + digit]). Tiles publish their own count as soon as they
 // have ranked their keys, so by the time a tile looks back its predecessors'
 // counts are normally all there: windows of 16 predecessors are loaded at
 // once and summed back to the first inclusive prefix. The wait for an
-// unpublished tile is bounded and reported through err.
+// unpublished tile is bounded (spin_limit sleeps without progress) and
+// reported through err; spin_limit 0 gives up before the first load, so that
+// the error path can be exercised with every kernel still exiting normally.
 template <uint32_t kStride = 256>
-__device__ inline uint32_t look_back(const uint32_t *st, uint32_t tile, uint32_t t, uint32_t *err)
+__device__ inline uint32_t look_back(const uint32_t *st, uint32_t tile, uint32_t t, uint32_t *err,
+                                     uint32_t spin_limit = kSpinLimit)
 {
     constexpr int kWin = 16;
+    if (spin_limit == 0) {
+        if (tile > 0) atomicOr(err, 1u);
+        return 0;
+    }
     uint32_t prefix = 0;
     int64_t j = (int64_t)tile - 1;   // nearest predecessor not yet summed
     uint32_t spins = 0;
@@ -50,7 +58,7 @@ __device__ inline uint32_t look_back(const uint32_t *st, uint32_t tile, uint32_t
         j -= used;
         if (used == 0) {
             __builtin_amdgcn_s_sleep(1);
-            if (++spins > kSpinLimit) {
+            if (++spins > spin_limit) {
                 atomicOr(err, 1u);
                 break;
             }

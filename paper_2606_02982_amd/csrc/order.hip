@@ -24,8 +24,10 @@ namespace ds {
 namespace {
 
 __global__ void k_copy_fifo(const uint32_t *__restrict__ fifo, const double *__restrict__ arrival,
-                            uint32_t n, uint32_t *__restrict__ perm, double *__restrict__ key)
+                            uint32_t n, uint32_t *__restrict__ perm, double *__restrict__ key,
+                            uint32_t *__restrict__ wait_status)
 {
+    if (wait_status && blockIdx.x == 0 && threadIdx.x == 0) *wait_status = 0;
     for (uint32_t j = blockIdx.x * blockDim.x + threadIdx.x; j < n; j += gridDim.x * blockDim.x) {
         perm[j] = fifo[j];
         if (key) key[j] = arrival[j];
@@ -75,7 +77,7 @@ size_t order_ws_bytes(uint64_t n, uint32_t npolicies)
     return n <= kSsMaxN ? sample : (radix > sample ? radix : sample);
 }
 
-hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_t s)
+hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_t s, WaitCfg wait)
 {
     const uint32_t n = a.n;
     if (flag) {
@@ -100,6 +102,7 @@ hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_
     in.aging_rate = a.aging_rate;
     in.t_now = a.t_now;
     in.aging_floor = a.aging_floor;
+    in.wait = wait;
     if (a.mask & (1u << 1)) {
         // priority classes: rank of each tier's priority among the distinct values
         double vals[16];
@@ -118,7 +121,8 @@ hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_
         uint64_t nb = cdiv(n, 256);
         uint32_t blocks = (uint32_t)(nb < 4096 ? nb : 4096);
         hipLaunchKernelGGL(k_copy_fifo, dim3(blocks), dim3(256), 0, s, a.fifo_in, a.arrival, n, a.perm[0],
-                           a.key[0]);
+                           a.key[0], wait.clear ? wait.status : nullptr);
+        in.wait.clear = false;
     }
     if (n <= kSsMaxN) {
         // one batch of sample sorts: FIFO (carrying Priority and Weighted),
@@ -160,6 +164,7 @@ hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_
         hipError_t err = sort_launch(in, &job, 1, sort_ws, s);
         if (err != hipSuccess) return err;
         fifo = job.out;
+        in.wait.clear = false;
     }
     in.fifo = fifo;
     if (nj == 0) return hipGetLastError();

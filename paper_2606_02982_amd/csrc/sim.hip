@@ -63,6 +63,7 @@ struct SetupArgs {
     uint8_t *val;
     uint32_t *seq;
     int32_t *tick_of;
+    uint32_t *wait_status;   // or NULL: zeroed here, before the FIFO sort's waits
 };
 
 struct EngineArgs {
@@ -87,6 +88,7 @@ struct EngineArgs {
 
 __global__ void k_sim_setup(SetupArgs a)
 {
+    if (a.wait_status && blockIdx.x == 0 && threadIdx.x == 0) *a.wait_status = 0;
     const double nan = __builtin_nan("");
     for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < a.n; i += gridDim.x * blockDim.x) {
         const uint32_t cat = a.category[i], ten = a.tenant[i];
@@ -550,7 +552,7 @@ size_t sim_ws_bytes(uint64_t n)
            align_up(n, 256) + sort_ws_bytes(n, 1);
 }
 
-hipError_t sim_launch(const SimArgs &a, void *ws, uint32_t *flag, hipStream_t s)
+hipError_t sim_launch(const SimArgs &a, void *ws, uint32_t *flag, hipStream_t s, WaitCfg wait)
 {
     const uint32_t n = a.n;
     if (flag) {
@@ -608,11 +610,14 @@ hipError_t sim_launch(const SimArgs &a, void *ws, uint32_t *flag, hipStream_t s)
     su.val = val;
     su.seq = a.seq;
     su.tick_of = a.tick_of;
+    su.wait_status = wait.clear ? wait.status : nullptr;
     hipLaunchKernelGGL(k_sim_setup, dim3(grid_for(n)), dim3(256), 0, s, su);
 
     SortInput in = {};
     in.n = n;
     in.arrival = a.arrival;
+    in.wait = wait;
+    in.wait.clear = false;
     SortJob job = {SortKind::Fifo, 64, nullptr, fifo};
     hipError_t e = sort_launch(in, &job, 1, sort_ws, s);
     if (e != hipSuccess) return e;

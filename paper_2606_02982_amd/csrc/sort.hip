@@ -23,9 +23,12 @@
 //                through LDS, coalesced runs of global writes. The buffer a
 //                pass reads, and whether it is the last active pass, follow
 //                from the active flags.
-// Tile t of a pass is block t. Blocks of a dispatch start in index order on
-// each XCD, so a tile only waits on tiles that have started or will start
-// without waiting on it.
+// Tile t of a pass is block t, and it waits only on tiles with a smaller
+// index. Blocks of a dispatch are handed out in index order on each XCD, so
+// the unfinished tile of smallest index has been started (every earlier
+// block of its XCD has finished and freed its slot) and waits on nobody: the
+// passes always make progress. The wait is bounded all the same; a wait that
+// runs out is reported in the caller's status word (WaitCfg).
 #include "common.h"
 #include "kernels.h"
 #include "keys.h"
@@ -92,6 +95,7 @@ __global__ __launch_bounds__(TPB) void k_sort_init(SortBatch b, uint64_t status_
         uint64_t t = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
         uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
         if (t == 0) d.ctl->error = 0;
+        if (t == 0 && blockIdx.y == 0 && b.in.wait.clear && b.in.wait.status) *b.in.wait.status = 0;
         uint64_t words = (uint64_t)P * status_words;
         for (uint64_t i = t; i < words; i += stride) d.status[i] = 0;
     }
@@ -327,7 +331,8 @@ __global__ __launch_bounds__(TPB) void k_sort_pass(SortBatch b, uint32_t p)
         texcl[t] = tex;
         uint32_t prefix = 0;
         if (tile > 0) {
-            prefix = look_back(st, tile, t, &ctl->error);
+            prefix = look_back(st, tile, t, b.in.wait.status ? b.in.wait.status : &ctl->error,
+                               b.in.wait.no_wait ? 0u : kSpinLimit);
             st_relaxed(&st[(uint64_t)tile * 256u + t], kPre | (prefix + tc));
         }
         gbase[t] = dexcl + prefix;

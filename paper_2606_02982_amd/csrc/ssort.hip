@@ -218,6 +218,7 @@ __device__ __forceinline__ void sample_body(const SsBatch &b, const SsDesc &d, S
     if (blockIdx.x == 0 && t == 0) {
         d.ctl->overflow = b.serial;
         d.ctl->lb_err = 0;
+        if (blockIdx.y == 0 && b.in.wait.clear && b.in.wait.status) *b.in.wait.status = 0;
         d.ctl->tiles_done = 0;
     }
     if (blockIdx.x == 0 && t < kQ && (d.pw_out[0] || d.pw_out[1])) d.tot[t] = 0;
@@ -429,7 +430,8 @@ __global__ __launch_bounds__(kScTPB) void k_ss_scatter(SsBatch b)
         texcl[t] = tex;
         uint32_t prefix = 0;
         if (tile > 0) {
-            prefix = look_back(st, tile, t, &d.ctl->overflow);
+            // a wait that runs out sends the sort to the single-workgroup path
+            prefix = look_back(st, tile, t, &d.ctl->overflow, b.in.wait.no_wait ? 0u : kSpinLimit);
             st_relaxed(&st[(uint64_t)tile * 256u + t], kPre | (prefix + tc));
         }
         gbase[t] = prefix;
@@ -1375,7 +1377,9 @@ __global__ __launch_bounds__(kBkTPB) void k_ss_bucket(SsBatch b)
         if (t < 2 * kQ) {
             uint32_t pre = 0;
             if (bkt > 0) {
-                pre = look_back<2 * kQ>(d.bstat, bkt, t, &d.ctl->lb_err);
+                pre = look_back<2 * kQ>(d.bstat, bkt, t,
+                                        b.in.wait.status ? b.in.wait.status : &d.ctl->lb_err,
+                                        b.in.wait.no_wait ? 0u : kSpinLimit);
                 st_relaxed(&d.bstat[(uint64_t)bkt * 2 * kQ + t], kPre | (pre + sh.pt.cnt[t]));
             }
             sh.pt.pre[t] = pre;

@@ -23,6 +23,9 @@ OP_CHARACTERIZE, OP_CALIBRATE, OP_SCORE, OP_ORDER, OP_ORDER_MULTI = 0, 1, 2, 3, 
 OP_ERROR_STATS, OP_CLASS_HIST, OP_SIMULATE = 5, 6, 7
 DS_VALIDATE = 1
 DS_SERIAL_SORT = 2
+DS_NO_WAIT = 4          # diagnostic: bounded device-side waits give up at once
+ERR_WAIT = -8           # DS_ERR_WAIT
+WS_STATUS_OFFSET = 4    # byte offset of the bounded-wait status word in a workspace
 MAX_TIERS = 16
 WRR_BLOCKED, WRR_SMOOTH, WRR_STRIDE = 0, 1, 2   # ds_order_params.weighted_mode
 WRR_MAX_WEIGHT_SUM = 1024
@@ -74,7 +77,7 @@ def _load():
                                    ctypes.POINTER(P), ctypes.POINTER(P), P, sz, u32, P]
     lib.ds_simulate.argtypes = [u32, P, P, P, P, P, P, P, P, u32, P, u32, u32, P, u32,
                                 ctypes.POINTER(SimParams), P, P, P, P, P, sz, u32, P]
-    for f in (lib.ds_characterize, lib.ds_calibrate, lib.ds_calibrate_ex, lib.ds_score, lib.ds_order,
+    for f in (lib.ds_characterize, lib.ds_characterize_score, lib.ds_calibrate, lib.ds_calibrate_ex, lib.ds_score, lib.ds_order,
               lib.ds_order_multi, lib.ds_error_stats, lib.ds_class_histogram, lib.ds_simulate):
         f.restype = i32
     lib.ds_workspace_bytes.argtypes = [i32, u64, u32]
@@ -124,8 +127,14 @@ def _stream():
     return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
 
 
-def _flags(validate):
-    return DS_VALIDATE if validate else 0
+def _flags(validate, no_wait=False):
+    return (DS_VALIDATE if validate else 0) | (DS_NO_WAIT if no_wait else 0)
+
+
+def wait_status(ws):
+    """The bounded-wait status word of a workspace after a call (0: no wait
+    ran out). Synchronizes with the current stream."""
+    return int(ws[WS_STATUS_OFFSET:WS_STATUS_OFFSET + 4].cpu().numpy().view("<u4")[0])
 
 
 def _dev(t, dtype, name):
@@ -154,7 +163,7 @@ def characterize(text, offsets, counts=None, ws=None, validate=False):
 
 
 def calibrate(group, est, observed, alpha, state, trace=True, ws=None, validate=False,
-              trace_before=None):
+              trace_before=None, no_wait=False):
     """EMA calibration factors (Eq. 5/6). Updates ``state`` in place.
 
     Returns (state, trace or None), and the factors before each event as a
@@ -178,7 +187,7 @@ def calibrate(group, est, observed, alpha, state, trace=True, ws=None, validate=
         ws = workspace(OP_CALIBRATE, n, state.numel(), group.device)
     _check(lib.ds_calibrate_ex(_ptr(group), _ptr(est), _ptr(observed), n, float(alpha),
                                state.numel(), _ptr(state), _ptr(tr), _ptr(tb), _ptr(ws), ws.numel(),
-                               _flags(validate), _stream()))
+                               _flags(validate, no_wait), _stream()))
     if trace_before is None or trace_before is False:
         return state, tr
     return state, tr, tb
@@ -323,7 +332,7 @@ def order_params(n_tiers=3, weights=(4, 2, 1), tier_priority=(0.0, 1.0, 2.0), ag
 
 
 def order(policy, tier, arrival, budget=None, fifo=None, params=None, perm=None, key=False,
-          ws=None, validate=False, serial_sort=False, **kw):
+          ws=None, validate=False, serial_sort=False, no_wait=False, **kw):
     """Dispatch permutation of one policy. Returns (perm, key or None).
 
     ``serial_sort`` sets DS_SERIAL_SORT (the single-workgroup sort; a
@@ -349,7 +358,7 @@ def order(policy, tier, arrival, budget=None, fifo=None, params=None, perm=None,
         k = _dev(key, torch.float64, "key")
     if ws is None:
         ws = workspace(OP_ORDER, n, 0, dev)
-    flags = _flags(validate) | (DS_SERIAL_SORT if serial_sort else 0)
+    flags = _flags(validate, no_wait) | (DS_SERIAL_SORT if serial_sort else 0)
     _check(lib.ds_order(int(policy), n, _ptr(tier), _ptr(arrival), _ptr(budget), _ptr(fifo),
                         ctypes.byref(params), _ptr(perm), _ptr(k), _ptr(ws), ws.numel(),
                         flags, _stream()))
@@ -357,7 +366,7 @@ def order(policy, tier, arrival, budget=None, fifo=None, params=None, perm=None,
 
 
 def order_multi(policies, tier, arrival, budget=None, fifo=None, params=None, perms=None,
-                keys=False, ws=None, validate=False, serial_sort=False, **kw):
+                keys=False, ws=None, validate=False, serial_sort=False, no_wait=False, **kw):
     """Dispatch permutations of several policies in one call (FIFO computed
     once, the policy sorts batched). Returns ({policy: perm}, {policy: key})."""
     pols = [POLICIES[p] if isinstance(p, str) else int(p) for p in policies]
@@ -388,7 +397,7 @@ def order_multi(policies, tier, arrival, budget=None, fifo=None, params=None, pe
             kk[p] = k.data_ptr()
     if ws is None:
         ws = workspace(OP_ORDER_MULTI, n, 0, dev)
-    flags = _flags(validate) | (DS_SERIAL_SORT if serial_sort else 0)
+    flags = _flags(validate, no_wait) | (DS_SERIAL_SORT if serial_sort else 0)
     _check(lib.ds_order_multi(mask, n, _ptr(tier), _ptr(arrival), _ptr(budget), _ptr(fifo),
                               ctypes.byref(params), pp, kk if keys else None, _ptr(ws), ws.numel(),
                               flags, _stream()))

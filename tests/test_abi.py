@@ -34,7 +34,7 @@ def test_exports_every_declared_symbol(ds):
 
 
 def test_status_strings(ds):
-    for code in range(-7, 1):
+    for code in range(-8, 1):
         s = ds.status_string(code)
         assert s and s != "unknown status"
     assert ds.status_string(-99) == "unknown status"

@@ -1,0 +1,98 @@
+"""Bounded device-side waits: a wait that runs out is reported, never silent.
+
+The flag DS_NO_WAIT makes every look-back wait give up at once, as if its
+spin limit had been reached, while every kernel still runs to its end (no
+wait at all takes place). The tests check what the header promises:
+  - a give-up in the radix passes, in the sample sort's bucket placement of
+    Priority/Weighted, or in the calibration partition sets the workspace's
+    status word, and DS_VALIDATE turns it into DS_ERR_WAIT;
+  - a give-up in a sample-sort scatter sends the sort to its single-workgroup
+    path, whose results are exact;
+  - the next call on the same workspace clears the word again.
+"""
+import numpy as np
+import pytest
+import torch
+
+from tests.gpu_util import dev, host
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def ds():
+    from paper_2606_02982_amd import driftsched
+    return driftsched
+
+
+def batch(n, seed):
+    rng = np.random.default_rng(seed)
+    tier = rng.integers(0, 3, n).astype(np.uint8)
+    arr = np.round(rng.uniform(0.0, 100.0, n), 3)
+    bud = np.round(rng.uniform(1.0, 3000.0, n), 1)
+    return tier, arr, bud
+
+
+def test_radix_pass_give_up_is_reported(ds, oracle):
+    n = 300000                       # above the sample-sort limit: radix passes
+    tier, arr, bud = batch(n, 1)
+    print("waits: radix FIFO n=%d" % n, flush=True)
+    ws = ds.workspace(ds.OP_ORDER, n)
+    with pytest.raises(ds.DriftSchedError) as e:
+        ds.order(0, dev(tier), dev(arr), ws=ws, validate=True, no_wait=True)
+    assert e.value.status == ds.ERR_WAIT
+    # without DS_VALIDATE the call returns DS_OK and leaves the word set
+    ds.order(0, dev(tier), dev(arr), ws=ws, no_wait=True)
+    assert ds.wait_status(ws) != 0
+    # an ordinary call clears it and is exact
+    perm, _ = ds.order(0, dev(tier), dev(arr), ws=ws, validate=True)
+    assert ds.wait_status(ws) == 0
+    w_perm, _ = oracle.order(0, tier, arr)
+    assert np.array_equal(host(perm, np.uint32), w_perm)
+
+
+def test_scatter_give_up_takes_the_exact_fallback(ds, oracle):
+    n = 50000                        # sample sorts, 25 scatter tiles
+    tier, arr, bud = batch(n, 2)
+    print("waits: sample-sort scatter n=%d" % n, flush=True)
+    ws = ds.workspace(ds.OP_ORDER_MULTI, n)
+    perms, _ = ds.order_multi((0, 1, 2, 3, 4), dev(tier), dev(arr), dev(bud), ws=ws,
+                              validate=True, no_wait=True, t_now=100.0)
+    assert ds.wait_status(ws) == 0
+    for p in range(5):
+        w_perm, _ = oracle.order(p, tier, arr, bud, t_now=100.0)
+        assert np.array_equal(host(perms[p], np.uint32), w_perm), "policy %d" % p
+
+
+def test_bucket_placement_give_up_is_reported(ds):
+    n = 2000                         # one scatter tile, several FIFO buckets
+    tier, arr, _ = batch(n, 3)
+    print("waits: bucket placement n=%d" % n, flush=True)
+    with pytest.raises(ds.DriftSchedError) as e:
+        ds.order(1, dev(tier), dev(arr), validate=True, no_wait=True)
+    assert e.value.status == ds.ERR_WAIT
+
+
+def test_calibration_partition_give_up_is_reported(ds, oracle):
+    n, G = 40000, 5000               # above 4096 groups: partition by a radix sort
+    rng = np.random.default_rng(4)
+    grp = rng.integers(0, G, n).astype(np.uint32)
+    est = rng.uniform(10.0, 500.0, n)
+    obs = rng.integers(1, 800, n).astype(np.uint32)
+    print("waits: calibration partition n=%d G=%d" % (n, G), flush=True)
+    ws = ds.workspace(ds.OP_CALIBRATE, n, G)
+    st = torch.ones(G, dtype=torch.float64, device="cuda")
+    with pytest.raises(ds.DriftSchedError) as e:
+        ds.calibrate(dev(grp), dev(est), dev(obs), 0.1, st, ws=ws, validate=True, no_wait=True)
+    assert e.value.status == ds.ERR_WAIT
+    st = torch.ones(G, dtype=torch.float64, device="cuda")
+    ds.calibrate(dev(grp), dev(est), dev(obs), 0.1, st, trace=False, ws=ws, validate=True)
+    assert ds.wait_status(ws) == 0
+    want, _ = oracle.calibrate(grp, est, obs, 0.1, np.ones(G), False)
+    got = host(st)
+    assert np.all(np.abs(got - want) <= 1e-12 * np.abs(want))
+    # the chunked path (no waits) clears a stale word too
+    ws[ds.WS_STATUS_OFFSET] = 1
+    st = torch.ones(64, dtype=torch.float64, device="cuda")
+    ds.calibrate(dev(grp % 64), dev(est), dev(obs), 0.1, st, trace=False, ws=ws, no_wait=True)
+    assert ds.wait_status(ws) == 0
