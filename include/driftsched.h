@@ -189,6 +189,35 @@ ds_status ds_characterize_score(const uint8_t *text, uint64_t text_bytes,
                                 uint32_t flags, ds_stream stream);
 
 /*
+ * ds_characterize_score for callers that cannot allocate device memory: code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation. It takes no workspace: its scratch memory is a static device
+ * array of the library, DS_NOALLOC_SCRATCH_BYTES on each GPU it runs on, held
+ * from the library's load until the process ends. The call itself allocates
+ * and frees nothing (its first call on a GPU looks up that GPU's copy of the
+ * array, once).
+ *
+ *  n          <= DS_NOALLOC_MAX_PROMPTS (else DS_ERR_SIZE)
+ *  flags      0 (else DS_ERR_ARG: DS_VALIDATE waits and copies to the host)
+ * Other arguments, results and errors as ds_characterize_score.
+ * Every call on one GPU uses that GPU's one array and leaves its contents
+ * behind (nothing in it needs clearing between calls): calls that overlap on
+ * one GPU (on two streams, or from host threads without ordering) race and
+ * give undefined results.
+ */
+#define DS_NOALLOC_MAX_PROMPTS (1u << 20)
+#define DS_NOALLOC_SCRATCH_BYTES 4456960u
+ds_status ds_characterize_score_noalloc(const uint8_t *text, uint64_t text_bytes,
+                                        const uint64_t *offsets, uint32_t n, uint32_t *counts,
+                                        const uint8_t *category, const uint32_t *tenant,
+                                        const uint32_t *group, const double *t_base, uint32_t n_cat,
+                                        const double *s_tenant, uint32_t n_tenants,
+                                        const double *state, uint32_t n_groups,
+                                        const ds_score_params *params, double *est_base, double *est,
+                                        double *budget, uint8_t *job_class, uint32_t flags,
+                                        ds_stream stream);
+
+/*
  * Stage 2: calibration factors, Eq. (5) with the ratio of Eq. (6)
  * (Sec. "Runtime Calibration and Feedback Adaptation").
  *

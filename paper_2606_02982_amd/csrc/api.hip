@@ -3,6 +3,8 @@
 #include <math.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "../../include/driftsched.h"
 #include "common.h"
 #include "kernels.h"
@@ -261,6 +263,71 @@ ds_status ds_characterize_score(const uint8_t *text, uint64_t text_bytes, const 
     return char_score_enqueue(text, text_bytes, offsets, n, counts, category, tenant, group, t_base, n_cat,
                               s_tenant, n_tenants, state, n_groups, params, est_base, est, budget,
                               job_class, ws, flags, static_cast<hipStream_t>(stream));
+}
+
+}  // extern "C"
+
+// ---- ds_characterize_score without a caller workspace ------------------------------
+// Its scratch memory is this static device array: one copy per GPU, held until
+// the process ends. On the host, `scratch` names a host-side stand-in, so the
+// device address of each GPU's copy is looked up once per device and kept.
+namespace {
+constexpr size_t kNoAllocScratch = DS_NOALLOC_SCRATCH_BYTES;
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_dev[kMaxDevices];
+}  // namespace
+
+static __device__ __align__(256) uint8_t scratch[kNoAllocScratch];
+
+// The device address of `scratch` on the device that stream s runs on (the
+// current device for the null stream).
+static ds_status scratch_for(hipStream_t s, void **out)
+{
+    int dev = 0;
+    hipError_t e = s ? hipStreamGetDevice(s, &dev) : hipGetDevice(&dev);
+    if (e != hipSuccess || dev < 0 || dev >= kMaxDevices) return DS_ERR_HIP;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_dev[dev]) {
+        int cur = 0;
+        if (hipGetDevice(&cur) != hipSuccess) return DS_ERR_HIP;
+        if (cur != dev && hipSetDevice(dev) != hipSuccess) return DS_ERR_HIP;
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (cur != dev) hipSetDevice(cur);
+        if (e != hipSuccess || !p) return DS_ERR_HIP;
+        g_scratch_dev[dev] = p;
+    }
+    *out = g_scratch_dev[dev];
+    return DS_OK;
+}
+
+extern "C" {
+
+ds_status ds_characterize_score_noalloc(const uint8_t *text, uint64_t text_bytes,
+                                        const uint64_t *offsets, uint32_t n, uint32_t *counts,
+                                        const uint8_t *category, const uint32_t *tenant,
+                                        const uint32_t *group, const double *t_base, uint32_t n_cat,
+                                        const double *s_tenant, uint32_t n_tenants,
+                                        const double *state, uint32_t n_groups,
+                                        const ds_score_params *params, double *est_base, double *est,
+                                        double *budget, uint8_t *job_class, uint32_t flags,
+                                        ds_stream stream)
+{
+    if (n > DS_NOALLOC_MAX_PROMPTS) return DS_ERR_SIZE;
+    if (flags != 0) return DS_ERR_ARG;
+    ds_status st = char_score_checks(text, text_bytes, offsets, n, counts, category, tenant, group, t_base,
+                                     n_cat, s_tenant, n_tenants, state, n_groups, params, est_base, est,
+                                     budget, job_class);
+    if (st != DS_OK || n == 0) return st;
+    if (ds_workspace_bytes(DS_OP_CHARACTERIZE, n, 0) > kNoAllocScratch) return DS_ERR_SIZE;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    void *ws = nullptr;
+    st = scratch_for(s, &ws);
+    if (st != DS_OK) return st;
+    return char_score_enqueue(text, text_bytes, offsets, n, counts, category, tenant, group, t_base, n_cat,
+                              s_tenant, n_tenants, state, n_groups, params, est_base, est, budget,
+                              job_class, ws, 0u, s);
 }
 
 static ds_status check_order_params(const ds_order_params *params, uint32_t mask)

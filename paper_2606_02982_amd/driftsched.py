@@ -72,12 +72,15 @@ def _load():
                              P, P, P, P, P, sz, u32, P]
     lib.ds_characterize_score.argtypes = [P, u64, P, u32, P, P, P, P, P, u32, P, u32, P, u32,
                                           ctypes.POINTER(ScoreParams), P, P, P, P, P, sz, u32, P]
+    lib.ds_characterize_score_noalloc.argtypes = [P, u64, P, u32, P, P, P, P, P, u32, P, u32, P, u32,
+                                                  ctypes.POINTER(ScoreParams), P, P, P, P, u32, P]
     lib.ds_order.argtypes = [i32, u32, P, P, P, P, ctypes.POINTER(OrderParams), P, P, P, sz, u32, P]
     lib.ds_order_multi.argtypes = [u32, u32, P, P, P, P, ctypes.POINTER(OrderParams),
                                    ctypes.POINTER(P), ctypes.POINTER(P), P, sz, u32, P]
     lib.ds_simulate.argtypes = [u32, P, P, P, P, P, P, P, P, u32, P, u32, u32, P, u32,
                                 ctypes.POINTER(SimParams), P, P, P, P, P, sz, u32, P]
-    for f in (lib.ds_characterize, lib.ds_characterize_score, lib.ds_calibrate, lib.ds_calibrate_ex, lib.ds_score, lib.ds_order,
+    for f in (lib.ds_characterize, lib.ds_characterize_score, lib.ds_characterize_score_noalloc,
+              lib.ds_calibrate, lib.ds_calibrate_ex, lib.ds_score, lib.ds_order,
               lib.ds_order_multi, lib.ds_error_stats, lib.ds_class_histogram, lib.ds_simulate):
         f.restype = i32
     lib.ds_workspace_bytes.argtypes = [i32, u64, u32]
@@ -310,6 +313,34 @@ def characterize_score(text, offsets, category, tenant, group, t_base, s_tenant,
                                      t_base.numel(), _ptr(s_tenant), s_tenant.numel(), _ptr(state),
                                      state.numel(), ctypes.byref(p), _ptr(est_base), _ptr(est), _ptr(budget),
                                      _ptr(cls), _ptr(ws), ws.numel(), _flags(validate), _stream()))
+    return counts, out
+
+
+NOALLOC_MAX_PROMPTS = 1 << 20
+
+
+def characterize_score_noalloc(text, offsets, category, tenant, group, t_base, s_tenant, state,
+                               f_ref=1024.0, short_max=128.0, medium_max=512.0, counts=None,
+                               out=None):
+    """``characterize_score`` through ds_characterize_score_noalloc: no
+    workspace (the library's static scratch array). ``counts`` and ``out``
+    (est_base or None, est, budget, class) are the caller's tensors; the
+    call itself allocates nothing. Returns (counts, out)."""
+    _dev(text, torch.uint8, "text")
+    _dev(offsets, torch.int64, "offsets")
+    for t, dt, name in ((category, torch.uint8, "category"), (tenant, torch.int32, "tenant"),
+                        (group, torch.int32, "group"), (t_base, torch.float64, "t_base"),
+                        (s_tenant, torch.float64, "s_tenant"), (state, torch.float64, "state"),
+                        (counts, torch.int32, "counts")):
+        _dev(t, dt, name)
+    n = offsets.numel() - 1
+    est_base, est, budget, cls = out
+    p = ScoreParams(float(f_ref), float(short_max), float(medium_max))
+    _check(lib.ds_characterize_score_noalloc(
+        _ptr(text) if text.numel() else None, text.numel(), _ptr(offsets), n, _ptr(counts),
+        _ptr(category), _ptr(tenant), _ptr(group), _ptr(t_base), t_base.numel(), _ptr(s_tenant),
+        s_tenant.numel(), _ptr(state), state.numel(), ctypes.byref(p), _ptr(est_base), _ptr(est),
+        _ptr(budget), _ptr(cls), 0, _stream()))
     return counts, out
 
 

@@ -26,7 +26,7 @@ def declared_functions():
 def test_exports_every_declared_symbol(ds):
     names = declared_functions()
     assert names == ["ds_calibrate", "ds_calibrate_ex", "ds_characterize", "ds_characterize_score",
-                     "ds_class_histogram", "ds_error_stats", "ds_order", "ds_order_multi",
+                     "ds_characterize_score_noalloc", "ds_class_histogram", "ds_error_stats", "ds_order", "ds_order_multi",
                      "ds_read_bandwidth", "ds_score", "ds_simulate", "ds_status_string", "ds_version",
                      "ds_workspace_bytes"]
     for name in names:
@@ -231,6 +231,19 @@ def test_characterize_score_host_errors(ds):
     assert f(FAKE, 16, FAKE, 4, FAKE, *sc, ctypes.byref(good), *outs, FAKE_WS, 16, 0, NULL) == -4
     assert f(FAKE, 16, FAKE, 0xFFFFFFFF, FAKE, *sc, ctypes.byref(good), *outs, FAKE_WS, ws, 0, NULL) == -3
     assert f(NULL, 0, NULL, 0, NULL, *sc, ctypes.byref(good), *outs, NULL, 0, 0, NULL) == 0
+
+
+def test_characterize_score_noalloc_host_errors(ds):
+    # checked before anything touches a GPU
+    P = ds.ScoreParams(1024.0, 128.0, 512.0)
+    x = ctypes.c_void_p(256)
+    call = lambda n, flags, params=P: ds.lib.ds_characterize_score_noalloc(
+        x, 16, x, n, x, x, x, x, x, 4, x, 3, x, 3, params, None, x, x, x, flags, None)
+    assert call(ds.NOALLOC_MAX_PROMPTS + 1, 0) == -3         # above the scratch array's limit
+    assert call(10, 1) == -2                                  # DS_VALIDATE refused
+    assert call(0, 0) == 0                                    # empty batch
+    assert call(10, 0, None) == -1
+    assert ds.workspace_bytes(ds.OP_CHARACTERIZE, ds.NOALLOC_MAX_PROMPTS) <= 4456960
 
 
 def test_read_bandwidth_host_errors(ds):
