@@ -262,6 +262,14 @@ ds_status ds_calibrate(const uint32_t *group, const double *est, const uint32_t 
  *  t_base     device, n_cat double (baseline estimate per semantic category)
  *  s_tenant   device, n_tenants double (tenant safety scaling)
  *  state      device, n_groups double (calibration factors, e.g. from ds_calibrate)
+ *  group      may be NULL: state then holds one factor per request (state[i]
+ *             scores request i; n_groups must be n, else DS_ERR_ARG). This is
+ *             as-of scoring: each request with the factor its group had when
+ *             it was admitted (Sec. "Runtime Calibration and Feedback
+ *             Adaptation": the updated factors serve later estimates), e.g.
+ *             trace_before of ds_calibrate_ex gathered to the requests'
+ *             positions. Calibration keyed by semantic category (the paper's
+ *             workload-specific factor) is group = category.
  *  est_base   device, n double, or NULL
  *  est, budget device, n double; job_class device, n uint8
  *  params     host; f_ref > 0
@@ -293,12 +301,13 @@ ds_status ds_score(uint32_t n, const uint32_t *counts, const uint8_t *category,
  *               DS_WRR_BLOCKED  round r serves, for q = 0, 1, ..., the
  *                 requests of tier q with FIFO rank within the tier in
  *                 [r w_q, (r+1) w_q); empty queues are passed over
- *               DS_WRR_SMOOTH  before each dispatch every non-empty queue's
- *                 credit grows by w_q; the largest credit (lowest tier on
- *                 ties) is served and gives up W, the sum of the non-empty
- *                 queues' weights; credits start at 0, and when a queue runs
- *                 empty a new cycle begins over the rest with every credit
- *                 at 0. W <= DS_WRR_MAX_WEIGHT_SUM (else DS_ERR_ARG)
+ *               DS_WRR_SMOOTH  smooth weighted round robin: before each
+ *                 dispatch every non-empty queue's credit grows by w_q; the
+ *                 largest credit (lowest tier on ties) is served and gives
+ *                 up W, the sum of the non-empty queues' weights; credits
+ *                 start at 0, and a queue that runs empty leaves while the
+ *                 others keep their credits. Sum of the weights <=
+ *                 DS_WRR_MAX_WEIGHT_SUM (else DS_ERR_ARG)
  *               DS_WRR_STRIDE  stride scheduling: the k-th request of tier q
  *                 (FIFO rank within the tier) has pass (k+1) / w_q, compared
  *                 exactly; smaller pass first, equal passes by lower tier

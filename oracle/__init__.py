@@ -157,12 +157,13 @@ def score(counts, category, tenant, group, t_base, s_tenant, state,
           f_ref=1024.0, short_max=128.0, medium_max=512.0):
     """Stage 3: Eq. (1)/(2) in Alg. 1's order and the classes of Eq. (4).
 
+    ``group`` None: ``state`` holds one factor per request (as-of scoring).
     Returns (est_base, est, budget, job_class).
     """
     counts = _c(counts, np.uint32)
     category = _c(category, np.uint8)
     tenant = _c(tenant, np.uint32)
-    group = _c(group, np.uint32)
+    group = None if group is None else _c(group, np.uint32)
     t_base = _c(t_base, np.float64)
     s_tenant = _c(s_tenant, np.float64)
     state = _c(state, np.float64)

@@ -272,7 +272,11 @@ int dsref_class_histogram(uint64_t n, const uint8_t *category, uint32_t n_cat,
  *   budget  = n_i + est                             (Eq. 1)
  *   class   = 0 short if budget <= short_max, 1 medium if <= medium_max,
  *             2 long otherwise                      (Eq. 4)
- * est_base may be NULL. Returns -1 if an index is out of range.
+ * est_base may be NULL. group may be NULL: then state holds one factor per
+ * request (state[i] scores request i, n_groups = n), the factor its group
+ * had when the request was admitted (as-of scoring; the paper's updated
+ * factors serve the estimates that follow them, Sec. "Runtime Calibration
+ * and Feedback Adaptation"). Returns -1 if an index is out of range.
  */
 int dsref_score(uint64_t n, const uint32_t *counts, const uint8_t *category,
                 const uint32_t *tenant, const uint32_t *group,
@@ -282,14 +286,16 @@ int dsref_score(uint64_t n, const uint32_t *counts, const uint8_t *category,
                 double f_ref, double short_max, double medium_max,
                 double *est_base, double *est, double *budget, uint8_t *job_class)
 {
+    if (!group && n_groups != n) return -1;
     for (uint64_t i = 0; i < n; i++) {
-        if (category[i] >= n_cat || tenant[i] >= n_tenants || group[i] >= n_groups)
+        uint64_t g = group ? group[i] : i;   /* no groups: request i's own factor */
+        if (category[i] >= n_cat || tenant[i] >= n_tenants || g >= n_groups)
             return -1;
         double words = (double)counts[i];
         double F = 1.0 + words / f_ref;
         double tb = t_base[category[i]];
         double s = s_tenant[tenant[i]];
-        double b = state[group[i]];
+        double b = state[g];
         double e = tb * b;
         e = e * s;
         e = e * F;
@@ -376,8 +382,9 @@ static void sort_requests(uint32_t *perm, uint32_t n, const double *primary,
  *            dispatch every non-empty queue's credit grows by its weight;
  *            the queue with the largest credit (the lowest tier on ties)
  *            dispatches its head and gives up the sum of the weights of the
- *            non-empty queues. When a queue runs empty it leaves and a new
- *            cycle begins over the queues left: every credit returns to 0.
+ *            non-empty queues. When a queue runs empty it leaves; the other
+ *            queues keep their credits (the published smooth weighted round
+ *            robin, which passes over an unavailable peer).
  *            key = floor(k / weight) for the k-th request of its tier, as
  *            for Weighted.
  *  Weighted, stride (policy 6; another reading of the same section):
@@ -464,8 +471,7 @@ int dsref_order(int policy, uint32_t n, const uint8_t *tier, const double *arriv
                 perm[pos++] = i;
                 if (key) key[i] = (double)(head[best] / weight[best]);
                 head[best]++;
-                if (head[best] == len[best])   /* a new cycle over the queues left */
-                    memset(credit, 0, sizeof(long long) * n_tiers);
+                /* a queue that runs empty leaves; the others keep their credits */
             }
             free(credit);
             free(fifo); free(len); free(start); free(head); free(queue);

@@ -45,6 +45,18 @@ ds_status run(void *ws, uint32_t flags, hipStream_t s, F &&enqueue)
 
 void *after_flag(void *ws) { return static_cast<uint8_t *>(ws) + kFlagBytes; }
 
+// The integer a C caller passed for an enum-typed argument. C allows any int
+// there; in C++ a value outside the enumeration's range may not be read as
+// the enum type, so it is copied out as bytes first.
+template <typename E>
+int enum_int(const E &e)
+{
+    static_assert(sizeof(E) == sizeof(int), "the ABI's enums are int-sized");
+    int v;
+    memcpy(&v, &e, sizeof v);
+    return v;
+}
+
 // The calls whose kernels wait on each other (the look-backs of the sorts)
 // keep a status word in the workspace, at byte DS_WS_STATUS_OFFSET: the
 // call's first kernel zeroes it and a wait that runs out sets it. With
@@ -77,9 +89,9 @@ extern "C" {
 
 uint32_t ds_version(void) { return 10000u; }
 
-const char *ds_status_string(ds_status st)
+const char *ds_status_string(ds_status status)
 {
-    switch (st) {
+    switch (enum_int(status)) {
     case DS_OK: return "ok";
     case DS_ERR_NULL: return "a required pointer is NULL";
     case DS_ERR_ARG: return "argument out of range";
@@ -93,9 +105,9 @@ const char *ds_status_string(ds_status st)
     return "unknown status";
 }
 
-size_t ds_workspace_bytes(ds_op op, uint64_t n, uint32_t n_groups)
+size_t ds_workspace_bytes(ds_op op_arg, uint64_t n, uint32_t n_groups)
 {
-    switch (op) {
+    switch (enum_int(op_arg)) {
     case DS_OP_CHARACTERIZE: return kFlagBytes + char_ws_bytes(n);
     case DS_OP_CALIBRATE: return kFlagBytes + cal_ws_bytes(n, n_groups ? n_groups : 1);
     case DS_OP_SCORE: return kFlagBytes;
@@ -172,9 +184,10 @@ ds_status ds_score(uint32_t n, const uint32_t *counts, const uint8_t *category,
     if (!params) return DS_ERR_NULL;
     if (!(params->f_ref > 0.0) || isnan(params->short_max) || isnan(params->medium_max))
         return DS_ERR_ARG;
-    if (n_cat == 0 || n_tenants == 0 || n_groups == 0) return DS_ERR_ARG;
+    if (n_cat == 0 || n_tenants == 0 || (group && n_groups == 0)) return DS_ERR_ARG;
     if (n == 0) return DS_OK;
-    if (!counts || !category || !tenant || !group || !t_base || !s_tenant || !state || !est ||
+    if (!group && n_groups != n) return DS_ERR_ARG;   // one factor per request
+    if (!counts || !category || !tenant || !t_base || !s_tenant || !state || !est ||
         !budget || !job_class)
         return DS_ERR_NULL;
     if (!aligned(counts, 4) || !aligned(tenant, 4) || !aligned(group, 4) || !aligned(t_base, 8) ||
@@ -209,10 +222,11 @@ static ds_status char_score_checks(const uint8_t *text, uint64_t text_bytes, con
     if (!params) return DS_ERR_NULL;
     if (!(params->f_ref > 0.0) || isnan(params->short_max) || isnan(params->medium_max))
         return DS_ERR_ARG;
-    if (n_cat == 0 || n_tenants == 0 || n_groups == 0) return DS_ERR_ARG;
+    if (n_cat == 0 || n_tenants == 0 || (group && n_groups == 0)) return DS_ERR_ARG;
     if (n == 0) return DS_OK;
+    if (!group && n_groups != n) return DS_ERR_ARG;   // one factor per request
     if (!offsets || !counts || (text_bytes > 0 && !text)) return DS_ERR_NULL;
-    if (!category || !tenant || !group || !t_base || !s_tenant || !state || !est || !budget || !job_class)
+    if (!category || !tenant || !t_base || !s_tenant || !state || !est || !budget || !job_class)
         return DS_ERR_NULL;
     if (text && !aligned(text, 16)) return DS_ERR_ALIGN;
     if (!aligned(offsets, 8) || !aligned(counts, 4)) return DS_ERR_ALIGN;
@@ -294,7 +308,7 @@ static ds_status scratch_for(hipStream_t s, void **out)
         if (cur != dev && hipSetDevice(dev) != hipSuccess) return DS_ERR_HIP;
         void *p = nullptr;
         e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
-        if (cur != dev) hipSetDevice(cur);
+        if (cur != dev) (void)hipSetDevice(cur);
         if (e != hipSuccess || !p) return DS_ERR_HIP;
         g_scratch_dev[dev] = p;
     }
@@ -404,12 +418,13 @@ ds_status ds_order(ds_policy policy, uint32_t n, const uint8_t *tier, const doub
                    uint32_t *perm, double *key, void *ws, size_t ws_bytes, uint32_t flags,
                    ds_stream stream)
 {
-    if ((int)policy < 0 || (int)policy > 4) return DS_ERR_ARG;
+    const int pol = enum_int(policy);
+    if (pol < 0 || pol > 4) return DS_ERR_ARG;
     uint32_t *perms[5] = {nullptr, nullptr, nullptr, nullptr, nullptr};
     double *keys[5] = {nullptr, nullptr, nullptr, nullptr, nullptr};
-    perms[policy] = perm;
-    keys[policy] = key;
-    return order_common(1u << policy, n, tier, arrival, budget, fifo_in, params, perms, keys, ws,
+    perms[pol] = perm;
+    keys[pol] = key;
+    return order_common(1u << pol, n, tier, arrival, budget, fifo_in, params, perms, keys, ws,
                         ws_bytes, DS_OP_ORDER, flags, stream);
 }
 
@@ -472,7 +487,7 @@ ds_status ds_simulate(uint32_t n, const double *arrival, const uint8_t *tier,
                       uint32_t flags, ds_stream stream)
 {
     if (!params) return DS_ERR_NULL;
-    const int policy = (int)params->policy;
+    const int policy = enum_int(params->policy);
     if (policy < 0 || policy > 4) return DS_ERR_ARG;
     if (params->batch < 1 || params->batch > DS_MAX_BATCH) return DS_ERR_ARG;
     if (!(params->alpha >= 0.0 && params->alpha <= 1.0)) return DS_ERR_ARG;

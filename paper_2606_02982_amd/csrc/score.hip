@@ -18,7 +18,9 @@ __global__ void k_score_validate(ScoreArgs a, uint32_t *__restrict__ flag)
 {
     uint32_t bad = 0;
     for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < a.n; i += gridDim.x * blockDim.x)
-        if (a.category[i] >= a.n_cat || a.tenant[i] >= a.n_tenants || a.group[i] >= a.n_groups) bad = 1;
+        if (a.category[i] >= a.n_cat || a.tenant[i] >= a.n_tenants ||
+            (a.group ? a.group[i] : i) >= a.n_groups)
+            bad = 1;
     if (bad) atomicOr(flag, 1u);
 }
 

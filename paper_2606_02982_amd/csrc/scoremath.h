@@ -14,7 +14,8 @@ namespace ds {
 __device__ __forceinline__ void score_one(const ScoreArgs &a, uint32_t i, uint32_t count)
 {
     const double nan = __builtin_nan("");
-    const uint32_t cat = a.category[i], ten = a.tenant[i], g = a.group[i];
+    // no group array: state holds each request's own factor (as-of scoring)
+    const uint32_t cat = a.category[i], ten = a.tenant[i], g = a.group ? a.group[i] : i;
     const double words = (double)count;
     const bool ok = cat < a.n_cat && ten < a.n_tenants && g < a.n_groups;
     const double tb = ok ? a.t_base[cat] : nan;

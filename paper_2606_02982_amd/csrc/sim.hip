@@ -300,8 +300,8 @@ __global__ __launch_bounds__(kTPB) void k_sim_engine(EngineArgs a)
             if (tid < m) s_selpos[tid] = tid;
         } else if (policy == kWeighted && a.wrr_mode == kWrrSmooth) {
             // the first m dispatches of a fresh smooth cycle, one per step,
-            // by one wave (lane q = tier q); a queue running empty starts a
-            // new cycle over the rest
+            // by one wave (lane q = tier q); a queue running empty leaves and
+            // the others keep their credits
             if (w == 0) {
                 const uint32_t len = lane < nq ? s_cnt[lane] : 0u;
                 const uint32_t wq = lane < nq ? s_wt[lane] : 0u;
@@ -313,10 +313,7 @@ __global__ __launch_bounds__(kTPB) void k_sim_engine(EngineArgs a)
                     const bool mine = lane == (uint32_t)b;
                     if (mine) s_selpos[pos] = s_big.first[lane][served];   // served < m <= batch
                     served += mine ? 1u : 0u;
-                    if (__ballot(mine && served == len) != 0ull) {
-                        credit = 0;
-                        W = wave_sum(served < len ? wq : 0u);
-                    }
+                    if (__ballot(mine && served == len) != 0ull) W = wave_sum(served < len ? wq : 0u);
                 }
             }
         } else if (queued) {

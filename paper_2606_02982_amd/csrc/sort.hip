@@ -60,6 +60,7 @@ struct SortDesc {
     uint32_t *val[2];
     uint32_t *status;      // [passes][tiles][256]
     WrrPlan *plan;         // Tier, smooth round robin: the period table (built by k_sort_plan)
+    uint32_t *tpos;        // its start-up positions (val[1]: a one-pass sort leaves it unused)
 };
 
 struct SortBatch {
@@ -191,7 +192,7 @@ __global__ __launch_bounds__(kPlanTPB) void k_sort_plan(SortBatch b)
         __shared__ uint16_t per[kWrrMaxWeightSum];
         const uint32_t nq = b.in.n_tiers < kWrrTiers ? b.in.n_tiers : kWrrTiers;
         const bool tl = t < nq;
-        wrr_plan_build(tl ? c : 0u, tl ? b.in.weight[t] : 0u, per, d.plan);
+        wrr_plan_build(tl ? c : 0u, tl ? b.in.weight[t] : 0u, per, d.plan, d.tpos);
     }
 }
 
@@ -370,7 +371,7 @@ __global__ __launch_bounds__(TPB) void k_sort_pass(SortBatch b, uint32_t p)
             uint64_t pos;
             if (smooth) {
                 uint32_t r32;
-                pos = wrr_smooth_pos(wh, d.plan->off, b.in.weight[q & 15u], q & 15u, (uint32_t)kq, r32);
+                pos = wrr_smooth_pos(wh, d.plan, d.tpos, b.in.weight[q & 15u], q & 15u, (uint32_t)kq, r32);
                 rnd = r32;
             } else if (b.in.wrr_mode == kWrrStride) {
                 const uint32_t qc = q & 15u, wq = b.in.weight[qc] ? b.in.weight[qc] : 1u;
@@ -429,6 +430,7 @@ void carve(uint8_t *p, uint64_t n, SortDesc &d)
     d.status = reinterpret_cast<uint32_t *>(p);
     p += align_up((uint64_t)kMaxPasses * cdiv(n, tile_keys(n)) * 256 * 4, 256);
     d.plan = reinterpret_cast<WrrPlan *>(p);
+    d.tpos = d.val[1];
 }
 
 }  // namespace

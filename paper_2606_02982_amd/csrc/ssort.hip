@@ -122,6 +122,7 @@ struct SsBatch {
     uint32_t nsorts;       // sorts of the batch (grid rows)
     uint32_t nsb;          // blocks of k_ss_sample per sort
     WrrPlan *plan;         // smooth round robin: the period table (built by the scatter)
+    uint32_t *tpos;        // [n] its start-up positions
     SsDesc s[kSsMaxSorts];
 };
 
@@ -477,7 +478,7 @@ __global__ __launch_bounds__(kScTPB) void k_ss_scatter(SsBatch b)
             const uint32_t nq = b.in.n_tiers < kQ ? b.in.n_tiers : kQ;
             const bool tl = (uint32_t)lane < nq;
             wrr_plan_build(tl ? ld_relaxed(&d.tot[lane]) : 0u, tl ? b.in.weight[lane] : 0u,
-                           reinterpret_cast<uint16_t *>(lj), b.plan);
+                           reinterpret_cast<uint16_t *>(lj), b.plan, b.tpos);
         }
     }
 }
@@ -532,7 +533,7 @@ __device__ __forceinline__ void pw_place(const SsBatch &b, const SsDesc &d, cons
         const uint32_t nq = b.in.n_tiers < kQ ? b.in.n_tiers : kQ;
         uint64_t pos;
         if (b.in.wrr_mode == kWrrSmooth) {
-            pos = wrr_smooth_pos(pt.wh, b.plan->off, pt.weight[q], q, kt, rnd);
+            pos = wrr_smooth_pos(pt.wh, b.plan, b.tpos, pt.weight[q], q, kt, rnd);
         } else if (b.in.wrr_mode == kWrrStride) {
             rnd = kt / (pt.weight[q] ? pt.weight[q] : 1u);
             pos = wrr_stride_pos(q, kt, pt.weight, nq, [&](uint32_t u) { return pt.tot[u]; });
@@ -1473,7 +1474,7 @@ void carve(uint8_t *p, uint64_t n, SsDesc &d)
 
 size_t ssort_ws_bytes(uint64_t n, uint32_t nsorts)
 {
-    return n <= kSsMaxN ? (size_t)(align_up(sizeof(WrrPlan), 256) +
+    return n <= kSsMaxN ? (size_t)(align_up(sizeof(WrrPlan), 256) + align_up(n * 4, 256) +
                                    (uint64_t)nsorts * region_bytes(n))
                         : 0;
 }
@@ -1496,6 +1497,8 @@ hipError_t ssort_launch(const SortInput &in, const SortJob *jobs, uint32_t nsort
     uint8_t *p = static_cast<uint8_t *>(ws);
     b.plan = reinterpret_cast<WrrPlan *>(p);
     p += align_up(sizeof(WrrPlan), 256);
+    b.tpos = reinterpret_cast<uint32_t *>(p);
+    p += align_up((uint64_t)in.n * 4, 256);
     for (uint32_t i = 0; i < nsorts; i++) {
         SsDesc &d = b.s[i];
         const SortKind k = jobs[i].kind;

@@ -2,18 +2,24 @@
 // paper fixes the dispatch ratio and the cyclic service, not the order of
 // the tiers inside a cycle): before each dispatch every non-empty queue's
 // credit grows by its weight; the largest credit (the lowest tier on ties)
-// is served and gives up the sum W of the non-empty queues' weights. When a
-// queue runs empty a new cycle begins over the queues left, every credit
-// back at 0. (Internal to the library.)
+// is served and gives up the sum W of the non-empty queues' weights. A queue
+// that runs empty leaves and the others keep their credits, as the
+// published rule passes over an unavailable peer. (Internal to the library.)
 //
-// From zero credits the rule serves queue q exactly w_q times in W
-// dispatches and brings the credits back to 0, so the dispatches repeat with
-// period W until a queue runs empty. The plan cuts the sequence into phases
-// at those points (at most one per tier); for each phase it records its
-// first position, W, every tier's dispatches before it, and the offsets of
-// each tier's dispatches inside one period. The k-th request of tier q (FIFO
-// order) is then served at
-//   start + floor(i / w_q) W + offset[i mod w_q],  i = k - (q's dispatches before the phase).
+// The sequence falls into phases, one per set of non-empty queues (a phase
+// ends where a queue runs empty; at most one per tier). Within a phase the
+// credits are a deterministic function of the previous ones on a finite
+// set, so they become periodic; once the credits after W dispatches equal
+// those before, the same W dispatches, w_q of them of queue q, repeat until
+// the phase ends. From zero credits (the first phase) that holds at once;
+// after a queue leaves with a non-zero credit there is a start-up stretch
+// first. The plan records for each phase its first position, W, the length
+// of its start-up stretch and each tier's dispatches in it (their positions,
+// in tpos), each tier's dispatches before the phase, and the offsets of each
+// tier's dispatches inside one period. The k-th request of tier q (FIFO
+// order) is then served at, with i = k - (q's dispatches before the phase):
+//   start + tpos[...]                                 if i < tcnt (start-up),
+//   start + tlen + floor(i' / w_q) W + offset[i' mod w_q],  i' = i - tcnt, else.
 #pragma once
 
 #include "common.h"
@@ -28,6 +34,7 @@ struct WrrPlanHead {
     uint32_t nph;                              // phases
     uint32_t start[kWrrTiers];                 // first position of each phase
     uint32_t W[kWrrTiers];                     // its period
+    uint32_t tlen[kWrrTiers];                  // dispatches of its start-up stretch (before the period)
     uint32_t used[kWrrTiers][kWrrTiers];       // [phase][tier] dispatches before the phase
     uint32_t offbase[kWrrTiers][kWrrTiers];    // [phase][tier] first offset in off[]
 };
@@ -35,6 +42,8 @@ struct WrrPlanHead {
 struct WrrPlan {
     WrrPlanHead h;
     uint16_t off[kWrrMaxOffsets];              // dispatch offsets inside a period, ascending per tier
+    uint32_t tcnt[kWrrTiers][kWrrTiers];       // [phase][tier] dispatches in the start-up stretch
+    uint32_t tbase[kWrrTiers][kWrrTiers];      // [phase][tier] their first entry in tpos
 };
 
 // Reductions over the 16 lanes of each DPP row (the tiers are lanes 0..15,
@@ -96,72 +105,131 @@ __device__ __forceinline__ int wrr_pick(int32_t &credit, bool active, uint32_t w
 
 // The plan for queue lengths len and weights wq held by lane q = tier q of
 // one wave (lanes of absent tiers, and every lane from 16 on, pass len = 0;
-// weights >= 1 for tiers with requests, their sum <= kWrrMaxWeightSum). per: LDS scratch of
-// kWrrMaxWeightSum entries. The plan goes to global memory, for later
-// launches.
-__device__ inline void wrr_plan_build(uint32_t len, uint32_t wq, uint16_t *per, WrrPlan *plan)
+// weights >= 1 for tiers with requests, their sum <= kWrrMaxWeightSum). per:
+// LDS scratch of kWrrMaxWeightSum entries. tpos: global, room for one entry
+// per request (the start-up stretches hold at most every request once). The
+// plan goes to global memory, for later launches.
+//
+// Per phase, the wave first plays the rule block by block (W dispatches
+// each) from the phase's credits until the credits after a block equal
+// those before it (that block is the period) or a queue runs empty (the
+// whole phase is then start-up stretch); then it plays the start-up
+// stretch again from the same credits, writing each dispatch's position.
+// The loops end: every dispatch serves one of the finitely many requests.
+__device__ inline void wrr_plan_build(uint32_t len, uint32_t wq, uint16_t *per, WrrPlan *plan,
+                                      uint32_t *tpos)
 {
     const int lane = lane_id();
     bool active = len > 0u;
-    uint32_t used = 0, pos = 0, ph = 0, offcur = 0;
+    uint32_t used = 0, pos = 0, ph = 0, offcur = 0, tcur = 0;
+    int32_t credit = 0;   // kept across phases
     while (__ballot(active) != 0ull) {
         const uint32_t mine = active ? wq : 0u;
         const uint32_t W = readlane32(row_sum_u32(mine), 0);   // row 0 holds every active lane
         const uint32_t base = wave_incl_scan_dpp(mine) - mine;   // this tier's offsets in the period
+        const uint32_t rem = active ? len - used : 0u;           // >= 1 when active
+        // 1. blocks of W dispatches until one repeats the credits, or the
+        //    phase ends
+        const int32_t c_in = credit;
+        uint32_t t = 0, got = 0;
+        bool ended = false;
+        for (;;) {
+            const int32_t c0 = credit;
+            uint32_t cnt = 0;
+            for (uint32_t s = 0; s < W; s++) {
+                const int b = wrr_pick(credit, active, wq, W);
+                const bool me = lane == b;
+                if (me) {
+                    // a block that turns out to be the period serves w_q of
+                    // tier q; the others' offsets are not used
+                    if (cnt < wq) per[base + cnt] = (uint16_t)s;
+                    cnt++;
+                    got++;
+                }
+                t++;
+                if (__ballot(me && got == rem) != 0ull) {
+                    ended = true;
+                    break;
+                }
+            }
+            if (ended || __ballot(active && credit != c0) == 0ull) break;
+        }
+        // 2. the start-up stretch: every dispatch of the phase if it ended,
+        //    else all but the last block (the period, w_q of tier q)
+        const uint32_t tl = ended ? t : t - W;
+        const uint32_t tc = ended ? got : (active ? got - wq : 0u);
+        const uint32_t tb = tcur + wave_incl_scan_dpp(tc) - tc;
+        credit = c_in;
+        {
+            uint32_t k = 0;
+            for (uint32_t s = 0; s < tl; s++) {
+                const int b = wrr_pick(credit, active, wq, W);
+                if (lane == b) tpos[tb + k++] = s;
+            }
+        }
         if (lane == 0) {
             plan->h.start[ph] = pos;
             plan->h.W[ph] = W;
+            plan->h.tlen[ph] = tl;
         }
         if ((uint32_t)lane < kWrrTiers) {
             plan->h.used[ph][lane] = used;
             plan->h.offbase[ph][lane] = offcur + base;
+            plan->tcnt[ph][lane] = tc;
+            plan->tbase[ph][lane] = tb;
         }
-        // one period from zero credits: the offsets of each tier's dispatches
-        int32_t credit = 0;
-        uint32_t cnt = 0;
-        for (uint32_t t = 0; t < W; t++) {
-            const int b = wrr_pick(credit, active, wq, W);
-            if (lane == b) {
-                per[base + cnt] = (uint16_t)t;
-                plan->off[offcur + base + cnt] = (uint16_t)t;
-                cnt++;
+        uint64_t T;   // dispatches of the phase
+        if (ended) {
+            T = tl;
+            used += tc;
+        } else {
+            // the period's offsets (each lane reads back only the ones it wrote)
+            if (active)
+                for (uint32_t i = 0; i < wq; i++) plan->off[offcur + base + i] = per[base + i];
+            // the phase ends where the first queue runs empty: a queue's last
+            // request is its (r - 1)-th after the start-up stretch
+            uint64_t Tq = ~0ull;
+            if (active) {
+                const uint32_t r = rem - tc;   // >= 1: no queue ran empty in the stretch
+                Tq = tl + (uint64_t)((r - 1u) / wq) * W + per[base + (r - 1u) % wq] + 1u;
             }
+            T = readlane64(row_min_u64(Tq), 0);   // <= the requests left
+            const uint32_t part = (uint32_t)((T - tl) % W);
+            uint32_t inpart = 0;
+            if (active)
+                for (uint32_t i = 0; i < wq; i++) inpart += per[base + i] < part ? 1u : 0u;
+            used += active ? tc + (uint32_t)((T - tl) / W) * wq + inpart : 0u;
+            // the credits at the phase's end: those of the period's start
+            // (now in credit) moved on by the part of a period
+            for (uint32_t s = 0; s < part; s++) wrr_pick(credit, active, wq, W);
         }
-        // the phase ends where the first queue runs empty, after T
-        // dispatches: a queue's last request is its (rem - 1)-th of the phase
-        // (each lane reads back only the offsets it wrote itself)
-        uint64_t Tq = ~0ull;
-        if (active) {
-            const uint32_t rem = len - used;   // >= 1
-            Tq = (uint64_t)((rem - 1u) / wq) * W + per[base + (rem - 1u) % wq] + 1u;
-        }
-        const uint64_t T = readlane64(row_min_u64(Tq), 0);   // <= the requests left
-        // each tier's dispatches among those T
-        const uint32_t part = (uint32_t)(T % W);
-        uint32_t inpart = 0;
-        if (active)
-            for (uint32_t i = 0; i < wq; i++) inpart += per[base + i] < part ? 1u : 0u;
-        used += active ? (uint32_t)(T / W) * wq + inpart : 0u;
         pos += (uint32_t)T;
         if (active && used == len) active = false;
         offcur += W;
+        tcur += readlane32(row_sum_u32(tc), 0);   // lanes 16..63 hold 0
         ph++;
     }
     if (lane == 0) plan->h.nph = ph;
 }
 
 // Position of the k-th request (FIFO order) of tier q, and its round
-// floor(k / w_q). head: the plan's header (a copy in LDS), off: its offsets.
-__device__ __forceinline__ uint64_t wrr_smooth_pos(const WrrPlanHead &head, const uint16_t *off, uint32_t wq,
-                                                   uint32_t q, uint32_t k, uint32_t &rnd)
+// floor(k / w_q). head: the plan's header (a copy in LDS), plan: the plan
+// (offsets and start-up counts), tpos: the start-up positions.
+__device__ __forceinline__ uint64_t wrr_smooth_pos(const WrrPlanHead &head, const WrrPlan *plan,
+                                                   const uint32_t *tpos, uint32_t wq, uint32_t q,
+                                                   uint32_t k, uint32_t &rnd)
 {
     wq = wq ? wq : 1u;
     rnd = k / wq;
     uint32_t ph = 0;
     for (uint32_t p = 1; p < head.nph; p++)
         if (head.used[p][q] <= k) ph = p;
-    const uint32_t i = k - head.used[ph][q];
-    return (uint64_t)head.start[ph] + (uint64_t)(i / wq) * head.W[ph] + off[head.offbase[ph][q] + i % wq];
+    uint32_t i = k - head.used[ph][q];
+    const uint32_t tc = plan->tcnt[ph][q];
+    if (i < tc) return (uint64_t)head.start[ph] + tpos[plan->tbase[ph][q] + i];
+    i -= tc;
+    return (uint64_t)head.start[ph] + head.tlen[ph] + (uint64_t)(i / wq) * head.W[ph] +
+           plan->off[head.offbase[ph][q] + i % wq];
 }
 
 // Stride scheduling, another reading of the same section: queue q's pass

@@ -256,11 +256,14 @@ def class_histogram(category, job_class, n_cat, out=None, ws=None, validate=Fals
 def score(counts, category, tenant, group, t_base, s_tenant, state, f_ref=1024.0,
           short_max=128.0, medium_max=512.0, want_est_base=True, out=None, ws=None,
           validate=False):
-    """Budget estimate (Eq. 1/2) and class (Eq. 4). Returns (est_base, est, budget, class)."""
+    """Budget estimate (Eq. 1/2) and class (Eq. 4). Returns (est_base, est, budget, class).
+
+    ``group`` None: ``state`` holds one factor per request (as-of scoring)."""
     _dev(counts, torch.int32, "counts")
     _dev(category, torch.uint8, "category")
     _dev(tenant, torch.int32, "tenant")
-    _dev(group, torch.int32, "group")
+    if group is not None:
+        _dev(group, torch.int32, "group")
     _dev(t_base, torch.float64, "t_base")
     _dev(s_tenant, torch.float64, "s_tenant")
     _dev(state, torch.float64, "state")
@@ -293,7 +296,8 @@ def characterize_score(text, offsets, category, tenant, group, t_base, s_tenant,
     for t, dt, name in ((category, torch.uint8, "category"), (tenant, torch.int32, "tenant"),
                         (group, torch.int32, "group"), (t_base, torch.float64, "t_base"),
                         (s_tenant, torch.float64, "s_tenant"), (state, torch.float64, "state")):
-        _dev(t, dt, name)
+        if t is not None or name != "group":
+            _dev(t, dt, name)
     n = offsets.numel() - 1
     dev = offsets.device
     if counts is None:

@@ -6,7 +6,8 @@ The order is integer work, so permutations and round keys must match
 exactly: on the sample-sort path (up to 2^18 requests, including the
 single-workgroup sort), on the radix path above it (with and without a
 given FIFO permutation), inside ds_order_multi, and in the dispatch-tick
-loop, where each tick starts a fresh cycle.
+loop, where each tick starts a fresh cycle. In the smooth mode a queue that
+runs empty leaves and the others keep their credits.
 """
 import numpy as np
 import pytest
@@ -142,6 +143,17 @@ def test_stride_large_weights(ds, oracle, n):
     tier, arr = batch(n + 7, n, 4)
     check(ds, oracle, "stride", tier, arr, (2 ** 31 + 11, 3, 1000003, 2 ** 32 - 1))
     check(ds, oracle, "stride", tier, arr, (1, 1, 1, 1))
+
+
+@pytest.mark.parametrize("sizes,weights", [((3, 1, 3), (1, 1, 1)), ((1, 10, 10), (3, 2, 1)),
+                                           ((2, 6, 6), (3, 1, 1)), ((40, 3, 900, 7), (9, 1, 17, 2))])
+def test_smooth_exhaustion_keeps_credits(ds, oracle, sizes, weights):
+    # the oracle's hand-traced exhaustion cases (and one with four tiers):
+    # after a queue runs empty the others keep their credits, which starts a
+    # stretch before the new period
+    tier = np.concatenate([np.full(s, q, np.uint8) for q, s in enumerate(sizes)])
+    check(ds, oracle, "smooth", tier, np.arange(tier.size, dtype=np.float64), weights)
+    check(ds, oracle, "smooth", tier, np.arange(tier.size, dtype=np.float64), weights, serial_sort=True)
 
 
 def test_blocked_mode_unchanged(ds, oracle):

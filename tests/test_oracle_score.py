@@ -80,3 +80,36 @@ def test_class_is_monotone_in_budget(oracle):
 def test_rejects_index_out_of_range(oracle):
     with pytest.raises(ValueError):
         oracle.score([1], [4], [0], [0], [1.0, 1.0, 1.0, 1.0], [1.0], [1.0])
+
+
+def test_as_of_factors_hand_case(oracle):
+    # as-of scoring (no group array): request i is scored with state[i].
+    # Three requests of one category and tenant (T_base 64, S 1.25, n 10, so
+    # F = 1.009765625 and the B-free estimate 80.78125) with the factors
+    # 1.5, 0.5, 2: est = 80.78125 * B exactly (dyadic), 121.171875,
+    # 40.390625, 161.5625; budgets 10 more; classes medium, short, medium
+    est_base, est, budget, cls = oracle.score([10, 10, 10], [0, 0, 0], [0, 0, 0], None, [64.0],
+                                              [1.25], [1.5, 0.5, 2.0])
+    assert list(est) == [121.171875, 40.390625, 161.5625]
+    assert list(est_base) == [80.78125] * 3
+    assert list(budget) == [131.171875, 50.390625, 171.5625]
+    assert list(cls) == [1, 0, 1]
+
+
+def test_as_of_needs_one_factor_per_request(oracle):
+    with pytest.raises(ValueError):
+        oracle.score([1, 2], [0, 0], [0, 0], None, [64.0], [1.0], [1.0])
+
+
+def test_as_of_with_the_groups_factors_is_the_group_mode(oracle):
+    # giving each request its group's factor reproduces the grouped call
+    rng = np.random.default_rng(3)
+    n, G = 500, 7
+    counts = rng.integers(0, 3000, n)
+    cat, ten, grp = rng.integers(0, 4, n), rng.integers(0, 5, n), rng.integers(0, G, n)
+    tb, s = [32.0, 128.0, 256.0, 512.0], [1.25, 1.125, 1.0, 1.0, 1.25]
+    state = rng.uniform(0.5, 1.5, G)
+    a = oracle.score(counts, cat, ten, grp, tb, s, state)
+    b = oracle.score(counts, cat, ten, None, tb, s, state[grp])
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)

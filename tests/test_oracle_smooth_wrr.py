@@ -4,9 +4,10 @@ cyclic service, not the order of the tiers inside a cycle. In the smooth
 reading every non-empty queue's credit grows by its weight before each
 dispatch, the largest credit (the lowest tier on ties) is served and gives
 up the sum of the non-empty queues' weights; a queue that runs empty
-leaves, and a new cycle over the queues left begins with every credit back
-at 0. Expected sequences are traced by hand below or follow from known
-properties of the rule, never from the oracle."""
+leaves and the others keep their credits (the published rule passes over
+an unavailable peer and leaves every credit as it is). Expected sequences
+are traced by hand below or follow from known properties of the rule, never
+from the oracle."""
 import numpy as np
 import pytest
 
@@ -47,14 +48,37 @@ def test_exhaustion_hand_case(oracle):
     assert [key[i] for i in perm] == [0, 0, 0, 0, 1, 2, 3, 4]
 
 
-def test_exhaustion_restarts_the_cycle(oracle):
+def test_exhaustion_keeps_the_credits(oracle):
     # weights (1,1,1), sizes (3,1,3), total 3:
-    #  (1,1,1) a -> (-2,1,1); (-1,2,2) b -> b is empty: credits (0,0), total 2;
-    #  (1,1) a -> (-1,1); (0,2) c -> (0,0); (1,1) a -> a is empty; c alone.
-    # (Had the credits been kept, (0,3) would serve c twice: "abccaca".)
+    #  (1,1,1) a -> (-2,1,1); (-1,2,2) b -> b is empty, the others keep
+    #  theirs: (a,c) = (-1,2), total 2; (0,3) c -> (0,1); (1,2) c -> (1,0);
+    #  (2,1) a -> (0,1); (1,2) c -> c is empty; a alone.
+    # (Restarting every credit at 0 instead would give "abacacc".)
     s, perm, key, tier = letters(oracle, (3, 1, 3), (1, 1, 1))
-    assert s == "abacacc"
-    assert [key[i] for i in perm] == [0, 0, 1, 0, 2, 1, 2]
+    assert s == "abccaca"
+    assert [key[i] for i in perm] == [0, 0, 0, 1, 1, 2, 2]
+
+
+def test_exhaustion_then_a_new_pattern(oracle):
+    # weights (3,2,1), sizes (1,10,10), total 6:
+    #  (3,2,1) a -> a is empty; (b,c) keep (2,1), total 3;
+    #  (4,2) b -> (1,2); (3,3) b -> (0,3); (2,4) c -> (2,1): the pattern
+    #  b b c repeats (a restart from (0,0) would repeat b c b instead);
+    #  b's tenth dispatch is the 14th after a's; then c alone
+    s, _, _, _ = letters(oracle, (1, 10, 10), (3, 2, 1))
+    assert s == "a" + "bbc" * 4 + "bb" + "c" * 6
+
+
+def test_exhaustion_with_a_transient(oracle):
+    # weights (3,1,1), sizes (2,6,6), total 5:
+    #  (3,1,1) a -> (-2,1,1); (1,2,2) b -> (1,-3,2); (4,-2,3) a -> a is
+    #  empty; (b,c) keep (-2,3), total 2: (-1,4) c -> (-1,2); (0,3) c ->
+    #  (0,1); (1,2) c -> (1,0); (2,1) b -> (0,1); from (0,1) the pattern
+    #  c b repeats (two dispatches of a start-up stretch before it); c's
+    #  sixth dispatch is the 12th overall, then b alone
+    s, perm, key, tier = letters(oracle, (2, 6, 6), (3, 1, 1))
+    assert s == "abacccbcbcbcbb"
+    assert [key[i] for i in perm] == [0, 0, 0, 0, 1, 2, 1, 3, 2, 4, 3, 5, 4, 5]
 
 
 def test_one_tier_is_fifo(oracle):
@@ -91,35 +115,28 @@ def test_period_counts_and_fifo(oracle, seed):
 
 
 @pytest.mark.parametrize("seed", range(10))
-def test_cycles_restart_when_a_queue_empties(oracle, seed):
-    # after each point where a queue runs empty, the rest is the smooth
-    # sequence of the queues left, from zero credits: its first W' dispatches
-    # (W' = their weights' sum) hold w_q of each if no queue empties earlier,
-    # and the pattern of one cycle repeats until a queue empties
+def test_exhaustion_at_a_period_end(oracle, seed):
+    # from zero credits the rule serves every queue w_q times in W
+    # dispatches and the credits come back to 0; when the first queue runs
+    # empty exactly at the end of such a period, the queues left hold zero
+    # credits, so what follows is the zero-credit cycle of the queues left:
+    # its first W' dispatches (W' = their weights' sum) hold w_q of each, and
+    # that pattern repeats while none of them runs empty
     rng = np.random.default_rng(700 + seed)
-    Q = int(rng.integers(2, 7))
-    w = [int(x) for x in rng.integers(1, 9, Q)]
-    sizes = [int(x) for x in rng.integers(1, 80, Q)]
+    Q = int(rng.integers(2, 6))
+    w = [int(x) for x in rng.integers(1, 7, Q)]
+    W = sum(w)
+    m = int(rng.integers(1, 4))
+    sizes = [m * x + int(rng.integers(40, 80)) for x in w]
+    sizes[0] = m * w[0]                   # queue 0 empties after m full periods
     s, perm, key, tier = letters(oracle, sizes, w)
     t = tier[perm]
-    left = list(sizes)
-    k = 0
-    while k < len(t):
-        act = [q for q in range(Q) if left[q] > 0]
-        Wp = sum(w[q] for q in act)
-        # the phase ends where the first of the active queues empties
-        served = dict((q, 0) for q in act)
-        end = k
-        while end < len(t):
-            served[int(t[end])] += 1
-            end += 1
-            if any(served[q] == left[q] for q in act):
-                break
-        seg = t[k:end]
-        for j in range(Wp, len(seg)):
-            assert seg[j] == seg[j - Wp]        # one cycle's pattern repeats
-        if len(seg) >= Wp:
-            assert all(int(np.sum(seg[:Wp] == q)) == w[q] for q in act)
-        for q in act:
-            left[q] -= served[q]
-        k = end
+    assert int(np.sum(t[:m * W] == 0)) == m * w[0]
+    rest = t[m * W:]
+    Wp = W - w[0]
+    left = [sizes[q] - m * w[q] for q in range(Q)]
+    end = min(((left[q] // w[q]) * Wp for q in range(1, Q)))   # whole cycles before any empties
+    for j in range(Wp, end):
+        assert rest[j] == rest[j - Wp]
+    for q in range(1, Q):
+        assert int(np.sum(rest[:Wp] == q)) == w[q]
