@@ -737,22 +737,29 @@ def cpu_baseline(b, budget_s, weighted_mode="blocked"):
     sample_bytes = int(b.offsets[done])
     # the other stages on the whole batch (the counts are the generator's, which
     # stage 1 reproduces exactly)
-    t0 = time.perf_counter()
+    t = [time.perf_counter()]
     state, _ = oracle.calibrate(b.ev_group, b.ev_est, b.ev_obs, b.alphas[0], np.ones(b.n_groups))
+    t.append(time.perf_counter())
     _, _, budget, _ = oracle.score(b.words, b.category, b.tenant, b.group, b.t_base,
                                    b.s_tenant, state)
+    t.append(time.perf_counter())
     weighted = {"blocked": 2, "smooth": oracle.WEIGHTED_SMOOTH, "stride": oracle.WEIGHTED_STRIDE}
     for pol in (0, 1, weighted[weighted_mode], 3, 4):
         oracle.order(pol, b.tier, b.arrival, budget, **kw)
-    t_rest = time.perf_counter() - t0
+        t.append(time.perf_counter())
+    t_rest = t[-1] - t[0]
     per_req = t_char / done + t_rest / N
     model, nproc = host_cpu()
+    stage_s = {"characterize": t_char / done * N, "calibrate": t[1] - t[0], "score": t[2] - t[1]}
+    for k, name in enumerate(("fifo", "priority", "weighted", "sjf", "aging")):
+        stage_s["order_" + name] = t[3 + k] - t[2 + k]
     return {"value": round(1.0 / per_req, 1), "unit": "requests/s", "cores": 1, "kind": "oracle",
             "host_cpu": model, "host_nproc": nproc,
             "sample": "stage 1 on the first %d of %d prompts (%d bytes, %.1f s); calibrate, score "
                       "and the five orders on the whole batch (%.1f s); step time per request = "
                       "the sum of the two per-request times" % (done, N, sample_bytes, t_char, t_rest),
-            "stage1_MB_per_s": round(sample_bytes / t_char / 1e6, 1)}
+            "stage1_MB_per_s": round(sample_bytes / t_char / 1e6, 1),
+            "stage_s": {k: round(v, 6) for k, v in stage_s.items()}}
 
 
 if __name__ == "__main__":
