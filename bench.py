@@ -570,6 +570,8 @@ def bench_drift(args, wl):
     from paper_2606_02982_amd import driftsched as ds
     b = load(wl)
     ob = oracle_events(b)
+    if args.copy_probe:
+        copy_probe()
     E, G = len(b.ev_group), b.n_groups
     group, est, obs = to_dev(b.ev_group), to_dev(b.ev_est), to_dev(b.ev_obs)
     state = torch.ones(G, dtype=torch.float64, device="cuda")

@@ -16,7 +16,7 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
 SOURCES = ["api.hip", "characterize.hip", "sort.hip", "calibrate.hip", "score.hip", "order.hip", "stats.hip",
-           "sim.hip", "ssort.hip", "calchunk.hip"]
+           "sim.hip", "ssort.hip", "calchunk.hip", "agmerge.hip"]
 
 HIP_FLAGS = [
     "--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC", "-Wall",

@@ -108,6 +108,15 @@ size_t ssort_ws_bytes(uint64_t n, uint32_t nsorts);   // 0 above kSsMaxN
 hipError_t ssort_launch(const SortInput &in, const SortJob *jobs, uint32_t nsorts, bool serial,
                         void *ws, hipStream_t s, const SsPartitions *parts = nullptr);
 
+// Aging above the sample-sort limit as a merge of the priority classes' runs
+// of the FIFO sequence (in.fifo, in.cls and the aging parameters set;
+// n_classes = the number of distinct priorities). wait_status (may be NULL):
+// zeroed by the first kernel (no waits here).
+constexpr uint32_t kAmMaxN = 1u << 24;
+size_t am_ws_bytes(uint64_t n);
+hipError_t am_launch(const SortInput &in, uint32_t n_classes, uint32_t *perm, double *key_out, void *ws,
+                     hipStream_t s, uint32_t *wait_status);
+
 // ---- stage 2: calibrate -------------------------------------------------------
 // Up to kCalGroupsLds groups: chunked scan without a global partition.
 constexpr uint32_t kCalGroupsLds = 4096;

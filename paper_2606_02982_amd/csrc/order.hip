@@ -103,12 +103,14 @@ hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_
     in.t_now = a.t_now;
     in.aging_floor = a.aging_floor;
     in.wait = wait;
-    if (a.mask & (1u << 1)) {
+    uint32_t n_classes = 1;
+    if (a.mask & ((1u << 1) | (1u << 4))) {
         // priority classes: rank of each tier's priority among the distinct values
         double vals[16];
         for (uint32_t q = 0; q < a.n_tiers; q++) vals[q] = a.prio[q];
         std::sort(vals, vals + a.n_tiers);
         uint32_t nd = (uint32_t)(std::unique(vals, vals + a.n_tiers) - vals);
+        n_classes = nd;
         for (uint32_t q = 0; q < 16; q++) {
             uint32_t c = 0;
             if (q < a.n_tiers)
@@ -146,13 +148,16 @@ hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_
         return ssort_launch(in, all, na, a.serial_sort, ws, s, parts ? &pw : nullptr);
     }
 
-    // the policy sorts over the FIFO sequence
+    // the policy sorts over the FIFO sequence; Aging as the merge of the
+    // priority classes' runs of that sequence (agmerge.hip) where its
+    // buffers fit the sort workspace, else as one more radix sort
+    const bool aging_merge = (a.mask & (1u << 4)) && n <= kAmMaxN && am_ws_bytes(n) <= sort_ws_bytes(n, 1);
     SortJob jobs[kMaxSorts];
     uint32_t nj = 0;
     if (a.mask & (1u << 1)) jobs[nj++] = {SortKind::Class, 8, a.key[1], a.perm[1]};
     if (a.mask & (1u << 2)) jobs[nj++] = {SortKind::Tier, 8, a.key[2], a.perm[2]};
     if (a.mask & (1u << 3)) jobs[nj++] = {SortKind::Budget, 64, a.key[3], a.perm[3]};
-    if (a.mask & (1u << 4)) jobs[nj++] = {SortKind::Aging, 64, a.key[4], a.perm[4]};
+    if ((a.mask & (1u << 4)) && !aging_merge) jobs[nj++] = {SortKind::Aging, 64, a.key[4], a.perm[4]};
 
     // radix sorts: the FIFO permutation first, then the policies over it
     uint8_t *p = static_cast<uint8_t *>(ws);
@@ -167,8 +172,16 @@ hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_
         in.wait.clear = false;
     }
     in.fifo = fifo;
-    if (nj == 0) return hipGetLastError();
-    return sort_launch(in, jobs, nj, sort_ws, s);
+    if (nj > 0) {
+        hipError_t err = sort_launch(in, jobs, nj, sort_ws, s);
+        if (err != hipSuccess) return err;
+        in.wait.clear = false;
+    }
+    // (after the sorts on the stream: the merge reuses their workspace)
+    if (aging_merge)
+        return am_launch(in, n_classes, a.perm[4], a.key[4], sort_ws, s,
+                         in.wait.clear ? in.wait.status : nullptr);
+    return hipGetLastError();
 }
 
 __global__ void k_fill_u32(uint32_t *__restrict__ p, uint32_t v, uint64_t n)

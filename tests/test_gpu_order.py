@@ -282,3 +282,52 @@ def test_small_batch_multi(ds, oracle, n):
         w_perm, w_key = oracle.order(p, tier, arr, bud, **kw)
         assert np.array_equal(host(perms[p], np.uint32), w_perm), "policy %d" % p
         assert np.array_equal(host(keys[p]), w_key), "policy %d" % p
+
+
+@pytest.mark.parametrize("case", ["three", "shared", "sixteen", "one_class", "skewed", "ties",
+                                  "no_floor", "fifo_given", "multi"])
+def test_aging_merge_path(ds, oracle, case):
+    """Aging above the sample-sort limit: the merge of the priority classes'
+    runs of the FIFO sequence, against the oracle's sort."""
+    n = 300001
+    rng = np.random.default_rng(len(case) * 7 + 1)
+    tiers = {"sixteen": 16, "one_class": 2, "shared": 5}.get(case, 3)
+    tier = rng.integers(0, tiers, n).astype(np.uint8)
+    arr = np.round(rng.uniform(0.0, 400.0, n), 3)
+    prio = tuple(float(q) for q in range(tiers))
+    kw = dict(t_now=400.0, aging_rate=0.01, aging_floor=0.0)
+    if case == "shared":
+        prio = (1.0, 0.0, 1.0, 2.0, 0.0)            # three classes over five tiers
+    elif case == "sixteen":
+        prio = tuple(float(x) for x in rng.permutation(16))
+        kw["aging_rate"] = 0.05
+    elif case == "one_class":
+        prio = (2.0, 2.0)
+    elif case == "skewed":
+        tier = np.where(rng.random(n) < 0.97, 0, tier).astype(np.uint8)
+    elif case == "ties":
+        arr = np.round(arr / 5.0) * 5.0              # many equal arrivals and equal scores
+        arr[:1000] = -0.0
+        kw["aging_rate"] = 0.25
+    elif case == "no_floor":
+        kw["aging_floor"] = -np.inf
+        kw["t_now"] = 200.0                          # some arrivals after t_now (wait 0)
+    print("aging merge %s n=%d tiers=%d" % (case, n, tiers), flush=True)
+    okw = dict(weights=(1,) * tiers, tier_priority=prio, **kw)
+    w_perm, w_key = oracle.order(4, tier, arr, None, **okw)
+    t, a = dev(tier), dev(arr)
+    params = ds.order_params(n_tiers=tiers, weights=(1,) * tiers, tier_priority=prio, **kw)
+    if case == "fifo_given":
+        fifo, _ = ds.order(0, t, a, params=params)
+        perm, key = ds.order(4, t, a, fifo=fifo, key=True, params=params, validate=True)
+    elif case == "multi":
+        bud = np.round(rng.uniform(1, 3000, n), 1)
+        perms, keys = ds.order_multi((0, 1, 2, 3, 4), t, a, dev(bud), keys=True, params=params)
+        for p in range(4):
+            w_p, _ = oracle.order(p, tier, arr, bud, **okw)
+            assert np.array_equal(host(perms[p], np.uint32), w_p), "policy %d" % p
+        perm, key = perms[4], keys[4]
+    else:
+        perm, key = ds.order(4, t, a, key=True, params=params, validate=True)
+    assert np.array_equal(host(perm, np.uint32), w_perm)
+    assert np.array_equal(host(key), w_key)
