@@ -673,6 +673,26 @@ def bench_simulate(args, wl):
                       "tick_s": 0.01}, "policies": {}}
     steps = max(1, args.steps // 10)
     a2 = argparse.Namespace(**dict(vars(args), steps=steps, warmup=1, settle=0.0))
+    # every policy (and the other two Weighted interleavings) in one launch
+    kw = dict(alpha=b.alphas[0], weights=tuple(int(w) for w in b.weights),
+              tier_priority=tuple(b.tier_priority), aging_rate=b.aging_rate)
+    runs = [(name, pol, "blocked") for name, pol in ds.POLICIES.items()] + \
+        [("weighted_smooth", ds.WEIGHTED, "smooth"), ("weighted_stride", ds.WEIGHTED, "stride")]
+    mparams = [ds.sim_params(pol, batch=32, weighted_mode=m, **kw) for _, pol, m in runs]
+    mstates = [torch.ones(b.n_groups, dtype=torch.float64, device="cuda") for _ in runs]
+    mws = ds.workspace(ds.OP_SIMULATE_MULTI, N, len(runs))
+
+    def run_multi():
+        for st in mstates:
+            st.fill_(1.0)
+        return ds.simulate_multi(d["arrival"], d["tier"], d["words"], d["category"], d["tenant"],
+                                 d["group"], d["observed"], d["t_base"], d["s_tenant"], mstates, tick_t,
+                                 mparams, ws=mws)
+    ms_multi = timed_ms(run_multi, a2)
+    _, nd_multi = run_multi()
+    res["one_launch"] = {"runs": [r[0] for r in runs], "ms": round(ms_multi, 3),
+                         "dispatched": [int(x) for x in nd_multi.cpu()],
+                         "ticks_per_s_per_run": round(len(ticks) / (ms_multi * 1e-3), 1)}
     for name, pol in ds.POLICIES.items():
         p = ds.sim_params(pol, batch=32, alpha=b.alphas[0], weights=tuple(int(w) for w in b.weights),
                           tier_priority=tuple(b.tier_priority), aging_rate=b.aging_rate,

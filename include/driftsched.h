@@ -24,6 +24,7 @@
  *
  *   ds_simulate         dispatch ticks: order the pending set, dispatch a
  *                       batch, feed its completions back into the factors
+ *   ds_simulate_multi   several such loops (e.g. the five policies) in one launch
  *
  * and one measurement aid:
  *
@@ -88,7 +89,8 @@ typedef enum {
     DS_OP_ORDER_MULTI = 4,
     DS_OP_ERROR_STATS = 5,
     DS_OP_CLASS_HIST = 6,
-    DS_OP_SIMULATE = 7
+    DS_OP_SIMULATE = 7,
+    DS_OP_SIMULATE_MULTI = 8   /* third argument of ds_workspace_bytes: the number of runs */
 } ds_op;
 
 /* flags */
@@ -472,6 +474,31 @@ ds_status ds_simulate(uint32_t n, const double *arrival, const uint8_t *tier,
                       const double *tick_t, uint32_t n_ticks, const ds_sim_params *params,
                       double *state, uint32_t *seq, int32_t *tick_of, uint32_t *n_dispatched,
                       void *ws, size_t ws_bytes, uint32_t flags, ds_stream stream);
+
+/*
+ * Several dispatch-tick loops over the same requests and ticks in one launch
+ * (one workgroup per run, after one shared FIFO sort), e.g. the five
+ * policies, or one policy at several EMA weights. Run r is ds_simulate with
+ * params[r], state[r], seq[r], tick_of[r] and n_dispatched[r]; its results
+ * are identical to that call's.
+ *
+ *  n_runs        1..DS_SIM_MAX_RUNS
+ *  params        HOST array of n_runs parameter sets (each checked as ds_simulate's)
+ *  state, seq, tick_of  HOST arrays of n_runs device pointers; the runs'
+ *                buffers must not overlap
+ *  n_dispatched  device, n_runs uint32
+ *  ws            workspace of ds_workspace_bytes(DS_OP_SIMULATE_MULTI, n, n_runs) bytes
+ * Other arguments and errors as ds_simulate.
+ */
+#define DS_SIM_MAX_RUNS 8
+ds_status ds_simulate_multi(uint32_t n_runs, uint32_t n, const double *arrival, const uint8_t *tier,
+                            const uint32_t *counts, const uint8_t *category, const uint32_t *tenant,
+                            const uint32_t *group, const uint32_t *observed, const double *t_base,
+                            uint32_t n_cat, const double *s_tenant, uint32_t n_tenants, uint32_t n_groups,
+                            const double *tick_t, uint32_t n_ticks, const ds_sim_params *params,
+                            double *const *state, uint32_t *const *seq, int32_t *const *tick_of,
+                            uint32_t *n_dispatched, void *ws, size_t ws_bytes, uint32_t flags,
+                            ds_stream stream);
 
 /*
  * Measurement aid: the practical HBM read rate of ds_characterize's access

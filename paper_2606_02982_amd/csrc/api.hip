@@ -11,6 +11,7 @@
 
 static_assert(DS_WRR_MAX_WEIGHT_SUM == ds::kWrrMaxWeightSum, "smooth round robin weight bound");
 static_assert(DS_READ_BW_WORDS == ds::kReadBwWords, "read-rate output words");
+static_assert(DS_SIM_MAX_RUNS == ds::kSimMaxRuns, "runs of one simulation launch");
 static_assert(DS_WRR_BLOCKED == ds::kWrrBlocked && DS_WRR_SMOOTH == ds::kWrrSmooth &&
                   DS_WRR_STRIDE == ds::kWrrStride,
               "weighted modes");
@@ -115,7 +116,9 @@ size_t ds_workspace_bytes(ds_op op_arg, uint64_t n, uint32_t n_groups)
     case DS_OP_ORDER_MULTI: return kFlagBytes + order_ws_bytes(n, 4);
     case DS_OP_ERROR_STATS: return kFlagBytes + err_ws_bytes(n, n_groups);
     case DS_OP_CLASS_HIST: return kFlagBytes;
-    case DS_OP_SIMULATE: return kFlagBytes + sim_ws_bytes(n);
+    case DS_OP_SIMULATE: return kFlagBytes + sim_ws_bytes(n, 1);
+    case DS_OP_SIMULATE_MULTI:
+        return n_groups >= 1 && n_groups <= DS_SIM_MAX_RUNS ? kFlagBytes + sim_ws_bytes(n, n_groups) : 0;
     }
     return 0;
 }
@@ -477,14 +480,10 @@ ds_status ds_class_histogram(uint32_t n, const uint8_t *category, uint32_t n_cat
     });
 }
 
-ds_status ds_simulate(uint32_t n, const double *arrival, const uint8_t *tier,
-                      const uint32_t *counts, const uint8_t *category, const uint32_t *tenant,
-                      const uint32_t *group, const uint32_t *observed, const double *t_base,
-                      uint32_t n_cat, const double *s_tenant, uint32_t n_tenants,
-                      uint32_t n_groups, const double *tick_t, uint32_t n_ticks,
-                      const ds_sim_params *params, double *state, uint32_t *seq,
-                      int32_t *tick_of, uint32_t *n_dispatched, void *ws, size_t ws_bytes,
-                      uint32_t flags, ds_stream stream)
+// Host checks of one run's parameters and outputs; fills a (shared inputs
+// set by the caller).
+static ds_status sim_run_args(const ds_sim_params *params, uint32_t n, double *state, uint32_t *seq,
+                              int32_t *tick_of, SimArgs &a)
 {
     if (!params) return DS_ERR_NULL;
     const int policy = enum_int(params->policy);
@@ -496,42 +495,12 @@ ds_status ds_simulate(uint32_t n, const double *arrival, const uint8_t *tier,
     op.t_now = 0.0;   // each tick ages to its own time
     ds_status st = check_order_params(&op, 1u << policy);
     if (st != DS_OK) return st;
-    if (n_cat == 0 || n_cat > 256 || n_tenants == 0 || n_groups == 0) return DS_ERR_ARG;
-    if (n > DS_MAX_ITEMS) return DS_ERR_SIZE;
-    if (n_ticks > 0x7FFFFFFFu) return DS_ERR_SIZE;
-    if (!n_dispatched) return DS_ERR_NULL;
-    if (n > 0 && (!arrival || !tier || !counts || !category || !tenant || !group || !observed ||
-                  !t_base || !s_tenant || !state || !seq || !tick_of || (n_ticks && !tick_t)))
-        return DS_ERR_NULL;
-    if (!aligned(n_dispatched, 4) || (arrival && !aligned(arrival, 8)) ||
-        (counts && !aligned(counts, 4)) || (tenant && !aligned(tenant, 4)) ||
-        (group && !aligned(group, 4)) || (observed && !aligned(observed, 4)) ||
-        (t_base && !aligned(t_base, 8)) || (s_tenant && !aligned(s_tenant, 8)) ||
-        (state && !aligned(state, 8)) || (seq && !aligned(seq, 4)) ||
-        (tick_of && !aligned(tick_of, 4)) || (tick_t && !aligned(tick_t, 8)))
+    if (n > 0 && (!state || !seq || !tick_of)) return DS_ERR_NULL;
+    if ((state && !aligned(state, 8)) || (seq && !aligned(seq, 4)) || (tick_of && !aligned(tick_of, 4)))
         return DS_ERR_ALIGN;
-    st = check_ws(ws, ws_bytes, ds_workspace_bytes(DS_OP_SIMULATE, n, 0));
-    if (st != DS_OK) return st;
-    SimArgs a;
-    memset(&a, 0, sizeof(a));
-    a.n = n;
-    a.n_groups = n_groups;
     a.policy = (uint32_t)policy;
     a.batch = params->batch;
-    a.n_ticks = n_ticks;
-    a.tick_t = tick_t;
     a.alpha = params->alpha;
-    a.arrival = arrival;
-    a.tier = tier;
-    a.counts = counts;
-    a.tenant = tenant;
-    a.group = group;
-    a.observed = observed;
-    a.category = category;
-    a.t_base = t_base;
-    a.s_tenant = s_tenant;
-    a.n_cat = n_cat;
-    a.n_tenants = n_tenants;
     a.f_ref = params->score.f_ref;
     a.n_tiers = params->order.n_tiers;
     for (uint32_t q = 0; q < DS_MAX_TIERS; q++) {
@@ -544,11 +513,92 @@ ds_status ds_simulate(uint32_t n, const double *arrival, const uint8_t *tier,
     a.state = state;
     a.seq = seq;
     a.tick_of = tick_of;
-    a.n_dispatched = n_dispatched;
+    return DS_OK;
+}
+
+static ds_status sim_common(uint32_t n_runs, uint32_t n, const double *arrival, const uint8_t *tier,
+                            const uint32_t *counts, const uint8_t *category, const uint32_t *tenant,
+                            const uint32_t *group, const uint32_t *observed, const double *t_base,
+                            uint32_t n_cat, const double *s_tenant, uint32_t n_tenants, uint32_t n_groups,
+                            const double *tick_t, uint32_t n_ticks, const ds_sim_params *params,
+                            double *const *state, uint32_t *const *seq, int32_t *const *tick_of,
+                            uint32_t *n_dispatched, void *ws, size_t ws_bytes, ds_op op, uint32_t flags,
+                            ds_stream stream)
+{
+    if (n_runs < 1 || n_runs > DS_SIM_MAX_RUNS) return DS_ERR_ARG;
+    if (!params || !state || !seq || !tick_of) return DS_ERR_NULL;
+    SimArgs runs[DS_SIM_MAX_RUNS];
+    memset(runs, 0, sizeof(runs));
+    for (uint32_t r = 0; r < n_runs; r++) {
+        ds_status st = sim_run_args(params + r, n, state[r], seq[r], tick_of[r], runs[r]);
+        if (st != DS_OK) return st;
+    }
+    if (n_cat == 0 || n_cat > 256 || n_tenants == 0 || n_groups == 0) return DS_ERR_ARG;
+    if (n > DS_MAX_ITEMS) return DS_ERR_SIZE;
+    if (n_ticks > 0x7FFFFFFFu) return DS_ERR_SIZE;
+    if (!n_dispatched) return DS_ERR_NULL;
+    if (n > 0 && (!arrival || !tier || !counts || !category || !tenant || !group || !observed ||
+                  !t_base || !s_tenant || (n_ticks && !tick_t)))
+        return DS_ERR_NULL;
+    if (!aligned(n_dispatched, 4) || (arrival && !aligned(arrival, 8)) ||
+        (counts && !aligned(counts, 4)) || (tenant && !aligned(tenant, 4)) ||
+        (group && !aligned(group, 4)) || (observed && !aligned(observed, 4)) ||
+        (t_base && !aligned(t_base, 8)) || (s_tenant && !aligned(s_tenant, 8)) ||
+        (tick_t && !aligned(tick_t, 8)))
+        return DS_ERR_ALIGN;
+    ds_status st = check_ws(ws, ws_bytes, ds_workspace_bytes(op, n, op == DS_OP_SIMULATE ? 0 : n_runs));
+    if (st != DS_OK) return st;
+    for (uint32_t r = 0; r < n_runs; r++) {
+        SimArgs &a = runs[r];
+        a.n = n;
+        a.n_groups = n_groups;
+        a.n_ticks = n_ticks;
+        a.tick_t = tick_t;
+        a.arrival = arrival;
+        a.tier = tier;
+        a.counts = counts;
+        a.tenant = tenant;
+        a.group = group;
+        a.observed = observed;
+        a.category = category;
+        a.t_base = t_base;
+        a.s_tenant = s_tenant;
+        a.n_cat = n_cat;
+        a.n_tenants = n_tenants;
+        a.n_dispatched = n_dispatched + r;
+    }
     hipStream_t s = static_cast<hipStream_t>(stream);
     return run_waits(ws, flags, s, [&](uint32_t *flag) {
-        return sim_launch(a, after_flag(ws), flag, s, wait_cfg(ws, flags));
+        return sim_launch(runs, n_runs, after_flag(ws), flag, s, wait_cfg(ws, flags));
     });
+}
+
+ds_status ds_simulate(uint32_t n, const double *arrival, const uint8_t *tier,
+                      const uint32_t *counts, const uint8_t *category, const uint32_t *tenant,
+                      const uint32_t *group, const uint32_t *observed, const double *t_base,
+                      uint32_t n_cat, const double *s_tenant, uint32_t n_tenants,
+                      uint32_t n_groups, const double *tick_t, uint32_t n_ticks,
+                      const ds_sim_params *params, double *state, uint32_t *seq,
+                      int32_t *tick_of, uint32_t *n_dispatched, void *ws, size_t ws_bytes,
+                      uint32_t flags, ds_stream stream)
+{
+    return sim_common(1, n, arrival, tier, counts, category, tenant, group, observed, t_base, n_cat, s_tenant,
+                      n_tenants, n_groups, tick_t, n_ticks, params, &state, &seq, &tick_of, n_dispatched, ws,
+                      ws_bytes, DS_OP_SIMULATE, flags, stream);
+}
+
+ds_status ds_simulate_multi(uint32_t n_runs, uint32_t n, const double *arrival, const uint8_t *tier,
+                            const uint32_t *counts, const uint8_t *category, const uint32_t *tenant,
+                            const uint32_t *group, const uint32_t *observed, const double *t_base,
+                            uint32_t n_cat, const double *s_tenant, uint32_t n_tenants, uint32_t n_groups,
+                            const double *tick_t, uint32_t n_ticks, const ds_sim_params *params,
+                            double *const *state, uint32_t *const *seq, int32_t *const *tick_of,
+                            uint32_t *n_dispatched, void *ws, size_t ws_bytes, uint32_t flags,
+                            ds_stream stream)
+{
+    return sim_common(n_runs, n, arrival, tier, counts, category, tenant, group, observed, t_base, n_cat,
+                      s_tenant, n_tenants, n_groups, tick_t, n_ticks, params, state, seq, tick_of, n_dispatched,
+                      ws, ws_bytes, DS_OP_SIMULATE_MULTI, flags, stream);
 }
 
 ds_status ds_read_bandwidth(const void *buf, uint64_t bytes, uint32_t *xor_out, ds_stream stream)

@@ -192,8 +192,11 @@ struct SimArgs {
     uint32_t *n_dispatched;
 };
 constexpr uint32_t kSimMaxBatch = 1024;
-size_t sim_ws_bytes(uint64_t n);
-hipError_t sim_launch(const SimArgs &a, void *ws, uint32_t *flag, hipStream_t s,
+constexpr uint32_t kSimMaxRuns = 8;
+size_t sim_ws_bytes(uint64_t n, uint32_t n_runs);
+// n_runs runs sharing every input array, the ticks and n (their parameters
+// and outputs may differ; run r's n_dispatched is runs[0].n_dispatched + r).
+hipError_t sim_launch(const SimArgs *runs, uint32_t n_runs, void *ws, uint32_t *flag, hipStream_t s,
                       WaitCfg wait = {});
 
 // ---- misc --------------------------------------------------------------------------

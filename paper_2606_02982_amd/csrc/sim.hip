@@ -14,8 +14,9 @@
 // order before the next tick.
 //
 // The loop is sequential across ticks and each tick needs only the first
-// `batch` requests of the order, so one workgroup runs every tick in a
-// single launch:
+// `batch` requests of the order, so one workgroup runs every tick of a run
+// in a single launch (several runs, e.g. the five policies, are blocks of
+// the same launch, after one shared FIFO sort):
 //   * the pending set is a list in FIFO order: arrivals join its end (they
 //     come after every pending request in FIFO order) and the previous
 //     tick's dispatches are compacted out in the same pass that computes
@@ -30,6 +31,8 @@
 //   * the EMA updates of a batch run per group in parallel, each group's
 //     events in dispatch order, so the factors are bit-identical to a
 //     sequential evaluation.
+#include <string.h>
+
 #include "common.h"
 #include "kernels.h"
 #include "wrrplan.h"
@@ -86,8 +89,19 @@ struct EngineArgs {
     uint32_t *n_dispatched;
 };
 
-__global__ void k_sim_setup(SetupArgs a)
+// Several runs share one launch: run r is block row r of the setup and block
+// r of the engine.
+struct SetupBatch {
+    SetupArgs r[kSimMaxRuns];
+};
+struct EngineBatch {
+    EngineArgs r[kSimMaxRuns];
+};
+static_assert(sizeof(SetupBatch) <= 4096 && sizeof(EngineBatch) <= 4096, "kernel arguments within 4 KB");
+
+__global__ void k_sim_setup(SetupBatch sb)
 {
+    const SetupArgs &a = sb.r[blockIdx.y];
     if (a.wait_status && blockIdx.x == 0 && threadIdx.x == 0) *a.wait_status = 0;
     const double nan = __builtin_nan("");
     for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < a.n; i += gridDim.x * blockDim.x) {
@@ -166,8 +180,9 @@ __device__ __forceinline__ uint32_t pair_digit(uint64_t K, uint32_t J, int d)
     return d >= 4 ? (uint32_t)(K >> (8 * (d - 4))) & 255u : (J >> (8 * d)) & 255u;
 }
 
-__global__ __launch_bounds__(kTPB) void k_sim_engine(EngineArgs a)
+__global__ __launch_bounds__(kTPB) void k_sim_engine(EngineBatch eb)
 {
+    const EngineArgs &a = eb.r[blockIdx.x];
     __shared__ uint32_t s_w[kNW];
     __shared__ uint32_t s_hist[256];
     __shared__ uint32_t s_vw[kNW][kMaxQ];
@@ -513,9 +528,9 @@ __global__ __launch_bounds__(kTPB) void k_sim_engine(EngineArgs a)
     if (tid == 0) a.n_dispatched[0] = total;
 }
 
-__global__ void k_sim_empty(uint32_t *__restrict__ n_dispatched)
+__global__ void k_sim_empty(uint32_t *__restrict__ n_dispatched, uint32_t n_runs)
 {
-    if (threadIdx.x == 0) n_dispatched[0] = 0;
+    if (threadIdx.x < n_runs) n_dispatched[threadIdx.x] = 0;
 }
 
 __global__ void k_sim_validate(const SimArgs a, uint32_t *__restrict__ flag)
@@ -542,23 +557,31 @@ uint32_t grid_for(uint64_t n)
 
 }  // namespace
 
-size_t sim_ws_bytes(uint64_t n)
+size_t sim_ws_bytes(uint64_t n, uint32_t n_runs)
 {
-    // fifo, list x2, est_base, key, aux, val, then the FIFO sort
-    return 3 * align_up(n * 4, 256) + 2 * align_up(n * 8, 256) + align_up(n * sizeof(Aux), 256) +
-           align_up(n, 256) + sort_ws_bytes(n, 1);
+    // shared: fifo, then the FIFO sort; per run: list x2, est_base, key, aux, val
+    const uint64_t per = 2 * align_up(n * 4, 256) + 2 * align_up(n * 8, 256) +
+                         align_up(n * sizeof(Aux), 256) + align_up(n, 256);
+    return align_up(n * 4, 256) + (uint64_t)(n_runs ? n_runs : 1) * per + sort_ws_bytes(n, 1);
 }
 
-hipError_t sim_launch(const SimArgs &a, void *ws, uint32_t *flag, hipStream_t s, WaitCfg wait)
+hipError_t sim_launch(const SimArgs *runs, uint32_t n_runs, void *ws, uint32_t *flag, hipStream_t s,
+                      WaitCfg wait)
 {
-    const uint32_t n = a.n;
+    if (n_runs < 1 || n_runs > kSimMaxRuns) return hipErrorInvalidValue;
+    const SimArgs &a0 = runs[0];
+    const uint32_t n = a0.n;
     if (flag) {
-        hipLaunchKernelGGL(k_sim_validate, dim3(grid_for(n > a.n_ticks ? n : a.n_ticks)), dim3(256),
-                           0, s, a, flag);
+        // the shared inputs, against the smallest tier count of the runs
+        SimArgs v = a0;
+        for (uint32_t r = 1; r < n_runs; r++) v.n_tiers = runs[r].n_tiers < v.n_tiers ? runs[r].n_tiers : v.n_tiers;
+        hipLaunchKernelGGL(k_sim_validate, dim3(grid_for(n > v.n_ticks ? n : v.n_ticks)), dim3(256),
+                           0, s, v, flag);
         return hipGetLastError();
     }
     if (n == 0) {
-        hipLaunchKernelGGL(k_sim_empty, dim3(1), dim3(64), 0, s, a.n_dispatched);
+        // the runs' counters are one array (n_dispatched of run r = runs[0].n_dispatched + r)
+        hipLaunchKernelGGL(k_sim_empty, dim3(1), dim3(64), 0, s, a0.n_dispatched, n_runs);
         return hipGetLastError();
     }
     uint8_t *p = static_cast<uint8_t *>(ws);
@@ -568,85 +591,92 @@ hipError_t sim_launch(const SimArgs &a, void *ws, uint32_t *flag, hipStream_t s,
         return q;
     };
     uint32_t *fifo = reinterpret_cast<uint32_t *>(take((uint64_t)n * 4));
-    uint32_t *list0 = reinterpret_cast<uint32_t *>(take((uint64_t)n * 4));
-    uint32_t *list1 = reinterpret_cast<uint32_t *>(take((uint64_t)n * 4));
-    double *est_base = reinterpret_cast<double *>(take((uint64_t)n * 8));
-    uint64_t *key = reinterpret_cast<uint64_t *>(take((uint64_t)n * 8));
-    Aux *aux = reinterpret_cast<Aux *>(take((uint64_t)n * sizeof(Aux)));
-    uint8_t *val = take(n);
-    void *sort_ws = p;
+    SetupBatch sb;
+    EngineBatch eb;
+    memset(&sb, 0, sizeof(sb));
+    memset(&eb, 0, sizeof(eb));
+    for (uint32_t r = 0; r < n_runs; r++) {
+        const SimArgs &a = runs[r];
+        uint32_t *list0 = reinterpret_cast<uint32_t *>(take((uint64_t)n * 4));
+        uint32_t *list1 = reinterpret_cast<uint32_t *>(take((uint64_t)n * 4));
+        double *est_base = reinterpret_cast<double *>(take((uint64_t)n * 8));
+        uint64_t *key = reinterpret_cast<uint64_t *>(take((uint64_t)n * 8));
+        Aux *aux = reinterpret_cast<Aux *>(take((uint64_t)n * sizeof(Aux)));
+        uint8_t *val = take(n);
 
-    SetupArgs su = {};
-    su.n = n;
-    su.policy = a.policy;
-    su.n_cat = a.n_cat;
-    su.n_tenants = a.n_tenants;
-    su.n_tiers = a.n_tiers;
-    su.counts = a.counts;
-    su.tenant = a.tenant;
-    su.category = a.category;
-    su.tier = a.tier;
-    su.t_base = a.t_base;
-    su.s_tenant = a.s_tenant;
-    su.arrival = a.arrival;
-    su.f_ref = a.f_ref;
-    // priority classes: rank of each tier's priority among the distinct values
-    for (uint32_t q = 0; q < kMaxQ; q++) {
-        su.prio[q] = a.prio[q];
-        uint32_t c = 0;
-        if (q < a.n_tiers)
-            for (uint32_t u = 0; u < a.n_tiers; u++) {
-                bool first = true;   // count each distinct smaller value once
-                for (uint32_t v = 0; v < u; v++) first = first && a.prio[v] != a.prio[u];
-                if (first && a.prio[u] < a.prio[q]) c++;
-            }
-        su.cls[q] = c;
+        SetupArgs &su = sb.r[r];
+        su.n = n;
+        su.policy = a.policy;
+        su.n_cat = a.n_cat;
+        su.n_tenants = a.n_tenants;
+        su.n_tiers = a.n_tiers;
+        su.counts = a.counts;
+        su.tenant = a.tenant;
+        su.category = a.category;
+        su.tier = a.tier;
+        su.t_base = a.t_base;
+        su.s_tenant = a.s_tenant;
+        su.arrival = a.arrival;
+        su.f_ref = a.f_ref;
+        // priority classes: rank of each tier's priority among the distinct values
+        for (uint32_t q = 0; q < kMaxQ; q++) {
+            su.prio[q] = a.prio[q];
+            uint32_t c = 0;
+            if (q < a.n_tiers)
+                for (uint32_t u = 0; u < a.n_tiers; u++) {
+                    bool first = true;   // count each distinct smaller value once
+                    for (uint32_t v = 0; v < u; v++) first = first && a.prio[v] != a.prio[u];
+                    if (first && a.prio[u] < a.prio[q]) c++;
+                }
+            su.cls[q] = c;
+        }
+        su.est_base = est_base;
+        su.aux = aux;
+        su.val = val;
+        su.seq = a.seq;
+        su.tick_of = a.tick_of;
+        su.wait_status = r == 0 && wait.clear ? wait.status : nullptr;
+
+        EngineArgs &ea = eb.r[r];
+        ea.n = n;
+        ea.n_groups = a.n_groups;
+        ea.policy = a.policy;
+        ea.batch = a.batch;
+        ea.n_ticks = a.n_ticks;
+        ea.n_q = a.n_tiers;
+        ea.tick_t = a.tick_t;
+        ea.fifo = fifo;
+        ea.arrival = a.arrival;
+        ea.group = a.group;
+        ea.observed = a.observed;
+        ea.est_base = est_base;
+        ea.aux = aux;
+        ea.val = val;
+        for (uint32_t q = 0; q < kMaxQ; q++) ea.weight[q] = q < a.n_tiers && a.weight[q] ? a.weight[q] : 1u;
+        ea.wrr_mode = a.wrr_mode;
+        ea.alpha = a.alpha;
+        ea.aging_rate = a.aging_rate;
+        ea.aging_floor = a.aging_floor;
+        ea.state = a.state;
+        ea.list[0] = list0;
+        ea.list[1] = list1;
+        ea.key = key;
+        ea.seq = a.seq;
+        ea.tick_of = a.tick_of;
+        ea.n_dispatched = a.n_dispatched;
     }
-    su.est_base = est_base;
-    su.aux = aux;
-    su.val = val;
-    su.seq = a.seq;
-    su.tick_of = a.tick_of;
-    su.wait_status = wait.clear ? wait.status : nullptr;
-    hipLaunchKernelGGL(k_sim_setup, dim3(grid_for(n)), dim3(256), 0, s, su);
+    void *sort_ws = p;
+    hipLaunchKernelGGL(k_sim_setup, dim3(grid_for(n), n_runs), dim3(256), 0, s, sb);
 
     SortInput in = {};
     in.n = n;
-    in.arrival = a.arrival;
+    in.arrival = a0.arrival;
     in.wait = wait;
     in.wait.clear = false;
     SortJob job = {SortKind::Fifo, 64, nullptr, fifo};
     hipError_t e = sort_launch(in, &job, 1, sort_ws, s);
     if (e != hipSuccess) return e;
-
-    EngineArgs ea = {};
-    ea.n = n;
-    ea.n_groups = a.n_groups;
-    ea.policy = a.policy;
-    ea.batch = a.batch;
-    ea.n_ticks = a.n_ticks;
-    ea.n_q = a.n_tiers;
-    ea.tick_t = a.tick_t;
-    ea.fifo = fifo;
-    ea.arrival = a.arrival;
-    ea.group = a.group;
-    ea.observed = a.observed;
-    ea.est_base = est_base;
-    ea.aux = aux;
-    ea.val = val;
-    for (uint32_t q = 0; q < kMaxQ; q++) ea.weight[q] = q < a.n_tiers && a.weight[q] ? a.weight[q] : 1u;
-    ea.wrr_mode = a.wrr_mode;
-    ea.alpha = a.alpha;
-    ea.aging_rate = a.aging_rate;
-    ea.aging_floor = a.aging_floor;
-    ea.state = a.state;
-    ea.list[0] = list0;
-    ea.list[1] = list1;
-    ea.key = key;
-    ea.seq = a.seq;
-    ea.tick_of = a.tick_of;
-    ea.n_dispatched = a.n_dispatched;
-    hipLaunchKernelGGL(k_sim_engine, dim3(1), dim3(kTPB), 0, s, ea);
+    hipLaunchKernelGGL(k_sim_engine, dim3(n_runs), dim3(kTPB), 0, s, eb);
     return hipGetLastError();
 }
 

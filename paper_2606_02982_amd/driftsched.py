@@ -20,7 +20,8 @@ LIB_PATH = os.path.join(HERE, "libdriftsched.so")
 FIFO, PRIORITY, WEIGHTED, SJF, AGING = 0, 1, 2, 3, 4
 POLICIES = {"fifo": FIFO, "priority": PRIORITY, "weighted": WEIGHTED, "sjf": SJF, "aging": AGING}
 OP_CHARACTERIZE, OP_CALIBRATE, OP_SCORE, OP_ORDER, OP_ORDER_MULTI = 0, 1, 2, 3, 4
-OP_ERROR_STATS, OP_CLASS_HIST, OP_SIMULATE = 5, 6, 7
+OP_ERROR_STATS, OP_CLASS_HIST, OP_SIMULATE, OP_SIMULATE_MULTI = 5, 6, 7, 8
+SIM_MAX_RUNS = 8
 DS_VALIDATE = 1
 DS_SERIAL_SORT = 2
 DS_NO_WAIT = 4          # diagnostic: bounded device-side waits give up at once
@@ -79,9 +80,13 @@ def _load():
                                    ctypes.POINTER(P), ctypes.POINTER(P), P, sz, u32, P]
     lib.ds_simulate.argtypes = [u32, P, P, P, P, P, P, P, P, u32, P, u32, u32, P, u32,
                                 ctypes.POINTER(SimParams), P, P, P, P, P, sz, u32, P]
+    lib.ds_simulate_multi.argtypes = [u32, u32, P, P, P, P, P, P, P, P, u32, P, u32, u32, P, u32,
+                                      ctypes.POINTER(SimParams), ctypes.POINTER(P), ctypes.POINTER(P),
+                                      ctypes.POINTER(P), P, P, sz, u32, P]
     for f in (lib.ds_characterize, lib.ds_characterize_score, lib.ds_characterize_score_noalloc,
               lib.ds_calibrate, lib.ds_calibrate_ex, lib.ds_score, lib.ds_order,
-              lib.ds_order_multi, lib.ds_error_stats, lib.ds_class_histogram, lib.ds_simulate):
+              lib.ds_order_multi, lib.ds_error_stats, lib.ds_class_histogram, lib.ds_simulate,
+              lib.ds_simulate_multi):
         f.restype = i32
     lib.ds_workspace_bytes.argtypes = [i32, u64, u32]
     lib.ds_workspace_bytes.restype = sz
@@ -487,3 +492,40 @@ def simulate(arrival, tier, counts, category, tenant, group, observed, t_base, s
                            _ptr(seq), _ptr(tick_of), _ptr(nd), _ptr(ws), ws.numel(),
                            _flags(validate), _stream()))
     return seq, tick_of, nd
+
+
+def simulate_multi(arrival, tier, counts, category, tenant, group, observed, t_base, s_tenant,
+                   states, tick_t, params, ws=None, validate=False):
+    """Several dispatch-tick loops in one launch (ds_simulate_multi): run r
+    uses params[r] and updates states[r] in place. Returns a list of
+    (seq, tick_of) per run and the n_dispatched tensor (one int32 per run)."""
+    for t, dt, name in ((arrival, torch.float64, "arrival"), (tier, torch.uint8, "tier"),
+                        (counts, torch.int32, "counts"), (category, torch.uint8, "category"),
+                        (tenant, torch.int32, "tenant"), (group, torch.int32, "group"),
+                        (observed, torch.int32, "observed"), (t_base, torch.float64, "t_base"),
+                        (s_tenant, torch.float64, "s_tenant"), (tick_t, torch.float64, "tick_t")):
+        _dev(t, dt, name)
+    R = len(params)
+    if R != len(states):
+        raise ValueError("one state per run")
+    for st in states:
+        _dev(st, torch.float64, "state")
+    n = arrival.numel()
+    dev = arrival.device
+    outs = [(torch.empty(n, dtype=torch.int32, device=dev), torch.empty(n, dtype=torch.int32, device=dev))
+            for _ in range(R)]
+    nd = torch.empty(R, dtype=torch.int32, device=dev)
+    if ws is None:
+        ws = workspace(OP_SIMULATE_MULTI, n, R, dev)
+    P = ctypes.c_void_p
+    pa = (SimParams * R)(*params)
+    st_p = (P * R)(*[st.data_ptr() for st in states])
+    sq_p = (P * R)(*[o[0].data_ptr() for o in outs])
+    tk_p = (P * R)(*[o[1].data_ptr() for o in outs])
+    n_groups = states[0].numel() if states else 1
+    _check(lib.ds_simulate_multi(R, n, _ptr(arrival), _ptr(tier), _ptr(counts), _ptr(category),
+                                 _ptr(tenant), _ptr(group), _ptr(observed), _ptr(t_base),
+                                 t_base.numel(), _ptr(s_tenant), s_tenant.numel(), n_groups,
+                                 _ptr(tick_t), tick_t.numel(), pa, st_p, sq_p, tk_p, _ptr(nd),
+                                 _ptr(ws), ws.numel(), _flags(validate), _stream()))
+    return outs, nd

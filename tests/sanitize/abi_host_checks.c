@@ -134,6 +134,32 @@ int main(void)
     EXPECT(ds_simulate(10, p, p, p, p, p, p, p, p, 4, p, 3, 2, p, 5, NULL, p, p, p, p, p, 1 << 24, 0, NULL),
            DS_ERR_NULL);
 
+    {
+        ds_sim_params runs[2];
+        runs[0] = sim;
+        runs[1] = sim;
+        double *st[2] = {p, p};
+        uint32_t *sq[2] = {p, p};
+        int32_t *tk[2] = {p, p};
+        EXPECT(ds_simulate_multi(0, 10, p, p, p, p, p, p, p, p, 4, p, 3, 2, p, 5, runs, st, sq, tk, p, p, 1 << 26,
+                                 0, NULL),
+               DS_ERR_ARG);
+        EXPECT(ds_simulate_multi(DS_SIM_MAX_RUNS + 1, 10, p, p, p, p, p, p, p, p, 4, p, 3, 2, p, 5, runs, st, sq,
+                                 tk, p, p, 1 << 26, 0, NULL),
+               DS_ERR_ARG);
+        runs[1].batch = 0;
+        EXPECT(ds_simulate_multi(2, 10, p, p, p, p, p, p, p, p, 4, p, 3, 2, p, 5, runs, st, sq, tk, p, p, 1 << 26,
+                                 0, NULL),
+               DS_ERR_ARG);
+        runs[1].batch = 32;
+        EXPECT(ds_simulate_multi(2, 10, p, p, p, p, p, p, p, p, 4, p, 3, 2, p, 5, runs, st, sq, tk, p, p, 64, 0,
+                                 NULL),
+               DS_ERR_WORKSPACE);
+        EXPECT(ds_simulate_multi(2, 10, p, p, p, p, p, p, p, p, 4, p, 3, 2, p, 5, NULL, st, sq, tk, p, p, 1 << 26, 0,
+                                 NULL),
+               DS_ERR_NULL);
+    }
+
     EXPECT(ds_read_bandwidth(odd, 16, p, NULL), DS_ERR_ALIGN);
     EXPECT(ds_read_bandwidth(p, 15, p, NULL), DS_ERR_ARG);
 

@@ -27,7 +27,7 @@ def test_exports_every_declared_symbol(ds):
     names = declared_functions()
     assert names == ["ds_calibrate", "ds_calibrate_ex", "ds_characterize", "ds_characterize_score",
                      "ds_characterize_score_noalloc", "ds_class_histogram", "ds_error_stats", "ds_order", "ds_order_multi",
-                     "ds_read_bandwidth", "ds_score", "ds_simulate", "ds_status_string", "ds_version",
+                     "ds_read_bandwidth", "ds_score", "ds_simulate", "ds_simulate_multi", "ds_status_string", "ds_version",
                      "ds_workspace_bytes"]
     for name in names:
         assert hasattr(ds.lib, name), name
@@ -50,6 +50,12 @@ def test_workspace_sizes(ds):
     assert ds.workspace_bytes(ds.OP_CLASS_HIST, 1 << 20) == 256
     # error statistics: sums for every group and for all events
     assert ds.workspace_bytes(ds.OP_ERROR_STATS, 10, 7) >= 256 + 4 * 8 * 8
+    # several tick loops: the third argument is the number of runs (1..8)
+    for n in (1, 4096, 65536):
+        assert ds.workspace_bytes(ds.OP_SIMULATE_MULTI, n, 1) == ds.workspace_bytes(ds.OP_SIMULATE, n)
+        assert ds.workspace_bytes(ds.OP_SIMULATE_MULTI, n, 8) > ds.workspace_bytes(ds.OP_SIMULATE_MULTI, n, 2)
+        assert ds.workspace_bytes(ds.OP_SIMULATE_MULTI, n, 0) == 0
+        assert ds.workspace_bytes(ds.OP_SIMULATE_MULTI, n, 9) == 0
 
 
 P = ctypes.c_void_p

@@ -197,3 +197,60 @@ def test_synthetic_workload(ds, oracle, policy):
                      batch=32, alpha=0.1, weights=tuple(b.weights),
                      tier_priority=tuple(b.tier_priority), aging_rate=b.aging_rate)
     assert len(seq) == b.n
+
+
+@pytest.mark.parametrize("case", ["random", "workload"])
+def test_multi_runs_in_one_launch(ds, oracle, case):
+    """ds_simulate_multi: the five policies, the smooth and stride Weighted and
+    SJF at a second EMA weight (8 runs) in one launch; each run equals the
+    oracle's loop for its parameters."""
+    import torch
+    if case == "random":
+        x = random_inputs(77, 3000)
+        ticks = np.linspace(0.05, 12.0, 240)
+        kw = dict(weights=(3, 2, 1), tier_priority=(0.0, 1.0, 2.0), aging_rate=0.3)
+    else:
+        b = wl.load("batch64k", n=20000, with_text=False)
+        x = dict(arrival=b.arrival, tier=b.tier, counts=b.words, category=b.category, tenant=b.tenant,
+                 group=b.group, observed=b.observed, t_base=b.t_base, s_tenant=b.s_tenant,
+                 state=np.ones(b.n_groups))
+        ticks = synth.sim_ticks(b.arrival)
+        kw = dict(weights=tuple(int(w) for w in b.weights), tier_priority=tuple(b.tier_priority),
+                  aging_rate=b.aging_rate)
+    runs = [(p, 0.1, "blocked") for p in ALL] + [(WEIGHTED, 0.1, "smooth"), (WEIGHTED, 0.1, "stride"),
+                                                (SJF, 0.25, "blocked")]
+    params = [ds.sim_params(p, batch=32, alpha=a, n_tiers=len(kw["weights"]), weighted_mode=m, **kw)
+              for p, a, m in runs]
+    states = [dev(np.asarray(x["state"], np.float64).copy()) for _ in runs]
+    print("simulate_multi %s: %d runs, n=%d, ticks=%d" % (case, len(runs), len(x["arrival"]), len(ticks)),
+          flush=True)
+    d = {k: dev(np.asarray(v)) for k, v in x.items() if k != "state"}
+    outs, nd = ds.simulate_multi(d["arrival"], d["tier"], d["counts"], d["category"], d["tenant"],
+                                 d["group"], d["observed"], d["t_base"], d["s_tenant"], states,
+                                 dev(np.asarray(ticks, np.float64)), params)
+    torch.cuda.synchronize()
+    nd = host(nd)
+    oracle_policy = {"blocked": None, "smooth": 5, "stride": 6}
+    for r, (p, a, m) in enumerate(runs):
+        op = oracle_policy[m] if p == WEIGHTED and oracle_policy[m] else p
+        w_seq, w_tick, w_state = oracle.simulate(op, x["arrival"], x["tier"], x["counts"], x["category"],
+                                                 x["tenant"], x["group"], x["observed"], x["t_base"],
+                                                 x["s_tenant"], x["state"], ticks, batch=32, alpha=a, **kw)
+        assert int(nd[r]) == len(w_seq), "run %d" % r
+        seq = host(outs[r][0], np.uint32)
+        assert np.array_equal(seq[:nd[r]], w_seq), "run %d" % r
+        assert np.array_equal(host(outs[r][1]), w_tick), "run %d" % r
+        assert np.array_equal(host(states[r]), w_state), "run %d" % r
+
+
+def test_multi_host_errors(ds):
+    x = random_inputs(5, 10)
+    d = {k: dev(np.asarray(v)) for k, v in x.items() if k != "state"}
+    p = ds.sim_params(FIFO)
+    for R in (0, 9):
+        with pytest.raises(ds.DriftSchedError) as e:
+            ds.simulate_multi(d["arrival"], d["tier"], d["counts"], d["category"], d["tenant"],
+                              d["group"], d["observed"], d["t_base"], d["s_tenant"],
+                              [dev(x["state"].copy()) for _ in range(R)], dev(np.array([1.0])), [p] * R,
+                              ws=ds.workspace(ds.OP_SIMULATE_MULTI, 10, 8))
+        assert e.value.status == -2
