@@ -103,27 +103,46 @@ __global__ __launch_bounds__(kAmTPB) void k_am_count(AmArgs a)
     if (t < kAmCls) a.cnt[tile * kAmCls + t] = c[t];
 }
 
-// Wave w scans class w over the tiles; then each class's start is added.
+// Wave w handles class w: its total over the tiles first, then (with every
+// class's total known, so with the class's start) the exclusive scan over
+// the tiles. Each lane takes contiguous runs of 16 tiles, all their loads in
+// flight together.
 __global__ __launch_bounds__(1024) void k_am_scan(AmArgs a)
 {
+    constexpr uint32_t kPer = 16;   // tiles per lane and step
     __shared__ uint32_t tot[kAmCls];
     const uint32_t w = threadIdx.x >> 6;
     const int lane = lane_id();
+    uint32_t sum = 0;
+    for (uint32_t t0 = 0; t0 < a.tiles; t0 += 64 * kPer) {
+        const uint32_t tl0 = t0 + (uint32_t)lane * kPer;
+#pragma unroll
+        for (uint32_t k = 0; k < kPer; k++) sum += tl0 + k < a.tiles ? a.cnt[(tl0 + k) * kAmCls + w] : 0u;
+    }
+    sum = wave_sum(sum);
+    if (lane == 0) tot[w] = sum;
+    __syncthreads();
     uint32_t run = 0;
-    for (uint32_t t0 = 0; t0 < a.tiles; t0 += 64) {
-        const uint32_t tl = t0 + (uint32_t)lane;
-        const uint32_t x = tl < a.tiles ? a.cnt[tl * kAmCls + w] : 0u;
-        const uint32_t incl = wave_incl_scan_dpp(x);
-        if (tl < a.tiles) a.cnt[tl * kAmCls + w] = run + incl - x;
+    for (uint32_t k = 0; k < w; k++) run += tot[k];
+    if (lane == 0) a.cstart[w] = run;
+    if (threadIdx.x == 0) a.cstart[kAmCls] = a.n;
+    for (uint32_t t0 = 0; t0 < a.tiles; t0 += 64 * kPer) {
+        const uint32_t tl0 = t0 + (uint32_t)lane * kPer;
+        uint32_t x[kPer];
+#pragma unroll
+        for (uint32_t k = 0; k < kPer; k++) x[k] = tl0 + k < a.tiles ? a.cnt[(tl0 + k) * kAmCls + w] : 0u;
+        uint32_t part = 0;
+#pragma unroll
+        for (uint32_t k = 0; k < kPer; k++) part += x[k];
+        const uint32_t incl = wave_incl_scan_dpp(part);
+        uint32_t ex = run + incl - part;
+#pragma unroll
+        for (uint32_t k = 0; k < kPer; k++) {
+            if (tl0 + k < a.tiles) a.cnt[(tl0 + k) * kAmCls + w] = ex;
+            ex += x[k];
+        }
         run += readlane32(incl, 63);
     }
-    if (lane == 0) tot[w] = run;
-    __syncthreads();
-    uint32_t start = 0;
-    for (uint32_t k = 0; k < w; k++) start += tot[k];
-    for (uint32_t tl = (uint32_t)lane; tl < a.tiles; tl += 64) a.cnt[tl * kAmCls + w] += start;
-    if (lane == 0) a.cstart[w] = start;
-    if (threadIdx.x == 0) a.cstart[kAmCls] = a.n;
 }
 
 __global__ __launch_bounds__(kAmTPB) void k_am_place(AmArgs a)
