@@ -22,6 +22,8 @@
 // Results are identical to sorting by (score, arrival, index): the scores
 // are computed with the same operations as the other paths, and FIFO
 // position order is (arrival, index) order.
+#include <string.h>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -313,6 +315,35 @@ __global__ __launch_bounds__(kMgTPB) void k_am_merge(AmArgs a, uint32_t span, ui
 }
 
 }  // namespace
+
+size_t am_partition_ws_bytes(uint64_t n)
+{
+    const uint64_t tiles = cdiv(n ? n : 1, kAmTile);
+    return align_up(tiles * kAmCls * 4, 256) + align_up(n * 8, 256);
+}
+
+hipError_t am_partition(const SortInput &in, uint32_t *run_pos, uint32_t *run_start, void *ws, hipStream_t s)
+{
+    const uint32_t n = in.n;
+    if (n == 0) return hipSuccess;
+    if (n > kAmMaxN || !in.fifo) return hipErrorInvalidValue;
+    AmArgs a;
+    memset(&a, 0, sizeof(a));
+    a.in = in;
+    a.n = n;
+    a.tiles = (uint32_t)cdiv(n, kAmTile);
+    a.K = kAmCls;
+    uint8_t *p = static_cast<uint8_t *>(ws);
+    a.cnt = reinterpret_cast<uint32_t *>(p);
+    p += align_up((uint64_t)a.tiles * kAmCls * 4, 256);
+    a.rk[0] = reinterpret_cast<uint64_t *>(p);   // the scores are not used here
+    a.rp[0] = run_pos;
+    a.cstart = run_start;
+    hipLaunchKernelGGL(k_am_count, dim3(a.tiles), dim3(kAmTPB), 0, s, a);
+    hipLaunchKernelGGL(k_am_scan, dim3(1), dim3(1024), 0, s, a);
+    hipLaunchKernelGGL(k_am_place, dim3(a.tiles), dim3(kAmTPB), 0, s, a);
+    return hipGetLastError();
+}
 
 size_t am_ws_bytes(uint64_t n)
 {

@@ -116,6 +116,11 @@ constexpr uint32_t kAmMaxN = 1u << 24;
 size_t am_ws_bytes(uint64_t n);
 hipError_t am_launch(const SortInput &in, uint32_t n_classes, uint32_t *perm, double *key_out, void *ws,
                      hipStream_t s, uint32_t *wait_status);
+// The stable partition of the FIFO sequence by in.cls[tier] alone (16
+// classes): run_pos (n) receives the FIFO positions class by class, each
+// class in FIFO order, run_start (17) each class's first entry and n.
+size_t am_partition_ws_bytes(uint64_t n);
+hipError_t am_partition(const SortInput &in, uint32_t *run_pos, uint32_t *run_start, void *ws, hipStream_t s);
 
 // ---- stage 2: calibrate -------------------------------------------------------
 // Up to kCalGroupsLds groups: chunked scan without a global partition.

@@ -87,6 +87,12 @@ struct EngineArgs {
     uint32_t *seq;
     int32_t *tick_of;
     uint32_t *n_dispatched;
+    // the queue engine (every policy but SJF): the FIFO positions tier by
+    // tier (rpos, with each tier's first entry in rstart), and candidate
+    // scratch of kMaxQ x batch entries
+    const uint32_t *rpos, *rstart;
+    uint64_t *cand_k;
+    uint32_t *cand_j, *cand_i;
 };
 
 // Several runs share one launch: run r is block row r of the setup and block
@@ -180,9 +186,8 @@ __device__ __forceinline__ uint32_t pair_digit(uint64_t K, uint32_t J, int d)
     return d >= 4 ? (uint32_t)(K >> (8 * (d - 4))) & 255u : (J >> (8 * d)) & 255u;
 }
 
-__global__ __launch_bounds__(kTPB) void k_sim_engine(EngineBatch eb)
+__device__ void engine_list(const EngineArgs &a)
 {
-    const EngineArgs &a = eb.r[blockIdx.x];
     __shared__ uint32_t s_w[kNW];
     __shared__ uint32_t s_hist[256];
     __shared__ uint32_t s_vw[kNW][kMaxQ];
@@ -528,6 +533,195 @@ __global__ __launch_bounds__(kTPB) void k_sim_engine(EngineBatch eb)
     if (tid == 0) a.n_dispatched[0] = total;
 }
 
+// The loop for FIFO, Priority, Weighted and Aging with one queue per tier.
+// Within a tier each of these orders is the FIFO order (Aging's score is
+// monotone in the arrival for a fixed priority), so the pending requests of
+// tier q are always the stretch [head_q, tail_q) of the tier's FIFO run:
+// arrivals move tail_q, dispatches move head_q. The first m dispatches of a
+// tick are among the first m pending requests of each tier; those
+// candidates are ranked by the policy's key across tiers (a binary search
+// in every other tier's candidates, which are in key order) or placed by
+// the round-robin closed forms, so a tick costs O(tiers x batch) rather
+// than a pass over the pending set. Results equal the list engine's.
+__device__ void engine_queues(const EngineArgs &a)
+{
+    __shared__ uint32_t s_head[kMaxQ], s_tail[kMaxQ], s_cnt[kMaxQ], s_d[kMaxQ], s_wt[kMaxQ];
+    __shared__ uint32_t s_sel[kSimMaxBatch];
+    __shared__ uint32_t s_evg[kSimMaxBatch], s_evo[kSimMaxBatch];
+    __shared__ double s_evx[kSimMaxBatch];
+    const uint32_t tid = threadIdx.x, lane = (uint32_t)lane_id(), w = tid >> 6;
+    const uint32_t n = a.n, policy = a.policy, batch = a.batch, nq = a.n_q;
+    const double oma = 1.0 - a.alpha;
+    if (tid < kMaxQ) {
+        s_head[tid] = 0;
+        s_tail[tid] = 0;
+        s_wt[tid] = a.weight[tid];
+    }
+    uint32_t total = 0;
+    __syncthreads();
+    for (uint32_t k = 0; k < a.n_ticks; k++) {
+        const double t = a.tick_t[k];
+        // 1. arrivals: wave q moves tier q's tail over its requests with
+        //    arrival <= t (a prefix of the rest of its FIFO run)
+        if (w < nq) {
+            const uint32_t r0 = a.rstart[w], len = a.rstart[w + 1] - r0;
+            uint32_t tail = s_tail[w];
+            for (;;) {
+                const uint32_t idx = tail + lane;
+                bool ok = false;
+                if (idx < len) {
+                    uint32_t id = a.fifo[a.rpos[r0 + idx]];
+                    id = id < n ? id : 0u;
+                    ok = a.arrival[id] <= t;
+                }
+                const uint64_t b = __ballot(ok);
+                const uint32_t c = ~b ? (uint32_t)__ffsll((unsigned long long)~b) - 1u : 64u;
+                tail += c;
+                if (c < 64u) break;
+            }
+            if (lane == 0) s_tail[w] = tail;
+        }
+        if (tid < kMaxQ) s_d[tid] = 0;
+        __syncthreads();
+        if (tid < kMaxQ) s_cnt[tid] = tid < nq ? s_tail[tid] - s_head[tid] : 0u;
+        __syncthreads();
+        uint32_t P = 0;
+        for (uint32_t q = 0; q < nq; q++) P += s_cnt[q];
+        const uint32_t m = P < batch ? P : batch;
+        if (m == 0) continue;   // uniform
+
+        // 2. candidates: the first min(m, pending) requests of each tier
+        const bool ranked = policy == kFifo || policy == kPriority || policy == kAging;
+        for (uint32_t p = tid; p < nq * batch; p += kTPB) {
+            const uint32_t q = p / batch, r = p - q * batch;
+            const uint32_t cq = s_cnt[q] < m ? s_cnt[q] : m;
+            if (r >= cq) continue;
+            const uint32_t j = a.rpos[a.rstart[q] + s_head[q] + r];
+            uint32_t id = a.fifo[j];
+            id = id < n ? id : 0u;
+            if (ranked) {
+                uint64_t K;
+                if (policy == kFifo) {
+                    K = 0;
+                } else if (policy == kPriority) {
+                    K = a.val[id];
+                } else {
+                    const Aux x = a.aux[id];
+                    double wt = t - x.a;
+                    if (wt < 0.0) wt = 0.0;
+                    const double d = a.aging_rate * wt;
+                    double e = x.b - d;
+                    if (e < a.aging_floor) e = a.aging_floor;
+                    K = ordered_bits(e);
+                }
+                a.cand_k[p] = K;
+                a.cand_j[p] = j;
+            } else if (a.wrr_mode != kWrrSmooth) {
+                const uint64_t pos = a.wrr_mode == kWrrStride
+                                         ? wrr_stride_pos(q, r, s_wt, nq, [&](uint32_t u) { return s_cnt[u]; })
+                                         : wrr_place(q, r, s_cnt, s_wt, nq);
+                if (pos < m) {
+                    s_sel[pos] = id;
+                    atomicAdd(&s_d[q], 1u);
+                }
+            }
+            a.cand_i[p] = id;
+        }
+        __syncthreads();
+        if (ranked) {
+            // rank of each candidate: its place in its tier plus, in every
+            // other tier, the candidates with a smaller (key, FIFO position)
+            for (uint32_t p = tid; p < nq * batch; p += kTPB) {
+                const uint32_t q = p / batch, r = p - q * batch;
+                const uint32_t cq = s_cnt[q] < m ? s_cnt[q] : m;
+                if (r >= cq) continue;
+                const uint64_t K = a.cand_k[p];
+                const uint32_t J = a.cand_j[p];
+                uint32_t rank = r;
+                for (uint32_t u = 0; u < nq && rank < m; u++) {
+                    if (u == q) continue;
+                    const uint32_t cu = s_cnt[u] < m ? s_cnt[u] : m;
+                    uint32_t lo = 0, hi = cu;
+                    while (lo < hi) {
+                        const uint32_t mid = (lo + hi) >> 1;
+                        const uint64_t K2 = a.cand_k[u * batch + mid];
+                        const uint32_t J2 = a.cand_j[u * batch + mid];
+                        if (K2 < K || (K2 == K && J2 < J)) lo = mid + 1u;
+                        else hi = mid;
+                    }
+                    rank += lo;
+                }
+                if (rank < m) {
+                    s_sel[rank] = a.cand_i[p];
+                    atomicAdd(&s_d[q], 1u);
+                }
+            }
+        } else if (a.wrr_mode == kWrrSmooth && w == 0) {
+            // the first m dispatches of a fresh smooth cycle (lane q = tier q);
+            // a queue running empty leaves and the others keep their credits
+            const uint32_t len = lane < nq ? s_cnt[lane] : 0u;
+            const uint32_t wq = lane < nq ? s_wt[lane] : 0u;
+            uint32_t served = 0;
+            int32_t credit = 0;
+            uint32_t W = wave_sum(len ? wq : 0u);
+            for (uint32_t pos = 0; pos < m; pos++) {
+                const int b = wrr_pick(credit, served < len, wq, W);
+                const bool mine = lane == (uint32_t)b;
+                if (mine) s_sel[pos] = a.cand_i[lane * batch + served];   // served < m
+                served += mine ? 1u : 0u;
+                if (__ballot(mine && served == len) != 0ull) W = wave_sum(served < len ? wq : 0u);
+            }
+            if (lane < kMaxQ) s_d[lane] = served;
+        }
+        __syncthreads();
+
+        // 3. dispatch, and the completion events of the batch
+        if (tid < m) {
+            const uint32_t id = s_sel[tid];
+            if (total + tid < n) a.seq[total + tid] = id;
+            a.tick_of[id] = (int32_t)k;
+            s_evg[tid] = a.group[id];
+            s_evx[tid] = a.est_base[id];
+            s_evo[tid] = a.observed[id];
+        }
+        __syncthreads();
+
+        // 4. Eq. (5) with the ratio of Eq. (6), each group's events of the
+        //    batch in dispatch order
+        if (tid < m) {
+            const uint32_t g = s_evg[tid];
+            bool lead = g < a.n_groups;
+            for (uint32_t r = 0; r < tid && lead; r++) lead = s_evg[r] != g;
+            if (lead) {
+                double c = a.state[g];
+                for (uint32_t r = tid; r < m; r++) {
+                    if (s_evg[r] != g) continue;
+                    const double x = s_evx[r];
+                    if (!(isfinite(x) && x > 0.0)) continue;
+                    const double ratio = (double)s_evo[r] / x;
+                    const double t1 = oma * c;
+                    const double t2 = a.alpha * ratio;
+                    c = t1 + t2;
+                }
+                a.state[g] = c;
+            }
+        }
+        if (tid < nq) s_head[tid] += s_d[tid];
+        total += m;
+        __syncthreads();
+    }
+    if (tid == 0) a.n_dispatched[0] = total;
+}
+
+// One workgroup per run: the queue engine where the run has its tier runs,
+// else (SJF) the list engine.
+__global__ __launch_bounds__(kTPB) void k_sim_engine(EngineBatch eb)
+{
+    const EngineArgs &a = eb.r[blockIdx.x];
+    if (a.rpos) engine_queues(a);
+    else engine_list(a);
+}
+
 __global__ void k_sim_empty(uint32_t *__restrict__ n_dispatched, uint32_t n_runs)
 {
     if (threadIdx.x < n_runs) n_dispatched[threadIdx.x] = 0;
@@ -557,12 +751,17 @@ uint32_t grid_for(uint64_t n)
 
 }  // namespace
 
+constexpr uint64_t kCandBytes = (uint64_t)kMaxQ * kSimMaxBatch * (8 + 4 + 4);
+
 size_t sim_ws_bytes(uint64_t n, uint32_t n_runs)
 {
-    // shared: fifo, then the FIFO sort; per run: list x2, est_base, key, aux, val
+    // shared: fifo, the tier runs (positions and starts), then the FIFO sort
+    // and the partition (one after the other); per run: list x2, est_base,
+    // key, aux, val, the queue engine's candidates
     const uint64_t per = 2 * align_up(n * 4, 256) + 2 * align_up(n * 8, 256) +
-                         align_up(n * sizeof(Aux), 256) + align_up(n, 256);
-    return align_up(n * 4, 256) + (uint64_t)(n_runs ? n_runs : 1) * per + sort_ws_bytes(n, 1);
+                         align_up(n * sizeof(Aux), 256) + align_up(n, 256) + kCandBytes;
+    const uint64_t sort = sort_ws_bytes(n, 1), part = am_partition_ws_bytes(n);
+    return 2 * align_up(n * 4, 256) + 256 + (uint64_t)(n_runs ? n_runs : 1) * per + (sort > part ? sort : part);
 }
 
 hipError_t sim_launch(const SimArgs *runs, uint32_t n_runs, void *ws, uint32_t *flag, hipStream_t s,
@@ -591,6 +790,11 @@ hipError_t sim_launch(const SimArgs *runs, uint32_t n_runs, void *ws, uint32_t *
         return q;
     };
     uint32_t *fifo = reinterpret_cast<uint32_t *>(take((uint64_t)n * 4));
+    uint32_t *rpos = reinterpret_cast<uint32_t *>(take((uint64_t)n * 4));
+    uint32_t *rstart = reinterpret_cast<uint32_t *>(take(256));
+    // every policy but SJF runs on the tier queues (up to the partition's limit)
+    bool any_queues = false;
+    for (uint32_t r = 0; r < n_runs; r++) any_queues = any_queues || (runs[r].policy != kSjf && n <= kAmMaxN);
     SetupBatch sb;
     EngineBatch eb;
     memset(&sb, 0, sizeof(sb));
@@ -603,6 +807,7 @@ hipError_t sim_launch(const SimArgs *runs, uint32_t n_runs, void *ws, uint32_t *
         uint64_t *key = reinterpret_cast<uint64_t *>(take((uint64_t)n * 8));
         Aux *aux = reinterpret_cast<Aux *>(take((uint64_t)n * sizeof(Aux)));
         uint8_t *val = take(n);
+        uint8_t *cand = take(kCandBytes);
 
         SetupArgs &su = sb.r[r];
         su.n = n;
@@ -664,6 +869,13 @@ hipError_t sim_launch(const SimArgs *runs, uint32_t n_runs, void *ws, uint32_t *
         ea.seq = a.seq;
         ea.tick_of = a.tick_of;
         ea.n_dispatched = a.n_dispatched;
+        if (a.policy != kSjf && n <= kAmMaxN) {
+            ea.rpos = rpos;
+            ea.rstart = rstart;
+            ea.cand_k = reinterpret_cast<uint64_t *>(cand);
+            ea.cand_j = reinterpret_cast<uint32_t *>(cand + (uint64_t)kMaxQ * kSimMaxBatch * 8);
+            ea.cand_i = reinterpret_cast<uint32_t *>(cand + (uint64_t)kMaxQ * kSimMaxBatch * 12);
+        }
     }
     void *sort_ws = p;
     hipLaunchKernelGGL(k_sim_setup, dim3(grid_for(n), n_runs), dim3(256), 0, s, sb);
@@ -676,6 +888,18 @@ hipError_t sim_launch(const SimArgs *runs, uint32_t n_runs, void *ws, uint32_t *
     SortJob job = {SortKind::Fifo, 64, nullptr, fifo};
     hipError_t e = sort_launch(in, &job, 1, sort_ws, s);
     if (e != hipSuccess) return e;
+    if (any_queues) {
+        // the FIFO sequence split by tier, each tier in FIFO order (the sort's
+        // workspace is free again on the stream)
+        SortInput pin = {};
+        pin.n = n;
+        pin.fifo = fifo;
+        pin.tier = a0.tier;
+        pin.arrival = a0.arrival;
+        for (uint32_t q = 0; q < kMaxQ; q++) pin.cls[q] = q;
+        e = am_partition(pin, rpos, rstart, sort_ws, s);
+        if (e != hipSuccess) return e;
+    }
     hipLaunchKernelGGL(k_sim_engine, dim3(n_runs), dim3(kTPB), 0, s, eb);
     return hipGetLastError();
 }

@@ -254,3 +254,32 @@ def test_multi_host_errors(ds):
                               [dev(x["state"].copy()) for _ in range(R)], dev(np.array([1.0])), [p] * R,
                               ws=ds.workspace(ds.OP_SIMULATE_MULTI, 10, 8))
         assert e.value.status == -2
+
+
+@pytest.mark.parametrize("policy", ALL)
+def test_drift_workload_prefix(ds, oracle, policy):
+    """The drift workload's first 60,000 requests (arrival order, 4,096
+    groups, drifting ratios) through 10 ms ticks of 32: the pending set grows
+    (5,000 arrivals/s against 3,200 dispatches/s) to about 20,000 before the
+    arrivals end. FIFO, Priority, Weighted and Aging run on the tier-queue
+    engine, SJF on the list engine."""
+    b = wl.load("drift4m", n=60000)
+    ticks = synth.sim_ticks(b.arrival)
+    seq, _, _ = both(ds, oracle, policy, b.arrival, b.tier, b.words, b.category, b.tenant,
+                     b.group, b.observed, b.t_base, b.s_tenant, np.ones(b.n_groups), ticks,
+                     batch=32, alpha=0.05, weights=tuple(int(w) for w in b.weights),
+                     tier_priority=tuple(b.tier_priority), aging_rate=b.aging_rate)
+    assert len(seq) == b.n
+
+
+@pytest.mark.parametrize("policy", [FIFO, PRIORITY, WEIGHTED, AGING])
+def test_queue_engine_tiers_and_batches(ds, oracle, policy):
+    # sixteen tiers with shared priorities, batches of 1 and 1024, ticks that
+    # repeat and ticks with no arrivals
+    for batch, tiers in ((1, 16), (1024, 16), (7, 2)):
+        x = random_inputs(batch * 31 + tiers, 6000, tiers=tiers, round_arrival=2)
+        ticks = np.concatenate([[0.0, 0.0, 0.5, 0.5], np.linspace(0.6, 11.0, 80)])
+        prio = tuple(float(q % 5) for q in range(tiers))
+        w = tuple(1 + (q * 7) % 5 for q in range(tiers))
+        both(ds, oracle, policy, ticks=ticks, batch=batch, alpha=0.1, weights=w, tier_priority=prio,
+             aging_rate=0.4, **x)
