@@ -392,8 +392,10 @@ ds_status ds_calibrate_ex(const uint32_t *group, const double *est, const uint32
  *  stats      device, 4 * (n_groups + 1) double; written
  *  n          <= DS_MAX_ITEMS
  *  ws         workspace of ds_workspace_bytes(DS_OP_ERROR_STATS, n, n_groups)
- * Sums use floating-point atomic adds, so results vary between runs within
- * the rounding of an n-term sum (relative error at most about n * 2^-53).
+ * Every sum is taken in an order fixed by the data and n (no floating-point
+ * atomics): the same inputs give the same bits on every run. Against exact
+ * arithmetic each sum is within the rounding of an n-term sum (relative
+ * error at most about n * 2^-53).
  * Unlike the stages, n == 0 still writes stats (counts 0).
  */
 ds_status ds_error_stats(uint64_t n, const double *est, const double *factor,

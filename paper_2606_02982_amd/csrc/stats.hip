@@ -6,13 +6,14 @@
 // Error: for every event with a usable estimate x = est[e] * factor[e]
 // (finite and > 0; no factor = 1), d = x - obs[e]; per group and over all
 // events: count, sum |d|, sum d^2 and sum obs / x. Each block takes a
-// contiguous range of events and accumulates per-group sums in LDS (fp64
-// atomic adds, 1024 groups per pass over its range) and the all-events sums
-// in registers; it stores its partial sums, and a last kernel adds the
-// blocks' partials in a fixed order and forms MAE = sum|d| / count,
-// RMSE = sqrt(sum d^2 / count), mean bias = sum(obs / x) / count. Only the
-// order of the LDS adds inside a block varies between runs, so results agree
-// with any sequential sum within the rounding of an n-term sum.
+// contiguous range of events and accumulates per-group sums in LDS (1024
+// groups per pass over its range) and the all-events sums in registers; it
+// stores its partial sums, and a last kernel adds the blocks' partials in a
+// fixed order and forms MAE = sum|d| / count, RMSE = sqrt(sum d^2 / count),
+// mean bias = sum(obs / x) / count. No sum uses floating-point atomics: every
+// order of addition is fixed by the data and the launch shape, so results
+// are the same from run to run and agree with any sequential sum within the
+// rounding of an n-term sum.
 #include "common.h"
 #include "kernels.h"
 
@@ -100,13 +101,22 @@ __global__ __launch_bounds__(kT) void k_err_accum(uint64_t n, const double *__re
     }
     if (!group) return;
 
-    // groups, kLdsGroups at a time
+    // groups, kLdsGroups at a time, in a fixed order: each step's events go
+    // to LDS in event order; wave w owns the groups g = w (mod kWaves) of
+    // the pass and walks the step's events round by round (64 at a time, in
+    // order); the lanes of one group in a round are added up in lane order
+    // by the lowest of them, which adds that to the group's sums. The result
+    // does not depend on scheduling.
+    constexpr uint32_t kWaves = kT / 64, kStep = kU * kT;
+    __shared__ uint32_t sg[kStep];
+    __shared__ double sv[3][kStep];
+    const uint32_t lane = (uint32_t)lane_id(), w = threadIdx.x >> 6;
     for (uint32_t c0 = 0; c0 < G; c0 += kLdsGroups) {
         const uint32_t cn = G - c0 < kLdsGroups ? G - c0 : kLdsGroups;
         for (uint32_t i = threadIdx.x; i < cn; i += kT)
             lacc[0][i] = lacc[1][i] = lacc[2][i] = lacc[3][i] = 0.0;
         __syncthreads();
-        for (uint64_t b0 = e0; b0 < e1; b0 += kU * kT) {
+        for (uint64_t b0 = e0; b0 < e1; b0 += kStep) {
             double x[kU], o[kU];
             uint32_t g[kU];
 #pragma unroll
@@ -117,15 +127,43 @@ __global__ __launch_bounds__(kT) void k_err_accum(uint64_t n, const double *__re
             load_events(est, factor, obs, b0, e1, x, o);
 #pragma unroll
             for (uint32_t u = 0; u < kU; u++) {
-                if (g[u] >= cn || !usable(x[u])) continue;
+                const uint32_t slot = u * kT + threadIdx.x;   // event order
+                const bool ok = g[u] < cn && usable(x[u]);
                 const double d = x[u] - o[u];
-                atomicAdd(&lacc[0][g[u]], 1.0);
-                atomicAdd(&lacc[1][g[u]], fabs(d));
-                atomicAdd(&lacc[2][g[u]], d * d);
-                atomicAdd(&lacc[3][g[u]], o[u] / x[u]);
+                sg[slot] = ok ? g[u] : 0xFFFFFFFFu;
+                sv[0][slot] = ok ? fabs(d) : 0.0;
+                sv[1][slot] = ok ? d * d : 0.0;
+                sv[2][slot] = ok ? o[u] / x[u] : 0.0;
             }
+            __syncthreads();
+            for (uint32_t r = 0; r < kStep / 64; r++) {
+                const uint32_t slot = r * 64 + lane;
+                const uint32_t gv = sg[slot];
+                const bool own = gv != 0xFFFFFFFFu && gv % kWaves == w;
+                uint64_t peers = __ballot(own);
+#pragma unroll
+                for (int bb = 0; bb < 10; bb++) {   // group bits within the pass (kLdsGroups = 1024)
+                    const bool bit = (gv >> bb) & 1u;
+                    const uint64_t mk = __ballot(bit);
+                    peers &= bit ? mk : ~mk;
+                }
+                if (own && (peers & lanemask_lt()) == 0) {
+                    double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+                    for (uint64_t m = peers; m; m &= m - 1) {
+                        const uint32_t q = r * 64 + (uint32_t)__builtin_ctzll(m);
+                        s0 += 1.0;
+                        s1 += sv[0][q];
+                        s2 += sv[1][q];
+                        s3 += sv[2][q];
+                    }
+                    lacc[0][gv] += s0;
+                    lacc[1][gv] += s1;
+                    lacc[2][gv] += s2;
+                    lacc[3][gv] += s3;
+                }
+            }
+            __syncthreads();
         }
-        __syncthreads();
         for (uint32_t i = threadIdx.x; i < cn; i += kT)
             for (int k = 0; k < 4; k++) mine[k * slots + c0 + i] = lacc[k][i];
         __syncthreads();

@@ -2,11 +2,12 @@
 each calibration event (within the calibration contract, 1e-12 relative),
 the estimation-error statistics, and the class histogram (exact).
 
-Error statistics are sums of n terms accumulated in a run-dependent order
-(floating-point atomics) on the GPU and sequentially in the oracle. Both are
-within (n - 1) * 2^-53 * sum|terms| of the exact sum of nonnegative terms, so
-the test allows a relative difference of 2 n 2^-53 on each sum and the
-corresponding bound on the means; counts are exact.
+Error statistics are sums of n terms, accumulated in a fixed blocked order
+on the GPU and sequentially in the oracle. Both are within
+(n - 1) * 2^-53 * sum|terms| of the exact sum of nonnegative terms, so the
+test allows a relative difference of 2 n 2^-53 on each sum and the
+corresponding bound on the means; counts are exact. The GPU's order does not
+depend on scheduling, so repeated calls agree bit for bit.
 """
 import numpy as np
 import pytest
@@ -90,6 +91,20 @@ def test_bias_off_on(ds, oracle, name):
                      n_groups=b.n_groups)
     # the calibrated estimates have the smaller error over all events
     assert on[-1, 1] < off[-1, 1] and on[-1, 2] < off[-1, 2]
+
+
+@pytest.mark.parametrize("n,G", [(70000, 1024), (300000, 5000), (1 << 22, 4096)])
+def test_same_bits_every_run(ds, n, G):
+    # many events per group and block, so atomics in any order would show
+    rng = np.random.default_rng(7 + G)
+    est = rng.uniform(0.5, 4000, n)
+    obs = rng.integers(0, 5000, n)
+    g = rng.integers(0, G, n) % (G // 64 + 1)   # few groups carry all the events
+    fac = rng.uniform(0.5, 1.5, n)
+    first = gpu_stats(ds, est, obs, factor=fac, group=g, n_groups=G)
+    for _ in range(3):
+        again = gpu_stats(ds, est, obs, factor=fac, group=g, n_groups=G)
+        assert first.tobytes() == again.tobytes()
 
 
 def test_validate(ds):
