@@ -16,7 +16,8 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
 SOURCES = ["api.hip", "characterize.hip", "sort.hip", "calibrate.hip", "score.hip", "order.hip", "stats.hip",
-           "sim.hip", "ssort.hip", "calchunk.hip", "agmerge.hip"]
+           "sim.hip", "ssort.hip", "calchunk.hip", "agmerge.hip",
+           "lsort.hip"]
 
 HIP_FLAGS = [
     "--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC", "-Wall",

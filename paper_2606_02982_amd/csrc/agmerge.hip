@@ -314,6 +314,23 @@ __global__ __launch_bounds__(kMgTPB) void k_am_merge(AmArgs a, uint32_t span, ui
     }
 }
 
+// ceil(log2 K) merge rounds over the runs in a.rk[0] / a.rp[0] (one copying
+// round when K = 1); the last one writes the permutation and the key.
+void merge_rounds(const AmArgs &a, hipStream_t s)
+{
+    uint32_t rounds = 0;
+    while ((1u << rounds) < a.K) rounds++;
+    if (rounds == 0) rounds = 1;
+    // blocks: every pair's tiles (at most n / kMgTile + one partial tile per pair)
+    const uint32_t blocks = (uint32_t)cdiv(a.n, kMgTile) + (a.K + 1) / 2;
+    uint32_t src = 0;
+    for (uint32_t r = 0; r < rounds; r++) {
+        hipLaunchKernelGGL(k_am_merge, dim3(blocks), dim3(kMgTPB), 0, s, a, 1u << r, src,
+                           r + 1 == rounds ? 1u : 0u);
+        src ^= 1u;
+    }
+}
+
 }  // namespace
 
 size_t am_partition_ws_bytes(uint64_t n)
@@ -382,17 +399,29 @@ hipError_t am_launch(const SortInput &in, uint32_t n_classes, uint32_t *perm, do
     hipLaunchKernelGGL(k_am_count, dim3(a.tiles), dim3(kAmTPB), 0, s, a);
     hipLaunchKernelGGL(k_am_scan, dim3(1), dim3(1024), 0, s, a);
     hipLaunchKernelGGL(k_am_place, dim3(a.tiles), dim3(kAmTPB), 0, s, a);
-    uint32_t rounds = 0;
-    while ((1u << rounds) < n_classes) rounds++;
-    if (rounds == 0) rounds = 1;   // one class: a single copying pass writes the result
-    // blocks: every pair's tiles (at most n / kMgTile + one partial tile per pair)
-    const uint32_t blocks = (uint32_t)cdiv(n, kMgTile) + (n_classes + 1) / 2;
-    uint32_t src = 0;
-    for (uint32_t r = 0; r < rounds; r++) {
-        hipLaunchKernelGGL(k_am_merge, dim3(blocks), dim3(kMgTPB), 0, s, a, 1u << r, src,
-                           r + 1 == rounds ? 1u : 0u);
-        src ^= 1u;
+    merge_rounds(a, s);
+    return hipGetLastError();
+}
+
+hipError_t am_merge_launch(const SortInput &in, uint32_t n_classes, uint32_t *cstart, uint64_t *const rk[2],
+                           uint32_t *const rp[2], uint32_t *perm, double *key_out, hipStream_t s)
+{
+    const uint32_t n = in.n;
+    if (n == 0) return hipSuccess;
+    if (n > kAmMaxN || !in.fifo || n_classes < 1 || n_classes > kAmCls) return hipErrorInvalidValue;
+    AmArgs a;
+    memset(&a, 0, sizeof(a));
+    a.in = in;
+    a.n = n;
+    a.K = n_classes;
+    a.cstart = cstart;
+    for (int k = 0; k < 2; k++) {
+        a.rk[k] = rk[k];
+        a.rp[k] = rp[k];
     }
+    a.perm = perm;
+    a.key_out = key_out;
+    merge_rounds(a, s);
     return hipGetLastError();
 }
 

@@ -108,6 +108,33 @@ size_t ssort_ws_bytes(uint64_t n, uint32_t nsorts);   // 0 above kSsMaxN
 hipError_t ssort_launch(const SortInput &in, const SortJob *jobs, uint32_t nsorts, bool serial,
                         void *ws, hipStream_t s, const SsPartitions *parts = nullptr);
 
+// The orders of kSsMaxN < n <= kLsMaxN requests, several in the same
+// launches: sorts (Fifo; Budget, Aging over in.fifo) by (key, position)
+// with sampled splitters, and partitions (Class, Tier over in.fifo) placed
+// at the Priority / Weighted positions. job.out receives the values in order
+// and job.key_out (if given) each request's key. No waits between blocks.
+// The FIFO sort can write the inputs in FIFO order (LsCopies; bud may be
+// NULL), which a batch over that sequence then reads instead of gathering
+// through in.fifo.
+constexpr uint32_t kLsMaxN = 1u << 20;
+struct LsCopies {
+    double *arr;
+    double *bud;
+    uint8_t *tier;
+};
+// A batch's Class partition can also lay out the priority classes' runs for
+// the Aging merge (am_merge_launch): each request's aged-score bits and FIFO
+// position at its Priority place, and the classes' starts (17 words).
+struct LsRuns {
+    uint64_t *rk;
+    uint32_t *rp;
+    uint32_t *cstart;
+};
+size_t lsort_ws_bytes(uint64_t n, uint32_t nsort, uint32_t npart);   // 0 outside (kSsMaxN, kLsMaxN]
+hipError_t lsort_launch(const SortInput &in, const SortJob *jobs, uint32_t njobs, void *ws, hipStream_t s,
+                        const LsCopies *fifo_in_copies = nullptr, const LsCopies *fifo_out_copies = nullptr,
+                        const LsRuns *aging_runs = nullptr);
+
 // Aging above the sample-sort limit as a merge of the priority classes' runs
 // of the FIFO sequence (in.fifo, in.cls and the aging parameters set;
 // n_classes = the number of distinct priorities). wait_status (may be NULL):
@@ -119,6 +146,11 @@ hipError_t am_launch(const SortInput &in, uint32_t n_classes, uint32_t *perm, do
 // The stable partition of the FIFO sequence by in.cls[tier] alone (16
 // classes): run_pos (n) receives the FIFO positions class by class, each
 // class in FIFO order, run_start (17) each class's first entry and n.
+// The merge rounds alone, over runs formed elsewhere: rk[0] / rp[0] hold
+// the K runs (aged-score bits, FIFO position) one after another from
+// cstart[0], cstart[K..16] = n; rk[1] / rp[1] are scratch of the same size.
+hipError_t am_merge_launch(const SortInput &in, uint32_t n_classes, uint32_t *cstart, uint64_t *const rk[2],
+                           uint32_t *const rp[2], uint32_t *perm, double *key_out, hipStream_t s);
 size_t am_partition_ws_bytes(uint64_t n);
 hipError_t am_partition(const SortInput &in, uint32_t *run_pos, uint32_t *run_start, void *ws, hipStream_t s);
 

@@ -72,7 +72,14 @@ size_t order_ws_bytes(uint64_t n, uint32_t npolicies)
     const uint32_t nss = np + 1 > kSsMaxSorts ? kSsMaxSorts : np + 1;
     const uint32_t nrs = np > kMaxSorts ? kMaxSorts : np;
     const size_t sample = ssort_ws_bytes(n < kSsMaxN ? n : kSsMaxN, nss);
-    const size_t radix = align_up(n * 4, 256) + sort_ws_bytes(n, nrs);
+    const size_t rs = sort_ws_bytes(n, nrs);
+    // (FIFO-ordered copies of arrival, budget and tier for the batch over the
+    // FIFO sequence, and the Aging runs with their merge scratch)
+    const size_t lb = lsort_ws_bytes(n, 1, 2);
+    const size_t ls = lb ? 2 * align_up(n * 8, 256) + align_up(n, 256) + 2 * align_up(n * 8, 256) +
+                               2 * align_up(n * 4, 256) + align_up(17 * 4, 256) + lb
+                         : 0;
+    const size_t radix = align_up(n * 4, 256) + (ls > rs ? ls : rs);
     // the larger of the two keeps the size non-decreasing in n
     return n <= kSsMaxN ? sample : (radix > sample ? radix : sample);
 }
@@ -148,6 +155,59 @@ hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_
         return ssort_launch(in, all, na, a.serial_sort, ws, s, parts ? &pw : nullptr);
     }
 
+    uint8_t *p = static_cast<uint8_t *>(ws);
+    uint32_t *fifo_ws = reinterpret_cast<uint32_t *>(p);
+    void *sort_ws = p + align_up((uint64_t)n * 4, 256);
+    if (n <= kLsMaxN) {
+        // the FIFO sort, then every other policy over the FIFO sequence in
+        // one batch of sample sorts and partitions (lsort.hip)
+        uint8_t *q = static_cast<uint8_t *>(sort_ws);
+        LsCopies cp;
+        cp.arr = reinterpret_cast<double *>(q);
+        q += align_up((uint64_t)n * 8, 256);
+        cp.bud = (a.mask & (1u << 3)) ? reinterpret_cast<double *>(q) : nullptr;
+        q += align_up((uint64_t)n * 8, 256);
+        cp.tier = q;
+        q += align_up(n, 256);
+        uint64_t *rk[2];
+        uint32_t *rp[2];
+        for (int e = 0; e < 2; e++) {
+            rk[e] = reinterpret_cast<uint64_t *>(q);
+            q += align_up((uint64_t)n * 8, 256);
+        }
+        for (int e = 0; e < 2; e++) {
+            rp[e] = reinterpret_cast<uint32_t *>(q);
+            q += align_up((uint64_t)n * 4, 256);
+        }
+        LsRuns runs = {rk[0], rp[0], reinterpret_cast<uint32_t *>(q)};
+        q += align_up(17 * 4, 256);
+        void *batch_ws = q;
+        const bool more = a.mask & ~1u;   // policies over the FIFO sequence
+        const uint32_t *fifo = a.fifo_in;
+        if (!fifo) {
+            SortJob job = {SortKind::Fifo, 64, want_fifo ? a.key[0] : nullptr, want_fifo ? a.perm[0] : fifo_ws};
+            hipError_t err = lsort_launch(in, &job, 1, batch_ws, s, nullptr, more ? &cp : nullptr);
+            if (err != hipSuccess) return err;
+            fifo = job.out;
+            in.wait.clear = false;
+        }
+        in.fifo = fifo;
+        // SJF sorts; Priority partitions (and lays out the priority classes'
+        // runs, which the Aging merge then combines); Weighted partitions
+        const bool prio = a.mask & (1u << 1), aging = a.mask & (1u << 4);
+        SortJob jobs[3];
+        uint32_t nj = 0;
+        if (a.mask & (1u << 3)) jobs[nj++] = {SortKind::Budget, 64, a.key[3], a.perm[3]};
+        if (prio || aging)
+            jobs[nj++] = {SortKind::Class, 8, prio ? a.key[1] : nullptr, prio ? a.perm[1] : nullptr};
+        if (a.mask & (1u << 2)) jobs[nj++] = {SortKind::Tier, 8, a.key[2], a.perm[2]};
+        if (nj == 0) return hipGetLastError();
+        hipError_t err = lsort_launch(in, jobs, nj, batch_ws, s, a.fifo_in ? nullptr : &cp, nullptr,
+                                      aging ? &runs : nullptr);
+        if (err != hipSuccess || !aging) return err;
+        return am_merge_launch(in, n_classes, runs.cstart, rk, rp, a.perm[4], a.key[4], s);
+    }
+
     // the policy sorts over the FIFO sequence; Aging as the merge of the
     // priority classes' runs of that sequence (agmerge.hip) where its
     // buffers fit the sort workspace, else as one more radix sort
@@ -160,9 +220,6 @@ hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_
     if ((a.mask & (1u << 4)) && !aging_merge) jobs[nj++] = {SortKind::Aging, 64, a.key[4], a.perm[4]};
 
     // radix sorts: the FIFO permutation first, then the policies over it
-    uint8_t *p = static_cast<uint8_t *>(ws);
-    uint32_t *fifo_ws = reinterpret_cast<uint32_t *>(p);
-    void *sort_ws = p + align_up((uint64_t)n * 4, 256);
     const uint32_t *fifo = a.fifo_in;
     if (!fifo) {
         SortJob job = {SortKind::Fifo, 64, want_fifo ? a.key[0] : nullptr, want_fifo ? a.perm[0] : fifo_ws};

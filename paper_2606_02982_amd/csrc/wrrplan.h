@@ -232,6 +232,30 @@ __device__ __forceinline__ uint64_t wrr_smooth_pos(const WrrPlanHead &head, cons
            plan->off[head.offbase[ph][q] + i % wq];
 }
 
+// The blocked interleaving (the default reading of the same section): round
+// r serves up to w_t requests of each tier t in tier order. The k-th request
+// (FIFO order) of tier q runs in round r = floor(k / w_q), after
+// sum_t min(n_t, r w_t) requests of the earlier rounds and, in round r,
+// min(w_t, max(0, n_t - r w_t)) of each tier t < q. cnt(t) = n_t; weights of
+// 0 count as 1 for the tier's own round.
+template <typename Cnt>
+__device__ __forceinline__ uint64_t wrr_blocked_pos(uint32_t q, uint64_t k, const uint32_t *w, uint32_t nq, Cnt cnt,
+                                                    uint64_t &rnd)
+{
+    const uint64_t wq = w[q] ? w[q] : 1u;
+    rnd = k / wq;
+    uint64_t pos = k - rnd * wq;
+    for (uint32_t t = 0; t < nq; t++) {
+        const uint64_t nt = cnt(t), wt = w[t], full = rnd * wt;
+        pos += nt < full ? nt : full;
+        if (t < q) {
+            const uint64_t left = nt > full ? nt - full : 0u;
+            pos += left < wt ? left : wt;
+        }
+    }
+    return pos;
+}
+
 // Stride scheduling, another reading of the same section: queue q's pass
 // starts at its stride 1 / w_q and grows by it per dispatch; the smallest
 // pass (the lowest tier on ties) is served. The k-th request (FIFO order)
