@@ -34,7 +34,7 @@ def batch(n, seed):
 
 
 def test_radix_pass_give_up_is_reported(ds, oracle):
-    n = 300000                       # above the sample-sort limit: radix passes
+    n = (1 << 20) + 99               # above the sample-sort limits: radix passes
     tier, arr, bud = batch(n, 1)
     print("waits: radix FIFO n=%d" % n, flush=True)
     ws = ds.workspace(ds.OP_ORDER, n)
@@ -49,6 +49,20 @@ def test_radix_pass_give_up_is_reported(ds, oracle):
     assert ds.wait_status(ws) == 0
     w_perm, _ = oracle.order(0, tier, arr)
     assert np.array_equal(host(perm, np.uint32), w_perm)
+
+
+def test_no_waits_between_the_sample_sort_limits(ds, oracle):
+    # 2^18 < n <= 2^20: the sorts have no waits, so DS_NO_WAIT changes nothing
+    n = 300000
+    tier, arr, bud = batch(n, 2)
+    print("waits: none at n=%d" % n, flush=True)
+    ws = ds.workspace(ds.OP_ORDER_MULTI, n)
+    perms, _ = ds.order_multi((0, 1, 2, 3, 4), dev(tier), dev(arr), dev(bud), ws=ws, validate=True,
+                              no_wait=True)
+    assert ds.wait_status(ws) == 0
+    for pol in range(5):
+        w_perm, _ = oracle.order(pol, tier, arr, bud)
+        assert np.array_equal(host(perms[pol], np.uint32), w_perm)
 
 
 def test_scatter_give_up_takes_the_exact_fallback(ds, oracle):
