@@ -7,10 +7,12 @@
 //
 //   k_ls_gather   the keys of S = 8 per bucket positions, one in each of S
 //                 equal strata of [0, n) (so the sample is in sequence order).
-//   k_ls_sample   every block stages all S keys in LDS and ranks 64 of them
-//                 by counting (each wave over a slice of the sample, the
-//                 slices' counts added): the sorted sample, of which every
-//                 (S/B)-th pair is one of the B - 1 splitters.
+//   k_ls_sample   each sample's rank by counting the samples below it, the
+//                 count of each group of 64 samples spread over four blocks
+//                 (each staging a quarter of the sample in LDS).
+//   k_ls_place    each sample at its rank (the four counts added): the
+//                 sorted sample, of which every (S/B)-th pair is one of the
+//                 B - 1 splitters.
 //   k_ls_count    per tile of 4096 positions: each position's bucket (a
 //                 descent of the splitters' search tree), stored, and the
 //                 tile's count of each bucket; the per-request key output.
@@ -75,6 +77,7 @@ struct LsRow {
     uint32_t *tcnt;        // [tiles][B] each tile's count of each bucket, then its first slot there
     uint16_t *bid;         // [n] bucket of each position (sorts)
     uint64_t *raw_k;       // [S] the sample's keys in sample order
+    uint32_t *rpart;       // [kSmP][S] each part's count of samples below each sample
     uint64_t *smp_k;       // [S] the sample in order
     uint32_t *smp_j;
     uint64_t *rk[2];       // [n] bucket regions, and the large-bucket path's second buffer
@@ -231,7 +234,9 @@ __global__ __launch_bounds__(256) void k_ls_gather(LsArgs a)
 {
     const LsRow &R = a.r[blockIdx.y];
     const uint32_t s = blockIdx.x * 256u + threadIdx.x;
-    if (s < R.S) R.raw_k[s] = ls_key(a, R, ls_pos(s, a.n, R.S));
+    if (s < R.S) {
+        R.raw_k[s] = ls_key(a, R, ls_pos(s, a.n, R.S));
+    }
 }
 
 constexpr int kSmT = 1024, kSmW = kSmT / 64;
@@ -239,35 +244,29 @@ constexpr int kSmT = 1024, kSmW = kSmT / 64;
 // Block b ranks samples 64 b .. 64 b + 63 (one per lane) among all S, staged
 // in LDS: wave w counts over its slice of the sample, the slices' counts are
 // added. (Rank by counting: LDS broadcast reads, eight in flight at a time.)
+// Ranks by counting, spread over kSmP blocks per group of 64 samples: block
+// (g, p) stages part p of the sample in LDS and counts, for each of the
+// group's samples (one per lane), the part's samples below it (each wave
+// over a slice, the slices added), stored as that part's count.
+constexpr uint32_t kSmP = 4;
+
 __global__ __launch_bounds__(kSmT) void k_ls_sample(LsArgs a)
 {
-    __shared__ uint64_t sk[kLsMaxS];
+    __shared__ uint64_t sk[kLsMaxS / kSmP];
     __shared__ uint32_t part[kSmW][64];
     const LsRow &R = a.r[blockIdx.y];
-    if (blockIdx.x * 64u >= R.S) return;   // a row with a smaller sample than the grid is wide
+    const uint32_t g = blockIdx.x / kSmP, pq = blockIdx.x % kSmP;
+    if (g * 64u >= R.S) return;   // a row with a smaller sample than the grid is wide
     const uint32_t t = threadIdx.x, lane = (uint32_t)lane_id(), w = t >> 6, S = R.S, n = a.n;
-    {
-        constexpr int kPer = kLsMaxS / kSmT;
-        uint64_t kk[kPer];
-#pragma unroll
-        for (int r = 0; r < kPer; r++) {
-            const uint32_t s = (uint32_t)r * kSmT + t;
-            kk[r] = s < S ? R.raw_k[s] : 0ull;
-        }
-#pragma unroll
-        for (int r = 0; r < kPer; r++) {
-            const uint32_t s = (uint32_t)r * kSmT + t;
-            if (s < S) sk[s] = kk[r];
-        }
-    }
+    const uint32_t q = S / kSmP, p0 = pq * q;   // this block's part [p0, p0 + q) (S is a multiple of 64)
+    for (uint32_t i = t; i < q; i += kSmT) sk[i] = R.raw_k[p0 + i];
+    const uint32_t s0 = g * 64u, s = s0 + lane;
+    const uint64_t ks = R.raw_k[s];
     __syncthreads();
-    // rank of sample s = samples u with (key_u, pos_u) < (key_s, pos_s); the
-    // positions increase with u, so a tie on the key goes by u < s. Wave w
-    // counts over u in its slice [u0, u1): below the block's 64 samples
-    // (key <=), above them (key <), and across them (exactly).
-    const uint32_t s0 = blockIdx.x * 64u, s = s0 + lane;   // S is a multiple of 64
-    const uint64_t ks = sk[s];
-    const uint32_t per = S / kSmW, u0 = w * per, u1 = u0 + per;
+    // samples u with (key_u, pos_u) < (key_s, pos_s); the positions increase
+    // with u, so a tie on the key goes by u < s: below the group's samples
+    // (key <=), above them (key <), across them (exactly)
+    const uint32_t per = q / kSmW, u0 = p0 + w * per, u1 = u0 + per;
     uint32_t c = 0;
     {
         const uint32_t e = u1 < s0 ? u1 : s0;
@@ -275,16 +274,16 @@ __global__ __launch_bounds__(kSmT) void k_ls_sample(LsArgs a)
         for (; u + 8u <= e; u += 8u) {
             uint64_t x[8];
 #pragma unroll
-            for (int q = 0; q < 8; q++) x[q] = sk[u + q];
+            for (int r = 0; r < 8; r++) x[r] = sk[u - p0 + r];
 #pragma unroll
-            for (int q = 0; q < 8; q++) c += x[q] <= ks ? 1u : 0u;
+            for (int r = 0; r < 8; r++) c += x[r] <= ks ? 1u : 0u;
         }
-        for (; u < e; u++) c += sk[u] <= ks ? 1u : 0u;
+        for (; u < e; u++) c += sk[u - p0] <= ks ? 1u : 0u;
     }
     {
         const uint32_t b0 = u0 > s0 ? u0 : s0, b1 = u1 < s0 + 64u ? u1 : s0 + 64u;
         for (uint32_t u = b0; u < b1; u++) {
-            const uint64_t x = sk[u];
+            const uint64_t x = sk[u - p0];
             c += (x < ks || (x == ks && u < s)) ? 1u : 0u;
         }
     }
@@ -293,21 +292,33 @@ __global__ __launch_bounds__(kSmT) void k_ls_sample(LsArgs a)
         for (; u + 8u <= u1; u += 8u) {
             uint64_t x[8];
 #pragma unroll
-            for (int q = 0; q < 8; q++) x[q] = sk[u + q];
+            for (int r = 0; r < 8; r++) x[r] = sk[u - p0 + r];
 #pragma unroll
-            for (int q = 0; q < 8; q++) c += x[q] < ks ? 1u : 0u;
+            for (int r = 0; r < 8; r++) c += x[r] < ks ? 1u : 0u;
         }
-        for (; u < u1; u++) c += sk[u] < ks ? 1u : 0u;
+        for (; u < u1; u++) c += sk[u - p0] < ks ? 1u : 0u;
     }
     part[w][lane] = c;
     __syncthreads();
     if (w == 0) {
         uint32_t r = 0;
 #pragma unroll
-        for (int q = 0; q < kSmW; q++) r += part[q][lane];
-        R.smp_k[r] = ks;
-        R.smp_j[r] = ls_pos(s, n, S);
+        for (int qq = 0; qq < kSmW; qq++) r += part[qq][lane];
+        R.rpart[(uint64_t)pq * S + s] = r;
     }
+}
+
+// Each sample at its rank (the sum of its parts' counts).
+__global__ __launch_bounds__(256) void k_ls_place(LsArgs a)
+{
+    const LsRow &R = a.r[blockIdx.y];
+    const uint32_t s = blockIdx.x * 256u + threadIdx.x, S = R.S;
+    if (s >= S) return;
+    uint32_t r = 0;
+#pragma unroll
+    for (uint32_t p = 0; p < kSmP; p++) r += R.rpart[(uint64_t)p * S + s];
+    R.smp_k[r] = R.raw_k[s];
+    R.smp_j[r] = ls_pos(s, a.n, S);
 }
 
 // The splitters in breadth-first (Eytzinger) order of a complete search tree
@@ -581,6 +592,7 @@ __global__ __launch_bounds__(kTT) void k_ls_scatter(LsArgs a)
     __shared__ uint32_t h[kLsMaxB], texcl[kLsMaxB], gb[kLsMaxB];
     __shared__ uint64_t lk[kTile];
     __shared__ uint32_t lj[kTile];
+    __shared__ uint16_t lb[kTile];
     __shared__ uint32_t wsum[kTT / 64];
     __shared__ uint32_t pwc[kTT / 64][kQ];
     __shared__ WrrPlanHead wh;
@@ -624,22 +636,6 @@ __global__ __launch_bounds__(kTT) void k_ls_scatter(LsArgs a)
     gb[b0] = rs + (b0 < B ? row[b0] : 0u);
     gb[b1] = rs + z0 + (b1 < B ? row[b1] : 0u);
     __syncthreads();
-    // the payloads ride along (read in sequence order, written at the
-    // entry's slot), so that the bucket sort gathers nothing
-    if (R.rv || R.rt) {
-#pragma unroll
-        for (int r = 0; r < kTR; r++) {
-            const uint32_t idx = (uint32_t)r * kTT + t;
-            if (idx < cnt) {
-                const uint32_t g = gb[b[r]] + sl[r], j = base + idx;
-                if (R.rv) R.rv[g] = ls_value(a, R, j);
-                if (R.rt) {
-                    R.rt[g] = a.in.tier[j];
-                    if (R.rb) R.rb[g] = a.in.budget[j];
-                }
-            }
-        }
-    }
 #pragma unroll
     for (int r = 0; r < kTR; r++) {
         const uint32_t idx = (uint32_t)r * kTT + t;
@@ -650,11 +646,42 @@ __global__ __launch_bounds__(kTT) void k_ls_scatter(LsArgs a)
         }
     }
     __syncthreads();
+    const bool pay = R.rv || R.rt;
     for (uint32_t s = t; s < cnt; s += kTT) {
         const uint32_t x = lj[s], bb = x >> kJBits;
         const uint32_t g = gb[bb] + (s - texcl[bb]);   // < n: a region holds its bucket's pairs
         R.rk[0][g] = lk[s];
         R.rj[0][g] = x & kJMask;
+        if (pay) lb[s] = (uint16_t)bb;
+    }
+    if (!pay) return;
+    // the payloads ride along the same way (read in sequence order, staged
+    // in the same places, written in the same runs), so that the bucket sort
+    // gathers nothing: the value of a sort over in.fifo, or the FIFO sort's
+    // tier and budget
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < kTR; r++) {
+        const uint32_t idx = (uint32_t)r * kTT + t;
+        if (idx < cnt) {
+            const uint32_t p = texcl[b[r]] + sl[r], j = base + idx;
+            if (R.rv) {
+                lj[p] = ls_value(a, R, j);
+            } else {
+                lj[p] = a.in.tier[j];
+                if (R.rb) lk[p] = (uint64_t)__double_as_longlong(a.in.budget[j]);
+            }
+        }
+    }
+    __syncthreads();
+    for (uint32_t s = t; s < cnt; s += kTT) {
+        const uint32_t bb = lb[s], g = gb[bb] + (s - texcl[bb]);
+        if (R.rv) {
+            R.rv[g] = lj[s];
+        } else {
+            R.rt[g] = (uint8_t)lj[s];
+            if (R.rb) R.rb[g] = __longlong_as_double((long long)lk[s]);
+        }
     }
 }
 
@@ -1041,7 +1068,8 @@ size_t lsort_ws_bytes(uint64_t n, uint32_t nsort, uint32_t npart)
     if (n <= kSsMaxN || n > kLsMaxN) return 0;
     const LsLayout l = ls_layout(n);
     const uint64_t sort = 2 * align_up(l.B * 4, 256) + align_up((uint64_t)l.tiles * l.B * 4, 256) +
-                          2 * align_up(l.S * 8, 256) + align_up(l.S * 4, 256) + align_up(n * 2, 256) +
+                          2 * align_up(l.S * 8, 256) + align_up(l.S * 4, 256) + align_up(kSmP * l.S * 4, 256) +
+                          align_up(n * 2, 256) +
                           2 * (align_up(n * 8, 256) + align_up(n * 4, 256)) +
                           align_up(n * 4, 256) + align_up(n, 256) + align_up(n * 8, 256);   // payloads
     const uint64_t part = 2 * align_up((kQ + 1) * 4, 256) + align_up((uint64_t)l.tiles * kQ * 4, 256);
@@ -1101,6 +1129,7 @@ hipError_t lsort_launch(const SortInput &in, const SortJob *jobs, uint32_t njobs
             R.start = reinterpret_cast<uint32_t *>(take(l.B * 4));
             R.tcnt = reinterpret_cast<uint32_t *>(take((uint64_t)l.tiles * l.B * 4));
             R.raw_k = reinterpret_cast<uint64_t *>(take(l.S * 8));
+            R.rpart = reinterpret_cast<uint32_t *>(take(kSmP * l.S * 4));
             R.smp_k = reinterpret_cast<uint64_t *>(take(l.S * 8));
             R.smp_j = reinterpret_cast<uint32_t *>(take(l.S * 4));
             R.bid = reinterpret_cast<uint16_t *>(take(n * 2));
@@ -1121,7 +1150,8 @@ hipError_t lsort_launch(const SortInput &in, const SortJob *jobs, uint32_t njobs
     const uint32_t maxb = a.nsort ? l.B : kQ;
     if (a.nsort) {
         hipLaunchKernelGGL(k_ls_gather, dim3(cdiv(l.S, 256), a.nsort), dim3(256), 0, s, a);
-        hipLaunchKernelGGL(k_ls_sample, dim3(l.S / 64, a.nsort), dim3(kSmT), 0, s, a);
+        hipLaunchKernelGGL(k_ls_sample, dim3(l.S / 64 * kSmP, a.nsort), dim3(kSmT), 0, s, a);
+        hipLaunchKernelGGL(k_ls_place, dim3(cdiv(l.S, 256), a.nsort), dim3(256), 0, s, a);
     }
     hipLaunchKernelGGL(k_ls_count, dim3(l.tiles, a.nrows), dim3(kTT), 0, s, a);
     hipLaunchKernelGGL(k_ls_scan, dim3(cdiv(maxb, 64), a.nrows), dim3(kScT), 0, s, a);
