@@ -105,8 +105,9 @@ typedef enum {
  * Bounded waits. The sorts behind ds_order, ds_order_multi, ds_calibrate
  * (above 4096 groups) and ds_simulate split their work into tiles that wait,
  * each for at most about 0.2 s, on counts published by tiles of smaller
- * index (decoupled look-back). In normal operation no wait runs out (a tile
- * waits only on tiles that have already started). If one does:
+ * index (decoupled look-back); the orders of more than 2^18 and at most
+ * 2^20 requests have no such waits. In normal operation no wait runs out (a
+ * tile waits only on tiles that have already started). If one does:
  *  - in a sample-sort scatter (up to 2^18 requests), the call finishes on
  *    the single-workgroup path instead, with exact results;
  *  - anywhere else the results are invalid, and the call's status word is
