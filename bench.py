@@ -671,15 +671,12 @@ def bench_simulate(args, wl):
     res = {"metric": "dispatch-tick loop: ticks/s and requests dispatched/s",
            "config": {"workload": wl.name, "requests": N, "ticks": len(ticks), "batch": 32,
                       "tick_s": 0.01}, "policies": {}}
-    # at a million requests and more the pending set outgrows the SJF list
-    # engine (one pass over it per tick): the tier-queue policies only
-    big = N > (1 << 20)
     steps = max(1, args.steps // 10)
     a2 = argparse.Namespace(**dict(vars(args), steps=steps, warmup=1, settle=0.0))
     # every policy (and the other two Weighted interleavings) in one launch
     kw = dict(alpha=b.alphas[0], weights=tuple(int(w) for w in b.weights),
               tier_priority=tuple(b.tier_priority), aging_rate=b.aging_rate)
-    runs = [(name, pol, "blocked") for name, pol in ds.POLICIES.items() if not (big and pol == ds.SJF)] + \
+    runs = [(name, pol, "blocked") for name, pol in ds.POLICIES.items()] + \
         [("weighted_smooth", ds.WEIGHTED, "smooth"), ("weighted_stride", ds.WEIGHTED, "stride")]
     mparams = [ds.sim_params(pol, batch=32, weighted_mode=m, **kw) for _, pol, m in runs]
     mstates = [torch.ones(b.n_groups, dtype=torch.float64, device="cuda") for _ in runs]
@@ -697,8 +694,6 @@ def bench_simulate(args, wl):
                          "dispatched": [int(x) for x in nd_multi.cpu()],
                          "ticks_per_s_per_run": round(len(ticks) / (ms_multi * 1e-3), 1)}
     for name, pol in ds.POLICIES.items():
-        if big:
-            break
         p = ds.sim_params(pol, batch=32, alpha=b.alphas[0], weights=tuple(int(w) for w in b.weights),
                           tier_priority=tuple(b.tier_priority), aging_rate=b.aging_rate,
                           weighted_mode=args.weighted_mode)

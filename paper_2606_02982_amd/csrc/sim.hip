@@ -93,6 +93,12 @@ struct EngineArgs {
     const uint32_t *rpos, *rstart;
     uint64_t *cand_k;
     uint32_t *cand_j, *cand_i;
+    // the class engine (SJF): each class's head bound, the pending bitmap over
+    // the class lists, rebuild keys
+    uint32_t *cls_head;
+    uint64_t *cls_elig, *cls_kk;
+    uint32_t *cls_kj;
+    double f_ref;
 };
 
 // Several runs share one launch: run r is block row r of the setup and block
@@ -103,7 +109,7 @@ struct SetupBatch {
 struct EngineBatch {
     EngineArgs r[kSimMaxRuns];
 };
-static_assert(sizeof(SetupBatch) <= 4096 && sizeof(EngineBatch) <= 4096, "kernel arguments within 4 KB");
+static_assert(sizeof(SetupBatch) <= 4096, "kernel arguments within 4 KB");
 
 __global__ void k_sim_setup(SetupBatch sb)
 {
@@ -186,29 +192,53 @@ __device__ __forceinline__ uint32_t pair_digit(uint64_t K, uint32_t J, int d)
     return d >= 4 ? (uint32_t)(K >> (8 * (d - 4))) & 255u : (J >> (8 * d)) & 255u;
 }
 
-__device__ void engine_list(const EngineArgs &a)
-{
-    __shared__ uint32_t s_w[kNW];
-    __shared__ uint32_t s_hist[256];
-    __shared__ uint32_t s_vw[kNW][kMaxQ];
-    __shared__ uint32_t s_cnt[kMaxQ];
-    __shared__ uint32_t s_wt[kMaxQ];
-    __shared__ uint32_t s_pick[4];
-    __shared__ uint64_t s_kmin[kNW], s_kmax[kNW];
-    __shared__ uint32_t s_selpos[kSimMaxBatch];
-    __shared__ uint64_t s_selK[kSimMaxBatch];
-    __shared__ uint32_t s_selJ[kSimMaxBatch];
-    __shared__ uint32_t s_evg[kSimMaxBatch], s_evo[kSimMaxBatch];
-    __shared__ double s_evx[kSimMaxBatch];
+// LDS of the list engine.
+struct ListLds {
+    uint32_t s_w[kNW];
+    uint32_t s_hist[256];
+    uint32_t s_vw[kNW][kMaxQ];
+    uint32_t s_cnt[kMaxQ];
+    uint32_t s_wt[kMaxQ];
+    uint32_t s_pick[4];
+    uint64_t s_kmin[kNW], s_kmax[kNW];
+    uint32_t s_selpos[kSimMaxBatch];
+    uint64_t s_selK[kSimMaxBatch];
+    uint32_t s_selJ[kSimMaxBatch];
+    uint32_t s_evg[kSimMaxBatch], s_evo[kSimMaxBatch];
+    double s_evx[kSimMaxBatch];
     // Priority/Weighted: list positions of the first `batch` pending requests
     // of each queue; SJF/Aging: the radix select's candidates
-    __shared__ union {
+    union {
         uint32_t first[kMaxQ][kSimMaxBatch];
         struct {
             uint64_t k[kCand];
             uint32_t j[kCand];
         } cand;
     } s_big;
+};
+
+// The list engine from tick k0 on. A0 > 0: another engine ran the ticks
+// before k0 (FIFO positions below A0 have arrived, total0 requests have been
+// dispatched and carry their tick in tick_of); the pending list is rebuilt
+// from those.
+__device__ void engine_list(const EngineArgs &a, ListLds &L, uint32_t k0 = 0, uint32_t A0 = 0,
+                            uint32_t total0 = 0)
+{
+    auto &s_w = L.s_w;
+    auto &s_hist = L.s_hist;
+    auto &s_vw = L.s_vw;
+    auto &s_cnt = L.s_cnt;
+    auto &s_wt = L.s_wt;
+    auto &s_pick = L.s_pick;
+    auto &s_kmin = L.s_kmin;
+    auto &s_kmax = L.s_kmax;
+    auto &s_selpos = L.s_selpos;
+    auto &s_selK = L.s_selK;
+    auto &s_selJ = L.s_selJ;
+    auto &s_evg = L.s_evg;
+    auto &s_evo = L.s_evo;
+    auto &s_evx = L.s_evx;
+    auto &s_big = L.s_big;
 
     const uint32_t tid = threadIdx.x, lane = (uint32_t)lane_id(), w = tid >> 6;
     const uint32_t n = a.n, policy = a.policy, batch = a.batch, nq = a.n_q;
@@ -218,12 +248,27 @@ __device__ void engine_list(const EngineArgs &a)
     const double nan = __builtin_nan("");
     if (tid < kMaxQ) s_wt[tid] = a.weight[tid];
 
-    uint32_t cur = 0;     // list buffer holding the pending list
-    uint32_t P = 0;       // its entries (pending + last tick's dispatches)
-    uint32_t A = 0;       // FIFO positions appended so far
-    uint32_t total = 0;   // requests dispatched so far
+    uint32_t cur = 0;          // list buffer holding the pending list
+    uint32_t P = 0;            // its entries (pending + last tick's dispatches)
+    uint32_t A = A0;           // FIFO positions appended so far
+    uint32_t total = total0;   // requests dispatched so far
+    // resumed: the arrived requests not yet dispatched, in FIFO order
+    for (uint32_t c0 = 0; c0 < A0; c0 += kTPB) {
+        const uint32_t j = c0 + tid;
+        uint32_t id = 0;
+        bool keep = false;
+        if (j < A0) {
+            id = a.fifo[j];
+            id = id < n ? id : 0u;
+            keep = a.tick_of[id] < 0;
+        }
+        uint32_t tot;
+        const uint32_t off = block_scan(keep ? 1u : 0u, s_w, tot);
+        if (keep) a.list[0][P + off] = id;
+        P += tot;
+    }
     __syncthreads();
-    for (uint32_t k = 0; k < a.n_ticks; k++) {
+    for (uint32_t k = k0; k < a.n_ticks; k++) {
         const double t = a.tick_t[k];
         uint32_t *L = a.list[cur];
         uint32_t *Ln = a.list[cur ^ 1u];
@@ -543,12 +588,24 @@ __device__ void engine_list(const EngineArgs &a)
 // in every other tier's candidates, which are in key order) or placed by
 // the round-robin closed forms, so a tick costs O(tiers x batch) rather
 // than a pass over the pending set. Results equal the list engine's.
-__device__ void engine_queues(const EngineArgs &a)
+struct QueueLds {
+    uint32_t s_head[kMaxQ], s_tail[kMaxQ], s_cnt[kMaxQ], s_d[kMaxQ], s_wt[kMaxQ];
+    uint32_t s_sel[kSimMaxBatch];
+    uint32_t s_evg[kSimMaxBatch], s_evo[kSimMaxBatch];
+    double s_evx[kSimMaxBatch];
+};
+
+__device__ void engine_queues(const EngineArgs &a, QueueLds &Q)
 {
-    __shared__ uint32_t s_head[kMaxQ], s_tail[kMaxQ], s_cnt[kMaxQ], s_d[kMaxQ], s_wt[kMaxQ];
-    __shared__ uint32_t s_sel[kSimMaxBatch];
-    __shared__ uint32_t s_evg[kSimMaxBatch], s_evo[kSimMaxBatch];
-    __shared__ double s_evx[kSimMaxBatch];
+    auto &s_head = Q.s_head;
+    auto &s_tail = Q.s_tail;
+    auto &s_cnt = Q.s_cnt;
+    auto &s_d = Q.s_d;
+    auto &s_wt = Q.s_wt;
+    auto &s_sel = Q.s_sel;
+    auto &s_evg = Q.s_evg;
+    auto &s_evo = Q.s_evo;
+    auto &s_evx = Q.s_evx;
     const uint32_t tid = threadIdx.x, lane = (uint32_t)lane_id(), w = tid >> 6;
     const uint32_t n = a.n, policy = a.policy, batch = a.batch, nq = a.n_q;
     const double oma = 1.0 - a.alpha;
@@ -713,13 +770,658 @@ __device__ void engine_queues(const EngineArgs &a)
     if (tid == 0) a.n_dispatched[0] = total;
 }
 
-// One workgroup per run: the queue engine where the run has its tier runs,
-// else (SJF) the list engine.
-__global__ __launch_bounds__(kTPB) void k_sim_engine(EngineBatch eb)
+// ---- SJF on class lists ---------------------------------------------------------
+//
+// A class is the set of requests that share category, tenant and group.
+// Within a class T_base, S_tenant and the factor B are common, so the budget
+// of Eq. (1) with the estimate of Eq. (2), words + ((T_base B) S_tenant) F,
+// is a strictly increasing function of the word count while E = (T_base B)
+// S_tenant is finite and non-negative and the class's budgets stay at or
+// below 2^50: F = 1 + words / f_ref is non-decreasing for f_ref > 0, every
+// rounding step is monotone, and below 2^50 the rounded sum still moves
+// with each extra word. The class's part of the SJF order (budget, FIFO
+// position) is then its (words, FIFO position) order whatever the factors
+// do. So every class is sorted once, the pending requests are bits of a
+// bitmap over the class lists, and a class's key is the (budget, FIFO
+// position) of its first pending member, its head. A tick:
+//   * arrivals set their bits and pull their class's head back;
+//   * the classes touched since the last tick (arrivals, the last batch's
+//     dispatches, every class of a group whose factor the batch moved) get
+//     their keys recomputed;
+//   * a pool in LDS, sorted by key, holds every class whose key is at most
+//     tau, at most kPool of them; every other class's key is above tau (or
+//     it has no pending member). A touched class at or below tau enters, one
+//     above it leaves; past kPool entries tau drops to the last one kept.
+//     Should fewer than m pool classes remain (tau finite), every key is
+//     recomputed and the kPool smallest are chosen by a radix select;
+//   * the first m = min(batch, pending) requests of the order are in the
+//     windows of the m best classes of the pool: the class of rank r holds at
+//     most m - r of them (the r better heads come before all its members) and
+//     none after the m-th best head. The windows come from the bitmap, their
+//     budgets from the current factors; the candidates are sorted and the
+//     first m dispatched.
+// Every key computation checks the conditions above; if one fails, the run
+// goes on from that tick with the list engine, so the result is the same.
+
+constexpr uint32_t kClsMaxBatch = 32;   // larger batches: the list engine
+constexpr uint32_t kPool = 512;          // pool classes kept after a tick
+constexpr uint32_t kCS = 1024;           // sort buffers (pool + entries; candidates)
+constexpr uint32_t kHash = 2048;         // touched-class set (open addressing)
+constexpr uint32_t kDirtyMax = 1024;     // touched classes per tick before a rebuild
+constexpr uint32_t kNone = 0xFFFFFFFFu;
+constexpr double kBudgetTop = 0x1p50;
+static_assert(kClsMaxBatch * kClsMaxBatch == kTPB, "a thread per window slot");
+static_assert(kCS == kTPB && kPool < kCS, "a thread per sort entry");
+
+// The class structure of a launch's requests, shared by its SJF runs.
+struct ClassShared {
+    const uint32_t *ctl;             // [0]: classes C; [1]: non-zero if an input is out of range
+    const uint32_t *clist;           // request ids by (class, words, FIFO position)
+    const uint32_t *lw, *lf;         // words and FIFO position of each list entry
+    const uint32_t *pos_f, *cls_f;   // list position and class of each FIFO position
+    const double *arr_f;             // arrival of each FIFO position
+    const uint32_t *cstart;          // first list position of each class, then n
+    const double *ctb, *cs;          // T_base and S_tenant of each class
+    const uint32_t *cg;              // group of each class (non-decreasing)
+    const uint32_t *gfirst, *gend;   // the classes of that group
+};
+
+struct ClassLds {
+    uint64_t pk[kCS];                // pool: key, FIFO position of the head, class
+    uint32_t pj[kCS], pc[kCS];
+    uint64_t wk[kCS];                // candidates: key, FIFO position, window slot
+    uint32_t wj[kCS], wv[kCS];
+    uint32_t wpos[kClsMaxBatch][kClsMaxBatch];   // window of rank r: list positions
+    uint32_t wn[kClsMaxBatch], sc[kClsMaxBatch], last[kClsMaxBatch];
+    double sE[kClsMaxBatch];
+    uint32_t hash[kHash], dirty[kDirtyMax];
+    uint32_t cnt[4];                 // touched classes, overflow, pool entries, candidates
+    uint32_t hist[256], w[kNW], pick[4];
+    uint32_t evg[kClsMaxBatch], evo[kClsMaxBatch], evc[kClsMaxBatch];
+    double evx[kClsMaxBatch];
+};
+
+struct Resume {
+    uint32_t k, A, total;
+};
+
+__device__ __forceinline__ bool pair_lt(uint64_t k1, uint32_t j1, uint64_t k2, uint32_t j2)
 {
+    return k1 < k2 || (k1 == k2 && j1 < j2);
+}
+
+__device__ __forceinline__ uint64_t ld_relaxed64(const uint64_t *p)
+{
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Ascending bitonic sort of N (a power of two, at most 2 kTPB) pairs with a
+// payload, in LDS, by the whole block.
+__device__ void bitonic(uint64_t *k, uint32_t *j, uint32_t *v, uint32_t N)
+{
+    const uint32_t t = threadIdx.x;
+    for (uint32_t size = 2; size <= N; size <<= 1) {
+        for (uint32_t stride = size >> 1; stride > 0; stride >>= 1) {
+            __syncthreads();
+            if (t < (N >> 1)) {
+                const uint32_t lo = ((t & ~(stride - 1)) << 1) | (t & (stride - 1)), hi = lo + stride;
+                const uint64_t k1 = k[lo], k2 = k[hi];
+                const uint32_t j1 = j[lo], j2 = j[hi];
+                if (pair_lt(k2, j2, k1, j1) == ((lo & size) == 0)) {
+                    k[lo] = k2;
+                    k[hi] = k1;
+                    j[lo] = j2;
+                    j[hi] = j1;
+                    const uint32_t v1 = v[lo];
+                    v[lo] = v[hi];
+                    v[hi] = v1;
+                }
+            }
+        }
+    }
+    __syncthreads();
+}
+
+// Adds class c to the touched set. Callers check the count before each
+// insertion, so with at most kTPB threads inserting at once the table never
+// fills; past kDirtyMax members the set overflows (the next tick rebuilds).
+__device__ void mark_dirty(uint32_t c, ClassLds &S)
+{
+    if (*(volatile uint32_t *)&S.cnt[0] >= kDirtyMax) {
+        S.cnt[1] = 1;
+        return;
+    }
+    uint32_t h = (c * 0x9E3779B1u) >> 21;
+    for (;;) {
+        const uint32_t old = atomicCAS(&S.hash[h], kNone, c);
+        if (old == kNone) {
+            const uint32_t i = atomicAdd(&S.cnt[0], 1u);
+            if (i < kDirtyMax) S.dirty[i] = c;
+            else S.cnt[1] = 1;
+            return;
+        }
+        if (old == c) return;
+        h = (h + 1) & (kHash - 1);
+    }
+}
+
+__device__ __forceinline__ bool is_dirty(uint32_t c, const ClassLds &S)
+{
+    uint32_t h = (c * 0x9E3779B1u) >> 21;
+    for (;;) {
+        const uint32_t x = S.hash[h];
+        if (x == c) return true;
+        if (x == kNone) return false;
+        h = (h + 1) & (kHash - 1);
+    }
+}
+
+// Key of class c: (budget bits, FIFO position) of its first pending member,
+// all ones if it has none; the class's head moves up to that member. ok
+// turns false if the class breaks the conditions of its static order.
+__device__ void class_key(const EngineArgs &a, const ClassShared &cs, uint32_t c, uint64_t &K, uint32_t &J,
+                          bool &ok)
+{
+    const uint32_t b0 = cs.cstart[c], e = cs.cstart[c + 1];
+    const uint32_t h0 = ld_relaxed(&a.cls_head[c]);
+    uint32_t p = e;
+    if (h0 < e) {
+        uint32_t wi = h0 >> 6;
+        uint64_t bits = ld_relaxed64(&a.cls_elig[wi]) & (~0ull << (h0 & 63u));
+        for (;;) {
+            if (bits) {
+                p = wi * 64u + (uint32_t)__ffsll((unsigned long long)bits) - 1u;
+                break;
+            }
+            wi++;
+            if ((uint64_t)wi * 64u >= e) break;
+            bits = ld_relaxed64(&a.cls_elig[wi]);
+        }
+        if (p > e) p = e;
+        if (p != h0) st_relaxed(&a.cls_head[c], p);
+    }
+    const double B = a.state[cs.cg[c]];
+    double E = cs.ctb[c] * B;
+    E = E * cs.cs[c];
+    const double wmax = (double)cs.lw[e > b0 ? e - 1 : b0];
+    double top = E * (1.0 + wmax / a.f_ref);
+    top = wmax + top;
+    if (!(E >= 0.0 && top <= kBudgetTop)) ok = false;
+    if (p >= e) {
+        K = ~0ull;
+        J = kNone;
+        return;
+    }
+    const double wd = (double)cs.lw[p];
+    double b = E * (1.0 + wd / a.f_ref);
+    b = wd + b;
+    K = ordered_bits(b);
+    J = cs.lf[p];
+}
+
+// (TK, TJ) with exactly `need` of the C pairs (kk, kj) at or below it, need
+// at most the number of finite pairs: an MSD radix select over the 96-bit
+// pair, a byte per pass, until the bucket of the need-th pair is exactly
+// what remains to select.
+__device__ void select_pairs(const uint64_t *kk, const uint32_t *kj, uint32_t C, uint32_t need, uint64_t &TK,
+                             uint32_t &TJ, ClassLds &S)
+{
+    uint64_t mK = 0;
+    uint32_t mJ = 0;
+    TK = 0;
+    TJ = 0;
+    for (int d = 11; d >= 0; d--) {
+        if (threadIdx.x < 256) S.hist[threadIdx.x] = 0;
+        __syncthreads();
+        for (uint32_t c = threadIdx.x; c < C; c += kTPB) {
+            const uint64_t K = kk[c];
+            const uint32_t J = kj[c];
+            if ((K & mK) == TK && (J & mJ) == TJ) atomicAdd(&S.hist[pair_digit(K, J, d)], 1u);
+        }
+        __syncthreads();
+        const uint32_t h = threadIdx.x < 256 ? S.hist[threadIdx.x] : 0u;
+        uint32_t tot;
+        const uint32_t ex = block_scan(h, S.w, tot);
+        if (threadIdx.x < 256 && ex < need && need <= ex + h) {
+            S.pick[0] = threadIdx.x;
+            S.pick[1] = ex;
+            S.pick[2] = h;
+        }
+        __syncthreads();
+        const uint32_t b = S.pick[0], cb = S.pick[2];
+        need -= S.pick[1];
+        __syncthreads();
+        if (d >= 4) {
+            TK |= (uint64_t)b << (8 * (d - 4));
+            mK |= 0xFFull << (8 * (d - 4));
+        } else {
+            TJ |= b << (8 * d);
+            mJ |= 0xFFu << (8 * d);
+        }
+        if (cb == need) {
+            // the whole bucket: up to its largest possible pair
+            if (d >= 4) {
+                TK |= (1ull << (8 * (d - 4))) - 1ull;
+                TJ = kNone;
+            } else {
+                TJ |= (1u << (8 * d)) - 1u;
+            }
+            return;
+        }
+    }
+}
+
+// Sorts the first N0 entries of a sort buffer (padding to a power of two).
+__device__ void sort_prefix(uint64_t *k, uint32_t *j, uint32_t *v, uint32_t N0)
+{
+    uint32_t N = 1;
+    while (N < N0) N <<= 1;
+    __syncthreads();
+    if (threadIdx.x >= N0 && threadIdx.x < N) {
+        k[threadIdx.x] = ~0ull;
+        j[threadIdx.x] = kNone;
+        v[threadIdx.x] = kNone;
+    }
+    bitonic(k, j, v, N);
+}
+
+// SJF ticks on the class lists. Returns where the list engine must take
+// over (k = n_ticks: every tick done, n_dispatched written).
+__device__ Resume engine_class(const EngineArgs &a, const ClassShared &cs, ClassLds &S)
+{
+    const uint32_t tid = threadIdx.x, lane = (uint32_t)lane_id(), w = tid >> 6;
+    const uint32_t n = a.n, batch = a.batch;
+    const double oma = 1.0 - a.alpha;
+    const uint32_t C = cs.ctl[0];
+    if (cs.ctl[1] != 0 || C == 0) return Resume{0, 0, 0};
+    for (uint32_t c = tid; c < C; c += kTPB) a.cls_head[c] = cs.cstart[c + 1];
+    for (uint32_t i = tid; i < (n + 63u) / 64u; i += kTPB) a.cls_elig[i] = 0;
+    for (uint32_t i = tid; i < kHash; i += kTPB) S.hash[i] = kNone;
+    if (tid < 4) S.cnt[tid] = 0;
+    bool ok = true;
+    __syncthreads();
+    for (uint32_t c = tid; c < C; c += kTPB) {
+        uint64_t K;
+        uint32_t J;
+        class_key(a, cs, c, K, J, ok);   // every head is the class end: the checks alone
+    }
+    if (__syncthreads_or(!ok)) return Resume{0, 0, 0};
+
+    uint32_t np = 0;                          // pool entries
+    uint64_t tK = ~0ull;                      // tau (all ones: every class with a key is in the pool)
+    uint32_t tJ = kNone;
+    uint32_t A = 0, P = 0, total = 0;         // FIFO positions arrived, pending, dispatched
+    for (uint32_t k = 0; k < a.n_ticks; k++) {
+        const double t = a.tick_t[k];
+        // 1. arrivals: a prefix of the rest of the FIFO order
+        while (A < n) {
+            const uint32_t j = A + tid;
+            const bool arrived = j < n && cs.arr_f[j] <= t;
+            const uint32_t c = (uint32_t)__syncthreads_count(arrived);
+            if (arrived) {
+                const uint32_t p = cs.pos_f[j], cl = cs.cls_f[j];
+                atomicOr((unsigned long long *)&a.cls_elig[p >> 6], 1ull << (p & 63u));
+                atomicMin(&a.cls_head[cl], p);
+                mark_dirty(cl, S);
+            }
+            A += c;
+            P += c;
+            __syncthreads();
+            if (c < kTPB) break;
+        }
+        const uint32_t m = P < batch ? P : batch;
+        if (m == 0) continue;   // uniform; the touched set carries over
+
+        // 2. keys of the touched classes into the pool, or a rebuild
+        bool rebuild = S.cnt[1] != 0;
+        if (!rebuild) {
+            const uint32_t nd = S.cnt[0];
+            for (uint32_t i = tid; i < nd; i += kTPB) {
+                const uint32_t c = S.dirty[i];
+                uint64_t K;
+                uint32_t J;
+                class_key(a, cs, c, K, J, ok);
+                if (K != ~0ull && !pair_lt(tK, tJ, K, J)) {
+                    const uint32_t slot = np + atomicAdd(&S.cnt[2], 1u);
+                    if (slot < kCS) {
+                        S.pk[slot] = K;
+                        S.pj[slot] = J;
+                        S.pc[slot] = c;
+                    }
+                }
+            }
+            for (uint32_t i = tid; i < np; i += kTPB)
+                if (is_dirty(S.pc[i], S)) {
+                    S.pk[i] = ~0ull;
+                    S.pj[i] = kNone;
+                }
+        }
+        if (__syncthreads_or(!ok)) return Resume{k, A, total};
+        const uint32_t nins = S.cnt[2];
+        __syncthreads();
+        // the touched set is consumed
+        for (uint32_t i = tid; i < kHash; i += kTPB) S.hash[i] = kNone;
+        if (tid < 3) S.cnt[tid] = 0;
+        if (!rebuild && np + nins <= kCS) {
+            sort_prefix(S.pk, S.pj, S.pc, np + nins);
+            const bool in = tid < np + nins && S.pk[tid] != ~0ull && !pair_lt(tK, tJ, S.pk[tid], S.pj[tid]);
+            uint32_t keep = (uint32_t)__syncthreads_count(in);
+            if (keep > kPool) {
+                keep = kPool;
+                tK = S.pk[kPool - 1];
+                tJ = S.pj[kPool - 1];
+            }
+            np = keep;
+            rebuild = np < m && tK != ~0ull;
+        } else {
+            rebuild = true;
+        }
+        if (rebuild) {
+            uint32_t fin = 0;
+            for (uint32_t c = tid; c < C; c += kTPB) {
+                uint64_t K;
+                uint32_t J;
+                class_key(a, cs, c, K, J, ok);
+                a.cls_kk[c] = K;
+                a.cls_kj[c] = J;
+                fin += K != ~0ull ? 1u : 0u;
+            }
+            if (__syncthreads_or(!ok)) return Resume{k, A, total};
+            block_scan(fin, S.w, fin);
+            uint64_t TK = ~0ull;
+            uint32_t TJ = kNone;
+            if (fin > kPool) select_pairs(a.cls_kk, a.cls_kj, C, kPool, TK, TJ, S);
+            if (tid == 0) S.cnt[2] = 0;
+            __syncthreads();
+            for (uint32_t c = tid; c < C; c += kTPB) {
+                const uint64_t K = a.cls_kk[c];
+                const uint32_t J = a.cls_kj[c];
+                if (K != ~0ull && !pair_lt(TK, TJ, K, J)) {
+                    const uint32_t slot = atomicAdd(&S.cnt[2], 1u);   // below kPool
+                    if (slot < kCS) {
+                        S.pk[slot] = K;
+                        S.pj[slot] = J;
+                        S.pc[slot] = c;
+                    }
+                }
+            }
+            __syncthreads();
+            np = S.cnt[2];
+            sort_prefix(S.pk, S.pj, S.pc, np);
+            tK = TK;
+            tJ = TJ;
+            if (tid == 0) S.cnt[2] = 0;
+        }
+
+        // 3. windows of the m best classes, a wave per class
+        const uint32_t R = m < np ? m : np;
+        for (uint32_t r = w; r < R; r += kNW) {
+            const uint32_t c = S.pc[r], e = cs.cstart[c + 1];
+            const uint32_t h = ld_relaxed(&a.cls_head[c]);
+            const uint32_t want = m - r;
+            uint32_t got = 0;
+            for (uint64_t wb = h >> 6; got < want && wb * 64u < e; wb += 64) {
+                const uint64_t wi = wb + lane;
+                uint64_t bits = 0;
+                if (wi * 64u < e) {
+                    bits = ld_relaxed64(&a.cls_elig[wi]);
+                    if (wi == (h >> 6)) bits &= ~0ull << (h & 63u);
+                    const uint64_t below = e - wi * 64u;
+                    if (below < 64) bits &= (1ull << below) - 1ull;
+                }
+                const uint32_t cnt = (uint32_t)__popcll(bits);
+                const uint32_t incl = wave_incl_scan_dpp(cnt);
+                uint32_t rank = got + incl - cnt;
+                while (bits && rank < want) {
+                    S.wpos[r][rank] = (uint32_t)(wi * 64u) + (uint32_t)__ffsll((unsigned long long)bits) - 1u;
+                    bits &= bits - 1ull;
+                    rank++;
+                }
+                const uint32_t tot = readlane32(incl, 63);
+                got = got + tot < want ? got + tot : want;
+            }
+            if (lane == 0) {
+                double E = cs.ctb[c] * a.state[cs.cg[c]];
+                E = E * cs.cs[c];
+                S.sE[r] = E;
+                S.wn[r] = got;
+                S.sc[r] = c;
+                S.last[r] = 0;
+            }
+        }
+        if (tid == 0) S.cnt[3] = 0;
+        __syncthreads();
+        {
+            const uint32_t r = tid >> 5, q = tid & 31u;
+            if (r < R && q < S.wn[r]) {
+                const uint32_t p = S.wpos[r][q];
+                const double wd = (double)cs.lw[p];
+                double b = S.sE[r] * (1.0 + wd / a.f_ref);
+                b = wd + b;
+                const uint64_t K = ordered_bits(b);
+                const uint32_t J = cs.lf[p];
+                // a member after the m-th best head is not among the first m
+                if (q == 0 || R < m || !pair_lt(S.pk[m - 1], S.pj[m - 1], K, J)) {
+                    const uint32_t slot = atomicAdd(&S.cnt[3], 1u);
+                    S.wk[slot] = K;
+                    S.wj[slot] = J;
+                    S.wv[slot] = tid;
+                }
+            }
+        }
+        __syncthreads();
+        const uint32_t nc = S.cnt[3];
+        if (nc < m) return Resume{k, A, total};   // not reached: the windows hold the first m
+        sort_prefix(S.wk, S.wj, S.wv, nc);
+
+        // 4. dispatch, and the completion events of the batch
+        if (tid < m) {
+            const uint32_t v = S.wv[tid], r = v >> 5, q = v & 31u;
+            const uint32_t p = S.wpos[r][q];
+            const uint32_t id = cs.clist[p];
+            if (total + tid < n) a.seq[total + tid] = id;
+            a.tick_of[id] = (int32_t)k;
+            atomicAnd((unsigned long long *)&a.cls_elig[p >> 6], ~(1ull << (p & 63u)));
+            atomicMax(&S.last[r], p + 1u);
+            S.evg[tid] = cs.cg[S.sc[r]];
+            S.evc[tid] = S.sc[r];
+            S.evx[tid] = a.est_base[id];
+            S.evo[tid] = a.observed[id];
+        }
+        __syncthreads();
+        // the classes served move their heads past what they dispatched
+        if (tid < R && S.last[tid]) {
+            st_relaxed(&a.cls_head[S.sc[tid]], S.last[tid]);
+            mark_dirty(S.sc[tid], S);
+        }
+        // 5. Eq. (5) with the ratio of Eq. (6), each group's events in
+        //    dispatch order; a group whose factor moved touches its classes
+        if (tid < m) {
+            const uint32_t g = S.evg[tid];
+            bool lead = true;
+            for (uint32_t r = 0; r < tid && lead; r++) lead = S.evg[r] != g;
+            if (lead) {
+                double c = a.state[g];
+                bool moved = false;
+                for (uint32_t r = tid; r < m; r++) {
+                    if (S.evg[r] != g) continue;
+                    const double x = S.evx[r];
+                    if (!(isfinite(x) && x > 0.0)) continue;
+                    const double ratio = (double)S.evo[r] / x;
+                    const double t1 = oma * c;
+                    const double t2 = a.alpha * ratio;
+                    c = t1 + t2;
+                    moved = true;
+                }
+                a.state[g] = c;
+                if (moved) {
+                    const uint32_t cl = S.evc[tid], g0 = cs.gfirst[cl], g1 = cs.gend[cl];
+                    if (g1 - g0 > kDirtyMax) S.cnt[1] = 1;
+                    else
+                        for (uint32_t u = g0; u < g1; u++) mark_dirty(u, S);
+                }
+            }
+        }
+        P -= m;
+        total += m;
+        __syncthreads();
+    }
+    if (tid == 0) a.n_dispatched[0] = total;
+    return Resume{a.n_ticks, A, total};
+}
+
+static_assert(sizeof(EngineBatch) + sizeof(ClassShared) <= 4096, "kernel arguments within 4 KB");
+
+// LDS of the three engines (a run uses one at a time).
+union EngineLds {
+    ListLds l;
+    QueueLds q;
+    ClassLds c;
+};
+
+// One workgroup per run: the queue engine where the run has its tier runs,
+// the class engine for SJF where it applies (the list engine taking over if
+// its conditions fail), else the list engine.
+__global__ __launch_bounds__(kTPB) void k_sim_engine(EngineBatch eb, ClassShared cs)
+{
+    __shared__ EngineLds lds;
     const EngineArgs &a = eb.r[blockIdx.x];
-    if (a.rpos) engine_queues(a);
-    else engine_list(a);
+    if (a.rpos) {
+        engine_queues(a, lds.q);
+    } else if (a.cls_head) {
+        const Resume r = engine_class(a, cs, lds.c);
+        __syncthreads();
+        if (r.k < a.n_ticks) engine_list(a, lds.l, r.k, r.A, r.total);
+    } else {
+        engine_list(a, lds.l);
+    }
+}
+
+// ---- class structure set-up (the class engine's) -------------------------------------
+
+struct ClassBuild {
+    uint32_t n, n_cat, n_tenants, n_groups;
+    const uint32_t *fifo, *counts, *tenant, *group;
+    const uint8_t *category;
+    const double *arrival, *t_base, *s_tenant;
+    uint32_t *ctl, *fpos, *clist, *lpos, *lw, *lf, *pos_f, *cls_f, *cls_pos, *cstart, *cg, *gfirst, *gend,
+        *bcnt;
+    double *wkey, *ckey, *arr_f, *ctb, *cs;
+};
+
+// FIFO position of each request; the two keys of the class sort (words,
+// then the class as one integer, both exact in a double); inputs out of range
+// leave the class engine out (ctl[1]).
+__global__ void k_cls_prep(const ClassBuild b)
+{
+    bool bad = false;
+    for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < b.n; i += gridDim.x * blockDim.x) {
+        const uint32_t id = b.fifo[i];
+        if (id < b.n) b.fpos[id] = i;
+        else bad = true;
+        const uint32_t cat = b.category[i], ten = b.tenant[i], g = b.group[i];
+        const bool ok = cat < b.n_cat && ten < b.n_tenants && g < b.n_groups;
+        bad = bad || !ok;
+        b.wkey[i] = (double)b.counts[i];
+        b.ckey[i] = ok ? (double)(((uint64_t)g * b.n_cat + cat) * b.n_tenants + ten) : 0.0;
+    }
+    if (bad) atomicOr(&b.ctl[1], 1u);
+}
+
+// Class boundaries of the sorted list, counted per block of kTPB positions;
+// each entry's words and FIFO position.
+__global__ __launch_bounds__(kTPB) void k_cls_mark(const ClassBuild b)
+{
+    const uint32_t p = blockIdx.x * kTPB + threadIdx.x;
+    bool first = false;
+    if (p < b.n) {
+        const uint32_t id = b.clist[p];
+        b.lpos[id] = p;
+        b.lw[p] = b.counts[id];
+        b.lf[p] = b.fpos[id];
+        first = p == 0 || b.ckey[id] != b.ckey[b.clist[p - 1]];
+    }
+    const uint32_t c = (uint32_t)__syncthreads_count(first);
+    if (threadIdx.x == 0) b.bcnt[blockIdx.x] = c;
+}
+
+// Exclusive scan of the block counts (one block); ctl[0] = the classes.
+__global__ __launch_bounds__(kTPB) void k_cls_scan(const ClassBuild b, uint32_t nb)
+{
+    __shared__ uint32_t s_w[kNW];
+    uint32_t run = 0;
+    for (uint32_t c0 = 0; c0 < nb; c0 += kTPB) {
+        const uint32_t i = c0 + threadIdx.x;
+        const uint32_t x = i < nb ? b.bcnt[i] : 0u;
+        uint32_t tot;
+        const uint32_t ex = block_scan(x, s_w, tot);
+        if (i < nb) b.bcnt[i] = run + ex;
+        run += tot;
+    }
+    if (threadIdx.x == 0) b.ctl[0] = run;
+}
+
+// Class of each list position; each class's first position and constants.
+__global__ __launch_bounds__(kTPB) void k_cls_ids(const ClassBuild b)
+{
+    __shared__ uint32_t s_w[kNW];
+    const uint32_t p = blockIdx.x * kTPB + threadIdx.x;
+    bool first = false;
+    uint32_t id = 0;
+    if (p < b.n) {
+        id = b.clist[p];
+        first = p == 0 || b.ckey[id] != b.ckey[b.clist[p - 1]];
+    }
+    uint32_t tot;
+    const uint32_t ex = block_scan(first ? 1u : 0u, s_w, tot);
+    if (p < b.n) {
+        const uint32_t c = b.bcnt[blockIdx.x] + ex + (first ? 1u : 0u) - 1u;
+        b.cls_pos[p] = c;
+        if (first) {
+            const double nan = __builtin_nan("");
+            const uint32_t cat = b.category[id], ten = b.tenant[id];
+            b.cstart[c] = p;
+            b.ctb[c] = cat < b.n_cat ? b.t_base[cat] : nan;
+            b.cs[c] = ten < b.n_tenants ? b.s_tenant[ten] : nan;
+            b.cg[c] = b.group[id];
+        }
+        if (p == b.n - 1) b.cstart[c + 1] = b.n;
+    }
+}
+
+// Each class's group range; list position, class and arrival of each FIFO
+// position.
+__global__ void k_cls_fin(const ClassBuild b)
+{
+    const uint32_t C = b.ctl[0];
+    const uint32_t stride = gridDim.x * blockDim.x;
+    for (uint32_t c = blockIdx.x * blockDim.x + threadIdx.x; c < C; c += stride) {
+        const uint32_t g = b.cg[c];
+        uint32_t lo = 0, hi = c;
+        while (lo < hi) {
+            const uint32_t mid = (lo + hi) >> 1;
+            if (b.cg[mid] < g) lo = mid + 1;
+            else hi = mid;
+        }
+        b.gfirst[c] = lo;
+        lo = c + 1;
+        hi = C;
+        while (lo < hi) {
+            const uint32_t mid = (lo + hi) >> 1;
+            if (b.cg[mid] <= g) lo = mid + 1;
+            else hi = mid;
+        }
+        b.gend[c] = lo;
+    }
+    for (uint32_t j = blockIdx.x * blockDim.x + threadIdx.x; j < b.n; j += stride) {
+        uint32_t id = b.fifo[j];
+        id = id < b.n ? id : 0u;
+        uint32_t p = b.lpos[id];
+        p = p < b.n ? p : 0u;   // the class list is a permutation of 0..n-1
+        b.pos_f[j] = p;
+        b.cls_f[j] = b.cls_pos[p];
+        b.arr_f[j] = b.arrival[id];
+    }
 }
 
 __global__ void k_sim_empty(uint32_t *__restrict__ n_dispatched, uint32_t n_runs)
@@ -753,15 +1455,42 @@ uint32_t grid_for(uint64_t n)
 
 constexpr uint64_t kCandBytes = (uint64_t)kMaxQ * kSimMaxBatch * (8 + 4 + 4);
 
+// The class structure: 13 arrays of n words (cstart has n + 1), 5 of n
+// doubles, the block counts and the control words.
+uint64_t cls_shared_bytes(uint64_t n)
+{
+    return 12 * align_up(n * 4, 256) + align_up((n + 1) * 4, 256) + 5 * align_up(n * 8, 256) +
+           align_up((n / kTPB + 1) * 4, 256) + 256;
+}
+
+// Per SJF run on the class engine: heads, the pending bitmap, rebuild keys.
+uint64_t cls_run_bytes(uint64_t n)
+{
+    return 2 * align_up(n * 4, 256) + align_up((n / 64 + 1) * 8, 256) + align_up(n * 8, 256);
+}
+
 size_t sim_ws_bytes(uint64_t n, uint32_t n_runs)
 {
-    // shared: fifo, the tier runs (positions and starts), then the FIFO sort
-    // and the partition (one after the other); per run: list x2, est_base,
-    // key, aux, val, the queue engine's candidates
+    // shared: fifo, the tier runs (positions and starts), the class structure,
+    // then the FIFO sort, the class sorts and the partition (one after the
+    // other); per run: list x2, est_base, key, aux, val, the queue engine's
+    // candidates, the class engine's state
     const uint64_t per = 2 * align_up(n * 4, 256) + 2 * align_up(n * 8, 256) +
-                         align_up(n * sizeof(Aux), 256) + align_up(n, 256) + kCandBytes;
+                         align_up(n * sizeof(Aux), 256) + align_up(n, 256) + kCandBytes + cls_run_bytes(n);
     const uint64_t sort = sort_ws_bytes(n, 1), part = am_partition_ws_bytes(n);
-    return 2 * align_up(n * 4, 256) + 256 + (uint64_t)(n_runs ? n_runs : 1) * per + (sort > part ? sort : part);
+    return 2 * align_up(n * 4, 256) + 256 + cls_shared_bytes(n) + (uint64_t)(n_runs ? n_runs : 1) * per +
+           (sort > part ? sort : part);
+}
+
+// SJF runs the class engine when its batches fit the windows, F is
+// non-decreasing in the words (f_ref > 0), the class key is exact in a
+// double and the run's index ranges are those the shared class structure
+// was built with (the first run's).
+bool class_engine_applies(const SimArgs &a, const SimArgs &a0)
+{
+    const double classes = (double)a.n_groups * (double)a.n_cat * (double)a.n_tenants;
+    return a.policy == kSjf && a.batch >= 1 && a.batch <= kClsMaxBatch && a.f_ref > 0.0 && classes < 0x1p52 &&
+           a.n_groups == a0.n_groups && a.n_cat == a0.n_cat && a.n_tenants == a0.n_tenants;
 }
 
 hipError_t sim_launch(const SimArgs *runs, uint32_t n_runs, void *ws, uint32_t *flag, hipStream_t s,
@@ -793,8 +1522,48 @@ hipError_t sim_launch(const SimArgs *runs, uint32_t n_runs, void *ws, uint32_t *
     uint32_t *rpos = reinterpret_cast<uint32_t *>(take((uint64_t)n * 4));
     uint32_t *rstart = reinterpret_cast<uint32_t *>(take(256));
     // every policy but SJF runs on the tier queues (up to the partition's limit)
-    bool any_queues = false;
-    for (uint32_t r = 0; r < n_runs; r++) any_queues = any_queues || (runs[r].policy != kSjf && n <= kAmMaxN);
+    bool any_queues = false, any_class = false;
+    for (uint32_t r = 0; r < n_runs; r++) {
+        any_queues = any_queues || (runs[r].policy != kSjf && n <= kAmMaxN);
+        any_class = any_class || class_engine_applies(runs[r], a0);
+    }
+    auto take32 = [&](uint64_t count) { return reinterpret_cast<uint32_t *>(take(count * 4)); };
+    auto take64 = [&](uint64_t count) { return reinterpret_cast<double *>(take(count * 8)); };
+    ClassBuild cb = {};
+    cb.n = n;
+    cb.n_cat = a0.n_cat;
+    cb.n_tenants = a0.n_tenants;
+    cb.n_groups = a0.n_groups;
+    cb.fifo = fifo;
+    cb.counts = a0.counts;
+    cb.tenant = a0.tenant;
+    cb.group = a0.group;
+    cb.category = a0.category;
+    cb.arrival = a0.arrival;
+    cb.t_base = a0.t_base;
+    cb.s_tenant = a0.s_tenant;
+    cb.ctl = reinterpret_cast<uint32_t *>(take(256));
+    cb.fpos = take32(n);
+    cb.clist = take32(n);
+    cb.lpos = take32(n);
+    cb.lw = take32(n);
+    cb.lf = take32(n);
+    cb.pos_f = take32(n);
+    cb.cls_f = take32(n);
+    cb.cls_pos = take32(n);
+    cb.cstart = take32((uint64_t)n + 1);
+    cb.cg = take32(n);
+    cb.gfirst = take32(n);
+    cb.gend = take32(n);
+    uint32_t *seq_words = take32(n);   // the requests by (words, FIFO position)
+    cb.bcnt = take32(n / kTPB + 1);
+    cb.wkey = take64(n);
+    cb.ckey = take64(n);
+    cb.arr_f = take64(n);
+    cb.ctb = take64(n);
+    cb.cs = take64(n);
+    const ClassShared cshared = {cb.ctl, cb.clist, cb.lw, cb.lf, cb.pos_f, cb.cls_f, cb.arr_f,
+                                 cb.cstart, cb.ctb, cb.cs, cb.cg, cb.gfirst, cb.gend};
     SetupBatch sb;
     EngineBatch eb;
     memset(&sb, 0, sizeof(sb));
@@ -808,6 +1577,10 @@ hipError_t sim_launch(const SimArgs *runs, uint32_t n_runs, void *ws, uint32_t *
         Aux *aux = reinterpret_cast<Aux *>(take((uint64_t)n * sizeof(Aux)));
         uint8_t *val = take(n);
         uint8_t *cand = take(kCandBytes);
+        uint32_t *cls_head = take32(n);
+        uint32_t *cls_kj = take32(n);
+        uint64_t *cls_elig = reinterpret_cast<uint64_t *>(take64(n / 64 + 1));
+        uint64_t *cls_kk = reinterpret_cast<uint64_t *>(take64(n));
 
         SetupArgs &su = sb.r[r];
         su.n = n;
@@ -876,6 +1649,13 @@ hipError_t sim_launch(const SimArgs *runs, uint32_t n_runs, void *ws, uint32_t *
             ea.cand_j = reinterpret_cast<uint32_t *>(cand + (uint64_t)kMaxQ * kSimMaxBatch * 8);
             ea.cand_i = reinterpret_cast<uint32_t *>(cand + (uint64_t)kMaxQ * kSimMaxBatch * 12);
         }
+        if (class_engine_applies(a, a0)) {
+            ea.cls_head = cls_head;
+            ea.cls_elig = cls_elig;
+            ea.cls_kk = cls_kk;
+            ea.cls_kj = cls_kj;
+        }
+        ea.f_ref = a.f_ref;
     }
     void *sort_ws = p;
     hipLaunchKernelGGL(k_sim_setup, dim3(grid_for(n), n_runs), dim3(256), 0, s, sb);
@@ -888,6 +1668,33 @@ hipError_t sim_launch(const SimArgs *runs, uint32_t n_runs, void *ws, uint32_t *
     SortJob job = {SortKind::Fifo, 64, nullptr, fifo};
     hipError_t e = sort_launch(in, &job, 1, sort_ws, s);
     if (e != hipSuccess) return e;
+    if (any_class) {
+        // the class lists: the FIFO sequence sorted stably by words, then by
+        // class (the sort's workspace is free again on the stream)
+        e = fill_u32(cb.ctl, 0u, 2, s);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(k_cls_prep, dim3(grid_for(n)), dim3(256), 0, s, cb);
+        SortInput cin = {};
+        cin.n = n;
+        cin.wait = in.wait;
+        cin.fifo = fifo;
+        cin.budget = cb.wkey;
+        SortJob cj = {SortKind::Budget, 64, nullptr, seq_words};
+        e = sort_launch(cin, &cj, 1, sort_ws, s);
+        if (e != hipSuccess) return e;
+        cin.fifo = seq_words;
+        cin.budget = cb.ckey;
+        cj.out = cb.clist;
+        e = sort_launch(cin, &cj, 1, sort_ws, s);
+        if (e != hipSuccess) return e;
+        const uint32_t nb = (uint32_t)cdiv(n, kTPB);
+        hipLaunchKernelGGL(k_cls_mark, dim3(nb), dim3(kTPB), 0, s, cb);
+        hipLaunchKernelGGL(k_cls_scan, dim3(1), dim3(kTPB), 0, s, cb, nb);
+        hipLaunchKernelGGL(k_cls_ids, dim3(nb), dim3(kTPB), 0, s, cb);
+        hipLaunchKernelGGL(k_cls_fin, dim3(grid_for(n)), dim3(256), 0, s, cb);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
     if (any_queues) {
         // the FIFO sequence split by tier, each tier in FIFO order (the sort's
         // workspace is free again on the stream)
@@ -900,7 +1707,7 @@ hipError_t sim_launch(const SimArgs *runs, uint32_t n_runs, void *ws, uint32_t *
         e = am_partition(pin, rpos, rstart, sort_ws, s);
         if (e != hipSuccess) return e;
     }
-    hipLaunchKernelGGL(k_sim_engine, dim3(n_runs), dim3(kTPB), 0, s, eb);
+    hipLaunchKernelGGL(k_sim_engine, dim3(n_runs), dim3(kTPB), 0, s, eb, cshared);
     return hipGetLastError();
 }
 

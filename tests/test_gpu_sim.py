@@ -27,13 +27,15 @@ def ds():
 
 def run_gpu(ds, policy, arrival, tier, counts, category, tenant, group, observed, t_base,
             s_tenant, state, ticks, batch=32, alpha=0.1, weights=(4, 2, 1),
-            tier_priority=(0.0, 1.0, 2.0), aging_rate=0.01, aging_floor=0.0, validate=False):
+            tier_priority=(0.0, 1.0, 2.0), aging_rate=0.01, aging_floor=0.0, validate=False,
+            f_ref=1024.0):
     """(seq, n_dispatched, tick_of, state) from ds_simulate."""
     arrival = np.asarray(arrival, np.float64)
     print("simulate policy=%d n=%d ticks=%d batch=%d" % (policy, len(arrival), len(ticks), batch),
           flush=True)
     p = ds.sim_params(policy, batch=batch, alpha=alpha, n_tiers=len(weights), weights=weights,
-                      tier_priority=tier_priority, aging_rate=aging_rate, aging_floor=aging_floor)
+                      tier_priority=tier_priority, aging_rate=aging_rate, aging_floor=aging_floor,
+                      f_ref=f_ref)
     st = dev(np.asarray(state, np.float64).copy())
     seq, tick_of, nd = ds.simulate(dev(arrival), dev(np.asarray(tier, np.uint8)),
                                    dev(np.asarray(counts, np.uint32)),
@@ -49,15 +51,17 @@ def run_gpu(ds, policy, arrival, tier, counts, category, tenant, group, observed
 
 def both(ds, oracle, policy, arrival, tier, counts, category, tenant, group, observed, t_base,
          s_tenant, state, ticks, batch=32, alpha=0.1, weights=(4, 2, 1),
-         tier_priority=(0.0, 1.0, 2.0), aging_rate=0.01, aging_floor=0.0, validate=False):
+         tier_priority=(0.0, 1.0, 2.0), aging_rate=0.01, aging_floor=0.0, validate=False,
+         f_ref=1024.0):
     w_seq, w_tick, w_state = oracle.simulate(policy, arrival, tier, counts, category, tenant,
                                              group, observed, t_base, s_tenant, state, ticks,
                                              batch=batch, alpha=alpha, weights=weights,
                                              tier_priority=tier_priority, aging_rate=aging_rate,
-                                             aging_floor=aging_floor)
+                                             aging_floor=aging_floor, f_ref=f_ref)
     seq, nd, tick_of, got = run_gpu(ds, policy, arrival, tier, counts, category, tenant, group,
                                     observed, t_base, s_tenant, state, ticks, batch, alpha,
-                                    weights, tier_priority, aging_rate, aging_floor, validate)
+                                    weights, tier_priority, aging_rate, aging_floor, validate,
+                                    f_ref)
     assert nd == len(w_seq), "dispatched %d, oracle %d" % (nd, len(w_seq))
     if nd:
         bad = np.flatnonzero(seq[:nd] != w_seq)
@@ -262,7 +266,8 @@ def test_drift_workload_prefix(ds, oracle, policy):
     groups, drifting ratios) through 10 ms ticks of 32: the pending set grows
     (5,000 arrivals/s against 3,200 dispatches/s) to about 20,000 before the
     arrivals end. FIFO, Priority, Weighted and Aging run on the tier-queue
-    engine, SJF on the list engine."""
+    engine, SJF on the class lists (16,384 classes, more than its pool
+    holds)."""
     b = wl.load("drift4m", n=60000)
     ticks = synth.sim_ticks(b.arrival)
     seq, _, _ = both(ds, oracle, policy, b.arrival, b.tier, b.words, b.category, b.tenant,
@@ -270,6 +275,56 @@ def test_drift_workload_prefix(ds, oracle, policy):
                      batch=32, alpha=0.05, weights=tuple(int(w) for w in b.weights),
                      tier_priority=tuple(b.tier_priority), aging_rate=b.aging_rate)
     assert len(seq) == b.n
+
+
+def _class_case(name, rng):
+    """Inputs that drive SJF's class lists (requests sharing category, tenant
+    and group, each class in its static (words, FIFO) order) through each of
+    its paths."""
+    if name in ("class_conditions_fail_at_start", "class_conditions_fail_mid_run", "f_ref_infinite"):
+        x = random_inputs(11, 3000, G=3)
+        if name == "class_conditions_fail_at_start":
+            x["t_base"] = np.array([50.0, -100.0, 300.0, 800.0])    # (T_base B) S below zero
+        elif name == "class_conditions_fail_mid_run":
+            # category 0's tiny estimates push its groups' factors up by about
+            # 1e12 at the first completions; category 1's budgets then pass 2^50
+            x["t_base"] = np.array([1e-9, 1e9, 300.0, 800.0])
+        return x, np.linspace(0.05, 12.0, 200), 8
+    n = {"many_classes_at_once": 6000, "one_class": 20000, "one_group": 8000}[name]
+    x = dict(tier=rng.integers(0, 3, n).astype(np.uint8),
+             counts=rng.integers(0, 3000, n).astype(np.uint32),
+             observed=rng.integers(0, 4000, n).astype(np.uint32),
+             t_base=np.array([50.0, 100.0, 300.0, 800.0]))
+    if name == "many_classes_at_once":
+        # 6,000 classes arriving at the first tick, 2,000 to a group: every
+        # tick touches more classes than the pool takes and rebuilds it
+        x.update(arrival=np.zeros(n), category=rng.integers(0, 4, n).astype(np.uint8),
+                 tenant=np.arange(n, dtype=np.uint32), group=rng.integers(0, 3, n).astype(np.uint32),
+                 s_tenant=rng.uniform(0.5, 1.5, n), state=np.ones(3))
+        return x, np.linspace(0.0, 5.0, 40), 32
+    if name == "one_class":
+        z8, z32 = np.zeros(n, np.uint8), np.zeros(n, np.uint32)
+        x.update(arrival=np.sort(rng.uniform(0, 10, n)), category=z8, tenant=z32, group=z32,
+                 t_base=np.array([100.0]), s_tenant=np.array([1.0]), state=np.ones(1))
+        return x, np.linspace(0.01, 12.0, 700), 32
+    # one group, 4 x 40 classes: every completion moves every class's key
+    x.update(arrival=rng.uniform(0, 10, n), category=rng.integers(0, 4, n).astype(np.uint8),
+             tenant=rng.integers(0, 40, n).astype(np.uint32), group=np.zeros(n, np.uint32),
+             s_tenant=rng.uniform(0.5, 1.5, 40), state=np.array([1.0]))
+    return x, np.linspace(0.02, 12.0, 400), 16
+
+
+@pytest.mark.parametrize("name", ["many_classes_at_once", "one_class", "one_group",
+                                  "class_conditions_fail_at_start", "class_conditions_fail_mid_run",
+                                  "f_ref_infinite"])
+def test_sjf_class_lists(ds, oracle, name):
+    """SJF's tick loop keeps each class's members in their static order while
+    the conditions of that order hold (also with F = 1 for every prompt, an
+    infinite f_ref), and continues on the pending list from the tick where one
+    fails: every case gives the oracle's loop exactly."""
+    x, ticks, batch = _class_case(name, np.random.default_rng(len(name)))
+    f_ref = np.inf if name == "f_ref_infinite" else 1024.0
+    both(ds, oracle, SJF, ticks=ticks, batch=batch, alpha=0.5 if batch == 8 else 0.1, f_ref=f_ref, **x)
 
 
 @pytest.mark.parametrize("policy", [FIFO, PRIORITY, WEIGHTED, AGING])
