@@ -805,19 +805,18 @@ __device__ void engine_queues(const EngineArgs &a, QueueLds &Q)
 
 constexpr uint32_t kClsMaxBatch = 32;   // larger batches: the list engine
 constexpr uint32_t kPool = 512;          // pool classes kept after a tick
-constexpr uint32_t kCS = 1024;           // sort buffers (pool + entries; candidates)
 constexpr uint32_t kHash = 2048;         // touched-class set (open addressing)
 constexpr uint32_t kDirtyMax = 1024;     // touched classes per tick before a rebuild
+constexpr uint32_t kWin = kClsMaxBatch * kClsMaxBatch;   // window slots
 constexpr uint32_t kNone = 0xFFFFFFFFu;
 constexpr double kBudgetTop = 0x1p50;
-static_assert(kClsMaxBatch * kClsMaxBatch == kTPB, "a thread per window slot");
-static_assert(kCS == kTPB && kPool < kCS, "a thread per sort entry");
+static_assert(kWin == kTPB && kDirtyMax == kTPB && kPool < kTPB, "a thread per slot, entry and pool class");
 
 // The class structure of a launch's requests, shared by its SJF runs.
 struct ClassShared {
     const uint32_t *ctl;             // [0]: classes C; [1]: non-zero if an input is out of range
     const uint32_t *clist;           // request ids by (class, words, FIFO position)
-    const uint32_t *lw, *lf;         // words and FIFO position of each list entry
+    const uint32_t *lw, *lf, *lobs;  // words, FIFO position, observed length of each list entry
     const uint32_t *pos_f, *cls_f;   // list position and class of each FIFO position
     const double *arr_f;             // arrival of each FIFO position
     const uint32_t *cstart;          // first list position of each class, then n
@@ -826,19 +825,37 @@ struct ClassShared {
     const uint32_t *gfirst, *gend;   // the classes of that group
 };
 
+// Class entries are (key, FIFO position of the head, list position of the
+// head, class); keys are the budget bits.
 struct ClassLds {
-    uint64_t pk[kCS];                // pool: key, FIFO position of the head, class
-    uint32_t pj[kCS], pc[kCS];
-    uint64_t wk[kCS];                // candidates: key, FIFO position, window slot
-    uint32_t wj[kCS], wv[kCS];
+    uint64_t pk[2][kPool];           // the pool, sorted, in one half at a time
+    uint32_t pj[2][kPool], ph[2][kPool], pc[2][kPool];
+    uint32_t pdrop[kPool + 1];       // pool entries leaving before each index
+    uint64_t ek[kDirtyMax];          // the tick's entering classes, unsorted
+    uint32_t ej[kDirtyMax], eh[kDirtyMax], ec[kDirtyMax];
+    union {
+        struct {                     // the entering classes, sorted
+            uint64_t k[kDirtyMax];
+            uint32_t j[kDirtyMax], h[kDirtyMax], c[kDirtyMax];
+        } e;
+        struct {                     // window candidates
+            uint64_t k[kWin];
+            double x[kWin];          // the B-free estimate of Eq. (2)
+            uint32_t j[kWin], id[kWin], obs[kWin], slot[kWin];
+        } w;
+    } u;
+    uint32_t sel[kClsMaxBatch];      // the candidate of each dispatch place
     uint32_t wpos[kClsMaxBatch][kClsMaxBatch];   // window of rank r: list positions
-    uint32_t wn[kClsMaxBatch], sc[kClsMaxBatch], last[kClsMaxBatch];
-    double sE[kClsMaxBatch];
+    uint32_t wn[kClsMaxBatch], sc[kClsMaxBatch], sg[kClsMaxBatch], sgf[kClsMaxBatch], sge[kClsMaxBatch],
+        last[kClsMaxBatch];
+    double sB[kClsMaxBatch];         // the factor of each window's group
     uint32_t hash[kHash], dirty[kDirtyMax];
-    uint32_t cnt[4];                 // touched classes, overflow, pool entries, candidates
+    uint32_t cnt[4];                 // touched classes, overflow, entering classes, candidates
+    uint32_t fail;
     uint32_t hist[256], w[kNW], pick[4];
-    uint32_t evg[kClsMaxBatch], evo[kClsMaxBatch], evc[kClsMaxBatch];
+    uint32_t evg[kClsMaxBatch], evo[kClsMaxBatch], evr[kClsMaxBatch];
     double evx[kClsMaxBatch];
+    uint32_t rg0[64], roff[64], rtot; // classes touched by the factor updates: ranges
 };
 
 struct Resume {
@@ -855,9 +872,9 @@ __device__ __forceinline__ uint64_t ld_relaxed64(const uint64_t *p)
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Ascending bitonic sort of N (a power of two, at most 2 kTPB) pairs with a
-// payload, in LDS, by the whole block.
-__device__ void bitonic(uint64_t *k, uint32_t *j, uint32_t *v, uint32_t N)
+// Ascending bitonic sort of N (a power of two, at most 2 kTPB) pairs with two
+// payloads, in LDS, by the whole block.
+__device__ void bitonic(uint64_t *k, uint32_t *j, uint32_t *v, uint32_t *u, uint32_t N)
 {
     const uint32_t t = threadIdx.x;
     for (uint32_t size = 2; size <= N; size <<= 1) {
@@ -872,9 +889,11 @@ __device__ void bitonic(uint64_t *k, uint32_t *j, uint32_t *v, uint32_t N)
                     k[hi] = k1;
                     j[lo] = j2;
                     j[hi] = j1;
-                    const uint32_t v1 = v[lo];
+                    const uint32_t v1 = v[lo], u1 = u[lo];
                     v[lo] = v[hi];
                     v[hi] = v1;
+                    u[lo] = u[hi];
+                    u[hi] = u1;
                 }
             }
         }
@@ -916,14 +935,18 @@ __device__ __forceinline__ bool is_dirty(uint32_t c, const ClassLds &S)
     }
 }
 
-// Key of class c: (budget bits, FIFO position) of its first pending member,
-// all ones if it has none; the class's head moves up to that member. ok
-// turns false if the class breaks the conditions of its static order.
+// Key of class c: (budget bits, FIFO position) of its first pending member
+// and that member's list position H, all ones if it has none; the class's
+// head moves up to that member. ok turns false if the class breaks the
+// conditions of its static order.
 __device__ void class_key(const EngineArgs &a, const ClassShared &cs, uint32_t c, uint64_t &K, uint32_t &J,
-                          bool &ok)
+                          uint32_t &H, bool &ok)
 {
     const uint32_t b0 = cs.cstart[c], e = cs.cstart[c + 1];
+    const double tb = cs.ctb[c], s = cs.cs[c];
+    const double B = a.state[cs.cg[c]];
     const uint32_t h0 = ld_relaxed(&a.cls_head[c]);
+    const double wmax = (double)cs.lw[e > b0 ? e - 1 : b0];
     uint32_t p = e;
     if (h0 < e) {
         uint32_t wi = h0 >> 6;
@@ -940,13 +963,12 @@ __device__ void class_key(const EngineArgs &a, const ClassShared &cs, uint32_t c
         if (p > e) p = e;
         if (p != h0) st_relaxed(&a.cls_head[c], p);
     }
-    const double B = a.state[cs.cg[c]];
-    double E = cs.ctb[c] * B;
-    E = E * cs.cs[c];
-    const double wmax = (double)cs.lw[e > b0 ? e - 1 : b0];
+    double E = tb * B;
+    E = E * s;
     double top = E * (1.0 + wmax / a.f_ref);
     top = wmax + top;
     if (!(E >= 0.0 && top <= kBudgetTop)) ok = false;
+    H = p;
     if (p >= e) {
         K = ~0ull;
         J = kNone;
@@ -1011,22 +1033,71 @@ __device__ void select_pairs(const uint64_t *kk, const uint32_t *kj, uint32_t C,
     }
 }
 
-// Sorts the first N0 entries of a sort buffer (padding to a power of two).
-__device__ void sort_prefix(uint64_t *k, uint32_t *j, uint32_t *v, uint32_t N0)
+// Entries of a sorted array (k, j) of length len below the pair (K, J).
+__device__ __forceinline__ uint32_t count_below(const uint64_t *k, const uint32_t *j, uint32_t len, uint64_t K,
+                                                uint32_t J)
 {
-    uint32_t N = 1;
-    while (N < N0) N <<= 1;
-    __syncthreads();
-    if (threadIdx.x >= N0 && threadIdx.x < N) {
-        k[threadIdx.x] = ~0ull;
-        j[threadIdx.x] = kNone;
-        v[threadIdx.x] = kNone;
+    uint32_t lo = 0, hi = len;
+    while (lo < hi) {
+        const uint32_t mid = (lo + hi) >> 1;
+        if (pair_lt(k[mid], j[mid], K, J)) lo = mid + 1;
+        else hi = mid;
     }
-    bitonic(k, j, v, N);
+    return lo;
+}
+
+// Barrier for LDS traffic alone: global stores and atomics may still be in
+// flight (every global hand-over between waves inside a tick of the class
+// engine is ordered by a full __syncthreads instead).
+__device__ __forceinline__ void lds_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// block_scan with LDS barriers.
+__device__ __forceinline__ uint32_t lds_scan(uint32_t x, uint32_t *s_w, uint32_t &total)
+{
+    const uint32_t inc = wave_incl_scan_dpp(x);
+    const uint32_t w = threadIdx.x >> 6;
+    if (lane_id() == 63) s_w[w] = inc;
+    lds_sync();
+    uint32_t off = 0, tot = 0;
+#pragma unroll
+    for (uint32_t k = 0; k < kNW; k++) {
+        const uint32_t v = s_w[k];
+        off += k < w ? v : 0u;
+        tot += v;
+    }
+    lds_sync();
+    total = tot;
+    return off + inc - x;
+}
+
+// Pairs of (k, j)[0, len) below (K, J), counted by one wave (64 entries at a
+// time, a ballot each); stops counting at `limit`.
+__device__ __forceinline__ uint32_t rank_in(const uint64_t *k, const uint32_t *j, uint32_t len, uint64_t K,
+                                            uint32_t J, uint32_t limit)
+{
+    uint32_t r = 0;
+    for (uint32_t c0 = 0; c0 < len && r < limit; c0 += 64) {
+        const uint32_t u = c0 + (uint32_t)lane_id();
+        const bool below = u < len && pair_lt(k[u], j[u], K, J);
+        r += (uint32_t)__popcll(__ballot(below));
+    }
+    return r;
 }
 
 // SJF ticks on the class lists. Returns where the list engine must take
 // over (k = n_ticks: every tick done, n_dispatched written).
+//
+// Global memory between waves: the bitmap and the head bounds change by the
+// arrivals' atomics, which come after a full barrier (the last tick's
+// stores are done) and before another (the keys below see them); a key
+// computation tightens its class's head bound with a plain store, done by
+// the next tick's first barrier. A dispatch does not move head bounds (a
+// bound below the first pending member stays valid); it touches the class.
 __device__ Resume engine_class(const EngineArgs &a, const ClassShared &cs, ClassLds &S)
 {
     const uint32_t tid = threadIdx.x, lane = (uint32_t)lane_id(), w = tid >> 6;
@@ -1038,90 +1109,131 @@ __device__ Resume engine_class(const EngineArgs &a, const ClassShared &cs, Class
     for (uint32_t i = tid; i < (n + 63u) / 64u; i += kTPB) a.cls_elig[i] = 0;
     for (uint32_t i = tid; i < kHash; i += kTPB) S.hash[i] = kNone;
     if (tid < 4) S.cnt[tid] = 0;
+    if (tid == 0) S.fail = 0;
     bool ok = true;
     __syncthreads();
     for (uint32_t c = tid; c < C; c += kTPB) {
         uint64_t K;
-        uint32_t J;
-        class_key(a, cs, c, K, J, ok);   // every head is the class end: the checks alone
+        uint32_t J, H;
+        class_key(a, cs, c, K, J, H, ok);   // every head is the class end: the checks alone
     }
     if (__syncthreads_or(!ok)) return Resume{0, 0, 0};
 
-    uint32_t np = 0;                          // pool entries
+    uint32_t cur = 0, np = 0;                 // pool half and entries
     uint64_t tK = ~0ull;                      // tau (all ones: every class with a key is in the pool)
     uint32_t tJ = kNone;
     uint32_t A = 0, P = 0, total = 0;         // FIFO positions arrived, pending, dispatched
     for (uint32_t k = 0; k < a.n_ticks; k++) {
         const double t = a.tick_t[k];
         // 1. arrivals: a prefix of the rest of the FIFO order
-        while (A < n) {
+        for (;;) {
             const uint32_t j = A + tid;
-            const bool arrived = j < n && cs.arr_f[j] <= t;
+            bool arrived = false;
+            uint32_t p = 0, cl = 0;
+            if (j < n) {
+                arrived = cs.arr_f[j] <= t;
+                p = cs.pos_f[j];
+                cl = cs.cls_f[j];
+            }
             const uint32_t c = (uint32_t)__syncthreads_count(arrived);
             if (arrived) {
-                const uint32_t p = cs.pos_f[j], cl = cs.cls_f[j];
                 atomicOr((unsigned long long *)&a.cls_elig[p >> 6], 1ull << (p & 63u));
                 atomicMin(&a.cls_head[cl], p);
                 mark_dirty(cl, S);
             }
             A += c;
             P += c;
-            __syncthreads();
             if (c < kTPB) break;
         }
+        __syncthreads();
         const uint32_t m = P < batch ? P : batch;
         if (m == 0) continue;   // uniform; the touched set carries over
 
-        // 2. keys of the touched classes into the pool, or a rebuild
+        // 2. keys of the touched classes; those at or below tau enter the
+        //    pool, the pool's touched classes leave it
         bool rebuild = S.cnt[1] != 0;
         if (!rebuild) {
-            const uint32_t nd = S.cnt[0];
-            for (uint32_t i = tid; i < nd; i += kTPB) {
-                const uint32_t c = S.dirty[i];
+            if (tid < S.cnt[0]) {
+                const uint32_t c = S.dirty[tid];
                 uint64_t K;
-                uint32_t J;
-                class_key(a, cs, c, K, J, ok);
+                uint32_t J, H;
+                class_key(a, cs, c, K, J, H, ok);
                 if (K != ~0ull && !pair_lt(tK, tJ, K, J)) {
-                    const uint32_t slot = np + atomicAdd(&S.cnt[2], 1u);
-                    if (slot < kCS) {
-                        S.pk[slot] = K;
-                        S.pj[slot] = J;
-                        S.pc[slot] = c;
-                    }
+                    const uint32_t slot = atomicAdd(&S.cnt[2], 1u);
+                    S.ek[slot] = K;
+                    S.ej[slot] = J;
+                    S.eh[slot] = H;
+                    S.ec[slot] = c;
                 }
             }
-            for (uint32_t i = tid; i < np; i += kTPB)
-                if (is_dirty(S.pc[i], S)) {
-                    S.pk[i] = ~0ull;
-                    S.pj[i] = kNone;
-                }
+            const bool drop = tid < np && is_dirty(S.pc[cur][tid], S);
+            uint32_t dropped;
+            const uint32_t before = lds_scan(drop ? 1u : 0u, S.w, dropped);
+            if (tid <= np) S.pdrop[tid] = before;
         }
-        if (__syncthreads_or(!ok)) return Resume{k, A, total};
-        const uint32_t nins = S.cnt[2];
-        __syncthreads();
+        if (!ok) S.fail = 1;
+        lds_sync();
+        if (S.fail) return Resume{k, A, total};
+        const uint32_t nin = S.cnt[2];
         // the touched set is consumed
         for (uint32_t i = tid; i < kHash; i += kTPB) S.hash[i] = kNone;
-        if (tid < 3) S.cnt[tid] = 0;
-        if (!rebuild && np + nins <= kCS) {
-            sort_prefix(S.pk, S.pj, S.pc, np + nins);
-            const bool in = tid < np + nins && S.pk[tid] != ~0ull && !pair_lt(tK, tJ, S.pk[tid], S.pj[tid]);
-            uint32_t keep = (uint32_t)__syncthreads_count(in);
-            if (keep > kPool) {
-                keep = kPool;
-                tK = S.pk[kPool - 1];
-                tJ = S.pj[kPool - 1];
+        if (!rebuild) {
+            // the entering classes in order (ranked by counting), then merged
+            // with the pool's remaining classes into the other half
+            for (uint32_t i = w; i < nin; i += kNW) {
+                const uint64_t K = S.ek[i];
+                const uint32_t J = S.ej[i];
+                const uint32_t r = rank_in(S.ek, S.ej, nin, K, J, ~0u);
+                if (lane == 0) {
+                    S.u.e.k[r] = K;
+                    S.u.e.j[r] = J;
+                    S.u.e.h[r] = S.eh[i];
+                    S.u.e.c[r] = S.ec[i];
+                }
             }
-            np = keep;
+            lds_sync();
+            const uint32_t nx = cur ^ 1u, stay = np - S.pdrop[np];
+            if (tid < np && S.pdrop[tid + 1] == S.pdrop[tid]) {
+                const uint64_t K = S.pk[cur][tid];
+                const uint32_t J = S.pj[cur][tid];
+                const uint32_t pos = tid - S.pdrop[tid] + count_below(S.u.e.k, S.u.e.j, nin, K, J);
+                if (pos < kPool) {
+                    S.pk[nx][pos] = K;
+                    S.pj[nx][pos] = J;
+                    S.ph[nx][pos] = S.ph[cur][tid];
+                    S.pc[nx][pos] = S.pc[cur][tid];
+                }
+            }
+            if (tid < nin) {
+                const uint64_t K = S.u.e.k[tid];
+                const uint32_t J = S.u.e.j[tid];
+                const uint32_t lb = count_below(S.pk[cur], S.pj[cur], np, K, J);
+                const uint32_t pos = tid + lb - S.pdrop[lb];
+                if (pos < kPool) {
+                    S.pk[nx][pos] = K;
+                    S.pj[nx][pos] = J;
+                    S.ph[nx][pos] = S.u.e.h[tid];
+                    S.pc[nx][pos] = S.u.e.c[tid];
+                }
+            }
+            lds_sync();
+            cur = nx;
+            np = stay + nin;
+            if (np > kPool) {
+                np = kPool;
+                tK = S.pk[cur][kPool - 1];
+                tJ = S.pj[cur][kPool - 1];
+            }
             rebuild = np < m && tK != ~0ull;
-        } else {
-            rebuild = true;
         }
+        if (tid < 4) S.cnt[tid] = 0;
         if (rebuild) {
+            __syncthreads();
             uint32_t fin = 0;
             for (uint32_t c = tid; c < C; c += kTPB) {
                 uint64_t K;
-                uint32_t J;
-                class_key(a, cs, c, K, J, ok);
+                uint32_t J, H;
+                class_key(a, cs, c, K, J, H, ok);
                 a.cls_kk[c] = K;
                 a.cls_kj[c] = J;
                 fin += K != ~0ull ? 1u : 0u;
@@ -1131,39 +1243,73 @@ __device__ Resume engine_class(const EngineArgs &a, const ClassShared &cs, Class
             uint64_t TK = ~0ull;
             uint32_t TJ = kNone;
             if (fin > kPool) select_pairs(a.cls_kk, a.cls_kj, C, kPool, TK, TJ, S);
-            if (tid == 0) S.cnt[2] = 0;
             __syncthreads();
             for (uint32_t c = tid; c < C; c += kTPB) {
                 const uint64_t K = a.cls_kk[c];
                 const uint32_t J = a.cls_kj[c];
                 if (K != ~0ull && !pair_lt(TK, TJ, K, J)) {
                     const uint32_t slot = atomicAdd(&S.cnt[2], 1u);   // below kPool
-                    if (slot < kCS) {
-                        S.pk[slot] = K;
-                        S.pj[slot] = J;
-                        S.pc[slot] = c;
+                    if (slot < kPool) {
+                        S.pk[cur][slot] = K;
+                        S.pj[cur][slot] = J;
+                        S.ph[cur][slot] = ld_relaxed(&a.cls_head[c]);
+                        S.pc[cur][slot] = c;
                     }
                 }
             }
             __syncthreads();
-            np = S.cnt[2];
-            sort_prefix(S.pk, S.pj, S.pc, np);
+            np = S.cnt[2] < kPool ? S.cnt[2] : kPool;
+            uint32_t N = 1;
+            while (N < np) N <<= 1;
+            if (tid >= np && tid < N) {
+                S.pk[cur][tid] = ~0ull;
+                S.pj[cur][tid] = kNone;
+            }
+            bitonic(S.pk[cur], S.pj[cur], S.ph[cur], S.pc[cur], N);
             tK = TK;
             tJ = TJ;
             if (tid == 0) S.cnt[2] = 0;
         }
 
-        // 3. windows of the m best classes, a wave per class
+        // 3. the windows of the m best classes, two per wave (a half-wave
+        //    each): their pending members from the bitmap, their keys and
+        //    what a dispatch needs of them; none after the m-th best head is
+        //    among the first m
         const uint32_t R = m < np ? m : np;
-        for (uint32_t r = w; r < R; r += kNW) {
-            const uint32_t c = S.pc[r], e = cs.cstart[c + 1];
-            const uint32_t h = ld_relaxed(&a.cls_head[c]);
-            const uint32_t want = m - r;
+        lds_sync();
+        {
+            const uint32_t half = lane >> 5, hl = lane & 31u, r = w + kNW * half;
+            const bool act = r < R;
+            uint32_t h = 0, e = 0, want = 0;
+            double E = 0.0, TS = 0.0;
+            if (act) {
+                const uint32_t c = S.pc[cur][r];
+                h = S.ph[cur][r];
+                e = cs.cstart[c + 1];
+                want = m - r;
+                if (hl == 0) {
+                    const uint32_t g = cs.cg[c];
+                    const double tb = cs.ctb[c], s = cs.cs[c], B = a.state[g];
+                    S.sc[r] = c;
+                    S.sg[r] = g;
+                    S.sgf[r] = cs.gfirst[c];
+                    S.sge[r] = cs.gend[c];
+                    S.sB[r] = B;
+                    S.last[r] = 0;
+                    E = tb * B;
+                    E = E * s;
+                    TS = tb * s;
+                }
+            }
+            E = __shfl(E, (int)(lane & 32u), 64);
+            TS = __shfl(TS, (int)(lane & 32u), 64);
             uint32_t got = 0;
-            for (uint64_t wb = h >> 6; got < want && wb * 64u < e; wb += 64) {
-                const uint64_t wi = wb + lane;
+            for (uint64_t wb = h >> 6;; wb += 32) {
+                const bool need = act && got < want && wb * 64u < e;
+                if (!__any(need)) break;
+                const uint64_t wi = wb + hl;
                 uint64_t bits = 0;
-                if (wi * 64u < e) {
+                if (need && wi * 64u < e) {
                     bits = ld_relaxed64(&a.cls_elig[wi]);
                     if (wi == (h >> 6)) bits &= ~0ull << (h & 63u);
                     const uint64_t below = e - wi * 64u;
@@ -1171,80 +1317,77 @@ __device__ Resume engine_class(const EngineArgs &a, const ClassShared &cs, Class
                 }
                 const uint32_t cnt = (uint32_t)__popcll(bits);
                 const uint32_t incl = wave_incl_scan_dpp(cnt);
-                uint32_t rank = got + incl - cnt;
+                const uint32_t lo = readlane32(incl, 31), hi = readlane32(incl, 63);
+                uint32_t rank = got + (half ? incl - lo : incl) - cnt;
                 while (bits && rank < want) {
                     S.wpos[r][rank] = (uint32_t)(wi * 64u) + (uint32_t)__ffsll((unsigned long long)bits) - 1u;
                     bits &= bits - 1ull;
                     rank++;
                 }
-                const uint32_t tot = readlane32(incl, 63);
+                const uint32_t tot = half ? hi - lo : lo;
                 got = got + tot < want ? got + tot : want;
             }
-            if (lane == 0) {
-                double E = cs.ctb[c] * a.state[cs.cg[c]];
-                E = E * cs.cs[c];
-                S.sE[r] = E;
-                S.wn[r] = got;
-                S.sc[r] = c;
-                S.last[r] = 0;
-            }
-        }
-        if (tid == 0) S.cnt[3] = 0;
-        __syncthreads();
-        {
-            const uint32_t r = tid >> 5, q = tid & 31u;
-            if (r < R && q < S.wn[r]) {
-                const uint32_t p = S.wpos[r][q];
-                const double wd = (double)cs.lw[p];
-                double b = S.sE[r] * (1.0 + wd / a.f_ref);
+            if (act && hl < got) {
+                // written by lanes of this wave above (LDS is in order per wave)
+                const uint32_t p = S.wpos[r][hl];
+                const uint32_t words = cs.lw[p], J = cs.lf[p], id = cs.clist[p], obs = cs.lobs[p];
+                const double wd = (double)words;
+                const double F = 1.0 + wd / a.f_ref;
+                double b = E * F;
                 b = wd + b;
                 const uint64_t K = ordered_bits(b);
-                const uint32_t J = cs.lf[p];
-                // a member after the m-th best head is not among the first m
-                if (q == 0 || R < m || !pair_lt(S.pk[m - 1], S.pj[m - 1], K, J)) {
+                if (hl == 0 || R < m || !pair_lt(S.pk[cur][m - 1], S.pj[cur][m - 1], K, J)) {
                     const uint32_t slot = atomicAdd(&S.cnt[3], 1u);
-                    S.wk[slot] = K;
-                    S.wj[slot] = J;
-                    S.wv[slot] = tid;
+                    S.u.w.k[slot] = K;
+                    S.u.w.j[slot] = J;
+                    S.u.w.x[slot] = TS * F;
+                    S.u.w.id[slot] = id;
+                    S.u.w.obs[slot] = obs;
+                    S.u.w.slot[slot] = (r << 5) | hl;
                 }
             }
         }
-        __syncthreads();
+        lds_sync();
         const uint32_t nc = S.cnt[3];
         if (nc < m) return Resume{k, A, total};   // not reached: the windows hold the first m
-        sort_prefix(S.wk, S.wj, S.wv, nc);
+        for (uint32_t i = w; i < nc; i += kNW) {
+            const uint32_t r = rank_in(S.u.w.k, S.u.w.j, nc, S.u.w.k[i], S.u.w.j[i], m);
+            if (lane == 0 && r < m) S.sel[r] = i;
+        }
+        lds_sync();
 
         // 4. dispatch, and the completion events of the batch
         if (tid < m) {
-            const uint32_t v = S.wv[tid], r = v >> 5, q = v & 31u;
-            const uint32_t p = S.wpos[r][q];
-            const uint32_t id = cs.clist[p];
+            const uint32_t i = S.sel[tid], v = S.u.w.slot[i], r = v >> 5;
+            const uint32_t p = S.wpos[r][v & 31u], id = S.u.w.id[i];
             if (total + tid < n) a.seq[total + tid] = id;
             a.tick_of[id] = (int32_t)k;
             atomicAnd((unsigned long long *)&a.cls_elig[p >> 6], ~(1ull << (p & 63u)));
-            atomicMax(&S.last[r], p + 1u);
-            S.evg[tid] = cs.cg[S.sc[r]];
-            S.evc[tid] = S.sc[r];
-            S.evx[tid] = a.est_base[id];
-            S.evo[tid] = a.observed[id];
+            S.last[r] = 1;
+            S.evg[tid] = S.sg[r];
+            S.evr[tid] = r;
+            S.evx[tid] = S.u.w.x[i];
+            S.evo[tid] = S.u.w.obs[i];
         }
-        __syncthreads();
-        // the classes served move their heads past what they dispatched
-        if (tid < R && S.last[tid]) {
-            st_relaxed(&a.cls_head[S.sc[tid]], S.last[tid]);
-            mark_dirty(S.sc[tid], S);
-        }
-        // 5. Eq. (5) with the ratio of Eq. (6), each group's events in
-        //    dispatch order; a group whose factor moved touches its classes
-        if (tid < m) {
-            const uint32_t g = S.evg[tid];
-            bool lead = true;
-            for (uint32_t r = 0; r < tid && lead; r++) lead = S.evg[r] != g;
-            if (lead) {
-                double c = a.state[g];
+        if (tid == 0) S.cnt[3] = 0;
+        lds_sync();
+        // the classes served get new heads
+        if (tid < R && S.last[tid]) mark_dirty(S.sc[tid], S);
+        // 5. Eq. (5) with the ratio of Eq. (6) on one wave (lane i: the
+        //    batch's i-th event): each group's first event walks that
+        //    group's events in dispatch order; a group whose factor moved
+        //    touches its classes (ranges, spread over the block below)
+        if (w == 0) {
+            const uint32_t g = lane < m ? S.evg[lane] : kNone;
+            uint64_t same = 0;
+            for (uint32_t j = 0; j < m; j++) same |= (uint64_t)(readlane32(g, (int)j) == g) << j;
+            uint32_t len = 0, g0 = 0;
+            if (lane < m && (same & lanemask_lt()) == 0) {
+                const uint32_t r0 = S.evr[lane];
+                double c = S.sB[r0];
                 bool moved = false;
-                for (uint32_t r = tid; r < m; r++) {
-                    if (S.evg[r] != g) continue;
+                for (uint64_t bits = same; bits; bits &= bits - 1ull) {
+                    const uint32_t r = (uint32_t)__ffsll((unsigned long long)bits) - 1u;
                     const double x = S.evx[r];
                     if (!(isfinite(x) && x > 0.0)) continue;
                     const double ratio = (double)S.evo[r] / x;
@@ -1253,24 +1396,38 @@ __device__ Resume engine_class(const EngineArgs &a, const ClassShared &cs, Class
                     c = t1 + t2;
                     moved = true;
                 }
-                a.state[g] = c;
                 if (moved) {
-                    const uint32_t cl = S.evc[tid], g0 = cs.gfirst[cl], g1 = cs.gend[cl];
-                    if (g1 - g0 > kDirtyMax) S.cnt[1] = 1;
-                    else
-                        for (uint32_t u = g0; u < g1; u++) mark_dirty(u, S);
+                    a.state[g] = c;
+                    g0 = S.sgf[r0];
+                    len = S.sge[r0] - g0;
+                    if (len > kDirtyMax) {
+                        S.cnt[1] = 1;
+                        len = 0;
+                    }
                 }
             }
+            const uint32_t incl = wave_incl_scan_dpp(len);
+            S.rg0[lane] = g0;
+            S.roff[lane] = incl - len;
+            if (lane == 63) S.rtot = incl;
+        }
+        lds_sync();
+        for (uint32_t i = tid; i < S.rtot && !S.cnt[1]; i += kTPB) {
+            uint32_t lo = 0, hi = 64;   // the last range starting at or before i
+            while (hi - lo > 1) {
+                const uint32_t mid = (lo + hi) >> 1;
+                if (S.roff[mid] <= i) lo = mid;
+                else hi = mid;
+            }
+            mark_dirty(S.rg0[lo] + (i - S.roff[lo]), S);
         }
         P -= m;
         total += m;
-        __syncthreads();
+        lds_sync();
     }
     if (tid == 0) a.n_dispatched[0] = total;
     return Resume{a.n_ticks, A, total};
 }
-
-static_assert(sizeof(EngineBatch) + sizeof(ClassShared) <= 4096, "kernel arguments within 4 KB");
 
 // LDS of the three engines (a run uses one at a time).
 union EngineLds {
@@ -1301,11 +1458,11 @@ __global__ __launch_bounds__(kTPB) void k_sim_engine(EngineBatch eb, ClassShared
 
 struct ClassBuild {
     uint32_t n, n_cat, n_tenants, n_groups;
-    const uint32_t *fifo, *counts, *tenant, *group;
+    const uint32_t *fifo, *counts, *tenant, *group, *observed;
     const uint8_t *category;
     const double *arrival, *t_base, *s_tenant;
-    uint32_t *ctl, *fpos, *clist, *lpos, *lw, *lf, *pos_f, *cls_f, *cls_pos, *cstart, *cg, *gfirst, *gend,
-        *bcnt;
+    uint32_t *ctl, *fpos, *clist, *lpos, *lw, *lf, *lobs, *pos_f, *cls_f, *cls_pos, *cstart, *cg, *gfirst,
+        *gend, *bcnt;
     double *wkey, *ckey, *arr_f, *ctb, *cs;
 };
 
@@ -1329,7 +1486,7 @@ __global__ void k_cls_prep(const ClassBuild b)
 }
 
 // Class boundaries of the sorted list, counted per block of kTPB positions;
-// each entry's words and FIFO position.
+// each entry's words, FIFO position and observed length.
 __global__ __launch_bounds__(kTPB) void k_cls_mark(const ClassBuild b)
 {
     const uint32_t p = blockIdx.x * kTPB + threadIdx.x;
@@ -1339,6 +1496,7 @@ __global__ __launch_bounds__(kTPB) void k_cls_mark(const ClassBuild b)
         b.lpos[id] = p;
         b.lw[p] = b.counts[id];
         b.lf[p] = b.fpos[id];
+        b.lobs[p] = b.observed[id];
         first = p == 0 || b.ckey[id] != b.ckey[b.clist[p - 1]];
     }
     const uint32_t c = (uint32_t)__syncthreads_count(first);
@@ -1455,11 +1613,11 @@ uint32_t grid_for(uint64_t n)
 
 constexpr uint64_t kCandBytes = (uint64_t)kMaxQ * kSimMaxBatch * (8 + 4 + 4);
 
-// The class structure: 13 arrays of n words (cstart has n + 1), 5 of n
+// The class structure: 14 arrays of n words (cstart has n + 1), 5 of n
 // doubles, the block counts and the control words.
 uint64_t cls_shared_bytes(uint64_t n)
 {
-    return 12 * align_up(n * 4, 256) + align_up((n + 1) * 4, 256) + 5 * align_up(n * 8, 256) +
+    return 13 * align_up(n * 4, 256) + align_up((n + 1) * 4, 256) + 5 * align_up(n * 8, 256) +
            align_up((n / kTPB + 1) * 4, 256) + 256;
 }
 
@@ -1538,6 +1696,7 @@ hipError_t sim_launch(const SimArgs *runs, uint32_t n_runs, void *ws, uint32_t *
     cb.counts = a0.counts;
     cb.tenant = a0.tenant;
     cb.group = a0.group;
+    cb.observed = a0.observed;
     cb.category = a0.category;
     cb.arrival = a0.arrival;
     cb.t_base = a0.t_base;
@@ -1548,6 +1707,7 @@ hipError_t sim_launch(const SimArgs *runs, uint32_t n_runs, void *ws, uint32_t *
     cb.lpos = take32(n);
     cb.lw = take32(n);
     cb.lf = take32(n);
+    cb.lobs = take32(n);
     cb.pos_f = take32(n);
     cb.cls_f = take32(n);
     cb.cls_pos = take32(n);
@@ -1562,7 +1722,7 @@ hipError_t sim_launch(const SimArgs *runs, uint32_t n_runs, void *ws, uint32_t *
     cb.arr_f = take64(n);
     cb.ctb = take64(n);
     cb.cs = take64(n);
-    const ClassShared cshared = {cb.ctl, cb.clist, cb.lw, cb.lf, cb.pos_f, cb.cls_f, cb.arr_f,
+    const ClassShared cshared = {cb.ctl, cb.clist, cb.lw, cb.lf, cb.lobs, cb.pos_f, cb.cls_f, cb.arr_f,
                                  cb.cstart, cb.ctb, cb.cs, cb.cg, cb.gfirst, cb.gend};
     SetupBatch sb;
     EngineBatch eb;
