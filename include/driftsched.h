@@ -465,9 +465,15 @@ typedef struct {
  *  tick_of    device, n int32: the tick that dispatched request i, -1 if none
  *  n_dispatched  device, 1 uint32: number of requests dispatched
  *  ws         workspace of ds_workspace_bytes(DS_OP_SIMULATE, n, 0) bytes
- * One workgroup runs all ticks in one launch, so the call is meant for
- * pending sets of up to about 10^5 requests; its time grows with the pending
- * set times the number of ticks. n == 0 writes *n_dispatched = 0.
+ * One workgroup runs all ticks in one launch. A tick's cost does not grow
+ * with the pending set for FIFO, Priority, Weighted and Aging (per-tier
+ * queues), nor for SJF with batch <= 32: requests sharing category, tenant
+ * and group keep one order whatever the factors, and a tick works on the
+ * classes it touches (about 16 us a tick with 1.5 M requests pending). SJF
+ * with a larger batch, or from the tick at which (T_base B) S_tenant turns
+ * negative or non-finite or a budget exceeds 2^50, passes over the whole
+ * pending set every tick (meant for pending sets up to about 10^5); results
+ * are the same either way. n == 0 writes *n_dispatched = 0.
  */
 ds_status ds_simulate(uint32_t n, const double *arrival, const uint8_t *tier,
                       const uint32_t *counts, const uint8_t *category, const uint32_t *tenant,
