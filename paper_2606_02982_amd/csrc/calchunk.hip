@@ -127,8 +127,56 @@ struct SubShared {
     uint8_t ok[kSub];        // usable
 };
 
-// The sub-tile starting at event s0 (m <= kSub events, m > 0), sorted by
-// group and scanned. On return (after a barrier that follows every thread's
+// The raw events of a sub-tile (wave-major slots as in load_sort_scan),
+// loaded one sub-tile ahead of their use.
+template <int kE>
+struct Raw {
+    uint32_t g[kE], o[kE];
+    double x[kE];
+};
+
+template <int kE>
+__device__ __forceinline__ void load_raw(const CalArgs &a, uint32_t s0, uint32_t m, Raw<kE> &raw)
+{
+    const int w = (int)(threadIdx.x >> 6), lane = lane_id();
+#pragma unroll
+    for (int r = 0; r < kE; r++) {
+        const uint32_t sl = (uint32_t)w * (64u * kE) + (uint32_t)r * 64u + (uint32_t)lane;
+        raw.g[r] = 0;
+        raw.o[r] = 0;
+        raw.x[r] = 0.0;
+        if (sl < m) {
+            const uint32_t e = s0 + sl;
+            raw.g[r] = a.group[e];
+            raw.x[r] = a.est[e];
+            raw.o[r] = a.obs[e];
+        }
+    }
+}
+
+// The big sub-tiles (several per chunk) are loaded one ahead: the current
+// one's events come from `next`, and the following one's loads are issued
+// before the current one is sorted (the barriers there wait on LDS only).
+// The small ones are loaded where they are used.
+template <int kE>
+constexpr bool kPrefetch = kE > 1;
+
+template <int kE>
+__device__ __forceinline__ void fetch(const CalArgs &a, uint64_t s0, uint64_t c1, uint32_t m, Raw<kE> &raw,
+                                      Raw<kE> &next)
+{
+    constexpr uint32_t kSub = kT * kE;
+    if constexpr (kPrefetch<kE>) {
+        raw = next;
+        if (s0 + kSub < c1)
+            load_raw<kE>(a, (uint32_t)(s0 + kSub), (uint32_t)(c1 - s0 - kSub < kSub ? c1 - s0 - kSub : kSub), next);
+    } else {
+        load_raw<kE>(a, (uint32_t)s0, m, raw);
+    }
+}
+
+// The sub-tile of m <= kSub events (m > 0) held in raw, sorted by group and
+// scanned. On return (after a barrier that follows every thread's
 // reads of sh.b, sh.slot and sh.ok), thread t holds sorted positions 4t ..
 // 4t+3: key, slot, b, usable and the segment-start flags; and, when its first
 // position continues a segment that starts at p < 4t, `excl`, the
@@ -142,7 +190,7 @@ struct Sub {
 };
 
 template <int kE>
-__device__ void load_sort_scan(const CalArgs &a, uint32_t s0, uint32_t m, SubShared<kE> &sh, Sub<kE> &out)
+__device__ void load_sort_scan(const CalArgs &a, const Raw<kE> &raw, uint32_t m, SubShared<kE> &sh, Sub<kE> &out)
 {
     const uint32_t t = threadIdx.x;
     const int w = (int)(t >> 6), lane = lane_id();
@@ -158,10 +206,9 @@ __device__ void load_sort_scan(const CalArgs &a, uint32_t s0, uint32_t m, SubSha
         ok[r] = 0;
         b[r] = 0.0;
         if (sl < m) {
-            const uint32_t e = s0 + sl;
-            const uint32_t g = a.group[e];
-            const double x = a.est[e];
-            const uint32_t o = a.obs[e];
+            const uint32_t g = raw.g[r];
+            const double x = raw.x[r];
+            const uint32_t o = raw.o[r];
             key[r] = g < a.G ? g : a.G;
             if (g < a.G && isfinite(x) && x > 0.0) {
                 const double ratio = (double)o / x;
@@ -173,7 +220,7 @@ __device__ void load_sort_scan(const CalArgs &a, uint32_t s0, uint32_t m, SubSha
     // stable LSD passes over the key (8 bits each); positions in LDS
     for (uint32_t p = 0; p < a.passes; p++) {
         for (uint32_t i = t; i < kW * 256u; i += kT) (&sh.wcnt[0][0])[i] = 0;
-        __syncthreads();
+        lds_sync();
         uint32_t rk[kE];
 #pragma unroll
         for (int r = 0; r < kE; r++) {
@@ -193,7 +240,7 @@ __device__ void load_sort_scan(const CalArgs &a, uint32_t s0, uint32_t m, SubSha
             if (v && below == 0) sh.wcnt[w][dg] = old + (uint32_t)__popcll(peers);
             __builtin_amdgcn_wave_barrier();
         }
-        __syncthreads();
+        lds_sync();
         if (w == 0) {
             // digits 4 l .. 4 l + 3: per-wave exclusive offsets and digit starts
             uint32_t c[4][kW], tot[4];
@@ -219,7 +266,7 @@ __device__ void load_sort_scan(const CalArgs &a, uint32_t s0, uint32_t m, SubSha
                 ex += tot[e];
             }
         }
-        __syncthreads();
+        lds_sync();
 #pragma unroll
         for (int r = 0; r < kE; r++) {
             const uint32_t sl = (uint32_t)w * (64u * kE) + (uint32_t)r * 64u + (uint32_t)lane;
@@ -232,7 +279,7 @@ __device__ void load_sort_scan(const CalArgs &a, uint32_t s0, uint32_t m, SubSha
                 sh.ok[q] = (uint8_t)ok[r];
             }
         }
-        __syncthreads();
+        lds_sync();
         if (p + 1 < a.passes) {
 #pragma unroll
             for (int r = 0; r < kE; r++) {
@@ -244,7 +291,7 @@ __device__ void load_sort_scan(const CalArgs &a, uint32_t s0, uint32_t m, SubSha
                     ok[r] = sh.ok[sl];
                 }
             }
-            __syncthreads();
+            lds_sync();
         }
     }
     // thread t takes sorted positions kE t .. kE t + kE - 1
@@ -274,7 +321,7 @@ __device__ void load_sort_scan(const CalArgs &a, uint32_t s0, uint32_t m, SubSha
     // exclusive scan of the threads' maps: wave scan, then the waves before
     const Map incl = wave_scan(agg);
     if (lane == 63) sh.wagg[w] = incl;
-    __syncthreads();
+    lds_sync();
     Map before = {1u, 0u, 1.0, 0.0};   // nothing before
     for (int q = 0; q < w; q++) before = (q == 0) ? sh.wagg[0] : combine(before, sh.wagg[q]);
     Map ex = shfl_up_map(incl, 1);
@@ -299,10 +346,14 @@ __global__ __launch_bounds__(kT) void k_calc_agg(CalArgs a)
     }
     const uint64_t c0 = (uint64_t)c * a.L;
     const uint64_t c1 = c0 + a.L < a.E ? c0 + a.L : a.E;
+    Raw<kE> next;
+    if (kPrefetch<kE> && c0 < c1) load_raw<kE>(a, (uint32_t)c0, (uint32_t)(c1 - c0 < kSub ? c1 - c0 : kSub), next);
     for (uint64_t s0 = c0; s0 < c1; s0 += kSub) {
         const uint32_t m = (uint32_t)(c1 - s0 < kSub ? c1 - s0 : kSub);
+        Raw<kE> raw;
+        fetch<kE>(a, s0, c1, m, raw, next);
         Sub<kE> sub;
-        load_sort_scan<kE>(a, (uint32_t)s0, m, sh, sub);   // (its first barrier orders the sA/sB writes)
+        load_sort_scan<kE>(a, raw, m, sh, sub);   // (its first barrier orders the sA/sB writes)
         // the segment of each group in this sub-tile, composed into the
         // group's map at the segment's last position (one thread per group)
         Map run = sub.excl;
@@ -331,7 +382,7 @@ __global__ __launch_bounds__(kT) void k_calc_agg(CalArgs a)
                 }
             }
         }
-        __syncthreads();
+        lds_sync();
     }
     for (uint32_t g = t; g < a.G; g += kT) {
         a.aggA[(uint64_t)c * a.G + g] = sA[g];
@@ -430,10 +481,14 @@ __global__ __launch_bounds__(kT) void k_calc_apply(CalArgs a)
     const uint64_t c1 = c0 + a.L < a.E ? c0 + a.L : a.E;
     const double nan = __builtin_nan("");
     double *tr = sh.b;
+    Raw<kE> next;
+    if (kPrefetch<kE> && c0 < c1) load_raw<kE>(a, (uint32_t)c0, (uint32_t)(c1 - c0 < kSub ? c1 - c0 : kSub), next);
     for (uint64_t s0 = c0; s0 < c1; s0 += kSub) {
         const uint32_t m = (uint32_t)(c1 - s0 < kSub ? c1 - s0 : kSub);
+        Raw<kE> raw;
+        fetch<kE>(a, s0, c1, m, raw, next);
         Sub<kE> sub;
-        load_sort_scan<kE>(a, (uint32_t)s0, m, sh, sub);
+        load_sort_scan<kE>(a, raw, m, sh, sub);
         if (quick && s0 == c0) {
             const uint32_t g = t / tpg, p = t % tpg;
             Map mp = {0u, 0u, 1.0, 0.0};
@@ -472,7 +527,7 @@ __global__ __launch_bounds__(kT) void k_calc_apply(CalArgs a)
                 sv[g] = v;
                 su[g] = (uint8_t)mp.u;
             }
-            __syncthreads();
+            lds_sync();
         }
         // the factor before this thread's first position: the group's factor
         // at the sub-tile start, through the earlier positions of its
@@ -505,7 +560,7 @@ __global__ __launch_bounds__(kT) void k_calc_apply(CalArgs a)
             tr[sub.slot[e]] = cv;
             after[e] = cv;
         }
-        __syncthreads();   // every read of sv above precedes the updates below
+        lds_sync();   // every read of sv above precedes the updates below
 #pragma unroll
         for (int e = 0; e < kE; e++) {
             const uint32_t i = t * kE + (uint32_t)e;
@@ -519,7 +574,7 @@ __global__ __launch_bounds__(kT) void k_calc_apply(CalArgs a)
             if (a.trace) a.trace[s0 + i] = tr[i];
             if (a.trace_before) a.trace_before[s0 + i] = trb[i];
         }
-        __syncthreads();
+        lds_sync();
     }
     if (a.small && c + 1 == a.C) {
         // the factors after all events: the groups with a usable event in

@@ -80,6 +80,16 @@ __device__ __forceinline__ void st_relaxed(uint32_t *p, uint32_t v)
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Block barrier for LDS traffic alone (s_waitcnt lgkmcnt(0); s_barrier):
+// global loads and stores may stay in flight across it, so it orders no
+// global memory between waves.
+__device__ __forceinline__ void lds_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 __host__ __device__ constexpr uint64_t cdiv(uint64_t a, uint64_t b) { return (a + b - 1) / b; }
 __host__ __device__ constexpr uint64_t align_up(uint64_t a, uint64_t b) { return cdiv(a, b) * b; }
 

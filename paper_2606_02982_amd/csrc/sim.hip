@@ -1046,16 +1046,6 @@ __device__ __forceinline__ uint32_t count_below(const uint64_t *k, const uint32_
     return lo;
 }
 
-// Barrier for LDS traffic alone: global stores and atomics may still be in
-// flight (every global hand-over between waves inside a tick of the class
-// engine is ordered by a full __syncthreads instead).
-__device__ __forceinline__ void lds_sync()
-{
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-}
-
 // block_scan with LDS barriers.
 __device__ __forceinline__ uint32_t lds_scan(uint32_t x, uint32_t *s_w, uint32_t &total)
 {
