@@ -10,9 +10,10 @@
 //                 as a segmented scan of maps, and each group's part is
 //                 composed into that group's map in LDS; the chunk writes
 //                 M(c, g) for every group (or "no usable event").
-//   k_calc_scan   per group (one wave): the group's factor before chunk c is
-//                 M(c-1, g) o ... o M(0, g) applied to its initial factor
-//                 (the maps composed per lane, then a wave scan); writes those
+//   k_calc_scan   per 64 groups (one block, lane = group): the group's
+//                 factor before chunk c is M(c-1, g) o ... o M(0, g) applied
+//                 to its initial factor (sixteen stretches of chunks composed
+//                 by sixteen waves, then chained in order); writes those
 //                 carries and the final factor.
 //   k_calc_apply  per chunk: the same sub-tile sort and scan; every event
 //                 then runs the exact update t1 = (1 - alpha) c, t2 =
@@ -390,27 +391,43 @@ __global__ __launch_bounds__(kT) void k_calc_agg(CalArgs a)
     }
 }
 
-// One wave per group: carries before every chunk, and the final factor.
-__global__ __launch_bounds__(256) void k_calc_scan(CalArgs a)
+// Carries before every chunk, and the final factors: one block per 64
+// groups (lane = group, so every read of a chunk's row is 512 contiguous
+// bytes), its sixteen waves over sixteen stretches of the chunks. Each wave
+// composes its stretch's maps per group; each then takes the initial factor
+// through the earlier stretches' maps in order and walks its own stretch,
+// writing the factor before each chunk.
+constexpr uint32_t kScanW = 16;
+__global__ __launch_bounds__(64 * kScanW) void k_calc_scan(CalArgs a)
 {
-    const uint32_t g = blockIdx.x * 4u + (threadIdx.x >> 6);
+    __shared__ double sA[kScanW][64], sB[kScanW][64];
+    __shared__ uint32_t sU[kScanW][64];
+    const uint32_t w = threadIdx.x >> 6;
     const int lane = lane_id();
-    if (g >= a.G) return;
-    const uint32_t per = (a.C + 63u) / 64u;
-    const uint32_t cb = (uint32_t)lane * per, ce = cb + per < a.C ? cb + per : a.C;
+    const uint32_t g = blockIdx.x * 64u + (uint32_t)lane;
+    const bool in = g < a.G;
+    const uint32_t per = (a.C + kScanW - 1) / kScanW;
+    const uint32_t cb = w * per < a.C ? w * per : a.C, ce = cb + per < a.C ? cb + per : a.C;
     Map agg = {0u, 0u, 1.0, 0.0};
-    for (uint32_t c = cb; c < ce; c++) {
-        const double A = a.aggA[(uint64_t)c * a.G + g], B = a.aggB[(uint64_t)c * a.G + g];
-        if (A >= 0.0) agg = combine(agg, Map{0u, 1u, A, B});
-    }
-    const Map incl = wave_scan(agg);
-    Map ex = shfl_up_map(incl, 1);
-    if (lane == 0) ex = Map{0u, 0u, 1.0, 0.0};
-    const double v0 = a.state[g];
-    double v = v0;
-    if (ex.u) {
-        const double tt = ex.a * v0;
-        v = tt + ex.b;
+    if (in)
+        for (uint32_t c = cb; c < ce; c++) {
+            const double A = a.aggA[(uint64_t)c * a.G + g], B = a.aggB[(uint64_t)c * a.G + g];
+            if (A >= 0.0) agg = combine(agg, Map{0u, 1u, A, B});
+        }
+    sA[w][lane] = agg.a;
+    sB[w][lane] = agg.b;
+    sU[w][lane] = agg.u;
+    __syncthreads();
+    if (!in) return;
+    double v = a.state[g];
+    bool touched = false;
+    for (uint32_t q = 0; q < kScanW; q++) {
+        if (!sU[q][lane]) continue;
+        touched = true;
+        if (q < w) {
+            const double tt = sA[q][lane] * v;
+            v = tt + sB[q][lane];
+        }
     }
     for (uint32_t c = cb; c < ce; c++) {
         a.carry[(uint64_t)c * a.G + g] = v;
@@ -420,9 +437,8 @@ __global__ __launch_bounds__(256) void k_calc_scan(CalArgs a)
             v = tt + B;
         }
     }
-    // the lane holding the last chunk writes the factor after all events
+    // the wave holding the last chunk writes the factor after all events
     // (a group without usable events keeps its factor untouched)
-    const bool touched = __ballot(incl.u != 0u) != 0ull;
     if (ce == a.C && cb < ce && touched) a.state[g] = v;
 }
 
@@ -648,7 +664,7 @@ hipError_t calc_launch(const uint32_t *group, const double *est, const uint32_t 
         hipLaunchKernelGGL(k_calc_apply<1>, dim3(a.C), dim3(kT), 0, s, a);
     } else {
         hipLaunchKernelGGL(k_calc_agg<4>, dim3(a.C), dim3(kT), 0, s, a);
-        hipLaunchKernelGGL(k_calc_scan, dim3((G + 3) / 4), dim3(256), 0, s, a);
+        hipLaunchKernelGGL(k_calc_scan, dim3((G + 63) / 64), dim3(64 * kScanW), 0, s, a);
         hipLaunchKernelGGL(k_calc_apply<4>, dim3(a.C), dim3(kT), 0, s, a);
     }
     return hipGetLastError();
