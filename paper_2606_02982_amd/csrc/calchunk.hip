@@ -408,11 +408,24 @@ __global__ __launch_bounds__(64 * kScanW) void k_calc_scan(CalArgs a)
     const bool in = g < a.G;
     const uint32_t per = (a.C + kScanW - 1) / kScanW;
     const uint32_t cb = w * per < a.C ? w * per : a.C, ce = cb + per < a.C ? cb + per : a.C;
+    // four chunks' maps in flight at a time
+    constexpr uint32_t kR = 4;
     Map agg = {0u, 0u, 1.0, 0.0};
     if (in)
-        for (uint32_t c = cb; c < ce; c++) {
-            const double A = a.aggA[(uint64_t)c * a.G + g], B = a.aggB[(uint64_t)c * a.G + g];
-            if (A >= 0.0) agg = combine(agg, Map{0u, 1u, A, B});
+        for (uint32_t c0 = cb; c0 < ce; c0 += kR) {
+            double A[kR], B[kR];
+#pragma unroll
+            for (uint32_t r = 0; r < kR; r++) {
+                A[r] = -1.0;
+                B[r] = 0.0;
+                if (c0 + r < ce) {
+                    A[r] = a.aggA[(uint64_t)(c0 + r) * a.G + g];
+                    B[r] = a.aggB[(uint64_t)(c0 + r) * a.G + g];
+                }
+            }
+#pragma unroll
+            for (uint32_t r = 0; r < kR; r++)
+                if (A[r] >= 0.0) agg = combine(agg, Map{0u, 1u, A[r], B[r]});
         }
     sA[w][lane] = agg.a;
     sB[w][lane] = agg.b;
@@ -429,12 +442,25 @@ __global__ __launch_bounds__(64 * kScanW) void k_calc_scan(CalArgs a)
             v = tt + sB[q][lane];
         }
     }
-    for (uint32_t c = cb; c < ce; c++) {
-        a.carry[(uint64_t)c * a.G + g] = v;
-        const double A = a.aggA[(uint64_t)c * a.G + g], B = a.aggB[(uint64_t)c * a.G + g];
-        if (A >= 0.0) {
-            const double tt = A * v;
-            v = tt + B;
+    for (uint32_t c0 = cb; c0 < ce; c0 += kR) {
+        double A[kR], B[kR];
+#pragma unroll
+        for (uint32_t r = 0; r < kR; r++) {
+            A[r] = -1.0;
+            B[r] = 0.0;
+            if (c0 + r < ce) {
+                A[r] = a.aggA[(uint64_t)(c0 + r) * a.G + g];
+                B[r] = a.aggB[(uint64_t)(c0 + r) * a.G + g];
+            }
+        }
+#pragma unroll
+        for (uint32_t r = 0; r < kR; r++) {
+            if (c0 + r >= ce) break;
+            a.carry[(uint64_t)(c0 + r) * a.G + g] = v;
+            if (A[r] >= 0.0) {
+                const double tt = A[r] * v;
+                v = tt + B[r];
+            }
         }
     }
     // the wave holding the last chunk writes the factor after all events
