@@ -91,6 +91,11 @@ struct EngineArgs {
     // tier (rpos, with each tier's first entry in rstart), and candidate
     // scratch of kMaxQ x batch entries
     const uint32_t *rpos, *rstart;
+    const uint32_t *qid;       // request, arrival, group, observed length and
+    const double *qarr;        // B-free estimate of each run entry
+    const uint32_t *qgrp, *qobs;
+    const double *qest;
+    double prio[kMaxQ];        // each tier's priority (Priority and Aging keys)
     uint64_t *cand_k;
     uint32_t *cand_j, *cand_i;
     // the class engine (SJF): each class's head bound, the pending bitmap over
@@ -578,6 +583,25 @@ __device__ void engine_list(const EngineArgs &a, ListLds &L, uint32_t k0 = 0, ui
     if (tid == 0) a.n_dispatched[0] = total;
 }
 
+// Batches up to kQLdsBatch with up to kQLdsGroups groups keep the queue
+// engine's candidates, their completion events and the factors in LDS;
+// other runs use the workspace and the state array.
+constexpr uint32_t kQLdsBatch = 128;
+constexpr uint32_t kQLdsGroups = 4096;
+constexpr uint32_t kNoGroup = 0xFFFFFFFFu;
+constexpr uint32_t kQCand = kMaxQ * kQLdsBatch;
+
+struct QueueLds {
+    uint32_t s_head[kMaxQ], s_tail[kMaxQ], s_cnt[kMaxQ], s_d[kMaxQ], s_wt[kMaxQ], s_rstart[kMaxQ + 1];
+    double sst[kQLdsGroups];         // the factors during the run
+    uint32_t s_sel[kSimMaxBatch];    // candidate of each dispatch place
+    uint32_t s_evg[kSimMaxBatch], s_evo[kSimMaxBatch];
+    double s_evx[kSimMaxBatch];
+    uint64_t ck[kQCand];             // candidates: key, FIFO position, request, event
+    uint32_t cj[kQCand], ci[kQCand], cg[kQCand], co[kQCand];
+    double cx[kQCand];
+};
+
 // The loop for FIFO, Priority, Weighted and Aging with one queue per tier.
 // Within a tier each of these orders is the FIFO order (Aging's score is
 // monotone in the arrival for a fixed priority), so the pending requests of
@@ -588,13 +612,15 @@ __device__ void engine_list(const EngineArgs &a, ListLds &L, uint32_t k0 = 0, ui
 // in every other tier's candidates, which are in key order) or placed by
 // the round-robin closed forms, so a tick costs O(tiers x batch) rather
 // than a pass over the pending set. Results equal the list engine's.
-struct QueueLds {
-    uint32_t s_head[kMaxQ], s_tail[kMaxQ], s_cnt[kMaxQ], s_d[kMaxQ], s_wt[kMaxQ];
-    uint32_t s_sel[kSimMaxBatch];
-    uint32_t s_evg[kSimMaxBatch], s_evo[kSimMaxBatch];
-    double s_evx[kSimMaxBatch];
-};
-
+//
+// Every key follows from the tier and the arrival (Priority: the tier's
+// priority; Aging: it aged to t), so a candidate needs only its run entry's
+// request, arrival, group, observed length and B-free estimate, laid out in
+// run order once (one round of loads). In LDS mode (kL) the candidates and
+// the factors stay in LDS (the factors are written back at the end), the
+// phases are separated by LDS-only barriers, and each batch's factor
+// updates run on one wave (lane i: the i-th event).
+template <bool kL>
 __device__ void engine_queues(const EngineArgs &a, QueueLds &Q)
 {
     auto &s_head = Q.s_head;
@@ -606,6 +632,13 @@ __device__ void engine_queues(const EngineArgs &a, QueueLds &Q)
     auto &s_evg = Q.s_evg;
     auto &s_evo = Q.s_evo;
     auto &s_evx = Q.s_evx;
+    uint64_t *ck = kL ? Q.ck : a.cand_k;
+    uint32_t *cj = kL ? Q.cj : a.cand_j;
+    uint32_t *ci = kL ? Q.ci : a.cand_i;
+    auto sync = [] {
+        if (kL) lds_sync();
+        else __syncthreads();
+    };
     const uint32_t tid = threadIdx.x, lane = (uint32_t)lane_id(), w = tid >> 6;
     const uint32_t n = a.n, policy = a.policy, batch = a.batch, nq = a.n_q;
     const double oma = 1.0 - a.alpha;
@@ -614,23 +647,22 @@ __device__ void engine_queues(const EngineArgs &a, QueueLds &Q)
         s_tail[tid] = 0;
         s_wt[tid] = a.weight[tid];
     }
+    if (tid <= kMaxQ) Q.s_rstart[tid] = a.rstart[tid];
+    if (kL)
+        for (uint32_t g = tid; g < a.n_groups; g += kTPB) Q.sst[g] = a.state[g];
     uint32_t total = 0;
     __syncthreads();
     for (uint32_t k = 0; k < a.n_ticks; k++) {
         const double t = a.tick_t[k];
+        if (!kL) __syncthreads();   // the last tick's factor updates, for every wave
         // 1. arrivals: wave q moves tier q's tail over its requests with
         //    arrival <= t (a prefix of the rest of its FIFO run)
         if (w < nq) {
-            const uint32_t r0 = a.rstart[w], len = a.rstart[w + 1] - r0;
+            const uint32_t r0 = Q.s_rstart[w], len = Q.s_rstart[w + 1] - r0;
             uint32_t tail = s_tail[w];
             for (;;) {
                 const uint32_t idx = tail + lane;
-                bool ok = false;
-                if (idx < len) {
-                    uint32_t id = a.fifo[a.rpos[r0 + idx]];
-                    id = id < n ? id : 0u;
-                    ok = a.arrival[id] <= t;
-                }
+                const bool ok = idx < len && a.qarr[r0 + idx] <= t;
                 const uint64_t b = __ballot(ok);
                 const uint32_t c = ~b ? (uint32_t)__ffsll((unsigned long long)~b) - 1u : 64u;
                 tail += c;
@@ -639,9 +671,9 @@ __device__ void engine_queues(const EngineArgs &a, QueueLds &Q)
             if (lane == 0) s_tail[w] = tail;
         }
         if (tid < kMaxQ) s_d[tid] = 0;
-        __syncthreads();
+        sync();
         if (tid < kMaxQ) s_cnt[tid] = tid < nq ? s_tail[tid] - s_head[tid] : 0u;
-        __syncthreads();
+        sync();
         uint32_t P = 0;
         for (uint32_t q = 0; q < nq; q++) P += s_cnt[q];
         const uint32_t m = P < batch ? P : batch;
@@ -653,38 +685,41 @@ __device__ void engine_queues(const EngineArgs &a, QueueLds &Q)
             const uint32_t q = p / batch, r = p - q * batch;
             const uint32_t cq = s_cnt[q] < m ? s_cnt[q] : m;
             if (r >= cq) continue;
-            const uint32_t j = a.rpos[a.rstart[q] + s_head[q] + r];
-            uint32_t id = a.fifo[j];
+            const uint32_t x = Q.s_rstart[q] + s_head[q] + r;
+            const uint32_t j = a.rpos[x];
+            uint32_t id = a.qid[x];
             id = id < n ? id : 0u;
             if (ranked) {
-                uint64_t K;
-                if (policy == kFifo) {
-                    K = 0;
-                } else if (policy == kPriority) {
-                    K = a.val[id];
-                } else {
-                    const Aux x = a.aux[id];
-                    double wt = t - x.a;
+                uint64_t K = 0;
+                if (policy == kPriority) {
+                    K = ordered_bits(a.prio[q]);
+                } else if (policy == kAging) {
+                    double wt = t - a.qarr[x];
                     if (wt < 0.0) wt = 0.0;
                     const double d = a.aging_rate * wt;
-                    double e = x.b - d;
+                    double e = a.prio[q] - d;
                     if (e < a.aging_floor) e = a.aging_floor;
                     K = ordered_bits(e);
                 }
-                a.cand_k[p] = K;
-                a.cand_j[p] = j;
+                ck[p] = K;
+                cj[p] = j;
             } else if (a.wrr_mode != kWrrSmooth) {
                 const uint64_t pos = a.wrr_mode == kWrrStride
                                          ? wrr_stride_pos(q, r, s_wt, nq, [&](uint32_t u) { return s_cnt[u]; })
                                          : wrr_place(q, r, s_cnt, s_wt, nq);
                 if (pos < m) {
-                    s_sel[pos] = id;
+                    s_sel[pos] = p;
                     atomicAdd(&s_d[q], 1u);
                 }
             }
-            a.cand_i[p] = id;
+            ci[p] = id;
+            if (kL) {
+                Q.cg[p] = a.qgrp[x];
+                Q.cx[p] = a.qest[x];
+                Q.co[p] = a.qobs[x];
+            }
         }
-        __syncthreads();
+        sync();
         if (ranked) {
             // rank of each candidate: its place in its tier plus, in every
             // other tier, the candidates with a smaller (key, FIFO position)
@@ -692,8 +727,8 @@ __device__ void engine_queues(const EngineArgs &a, QueueLds &Q)
                 const uint32_t q = p / batch, r = p - q * batch;
                 const uint32_t cq = s_cnt[q] < m ? s_cnt[q] : m;
                 if (r >= cq) continue;
-                const uint64_t K = a.cand_k[p];
-                const uint32_t J = a.cand_j[p];
+                const uint64_t K = ck[p];
+                const uint32_t J = cj[p];
                 uint32_t rank = r;
                 for (uint32_t u = 0; u < nq && rank < m; u++) {
                     if (u == q) continue;
@@ -701,15 +736,15 @@ __device__ void engine_queues(const EngineArgs &a, QueueLds &Q)
                     uint32_t lo = 0, hi = cu;
                     while (lo < hi) {
                         const uint32_t mid = (lo + hi) >> 1;
-                        const uint64_t K2 = a.cand_k[u * batch + mid];
-                        const uint32_t J2 = a.cand_j[u * batch + mid];
-                        if (K2 < K || (K2 == K && J2 < J)) lo = mid + 1u;
+                        const uint64_t K2 = ck[u * batch + mid];
+                        const uint32_t J2 = cj[u * batch + mid];
+                        if (K2 < K || (K2 == K && J2 < J)) lo = mid + 1;
                         else hi = mid;
                     }
                     rank += lo;
                 }
                 if (rank < m) {
-                    s_sel[rank] = a.cand_i[p];
+                    s_sel[rank] = p;
                     atomicAdd(&s_d[q], 1u);
                 }
             }
@@ -724,33 +759,58 @@ __device__ void engine_queues(const EngineArgs &a, QueueLds &Q)
             for (uint32_t pos = 0; pos < m; pos++) {
                 const int b = wrr_pick(credit, served < len, wq, W);
                 const bool mine = lane == (uint32_t)b;
-                if (mine) s_sel[pos] = a.cand_i[lane * batch + served];   // served < m
+                if (mine) s_sel[pos] = lane * batch + served;   // served < m
                 served += mine ? 1u : 0u;
                 if (__ballot(mine && served == len) != 0ull) W = wave_sum(served < len ? wq : 0u);
             }
             if (lane < kMaxQ) s_d[lane] = served;
         }
-        __syncthreads();
+        sync();
 
         // 3. dispatch, and the completion events of the batch
         if (tid < m) {
-            const uint32_t id = s_sel[tid];
+            const uint32_t p = s_sel[tid], id = ci[p];
             if (total + tid < n) a.seq[total + tid] = id;
             a.tick_of[id] = (int32_t)k;
-            s_evg[tid] = a.group[id];
-            s_evx[tid] = a.est_base[id];
-            s_evo[tid] = a.observed[id];
+            if (kL) {
+                s_evg[tid] = Q.cg[p];
+                s_evx[tid] = Q.cx[p];
+                s_evo[tid] = Q.co[p];
+            } else {
+                s_evg[tid] = a.group[id];
+                s_evx[tid] = a.est_base[id];
+                s_evo[tid] = a.observed[id];
+            }
         }
-        __syncthreads();
+        sync();
 
         // 4. Eq. (5) with the ratio of Eq. (6), each group's events of the
         //    batch in dispatch order
-        if (tid < m) {
+        if (kL && m <= 64) {
+            if (w == 0) {
+                const uint32_t g = lane < m ? s_evg[lane] : kNoGroup;
+                uint64_t same = 0;
+                for (uint32_t j = 0; j < m; j++) same |= (uint64_t)(readlane32(g, (int)j) == g) << j;
+                if (lane < m && g < a.n_groups && (same & lanemask_lt()) == 0) {
+                    double c = Q.sst[g];
+                    for (uint64_t bits = same; bits; bits &= bits - 1ull) {
+                        const uint32_t r = (uint32_t)__ffsll((unsigned long long)bits) - 1u;
+                        const double x = s_evx[r];
+                        if (!(isfinite(x) && x > 0.0)) continue;
+                        const double ratio = (double)s_evo[r] / x;
+                        const double t1 = oma * c;
+                        const double t2 = a.alpha * ratio;
+                        c = t1 + t2;
+                    }
+                    Q.sst[g] = c;
+                }
+            }
+        } else if (tid < m) {
             const uint32_t g = s_evg[tid];
             bool lead = g < a.n_groups;
             for (uint32_t r = 0; r < tid && lead; r++) lead = s_evg[r] != g;
             if (lead) {
-                double c = a.state[g];
+                double c = kL ? Q.sst[g] : a.state[g];
                 for (uint32_t r = tid; r < m; r++) {
                     if (s_evg[r] != g) continue;
                     const double x = s_evx[r];
@@ -760,13 +820,16 @@ __device__ void engine_queues(const EngineArgs &a, QueueLds &Q)
                     const double t2 = a.alpha * ratio;
                     c = t1 + t2;
                 }
-                a.state[g] = c;
+                if (kL) Q.sst[g] = c;
+                else a.state[g] = c;
             }
         }
         if (tid < nq) s_head[tid] += s_d[tid];
         total += m;
-        __syncthreads();
+        sync();
     }
+    if (kL)
+        for (uint32_t g = tid; g < a.n_groups; g += kTPB) a.state[g] = Q.sst[g];
     if (tid == 0) a.n_dispatched[0] = total;
 }
 
@@ -1434,7 +1497,8 @@ __global__ __launch_bounds__(kTPB) void k_sim_engine(EngineBatch eb, ClassShared
     __shared__ EngineLds lds;
     const EngineArgs &a = eb.r[blockIdx.x];
     if (a.rpos) {
-        engine_queues(a, lds.q);
+        if (a.batch <= kQLdsBatch && a.n_groups <= kQLdsGroups) engine_queues<true>(a, lds.q);
+        else engine_queues<false>(a, lds.q);
     } else if (a.cls_head) {
         const Resume r = engine_class(a, cs, lds.c);
         __syncthreads();
@@ -1572,6 +1636,38 @@ __global__ void k_cls_fin(const ClassBuild b)
     }
 }
 
+// The tier runs' entries in run order: request, arrival, group and
+// observed length; and, per run on the queue engine (blockIdx.y), the B-free
+// estimate.
+struct QPrep {
+    const uint32_t *rpos, *fifo, *group, *observed;
+    const double *arrival;
+    uint32_t n;
+    uint32_t *qid, *qgrp, *qobs;
+    double *qarr;
+    const double *est[kSimMaxRuns];
+    double *qest[kSimMaxRuns];
+};
+
+__global__ void k_sim_qprep(const QPrep q)
+{
+    const double *est = q.est[blockIdx.y];
+    double *qest = q.qest[blockIdx.y];
+    for (uint32_t r = blockIdx.x * blockDim.x + threadIdx.x; r < q.n; r += gridDim.x * blockDim.x) {
+        uint32_t j = q.rpos[r];
+        j = j < q.n ? j : 0u;
+        uint32_t id = q.fifo[j];
+        id = id < q.n ? id : 0u;   // the FIFO order is a permutation of 0..n-1
+        if (blockIdx.y == 0) {
+            q.qid[r] = id;
+            q.qarr[r] = q.arrival[id];
+            q.qgrp[r] = q.group[id];
+            q.qobs[r] = q.observed[id];
+        }
+        if (qest) qest[r] = est[id];
+    }
+}
+
 __global__ void k_sim_empty(uint32_t *__restrict__ n_dispatched, uint32_t n_runs)
 {
     if (threadIdx.x < n_runs) n_dispatched[threadIdx.x] = 0;
@@ -1619,15 +1715,16 @@ uint64_t cls_run_bytes(uint64_t n)
 
 size_t sim_ws_bytes(uint64_t n, uint32_t n_runs)
 {
-    // shared: fifo, the tier runs (positions and starts), the class structure,
-    // then the FIFO sort, the class sorts and the partition (one after the
-    // other); per run: list x2, est_base, key, aux, val, the queue engine's
+    // shared: fifo, the tier runs (positions, starts, and each entry's
+    // request, group, observed length and arrival), the class structure, then
+    // the FIFO sort, the class sorts and the partition (one after the other);
+    // per run: list x2, est_base, key, aux, val, the queue engine's
     // candidates, the class engine's state
     const uint64_t per = 2 * align_up(n * 4, 256) + 2 * align_up(n * 8, 256) +
                          align_up(n * sizeof(Aux), 256) + align_up(n, 256) + kCandBytes + cls_run_bytes(n);
     const uint64_t sort = sort_ws_bytes(n, 1), part = am_partition_ws_bytes(n);
-    return 2 * align_up(n * 4, 256) + 256 + cls_shared_bytes(n) + (uint64_t)(n_runs ? n_runs : 1) * per +
-           (sort > part ? sort : part);
+    return 5 * align_up(n * 4, 256) + align_up(n * 8, 256) + 256 + cls_shared_bytes(n) +
+           (uint64_t)(n_runs ? n_runs : 1) * per + (sort > part ? sort : part);
 }
 
 // SJF runs the class engine when its batches fit the windows, F is
@@ -1669,6 +1766,17 @@ hipError_t sim_launch(const SimArgs *runs, uint32_t n_runs, void *ws, uint32_t *
     uint32_t *fifo = reinterpret_cast<uint32_t *>(take((uint64_t)n * 4));
     uint32_t *rpos = reinterpret_cast<uint32_t *>(take((uint64_t)n * 4));
     uint32_t *rstart = reinterpret_cast<uint32_t *>(take(256));
+    QPrep qp = {};
+    qp.n = n;
+    qp.rpos = rpos;
+    qp.fifo = fifo;
+    qp.group = a0.group;
+    qp.observed = a0.observed;
+    qp.arrival = a0.arrival;
+    qp.qid = reinterpret_cast<uint32_t *>(take((uint64_t)n * 4));
+    qp.qgrp = reinterpret_cast<uint32_t *>(take((uint64_t)n * 4));
+    qp.qobs = reinterpret_cast<uint32_t *>(take((uint64_t)n * 4));
+    qp.qarr = reinterpret_cast<double *>(take((uint64_t)n * 8));
     // every policy but SJF runs on the tier queues (up to the partition's limit)
     bool any_queues = false, any_class = false;
     for (uint32_t r = 0; r < n_runs; r++) {
@@ -1780,7 +1888,10 @@ hipError_t sim_launch(const SimArgs *runs, uint32_t n_runs, void *ws, uint32_t *
         ea.est_base = est_base;
         ea.aux = aux;
         ea.val = val;
-        for (uint32_t q = 0; q < kMaxQ; q++) ea.weight[q] = q < a.n_tiers && a.weight[q] ? a.weight[q] : 1u;
+        for (uint32_t q = 0; q < kMaxQ; q++) {
+            ea.weight[q] = q < a.n_tiers && a.weight[q] ? a.weight[q] : 1u;
+            ea.prio[q] = a.prio[q];
+        }
         ea.wrr_mode = a.wrr_mode;
         ea.alpha = a.alpha;
         ea.aging_rate = a.aging_rate;
@@ -1795,6 +1906,14 @@ hipError_t sim_launch(const SimArgs *runs, uint32_t n_runs, void *ws, uint32_t *
         if (a.policy != kSjf && n <= kAmMaxN) {
             ea.rpos = rpos;
             ea.rstart = rstart;
+            ea.qid = qp.qid;
+            ea.qarr = qp.qarr;
+            ea.qgrp = qp.qgrp;
+            ea.qobs = qp.qobs;
+            // the list engine's key buffer, unused on this engine
+            ea.qest = reinterpret_cast<double *>(key);
+            qp.est[r] = est_base;
+            qp.qest[r] = reinterpret_cast<double *>(key);
             ea.cand_k = reinterpret_cast<uint64_t *>(cand);
             ea.cand_j = reinterpret_cast<uint32_t *>(cand + (uint64_t)kMaxQ * kSimMaxBatch * 8);
             ea.cand_i = reinterpret_cast<uint32_t *>(cand + (uint64_t)kMaxQ * kSimMaxBatch * 12);
@@ -1856,6 +1975,7 @@ hipError_t sim_launch(const SimArgs *runs, uint32_t n_runs, void *ws, uint32_t *
         for (uint32_t q = 0; q < kMaxQ; q++) pin.cls[q] = q;
         e = am_partition(pin, rpos, rstart, sort_ws, s);
         if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(k_sim_qprep, dim3(grid_for(n), n_runs), dim3(256), 0, s, qp);
     }
     hipLaunchKernelGGL(k_sim_engine, dim3(n_runs), dim3(kTPB), 0, s, eb, cshared);
     return hipGetLastError();
