@@ -583,6 +583,26 @@ __device__ void engine_list(const EngineArgs &a, ListLds &L, uint32_t k0 = 0, ui
     if (tid == 0) a.n_dispatched[0] = total;
 }
 
+// Lanes below m whose g equals this lane's, matched bit by bit with ballots
+// over the bits a group below n_groups can have (a lane at or past m, or
+// with g >= n_groups, is its own class of one: its result is not used).
+__device__ __forceinline__ uint64_t same_group_lanes(uint32_t g, uint32_t m, uint32_t n_groups)
+{
+    const int bits = n_groups > 1 ? 32 - __clz((int)(n_groups - 1)) : 1;
+    const uint64_t active = m >= 64 ? ~0ull : (1ull << m) - 1ull;
+    uint64_t same = active;
+    for (int b = 0; b < bits; b++) {
+        const bool one = (g >> b) & 1u;
+        const uint64_t mk = __ballot(one);
+        same &= one ? mk : ~mk;
+    }
+    // lanes whose g has higher bits set match only lanes with the same g
+    // above the compared bits; a lane below n_groups has none of those
+    const bool high = bits < 32 && (g >> bits) != 0u;
+    const uint64_t hk = __ballot(high);
+    return high ? (same & hk & (1ull << (uint32_t)lane_id())) : (same & ~hk);
+}
+
 // Batches up to kQLdsBatch with up to kQLdsGroups groups keep the queue
 // engine's candidates, their completion events and the factors in LDS;
 // other runs use the workspace and the state array.
@@ -597,9 +617,9 @@ struct QueueLds {
     uint32_t s_sel[kSimMaxBatch];    // candidate of each dispatch place
     uint32_t s_evg[kSimMaxBatch], s_evo[kSimMaxBatch];
     double s_evx[kSimMaxBatch];
-    uint64_t ck[kQCand];             // candidates: key, FIFO position, request, event
-    uint32_t cj[kQCand], ci[kQCand], cg[kQCand], co[kQCand];
-    double cx[kQCand];
+    uint64_t ck[kQCand];             // candidates: key, FIFO position, request, and its
+    uint32_t cj[kQCand], ci[kQCand], cg[kQCand], co[kQCand];   // event: group, observed
+    double cx[kQCand];                                          // length, B-free estimate
 };
 
 // The loop for FIFO, Priority, Weighted and Aging with one queue per tier.
@@ -767,41 +787,44 @@ __device__ void engine_queues(const EngineArgs &a, QueueLds &Q)
         }
         sync();
 
-        // 3. dispatch, and the completion events of the batch
-        if (tid < m) {
-            const uint32_t p = s_sel[tid], id = ci[p];
-            if (total + tid < n) a.seq[total + tid] = id;
+        // 3. dispatch, and the completion events of the batch (in LDS mode
+        //    from wave 1 on: the global stores stay in flight on waves other
+        //    than the one that runs the factor updates next)
+        const uint32_t d = kL ? tid - 64 : tid;
+        if ((!kL || tid >= 64) && d < m) {
+            const uint32_t p = s_sel[d], id = ci[p];
+            if (total + d < n) a.seq[total + d] = id;
             a.tick_of[id] = (int32_t)k;
             if (kL) {
-                s_evg[tid] = Q.cg[p];
-                s_evx[tid] = Q.cx[p];
-                s_evo[tid] = Q.co[p];
+                s_evg[d] = Q.cg[p];
+                s_evx[d] = Q.cx[p];
+                s_evo[d] = Q.co[p];
             } else {
-                s_evg[tid] = a.group[id];
-                s_evx[tid] = a.est_base[id];
-                s_evo[tid] = a.observed[id];
+                s_evg[d] = a.group[id];
+                s_evx[d] = a.est_base[id];
+                s_evo[d] = a.observed[id];
             }
         }
         sync();
 
         // 4. Eq. (5) with the ratio of Eq. (6), each group's events of the
         //    batch in dispatch order
+        auto step = [&](double c, uint32_t r) {
+            const double x = s_evx[r];
+            if (!(isfinite(x) && x > 0.0)) return c;
+            const double ratio = (double)s_evo[r] / x;
+            const double t1 = oma * c;
+            const double t2 = a.alpha * ratio;
+            return t1 + t2;
+        };
         if (kL && m <= 64) {
             if (w == 0) {
                 const uint32_t g = lane < m ? s_evg[lane] : kNoGroup;
-                uint64_t same = 0;
-                for (uint32_t j = 0; j < m; j++) same |= (uint64_t)(readlane32(g, (int)j) == g) << j;
+                const uint64_t same = same_group_lanes(g, m, a.n_groups);
                 if (lane < m && g < a.n_groups && (same & lanemask_lt()) == 0) {
                     double c = Q.sst[g];
-                    for (uint64_t bits = same; bits; bits &= bits - 1ull) {
-                        const uint32_t r = (uint32_t)__ffsll((unsigned long long)bits) - 1u;
-                        const double x = s_evx[r];
-                        if (!(isfinite(x) && x > 0.0)) continue;
-                        const double ratio = (double)s_evo[r] / x;
-                        const double t1 = oma * c;
-                        const double t2 = a.alpha * ratio;
-                        c = t1 + t2;
-                    }
+                    for (uint64_t bits = same; bits; bits &= bits - 1ull)
+                        c = step(c, (uint32_t)__ffsll((unsigned long long)bits) - 1u);
                     Q.sst[g] = c;
                 }
             }
@@ -811,15 +834,8 @@ __device__ void engine_queues(const EngineArgs &a, QueueLds &Q)
             for (uint32_t r = 0; r < tid && lead; r++) lead = s_evg[r] != g;
             if (lead) {
                 double c = kL ? Q.sst[g] : a.state[g];
-                for (uint32_t r = tid; r < m; r++) {
-                    if (s_evg[r] != g) continue;
-                    const double x = s_evx[r];
-                    if (!(isfinite(x) && x > 0.0)) continue;
-                    const double ratio = (double)s_evo[r] / x;
-                    const double t1 = oma * c;
-                    const double t2 = a.alpha * ratio;
-                    c = t1 + t2;
-                }
+                for (uint32_t r = tid; r < m; r++)
+                    if (s_evg[r] == g) c = step(c, r);
                 if (kL) Q.sst[g] = c;
                 else a.state[g] = c;
             }
@@ -903,8 +919,8 @@ struct ClassLds {
         } e;
         struct {                     // window candidates
             uint64_t k[kWin];
-            double x[kWin];          // the B-free estimate of Eq. (2)
-            uint32_t j[kWin], id[kWin], obs[kWin], slot[kWin];
+            double t2[kWin];         // alpha x its Eq. (6) ratio, if usable
+            uint32_t j[kWin], id[kWin], use[kWin], slot[kWin];
         } w;
     } u;
     uint32_t sel[kClsMaxBatch];      // the candidate of each dispatch place
@@ -916,9 +932,9 @@ struct ClassLds {
     uint32_t cnt[4];                 // touched classes, overflow, entering classes, candidates
     uint32_t fail;
     uint32_t hist[256], w[kNW], pick[4];
-    uint32_t evg[kClsMaxBatch], evo[kClsMaxBatch], evr[kClsMaxBatch];
-    double evx[kClsMaxBatch];
-    uint32_t rg0[64], roff[64], rtot; // classes touched by the factor updates: ranges
+    uint32_t evg[kClsMaxBatch], evo[kClsMaxBatch], evr[kClsMaxBatch];   // evo: usable
+    double evx[kClsMaxBatch];                                           // alpha x ratio
+    uint32_t rg0[kClsMaxBatch], rlen[kClsMaxBatch];   // classes touched by the factor updates
 };
 
 struct Resume {
@@ -1390,12 +1406,15 @@ __device__ Resume engine_class(const EngineArgs &a, const ClassShared &cs, Class
                 b = wd + b;
                 const uint64_t K = ordered_bits(b);
                 if (hl == 0 || R < m || !pair_lt(S.pk[cur][m - 1], S.pj[cur][m - 1], K, J)) {
+                    // the completion's term of Eq. (5), ahead of the serial updates
+                    const double x = TS * F;
+                    const bool use = isfinite(x) && x > 0.0;
                     const uint32_t slot = atomicAdd(&S.cnt[3], 1u);
                     S.u.w.k[slot] = K;
                     S.u.w.j[slot] = J;
-                    S.u.w.x[slot] = TS * F;
+                    S.u.w.t2[slot] = use ? a.alpha * ((double)obs / x) : 0.0;
                     S.u.w.id[slot] = id;
-                    S.u.w.obs[slot] = obs;
+                    S.u.w.use[slot] = use ? 1u : 0u;
                     S.u.w.slot[slot] = (r << 5) | hl;
                 }
             }
@@ -1409,31 +1428,33 @@ __device__ Resume engine_class(const EngineArgs &a, const ClassShared &cs, Class
         }
         lds_sync();
 
-        // 4. dispatch, and the completion events of the batch
-        if (tid < m) {
-            const uint32_t i = S.sel[tid], v = S.u.w.slot[i], r = v >> 5;
+        // 4. dispatch, and the completion events of the batch (wave 1: the
+        //    global stores stay in flight on a wave other than the one that
+        //    runs the factor updates next)
+        if (tid >= 64 && tid - 64 < m) {
+            const uint32_t d = tid - 64;
+            const uint32_t i = S.sel[d], v = S.u.w.slot[i], r = v >> 5;
             const uint32_t p = S.wpos[r][v & 31u], id = S.u.w.id[i];
-            if (total + tid < n) a.seq[total + tid] = id;
+            if (total + d < n) a.seq[total + d] = id;
             a.tick_of[id] = (int32_t)k;
             atomicAnd((unsigned long long *)&a.cls_elig[p >> 6], ~(1ull << (p & 63u)));
             S.last[r] = 1;
-            S.evg[tid] = S.sg[r];
-            S.evr[tid] = r;
-            S.evx[tid] = S.u.w.x[i];
-            S.evo[tid] = S.u.w.obs[i];
+            S.evg[d] = S.sg[r];
+            S.evr[d] = r;
+            S.evx[d] = S.u.w.t2[i];
+            S.evo[d] = S.u.w.use[i];
         }
         if (tid == 0) S.cnt[3] = 0;
         lds_sync();
-        // the classes served get new heads
-        if (tid < R && S.last[tid]) mark_dirty(S.sc[tid], S);
+        // the classes served get new heads (wave 2, beside wave 0's updates)
+        if (tid >= 128 && tid - 128 < R && S.last[tid - 128]) mark_dirty(S.sc[tid - 128], S);
         // 5. Eq. (5) with the ratio of Eq. (6) on one wave (lane i: the
         //    batch's i-th event): each group's first event walks that
         //    group's events in dispatch order; a group whose factor moved
         //    touches its classes (ranges, spread over the block below)
         if (w == 0) {
             const uint32_t g = lane < m ? S.evg[lane] : kNone;
-            uint64_t same = 0;
-            for (uint32_t j = 0; j < m; j++) same |= (uint64_t)(readlane32(g, (int)j) == g) << j;
+            const uint64_t same = same_group_lanes(g, m, a.n_groups);
             uint32_t len = 0, g0 = 0;
             if (lane < m && (same & lanemask_lt()) == 0) {
                 const uint32_t r0 = S.evr[lane];
@@ -1441,12 +1462,9 @@ __device__ Resume engine_class(const EngineArgs &a, const ClassShared &cs, Class
                 bool moved = false;
                 for (uint64_t bits = same; bits; bits &= bits - 1ull) {
                     const uint32_t r = (uint32_t)__ffsll((unsigned long long)bits) - 1u;
-                    const double x = S.evx[r];
-                    if (!(isfinite(x) && x > 0.0)) continue;
-                    const double ratio = (double)S.evo[r] / x;
+                    if (!S.evo[r]) continue;
                     const double t1 = oma * c;
-                    const double t2 = a.alpha * ratio;
-                    c = t1 + t2;
+                    c = t1 + S.evx[r];
                     moved = true;
                 }
                 if (moved) {
@@ -1459,20 +1477,16 @@ __device__ Resume engine_class(const EngineArgs &a, const ClassShared &cs, Class
                     }
                 }
             }
-            const uint32_t incl = wave_incl_scan_dpp(len);
-            S.rg0[lane] = g0;
-            S.roff[lane] = incl - len;
-            if (lane == 63) S.rtot = incl;
+            if (lane < kClsMaxBatch) {
+                S.rg0[lane] = g0;
+                S.rlen[lane] = len;
+            }
         }
         lds_sync();
-        for (uint32_t i = tid; i < S.rtot && !S.cnt[1]; i += kTPB) {
-            uint32_t lo = 0, hi = 64;   // the last range starting at or before i
-            while (hi - lo > 1) {
-                const uint32_t mid = (lo + hi) >> 1;
-                if (S.roff[mid] <= i) lo = mid;
-                else hi = mid;
-            }
-            mark_dirty(S.rg0[lo] + (i - S.roff[lo]), S);
+        {
+            // range r = tid / 32, its classes i, i + 32, ... from i = tid % 32
+            const uint32_t r = tid >> 5, len = r < m ? S.rlen[r] : 0u;
+            for (uint32_t u = tid & 31u; u < len && !S.cnt[1]; u += 32) mark_dirty(S.rg0[r] + u, S);
         }
         P -= m;
         total += m;
