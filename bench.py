@@ -693,6 +693,33 @@ def bench_simulate(args, wl):
     res["one_launch"] = {"runs": [r[0] for r in runs], "ms": round(ms_multi, 3),
                          "dispatched": [int(x) for x in nd_multi.cpu()],
                          "ticks_per_s_per_run": round(len(ticks) / (ms_multi * 1e-3), 1)}
+    # a sweep that fills the GPU (one workgroup per run, up to one per CU):
+    # the five policies in turn at EMA weights spread over [0.02, 0.5], as
+    # many runs as ds.SIM_MAX_RUNS allows within a 48 GB workspace
+    per_run = ds.workspace_bytes(ds.OP_SIMULATE_MULTI, N, 2) - ds.workspace_bytes(ds.OP_SIMULATE_MULTI, N, 1)
+    R = int(min(ds.SIM_MAX_RUNS, max(8, (48 << 30) // max(per_run, 1))))
+    pols = list(ds.POLICIES.values())
+    sweep_alpha = [0.02 + 0.48 * (r // 5) / max(1, (R - 1) // 5) for r in range(R)]
+    kw_sweep = {k: v for k, v in kw.items() if k != "alpha"}
+    sweep = [ds.sim_params(pols[r % 5], batch=32, alpha=sweep_alpha[r], **kw_sweep) for r in range(R)]
+    sstates = [torch.ones(b.n_groups, dtype=torch.float64, device="cuda") for _ in range(R)]
+    sws = ds.workspace(ds.OP_SIMULATE_MULTI, N, R)
+
+    def run_sweep():
+        for st in sstates:
+            st.fill_(1.0)
+        return ds.simulate_multi(d["arrival"], d["tier"], d["words"], d["category"], d["tenant"],
+                                 d["group"], d["observed"], d["t_base"], d["s_tenant"], sstates, tick_t,
+                                 sweep, ws=sws)
+    ms_sweep = timed_ms(run_sweep, a2)
+    _, nd_sweep = run_sweep()
+    tot = int(nd_sweep.to(torch.int64).sum().cpu())
+    res["sweep"] = {"runs": R, "policies": "the five in turn", "alphas": [round(sweep_alpha[0], 4),
+                                                                          round(sweep_alpha[-1], 4)],
+                    "ms": round(ms_sweep, 3), "dispatched_total": tot,
+                    "requests_per_s": round(tot / (ms_sweep * 1e-3), 1),
+                    "ticks_per_s_per_run": round(len(ticks) / (ms_sweep * 1e-3), 1)}
+    del sws, sstates
     for name, pol in ds.POLICIES.items():
         p = ds.sim_params(pol, batch=32, alpha=b.alphas[0], weights=tuple(int(w) for w in b.weights),
                           tier_priority=tuple(b.tier_priority), aging_rate=b.aging_rate,

@@ -487,9 +487,11 @@ ds_status ds_simulate(uint32_t n, const double *arrival, const uint8_t *tier,
 /*
  * Several dispatch-tick loops over the same requests and ticks in one launch
  * (one workgroup per run, after one shared FIFO sort), e.g. the five
- * policies, or one policy at several EMA weights. Run r is ds_simulate with
- * params[r], state[r], seq[r], tick_of[r] and n_dispatched[r]; its results
- * are identical to that call's.
+ * policies, or a sweep of EMA weights: up to DS_SIM_MAX_RUNS runs, one per
+ * compute unit of the device. Run r is ds_simulate with params[r],
+ * state[r], seq[r], tick_of[r] and n_dispatched[r]; its results are
+ * identical to that call's. The workspace grows with n_runs (about 75 bytes
+ * per request per run, plus the shared part).
  *
  *  n_runs        1..DS_SIM_MAX_RUNS
  *  params        HOST array of n_runs parameter sets (each checked as ds_simulate's)
@@ -499,7 +501,7 @@ ds_status ds_simulate(uint32_t n, const double *arrival, const uint8_t *tier,
  *  ws            workspace of ds_workspace_bytes(DS_OP_SIMULATE_MULTI, n, n_runs) bytes
  * Other arguments and errors as ds_simulate.
  */
-#define DS_SIM_MAX_RUNS 8
+#define DS_SIM_MAX_RUNS 256
 ds_status ds_simulate_multi(uint32_t n_runs, uint32_t n, const double *arrival, const uint8_t *tier,
                             const uint32_t *counts, const uint8_t *category, const uint32_t *tenant,
                             const uint32_t *group, const uint32_t *observed, const double *t_base,

@@ -3,6 +3,9 @@
 #include <math.h>
 #include <string.h>
 
+#include <memory>
+#include <new>
+
 #include <mutex>
 
 #include "../../include/driftsched.h"
@@ -527,8 +530,9 @@ static ds_status sim_common(uint32_t n_runs, uint32_t n, const double *arrival, 
 {
     if (n_runs < 1 || n_runs > DS_SIM_MAX_RUNS) return DS_ERR_ARG;
     if (!params || !state || !seq || !tick_of) return DS_ERR_NULL;
-    SimArgs runs[DS_SIM_MAX_RUNS];
-    memset(runs, 0, sizeof(runs));
+    std::unique_ptr<SimArgs[]> runs(new (std::nothrow) SimArgs[n_runs]);
+    if (!runs) return DS_ERR_HIP;
+    memset(runs.get(), 0, n_runs * sizeof(SimArgs));
     for (uint32_t r = 0; r < n_runs; r++) {
         ds_status st = sim_run_args(params + r, n, state[r], seq[r], tick_of[r], runs[r]);
         if (st != DS_OK) return st;
@@ -569,7 +573,7 @@ static ds_status sim_common(uint32_t n_runs, uint32_t n, const double *arrival, 
     }
     hipStream_t s = static_cast<hipStream_t>(stream);
     return run_waits(ws, flags, s, [&](uint32_t *flag) {
-        return sim_launch(runs, n_runs, after_flag(ws), flag, s, wait_cfg(ws, flags));
+        return sim_launch(runs.get(), n_runs, after_flag(ws), flag, s, wait_cfg(ws, flags));
     });
 }
 

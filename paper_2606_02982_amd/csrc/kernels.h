@@ -229,7 +229,7 @@ struct SimArgs {
     uint32_t *n_dispatched;
 };
 constexpr uint32_t kSimMaxBatch = 1024;
-constexpr uint32_t kSimMaxRuns = 8;
+constexpr uint32_t kSimMaxRuns = 256;
 size_t sim_ws_bytes(uint64_t n, uint32_t n_runs);
 // n_runs runs sharing every input array, the ticks and n (their parameters
 // and outputs may differ; run r's n_dispatched is runs[0].n_dispatched + r).

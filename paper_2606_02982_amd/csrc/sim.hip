@@ -33,6 +33,9 @@
 //     sequential evaluation.
 #include <string.h>
 
+#include <memory>
+#include <new>
+
 #include "common.h"
 #include "kernels.h"
 #include "wrrplan.h"
@@ -106,13 +109,18 @@ struct EngineArgs {
     double f_ref;
 };
 
-// Several runs share one launch: run r is block row r of the setup and block
-// r of the engine.
+// Several runs share one launch: run r is block r of the engine. Their
+// arguments go by value, kSimChunk runs per kernel argument block: the
+// set-up runs chunk by chunk (block row = run of the chunk); an engine
+// launch of at most kSimChunk runs takes them directly, a larger one from
+// the workspace, where a small kernel per chunk has copied them (kernel
+// arguments are captured by value, so the launch stays capturable).
+constexpr uint32_t kSimChunk = 8;
 struct SetupBatch {
-    SetupArgs r[kSimMaxRuns];
+    SetupArgs r[kSimChunk];
 };
 struct EngineBatch {
-    EngineArgs r[kSimMaxRuns];
+    EngineArgs r[kSimChunk];
 };
 static_assert(sizeof(SetupBatch) <= 4096, "kernel arguments within 4 KB");
 
@@ -1506,10 +1514,8 @@ union EngineLds {
 // One workgroup per run: the queue engine where the run has its tier runs,
 // the class engine for SJF where it applies (the list engine taking over if
 // its conditions fail), else the list engine.
-__global__ __launch_bounds__(kTPB) void k_sim_engine(EngineBatch eb, ClassShared cs)
+__device__ __forceinline__ void engine_run(const EngineArgs &a, const ClassShared &cs, EngineLds &lds)
 {
-    __shared__ EngineLds lds;
-    const EngineArgs &a = eb.r[blockIdx.x];
     if (a.rpos) {
         if (a.batch <= kQLdsBatch && a.n_groups <= kQLdsGroups) engine_queues<true>(a, lds.q);
         else engine_queues<false>(a, lds.q);
@@ -1520,6 +1526,27 @@ __global__ __launch_bounds__(kTPB) void k_sim_engine(EngineBatch eb, ClassShared
     } else {
         engine_list(a, lds.l);
     }
+}
+
+static_assert(sizeof(EngineBatch) + sizeof(ClassShared) <= 4096, "kernel arguments within 4 KB");
+
+__global__ __launch_bounds__(kTPB) void k_sim_engine(EngineBatch eb, ClassShared cs)
+{
+    __shared__ EngineLds lds;
+    engine_run(eb.r[blockIdx.x], cs, lds);
+}
+
+__global__ __launch_bounds__(kTPB) void k_sim_engine_many(const EngineArgs *__restrict__ runs, ClassShared cs)
+{
+    __shared__ EngineLds lds;
+    engine_run(runs[blockIdx.x], cs, lds);
+}
+
+// A chunk's engine arguments (count runs) into their slots of the
+// workspace's array.
+__global__ void k_sim_stage(EngineBatch eb, EngineArgs *__restrict__ dst, uint32_t count)
+{
+    if (threadIdx.x < count) dst[threadIdx.x] = eb.r[threadIdx.x];
 }
 
 // ---- class structure set-up (the class engine's) -------------------------------------
@@ -1651,16 +1678,16 @@ __global__ void k_cls_fin(const ClassBuild b)
 }
 
 // The tier runs' entries in run order: request, arrival, group and
-// observed length; and, per run on the queue engine (blockIdx.y), the B-free
-// estimate.
+// observed length (with `shared`); and, per run of a chunk on the queue
+// engine (blockIdx.y), the B-free estimate.
 struct QPrep {
     const uint32_t *rpos, *fifo, *group, *observed;
     const double *arrival;
-    uint32_t n;
+    uint32_t n, shared;
     uint32_t *qid, *qgrp, *qobs;
     double *qarr;
-    const double *est[kSimMaxRuns];
-    double *qest[kSimMaxRuns];
+    const double *est[kSimChunk];
+    double *qest[kSimChunk];
 };
 
 __global__ void k_sim_qprep(const QPrep q)
@@ -1672,7 +1699,7 @@ __global__ void k_sim_qprep(const QPrep q)
         j = j < q.n ? j : 0u;
         uint32_t id = q.fifo[j];
         id = id < q.n ? id : 0u;   // the FIFO order is a permutation of 0..n-1
-        if (blockIdx.y == 0) {
+        if (q.shared && blockIdx.y == 0) {
             q.qid[r] = id;
             q.qarr[r] = q.arrival[id];
             q.qgrp[r] = q.group[id];
@@ -1738,6 +1765,7 @@ size_t sim_ws_bytes(uint64_t n, uint32_t n_runs)
                          align_up(n * sizeof(Aux), 256) + align_up(n, 256) + kCandBytes + cls_run_bytes(n);
     const uint64_t sort = sort_ws_bytes(n, 1), part = am_partition_ws_bytes(n);
     return 5 * align_up(n * 4, 256) + align_up(n * 8, 256) + 256 + cls_shared_bytes(n) +
+           align_up((uint64_t)(n_runs ? n_runs : 1) * sizeof(EngineArgs), 256) +
            (uint64_t)(n_runs ? n_runs : 1) * per + (sort > part ? sort : part);
 }
 
@@ -1768,7 +1796,7 @@ hipError_t sim_launch(const SimArgs *runs, uint32_t n_runs, void *ws, uint32_t *
     }
     if (n == 0) {
         // the runs' counters are one array (n_dispatched of run r = runs[0].n_dispatched + r)
-        hipLaunchKernelGGL(k_sim_empty, dim3(1), dim3(64), 0, s, a0.n_dispatched, n_runs);
+        hipLaunchKernelGGL(k_sim_empty, dim3(1), dim3(kSimMaxRuns), 0, s, a0.n_dispatched, n_runs);
         return hipGetLastError();
     }
     uint8_t *p = static_cast<uint8_t *>(ws);
@@ -1836,10 +1864,19 @@ hipError_t sim_launch(const SimArgs *runs, uint32_t n_runs, void *ws, uint32_t *
     cb.cs = take64(n);
     const ClassShared cshared = {cb.ctl, cb.clist, cb.lw, cb.lf, cb.lobs, cb.pos_f, cb.cls_f, cb.arr_f,
                                  cb.cstart, cb.ctb, cb.cs, cb.cg, cb.gfirst, cb.gend};
-    SetupBatch sb;
-    EngineBatch eb;
-    memset(&sb, 0, sizeof(sb));
-    memset(&eb, 0, sizeof(eb));
+    EngineArgs *staged = reinterpret_cast<EngineArgs *>(take((uint64_t)n_runs * sizeof(EngineArgs)));
+    // the runs' arguments, built here and launched chunk by chunk below
+    std::unique_ptr<SetupArgs[]> sv(new (std::nothrow) SetupArgs[n_runs]);
+    std::unique_ptr<EngineArgs[]> ev(new (std::nothrow) EngineArgs[n_runs]);
+    std::unique_ptr<const double *[]> qest_in(new (std::nothrow) const double *[n_runs]);
+    std::unique_ptr<double *[]> qest_out(new (std::nothrow) double *[n_runs]);
+    if (!sv || !ev || !qest_in || !qest_out) return hipErrorOutOfMemory;
+    memset(sv.get(), 0, n_runs * sizeof(SetupArgs));
+    memset(ev.get(), 0, n_runs * sizeof(EngineArgs));
+    for (uint32_t r = 0; r < n_runs; r++) {
+        qest_in[r] = nullptr;
+        qest_out[r] = nullptr;
+    }
     for (uint32_t r = 0; r < n_runs; r++) {
         const SimArgs &a = runs[r];
         uint32_t *list0 = reinterpret_cast<uint32_t *>(take((uint64_t)n * 4));
@@ -1854,7 +1891,7 @@ hipError_t sim_launch(const SimArgs *runs, uint32_t n_runs, void *ws, uint32_t *
         uint64_t *cls_elig = reinterpret_cast<uint64_t *>(take64(n / 64 + 1));
         uint64_t *cls_kk = reinterpret_cast<uint64_t *>(take64(n));
 
-        SetupArgs &su = sb.r[r];
+        SetupArgs &su = sv[r];
         su.n = n;
         su.policy = a.policy;
         su.n_cat = a.n_cat;
@@ -1887,7 +1924,7 @@ hipError_t sim_launch(const SimArgs *runs, uint32_t n_runs, void *ws, uint32_t *
         su.tick_of = a.tick_of;
         su.wait_status = r == 0 && wait.clear ? wait.status : nullptr;
 
-        EngineArgs &ea = eb.r[r];
+        EngineArgs &ea = ev[r];
         ea.n = n;
         ea.n_groups = a.n_groups;
         ea.policy = a.policy;
@@ -1926,8 +1963,8 @@ hipError_t sim_launch(const SimArgs *runs, uint32_t n_runs, void *ws, uint32_t *
             ea.qobs = qp.qobs;
             // the list engine's key buffer, unused on this engine
             ea.qest = reinterpret_cast<double *>(key);
-            qp.est[r] = est_base;
-            qp.qest[r] = reinterpret_cast<double *>(key);
+            qest_in[r] = est_base;
+            qest_out[r] = reinterpret_cast<double *>(key);
             ea.cand_k = reinterpret_cast<uint64_t *>(cand);
             ea.cand_j = reinterpret_cast<uint32_t *>(cand + (uint64_t)kMaxQ * kSimMaxBatch * 8);
             ea.cand_i = reinterpret_cast<uint32_t *>(cand + (uint64_t)kMaxQ * kSimMaxBatch * 12);
@@ -1941,7 +1978,13 @@ hipError_t sim_launch(const SimArgs *runs, uint32_t n_runs, void *ws, uint32_t *
         ea.f_ref = a.f_ref;
     }
     void *sort_ws = p;
-    hipLaunchKernelGGL(k_sim_setup, dim3(grid_for(n), n_runs), dim3(256), 0, s, sb);
+    for (uint32_t r0 = 0; r0 < n_runs; r0 += kSimChunk) {
+        const uint32_t cnt = n_runs - r0 < kSimChunk ? n_runs - r0 : kSimChunk;
+        SetupBatch sb;
+        memset(&sb, 0, sizeof(sb));
+        for (uint32_t i = 0; i < cnt; i++) sb.r[i] = sv[r0 + i];
+        hipLaunchKernelGGL(k_sim_setup, dim3(grid_for(n), cnt), dim3(256), 0, s, sb);
+    }
 
     SortInput in = {};
     in.n = n;
@@ -1989,9 +2032,31 @@ hipError_t sim_launch(const SimArgs *runs, uint32_t n_runs, void *ws, uint32_t *
         for (uint32_t q = 0; q < kMaxQ; q++) pin.cls[q] = q;
         e = am_partition(pin, rpos, rstart, sort_ws, s);
         if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(k_sim_qprep, dim3(grid_for(n), n_runs), dim3(256), 0, s, qp);
+        for (uint32_t r0 = 0; r0 < n_runs; r0 += kSimChunk) {
+            const uint32_t cnt = n_runs - r0 < kSimChunk ? n_runs - r0 : kSimChunk;
+            qp.shared = r0 == 0;
+            for (uint32_t i = 0; i < kSimChunk; i++) {
+                qp.est[i] = i < cnt ? qest_in[r0 + i] : nullptr;
+                qp.qest[i] = i < cnt ? qest_out[r0 + i] : nullptr;
+            }
+            hipLaunchKernelGGL(k_sim_qprep, dim3(grid_for(n), cnt), dim3(256), 0, s, qp);
+        }
     }
-    hipLaunchKernelGGL(k_sim_engine, dim3(n_runs), dim3(kTPB), 0, s, eb, cshared);
+    if (n_runs <= kSimChunk) {
+        EngineBatch eb;
+        memset(&eb, 0, sizeof(eb));
+        for (uint32_t r = 0; r < n_runs; r++) eb.r[r] = ev[r];
+        hipLaunchKernelGGL(k_sim_engine, dim3(n_runs), dim3(kTPB), 0, s, eb, cshared);
+    } else {
+        for (uint32_t r0 = 0; r0 < n_runs; r0 += kSimChunk) {
+            const uint32_t cnt = n_runs - r0 < kSimChunk ? n_runs - r0 : kSimChunk;
+            EngineBatch eb;
+            memset(&eb, 0, sizeof(eb));
+            for (uint32_t i = 0; i < cnt; i++) eb.r[i] = ev[r0 + i];
+            hipLaunchKernelGGL(k_sim_stage, dim3(1), dim3(64), 0, s, eb, staged + r0, cnt);
+        }
+        hipLaunchKernelGGL(k_sim_engine_many, dim3(n_runs), dim3(kTPB), 0, s, staged, cshared);
+    }
     return hipGetLastError();
 }
 

@@ -21,7 +21,7 @@ FIFO, PRIORITY, WEIGHTED, SJF, AGING = 0, 1, 2, 3, 4
 POLICIES = {"fifo": FIFO, "priority": PRIORITY, "weighted": WEIGHTED, "sjf": SJF, "aging": AGING}
 OP_CHARACTERIZE, OP_CALIBRATE, OP_SCORE, OP_ORDER, OP_ORDER_MULTI = 0, 1, 2, 3, 4
 OP_ERROR_STATS, OP_CLASS_HIST, OP_SIMULATE, OP_SIMULATE_MULTI = 5, 6, 7, 8
-SIM_MAX_RUNS = 8
+SIM_MAX_RUNS = 256
 DS_VALIDATE = 1
 DS_SERIAL_SORT = 2
 DS_NO_WAIT = 4          # diagnostic: bounded device-side waits give up at once

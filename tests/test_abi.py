@@ -50,12 +50,13 @@ def test_workspace_sizes(ds):
     assert ds.workspace_bytes(ds.OP_CLASS_HIST, 1 << 20) == 256
     # error statistics: sums for every group and for all events
     assert ds.workspace_bytes(ds.OP_ERROR_STATS, 10, 7) >= 256 + 4 * 8 * 8
-    # several tick loops: the third argument is the number of runs (1..8)
+    # several tick loops: the third argument is the number of runs (1..256)
     for n in (1, 4096, 65536):
         assert ds.workspace_bytes(ds.OP_SIMULATE_MULTI, n, 1) == ds.workspace_bytes(ds.OP_SIMULATE, n)
         assert ds.workspace_bytes(ds.OP_SIMULATE_MULTI, n, 8) > ds.workspace_bytes(ds.OP_SIMULATE_MULTI, n, 2)
         assert ds.workspace_bytes(ds.OP_SIMULATE_MULTI, n, 0) == 0
-        assert ds.workspace_bytes(ds.OP_SIMULATE_MULTI, n, 9) == 0
+        assert ds.workspace_bytes(ds.OP_SIMULATE_MULTI, n, ds.SIM_MAX_RUNS) > 0
+        assert ds.workspace_bytes(ds.OP_SIMULATE_MULTI, n, ds.SIM_MAX_RUNS + 1) == 0
 
 
 P = ctypes.c_void_p

@@ -247,11 +247,45 @@ def test_multi_runs_in_one_launch(ds, oracle, case):
         assert np.array_equal(host(states[r]), w_state), "run %d" % r
 
 
+def test_multi_many_runs_in_one_launch(ds, oracle):
+    """37 runs in one launch (more than the runs whose arguments fit one
+    kernel argument block: they are staged through the workspace, in chunks
+    of 8, the last one partial): the five policies and the smooth and stride
+    Weighted at several EMA weights, each equal to the oracle's loop."""
+    import torch
+    x = random_inputs(91, 2000, G=7)
+    ticks = np.linspace(0.05, 12.0, 160)
+    kw = dict(weights=(3, 2, 1), tier_priority=(0.0, 1.0, 2.0), aging_rate=0.3)
+    kinds = [(p, "blocked") for p in ALL] + [(WEIGHTED, "smooth"), (WEIGHTED, "stride")]
+    runs = [(kinds[r % len(kinds)][0], 0.03 + 0.02 * r, kinds[r % len(kinds)][1]) for r in range(37)]
+    params = [ds.sim_params(p, batch=32 if r % 3 else 8, alpha=a, n_tiers=3, weighted_mode=m, **kw)
+              for r, (p, a, m) in enumerate(runs)]
+    states = [dev(np.asarray(x["state"], np.float64).copy()) for _ in runs]
+    print("simulate_multi: %d runs, n=%d, ticks=%d" % (len(runs), len(x["arrival"]), len(ticks)), flush=True)
+    d = {k: dev(np.asarray(v)) for k, v in x.items() if k != "state"}
+    outs, nd = ds.simulate_multi(d["arrival"], d["tier"], d["counts"], d["category"], d["tenant"],
+                                 d["group"], d["observed"], d["t_base"], d["s_tenant"], states,
+                                 dev(np.asarray(ticks, np.float64)), params)
+    torch.cuda.synchronize()
+    nd = host(nd)
+    oracle_policy = {"blocked": None, "smooth": 5, "stride": 6}
+    for r, (p, a, m) in enumerate(runs):
+        op = oracle_policy[m] if p == WEIGHTED and oracle_policy[m] else p
+        w_seq, w_tick, w_state = oracle.simulate(op, x["arrival"], x["tier"], x["counts"], x["category"],
+                                                 x["tenant"], x["group"], x["observed"], x["t_base"],
+                                                 x["s_tenant"], x["state"], ticks, batch=32 if r % 3 else 8,
+                                                 alpha=a, **kw)
+        assert int(nd[r]) == len(w_seq), "run %d" % r
+        assert np.array_equal(host(outs[r][0], np.uint32)[:nd[r]], w_seq), "run %d" % r
+        assert np.array_equal(host(outs[r][1]), w_tick), "run %d" % r
+        assert np.array_equal(host(states[r]), w_state), "run %d" % r
+
+
 def test_multi_host_errors(ds):
     x = random_inputs(5, 10)
     d = {k: dev(np.asarray(v)) for k, v in x.items() if k != "state"}
     p = ds.sim_params(FIFO)
-    for R in (0, 9):
+    for R in (0, ds.SIM_MAX_RUNS + 1):
         with pytest.raises(ds.DriftSchedError) as e:
             ds.simulate_multi(d["arrival"], d["tier"], d["counts"], d["category"], d["tenant"],
                               d["group"], d["observed"], d["t_base"], d["s_tenant"],
