@@ -146,3 +146,53 @@ def test_order_modes_graph_replays(ds, mode, n):
             assert torch.equal(perms[p].cpu(), want[p]), "replay %d policy %d" % (rep, p)
         ds.order_multi((2,), tier, arrival, budget, params=params, ws=ws)   # eager work between replays
         torch.cuda.synchronize()
+
+
+def test_simulate_multi_graph_replays(ds):
+    """Twelve tick loops in one ds_simulate_multi launch (more runs than one
+    kernel argument block holds: their arguments are copied into the
+    workspace by small kernels) captured in a graph; every replay, with
+    eager calls in between, equals the eager call."""
+    from tests.test_gpu_sim import random_inputs
+    n, R = 3000, 12
+    x = random_inputs(17, n, G=5)
+    d = {k: dev(np.asarray(v)) for k, v in x.items() if k != "state"}
+    ticks = dev(np.linspace(0.05, 12.0, 120))
+    params = [ds.sim_params(r % 5, batch=32 if r % 4 else 8, alpha=0.05 + 0.03 * r, n_tiers=3,
+                            weights=(3, 2, 1), tier_priority=(0.0, 1.0, 2.0), aging_rate=0.3)
+              for r in range(R)]
+    ws = ds.workspace(ds.OP_SIMULATE_MULTI, n, R)
+    states = [torch.ones(5, dtype=torch.float64, device="cuda") for _ in range(R)]
+
+    def call():
+        for st in states:
+            st.fill_(1.0)   # a fill kernel, not a memset
+        return ds.simulate_multi(d["arrival"], d["tier"], d["counts"], d["category"], d["tenant"],
+                                 d["group"], d["observed"], d["t_base"], d["s_tenant"], states, ticks,
+                                 params, ws=ws)
+
+    print("graph simulate_multi: %d runs, n=%d" % (R, n), flush=True)
+    outs, nd = call()
+    torch.cuda.synchronize()
+    want = [t.cpu().clone() for o in outs for t in o] + [nd.cpu().clone()] + [s.cpu().clone() for s in states]
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        call()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=side):
+            gouts, gnd = call()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        for t in [t for o in gouts for t in o] + [gnd] + states:
+            t.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        got = [t.cpu() for o in gouts for t in o] + [gnd.cpu()] + [s.cpu() for s in states]
+        for i, (a, w) in enumerate(zip(got, want)):
+            assert torch.equal(a, w), "replay %d: output %d differs" % (rep, i)
+        call()   # eager work between the replays
+        torch.cuda.synchronize()
