@@ -106,8 +106,11 @@ typedef enum {
  * (above 4096 groups) and ds_simulate split their work into tiles that wait,
  * each for at most about 0.2 s, on counts published by tiles of smaller
  * index (decoupled look-back); the orders of more than 2^18 and at most
- * 2^20 requests have no such waits. In normal operation no wait runs out (a
- * tile waits only on tiles that have already started). If one does:
+ * 2^20 requests have no such waits. ds_calibrate of at most 64 chunks of
+ * 512, 1024 or 2048 events (and at most 16384 chunk-group pairs) runs in one
+ * launch whose chunks wait the same way for the maps of the chunks before
+ * them. In normal operation no wait runs out (a tile waits only on tiles
+ * that have already started and publish before they wait). If one does:
  *  - in a sample-sort scatter (up to 2^18 requests), the call finishes on
  *    the single-workgroup path instead, with exact results;
  *  - anywhere else the results are invalid, and the call's status word is

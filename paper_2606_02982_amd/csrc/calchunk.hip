@@ -23,10 +23,16 @@
 // is left out: each k_calc_apply block applies the maps of the chunks before
 // it to the initial factors itself (k_calc_agg keeps a copy of them), and
 // the last chunk's block writes the final factors.
+// When besides there are at most kOneChunks chunks of one sub-tile each,
+// k_calc_one does all of it in one pass over the events: each block sorts
+// and scans its sub-tile once, publishes its chunk's maps, reads those of
+// the chunks before it (a bounded wait for words not yet written), and
+// applies the updates; a small launch before it marks the words unwritten.
 // Results match the sequential recurrence up to the rounding of the
 // composed maps (a few ulps; the contract is 1e-12 relative).
 #include "common.h"
 #include "kernels.h"
+#include "lookback.h"
 
 namespace ds {
 namespace {
@@ -57,7 +63,9 @@ struct CalArgs {
     uint32_t small;          // C x G <= kSmallTable
     double *state;           // [G] in: before all events, out: after
     double *trace, *trace_before;
-    uint32_t *wait_status;   // or NULL: zeroed by k_calc_agg (this path has no waits)
+    uint32_t *status;        // the call's wait status word, or NULL: set by a wait that runs out
+    uint32_t clear;          // the call's first kernel zeroes *status
+    uint32_t no_wait;        // every wait gives up at once (a diagnostic of the error path)
 };
 
 // A composed affine map: x -> a x + b, f = a segment starts inside,
@@ -339,7 +347,7 @@ __global__ __launch_bounds__(kT) void k_calc_agg(CalArgs a)
     __shared__ SubShared<kE> sh;
     __shared__ double sA[kG], sB[kG];   // the chunk's map per group so far (A < 0: none)
     const uint32_t t = threadIdx.x, c = blockIdx.x;
-    if (a.wait_status && c == 0 && t == 0) *a.wait_status = 0;
+    if (a.clear && a.status && c == 0 && t == 0) *a.status = 0;
     for (uint32_t g = t; g < a.G; g += kT) {
         sA[g] = -1.0;
         sB[g] = 0.0;
@@ -626,6 +634,217 @@ __global__ __launch_bounds__(kT) void k_calc_apply(CalArgs a)
     }
 }
 
+// ---- one launch for small tables of one sub-tile per chunk -------------------
+//
+// Each block publishes its chunk's maps M(c, g) as two 64-bit words per group
+// (A, then B) as soon as it has formed them, and only then reads the words
+// of the chunks before it, so a block never waits before publishing. Every
+// word was set to kUnset (a signalling NaN) by k_calc_unset just before: A
+// is -1 or in [0, 1] and B an arithmetic result (never a signalling NaN), so
+// each word shows by itself whether it has been written, and no ordering
+// between the stores of a block is needed.
+constexpr uint64_t kUnset = 0x7FF4DEADBEEF0001ull;
+constexpr uint32_t kOneChunks = 64;   // chunks of the one-launch path at most
+constexpr uint32_t kOneR = 16;   // chunk maps per thread loaded at once
+
+__device__ __forceinline__ uint64_t ld_relaxed64(const uint64_t *p)
+{
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ void st_relaxed64(uint64_t *p, uint64_t v)
+{
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__global__ __launch_bounds__(256) void k_calc_unset(uint64_t *w, uint32_t nw, uint32_t *wait_status)
+{
+    const uint32_t i = blockIdx.x * 256u + threadIdx.x;
+    if (wait_status && i == 0) *wait_status = 0;
+    for (uint32_t k = i; k < nw; k += gridDim.x * 256u) w[k] = kUnset;
+}
+
+template <int kE>
+__global__ __launch_bounds__(kT) void k_calc_one(CalArgs a)
+{
+    constexpr uint32_t kSub = kT * kE;
+    static_assert(kSub <= kG, "the trace_before staging shares sA");
+    __shared__ SubShared<kE> sh;
+    __shared__ double sA[kG], sB[kG];   // this chunk's map per group; sA then stages trace_before
+    __shared__ double sv[kG];           // each group's factor (initial, then at the current point)
+    __shared__ uint8_t su[kG];          // the group has a usable event so far
+    const uint32_t t = threadIdx.x, c = blockIdx.x;
+    // the initial factors are read before this block publishes anything: the
+    // last block overwrites them only after every other block has published
+    for (uint32_t g = t; g < a.G; g += kT) {
+        sA[g] = -1.0;
+        sB[g] = 0.0;
+        sv[g] = a.state[g];
+        su[g] = 0;
+    }
+    const uint64_t c0 = (uint64_t)c * kSub;
+    const uint32_t m = (uint32_t)(a.E - c0 < kSub ? a.E - c0 : kSub);
+    Raw<kE> raw;
+    load_raw<kE>(a, (uint32_t)c0, m, raw);
+    Sub<kE> sub;
+    load_sort_scan<kE>(a, raw, m, sh, sub);   // (its first barrier orders the writes above)
+    // which positions end their group's segment
+    uint32_t lastm = 0;
+#pragma unroll
+    for (int e = 0; e < kE; e++) {
+        const uint32_t i = t * kE + (uint32_t)e;
+        if (i < m && ((i + 1 == m) || (e + 1 < kE ? sub.flag[e + 1] != 0u : sh.key[i + 1] != sh.key[i])))
+            lastm |= 1u << e;
+    }
+    // this chunk's map of each group: its segment composed at its last position
+    {
+        Map run = sub.excl;
+#pragma unroll
+        for (int e = 0; e < kE; e++) {
+            if (t * kE + (uint32_t)e >= m) break;
+            Map mp;
+            mp.f = sub.flag[e];
+            mp.u = sub.ok[e];
+            mp.a = sub.ok[e] ? a.oma : 1.0;
+            mp.b = sub.ok[e] ? sub.b[e] : 0.0;
+            run = mp.f ? mp : combine(run, mp);
+            const uint32_t g = sub.key[e];
+            if (((lastm >> e) & 1u) && g < a.G && run.u) {
+                sA[g] = run.a;
+                sB[g] = run.b;
+            }
+        }
+    }
+    lds_sync();
+    uint64_t *pubA = reinterpret_cast<uint64_t *>(a.aggA), *pubB = reinterpret_cast<uint64_t *>(a.aggB);
+    if (c + 1 < a.C)   // the last chunk's maps are read by nobody
+        for (uint32_t g = t; g < a.G; g += kT) {
+            st_relaxed64(&pubA[(uint64_t)c * a.G + g], (uint64_t)__double_as_longlong(sA[g]));
+            st_relaxed64(&pubB[(uint64_t)c * a.G + g], (uint64_t)__double_as_longlong(sB[g]));
+        }
+    // the carry of each group: the maps of chunks 0 .. c-1 composed in order
+    // (tpg threads per group, each over a contiguous range of them, then an
+    // ordered tree of shuffles), applied to the initial factor
+    uint32_t tpg = 1;
+    while (tpg < 64 && tpg * 2 * a.G <= (uint32_t)kT) tpg *= 2;
+    const uint32_t p = t % tpg, jb = p * c / tpg, je = (p + 1) * c / tpg;
+    bool gave_up = false;
+    for (uint32_t g0 = 0; g0 < a.G; g0 += kT / tpg) {
+        const uint32_t g = g0 + t / tpg;
+        const bool gin = g < a.G;
+        Map mp = {0u, 0u, 1.0, 0.0};
+        if (c > 0 && a.no_wait) gave_up = true;
+        for (uint32_t j0 = jb; gin && !gave_up && j0 < je; j0 += kOneR) {
+            uint64_t A[kOneR], B[kOneR];
+#pragma unroll
+            for (uint32_t r = 0; r < kOneR; r++) {
+                A[r] = 0;
+                B[r] = 0;
+                if (j0 + r < je) {
+                    A[r] = ld_relaxed64(&pubA[(uint64_t)(j0 + r) * a.G + g]);
+                    B[r] = ld_relaxed64(&pubB[(uint64_t)(j0 + r) * a.G + g]);
+                }
+            }
+            // a word still unset is read again until it is written (bounded)
+            uint32_t spins = 0;
+            for (;;) {
+                bool ready = true;
+#pragma unroll
+                for (uint32_t r = 0; r < kOneR; r++) ready = ready && A[r] != kUnset && B[r] != kUnset;
+                if (ready) break;
+                if (++spins > kSpinLimit) {
+                    gave_up = true;
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+                for (uint32_t r = 0; r < kOneR; r++) {
+                    if (A[r] == kUnset) A[r] = ld_relaxed64(&pubA[(uint64_t)(j0 + r) * a.G + g]);
+                    if (B[r] == kUnset) B[r] = ld_relaxed64(&pubB[(uint64_t)(j0 + r) * a.G + g]);
+                }
+            }
+#pragma unroll
+            for (uint32_t r = 0; r < kOneR; r++) {
+                const double av = __longlong_as_double((long long)A[r]);
+                if (j0 + r < je && av >= 0.0)
+                    mp = combine(mp, Map{0u, 1u, av, __longlong_as_double((long long)B[r])});
+            }
+        }
+        for (uint32_t d = 1; d < tpg; d <<= 1) {
+            Map o;
+            o.f = 0u;
+            o.u = (uint32_t)__shfl_down((int)mp.u, (int)d, 64);
+            o.a = shfl_down_d(mp.a, (int)d);
+            o.b = shfl_down_d(mp.b, (int)d);
+            if (p % (2 * d) == 0) mp = combine(mp, o);
+        }
+        if (gin && p == 0 && mp.u) {
+            const double tt = mp.a * sv[g];
+            sv[g] = tt + mp.b;
+            su[g] = 1;
+        }
+    }
+    if (gave_up && a.status) atomicOr(a.status, 1u);
+    lds_sync();
+    // every event's exact update from its factor before (as in k_calc_apply)
+    const double nan = __builtin_nan("");
+    double *tr = sh.b, *trb = sA;
+    double cv;
+    {
+        const uint32_t g0 = sub.key[0];
+        const double base = g0 < a.G ? sv[g0] : nan;
+        cv = base;
+        if (!sub.flag[0] && sub.excl.u) {
+            const double tt = sub.excl.a * base;
+            cv = tt + sub.excl.b;
+        }
+    }
+    double after[kE];
+#pragma unroll
+    for (int e = 0; e < kE; e++) {
+        const uint32_t i = t * kE + (uint32_t)e;
+        after[e] = cv;
+        if (i >= m) continue;
+        const uint32_t g = sub.key[e];
+        if (sub.flag[e]) cv = g < a.G ? sv[g] : nan;
+        trb[sub.slot[e]] = cv;
+        if (sub.ok[e]) {
+            su[g] = 1;
+            const double t1 = a.oma * cv;
+            cv = t1 + sub.b[e];
+        }
+        tr[sub.slot[e]] = cv;
+        after[e] = cv;
+    }
+    lds_sync();   // every read of sv above precedes the updates below
+#pragma unroll
+    for (int e = 0; e < kE; e++) {
+        const uint32_t g = sub.key[e];
+        if (((lastm >> e) & 1u) && g < a.G) sv[g] = after[e];
+    }
+    for (uint32_t i = t; i < m; i += kT) {
+        if (a.trace) a.trace[c0 + i] = tr[i];
+        if (a.trace_before) a.trace_before[c0 + i] = trb[i];
+    }
+    if (c + 1 == a.C) {
+        lds_sync();
+        for (uint32_t g = t; g < a.G; g += kT)
+            if (su[g]) a.state[g] = sv[g];
+    }
+}
+
+// Events per thread of the one-launch path for E events and G groups (a
+// chunk is one sub-tile of kT times that many events), or 0 when the chunks
+// would be too many or their table of maps too large for it.
+uint32_t one_e(uint64_t E, uint32_t G)
+{
+    for (uint32_t e = 1; e <= 4; e *= 2) {
+        const uint64_t C = cdiv(E ? E : 1, (uint64_t)kT * e);
+        if (C <= kOneChunks && C * G <= kSmallTable) return e;
+    }
+    return 0;
+}
+
 uint32_t sub_per_chunk(uint64_t E, uint32_t G, uint32_t kSub)
 {
     uint64_t cmax = kMaxTable / (G ? G : 1);
@@ -657,7 +876,7 @@ size_t calc_ws_bytes(uint64_t n, uint32_t G)
 
 hipError_t calc_launch(const uint32_t *group, const double *est, const uint32_t *obs, uint32_t n,
                        double alpha, uint32_t G, double *state, double *trace, double *trace_before,
-                       void *ws, hipStream_t s, uint32_t *wait_status)
+                       void *ws, hipStream_t s, WaitCfg wait)
 {
     if (n == 0) return hipSuccess;
     if (G == 0 || G > kG) return hipErrorInvalidValue;
@@ -669,11 +888,19 @@ hipError_t calc_launch(const uint32_t *group, const double *est, const uint32_t 
     a.G = G;
     a.alpha = alpha;
     a.oma = 1.0 - alpha;
-    // sub-tiles of 512 events when the table of chunk maps stays small (the
-    // carries are then formed in k_calc_apply), else of 2048
-    chunking(n, G, 1, a.L, a.C);
-    a.small = (uint64_t)a.C * G <= kSmallTable ? 1u : 0u;
-    if (!a.small) chunking(n, G, 4, a.L, a.C);
+    // few chunks of one sub-tile each: one launch (after the unset words);
+    // else sub-tiles of 512 events when the table of chunk maps stays small
+    // (the carries are then formed in k_calc_apply), else of 2048
+    const uint32_t one = one_e(n, G);
+    if (one) {
+        a.L = kT * one;
+        a.C = (uint32_t)cdiv(n, a.L);
+        a.small = 1;
+    } else {
+        chunking(n, G, 1, a.L, a.C);
+        a.small = (uint64_t)a.C * G <= kSmallTable ? 1u : 0u;
+        if (!a.small) chunking(n, G, 4, a.L, a.C);
+    }
     a.passes = G < 256 ? 1u : 2u;   // keys 0..G fit in 8 or 16 bits
     uint8_t *p = static_cast<uint8_t *>(ws);
     const uint64_t tb = align_up((uint64_t)a.C * G * 8, 256);
@@ -684,8 +911,20 @@ hipError_t calc_launch(const uint32_t *group, const double *est, const uint32_t 
     a.state = state;
     a.trace = trace;
     a.trace_before = trace_before;
-    a.wait_status = wait_status;
-    if (a.small) {
+    a.status = wait.status;
+    a.clear = wait.clear ? 1u : 0u;
+    a.no_wait = wait.no_wait ? 1u : 0u;
+    if (one) {
+        // one sub-tile per chunk: the words the chunks publish are unset
+        // first, then one launch does the rest
+        const uint32_t nw = (uint32_t)(tb / 8 + (uint64_t)a.C * G);
+        const uint32_t fb = (uint32_t)(cdiv(nw, 256) < 256 ? cdiv(nw, 256) : 256);
+        hipLaunchKernelGGL(k_calc_unset, dim3(fb), dim3(256), 0, s, reinterpret_cast<uint64_t *>(a.aggA), nw,
+                           a.clear ? a.status : nullptr);
+        if (one == 1) hipLaunchKernelGGL(k_calc_one<1>, dim3(a.C), dim3(kT), 0, s, a);
+        else if (one == 2) hipLaunchKernelGGL(k_calc_one<2>, dim3(a.C), dim3(kT), 0, s, a);
+        else hipLaunchKernelGGL(k_calc_one<4>, dim3(a.C), dim3(kT), 0, s, a);
+    } else if (a.small) {
         hipLaunchKernelGGL(k_calc_agg<1>, dim3(a.C), dim3(kT), 0, s, a);
         hipLaunchKernelGGL(k_calc_apply<1>, dim3(a.C), dim3(kT), 0, s, a);
     } else {

@@ -280,8 +280,7 @@ hipError_t cal_launch(const uint32_t *group, const double *est, const uint32_t *
     }
     if (n == 0) return hipSuccess;
     if (G <= kCalGroupsLds)
-        return calc_launch(group, est, obs, n, alpha, G, state, trace, trace_before, ws, s,
-                           wait.clear ? wait.status : nullptr);
+        return calc_launch(group, est, obs, n, alpha, G, state, trace, trace_before, ws, s, wait);
     const uint32_t T = (uint32_t)cdiv(n, kTile);
     const uint32_t kb = bits_for(G);
     uint8_t *p = static_cast<uint8_t *>(ws);

@@ -158,11 +158,11 @@ hipError_t am_partition(const SortInput &in, uint32_t *run_pos, uint32_t *run_st
 // Up to kCalGroupsLds groups: chunked scan without a global partition.
 constexpr uint32_t kCalGroupsLds = 4096;
 size_t calc_ws_bytes(uint64_t n, uint32_t n_groups);
-// wait_status (may be NULL): zeroed by the first kernel (no waits here).
+// wait.status (may be NULL): zeroed by the first kernel when wait.clear, set
+// when a chunk's wait for the maps of the chunks before it runs out.
 hipError_t calc_launch(const uint32_t *group, const double *est, const uint32_t *obs, uint32_t n,
                        double alpha, uint32_t n_groups, double *state, double *trace,
-                       double *trace_before, void *ws, hipStream_t s,
-                       uint32_t *wait_status = nullptr);
+                       double *trace_before, void *ws, hipStream_t s, WaitCfg wait = {});
 size_t cal_ws_bytes(uint64_t n, uint32_t n_groups);
 hipError_t cal_launch(const uint32_t *group, const double *est, const uint32_t *obs,
                       uint32_t n, double alpha, uint32_t n_groups, double *state,

@@ -62,7 +62,14 @@ def test_drift_events(ds, oracle, alpha):
                                  # one or two LDS sort passes, chunked or partitioned
                                  (12000, 255), (12000, 256), (50000, 4096), (50000, 4097),
                                  # several 4096-event sub-tiles per chunk, ragged tail
-                                 (1310720 + 777, 4096), (700001, 1000)])
+                                 (1310720 + 777, 4096), (700001, 1000),
+                                 # one launch: 4096 groups over four chunks, two LDS passes
+                                 # over chunks of 1024 events, 64 chunks of 2048; one chunk
+                                 # more takes two launches
+                                 (2048, 4096), (32773, 256), (131072, 128), (131073, 128),
+                                 # two launches: 512 chunks (more blocks than are resident
+                                 # at once), full and ragged; chunks of two sub-tiles
+                                 (262144, 32), (262143, 32), (262145, 1)])
 def test_shapes(ds, oracle, E, G):
     rng = np.random.default_rng(E + G)
     g = rng.integers(0, G, E).astype(np.uint32)

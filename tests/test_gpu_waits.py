@@ -4,8 +4,9 @@ The flag DS_NO_WAIT makes every look-back wait give up at once, as if its
 spin limit had been reached, while every kernel still runs to its end (no
 wait at all takes place). The tests check what the header promises:
   - a give-up in the radix passes, in the sample sort's bucket placement of
-    Priority/Weighted, or in the calibration partition sets the workspace's
-    status word, and DS_VALIDATE turns it into DS_ERR_WAIT;
+    Priority/Weighted, in the calibration partition or in the one-launch
+    calibration of small tables sets the workspace's status word, and
+    DS_VALIDATE turns it into DS_ERR_WAIT;
   - a give-up in a sample-sort scatter sends the sort to its single-workgroup
     path, whose results are exact;
   - the next call on the same workspace clears the word again.
@@ -105,8 +106,36 @@ def test_calibration_partition_give_up_is_reported(ds, oracle):
     want, _ = oracle.calibrate(grp, est, obs, 0.1, np.ones(G), False)
     got = host(st)
     assert np.all(np.abs(got - want) <= 1e-12 * np.abs(want))
-    # the chunked path (no waits) clears a stale word too
+    # the chunked path of large tables (no waits) clears a stale word too
     ws[ds.WS_STATUS_OFFSET] = 1
-    st = torch.ones(64, dtype=torch.float64, device="cuda")
-    ds.calibrate(dev(grp % 64), dev(est), dev(obs), 0.1, st, trace=False, ws=ws, no_wait=True)
+    st = torch.ones(4096, dtype=torch.float64, device="cuda")
+    ds.calibrate(dev(grp % 4096), dev(est), dev(obs), 0.1, st, trace=False, ws=ws, no_wait=True)
     assert ds.wait_status(ws) == 0
+
+
+def test_calibration_one_launch_give_up_is_reported(ds, oracle):
+    # 79 chunks of 512 events over 64 groups: one launch, in which each chunk
+    # waits for the maps of the chunks before it
+    n, G = 40000, 64
+    rng = np.random.default_rng(5)
+    grp = rng.integers(0, G, n).astype(np.uint32)
+    est = rng.uniform(10.0, 500.0, n)
+    obs = rng.integers(1, 800, n).astype(np.uint32)
+    print("waits: calibration in one launch n=%d G=%d" % (n, G), flush=True)
+    ws = ds.workspace(ds.OP_CALIBRATE, n, G)
+    st = torch.ones(G, dtype=torch.float64, device="cuda")
+    with pytest.raises(ds.DriftSchedError) as e:
+        ds.calibrate(dev(grp), dev(est), dev(obs), 0.1, st, ws=ws, validate=True, no_wait=True)
+    assert e.value.status == ds.ERR_WAIT
+    st = torch.ones(G, dtype=torch.float64, device="cuda")
+    _, tr = ds.calibrate(dev(grp), dev(est), dev(obs), 0.1, st, ws=ws, validate=True)
+    assert ds.wait_status(ws) == 0
+    want, w_tr = oracle.calibrate(grp, est, obs, 0.1, np.ones(G))
+    assert np.all(np.abs(host(st) - want) <= 1e-12 * np.abs(want))
+    assert np.all(np.abs(host(tr) - w_tr) <= 1e-12 * np.abs(w_tr))
+    # a single chunk waits for nothing
+    st = torch.ones(G, dtype=torch.float64, device="cuda")
+    ds.calibrate(dev(grp[:500]), dev(est[:500]), dev(obs[:500]), 0.1, st, ws=ws, validate=True,
+                 no_wait=True)
+    want, _ = oracle.calibrate(grp[:500], est[:500], obs[:500], 0.1, np.ones(G), False)
+    assert np.all(np.abs(host(st) - want) <= 1e-12 * np.abs(want))
