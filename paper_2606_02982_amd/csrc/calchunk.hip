@@ -66,13 +66,20 @@ struct CalArgs {
     uint32_t *status;        // the call's wait status word, or NULL: set by a wait that runs out
     uint32_t clear;          // the call's first kernel zeroes *status
     uint32_t no_wait;        // every wait gives up at once (a diagnostic of the error path)
+    // large tables with traces: each event's map from its chunk's start to
+    // just before it, x -> (1 - alpha)^xk x + xb, in event order; pw[j][d] =
+    // (1 - alpha)^(d 256^j)
+    double *xb;
+    uint32_t *xk;
+    double *pw;
 };
 
 // A composed affine map: x -> a x + b, f = a segment starts inside,
-// u = some usable event inside.
+// u = some usable event inside, k = how many (a = (1 - alpha)^k).
 struct Map {
     uint32_t f, u;
     double a, b;
+    uint32_t k;
 };
 
 // x then y
@@ -85,6 +92,7 @@ __device__ __forceinline__ Map combine(const Map &x, const Map &y)
     r.a = y.a * x.a;
     const double t = y.a * x.b;
     r.b = t + y.b;
+    r.k = x.k + y.k;
     return r;
 }
 
@@ -109,6 +117,7 @@ __device__ __forceinline__ Map shfl_up_map(const Map &m, int d)
     r.u = (uint32_t)__shfl_up((int)m.u, d, 64);
     r.a = shfl_up_d(m.a, d);
     r.b = shfl_up_d(m.b, d);
+    r.k = (uint32_t)__shfl_up((int)m.k, d, 64);
     return r;
 }
 
@@ -324,6 +333,7 @@ __device__ void load_sort_scan(const CalArgs &a, const Raw<kE> &raw, uint32_t m,
             mp.u = out.ok[e];
             mp.a = out.ok[e] ? a.oma : 1.0;
             mp.b = out.ok[e] ? out.b[e] : 0.0;
+            mp.k = out.ok[e];
             agg = (e == 0) ? mp : combine(agg, mp);
         }
     }
@@ -340,17 +350,22 @@ __device__ void load_sort_scan(const CalArgs &a, const Raw<kE> &raw, uint32_t m,
     out.excl = ex;
 }
 
-template <int kE>
+// kEv: each event's map from the chunk's start to just before it is
+// written as well (xb, xk), so that the updates need no second sort.
+template <int kE, bool kEv>
 __global__ __launch_bounds__(kT) void k_calc_agg(CalArgs a)
 {
     constexpr uint32_t kSub = kT * kE;
+    static_assert(!kEv || kSub <= kW * 256u, "the per-event counts are staged in sh.wcnt");
     __shared__ SubShared<kE> sh;
     __shared__ double sA[kG], sB[kG];   // the chunk's map per group so far (A < 0: none)
+    __shared__ uint32_t sK[kEv ? kG : 1];   // its count of usable events
     const uint32_t t = threadIdx.x, c = blockIdx.x;
     if (a.clear && a.status && c == 0 && t == 0) *a.status = 0;
     for (uint32_t g = t; g < a.G; g += kT) {
         sA[g] = -1.0;
         sB[g] = 0.0;
+        if constexpr (kEv) sK[g] = 0;
         if (a.small && c == 0) a.s0[g] = a.state[g];
     }
     const uint64_t c0 = (uint64_t)c * a.L;
@@ -363,6 +378,48 @@ __global__ __launch_bounds__(kT) void k_calc_agg(CalArgs a)
         fetch<kE>(a, s0, c1, m, raw, next);
         Sub<kE> sub;
         load_sort_scan<kE>(a, raw, m, sh, sub);   // (its first barrier orders the sA/sB writes)
+        if constexpr (kEv) {
+            // each event's map from the chunk's start: the chunk's map of
+            // its group before this sub-tile, then the group's events of
+            // this sub-tile before it; staged by slot, then written in
+            // event order
+            double *stB = sh.b;                  // read into sub by now
+            uint32_t *stK = &sh.wcnt[0][0];      // free after the sort
+            Map pre = sub.excl;
+#pragma unroll
+            for (int e = 0; e < kE; e++) {
+                const uint32_t i = t * kE + (uint32_t)e;
+                if (i >= m) break;
+                if (sub.flag[e]) pre = Map{0u, 0u, 1.0, 0.0, 0u};
+                const uint32_t g = sub.key[e];
+                double xb = pre.u ? pre.b : 0.0;
+                uint32_t xk = pre.k;
+                if (g < a.G && sA[g] >= 0.0) {
+                    const double pb = sB[g];
+                    if (pre.u) {
+                        const double tt = pre.a * pb;
+                        xb = tt + pre.b;
+                    } else {
+                        xb = pb;
+                    }
+                    xk += sK[g];
+                }
+                stB[sub.slot[e]] = xb;
+                stK[sub.slot[e]] = xk;
+                Map mp;
+                mp.f = sub.flag[e];
+                mp.u = sub.ok[e];
+                mp.a = sub.ok[e] ? a.oma : 1.0;
+                mp.b = sub.ok[e] ? sub.b[e] : 0.0;
+                mp.k = sub.ok[e];
+                pre = mp.f ? mp : combine(pre, mp);
+            }
+            lds_sync();   // every read of sA, sB, sK above precedes the updates below
+            for (uint32_t i = t; i < m; i += kT) {
+                a.xb[s0 + i] = stB[i];
+                a.xk[s0 + i] = stK[i];
+            }
+        }
         // the segment of each group in this sub-tile, composed into the
         // group's map at the segment's last position (one thread per group)
         Map run = sub.excl;
@@ -375,6 +432,7 @@ __global__ __launch_bounds__(kT) void k_calc_agg(CalArgs a)
             mp.u = sub.ok[e];
             mp.a = sub.ok[e] ? a.oma : 1.0;
             mp.b = sub.ok[e] ? sub.b[e] : 0.0;
+            mp.k = sub.ok[e];
             run = mp.f ? mp : combine(run, mp);
             const bool last = (i + 1 == m) || (e + 1 < kE ? sub.flag[e + 1] != 0u : sh.key[i + 1] != sh.key[i]);
             const uint32_t g = sub.key[e];
@@ -383,11 +441,13 @@ __global__ __launch_bounds__(kT) void k_calc_agg(CalArgs a)
                 if (pa < 0.0) {
                     sA[g] = run.a;
                     sB[g] = run.b;
+                    if constexpr (kEv) sK[g] = run.k;
                 } else {
                     // the chunk so far, then this segment
                     sA[g] = run.a * pa;
                     const double tt = run.a * sB[g];
                     sB[g] = tt + run.b;
+                    if constexpr (kEv) sK[g] += run.k;
                 }
             }
         }
@@ -410,6 +470,11 @@ __global__ __launch_bounds__(64 * kScanW) void k_calc_scan(CalArgs a)
 {
     __shared__ double sA[kScanW][64], sB[kScanW][64];
     __shared__ uint32_t sU[kScanW][64];
+    // the powers of 1 - alpha for the per-event maps: digit d of place j
+    if (a.pw && blockIdx.x == 0) {
+        const uint32_t j = threadIdx.x >> 8, d = threadIdx.x & 255u;
+        a.pw[threadIdx.x] = pow(a.oma, (double)d * (double)(1u << (8 * j)));
+    }
     const uint32_t w = threadIdx.x >> 6;
     const int lane = lane_id();
     const uint32_t g = blockIdx.x * 64u + (uint32_t)lane;
@@ -474,6 +539,72 @@ __global__ __launch_bounds__(64 * kScanW) void k_calc_scan(CalArgs a)
     // the wave holding the last chunk writes the factor after all events
     // (a group without usable events keeps its factor untouched)
     if (ce == a.C && cb < ce && touched) a.state[g] = v;
+}
+
+// Large tables: every event's factor before it from its chunk's carry and
+// its map from the chunk's start, then the exact update (Eq. 5 with the
+// ratio of Eq. 6) for a usable event. Blocks of 1024 events, which lie in
+// one chunk (chunks are a multiple of 2048 events).
+constexpr uint32_t kEvR = 4;
+static_assert(64 * 4 * kEvR == 1024, "");
+__global__ __launch_bounds__(256) void k_calc_ev(CalArgs a)
+{
+    __shared__ double pw[1024];
+    const uint32_t t = threadIdx.x;
+    for (uint32_t i = t; i < 1024; i += 256) pw[i] = a.pw[i];
+    const uint32_t e0 = blockIdx.x * 1024u;
+    const uint64_t row = (uint64_t)(e0 / a.L) * a.G;
+    uint32_t g[kEvR], k[kEvR], o[kEvR];
+    double xb[kEvR], x[kEvR];
+#pragma unroll
+    for (uint32_t r = 0; r < kEvR; r++) {
+        const uint32_t i = e0 + r * 256u + t;
+        g[r] = a.G;
+        k[r] = 0;
+        o[r] = 0;
+        xb[r] = 0.0;
+        x[r] = 0.0;
+        if (i < a.E) {
+            g[r] = a.group[i];
+            k[r] = a.xk[i];
+            xb[r] = a.xb[i];
+            x[r] = a.est[i];
+            o[r] = a.obs[i];
+        }
+    }
+    double cv[kEvR];
+#pragma unroll
+    for (uint32_t r = 0; r < kEvR; r++) cv[r] = g[r] < a.G ? a.carry[row + g[r]] : 0.0;
+    __syncthreads();
+    const double nan = __builtin_nan("");
+#pragma unroll
+    for (uint32_t r = 0; r < kEvR; r++) {
+        const uint32_t i = e0 + r * 256u + t;
+        if (i >= a.E) break;
+        double before = nan, after = nan;
+        if (g[r] < a.G) {
+            double v = cv[r];
+            if (k[r]) {
+                // (1 - alpha)^k from its base-256 digits
+                const uint32_t kk = k[r];
+                double p = pw[kk & 255u];
+                p *= pw[256u + ((kk >> 8) & 255u)];
+                p *= pw[512u + ((kk >> 16) & 255u)];
+                p *= pw[768u + (kk >> 24)];
+                const double tt = p * v;
+                v = tt + xb[r];
+            }
+            before = v;
+            if (isfinite(x[r]) && x[r] > 0.0) {
+                const double ratio = (double)o[r] / x[r];
+                const double t1 = a.oma * v;
+                v = t1 + a.alpha * ratio;
+            }
+            after = v;
+        }
+        if (a.trace) a.trace[i] = after;
+        if (a.trace_before) a.trace_before[i] = before;
+    }
 }
 
 template <int kE>
@@ -707,6 +838,7 @@ __global__ __launch_bounds__(kT) void k_calc_one(CalArgs a)
             mp.u = sub.ok[e];
             mp.a = sub.ok[e] ? a.oma : 1.0;
             mp.b = sub.ok[e] ? sub.b[e] : 0.0;
+            mp.k = sub.ok[e];
             run = mp.f ? mp : combine(run, mp);
             const uint32_t g = sub.key[e];
             if (((lastm >> e) & 1u) && g < a.G && run.u) {
@@ -871,7 +1003,10 @@ size_t calc_ws_bytes(uint64_t n, uint32_t G)
     chunking(n, G, 1, L1, C1);
     chunking(n, G, 4, L4, C4);
     const uint64_t C = C1 > C4 ? C1 : C4;
-    return 3 * align_up(C * G * 8, 256) + align_up((uint64_t)G * 8, 256);
+    const size_t base = 3 * align_up(C * G * 8, 256) + align_up((uint64_t)G * 8, 256);
+    // the large tables' per-event maps and power tables (k_calc_ev)
+    const bool large = one_e(n, G) == 0 && (uint64_t)C1 * G > kSmallTable;
+    return large ? base + align_up(1024 * 8, 256) + align_up(n * 8, 256) + align_up(n * 4, 256) : base;
 }
 
 hipError_t calc_launch(const uint32_t *group, const double *est, const uint32_t *obs, uint32_t n,
@@ -908,6 +1043,20 @@ hipError_t calc_launch(const uint32_t *group, const double *est, const uint32_t 
     a.aggB = reinterpret_cast<double *>(p + tb);
     a.carry = reinterpret_cast<double *>(p + 2 * tb);
     a.s0 = reinterpret_cast<double *>(p + 3 * tb);
+    // per-event maps (large tables): after the other arrays, at the offsets
+    // calc_ws_bytes reserves
+    {
+        uint32_t L1, C1, L4, C4;
+        chunking(n, G, 1, L1, C1);
+        chunking(n, G, 4, L4, C4);
+        const uint64_t Cm = C1 > C4 ? C1 : C4;
+        uint8_t *q = p + 3 * align_up(Cm * G * 8, 256) + align_up((uint64_t)G * 8, 256);
+        a.pw = reinterpret_cast<double *>(q);
+        q += align_up(1024 * 8, 256);
+        a.xb = reinterpret_cast<double *>(q);
+        q += align_up((uint64_t)n * 8, 256);
+        a.xk = reinterpret_cast<uint32_t *>(q);
+    }
     a.state = state;
     a.trace = trace;
     a.trace_before = trace_before;
@@ -925,12 +1074,17 @@ hipError_t calc_launch(const uint32_t *group, const double *est, const uint32_t 
         else if (one == 2) hipLaunchKernelGGL(k_calc_one<2>, dim3(a.C), dim3(kT), 0, s, a);
         else hipLaunchKernelGGL(k_calc_one<4>, dim3(a.C), dim3(kT), 0, s, a);
     } else if (a.small) {
-        hipLaunchKernelGGL(k_calc_agg<1>, dim3(a.C), dim3(kT), 0, s, a);
+        hipLaunchKernelGGL((k_calc_agg<1, false>), dim3(a.C), dim3(kT), 0, s, a);
         hipLaunchKernelGGL(k_calc_apply<1>, dim3(a.C), dim3(kT), 0, s, a);
-    } else {
-        hipLaunchKernelGGL(k_calc_agg<4>, dim3(a.C), dim3(kT), 0, s, a);
+    } else if (!trace && !trace_before) {
+        // the final factors alone
+        a.pw = nullptr;
+        hipLaunchKernelGGL((k_calc_agg<4, false>), dim3(a.C), dim3(kT), 0, s, a);
         hipLaunchKernelGGL(k_calc_scan, dim3((G + 63) / 64), dim3(64 * kScanW), 0, s, a);
-        hipLaunchKernelGGL(k_calc_apply<4>, dim3(a.C), dim3(kT), 0, s, a);
+    } else {
+        hipLaunchKernelGGL((k_calc_agg<4, true>), dim3(a.C), dim3(kT), 0, s, a);
+        hipLaunchKernelGGL(k_calc_scan, dim3((G + 63) / 64), dim3(64 * kScanW), 0, s, a);
+        hipLaunchKernelGGL(k_calc_ev, dim3((uint32_t)cdiv(n, 1024)), dim3(256), 0, s, a);
     }
     return hipGetLastError();
 }
