@@ -5,20 +5,27 @@
 // The events, in completion order, are cut into C chunks of L events (L a
 // multiple of the sub-tile). With M(c, g) the composition of the affine maps
 // x -> (1 - alpha) x + alpha r of group g's events in chunk c (in order):
-//   k_calc_agg    per chunk (one block): each sub-tile (512 or 2048 events) is sorted
-//                 by group in LDS (stable LSD passes, wave ballots), scanned
-//                 as a segmented scan of maps, and each group's part is
-//                 composed into that group's map in LDS; the chunk writes
-//                 M(c, g) for every group (or "no usable event").
+//   k_calc_agg    per chunk (one block): each sub-tile (512 or 4096 events) is
+//                 sorted by group in LDS (stable LSD passes, wave ballots),
+//                 scanned as a segmented scan of maps, and each group's part
+//                 is composed into that group's map in LDS; the chunk writes
+//                 M(c, g) for every group (or "no usable event"). For the
+//                 large tables it also writes each event's map from the
+//                 chunk's start (through the event when only the trace is
+//                 wanted, else to just before it), as a count k of usable
+//                 events (its slope is (1 - alpha)^k) and an offset.
 //   k_calc_scan   per 64 groups (one block, lane = group): the group's
 //                 factor before chunk c is M(c-1, g) o ... o M(0, g) applied
 //                 to its initial factor (sixteen stretches of chunks composed
 //                 by sixteen waves, then chained in order); writes those
-//                 carries and the final factor.
-//   k_calc_apply  per chunk: the same sub-tile sort and scan; every event
-//                 then runs the exact update t1 = (1 - alpha) c, t2 =
-//                 alpha r, c = t1 + t2 from its carried factor, in order, and
-//                 the traces are staged in LDS and written in event order.
+//                 carries and the final factor, and the powers of 1 - alpha.
+//   k_calc_ev     large tables, per event: its chunk's carry through its
+//                 map; without the event, followed by the exact update t1 =
+//                 (1 - alpha) c, t2 = alpha r, c = t1 + t2.
+//   k_calc_apply  small tables, per chunk: the same sub-tile sort and scan;
+//                 every event then runs the exact update from its carried
+//                 factor, in order, and the traces are staged in LDS and
+//                 written in event order.
 // When the table of chunk maps is small (C x G <= kSmallTable), k_calc_scan
 // is left out: each k_calc_apply block applies the maps of the chunks before
 // it to the initial factors itself (k_calc_agg keeps a copy of them), and
@@ -39,14 +46,15 @@ namespace {
 
 constexpr int kT = 512;                  // threads per block
 // events per thread per sub-tile (kE) is a template parameter: 1 for the
-// small tables (more, shorter blocks), 4 otherwise; kSub = kT * kE events
-// per sub-tile
+// small tables (more, shorter blocks; 1, 2 or 4 in one launch), kBigE for
+// the large ones; kSub = kT * kE events per sub-tile
 constexpr int kW = kT / 64;
 constexpr uint32_t kG = kCalGroupsLds;   // groups held in LDS
 constexpr uint32_t kMaxTable = 1u << 20; // C x G entries at most (C >= 1)
 constexpr uint32_t kMaxChunks = 512;
 constexpr uint32_t kSmallTable = 16384;  // C x G up to which the carries are formed in k_calc_apply
 constexpr uint32_t kCarryR = 4;          // chunk maps per thread held in registers for the carry
+constexpr uint32_t kBigE = 8;            // events per thread per sub-tile of the large tables
 
 struct CalArgs {
     const uint32_t *group;
@@ -57,6 +65,7 @@ struct CalArgs {
     uint32_t C;              // chunks
     uint32_t L;              // events per chunk
     uint32_t passes;         // 8-bit LSD passes over the group key (key < 2^(8 passes))
+    uint32_t keybits;        // bits of the largest key (G, for an event outside the groups)
     double *aggA, *aggB;     // [C][G]: M(c, g) = x -> A x + B; A < 0: no usable event
     double *carry;           // [C][G]: factor of g before chunk c
     double *s0;              // [G] the initial factors (small tables: no k_calc_scan)
@@ -69,9 +78,11 @@ struct CalArgs {
     // large tables with traces: each event's map from its chunk's start to
     // just before it, x -> (1 - alpha)^xk x + xb, in event order; pw[j][d] =
     // (1 - alpha)^(d 256^j)
+    // incl: the maps include the event itself (only the trace is wanted)
     double *xb;
     uint32_t *xk;
     double *pw;
+    uint32_t incl;
 };
 
 // A composed affine map: x -> a x + b, f = a segment starts inside,
@@ -248,6 +259,7 @@ __device__ void load_sort_scan(const CalArgs &a, const Raw<kE> &raw, uint32_t m,
             uint64_t peers = __ballot(v);
 #pragma unroll
             for (int bb = 0; bb < 8; bb++) {
+                if (8 * p + bb >= a.keybits) break;   // a bit no key has
                 const bool bit = (dg >> bb) & 1u;
                 const uint64_t mk = __ballot(bit);
                 peers &= bit ? mk : ~mk;
@@ -356,10 +368,10 @@ template <int kE, bool kEv>
 __global__ __launch_bounds__(kT) void k_calc_agg(CalArgs a)
 {
     constexpr uint32_t kSub = kT * kE;
-    static_assert(!kEv || kSub <= kW * 256u, "the per-event counts are staged in sh.wcnt");
     __shared__ SubShared<kE> sh;
     __shared__ double sA[kG], sB[kG];   // the chunk's map per group so far (A < 0: none)
     __shared__ uint32_t sK[kEv ? kG : 1];   // its count of usable events
+    __shared__ uint32_t stK[kEv ? kSub : 1];   // per-event counts staged by slot
     const uint32_t t = threadIdx.x, c = blockIdx.x;
     if (a.clear && a.status && c == 0 && t == 0) *a.status = 0;
     for (uint32_t g = t; g < a.G; g += kT) {
@@ -384,13 +396,20 @@ __global__ __launch_bounds__(kT) void k_calc_agg(CalArgs a)
             // this sub-tile before it; staged by slot, then written in
             // event order
             double *stB = sh.b;                  // read into sub by now
-            uint32_t *stK = &sh.wcnt[0][0];      // free after the sort
             Map pre = sub.excl;
 #pragma unroll
             for (int e = 0; e < kE; e++) {
                 const uint32_t i = t * kE + (uint32_t)e;
                 if (i >= m) break;
                 if (sub.flag[e]) pre = Map{0u, 0u, 1.0, 0.0, 0u};
+                Map mp;
+                mp.f = sub.flag[e];
+                mp.u = sub.ok[e];
+                mp.a = sub.ok[e] ? a.oma : 1.0;
+                mp.b = sub.ok[e] ? sub.b[e] : 0.0;
+                mp.k = sub.ok[e];
+                const Map inc = combine(pre, mp);   // the group's events through this one
+                if (a.incl) pre = inc;
                 const uint32_t g = sub.key[e];
                 double xb = pre.u ? pre.b : 0.0;
                 uint32_t xk = pre.k;
@@ -406,13 +425,7 @@ __global__ __launch_bounds__(kT) void k_calc_agg(CalArgs a)
                 }
                 stB[sub.slot[e]] = xb;
                 stK[sub.slot[e]] = xk;
-                Map mp;
-                mp.f = sub.flag[e];
-                mp.u = sub.ok[e];
-                mp.a = sub.ok[e] ? a.oma : 1.0;
-                mp.b = sub.ok[e] ? sub.b[e] : 0.0;
-                mp.k = sub.ok[e];
-                pre = mp.f ? mp : combine(pre, mp);
+                pre = inc;
             }
             lds_sync();   // every read of sA, sB, sK above precedes the updates below
             for (uint32_t i = t; i < m; i += kT) {
@@ -541,17 +554,18 @@ __global__ __launch_bounds__(64 * kScanW) void k_calc_scan(CalArgs a)
     if (ce == a.C && cb < ce && touched) a.state[g] = v;
 }
 
-// Large tables: every event's factor before it from its chunk's carry and
-// its map from the chunk's start, then the exact update (Eq. 5 with the
-// ratio of Eq. 6) for a usable event. Blocks of 1024 events, which lie in
-// one chunk (chunks are a multiple of 2048 events).
+// Large tables: every event's factor from its chunk's carry and its map
+// from the chunk's start. With incl (the trace alone) the map includes the
+// event and gives its trace; otherwise it gives the factor before the
+// event, followed by the exact update (Eq. 5 with the ratio of Eq. 6) for a
+// usable event. Blocks of 1024 events, which lie in one chunk (chunks are a
+// multiple of 2048 events).
 constexpr uint32_t kEvR = 4;
-static_assert(64 * 4 * kEvR == 1024, "");
+static_assert(256 * kEvR == 1024, "");
 __global__ __launch_bounds__(256) void k_calc_ev(CalArgs a)
 {
     __shared__ double pw[1024];
     const uint32_t t = threadIdx.x;
-    for (uint32_t i = t; i < 1024; i += 256) pw[i] = a.pw[i];
     const uint32_t e0 = blockIdx.x * 1024u;
     const uint64_t row = (uint64_t)(e0 / a.L) * a.G;
     uint32_t g[kEvR], k[kEvR], o[kEvR];
@@ -568,13 +582,20 @@ __global__ __launch_bounds__(256) void k_calc_ev(CalArgs a)
             g[r] = a.group[i];
             k[r] = a.xk[i];
             xb[r] = a.xb[i];
-            x[r] = a.est[i];
-            o[r] = a.obs[i];
+            if (!a.incl) {
+                x[r] = a.est[i];
+                o[r] = a.obs[i];
+            }
         }
     }
+    double pv[4];
+#pragma unroll
+    for (uint32_t r = 0; r < 4; r++) pv[r] = a.pw[r * 256u + t];
     double cv[kEvR];
 #pragma unroll
     for (uint32_t r = 0; r < kEvR; r++) cv[r] = g[r] < a.G ? a.carry[row + g[r]] : 0.0;
+#pragma unroll
+    for (uint32_t r = 0; r < 4; r++) pw[r * 256u + t] = pv[r];
     __syncthreads();
     const double nan = __builtin_nan("");
 #pragma unroll
@@ -595,7 +616,7 @@ __global__ __launch_bounds__(256) void k_calc_ev(CalArgs a)
                 v = tt + xb[r];
             }
             before = v;
-            if (isfinite(x[r]) && x[r] > 0.0) {
+            if (!a.incl && isfinite(x[r]) && x[r] > 0.0) {
                 const double ratio = (double)o[r] / x[r];
                 const double t1 = a.oma * v;
                 v = t1 + a.alpha * ratio;
@@ -1001,7 +1022,7 @@ size_t calc_ws_bytes(uint64_t n, uint32_t G)
     // the larger of the two chunkings' tables
     uint32_t L1, C1, L4, C4;
     chunking(n, G, 1, L1, C1);
-    chunking(n, G, 4, L4, C4);
+    chunking(n, G, kBigE, L4, C4);
     const uint64_t C = C1 > C4 ? C1 : C4;
     const size_t base = 3 * align_up(C * G * 8, 256) + align_up((uint64_t)G * 8, 256);
     // the large tables' per-event maps and power tables (k_calc_ev)
@@ -1025,7 +1046,7 @@ hipError_t calc_launch(const uint32_t *group, const double *est, const uint32_t 
     a.oma = 1.0 - alpha;
     // few chunks of one sub-tile each: one launch (after the unset words);
     // else sub-tiles of 512 events when the table of chunk maps stays small
-    // (the carries are then formed in k_calc_apply), else of 2048
+    // (the carries are then formed in k_calc_apply), else of 4096
     const uint32_t one = one_e(n, G);
     if (one) {
         a.L = kT * one;
@@ -1034,9 +1055,11 @@ hipError_t calc_launch(const uint32_t *group, const double *est, const uint32_t 
     } else {
         chunking(n, G, 1, a.L, a.C);
         a.small = (uint64_t)a.C * G <= kSmallTable ? 1u : 0u;
-        if (!a.small) chunking(n, G, 4, a.L, a.C);
+        if (!a.small) chunking(n, G, kBigE, a.L, a.C);
     }
     a.passes = G < 256 ? 1u : 2u;   // keys 0..G fit in 8 or 16 bits
+    a.keybits = 1;
+    while ((1u << a.keybits) <= G) a.keybits++;
     uint8_t *p = static_cast<uint8_t *>(ws);
     const uint64_t tb = align_up((uint64_t)a.C * G * 8, 256);
     a.aggA = reinterpret_cast<double *>(p);
@@ -1048,7 +1071,7 @@ hipError_t calc_launch(const uint32_t *group, const double *est, const uint32_t 
     {
         uint32_t L1, C1, L4, C4;
         chunking(n, G, 1, L1, C1);
-        chunking(n, G, 4, L4, C4);
+        chunking(n, G, kBigE, L4, C4);
         const uint64_t Cm = C1 > C4 ? C1 : C4;
         uint8_t *q = p + 3 * align_up(Cm * G * 8, 256) + align_up((uint64_t)G * 8, 256);
         a.pw = reinterpret_cast<double *>(q);
@@ -1063,6 +1086,7 @@ hipError_t calc_launch(const uint32_t *group, const double *est, const uint32_t 
     a.status = wait.status;
     a.clear = wait.clear ? 1u : 0u;
     a.no_wait = wait.no_wait ? 1u : 0u;
+    a.incl = trace_before ? 0u : 1u;
     if (one) {
         // one sub-tile per chunk: the words the chunks publish are unset
         // first, then one launch does the rest
@@ -1079,10 +1103,10 @@ hipError_t calc_launch(const uint32_t *group, const double *est, const uint32_t 
     } else if (!trace && !trace_before) {
         // the final factors alone
         a.pw = nullptr;
-        hipLaunchKernelGGL((k_calc_agg<4, false>), dim3(a.C), dim3(kT), 0, s, a);
+        hipLaunchKernelGGL((k_calc_agg<kBigE, false>), dim3(a.C), dim3(kT), 0, s, a);
         hipLaunchKernelGGL(k_calc_scan, dim3((G + 63) / 64), dim3(64 * kScanW), 0, s, a);
     } else {
-        hipLaunchKernelGGL((k_calc_agg<4, true>), dim3(a.C), dim3(kT), 0, s, a);
+        hipLaunchKernelGGL((k_calc_agg<kBigE, true>), dim3(a.C), dim3(kT), 0, s, a);
         hipLaunchKernelGGL(k_calc_scan, dim3((G + 63) / 64), dim3(64 * kScanW), 0, s, a);
         hipLaunchKernelGGL(k_calc_ev, dim3((uint32_t)cdiv(n, 1024)), dim3(256), 0, s, a);
     }
