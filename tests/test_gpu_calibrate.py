@@ -135,3 +135,34 @@ def test_validate_flag(ds):
         ds.calibrate(dev(np.array([0, 2], np.uint32)), dev(np.ones(2)), dev(np.ones(2, np.uint32)),
                      0.1, st, validate=True)
     assert e.value.status == -5
+
+
+# one launch; two launches (small table, more chunks than one launch takes);
+# large table
+@pytest.mark.parametrize("E,G", [(20000, 17), (200000, 32), (300001, 1000)])
+@pytest.mark.parametrize("outs", ["state", "before", "both"])
+def test_outputs(ds, oracle, E, G, outs):
+    # the final factors alone, the factors before each event alone, or both
+    # traces: each path forms what is asked, and only that
+    rng = np.random.default_rng(3 * E + G)
+    g = rng.integers(0, G, E).astype(np.uint32)
+    est = rng.uniform(1, 500, E)
+    est[rng.random(E) < 0.05] = 0.0
+    obs = rng.integers(0, 1000, E).astype(np.uint32)
+    st0 = rng.uniform(0.5, 1.5, G)
+    w_st, w_tr, w_before = oracle.calibrate(g, est, obs, 0.1, st0, with_before=True)
+    st = dev(st0.copy())
+    res = ds.calibrate(dev(g), dev(est), dev(obs), 0.1, st, trace=outs == "both",
+                       trace_before=outs != "state")
+    ok, worst = rel_close(host(st), w_st, RTOL)
+    assert ok, "state worst relative difference %.3g" % worst
+    if outs == "state":
+        assert res[1] is None
+        return
+    ok, worst = rel_close(host(res[2]), w_before, RTOL)
+    assert ok, "trace_before worst relative difference %.3g" % worst
+    if outs == "both":
+        ok, worst = rel_close(host(res[1]), w_tr, RTOL)
+        assert ok, "trace worst relative difference %.3g" % worst
+    else:
+        assert res[1] is None
