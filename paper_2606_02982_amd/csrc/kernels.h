@@ -130,10 +130,25 @@ struct LsRuns {
     uint32_t *rp;
     uint32_t *cstart;
 };
+// SJF's splitter sample drawn beside the FIFO sort (draw: that call draws
+// it): its keys are the budgets of the sampled requests, with the request
+// index standing in for the FIFO position on ties, so it needs no FIFO
+// order; a later batch's Budget row (draw false) takes its splitters from
+// here. Any sorted splitters give exact results: the bucket sizes come from
+// the counts.
+struct LsSample {
+    uint64_t *raw_k;
+    uint32_t *rpart;
+    uint64_t *smp_k;
+    uint32_t *smp_j;
+    bool draw;
+};
+size_t lsort_sample_bytes(uint64_t n);               // 0 outside (kSsMaxN, kLsMaxN]
+LsSample lsort_sample_at(uint64_t n, void *p);       // the buffers at p (lsort_sample_bytes(n) bytes)
 size_t lsort_ws_bytes(uint64_t n, uint32_t nsort, uint32_t npart);   // 0 outside (kSsMaxN, kLsMaxN]
 hipError_t lsort_launch(const SortInput &in, const SortJob *jobs, uint32_t njobs, void *ws, hipStream_t s,
                         const LsCopies *fifo_in_copies = nullptr, const LsCopies *fifo_out_copies = nullptr,
-                        const LsRuns *aging_runs = nullptr);
+                        const LsRuns *aging_runs = nullptr, const LsSample *sjf = nullptr);
 
 // Aging above the sample-sort limit as a merge of the priority classes' runs
 // of the FIFO sequence (in.fifo, in.cls and the aging parameters set;

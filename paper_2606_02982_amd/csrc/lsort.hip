@@ -76,6 +76,8 @@ struct LsRow {
     uint32_t *start;       // [B] first place of each bucket's region (each digit's range)
     uint32_t *tcnt;        // [tiles][B] each tile's count of each bucket, then its first slot there
     uint16_t *bid;         // [n] bucket of each position (sorts)
+    uint32_t by_req;       // the sample's keys are the budgets of the sampled requests
+                           // (request index standing in for the FIFO position)
     uint64_t *raw_k;       // [S] the sample's keys in sample order
     uint32_t *rpart;       // [kSmP][S] each part's count of samples below each sample
     uint64_t *smp_k;       // [S] the sample in order
@@ -96,6 +98,8 @@ struct LsArgs {
     uint32_t n, tiles;
     uint32_t nrows;        // rows [0, nsort) are sorts, the rest partitions
     uint32_t nsort;
+    uint32_t nsamp;        // rows that draw their splitters in this call: r[srow[0 .. nsamp)]
+    uint32_t srow[kLsMaxRows];
     WrrPlan *plan;         // Tier, smooth interleaving: the period table (built by the scan)
     uint32_t *tpos;        // its start-up positions
     LsRow r[kLsMaxRows];
@@ -232,10 +236,11 @@ __device__ __forceinline__ uint32_t blk_excl_scan(uint32_t x, uint32_t *wsum)
 
 __global__ __launch_bounds__(256) void k_ls_gather(LsArgs a)
 {
-    const LsRow &R = a.r[blockIdx.y];
+    const LsRow &R = a.r[a.srow[blockIdx.y]];
     const uint32_t s = blockIdx.x * 256u + threadIdx.x;
     if (s < R.S) {
-        R.raw_k[s] = ls_key(a, R, ls_pos(s, a.n, R.S));
+        const uint32_t j = ls_pos(s, a.n, R.S);
+        R.raw_k[s] = R.by_req ? ordered_bits(a.in.budget[j]) : ls_key(a, R, j);
     }
 }
 
@@ -254,7 +259,7 @@ __global__ __launch_bounds__(kSmT) void k_ls_sample(LsArgs a)
 {
     __shared__ uint64_t sk[kLsMaxS / kSmP];
     __shared__ uint32_t part[kSmW][64];
-    const LsRow &R = a.r[blockIdx.y];
+    const LsRow &R = a.r[a.srow[blockIdx.y]];
     const uint32_t g = blockIdx.x / kSmP, pq = blockIdx.x % kSmP;
     if (g * 64u >= R.S) return;   // a row with a smaller sample than the grid is wide
     const uint32_t t = threadIdx.x, lane = (uint32_t)lane_id(), w = t >> 6, S = R.S, n = a.n;
@@ -311,7 +316,7 @@ __global__ __launch_bounds__(kSmT) void k_ls_sample(LsArgs a)
 // Each sample at its rank (the sum of its parts' counts).
 __global__ __launch_bounds__(256) void k_ls_place(LsArgs a)
 {
-    const LsRow &R = a.r[blockIdx.y];
+    const LsRow &R = a.r[a.srow[blockIdx.y]];
     const uint32_t s = blockIdx.x * 256u + threadIdx.x, S = R.S;
     if (s >= S) return;
     uint32_t r = 0;
@@ -1063,6 +1068,29 @@ LsLayout ls_layout(uint64_t n)
 
 }  // namespace
 
+size_t lsort_sample_bytes(uint64_t n)
+{
+    if (n <= kSsMaxN || n > kLsMaxN) return 0;
+    const LsLayout l = ls_layout(n);
+    return 2 * align_up(l.S * 8, 256) + align_up(l.S * 4, 256) + align_up(kSmP * l.S * 4, 256);
+}
+
+LsSample lsort_sample_at(uint64_t n, void *p)
+{
+    const LsLayout l = ls_layout(n > kSsMaxN ? n : kSsMaxN + 1);
+    uint8_t *q = static_cast<uint8_t *>(p);
+    LsSample y;
+    y.raw_k = reinterpret_cast<uint64_t *>(q);
+    q += align_up(l.S * 8, 256);
+    y.smp_k = reinterpret_cast<uint64_t *>(q);
+    q += align_up(l.S * 8, 256);
+    y.smp_j = reinterpret_cast<uint32_t *>(q);
+    q += align_up(l.S * 4, 256);
+    y.rpart = reinterpret_cast<uint32_t *>(q);
+    y.draw = true;
+    return y;
+}
+
 size_t lsort_ws_bytes(uint64_t n, uint32_t nsort, uint32_t npart)
 {
     if (n <= kSsMaxN || n > kLsMaxN) return 0;
@@ -1078,7 +1106,8 @@ size_t lsort_ws_bytes(uint64_t n, uint32_t nsort, uint32_t npart)
 }
 
 hipError_t lsort_launch(const SortInput &in, const SortJob *jobs, uint32_t njobs, void *ws, hipStream_t s,
-                        const LsCopies *fifo_in_copies, const LsCopies *fifo_out_copies, const LsRuns *aging_runs)
+                        const LsCopies *fifo_in_copies, const LsCopies *fifo_out_copies, const LsRuns *aging_runs,
+                        const LsSample *sjf)
 {
     const uint64_t n = in.n;
     if (n <= kSsMaxN || n > kLsMaxN || njobs == 0 || njobs > kLsMaxRows) return hipErrorInvalidValue;
@@ -1132,6 +1161,13 @@ hipError_t lsort_launch(const SortInput &in, const SortJob *jobs, uint32_t njobs
             R.rpart = reinterpret_cast<uint32_t *>(take(kSmP * l.S * 4));
             R.smp_k = reinterpret_cast<uint64_t *>(take(l.S * 8));
             R.smp_j = reinterpret_cast<uint32_t *>(take(l.S * 4));
+            if (k == SortKind::Budget && sjf && !sjf->draw) {
+                // splitters drawn beside the FIFO sort
+                R.smp_k = sjf->smp_k;
+                R.smp_j = sjf->smp_j;
+            } else {
+                a.srow[a.nsamp++] = a.nrows - 1;
+            }
             R.bid = reinterpret_cast<uint16_t *>(take(n * 2));
             for (int e = 0; e < 2; e++) {
                 R.rk[e] = reinterpret_cast<uint64_t *>(take(n * 8));
@@ -1147,11 +1183,27 @@ hipError_t lsort_launch(const SortInput &in, const SortJob *jobs, uint32_t njobs
         a.plan = reinterpret_cast<WrrPlan *>(take(sizeof(WrrPlan)));
         a.tpos = reinterpret_cast<uint32_t *>(take(n * 4));
     }
+    if (sjf && sjf->draw) {
+        // a row after the others, sampled only: SJF's splitters by request
+        // index, so that the batch over the FIFO sequence skips its sampling
+        if (a.nrows >= kLsMaxRows) return hipErrorInvalidValue;
+        LsRow &R = a.r[a.nrows];
+        R.kind = SortKind::Budget;
+        R.by_req = 1;
+        R.B = l.B;
+        R.S = l.S;
+        R.hgt = l.hgt;
+        R.raw_k = sjf->raw_k;
+        R.rpart = sjf->rpart;
+        R.smp_k = sjf->smp_k;
+        R.smp_j = sjf->smp_j;
+        a.srow[a.nsamp++] = a.nrows;
+    }
     const uint32_t maxb = a.nsort ? l.B : kQ;
-    if (a.nsort) {
-        hipLaunchKernelGGL(k_ls_gather, dim3(cdiv(l.S, 256), a.nsort), dim3(256), 0, s, a);
-        hipLaunchKernelGGL(k_ls_sample, dim3(l.S / 64 * kSmP, a.nsort), dim3(kSmT), 0, s, a);
-        hipLaunchKernelGGL(k_ls_place, dim3(cdiv(l.S, 256), a.nsort), dim3(256), 0, s, a);
+    if (a.nsamp) {
+        hipLaunchKernelGGL(k_ls_gather, dim3(cdiv(l.S, 256), a.nsamp), dim3(256), 0, s, a);
+        hipLaunchKernelGGL(k_ls_sample, dim3(l.S / 64 * kSmP, a.nsamp), dim3(kSmT), 0, s, a);
+        hipLaunchKernelGGL(k_ls_place, dim3(cdiv(l.S, 256), a.nsamp), dim3(256), 0, s, a);
     }
     hipLaunchKernelGGL(k_ls_count, dim3(l.tiles, a.nrows), dim3(kTT), 0, s, a);
     hipLaunchKernelGGL(k_ls_scan, dim3(cdiv(maxb, 64), a.nrows), dim3(kScT), 0, s, a);

@@ -77,7 +77,7 @@ size_t order_ws_bytes(uint64_t n, uint32_t npolicies)
     // FIFO sequence, and the Aging runs with their merge scratch)
     const size_t lb = lsort_ws_bytes(n, 1, 2);
     const size_t ls = lb ? 2 * align_up(n * 8, 256) + align_up(n, 256) + 2 * align_up(n * 8, 256) +
-                               2 * align_up(n * 4, 256) + align_up(17 * 4, 256) + lb
+                               2 * align_up(n * 4, 256) + align_up(17 * 4, 256) + lsort_sample_bytes(n) + lb
                          : 0;
     const size_t radix = align_up(n * 4, 256) + (ls > rs ? ls : rs);
     // the larger of the two keeps the size non-decreasing in n
@@ -181,16 +181,23 @@ hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_
         }
         LsRuns runs = {rk[0], rp[0], reinterpret_cast<uint32_t *>(q)};
         q += align_up(17 * 4, 256);
+        LsSample sjf = lsort_sample_at(n, q);
+        q += lsort_sample_bytes(n);
         void *batch_ws = q;
         const bool more = a.mask & ~1u;   // policies over the FIFO sequence
         const uint32_t *fifo = a.fifo_in;
+        bool sjf_drawn = false;
         if (!fifo) {
+            // (SJF's splitters are drawn in the same launches)
+            sjf_drawn = (a.mask & (1u << 3)) != 0;
             SortJob job = {SortKind::Fifo, 64, want_fifo ? a.key[0] : nullptr, want_fifo ? a.perm[0] : fifo_ws};
-            hipError_t err = lsort_launch(in, &job, 1, batch_ws, s, nullptr, more ? &cp : nullptr);
+            hipError_t err = lsort_launch(in, &job, 1, batch_ws, s, nullptr, more ? &cp : nullptr, nullptr,
+                                          sjf_drawn ? &sjf : nullptr);
             if (err != hipSuccess) return err;
             fifo = job.out;
             in.wait.clear = false;
         }
+        sjf.draw = false;
         in.fifo = fifo;
         // SJF sorts; Priority partitions (and lays out the priority classes'
         // runs, which the Aging merge then combines); Weighted partitions
@@ -203,7 +210,7 @@ hipError_t order_launch(const OrderArgs &a, void *ws, uint32_t *flag, hipStream_
         if (a.mask & (1u << 2)) jobs[nj++] = {SortKind::Tier, 8, a.key[2], a.perm[2]};
         if (nj == 0) return hipGetLastError();
         hipError_t err = lsort_launch(in, jobs, nj, batch_ws, s, a.fifo_in ? nullptr : &cp, nullptr,
-                                      aging ? &runs : nullptr);
+                                      aging ? &runs : nullptr, sjf_drawn ? &sjf : nullptr);
         if (err != hipSuccess || !aging) return err;
         return am_merge_launch(in, n_classes, runs.cstart, rk, rp, a.perm[4], a.key[4], s);
     }
