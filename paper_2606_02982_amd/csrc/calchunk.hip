@@ -559,14 +559,19 @@ __global__ __launch_bounds__(64 * kScanW) void k_calc_scan(CalArgs a)
 // event and gives its trace; otherwise it gives the factor before the
 // event, followed by the exact update (Eq. 5 with the ratio of Eq. 6) for a
 // usable event. Blocks of 1024 events, which lie in one chunk (chunks are a
-// multiple of 2048 events).
+// multiple of 2048 events). The dispatcher deals blocks to the 8 XCDs round
+// robin; consecutive event ranges go to blocks on the same XCD, so that each
+// chunk's row of carries is fetched into one XCD's L2 (not all eight).
 constexpr uint32_t kEvR = 4;
+constexpr uint32_t kXcds = 8;
 static_assert(256 * kEvR == 1024, "");
 __global__ __launch_bounds__(256) void k_calc_ev(CalArgs a)
 {
     __shared__ double pw[1024];
     const uint32_t t = threadIdx.x;
-    const uint32_t e0 = blockIdx.x * 1024u;
+    const uint32_t per = gridDim.x / kXcds, b = blockIdx.x;
+    const uint32_t lb = b < per * kXcds ? (b % kXcds) * per + b / kXcds : b;
+    const uint32_t e0 = lb * 1024u;
     const uint64_t row = (uint64_t)(e0 / a.L) * a.G;
     uint32_t g[kEvR], k[kEvR], o[kEvR];
     double xb[kEvR], x[kEvR];
