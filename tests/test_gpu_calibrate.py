@@ -166,3 +166,26 @@ def test_outputs(ds, oracle, E, G, outs):
         assert ok, "trace worst relative difference %.3g" % worst
     else:
         assert res[1] is None
+
+
+def test_one_workspace_across_paths(ds, oracle):
+    # one workspace, sized for the largest call, reused by calls that take
+    # the one-launch, two-launch and large-table paths in turn (the
+    # one-launch words are marked unwritten again by every call)
+    shapes = [(40000, 64), (300001, 1000), (65536, 64), (200000, 32), (9000, 300), (40000, 64)]
+    ws = ds.workspace(ds.OP_CALIBRATE, max(e for e, _ in shapes), 1000)
+    for k, (E, G) in enumerate(shapes):
+        need = ds.workspace_bytes(ds.OP_CALIBRATE, E, G)
+        assert ws.numel() >= need
+        rng = np.random.default_rng(100 + k)
+        g = rng.integers(0, G, E).astype(np.uint32)
+        est = rng.uniform(1, 500, E)
+        obs = rng.integers(0, 1000, E).astype(np.uint32)
+        st0 = rng.uniform(0.5, 1.5, G)
+        w_st, w_tr = oracle.calibrate(g, est, obs, 0.2, st0)
+        st = dev(st0.copy())
+        _, tr = ds.calibrate(dev(g), dev(est), dev(obs), 0.2, st, ws=ws, validate=True)
+        ok, worst = rel_close(host(tr), w_tr, RTOL)
+        assert ok, "call %d (%d x %d): trace worst relative difference %.3g" % (k, E, G, worst)
+        ok, worst = rel_close(host(st), w_st, RTOL)
+        assert ok, "call %d: state worst relative difference %.3g" % (k, worst)
