@@ -6,10 +6,12 @@
 // produce() (keys.h).
 //
 //   k_ls_gather   the keys of S = 8 per bucket positions, one in each of S
-//                 equal strata of [0, n) (so the sample is in sequence order).
+//                 equal strata of [0, n) (so the sample is in sequence order),
+//                 and each wave's 64 of them sorted (a bitonic network).
 //   k_ls_sample   each sample's rank by counting the samples below it, the
 //                 count of each group of 64 samples spread over four blocks
-//                 (each staging a quarter of the sample in LDS).
+//                 (each staging a quarter of the sorted 64-sample blocks in
+//                 LDS, one binary search per block).
 //   k_ls_place    each sample at its rank (the four counts added): the
 //                 sorted sample, of which every (S/B)-th pair is one of the
 //                 B - 1 splitters.
@@ -234,74 +236,86 @@ __device__ __forceinline__ uint32_t blk_excl_scan(uint32_t x, uint32_t *wsum)
     return off + incl - x;
 }
 
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t x, int m)
+{
+    const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)x, m, 64);
+    const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(x >> 32), m, 64);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// The sample's keys in sample order (raw_k), and each wave's 64 samples
+// sorted by (key, sample index) with a bitonic network across the lanes,
+// stored as sorted blocks of 64 in smp_k / smp_j for the ranking (the
+// placement overwrites them with the sorted sample).
 __global__ __launch_bounds__(256) void k_ls_gather(LsArgs a)
 {
     const LsRow &R = a.r[a.srow[blockIdx.y]];
     const uint32_t s = blockIdx.x * 256u + threadIdx.x;
-    if (s < R.S) {
-        const uint32_t j = ls_pos(s, a.n, R.S);
-        R.raw_k[s] = R.by_req ? ordered_bits(a.in.budget[j]) : ls_key(a, R, j);
-    }
+    if (blockIdx.x * 256u + (threadIdx.x & ~63u) >= R.S) return;   // a whole wave past S (a multiple of 64)
+    const uint32_t j = ls_pos(s, a.n, R.S);
+    uint64_t k = R.by_req ? ordered_bits(a.in.budget[j]) : ls_key(a, R, j);
+    R.raw_k[s] = k;
+    uint32_t i = s;
+    const uint32_t lane = (uint32_t)lane_id();
+    for (uint32_t kk = 2; kk <= 64; kk <<= 1)
+        for (uint32_t jj = kk >> 1; jj > 0; jj >>= 1) {
+            const uint64_t pk = shfl_xor_u64(k, (int)jj);
+            const uint32_t pi = (uint32_t)__shfl_xor((int)i, (int)jj, 64);
+            const bool pl = pk < k || (pk == k && pi < i);   // the partner's pair is the smaller
+            const bool up = (lane & kk) == 0, lower = (lane & jj) == 0;
+            if (lower == up ? pl : !pl) {
+                k = pk;
+                i = pi;
+            }
+        }
+    R.smp_k[s] = k;
+    R.smp_j[s] = i;
 }
 
 constexpr int kSmT = 1024, kSmW = kSmT / 64;
 
-// Block b ranks samples 64 b .. 64 b + 63 (one per lane) among all S, staged
-// in LDS: wave w counts over its slice of the sample, the slices' counts are
-// added. (Rank by counting: LDS broadcast reads, eight in flight at a time.)
 // Ranks by counting, spread over kSmP blocks per group of 64 samples: block
-// (g, p) stages part p of the sample in LDS and counts, for each of the
-// group's samples (one per lane), the part's samples below it (each wave
-// over a slice, the slices added), stored as that part's count.
+// (g, p) stages part p of the sorted 64-sample blocks in LDS and counts, for
+// each of the group's samples (one per lane), the part's samples below it
+// by (key, sample index): one binary search per sorted block (each wave
+// over a share of the part's blocks, the waves' counts added), stored as
+// that part's count. Sample indices increase with the positions, so the
+// order is the pair order by (key, position).
 constexpr uint32_t kSmP = 4;
 
 __global__ __launch_bounds__(kSmT) void k_ls_sample(LsArgs a)
 {
     __shared__ uint64_t sk[kLsMaxS / kSmP];
+    __shared__ uint16_t si[kLsMaxS / kSmP];
     __shared__ uint32_t part[kSmW][64];
     const LsRow &R = a.r[a.srow[blockIdx.y]];
     const uint32_t g = blockIdx.x / kSmP, pq = blockIdx.x % kSmP;
     if (g * 64u >= R.S) return;   // a row with a smaller sample than the grid is wide
-    const uint32_t t = threadIdx.x, lane = (uint32_t)lane_id(), w = t >> 6, S = R.S, n = a.n;
-    const uint32_t q = S / kSmP, p0 = pq * q;   // this block's part [p0, p0 + q) (S is a multiple of 64)
-    for (uint32_t i = t; i < q; i += kSmT) sk[i] = R.raw_k[p0 + i];
-    const uint32_t s0 = g * 64u, s = s0 + lane;
+    const uint32_t t = threadIdx.x, lane = (uint32_t)lane_id(), w = t >> 6, S = R.S;
+    const uint32_t nb = S / 64u, b0 = pq * nb / kSmP, b1 = (pq + 1u) * nb / kSmP;   // sorted blocks [b0, b1)
+    const uint32_t e0 = b0 * 64u, ne = (b1 - b0) * 64u;   // <= kLsMaxS / kSmP
+    for (uint32_t x = t; x < ne; x += kSmT) {
+        sk[x] = R.smp_k[e0 + x];
+        si[x] = (uint16_t)R.smp_j[e0 + x];
+    }
+    const uint32_t s = g * 64u + lane;
     const uint64_t ks = R.raw_k[s];
     __syncthreads();
-    // samples u with (key_u, pos_u) < (key_s, pos_s); the positions increase
-    // with u, so a tie on the key goes by u < s: below the group's samples
-    // (key <=), above them (key <), across them (exactly)
-    const uint32_t per = q / kSmW, u0 = p0 + w * per, u1 = u0 + per;
     uint32_t c = 0;
-    {
-        const uint32_t e = u1 < s0 ? u1 : s0;
-        uint32_t u = u0;
-        for (; u + 8u <= e; u += 8u) {
-            uint64_t x[8];
+    for (uint32_t b = w; b < b1 - b0; b += kSmW) {
+        // the block's pairs below (ks, s): steps of 32 .. 1, then the last one
+        const uint32_t base = b * 64u;
+        uint32_t pos = 0;
 #pragma unroll
-            for (int r = 0; r < 8; r++) x[r] = sk[u - p0 + r];
-#pragma unroll
-            for (int r = 0; r < 8; r++) c += x[r] <= ks ? 1u : 0u;
+        for (uint32_t step = 32; step > 0; step >>= 1) {
+            const uint32_t q = base + pos + step - 1u;
+            const uint64_t x = sk[q];
+            if (x < ks || (x == ks && si[q] < s)) pos += step;
         }
-        for (; u < e; u++) c += sk[u - p0] <= ks ? 1u : 0u;
-    }
-    {
-        const uint32_t b0 = u0 > s0 ? u0 : s0, b1 = u1 < s0 + 64u ? u1 : s0 + 64u;
-        for (uint32_t u = b0; u < b1; u++) {
-            const uint64_t x = sk[u - p0];
-            c += (x < ks || (x == ks && u < s)) ? 1u : 0u;
-        }
-    }
-    {
-        uint32_t u = u0 > s0 + 64u ? u0 : s0 + 64u;
-        for (; u + 8u <= u1; u += 8u) {
-            uint64_t x[8];
-#pragma unroll
-            for (int r = 0; r < 8; r++) x[r] = sk[u - p0 + r];
-#pragma unroll
-            for (int r = 0; r < 8; r++) c += x[r] < ks ? 1u : 0u;
-        }
-        for (; u < u1; u++) c += sk[u - p0] < ks ? 1u : 0u;
+        const uint32_t q = base + pos;   // pos <= 63
+        const uint64_t x = sk[q];
+        if (x < ks || (x == ks && si[q] < s)) pos++;
+        c += pos;
     }
     part[w][lane] = c;
     __syncthreads();
@@ -702,13 +716,6 @@ struct BkLs {
     uint32_t wmax[kBW];
     uint64_t red[4][kBW];
 };
-
-__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t x, int m)
-{
-    const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)x, m, 64);
-    const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(x >> 32), m, 64);
-    return ((uint64_t)hi << 32) | lo;
-}
 
 enum class Red { Min, Max, Or };
 
