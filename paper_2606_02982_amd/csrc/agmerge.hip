@@ -219,7 +219,9 @@ __device__ inline uint32_t merge_split(const uint64_t *ak, const uint32_t *ap, u
     while (hi > lo) {
         const uint32_t span = hi - lo;
         const uint32_t m = lo + (uint32_t)(((uint64_t)span * lane) >> 6);   // lo <= m < hi
-        const bool p = am_less(ak[m], ap[m], bk[d - 1u - m], bp[d - 1u - m]);
+        // (the positions are read only on a tie of the keys)
+        const uint64_t ka = ak[m], kb = bk[d - 1u - m];
+        const bool p = ka < kb || (ka == kb && ap[m] < bp[d - 1u - m]);
         const uint32_t f = (uint32_t)__popcll(__ballot(p));   // probes 0..f-1 hold, f.. do not
         const uint32_t mf1 = f ? lo + (uint32_t)(((uint64_t)span * (f - 1u)) >> 6) : 0u;
         const uint32_t mf = f < 64u ? lo + (uint32_t)(((uint64_t)span * f) >> 6) : hi;
