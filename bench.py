@@ -196,8 +196,8 @@ def main():
         return bench_split(workloads.WORKLOADS["batch4k"])
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py: this build runs the admission hot path on one GPU; --gpus %d is not "
-              "supported (the design note on sharding is in the documentation)" % args.gpus,
+        print("bench.py: the admission hot path runs on one GPU here; --gpus %d is not "
+              "supported (how the path would shard is described in the documentation)" % args.gpus,
               file=sys.stderr)
         sys.exit(2)
 
