@@ -59,9 +59,11 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--stage", choices=["pipeline", "characterize", "errors", "drift", "simulate", "split",
-                                        "ceiling"],
+                                        "ceiling", "calibrate"],
                     default="pipeline",
                     help="characterize: time only stage 1 on --workload (any workload with text); "
+                         "calibrate: stage 2 alone per call on the completion events of batch4k, "
+                         "long16k, batch64k and chat1m, eager and as replays of a captured graph; "
                          "split: Python len(p.split()) per prompt of batch4k on one host core, "
                          "ceiling: the read side of characterize alone over --workload's text size "
                          "(ds_read_bandwidth: the practical read rate of its access pattern); "
@@ -217,6 +219,8 @@ def main():
         return bench_drift(args, workloads.WORKLOADS["drift4m"] if wl.has_text else wl)
     if args.stage == "simulate":
         return bench_simulate(args, wl)
+    if args.stage == "calibrate":
+        return bench_calibrate(args)
     if not wl.has_text or len(wl.policies) < 5:
         print("bench.py: the step needs a workload with text and all five policies", file=sys.stderr)
         sys.exit(2)
@@ -556,6 +560,54 @@ def timed_ms(fn, args):
     ev[1].record()
     torch.cuda.synchronize()
     return ev[0].elapsed_time(ev[1]) / args.steps
+
+
+def bench_calibrate(args):
+    """Stage 2 alone on each workload's completion events: microseconds per
+    call, eager (HIP events around args.steps calls) and as replays of a
+    graph capturing 20 calls (no host launch gaps), with the final factors of
+    one call from 1.0 checked against the oracle."""
+    import torch
+    import oracle
+    import workloads
+    from paper_2606_02982_amd import driftsched as ds
+    res = {"metric": "calibration microseconds per call (stage 2 alone)", "steps": args.steps,
+           "workloads": {}}
+    for name in ("batch4k", "long16k", "batch64k", "chat1m"):
+        b = load(workloads.WORKLOADS[name], with_text=False)
+        ob = oracle_events(b)
+        E, G = len(b.ev_group), b.n_groups
+        group, est, obs = to_dev(b.ev_group), to_dev(b.ev_est), to_dev(b.ev_obs)
+        state = torch.ones(G, dtype=torch.float64, device="cuda")
+        trace = torch.empty(E, dtype=torch.float64, device="cuda")
+        ws = ds.workspace(ds.OP_CALIBRATE, E, G)
+        alpha = b.alphas[0]
+
+        def cal():
+            ds.calibrate(group, est, obs, alpha, state, trace=trace, ws=ws)
+        eager_ms = timed_ms(cal, args)
+        k = 20
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            cal()
+            torch.cuda.synchronize()
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=side):
+                for _ in range(k):
+                    cal()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        graph_ms = timed_ms(g.replay, args) / k
+        state.fill_(1.0)
+        cal()
+        want, _ = oracle.calibrate(ob.ev_group, ob.ev_est, ob.ev_obs, alpha, np.ones(G))
+        assert np.all(np.abs(state.cpu().numpy() - want) <= 1e-12 * np.abs(want)), "calibration mismatch"
+        cal_bytes = E * (4 + 8 + 4) + E * 8 + 16 * G
+        res["workloads"][name] = {"events": E, "groups": G, "us_per_call_eager": round(eager_ms * 1e3, 2),
+                                  "us_per_call_graph": round(graph_ms * 1e3, 2),
+                                  "GBs_graph": round(cal_bytes / (graph_ms * 1e-3) / 1e9, 1)}
+    print(json.dumps(res))
 
 
 def bench_drift(args, wl):
