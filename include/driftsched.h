@@ -38,7 +38,8 @@
  *    device memory and keeps no state between calls. Scratch memory is a
  *    caller-provided workspace of at least ds_workspace_bytes() bytes,
  *    256-byte aligned; its contents need no initialisation and are
- *    undefined after the call.
+ *    undefined after the call. Calls that may run at the same time (on
+ *    different streams) need workspaces of their own.
  *  - Work is enqueued on `stream` (a hipStream_t; NULL is the null stream)
  *    and the call returns without waiting, except with DS_VALIDATE, where
  *    it waits for the stream to report data errors.
