@@ -479,6 +479,7 @@ __global__ __launch_bounds__(kT) void k_calc_agg(CalArgs a)
 // through the earlier stretches' maps in order and walks its own stretch,
 // writing the factor before each chunk.
 constexpr uint32_t kScanW = 16;
+constexpr uint32_t kScanRegs = 16;   // a wave's stretch of chunk maps held in registers, at most
 __global__ __launch_bounds__(64 * kScanW) void k_calc_scan(CalArgs a)
 {
     __shared__ double sA[kScanW][64], sB[kScanW][64];
@@ -494,6 +495,51 @@ __global__ __launch_bounds__(64 * kScanW) void k_calc_scan(CalArgs a)
     const bool in = g < a.G;
     const uint32_t per = (a.C + kScanW - 1) / kScanW;
     const uint32_t cb = w * per < a.C ? w * per : a.C, ce = cb + per < a.C ? cb + per : a.C;
+    if (per <= kScanRegs) {
+        // the stretch's maps in registers: one round of loads, walked twice
+        double A[kScanRegs], B[kScanRegs];
+        Map agg = {0u, 0u, 1.0, 0.0};
+#pragma unroll
+        for (uint32_t r = 0; r < kScanRegs; r++) {
+            A[r] = -1.0;
+            B[r] = 0.0;
+            if (in && cb + r < ce) {
+                A[r] = a.aggA[(uint64_t)(cb + r) * a.G + g];
+                B[r] = a.aggB[(uint64_t)(cb + r) * a.G + g];
+            }
+        }
+#pragma unroll
+        for (uint32_t r = 0; r < kScanRegs; r++)
+            if (A[r] >= 0.0) agg = combine(agg, Map{0u, 1u, A[r], B[r]});
+        sA[w][lane] = agg.a;
+        sB[w][lane] = agg.b;
+        sU[w][lane] = agg.u;
+        __syncthreads();
+        if (!in) return;
+        double v = a.state[g];
+        bool touched = false;
+        for (uint32_t q = 0; q < kScanW; q++) {
+            if (!sU[q][lane]) continue;
+            touched = true;
+            if (q < w) {
+                const double tt = sA[q][lane] * v;
+                v = tt + sB[q][lane];
+            }
+        }
+#pragma unroll
+        for (uint32_t r = 0; r < kScanRegs; r++) {
+            if (cb + r >= ce) break;
+            a.carry[(uint64_t)(cb + r) * a.G + g] = v;
+            if (A[r] >= 0.0) {
+                const double tt = A[r] * v;
+                v = tt + B[r];
+            }
+        }
+        // the wave holding the last chunk writes the factor after all events
+        // (a group without usable events keeps its factor untouched)
+        if (ce == a.C && cb < ce && touched) a.state[g] = v;
+        return;
+    }
     // four chunks' maps in flight at a time
     constexpr uint32_t kR = 4;
     Map agg = {0u, 0u, 1.0, 0.0};
