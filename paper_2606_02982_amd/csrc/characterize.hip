@@ -363,17 +363,21 @@ __device__ int superround_separators(WaveLds &L, const uint4 (&d)[kLoadRounds], 
     for (uint32_t u = 0; u < kLoadRounds; u++)
         *reinterpret_cast<uint4 *>(&L.data[(u * kRound + 16u * (uint32_t)lane) / 4]) = d[u];
     if (lane == 0) *reinterpret_cast<uint4 *>(&L.data[kSR / 4]) = make_uint4(tail, 0u, 0u, 0u);
-    // list the leads: byte offsets within the super-round
+    // list the leads as (lane, bit of M), the two halves of M one after the
+    // other (32-bit steps); the checking lane finds the byte offset
     uint32_t r = excl;
-    while (__ballot(M != 0)) {
-        if (M) {
-            uint32_t lo = (uint32_t)M, hi = (uint32_t)(M >> 32);
-            uint32_t p = lo ? (uint32_t)__ffs(lo) - 1 : 32u + (uint32_t)__ffs(hi) - 1;
-            M &= M - 1;
-            uint32_t q = p & 31u;
-            uint32_t u = ((p >> 5) << 1) | ((q >> 2) & 1u);
-            uint32_t off = ((q & 3u) << 2) | (q >> 3);
-            L.slot[r++] = (uint16_t)(u * kRound + 16u * (uint32_t)lane + off);
+    const uint32_t lb = (uint32_t)lane << 6;
+    uint32_t mlo = (uint32_t)M, mhi = (uint32_t)(M >> 32);
+    while (__ballot(mlo != 0)) {
+        if (mlo) {
+            L.slot[r++] = (uint16_t)(lb | ((uint32_t)__ffs(mlo) - 1u));
+            mlo &= mlo - 1u;
+        }
+    }
+    while (__ballot(mhi != 0)) {
+        if (mhi) {
+            L.slot[r++] = (uint16_t)(lb | ((uint32_t)__ffs(mhi) + 31u));
+            mhi &= mhi - 1u;
         }
     }
     wave_lds_fence();
@@ -384,7 +388,10 @@ __device__ int superround_separators(WaveLds &L, const uint4 (&d)[kLoadRounds], 
         uint32_t t = base + (uint32_t)lane;
         uint32_t len = 0, pos = 0;
         if (t < total) {
-            pos = L.slot[t];
+            // bit p of lane l's M: round u, byte off of the lane's 16
+            const uint32_t e = L.slot[t], p = e & 63u, q = p & 31u;
+            const uint32_t u = ((p >> 5) << 1) | ((q >> 2) & 1u);
+            pos = u * kRound + 16u * (e >> 6) + (((q & 3u) << 2) | (q >> 3));
             uint32_t w0 = L.data[pos >> 2], w1 = L.data[(pos >> 2) + 1];
             len = mb_space_len_nb(__builtin_amdgcn_alignbyte(w1, w0, pos & 3u));
         }
