@@ -453,8 +453,13 @@ __device__ void boundary_superround(WaveState &st, const RangeCtx &rc, const uin
         const uint32_t v2 = __builtin_amdgcn_alignbyte(h2, h1, 3);
         const uint32_t v3 = __builtin_amdgcn_alignbyte(h3, h2, 3);
         const uint32_t s0 = ~h0 & v0, s1 = ~h1 & v1, s2 = ~h2 & v2, s3 = ~h3 & v3;
-        const uint32_t c = (uint32_t)(__popc(s0) + __popc(s1) + __popc(s2) + __popc(s3));
+        const uint32_t c0 = (uint32_t)__popc(s0), c01 = c0 + (uint32_t)__popc(s1);
+        const uint32_t c012 = c01 + (uint32_t)__popc(s2), c = c012 + (uint32_t)__popc(s3);
         const uint32_t incl = wave_incl_scan_dpp(c);
+        // one word per lane for the boundaries: the starts in the lanes
+        // before it (< 1024, 11 bits), then those in its first one, two and
+        // three dwords (<= 12 each, 5 bits)
+        const uint32_t pk = (incl - c) | (c0 << 11) | (c01 << 16) | (c012 << 21);
         carry = readlane32(h3, 63) >> 31;
         const uint64_t rend = sb + (uint64_t)(u + 1) * kRound;
         uint32_t fbr = 0, pend = 0;   // forced starts before P / at the last P
@@ -467,25 +472,28 @@ __device__ void boundary_superround(WaveState &st, const RangeCtx &rc, const uin
             const uint32_t rel = (uint32_t)(P - (rend - kRound));
             const int L = (int)(rel >> 4);
             const uint32_t r = rel & 15u, k = r >> 2, sh = 8u * (r & 3u);
+            // lane L's dword k: its start bits and whitespace bits
+            uint32_t wk, hk;
+            if (k == 0) { wk = readlane32(s0, L); hk = readlane32(h0, L); }
+            else if (k == 1) { wk = readlane32(s1, L); hk = readlane32(h1, L); }
+            else if (k == 2) { wk = readlane32(s2, L); hk = readlane32(h2, L); }
+            else { wk = readlane32(s3, L); hk = readlane32(h3, L); }
             if (P != lastP) {
                 fbr += pend;
                 lastP = P;
-                uint32_t hk, vk;
-                if (k == 0) { hk = readlane32(h0, L); vk = readlane32(v0, L); }
-                else if (k == 1) { hk = readlane32(h1, L); vk = readlane32(v1, L); }
-                else if (k == 2) { hk = readlane32(h2, L); vk = readlane32(v2, L); }
-                else { hk = readlane32(h3, L); vk = readlane32(v3, L); }
-                pend = ((hk | vk) >> (sh + 7)) & 1u ? 0u : 1u;
+                // whitespace at P-1: in the same dword unless P starts it
+                uint32_t prev;
+                if (sh) prev = hk >> (sh - 1u);
+                else if (k == 0) prev = readlane32(v0, L) >> 7;
+                else if (k == 1) prev = readlane32(v1, L) >> 7;
+                else if (k == 2) prev = readlane32(v2, L) >> 7;
+                else prev = readlane32(v3, L) >> 7;
+                pend = ((hk >> (sh + 7)) | prev) & 1u ? 0u : 1u;
             }
-            const uint32_t e = L ? readlane32(incl, L - 1) : 0u;
-            const uint32_t low = (1u << sh) - 1u;
-            const uint32_t w0 = readlane32(s0, L), w1 = readlane32(s1, L);
-            const uint32_t w2 = readlane32(s2, L), w3 = readlane32(s3, L);
-            uint32_t part = (uint32_t)__popc(k == 0 ? (w0 & low) : w0);
-            part += k >= 1 ? (uint32_t)__popc(k == 1 ? (w1 & low) : w1) : 0u;
-            part += k >= 2 ? (uint32_t)__popc(k == 2 ? (w2 & low) : w2) : 0u;
-            part += k == 3 ? (uint32_t)__popc(w3 & low) : 0u;
-            const uint32_t val = (uint32_t)(base + fbr + e + part);
+            const uint32_t q = readlane32(pk, L);
+            const uint32_t below = k ? (q >> (6u + 5u * k)) & 31u : 0u;   // starts in dwords 0 .. k-1
+            const uint32_t part = below + (uint32_t)__popc(wk & ((1u << sh) - 1u));
+            const uint32_t val = (uint32_t)(base + fbr + (q & 0x7FFu) + part);
             plv = lane == j ? val : plv;
         }
         base += readlane32(incl, 63) + fbr + pend;
