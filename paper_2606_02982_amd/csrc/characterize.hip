@@ -443,6 +443,8 @@ __device__ void boundary_superround(WaveState &st, const RangeCtx &rc, const uin
     uint32_t carry = st.ws_prev;
     uint64_t rem = bm;
     uint32_t plv = 0;
+    // the boundaries' offsets in the super-round (window lanes in bm: < 4 KiB)
+    const uint32_t wrel = (uint32_t)(st.win - sb);
 #pragma unroll
     for (uint32_t u = 0; u < kLoadRounds; u++) {
         const uint32_t h0 = ascii_space_hb(d[u].x), h1 = ascii_space_hb(d[u].y);
@@ -461,15 +463,14 @@ __device__ void boundary_superround(WaveState &st, const RangeCtx &rc, const uin
         // three dwords (<= 12 each, 5 bits)
         const uint32_t pk = (incl - c) | (c0 << 11) | (c01 << 16) | (c012 << 21);
         carry = readlane32(h3, 63) >> 31;
-        const uint64_t rend = sb + (uint64_t)(u + 1) * kRound;
         uint32_t fbr = 0, pend = 0;   // forced starts before P / at the last P
-        uint64_t lastP = kNone;
+        uint32_t lastP = ~0u;
         while (rem) {
             const int j = __ffsll((unsigned long long)rem) - 1;
-            const uint64_t P = readlane64(st.win, j);
-            if (P >= rend) break;
+            const uint32_t P = readlane32(wrel, j);
+            if (P >= (u + 1u) * kRound) break;
             rem &= rem - 1;
-            const uint32_t rel = (uint32_t)(P - (rend - kRound));
+            const uint32_t rel = P - u * kRound;
             const int L = (int)(rel >> 4);
             const uint32_t r = rel & 15u, k = r >> 2, sh = 8u * (r & 3u);
             // lane L's dword k: its start bits and whitespace bits
