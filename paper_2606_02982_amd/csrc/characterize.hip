@@ -323,7 +323,7 @@ __device__ __forceinline__ void process_round(WaveState &st, const RangeCtx &rc,
 // next 16), the list of lead-byte offsets, and separator coverage per
 // (lane, round).
 constexpr uint32_t kSR = kRound * kLoadRounds;   // 4 KiB
-constexpr uint32_t kMaxLeads = 224;              // more leads: per-round path
+constexpr uint32_t kMaxLeads = 512;              // more leads: per-round path
 struct WaveLds {
     uint32_t data[(kSR + 16) / 4];
     uint16_t slot[kMaxLeads];
